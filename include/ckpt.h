@@ -1,0 +1,245 @@
+/*
+ * ckpt.h -- C ABI of libckpt: per-iteration in-memory snapshots of one
+ * rank's training state on an MI355X (gfx950), with a per-chunk integrity
+ * sum, streamed to pinned host memory off the critical path.
+ *
+ * What the paper defines (PHOENIX):
+ *   - Sec. V-B, "Device-to-host (D2H)": once per iteration the rank's full
+ *     state (optimizer shard, parameter shard, metadata envelope with the
+ *     step index, parallel configuration and RNG states) is packed into one
+ *     contiguous buffer and copied asynchronously to pinned host memory on a
+ *     dedicated stream, so that local recovery needs no network transfer.
+ *   - Sec. VI-A: two host buffers alternate roles -- one holds the committed
+ *     snapshot of the previous iteration, the other receives the current one
+ *     -- so an interrupted offload never destroys the last good snapshot.
+ *     The training loop has one synchronization point: a wait right before
+ *     the optimizer step, so the protected state is captured before the
+ *     optimizer mutates it.
+ *   - Sec. V-C, invariant I4 (step atomicity): a partially written snapshot
+ *     is never used for recovery.
+ *   - Sec. V-C (third recovery stage) and Sec. VI-E: recovery writes the
+ *     saved state back into the live tensors.
+ *
+ * What this library adds: the packed buffer ("image") is cut into
+ * fixed-size chunks; each chunk carries the sum of its 8-byte little-endian
+ * words modulo 2^64.  The sums are computed on the GPU while packing and
+ * re-checked on the GPU when a snapshot is restored or verified.  The wait
+ * before the optimizer step is refined to chunk granularity: it covers only
+ * the chunks holding the fragments the caller is about to overwrite.
+ *
+ * Image layout.  Fragments keep registration order.  off[0] = 0,
+ * off[i] = align_up(off[i-1] + nbytes[i-1], align); the image is
+ * align_up(off[n-1] + nbytes[n-1], align) bytes; padding bytes are zero and
+ * are covered by the sums.  Chunk c is the window
+ * [c*chunk_bytes, min((c+1)*chunk_bytes, image_bytes)).
+ *
+ * Conventions.
+ *   - Every call returns ckpt_status: 0 on success, a negative CKPT_E* code
+ *     on failure.  Nothing is thrown across the ABI.  The text of the last
+ *     error of a context is available from ckpt_last_error().
+ *   - "Device pointer" means memory of the context's GPU (hipMalloc,
+ *     torch's caching allocator).  Streams are hipStream_t handles passed as
+ *     void*; NULL means the device's null stream.
+ *   - One host thread drives a context at a time; contexts are independent.
+ *   - The library never allocates or frees the caller's tensors.  It owns
+ *     its pinned host images, device staging, sums, events and streams, and
+ *     frees them in ckpt_destroy().
+ */
+#ifndef CKPT_H
+#define CKPT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t ckpt_status;
+
+#define CKPT_OK 0
+#define CKPT_EINVAL (-1)   /* bad argument (null pointer, size, alignment, range) */
+#define CKPT_ESTATE (-2)   /* call not valid in the context's current state */
+#define CKPT_ENOMEM (-3)   /* pinned host or device allocation failed */
+#define CKPT_EHIP (-4)     /* a HIP runtime call failed; see ckpt_last_error() */
+#define CKPT_ECORRUPT (-5) /* one or more chunk sums did not match; list filled */
+#define CKPT_ENOSNAP (-6)  /* no committed snapshot (or the requested one is gone) */
+#define CKPT_EBUSY (-7)    /* both host buffers are still in flight */
+#define CKPT_ERANGE (-8)   /* snapshot id unknown or no longer retained */
+
+/* ckpt_wait modes */
+#define CKPT_WAIT_CAPTURED 0  /* stream-ordered: packed into device staging */
+#define CKPT_WAIT_COMMITTED 1 /* host-blocking: image and sums landed in pinned memory */
+
+/* ckpt_snapshot_state results */
+#define CKPT_SNAP_IN_FLIGHT 0
+#define CKPT_SNAP_COMMITTED 1
+#define CKPT_SNAP_ABORTED 2    /* interrupted; never committed (invariant I4) */
+#define CKPT_SNAP_SUPERSEDED 3 /* committed once, host buffer since reused */
+
+typedef struct ckpt_ctx ckpt_ctx;
+
+typedef struct {
+    uint64_t chunk_bytes;          /* chunk size; 0 = 64 MiB.  Multiple of align_bytes. */
+    uint32_t align_bytes;          /* fragment alignment in the image; 0 = 256.  Power of two, 16..4096. */
+    uint32_t host_buffers;         /* pinned host images; 0 = 2 (ping-pong).  Only 2 is accepted. */
+    uint64_t device_staging_bytes; /* 0 = a full-size device image; otherwise a ring of chunk-sized
+                                      slots of at most this many bytes (at least 2 chunks) */
+    uint64_t group_bytes;          /* full-image mode: bytes packed per kernel launch and copied per
+                                      DMA request; 0 = 1 GiB (rounded to whole chunks) */
+    int32_t device;                /* HIP device ordinal */
+    uint32_t grid_blocks;          /* kernel grid cap; 0 = chosen by the library */
+} ckpt_config;
+
+typedef struct {
+    const void* dev_ptr; /* device address of the fragment's first byte; any alignment */
+    uint64_t nbytes;     /* bytes; 0 is allowed (the fragment takes no image space) */
+    uint32_t dtype;      /* caller's tag, stored in the envelope; bytes are never interpreted */
+    uint32_t cls;        /* caller's tag (parameter / master / moment ...), stored in the envelope */
+} ckpt_tensor;
+
+/* Create a context on cfg->device (NULL cfg = all defaults on device 0).
+ * Allocates nothing large until ckpt_register_tensors().
+ * Errors: EINVAL (bad config), EHIP. */
+ckpt_status ckpt_create(const ckpt_config* cfg, ckpt_ctx** out);
+
+/* Waits for the context's outstanding GPU work, then frees everything it
+ * owns.  NULL is accepted. */
+ckpt_status ckpt_destroy(ckpt_ctx* ctx);
+
+/* Register the rank's state: n fragments in the order that defines the image
+ * layout (Sec. V-B: the state is packed into one contiguous buffer).  The
+ * tensors stay owned by the caller and must stay allocated and unmoved while
+ * the context lives.  Computes the layout, uploads the fragment and tile
+ * tables, allocates device staging and two pinned host images.  Callable
+ * once per context; a different layout needs a new context.
+ * Errors: ESTATE (already registered), EINVAL (null pointer with nbytes > 0,
+ * n == 0, or overlapping fragments are NOT checked), ENOMEM, EHIP. */
+ckpt_status ckpt_register_tensors(ckpt_ctx* ctx, const ckpt_tensor* t, uint32_t n);
+
+/* Start snapshot `step` (Sec. V-B D2H; Sec. VI-A ping-pong).  Stream-ordered
+ * after all work already enqueued on after_stream (call it right after the
+ * previous optimizer step).  Packs every fragment with its chunk sums into
+ * device staging on the library's side stream, then copies the image and the
+ * sums chunk group by chunk group into the pinned host buffer that does not
+ * hold the newest committed snapshot.  Returns at once with *snap_id
+ * (increasing from 1).  meta (may be NULL when meta_len == 0) is the caller's
+ * envelope blob -- parallel configuration, RNG states -- copied before the
+ * call returns; at most 1 MiB.
+ * Errors: ESTATE (nothing registered), EBUSY (two earlier snapshots are
+ * both still uncommitted), EINVAL, EHIP. */
+ckpt_status ckpt_snapshot_async(ckpt_ctx* ctx, void* after_stream, uint64_t step, const void* meta,
+                                uint32_t meta_len, uint64_t* snap_id);
+
+/* The synchronization point before the optimizer step (Sec. VI-A), refined to
+ * chunk granularity.  mode CKPT_WAIT_CAPTURED: makes `stream` wait (no host
+ * block) until every chunk holding bytes of fragments [frag_lo, frag_hi) of
+ * snapshot snap_id has been packed, so the caller may overwrite those
+ * fragments afterwards on `stream` (frag_hi above the fragment count is
+ * clamped to it).  mode CKPT_WAIT_COMMITTED: blocks the
+ * host until the snapshot's image and sums are in pinned memory (fragment
+ * range ignored).  Errors: ERANGE (unknown or expired snap_id), EINVAL,
+ * ESTATE (COMMITTED on an aborted snapshot), EHIP. */
+ckpt_status ckpt_wait(ckpt_ctx* ctx, uint64_t snap_id, uint32_t mode, void* stream, uint32_t frag_lo,
+                      uint32_t frag_hi);
+
+/* Non-blocking state query: CKPT_SNAP_* in *state. Errors: ERANGE. */
+ckpt_status ckpt_snapshot_state(ckpt_ctx* ctx, uint64_t snap_id, uint32_t* state);
+
+/* Recovery (Sec. V-C third stage; Sec. VI-E, local case): first waits for the
+ * context's outstanding snapshot work, then copies the committed image
+ * snap_id (0 = the newest committed) to the device chunk group by chunk
+ * group and scatters every byte back into the registered fragments, while
+ * recomputing every chunk sum on the GPU.  The work is ordered after what is
+ * already enqueued on `stream`, and `stream` waits for it; the call returns
+ * when it is done.  Chunks whose recomputed sum differs from the stored one
+ * are listed in increasing order in bad_chunks (up to cap entries, NULL
+ * allowed when cap == 0); *n_bad receives the true count.  All bytes are
+ * written even when some chunk is bad; the caller then treats the fragments
+ * overlapping those chunks as invalid (ckpt_chunk_fragments) and may restore
+ * the other buffer instead.
+ * Errors: ENOSNAP (nothing committed / snap_id superseded or aborted),
+ * ECORRUPT (n_bad > 0), EINVAL, EHIP. */
+ckpt_status ckpt_restore(ckpt_ctx* ctx, uint64_t snap_id, void* stream, uint32_t* bad_chunks, uint32_t cap,
+                         uint32_t* n_bad);
+
+/* Integrity check of a committed host image without touching the live
+ * tensors: copies it to the device and recomputes every chunk sum on the
+ * GPU.  Same snap_id, list and error conventions as ckpt_restore. */
+ckpt_status ckpt_verify(ckpt_ctx* ctx, uint64_t snap_id, uint32_t* bad_chunks, uint32_t cap, uint32_t* n_bad);
+
+/* Layout accessors.  frag_off may be NULL; otherwise it receives n offsets. */
+ckpt_status ckpt_layout(ckpt_ctx* ctx, uint64_t* frag_off, uint64_t* image_bytes, uint64_t* n_chunks);
+
+/* Locate: byte range of chunk c and the range [*frag_first, *frag_last] of
+ * fragments that may hold its bytes (empty fragments inside it hold none).
+ * Errors: EINVAL (c out of range). */
+ckpt_status ckpt_chunk_fragments(ckpt_ctx* ctx, uint64_t c, uint64_t* byte_lo, uint64_t* byte_hi,
+                                 uint32_t* frag_first, uint32_t* frag_last);
+
+/* Borrowed view of a snapshot's pinned host image and its stored sums (valid
+ * until the buffer is reused or the context destroyed).  Writable: tests
+ * inject bit flips through it.  Errors: ENOSNAP (not committed), ERANGE. */
+ckpt_status ckpt_host_image(ckpt_ctx* ctx, uint64_t snap_id, void** image, uint64_t* image_bytes,
+                            uint64_t** sums);
+
+/* The sums recomputed by the last ckpt_restore / ckpt_verify (n_chunks
+ * entries). Errors: ESTATE (none yet). */
+ckpt_status ckpt_last_sums(ckpt_ctx* ctx, uint64_t* sums, uint64_t n);
+
+/* Serialized metadata envelope of a committed snapshot: magic "CKPTENV1",
+ * version, alignment, step, chunk bytes, image bytes, chunk count, fragment
+ * count, blob length, fragment table (offset, bytes, dtype, class), chunk
+ * sums, caller blob zero-padded to 8 bytes, and the word-sum of all of it;
+ * little-endian.  *len receives the size; with cap too small nothing is
+ * written and EINVAL is returned.  Errors: ENOSNAP, ERANGE, EINVAL. */
+ckpt_status ckpt_envelope(ckpt_ctx* ctx, uint64_t snap_id, void* out, uint64_t cap, uint64_t* len);
+
+/* Fault injection for tests of invariant I4: the next snapshot issues only its
+ * first `groups` D2H copies and never commits (it reports ABORTED).  A
+ * negative value cancels. */
+ckpt_status ckpt_debug_interrupt_next(ckpt_ctx* ctx, int32_t groups);
+
+/* GPU timing of the last operation of each kind, from HIP events recorded
+ * on the library's own streams (enable with ckpt_set_timing(ctx, 1) before
+ * the operation; timing adds one event pair per kernel launch and per copy
+ * request).  which: 0 = snapshot, 1 = restore, 2 = verify.
+ * Errors: EINVAL (bad `which`), ESTATE (no timed operation of that kind). */
+typedef struct {
+    float kernel_ms;     /* sum of the kernel launches' durations */
+    uint32_t kernels;    /* number of kernel launches */
+    uint32_t copies;     /* number of DMA copy requests (image bytes only) */
+    float copy_ms;       /* first image copy start to last image copy end */
+    float total_ms;      /* operation start (after the trigger) to its last event */
+    uint64_t kernel_bytes; /* algorithmic HBM bytes of the kernels: 2*payload (pack,
+                              scatter) or image bytes (verify) */
+    uint64_t copy_bytes;   /* image bytes moved over the host link */
+} ckpt_timing;
+#define CKPT_OP_SNAPSHOT 0
+#define CKPT_OP_RESTORE 1
+#define CKPT_OP_VERIFY 2
+ckpt_status ckpt_set_timing(ckpt_ctx* ctx, int32_t enable);
+ckpt_status ckpt_last_timing(ckpt_ctx* ctx, uint32_t which, ckpt_timing* out);
+
+/* Host-only planning (no GPU, no context): the layout that
+ * ckpt_register_tensors() would compute for fragments of these sizes with
+ * this chunk size and alignment (0 = defaults).  frag_off (n entries) may be
+ * NULL.  Lets a caller size pinned and device memory before registering.
+ * Errors: EINVAL (bad geometry, n == 0, all fragments empty). */
+ckpt_status ckpt_plan(const uint64_t* nbytes, uint32_t n, uint64_t chunk_bytes, uint32_t align_bytes,
+                      uint64_t* frag_off, uint64_t* image_bytes, uint64_t* n_chunks);
+
+/* Test access to the kernels' tile table (host-only): the tile size and, per
+ * tile, the first and last fragment holding one of its bytes.  Call with
+ * tile_first == NULL to get *n_tiles first. */
+ckpt_status ckpt_debug_tile_plan(const uint64_t* nbytes, uint32_t n, uint64_t chunk_bytes, uint32_t align_bytes,
+                                 uint64_t* tile_bytes, uint64_t* n_tiles, uint32_t* tile_first,
+                                 uint32_t* tile_last);
+
+/* Text of the context's last error ("" if none).  Valid until the next call. */
+const char* ckpt_last_error(const ckpt_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CKPT_H */

@@ -1,0 +1,372 @@
+// ckpt_kernels.hip -- gfx950 kernels of libckpt.
+//
+// Three bandwidth-bound tile kernels over the snapshot image (the contiguous
+// buffer of the D2H phase, paper Sec. V-B):
+//   PACK     gather fragment bytes into the image window and sum each chunk,
+//   SCATTER  write an image window back into the fragments (recovery, paper
+//            Sec. VI-E) while re-summing and checking each chunk,
+//   VERIFY   re-sum and check an image window only.
+// The chunk sum is the sum of the chunk's 8-byte little-endian words modulo
+// 2^64 (padding included).  Bytes are moved as opaque 128-bit words: no
+// floating-point instruction touches them, so NaN payloads, -0 and
+// subnormals pass unchanged.
+//
+// Work split.  The image is cut into power-of-two tiles that never cross a
+// chunk.  A workgroup of 256 lanes (4 wave64) takes tiles grid-stride; each
+// lane moves 16-byte vectors.  A tile inside one 16-byte-aligned fragment
+// takes an unrolled non-temporal stream; otherwise each vector finds its
+// fragment (binary search over the tile's fragment offsets in LDS), loads
+// aligned 16-byte blocks and funnel-shifts them when the fragment is
+// misaligned, masks the fragment tail and writes zeros for padding.
+// Sum reduction: per lane in 64 bits, across the wave with lane shuffles,
+// across the 4 waves in LDS; then one atomic add per tile into the chunk's
+// accumulator.  The tile that finishes a chunk (a counter per chunk) reads
+// and clears the accumulator and writes the chunk result, so consecutive
+// launches need no clearing pass.  Addition modulo 2^64 is associative and
+// commutative, so any tile order gives the same bits.
+#include "ckpt_internal.h"
+
+namespace ckpt {
+namespace {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kBlock = 256;
+constexpr int kWaves = kBlock / 64;
+constexpr int kLdsFrags = 1024; // fragment offsets cached per tile
+constexpr int kUnroll = 4;      // 16-byte vectors in flight per lane on the streaming path
+
+enum Mode { PACK = 0, SCATTER = 1, VERIFY = 2 };
+
+struct Args {
+    const FragDev* frags;
+    const uint32_t* tile_first; // first fragment holding a byte of tile t
+    const uint32_t* tile_last;  // last fragment holding a byte of tile t
+    Geometry g;
+    uint64_t t_lo, t_hi;
+    uint8_t* img; // PACK: destination window; SCATTER/VERIFY: source window
+    uint64_t origin;
+    ChunkReduce red;
+    unsigned long long* sums_out; // PACK: chunk sums; SCATTER/VERIFY: recomputed sums
+    const unsigned long long* expected;
+    uint8_t* bad;
+};
+
+__device__ __forceinline__ unsigned long long vsum(u32x4 v)
+{
+    const unsigned long long w0 = (unsigned long long)v.x | ((unsigned long long)v.y << 32);
+    const unsigned long long w1 = (unsigned long long)v.z | ((unsigned long long)v.w << 32);
+    return w0 + w1;
+}
+
+__device__ __forceinline__ u32x4 load16(uint64_t a) { return *reinterpret_cast<const u32x4*>(a); }
+
+__device__ __forceinline__ u32x4 make4(uint64_t r0, uint64_t r1)
+{
+    u32x4 v;
+    v.x = (unsigned)r0;
+    v.y = (unsigned)(r0 >> 32);
+    v.z = (unsigned)r1;
+    v.w = (unsigned)(r1 >> 32);
+    return v;
+}
+
+// Bytes [p, p+16) of a fragment (ptr, nbytes), p a multiple of 16; bytes at
+// or past nbytes read as zero.  Only aligned 16-byte blocks that contain at
+// least one byte of the fragment are loaded.
+__device__ u32x4 fetch_general(uint64_t ptr, uint64_t nbytes, uint64_t p)
+{
+    u32x4 r = {0u, 0u, 0u, 0u};
+    if (p >= nbytes) return r;
+    const uint64_t left = nbytes - p;
+    const uint64_t a = ptr + p;
+    uint32_t s = (uint32_t)(a & 15);
+    if (s == 0 && left >= 16) return load16(a);
+    const uint64_t a0 = a - s;
+    const u32x4 lo = load16(a0); // holds byte a, a fragment byte
+    u32x4 hi = r;
+    if (s != 0 && a0 + 16 < ptr + nbytes) hi = load16(a0 + 16); // first byte is a fragment byte
+    uint64_t w0 = (uint64_t)lo.x | ((uint64_t)lo.y << 32);
+    uint64_t w1 = (uint64_t)lo.z | ((uint64_t)lo.w << 32);
+    uint64_t w2 = (uint64_t)hi.x | ((uint64_t)hi.y << 32);
+    const uint64_t w3 = (uint64_t)hi.z | ((uint64_t)hi.w << 32);
+    if (s >= 8) {
+        w0 = w1;
+        w1 = w2;
+        w2 = w3;
+        s -= 8;
+    }
+    uint64_t r0 = w0, r1 = w1;
+    if (s != 0) {
+        r0 = (w0 >> (8 * s)) | (w1 << (64 - 8 * s));
+        r1 = (w1 >> (8 * s)) | (w2 << (64 - 8 * s));
+    }
+    if (left < 16) {
+        if (left < 8) {
+            r0 &= (1ull << (8 * left)) - 1;
+            r1 = 0;
+        } else if (left == 8) {
+            r1 = 0;
+        } else {
+            r1 &= (1ull << (8 * (left - 8))) - 1;
+        }
+    }
+    return make4(r0, r1);
+}
+
+// Write the fragment bytes among [p, p+16) from v; p a multiple of 16.
+// Stores never touch a byte outside the fragment.
+__device__ void store_general(uint64_t ptr, uint64_t nbytes, uint64_t p, u32x4 v)
+{
+    if (p >= nbytes) return;
+    const uint64_t left = nbytes - p;
+    const uint64_t d = ptr + p;
+    if ((d & 15) == 0 && left >= 16) {
+        *reinterpret_cast<u32x4*>(d) = v;
+        return;
+    }
+    const uint32_t nb = left < 16 ? (uint32_t)left : 16u;
+    const unsigned w[4] = {v.x, v.y, v.z, v.w};
+    if ((d & 3) == 0 && (nb & 3) == 0) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            if (4u * k < nb) reinterpret_cast<unsigned*>(d)[k] = w[k];
+    } else if ((d & 1) == 0 && (nb & 1) == 0) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+            if (2u * k < nb) reinterpret_cast<unsigned short*>(d)[k] = (unsigned short)(w[k >> 1] >> (16 * (k & 1)));
+    } else {
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+            if ((uint32_t)k < nb) reinterpret_cast<unsigned char*>(d)[k] = (unsigned char)(w[k >> 2] >> (8 * (k & 3)));
+    }
+}
+
+// Streaming copy of nvec aligned 16-byte vectors with their sum.
+__device__ __forceinline__ unsigned long long stream_copy(const u32x4* __restrict__ s, u32x4* __restrict__ d,
+                                                          uint32_t nvec, uint32_t tid)
+{
+    unsigned long long acc = 0;
+    uint32_t v = tid;
+    for (; v + (kUnroll - 1) * kBlock < nvec; v += kUnroll * kBlock) {
+        u32x4 r[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) r[u] = __builtin_nontemporal_load(s + v + u * kBlock);
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            __builtin_nontemporal_store(r[u], d + v + u * kBlock);
+            acc += vsum(r[u]);
+        }
+    }
+    for (; v < nvec; v += kBlock) {
+        const u32x4 r = __builtin_nontemporal_load(s + v);
+        __builtin_nontemporal_store(r, d + v);
+        acc += vsum(r);
+    }
+    return acc;
+}
+
+__device__ __forceinline__ unsigned long long stream_sum(const u32x4* __restrict__ s, uint32_t nvec, uint32_t tid)
+{
+    unsigned long long acc = 0;
+    uint32_t v = tid;
+    for (; v + (kUnroll - 1) * kBlock < nvec; v += kUnroll * kBlock) {
+        u32x4 r[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) r[u] = __builtin_nontemporal_load(s + v + u * kBlock);
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) acc += vsum(r[u]);
+    }
+    for (; v < nvec; v += kBlock) acc += vsum(__builtin_nontemporal_load(s + v));
+    return acc;
+}
+
+__device__ __forceinline__ unsigned long long shfl_xor64(unsigned long long v, int m)
+{
+    const unsigned lo = __shfl_xor((unsigned)v, m);
+    const unsigned hi = __shfl_xor((unsigned)(v >> 32), m);
+    return ((unsigned long long)hi << 32) | lo;
+}
+
+// Sum over the workgroup; the result is valid in thread 0.
+__device__ __forceinline__ unsigned long long block_sum(unsigned long long v, unsigned long long* s_red)
+{
+#pragma unroll
+    for (int m = 32; m > 0; m >>= 1) v += shfl_xor64(v, m);
+    const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) s_red[wave] = v;
+    __syncthreads();
+    unsigned long long r = 0;
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) r += s_red[w];
+    }
+    __syncthreads();
+    return r;
+}
+
+template <int MODE>
+__device__ __forceinline__ void chunk_result(const Args& a, uint64_t c, unsigned long long s)
+{
+    a.sums_out[c] = s;
+    if (MODE != PACK) a.bad[c] = (s != a.expected[c]) ? 1 : 0;
+}
+
+// Called by thread 0 with the tile's sum.
+template <int MODE>
+__device__ void finish_tile(const Args& a, uint64_t t, unsigned long long tile_sum)
+{
+    const uint64_t c = t / a.g.tiles_per_chunk;
+    const uint32_t tiles_in =
+        (c + 1 < a.g.n_chunks) ? a.g.tiles_per_chunk : (uint32_t)(a.g.n_tiles - c * a.g.tiles_per_chunk);
+    if (tiles_in == 1) {
+        chunk_result<MODE>(a, c, tile_sum);
+        return;
+    }
+    atomicAdd(&a.red.acc[c], tile_sum);
+    __threadfence();
+    const unsigned prev = atomicAdd(&a.red.done[c], 1u);
+    if (prev + 1 == tiles_in) {
+        __threadfence();
+        const unsigned long long s = atomicExch(&a.red.acc[c], 0ull);
+        atomicExch(&a.red.done[c], 0u);
+        chunk_result<MODE>(a, c, s);
+    }
+}
+
+// Index (relative to f0) of the fragment holding image byte x: the largest k
+// with s_off[k] <= x.  Empty fragments share their offset with the next
+// fragment, so the largest such k is never an empty one.
+__device__ __forceinline__ uint32_t find_frag_lds(const uint64_t* s_off, uint32_t n, uint64_t x)
+{
+    uint32_t lo = 0, hi = n - 1;
+    while (lo < hi) {
+        const uint32_t mid = (lo + hi + 1) >> 1;
+        if (s_off[mid] <= x) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ uint32_t find_frag_global(const FragDev* frags, uint32_t f0, uint32_t f1, uint64_t x)
+{
+    uint32_t lo = f0, hi = f1;
+    while (lo < hi) {
+        const uint32_t mid = lo + ((hi - lo + 1) >> 1);
+        if (frags[mid].off <= x) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
+template <int MODE>
+__global__ __launch_bounds__(kBlock) void tile_kernel(Args a)
+{
+    __shared__ unsigned long long s_red[kWaves];
+    __shared__ uint64_t s_off[kLdsFrags];
+    const uint32_t tid = threadIdx.x;
+    for (uint64_t t = a.t_lo + blockIdx.x; t < a.t_hi; t += gridDim.x) {
+        const uint64_t base = t << a.g.tile_shift;
+        uint64_t end = base + (1ull << a.g.tile_shift);
+        if (end > a.g.image_bytes) end = a.g.image_bytes;
+        const uint32_t nvec = (uint32_t)((end - base) >> 4);
+        uint8_t* win = a.img + (base - a.origin);
+        unsigned long long acc = 0;
+        if (MODE == VERIFY) {
+            acc = stream_sum(reinterpret_cast<const u32x4*>(win), nvec, tid);
+        } else {
+            const uint32_t f0 = a.tile_first[t], f1 = a.tile_last[t];
+            if (f0 == f1) {
+                const FragDev F = a.frags[f0];
+                const uint64_t p0 = base - F.off;
+                if ((F.ptr & 15) == 0 && p0 + (end - base) <= F.nbytes) {
+                    u32x4* fr = reinterpret_cast<u32x4*>(F.ptr + p0);
+                    if (MODE == PACK) acc = stream_copy(fr, reinterpret_cast<u32x4*>(win), nvec, tid);
+                    else acc = stream_copy(reinterpret_cast<const u32x4*>(win), fr, nvec, tid);
+                } else {
+                    for (uint32_t v = tid; v < nvec; v += kBlock) {
+                        const uint64_t p = p0 + 16ull * v;
+                        u32x4* w = reinterpret_cast<u32x4*>(win) + v;
+                        if (MODE == PACK) {
+                            const u32x4 r = fetch_general(F.ptr, F.nbytes, p);
+                            __builtin_nontemporal_store(r, w);
+                            acc += vsum(r);
+                        } else {
+                            const u32x4 r = __builtin_nontemporal_load(w);
+                            store_general(F.ptr, F.nbytes, p, r);
+                            acc += vsum(r);
+                        }
+                    }
+                }
+            } else {
+                const uint32_t nf = f1 - f0 + 1;
+                const bool in_lds = nf <= (uint32_t)kLdsFrags;
+                if (in_lds) {
+                    for (uint32_t k = tid; k < nf; k += kBlock) s_off[k] = a.frags[f0 + k].off;
+                }
+                __syncthreads();
+                for (uint32_t v = tid; v < nvec; v += kBlock) {
+                    const uint64_t x = base + 16ull * v;
+                    const uint32_t i = in_lds ? f0 + find_frag_lds(s_off, nf, x) : find_frag_global(a.frags, f0, f1, x);
+                    const FragDev F = a.frags[i];
+                    const uint64_t p = x - F.off;
+                    u32x4* w = reinterpret_cast<u32x4*>(win) + v;
+                    if (MODE == PACK) {
+                        const u32x4 r = fetch_general(F.ptr, F.nbytes, p);
+                        __builtin_nontemporal_store(r, w);
+                        acc += vsum(r);
+                    } else {
+                        const u32x4 r = __builtin_nontemporal_load(w);
+                        store_general(F.ptr, F.nbytes, p, r);
+                        acc += vsum(r);
+                    }
+                }
+            }
+        }
+        // block_sum's barriers also retire every lane's use of s_off before
+        // the next tile refills it.
+        const unsigned long long tile_sum = block_sum(acc, s_red);
+        if (tid == 0) finish_tile<MODE>(a, t, tile_sum);
+    }
+}
+
+template <int MODE>
+hipError_t launch(const Args& a, uint32_t grid_cap, hipStream_t s)
+{
+    if (a.t_hi <= a.t_lo) return hipSuccess;
+    const uint64_t n = a.t_hi - a.t_lo;
+    const uint32_t grid = (uint32_t)(n < grid_cap ? n : grid_cap);
+    hipLaunchKernelGGL(tile_kernel<MODE>, dim3(grid), dim3(kBlock), 0, s, a);
+    return hipGetLastError();
+}
+
+} // namespace
+
+hipError_t launch_pack(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
+                       const Geometry& g, uint64_t t_lo, uint64_t t_hi, uint8_t* dst, uint64_t dst_origin,
+                       ChunkReduce red, unsigned long long* sums_out, uint32_t grid_cap, hipStream_t s)
+{
+    Args a{frags, tile_first, tile_last, g, t_lo, t_hi, dst, dst_origin, red, sums_out, nullptr, nullptr};
+    return launch<PACK>(a, grid_cap, s);
+}
+
+hipError_t launch_scatter_verify(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
+                                 const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src,
+                                 uint64_t src_origin, ChunkReduce red, const unsigned long long* expected,
+                                 unsigned long long* recomputed, uint8_t* bad, uint32_t grid_cap, hipStream_t s)
+{
+    Args a{frags, tile_first, tile_last, g, t_lo, t_hi, const_cast<uint8_t*>(src), src_origin, red, recomputed,
+           expected, bad};
+    return launch<SCATTER>(a, grid_cap, s);
+}
+
+hipError_t launch_checksum_verify(const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src,
+                                  uint64_t src_origin, ChunkReduce red, const unsigned long long* expected,
+                                  unsigned long long* recomputed, uint8_t* bad, uint32_t grid_cap, hipStream_t s)
+{
+    Args a{nullptr, nullptr, nullptr, g, t_lo, t_hi, const_cast<uint8_t*>(src), src_origin, red, recomputed,
+           expected, bad};
+    return launch<VERIFY>(a, grid_cap, s);
+}
+
+} // namespace ckpt

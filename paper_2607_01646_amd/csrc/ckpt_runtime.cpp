@@ -1,0 +1,987 @@
+// ckpt_runtime.cpp -- host side of libckpt (the C ABI of include/ckpt.h).
+//
+// Pipeline of one snapshot (paper Sec. V-B, D2H phase; Sec. VI-A):
+//   caller stream --event--> pack stream: for each chunk group g
+//       [wait until the copy that last read g's staging area is done]
+//       pack kernel (fragments -> staging, chunk sums)   -> event captured[g]
+//   copy stream: for each group g
+//       wait captured[g]; DMA staging -> pinned host image; event area_free
+//   copy stream: DMA chunk sums -> pinned sums; event commit
+// The two pinned host images alternate (ping-pong): a snapshot targets the
+// image that does not hold the newest live (in-flight or committed)
+// snapshot.  Because one copy stream carries every snapshot's copies in
+// order, a snapshot's first byte lands only after the previous snapshot's
+// commit event, so a committed image exists at every point (invariant I4 of
+// Sec. V-C: an unfinished snapshot is never the recovery point).
+// "Committed" is the completion of the commit event; it is queried, not
+// signalled, so the library runs no helper thread.
+//
+// Recovery (Sec. V-C third stage, Sec. VI-E) reverses the path group by
+// group: DMA host image -> staging on the copy stream, then the scatter
+// kernel on the pack stream writes the fragments and checks the sums.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "../../include/ckpt.h"
+#include "ckpt_internal.h"
+
+using namespace ckpt;
+
+namespace {
+
+constexpr uint64_t kDefaultChunk = 64ull << 20;
+constexpr uint32_t kDefaultAlign = 256;
+constexpr uint64_t kDefaultGroup = 1ull << 30;
+constexpr uint32_t kMaxTileShift = 16; // 64 KiB tiles at most
+constexpr uint32_t kMaxMeta = 1u << 20;
+constexpr uint32_t kDefaultGrid = 2048; // 256 CUs x 8 workgroups
+
+struct Frag {
+    uint64_t ptr, nbytes, off;
+    uint32_t dtype, cls;
+};
+
+// GPU resources of one snapshot record, recycled between snapshots.
+struct RecRes {
+    std::vector<hipEvent_t> captured; // per group, on the pack stream
+    hipEvent_t commit = nullptr;      // on the copy stream, after the sums landed
+    unsigned long long* d_sums = nullptr;
+    // timing (only with timing on)
+    std::vector<hipEvent_t> k0, k1; // per group around the pack launch
+    hipEvent_t t0 = nullptr, c0 = nullptr, c1 = nullptr;
+};
+
+struct SnapRec {
+    uint64_t id = 0, step = 0;
+    int buf = -1;
+    bool aborted = false;
+    bool committed = false; // cached once the commit event has completed
+    bool timed = false;
+    uint32_t groups_copied = 0;
+    std::vector<uint8_t> meta;
+    RecRes* res = nullptr;
+};
+
+struct OpTiming {
+    bool valid = false;
+    ckpt_timing t{};
+};
+
+} // namespace
+
+struct ckpt_ctx {
+    // configuration
+    int device = 0;
+    uint64_t C = kDefaultChunk;
+    uint32_t A = kDefaultAlign;
+    uint64_t staging_cap = 0; // 0 = full image
+    uint64_t group_cfg = kDefaultGroup;
+    uint32_t grid_cap = kDefaultGrid;
+    bool timing = false;
+
+    // layout
+    bool registered = false;
+    std::vector<Frag> frags;
+    uint64_t I = 0, n_chunks = 0, payload = 0;
+    Geometry geo{};
+    uint64_t G = 1;        // chunks per group
+    uint64_t n_groups = 0; // groups
+    bool ring = false;
+    uint64_t n_slots = 0;  // ring slots (ring mode)
+    std::vector<uint64_t> group_payload; // fragment bytes inside each group
+
+    // device memory
+    FragDev* d_frags = nullptr;
+    uint32_t* d_tile_first = nullptr;
+    uint32_t* d_tile_last = nullptr;
+    uint8_t* d_staging = nullptr;
+    unsigned long long* d_acc = nullptr; // [2][n_chunks]: pack, check
+    unsigned int* d_done = nullptr;      // [2][n_chunks]
+    unsigned long long* d_expected = nullptr;
+    unsigned long long* d_recomputed = nullptr;
+    uint8_t* d_bad = nullptr;
+
+    // pinned host memory
+    uint8_t* h_img[2] = {nullptr, nullptr};
+    uint64_t* h_sums[2] = {nullptr, nullptr};
+    uint64_t holder[2] = {0, 0}; // snapshot id whose bytes each image holds (0 = none)
+    uint8_t* h_bad = nullptr;
+    unsigned long long* h_recomputed = nullptr;
+
+    // streams and events
+    hipStream_t s_pack = nullptr, s_copy = nullptr;
+    hipEvent_t ev_trigger = nullptr, ev_done = nullptr;
+    std::vector<hipEvent_t> area_free; // per staging area (group in full mode, slot in ring mode)
+    std::vector<hipEvent_t> ev_loaded; // per group, restore/verify
+    std::vector<RecRes*> free_res;
+    std::map<uint64_t, SnapRec> recs;
+    uint64_t next_id = 1;
+    int32_t interrupt_next = -1;
+
+    // results of the last restore / verify
+    bool have_last_sums = false;
+    std::vector<uint64_t> last_sums;
+    OpTiming op_timing[3];
+
+    std::string err;
+};
+
+namespace {
+
+ckpt_status fail(ckpt_ctx* c, ckpt_status code, const char* fmt, ...)
+{
+    if (c) {
+        char buf[512];
+        va_list ap;
+        va_start(ap, fmt);
+        vsnprintf(buf, sizeof buf, fmt, ap);
+        va_end(ap);
+        c->err = buf;
+    }
+    return code;
+}
+
+#define HIPCHK(ctx, expr)                                                                                    \
+    do {                                                                                                     \
+        hipError_t e_ = (expr);                                                                              \
+        if (e_ != hipSuccess)                                                                                \
+            return fail((ctx), CKPT_EHIP, "%s failed: %s (%d)", #expr, hipGetErrorString(e_), (int)e_);       \
+    } while (0)
+
+bool is_pow2(uint64_t x) { return x && !(x & (x - 1)); }
+uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
+bool geometry_ok(uint64_t C, uint32_t A) { return is_pow2(A) && A >= 16 && A <= 4096 && C && C % A == 0; }
+
+// Layout and tile table of a fragment list (no GPU involved).
+struct Plan {
+    std::vector<uint64_t> off, end; // image offset and end of the padded span per fragment
+    uint64_t I = 0, n_chunks = 0, n_tiles = 0;
+    uint32_t tile_shift = 4;
+    std::vector<uint32_t> tile_first, tile_last;
+};
+
+bool plan(const uint64_t* nb, uint32_t n, uint64_t C, uint32_t A, Plan* p, bool tiles = true)
+{
+    // Registration order; each fragment starts at the previous end rounded
+    // up to the alignment; the image ends on the alignment too.
+    p->off.resize(n);
+    p->end.resize(n);
+    uint64_t end = 0;
+    for (uint32_t i = 0; i < n; ++i) {
+        p->off[i] = round_up(end, A);
+        end = p->off[i] + nb[i];
+    }
+    p->I = round_up(end, A);
+    if (p->I == 0) return false;
+    for (uint32_t i = 0; i < n; ++i) p->end[i] = (i + 1 < n) ? p->off[i + 1] : p->I;
+    p->n_chunks = (p->I + C - 1) / C;
+    // Tiles: the largest power of two <= 64 KiB dividing the chunk size.
+    uint32_t ts = 4;
+    while (ts < kMaxTileShift && C % (1ull << (ts + 1)) == 0) ++ts;
+    p->tile_shift = ts;
+    p->n_tiles = (p->I + (1ull << ts) - 1) >> ts;
+    if (!tiles) return true;
+    p->tile_first.resize(p->n_tiles);
+    p->tile_last.resize(p->n_tiles);
+    // The fragment holding byte x is the first one whose padded span
+    // [off, end) ends past x (empty fragments have empty spans).
+    uint32_t i = 0;
+    for (uint64_t t = 0; t < p->n_tiles; ++t) {
+        const uint64_t x0 = t << ts;
+        const uint64_t x1 = std::min<uint64_t>(x0 + (1ull << ts), p->I) - 1;
+        while (i + 1 < n && p->end[i] <= x0) ++i;
+        p->tile_first[t] = i;
+        uint32_t j = i;
+        while (j + 1 < n && p->end[j] <= x1) ++j;
+        p->tile_last[t] = j;
+    }
+    return true;
+}
+
+uint64_t group_lo(const ckpt_ctx* c, uint64_t g) { return g * c->G * c->C; }
+uint64_t group_hi(const ckpt_ctx* c, uint64_t g) { return std::min((g + 1) * c->G * c->C, c->I); }
+uint64_t tiles_lo(const ckpt_ctx* c, uint64_t g) { return group_lo(c, g) >> c->geo.tile_shift; }
+uint64_t tiles_hi(const ckpt_ctx* c, uint64_t g)
+{
+    return (group_hi(c, g) + (1ull << c->geo.tile_shift) - 1) >> c->geo.tile_shift;
+}
+uint64_t area_of(const ckpt_ctx* c, uint64_t g) { return c->ring ? g % c->n_slots : g; }
+uint8_t* staging_of(const ckpt_ctx* c, uint64_t g)
+{
+    return c->ring ? c->d_staging + (g % c->n_slots) * c->C : c->d_staging + group_lo(c, g);
+}
+
+ckpt_status make_event(ckpt_ctx* c, hipEvent_t* e, bool timed)
+{
+    HIPCHK(c, hipEventCreateWithFlags(e, timed ? hipEventDefault : hipEventDisableTiming));
+    return CKPT_OK;
+}
+
+void destroy_res(RecRes* r)
+{
+    for (auto e : r->captured) (void)hipEventDestroy(e);
+    for (auto e : r->k0) (void)hipEventDestroy(e);
+    for (auto e : r->k1) (void)hipEventDestroy(e);
+    if (r->commit) (void)hipEventDestroy(r->commit);
+    if (r->t0) (void)hipEventDestroy(r->t0);
+    if (r->c0) (void)hipEventDestroy(r->c0);
+    if (r->c1) (void)hipEventDestroy(r->c1);
+    if (r->d_sums) (void)hipFree(r->d_sums);
+    delete r;
+}
+
+ckpt_status get_res(ckpt_ctx* c, RecRes** out)
+{
+    if (!c->free_res.empty()) {
+        *out = c->free_res.back();
+        c->free_res.pop_back();
+        return CKPT_OK;
+    }
+    RecRes* r = new RecRes();
+    r->captured.resize(c->n_groups, nullptr);
+    r->k0.resize(c->n_groups, nullptr);
+    r->k1.resize(c->n_groups, nullptr);
+    ckpt_status st = CKPT_OK;
+    for (uint64_t g = 0; g < c->n_groups && st == CKPT_OK; ++g) {
+        st = make_event(c, &r->captured[g], false);
+        if (st == CKPT_OK) st = make_event(c, &r->k0[g], true);
+        if (st == CKPT_OK) st = make_event(c, &r->k1[g], true);
+    }
+    if (st == CKPT_OK) st = make_event(c, &r->commit, false);
+    if (st == CKPT_OK) st = make_event(c, &r->t0, true);
+    if (st == CKPT_OK) st = make_event(c, &r->c0, true);
+    if (st == CKPT_OK) st = make_event(c, &r->c1, true);
+    if (st == CKPT_OK && hipMalloc(&r->d_sums, std::max<uint64_t>(c->n_chunks, 1) * 8) != hipSuccess) {
+        r->d_sums = nullptr;
+        st = fail(c, CKPT_ENOMEM, "hipMalloc of %llu chunk sums failed", (unsigned long long)c->n_chunks);
+    }
+    if (st != CKPT_OK) {
+        destroy_res(r);
+        return st;
+    }
+    *out = r;
+    return CKPT_OK;
+}
+
+// Is the snapshot's commit event complete?  (Never true for an aborted one.)
+ckpt_status query_committed(ckpt_ctx* c, SnapRec& r, bool* out)
+{
+    if (r.aborted) {
+        *out = false;
+        return CKPT_OK;
+    }
+    if (!r.committed) {
+        hipError_t q = hipEventQuery(r.res->commit);
+        if (q == hipSuccess) r.committed = true;
+        else if (q != hipErrorNotReady)
+            return fail(c, CKPT_EHIP, "hipEventQuery(commit) failed: %s", hipGetErrorString(q));
+    }
+    *out = r.committed;
+    return CKPT_OK;
+}
+
+// Drop records that are neither among the newest four nor held by an image.
+void prune(ckpt_ctx* c)
+{
+    for (auto it = c->recs.begin(); it != c->recs.end();) {
+        SnapRec& r = it->second;
+        const bool held = (c->holder[0] == r.id || c->holder[1] == r.id);
+        bool done = r.aborted || r.committed;
+        if (!done) {
+            hipError_t q = hipEventQuery(r.res->commit);
+            done = (q == hipSuccess);
+            if (done) r.committed = true;
+        }
+        if (!held && done && r.id + 4 < c->next_id) {
+            c->free_res.push_back(r.res);
+            it = c->recs.erase(it);
+        } else {
+            ++it;
+        }
+    }
+}
+
+ckpt_status drain(ckpt_ctx* c)
+{
+    HIPCHK(c, hipStreamSynchronize(c->s_pack));
+    HIPCHK(c, hipStreamSynchronize(c->s_copy));
+    return CKPT_OK;
+}
+
+// Resolve snap_id (0 = newest committed) to a committed, still-held record.
+ckpt_status pick_committed(ckpt_ctx* c, uint64_t snap_id, SnapRec** out)
+{
+    SnapRec* best = nullptr;
+    for (auto& kv : c->recs) {
+        SnapRec& r = kv.second;
+        bool com = false;
+        ckpt_status st = query_committed(c, r, &com);
+        if (st) return st;
+        if (!com || c->holder[r.buf] != r.id) continue;
+        if (snap_id != 0 && r.id != snap_id) continue;
+        if (!best || r.id > best->id) best = &r;
+    }
+    if (!best) {
+        if (snap_id != 0 && !c->recs.count(snap_id) && snap_id >= c->next_id)
+            return fail(c, CKPT_ERANGE, "snapshot %llu does not exist", (unsigned long long)snap_id);
+        return fail(c, CKPT_ENOSNAP, "no committed snapshot%s", snap_id ? " with that id is still held" : "");
+    }
+    *out = best;
+    return CKPT_OK;
+}
+
+float elapsed(hipEvent_t a, hipEvent_t b)
+{
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, a, b) != hipSuccess) return -1.f;
+    return ms;
+}
+
+// Restore (scatter=true) or verify (scatter=false) from a committed image.
+ckpt_status run_check(ckpt_ctx* c, uint64_t snap_id, hipStream_t stream, bool scatter, uint32_t* bad_chunks,
+                      uint32_t cap, uint32_t* n_bad)
+{
+    if (!c->registered) return fail(c, CKPT_ESTATE, "no tensors registered");
+    if (!n_bad || (cap && !bad_chunks)) return fail(c, CKPT_EINVAL, "null output pointer");
+    HIPCHK(c, hipSetDevice(c->device));
+    ckpt_status st = drain(c);
+    if (st) return st;
+    SnapRec* r = nullptr;
+    st = pick_committed(c, snap_id, &r);
+    if (st) return st;
+    const int b = r->buf;
+    const int op = scatter ? CKPT_OP_RESTORE : CKPT_OP_VERIFY;
+    RecRes* tr = nullptr; // timing events borrowed from a free record
+    if (c->timing) {
+        st = get_res(c, &tr);
+        if (st) return st;
+    }
+    ChunkReduce red{c->d_acc + c->n_chunks, c->d_done + c->n_chunks};
+    HIPCHK(c, hipMemcpyAsync(c->d_expected, c->h_sums[b], c->n_chunks * 8, hipMemcpyHostToDevice, c->s_copy));
+    if (scatter) {
+        HIPCHK(c, hipEventRecord(c->ev_trigger, stream));
+        HIPCHK(c, hipStreamWaitEvent(c->s_pack, c->ev_trigger, 0));
+    }
+    if (tr) HIPCHK(c, hipEventRecord(tr->t0, c->s_copy));
+    for (uint64_t g = 0; g < c->n_groups; ++g) {
+        const uint64_t lo = group_lo(c, g), hi = group_hi(c, g);
+        HIPCHK(c, hipStreamWaitEvent(c->s_copy, c->area_free[area_of(c, g)], 0));
+        if (tr && g == 0) HIPCHK(c, hipEventRecord(tr->c0, c->s_copy));
+        HIPCHK(c, hipMemcpyAsync(staging_of(c, g), c->h_img[b] + lo, hi - lo, hipMemcpyHostToDevice, c->s_copy));
+        if (tr && g + 1 == c->n_groups) HIPCHK(c, hipEventRecord(tr->c1, c->s_copy));
+        HIPCHK(c, hipEventRecord(c->ev_loaded[g], c->s_copy));
+        HIPCHK(c, hipStreamWaitEvent(c->s_pack, c->ev_loaded[g], 0));
+        if (tr) HIPCHK(c, hipEventRecord(tr->k0[g], c->s_pack));
+        const uint64_t t_lo = tiles_lo(c, g), t_hi = tiles_hi(c, g);
+        hipError_t e;
+        if (scatter)
+            e = launch_scatter_verify(c->d_frags, c->d_tile_first, c->d_tile_last, c->geo, t_lo, t_hi,
+                                      staging_of(c, g), lo, red, c->d_expected, c->d_recomputed, c->d_bad,
+                                      c->grid_cap, c->s_pack);
+        else
+            e = launch_checksum_verify(c->geo, t_lo, t_hi, staging_of(c, g), lo, red, c->d_expected,
+                                       c->d_recomputed, c->d_bad, c->grid_cap, c->s_pack);
+        if (e != hipSuccess) return fail(c, CKPT_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
+        if (tr) HIPCHK(c, hipEventRecord(tr->k1[g], c->s_pack));
+        HIPCHK(c, hipEventRecord(c->area_free[area_of(c, g)], c->s_pack));
+    }
+    HIPCHK(c, hipMemcpyAsync(c->h_bad, c->d_bad, c->n_chunks, hipMemcpyDeviceToHost, c->s_pack));
+    HIPCHK(c, hipMemcpyAsync(c->h_recomputed, c->d_recomputed, c->n_chunks * 8, hipMemcpyDeviceToHost, c->s_pack));
+    HIPCHK(c, hipEventRecord(c->ev_done, c->s_pack));
+    if (scatter) HIPCHK(c, hipStreamWaitEvent(stream, c->ev_done, 0));
+    HIPCHK(c, hipEventSynchronize(c->ev_done));
+    if (tr) {
+        ckpt_timing t{};
+        for (uint64_t g = 0; g < c->n_groups; ++g) t.kernel_ms += elapsed(tr->k0[g], tr->k1[g]);
+        t.kernels = (uint32_t)c->n_groups;
+        t.copies = (uint32_t)c->n_groups;
+        t.copy_ms = elapsed(tr->c0, tr->c1);
+        t.total_ms = elapsed(tr->t0, tr->k1[c->n_groups - 1]);
+        t.kernel_bytes = scatter ? 2 * c->payload : c->I;
+        t.copy_bytes = c->I;
+        c->op_timing[op].t = t;
+        c->op_timing[op].valid = true;
+        c->free_res.push_back(tr);
+    }
+    c->last_sums.assign(c->h_recomputed, c->h_recomputed + c->n_chunks);
+    c->have_last_sums = true;
+    uint32_t nb = 0;
+    for (uint64_t k = 0; k < c->n_chunks; ++k) {
+        if (c->h_bad[k]) {
+            if (nb < cap) bad_chunks[nb] = (uint32_t)k;
+            ++nb;
+        }
+    }
+    *n_bad = nb;
+    if (nb) return fail(c, CKPT_ECORRUPT, "%u of %llu chunks failed their checksum", nb,
+                        (unsigned long long)c->n_chunks);
+    return CKPT_OK;
+}
+
+void free_ctx(ckpt_ctx* c)
+{
+    for (auto& kv : c->recs) c->free_res.push_back(kv.second.res);
+    c->recs.clear();
+    for (auto r : c->free_res) destroy_res(r);
+    c->free_res.clear();
+    for (auto e : c->area_free) (void)hipEventDestroy(e);
+    for (auto e : c->ev_loaded) (void)hipEventDestroy(e);
+    if (c->ev_trigger) (void)hipEventDestroy(c->ev_trigger);
+    if (c->ev_done) (void)hipEventDestroy(c->ev_done);
+    (void)hipFree(c->d_frags);
+    (void)hipFree(c->d_tile_first);
+    (void)hipFree(c->d_tile_last);
+    (void)hipFree(c->d_staging);
+    (void)hipFree(c->d_acc);
+    (void)hipFree(c->d_done);
+    (void)hipFree(c->d_expected);
+    (void)hipFree(c->d_recomputed);
+    (void)hipFree(c->d_bad);
+    for (int b = 0; b < 2; ++b) {
+        if (c->h_img[b]) (void)hipHostFree(c->h_img[b]);
+        if (c->h_sums[b]) (void)hipHostFree(c->h_sums[b]);
+    }
+    if (c->h_bad) (void)hipHostFree(c->h_bad);
+    if (c->h_recomputed) (void)hipHostFree(c->h_recomputed);
+    if (c->s_pack) (void)hipStreamDestroy(c->s_pack);
+    if (c->s_copy) (void)hipStreamDestroy(c->s_copy);
+}
+
+} // namespace
+
+extern "C" {
+
+ckpt_status ckpt_create(const ckpt_config* cfg, ckpt_ctx** out)
+{
+    if (!out) return CKPT_EINVAL;
+    *out = nullptr;
+    ckpt_config d{};
+    if (cfg) d = *cfg;
+    const uint64_t C = d.chunk_bytes ? d.chunk_bytes : kDefaultChunk;
+    const uint32_t A = d.align_bytes ? d.align_bytes : kDefaultAlign;
+    if (!geometry_ok(C, A)) return CKPT_EINVAL;
+    if (d.host_buffers != 0 && d.host_buffers != 2) return CKPT_EINVAL;
+    if (d.device_staging_bytes && d.device_staging_bytes < 2 * C) return CKPT_EINVAL;
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || d.device < 0 || d.device >= ndev) return CKPT_EINVAL;
+    ckpt_ctx* c = new ckpt_ctx();
+    c->device = d.device;
+    c->C = C;
+    c->A = A;
+    c->staging_cap = d.device_staging_bytes;
+    c->group_cfg = d.group_bytes ? d.group_bytes : kDefaultGroup;
+    c->grid_cap = d.grid_blocks ? d.grid_blocks : kDefaultGrid;
+    ckpt_status st = CKPT_OK;
+    if (hipSetDevice(c->device) != hipSuccess ||
+        hipStreamCreateWithFlags(&c->s_pack, hipStreamNonBlocking) != hipSuccess ||
+        hipStreamCreateWithFlags(&c->s_copy, hipStreamNonBlocking) != hipSuccess)
+        st = CKPT_EHIP;
+    if (st == CKPT_OK) st = make_event(c, &c->ev_trigger, false);
+    if (st == CKPT_OK) st = make_event(c, &c->ev_done, false);
+    if (st != CKPT_OK) {
+        free_ctx(c);
+        delete c;
+        return st;
+    }
+    *out = c;
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_destroy(ckpt_ctx* ctx)
+{
+    if (!ctx) return CKPT_OK;
+    (void)hipSetDevice(ctx->device);
+    if (ctx->s_pack) (void)hipStreamSynchronize(ctx->s_pack);
+    if (ctx->s_copy) (void)hipStreamSynchronize(ctx->s_copy);
+    free_ctx(ctx);
+    delete ctx;
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
+{
+    if (!c) return CKPT_EINVAL;
+    if (c->registered) return fail(c, CKPT_ESTATE, "tensors already registered");
+    if (!t || n == 0) return fail(c, CKPT_EINVAL, "need at least one fragment");
+    HIPCHK(c, hipSetDevice(c->device));
+
+    std::vector<uint64_t> nb(n), off(n);
+    for (uint32_t i = 0; i < n; ++i) {
+        if (t[i].nbytes && !t[i].dev_ptr) return fail(c, CKPT_EINVAL, "fragment %u: null pointer", i);
+        nb[i] = t[i].nbytes;
+    }
+    Plan pl;
+    if (!plan(nb.data(), n, c->C, c->A, &pl)) return fail(c, CKPT_EINVAL, "all fragments are empty");
+    c->frags.resize(n);
+    uint64_t payload = 0;
+    for (uint32_t i = 0; i < n; ++i) {
+        Frag& f = c->frags[i];
+        f.ptr = (uint64_t)(uintptr_t)t[i].dev_ptr;
+        f.nbytes = nb[i];
+        f.dtype = t[i].dtype;
+        f.cls = t[i].cls;
+        f.off = pl.off[i];
+        payload += nb[i];
+    }
+    c->I = pl.I;
+    c->payload = payload;
+    c->n_chunks = pl.n_chunks;
+    c->geo.image_bytes = c->I;
+    c->geo.tile_shift = pl.tile_shift;
+    c->geo.tiles_per_chunk = (uint32_t)(c->C >> pl.tile_shift);
+    c->geo.n_tiles = pl.n_tiles;
+    c->geo.n_chunks = c->n_chunks;
+    const uint32_t ts = pl.tile_shift;
+
+    // Groups: whole chunks per pack launch / DMA request; one chunk per slot in ring mode.
+    if (c->staging_cap) {
+        c->ring = true;
+        c->G = 1;
+        c->n_slots = std::min<uint64_t>(c->staging_cap / c->C, c->n_chunks);
+        if (c->n_slots < 1) c->n_slots = 1;
+    } else {
+        c->G = std::max<uint64_t>(1, c->group_cfg / c->C);
+    }
+    c->n_groups = (c->n_chunks + c->G - 1) / c->G;
+
+    std::vector<FragDev> fd(n);
+    for (uint32_t i = 0; i < n; ++i) {
+        fd[i].ptr = c->frags[i].ptr;
+        fd[i].nbytes = nb[i];
+        fd[i].off = pl.off[i];
+        fd[i].end = pl.end[i];
+    }
+    const uint64_t nt = pl.n_tiles;
+    std::vector<uint32_t>& tf = pl.tile_first;
+    std::vector<uint32_t>& tl = pl.tile_last;
+    std::vector<uint64_t> gp(c->n_groups, 0);
+    for (uint32_t i = 0; i < n; ++i) {
+        uint64_t a = fd[i].off, b = fd[i].off + fd[i].nbytes;
+        while (a < b) {
+            const uint64_t g = a / (c->G * c->C);
+            const uint64_t ge = std::min(b, (g + 1) * c->G * c->C);
+            gp[g] += ge - a;
+            a = ge;
+        }
+    }
+    c->group_payload = gp;
+    (void)ts;
+
+#define ALLOC(ptr, bytes)                                                                                   \
+    do {                                                                                                    \
+        if (hipMalloc((void**)&(ptr), (bytes)) != hipSuccess) {                                             \
+            (ptr) = nullptr;                                                                                \
+            return fail(c, CKPT_ENOMEM, "hipMalloc(%llu) failed for " #ptr, (unsigned long long)(bytes));    \
+        }                                                                                                   \
+    } while (0)
+    ALLOC(c->d_frags, n * sizeof(FragDev));
+    ALLOC(c->d_tile_first, nt * 4);
+    ALLOC(c->d_tile_last, nt * 4);
+    ALLOC(c->d_acc, 2 * c->n_chunks * 8);
+    ALLOC(c->d_done, 2 * c->n_chunks * 4);
+    ALLOC(c->d_expected, c->n_chunks * 8);
+    ALLOC(c->d_recomputed, c->n_chunks * 8);
+    ALLOC(c->d_bad, c->n_chunks);
+    ALLOC(c->d_staging, c->ring ? c->n_slots * c->C : c->I);
+#undef ALLOC
+    HIPCHK(c, hipMemcpy(c->d_frags, fd.data(), n * sizeof(FragDev), hipMemcpyHostToDevice));
+    HIPCHK(c, hipMemcpy(c->d_tile_first, tf.data(), nt * 4, hipMemcpyHostToDevice));
+    HIPCHK(c, hipMemcpy(c->d_tile_last, tl.data(), nt * 4, hipMemcpyHostToDevice));
+    HIPCHK(c, hipMemset(c->d_acc, 0, 2 * c->n_chunks * 8));
+    HIPCHK(c, hipMemset(c->d_done, 0, 2 * c->n_chunks * 4));
+    for (int b = 0; b < 2; ++b) {
+        if (hipHostMalloc((void**)&c->h_img[b], c->I, hipHostMallocDefault) != hipSuccess) {
+            c->h_img[b] = nullptr;
+            return fail(c, CKPT_ENOMEM, "pinned host image of %llu bytes", (unsigned long long)c->I);
+        }
+        if (hipHostMalloc((void**)&c->h_sums[b], c->n_chunks * 8, hipHostMallocDefault) != hipSuccess) {
+            c->h_sums[b] = nullptr;
+            return fail(c, CKPT_ENOMEM, "pinned sums");
+        }
+    }
+    if (hipHostMalloc((void**)&c->h_bad, c->n_chunks, hipHostMallocDefault) != hipSuccess ||
+        hipHostMalloc((void**)&c->h_recomputed, c->n_chunks * 8, hipHostMallocDefault) != hipSuccess)
+        return fail(c, CKPT_ENOMEM, "pinned result buffers");
+    const uint64_t n_areas = c->ring ? c->n_slots : c->n_groups;
+    c->area_free.resize(n_areas, nullptr);
+    for (auto& e : c->area_free) {
+        ckpt_status st = make_event(c, &e, false);
+        if (st) return st;
+        HIPCHK(c, hipEventRecord(e, c->s_copy)); // every area starts free
+    }
+    c->ev_loaded.resize(c->n_groups, nullptr);
+    for (auto& e : c->ev_loaded) {
+        ckpt_status st = make_event(c, &e, false);
+        if (st) return st;
+    }
+    HIPCHK(c, hipDeviceSynchronize());
+    c->registered = true;
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, const void* meta,
+                                uint32_t meta_len, uint64_t* snap_id)
+{
+    if (!c || !snap_id) return fail(c, CKPT_EINVAL, "null argument");
+    if (!c->registered) return fail(c, CKPT_ESTATE, "no tensors registered");
+    if (meta_len && !meta) return fail(c, CKPT_EINVAL, "meta is null");
+    if (meta_len > kMaxMeta) return fail(c, CKPT_EINVAL, "meta blob larger than 1 MiB");
+    HIPCHK(c, hipSetDevice(c->device));
+    prune(c);
+    // At most two uncommitted snapshots; find the newest live one.
+    int in_flight = 0;
+    SnapRec* newest_live = nullptr;
+    for (auto& kv : c->recs) {
+        SnapRec& r = kv.second;
+        if (r.aborted) continue;
+        bool com = false;
+        ckpt_status st = query_committed(c, r, &com);
+        if (st) return st;
+        if (!com) ++in_flight;
+        if (!newest_live || r.id > newest_live->id) newest_live = &r;
+    }
+    if (in_flight >= 2) return fail(c, CKPT_EBUSY, "both host images are still being written");
+
+    RecRes* res = nullptr;
+    ckpt_status st = get_res(c, &res);
+    if (st) return st;
+    const uint64_t id = c->next_id++;
+    SnapRec& r = c->recs[id];
+    r.id = id;
+    r.step = step;
+    r.res = res;
+    r.buf = newest_live ? 1 - newest_live->buf : (c->holder[0] == 0 ? 0 : (c->holder[1] == 0 ? 1 : 0));
+    if (!newest_live) {
+        // No live snapshot: never take an image that holds a committed one.
+        for (int b = 0; b < 2; ++b) {
+            auto it = c->recs.find(c->holder[b]);
+            if (c->holder[b] == 0 || it == c->recs.end() || it->second.aborted) {
+                r.buf = b;
+                break;
+            }
+        }
+    }
+    r.meta.assign((const uint8_t*)meta, (const uint8_t*)meta + meta_len);
+    r.timed = c->timing;
+    c->holder[r.buf] = id;
+    const int32_t stop = c->interrupt_next;
+    c->interrupt_next = -1;
+    hipStream_t after = (hipStream_t)after_stream;
+    uint8_t* himg = c->h_img[r.buf];
+    ChunkReduce red{c->d_acc, c->d_done};
+
+    HIPCHK(c, hipEventRecord(c->ev_trigger, after));
+    HIPCHK(c, hipStreamWaitEvent(c->s_pack, c->ev_trigger, 0));
+    if (r.timed) HIPCHK(c, hipEventRecord(res->t0, c->s_pack));
+    uint32_t copied = 0;
+    for (uint64_t g = 0; g < c->n_groups; ++g) {
+        const uint64_t lo = group_lo(c, g), hi = group_hi(c, g);
+        hipEvent_t& af = c->area_free[area_of(c, g)];
+        HIPCHK(c, hipStreamWaitEvent(c->s_pack, af, 0));
+        if (r.timed) HIPCHK(c, hipEventRecord(res->k0[g], c->s_pack));
+        hipError_t e = launch_pack(c->d_frags, c->d_tile_first, c->d_tile_last, c->geo, tiles_lo(c, g),
+                                   tiles_hi(c, g), staging_of(c, g), lo, red, res->d_sums, c->grid_cap, c->s_pack);
+        if (e != hipSuccess) return fail(c, CKPT_EHIP, "pack launch failed: %s", hipGetErrorString(e));
+        if (r.timed) HIPCHK(c, hipEventRecord(res->k1[g], c->s_pack));
+        HIPCHK(c, hipEventRecord(res->captured[g], c->s_pack));
+        if (stop < 0 || (int64_t)g < stop) {
+            HIPCHK(c, hipStreamWaitEvent(c->s_copy, res->captured[g], 0));
+            if (r.timed && g == 0) HIPCHK(c, hipEventRecord(res->c0, c->s_copy));
+            HIPCHK(c, hipMemcpyAsync(himg + lo, staging_of(c, g), hi - lo, hipMemcpyDeviceToHost, c->s_copy));
+            if (r.timed && g + 1 == c->n_groups) HIPCHK(c, hipEventRecord(res->c1, c->s_copy));
+            HIPCHK(c, hipEventRecord(af, c->s_copy));
+            ++copied;
+        } else {
+            HIPCHK(c, hipEventRecord(af, c->s_pack)); // nothing will read this area
+        }
+    }
+    r.groups_copied = copied;
+    if (stop >= 0) {
+        r.aborted = true; // interrupted offload: never committed
+        r.timed = false;
+    } else {
+        HIPCHK(c, hipMemcpyAsync(c->h_sums[r.buf], res->d_sums, c->n_chunks * 8, hipMemcpyDeviceToHost, c->s_copy));
+        HIPCHK(c, hipEventRecord(res->commit, c->s_copy));
+    }
+    *snap_id = id;
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_wait(ckpt_ctx* c, uint64_t snap_id, uint32_t mode, void* stream, uint32_t frag_lo,
+                      uint32_t frag_hi)
+{
+    if (!c) return CKPT_EINVAL;
+    auto it = c->recs.find(snap_id);
+    if (it == c->recs.end()) return fail(c, CKPT_ERANGE, "snapshot %llu not retained", (unsigned long long)snap_id);
+    SnapRec& r = it->second;
+    HIPCHK(c, hipSetDevice(c->device));
+    if (mode == CKPT_WAIT_COMMITTED) {
+        if (r.aborted) return fail(c, CKPT_ESTATE, "snapshot %llu was interrupted", (unsigned long long)snap_id);
+        HIPCHK(c, hipEventSynchronize(r.res->commit));
+        r.committed = true;
+        return CKPT_OK;
+    }
+    if (mode != CKPT_WAIT_CAPTURED) return fail(c, CKPT_EINVAL, "unknown wait mode %u", mode);
+    const uint32_t n = (uint32_t)c->frags.size();
+    if (frag_hi > n) frag_hi = n;
+    if (frag_lo >= frag_hi) return fail(c, CKPT_EINVAL, "empty fragment range [%u, %u) of %u", frag_lo, frag_hi, n);
+    // Last image byte of the range's non-empty fragments; packs run in group
+    // order on one stream, so waiting for that byte's group covers the rest.
+    uint64_t last = 0;
+    bool any = false;
+    for (uint32_t i = frag_hi; i-- > frag_lo;) {
+        if (c->frags[i].nbytes) {
+            last = c->frags[i].off + c->frags[i].nbytes - 1;
+            any = true;
+            break;
+        }
+    }
+    if (!any) return CKPT_OK; // only empty fragments: nothing to protect
+    const uint64_t g = last / (c->G * c->C);
+    HIPCHK(c, hipStreamWaitEvent((hipStream_t)stream, r.res->captured[g], 0));
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_snapshot_state(ckpt_ctx* c, uint64_t snap_id, uint32_t* state)
+{
+    if (!c || !state) return CKPT_EINVAL;
+    auto it = c->recs.find(snap_id);
+    if (it == c->recs.end()) return fail(c, CKPT_ERANGE, "snapshot %llu not retained", (unsigned long long)snap_id);
+    SnapRec& r = it->second;
+    if (r.aborted) {
+        *state = CKPT_SNAP_ABORTED;
+        return CKPT_OK;
+    }
+    bool com = false;
+    ckpt_status st = query_committed(c, r, &com);
+    if (st) return st;
+    if (!com) *state = CKPT_SNAP_IN_FLIGHT;
+    else *state = (c->holder[r.buf] == r.id) ? CKPT_SNAP_COMMITTED : CKPT_SNAP_SUPERSEDED;
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_restore(ckpt_ctx* c, uint64_t snap_id, void* stream, uint32_t* bad_chunks, uint32_t cap,
+                         uint32_t* n_bad)
+{
+    if (!c) return CKPT_EINVAL;
+    return run_check(c, snap_id, (hipStream_t)stream, true, bad_chunks, cap, n_bad);
+}
+
+ckpt_status ckpt_verify(ckpt_ctx* c, uint64_t snap_id, uint32_t* bad_chunks, uint32_t cap, uint32_t* n_bad)
+{
+    if (!c) return CKPT_EINVAL;
+    return run_check(c, snap_id, nullptr, false, bad_chunks, cap, n_bad);
+}
+
+ckpt_status ckpt_layout(ckpt_ctx* c, uint64_t* frag_off, uint64_t* image_bytes, uint64_t* n_chunks)
+{
+    if (!c) return CKPT_EINVAL;
+    if (!c->registered) return fail(c, CKPT_ESTATE, "no tensors registered");
+    if (frag_off)
+        for (size_t i = 0; i < c->frags.size(); ++i) frag_off[i] = c->frags[i].off;
+    if (image_bytes) *image_bytes = c->I;
+    if (n_chunks) *n_chunks = c->n_chunks;
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_chunk_fragments(ckpt_ctx* c, uint64_t k, uint64_t* byte_lo, uint64_t* byte_hi,
+                                 uint32_t* frag_first, uint32_t* frag_last)
+{
+    if (!c) return CKPT_EINVAL;
+    if (!c->registered) return fail(c, CKPT_ESTATE, "no tensors registered");
+    if (k >= c->n_chunks) return fail(c, CKPT_EINVAL, "chunk %llu out of range", (unsigned long long)k);
+    const uint64_t lo = k * c->C, hi = std::min(lo + c->C, c->I);
+    // First fragment whose padded span reaches past lo; last whose offset is below hi.
+    const uint32_t n = (uint32_t)c->frags.size();
+    uint32_t a = 0, b = n - 1;
+    {
+        uint32_t l = 0, h = n; // first i with end(i) > lo
+        while (l < h) {
+            uint32_t m = (l + h) / 2;
+            uint64_t end = (m + 1 < n) ? c->frags[m + 1].off : c->I;
+            if (end > lo) h = m;
+            else l = m + 1;
+        }
+        a = l;
+        l = 0;
+        h = n; // first i with off(i) >= hi
+        while (l < h) {
+            uint32_t m = (l + h) / 2;
+            if (c->frags[m].off >= hi) h = m;
+            else l = m + 1;
+        }
+        b = l ? l - 1 : 0;
+    }
+    if (byte_lo) *byte_lo = lo;
+    if (byte_hi) *byte_hi = hi;
+    if (frag_first) *frag_first = a;
+    if (frag_last) *frag_last = b;
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_host_image(ckpt_ctx* c, uint64_t snap_id, void** image, uint64_t* image_bytes, uint64_t** sums)
+{
+    if (!c) return CKPT_EINVAL;
+    auto it = c->recs.find(snap_id);
+    if (it == c->recs.end()) return fail(c, CKPT_ERANGE, "snapshot %llu not retained", (unsigned long long)snap_id);
+    SnapRec& r = it->second;
+    bool com = false;
+    ckpt_status st = query_committed(c, r, &com);
+    if (st) return st;
+    if (!com || c->holder[r.buf] != r.id) return fail(c, CKPT_ENOSNAP, "snapshot not committed or superseded");
+    if (image) *image = c->h_img[r.buf];
+    if (image_bytes) *image_bytes = c->I;
+    if (sums) *sums = c->h_sums[r.buf];
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_last_sums(ckpt_ctx* c, uint64_t* sums, uint64_t n)
+{
+    if (!c || !sums) return CKPT_EINVAL;
+    if (!c->have_last_sums) return fail(c, CKPT_ESTATE, "no restore or verify has run");
+    if (n < c->n_chunks) return fail(c, CKPT_EINVAL, "need room for %llu sums", (unsigned long long)c->n_chunks);
+    std::memcpy(sums, c->last_sums.data(), c->n_chunks * 8);
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_envelope(ckpt_ctx* c, uint64_t snap_id, void* out, uint64_t cap, uint64_t* len)
+{
+    if (!c || !len) return CKPT_EINVAL;
+    auto it = c->recs.find(snap_id);
+    if (it == c->recs.end()) return fail(c, CKPT_ERANGE, "snapshot %llu not retained", (unsigned long long)snap_id);
+    SnapRec& r = it->second;
+    bool com = false;
+    ckpt_status st = query_committed(c, r, &com);
+    if (st) return st;
+    if (!com || c->holder[r.buf] != r.id) return fail(c, CKPT_ENOSNAP, "snapshot not committed or superseded");
+    const uint32_t nf = (uint32_t)c->frags.size();
+    const uint64_t meta_pad = round_up(r.meta.size(), 8);
+    const uint64_t total = 56 + 24ull * nf + 8 * c->n_chunks + meta_pad + 8;
+    *len = total;
+    if (!out || cap < total) return fail(c, CKPT_EINVAL, "envelope needs %llu bytes", (unsigned long long)total);
+    // x86-64 and gfx950 are little-endian: fields are stored in native order.
+    std::vector<uint8_t> buf(total, 0);
+    uint8_t* p = buf.data();
+    struct __attribute__((packed)) Head {
+        char magic[8];
+        uint32_t version, align;
+        uint64_t step, chunk, image, n_chunks;
+        uint32_t n_frag, meta_len;
+    } h;
+    static_assert(sizeof(Head) == 56, "envelope header is 56 bytes");
+    std::memcpy(h.magic, "CKPTENV1", 8);
+    h.version = 1;
+    h.align = c->A;
+    h.step = r.step;
+    h.chunk = c->C;
+    h.image = c->I;
+    h.n_chunks = c->n_chunks;
+    h.n_frag = nf;
+    h.meta_len = (uint32_t)r.meta.size();
+    std::memcpy(p, &h, sizeof h);
+    p += sizeof h;
+    for (uint32_t i = 0; i < nf; ++i) {
+        struct __attribute__((packed)) Ent {
+            uint64_t off, nbytes;
+            uint32_t dtype, cls;
+        } e{c->frags[i].off, c->frags[i].nbytes, c->frags[i].dtype, c->frags[i].cls};
+        std::memcpy(p, &e, sizeof e);
+        p += sizeof e;
+    }
+    std::memcpy(p, c->h_sums[r.buf], c->n_chunks * 8);
+    p += c->n_chunks * 8;
+    if (!r.meta.empty()) std::memcpy(p, r.meta.data(), r.meta.size());
+    p += meta_pad;
+    uint64_t s = 0;
+    for (const uint8_t* q = buf.data(); q < p; q += 8) {
+        uint64_t w;
+        std::memcpy(&w, q, 8);
+        s += w;
+    }
+    std::memcpy(p, &s, 8);
+    std::memcpy(out, buf.data(), total);
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_debug_interrupt_next(ckpt_ctx* c, int32_t groups)
+{
+    if (!c) return CKPT_EINVAL;
+    c->interrupt_next = groups < 0 ? -1 : groups;
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_set_timing(ckpt_ctx* c, int32_t enable)
+{
+    if (!c) return CKPT_EINVAL;
+    c->timing = enable != 0;
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_last_timing(ckpt_ctx* c, uint32_t which, ckpt_timing* out)
+{
+    if (!c || !out || which > CKPT_OP_VERIFY) return fail(c, CKPT_EINVAL, "bad timing query");
+    if (which == CKPT_OP_SNAPSHOT) {
+        // newest timed, committed snapshot
+        SnapRec* best = nullptr;
+        for (auto& kv : c->recs)
+            if (kv.second.timed && !kv.second.aborted && (!best || kv.first > best->id)) best = &kv.second;
+        if (!best) return fail(c, CKPT_ESTATE, "no timed snapshot retained");
+        HIPCHK(c, hipEventSynchronize(best->res->commit));
+        RecRes* r = best->res;
+        ckpt_timing t{};
+        for (uint64_t g = 0; g < c->n_groups; ++g) t.kernel_ms += elapsed(r->k0[g], r->k1[g]);
+        t.kernels = (uint32_t)c->n_groups;
+        t.copies = (uint32_t)c->n_groups;
+        t.copy_ms = elapsed(r->c0, r->c1);
+        t.total_ms = elapsed(r->t0, r->c1);
+        t.kernel_bytes = 2 * c->payload;
+        t.copy_bytes = c->I;
+        *out = t;
+        return CKPT_OK;
+    }
+    if (!c->op_timing[which].valid) return fail(c, CKPT_ESTATE, "no timed operation of that kind");
+    *out = c->op_timing[which].t;
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_plan(const uint64_t* nbytes, uint32_t n, uint64_t chunk_bytes, uint32_t align_bytes,
+                      uint64_t* frag_off, uint64_t* image_bytes, uint64_t* n_chunks)
+{
+    const uint64_t C = chunk_bytes ? chunk_bytes : kDefaultChunk;
+    const uint32_t A = align_bytes ? align_bytes : kDefaultAlign;
+    if (!nbytes || n == 0 || !geometry_ok(C, A)) return CKPT_EINVAL;
+    Plan p;
+    if (!plan(nbytes, n, C, A, &p, false)) return CKPT_EINVAL;
+    if (frag_off) std::memcpy(frag_off, p.off.data(), 8ull * n);
+    if (image_bytes) *image_bytes = p.I;
+    if (n_chunks) *n_chunks = p.n_chunks;
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_debug_tile_plan(const uint64_t* nbytes, uint32_t n, uint64_t chunk_bytes, uint32_t align_bytes,
+                                 uint64_t* tile_bytes, uint64_t* n_tiles, uint32_t* tile_first,
+                                 uint32_t* tile_last)
+{
+    const uint64_t C = chunk_bytes ? chunk_bytes : kDefaultChunk;
+    const uint32_t A = align_bytes ? align_bytes : kDefaultAlign;
+    if (!nbytes || n == 0 || !geometry_ok(C, A)) return CKPT_EINVAL;
+    Plan p;
+    if (!plan(nbytes, n, C, A, &p, tile_first != nullptr)) return CKPT_EINVAL;
+    if (tile_bytes) *tile_bytes = 1ull << p.tile_shift;
+    if (n_tiles) *n_tiles = p.n_tiles;
+    if (tile_first) std::memcpy(tile_first, p.tile_first.data(), 4 * p.n_tiles);
+    if (tile_last && tile_first) std::memcpy(tile_last, p.tile_last.data(), 4 * p.n_tiles);
+    return CKPT_OK;
+}
+
+const char* ckpt_last_error(const ckpt_ctx* c) { return c ? c->err.c_str() : "null context"; }
+
+} // extern "C"

@@ -1,0 +1,314 @@
+"""GPU path against the CPU oracle, bit for bit (needs an MI355X).
+
+Every comparison is byte-exact: the snapshot image, the chunk sums, the
+restored tensors, the bad-chunk lists and the envelope.  Inputs come from the
+seeded generators in `workloads` or numpy; expected values come only from
+`oracle`.
+"""
+import struct
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+from gpu_util import garbage_fill, host_bytes, random_byte_fragments
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    import paper_2607_01646_amd as P
+
+
+def snapshot_and_check(tensors, host, chunk, align=256, staging=0, group=0, dtypes=None, classes=None,
+                       meta=b"", step=3):
+    """Snapshot, compare image and sums with the oracle, trash the tensors,
+    restore and compare them; returns the Checkpointer and snapshot id."""
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=chunk, align_bytes=align,
+                        device_staging_bytes=staging, group_bytes=group)
+    snap = ck.snapshot(step=step, meta=meta)
+    ck.wait_committed(snap)
+    assert ck.state(snap) == P.CKPT_SNAP_COMMITTED
+    img, sums = ck.host_image(snap)
+    want, off, nc = O.pack(host, align, chunk)
+    assert np.array_equal(ck.offsets, off)
+    assert (ck.image_bytes, ck.n_chunks) == (want.size, nc)
+    assert img.size == want.size
+    diff = np.flatnonzero(img != want)
+    assert diff.size == 0, "image differs at %d bytes, first at %d" % (diff.size, diff[0])
+    want_sums = O.chunk_sums(want, 0, want.size, chunk)
+    assert np.array_equal(sums, want_sums)
+    assert ck.verify(snap) == []
+    garbage_fill(tensors)
+    assert ck.restore(snap) == []
+    torch.cuda.synchronize()
+    for i, (t, h) in enumerate(zip(tensors, host)):
+        assert np.array_equal(host_bytes(t), h), "fragment %d not restored" % i
+    assert np.array_equal(P.ckpt_last_sums(ck.ctx), want_sums)
+    return ck, snap
+
+
+EDGE_SIZES = [1, 2, 3, 15, 16, 17, 255, 256, 257, 0, 4095, 4096, 4097, 100_003, 0, 0, 65536, 65537, 1 << 20, 7]
+
+
+@pytest.mark.parametrize("chunk,align,staging,group", [
+    (4096, 256, 0, 0),                 # many chunks, one launch
+    (4096, 256, 0, 3 * 4096),          # three chunks per launch and copy
+    (768, 256, 0, 0),                  # chunk not a power of two (256-byte tiles)
+    (1 << 20, 256, 0, 0),              # chunk larger than most fragments
+    (65536, 16, 0, 65536),             # 16-byte alignment, one chunk per group
+    (8192, 256, 4 * 8192, 0),          # ring of four device slots
+    (1 << 16, 4096, 2 * (1 << 16), 0), # ring of two slots, 4 KiB alignment
+])
+def test_edge_sizes_all_geometries(chunk, align, staging, group):
+    tensors, host = random_byte_fragments(EDGE_SIZES, seed=chunk + align)
+    ck, _ = snapshot_and_check(tensors, host, chunk, align, staging, group)
+    ck.close()
+
+
+def test_single_fragment_and_ragged_tail():
+    for n in [1, 16, 17, 4 << 20, (4 << 20) + 3]:
+        tensors, host = random_byte_fragments([n], seed=n)
+        ck, _ = snapshot_and_check(tensors, host, 1 << 20)
+        ck.close()
+
+
+def test_many_small_fragments_in_one_tile():
+    # 600 fragments of 1..40 bytes: several hundred fragments per 64 KiB tile
+    rng = np.random.default_rng(21)
+    sizes = [int(s) for s in rng.integers(1, 41, 600)]
+    tensors, host = random_byte_fragments(sizes, seed=22)
+    ck, _ = snapshot_and_check(tensors, host, 1 << 20)
+    ck.close()
+    # more fragments in a tile than the LDS offset cache holds (empty ones are free)
+    sizes = [0] * 3000 + [5, 0, 9] + [0] * 1500 + [300]
+    tensors, host = random_byte_fragments(sizes, seed=23)
+    ck, _ = snapshot_and_check(tensors, host, 1 << 16)
+    ck.close()
+
+
+def test_tiny_gpt_shard_bit_exact():
+    """Workload 1: 4-layer GPT shard (208 fragments, 238.9 MB), 4 MiB chunks."""
+    tensors, plan = W.make_state(1, device="cuda")
+    torch.cuda.synchronize()
+    host = [host_bytes(t) for t in tensors]
+    ck, snap = snapshot_and_check(tensors, host, W.WORKLOADS[1]["chunk"], dtypes=[p[2] for p in plan],
+                                  classes=[p[3] for p in plan])
+    assert ck.n_chunks == 57 and sum(p[1] for p in plan) == 238_938_112
+    ck.close()
+
+
+def test_adversarial_bit_patterns_pass_unchanged():
+    frags = W.adversarial_fragments("cuda")
+    host = [host_bytes(t) for t in frags]
+    ck, _ = snapshot_and_check(frags, host, 4096)
+    ck.close()
+
+
+def test_misaligned_views_restore_without_touching_neighbours():
+    views, flats = W.misaligned_views("cuda")
+    torch.cuda.synchronize()
+    host = [host_bytes(v) for v in views]
+    flat_before = [host_bytes(f) for f in flats]
+    ck = P.Checkpointer(views, chunk_bytes=1 << 16)
+    snap = ck.snapshot()
+    ck.wait_committed(snap)
+    img, sums = ck.host_image(snap)
+    want, off, nc = O.pack(host, 256, 1 << 16)
+    assert np.array_equal(img, want)
+    assert np.array_equal(sums, O.chunk_sums(want, 0, want.size, 1 << 16))
+    for v in views:  # trash only the registered views
+        v.view(torch.uint8).fill_(0xEE) if v.dtype == torch.uint8 else v.view(torch.int16 if v.element_size() == 2
+                                                                              else torch.int32).fill_(-7)
+    assert ck.restore(snap) == []
+    torch.cuda.synchronize()
+    for f, b in zip(flats, flat_before):  # views restored, bytes between them untouched
+        assert np.array_equal(host_bytes(f), b)
+    ck.close()
+
+
+def test_single_bit_flips_are_reported_and_located():
+    """Seeded flips, one per chunk, in the committed pinned image: restore and
+    verify report exactly those chunks; the recomputed sums equal the oracle's
+    sums of the flipped image, and each delta is +-2^k as the closed form says."""
+    sizes = [int(s) for s in np.random.default_rng(31).integers(1000, 300_000, 64)]
+    tensors, host = random_byte_fragments(sizes, seed=32)
+    chunk = 65536
+    ck = P.Checkpointer(tensors, chunk_bytes=chunk)
+    snap = ck.snapshot()
+    ck.wait_committed(snap)
+    img, sums = ck.host_image(snap)
+    stored = sums.copy()
+    ranges = [(c * chunk, min((c + 1) * chunk, img.size)) for c in range(ck.n_chunks)]
+    flips = W.flip_positions(ranges, n_flips=32, seed=2005)
+    for c, byte, bit in flips:
+        img[byte] ^= np.uint8(1 << bit)
+    want_bad = sorted(c for c, _, _ in flips)
+    assert ck.verify(snap) == want_bad
+    flipped = img.copy()
+    recomputed = P.ckpt_last_sums(ck.ctx)
+    assert np.array_equal(recomputed, O.chunk_sums(flipped, 0, flipped.size, chunk))
+    for c, byte, bit in flips:
+        k = 8 * (byte % 8) + bit
+        was_set = (int(flipped[byte]) >> bit) & 1 == 0  # bit value before the flip
+        delta = (int(recomputed[c]) - int(stored[c])) % (1 << 64)
+        assert delta == ((-(1 << k)) % (1 << 64) if was_set else (1 << k))
+        lo, hi, f0, f1 = ck.chunk_fragments(c)
+        (olo, ohi), ids = O.locate(c, chunk, ck.image_bytes, ck.offsets, sizes)
+        assert (lo, hi) == (olo, ohi) and f0 <= min(ids) and max(ids) <= f1
+    garbage_fill(tensors)
+    assert ck.restore(snap) == want_bad  # every byte is still written back
+    torch.cuda.synchronize()
+    back = O.restore_window(flipped, 0, flipped.size, ck.offsets, sizes)
+    for t, b in zip(tensors, back):
+        assert np.array_equal(host_bytes(t), b)
+    ck.close()
+
+
+def _step_state(n_frag=48, numel=1 << 20, seed=41):
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    return [torch.randn(numel, generator=g, device="cuda") for _ in range(n_frag)]
+
+
+def test_gate_orders_optimizer_after_capture():
+    """The wait before the optimizer step: an in-place update launched right
+    after ckpt_wait(CAPTURED) must not leak into the snapshot.  A first
+    snapshot keeps the copy engine busy so the second snapshot's pack is
+    delayed behind it -- the window in which an ungated update would win."""
+    tensors = _step_state(n_frag=96)
+    ck = P.Checkpointer(tensors, chunk_bytes=1 << 20)
+    before = [host_bytes(t) for t in tensors]  # values at both snapshots
+    ck.snapshot(step=1)
+    s2 = ck.snapshot(step=2)  # its pack waits for snapshot 1's copies (~7 ms)
+    ck.wait_captured(s2, 0, len(tensors))
+    for t in tensors:
+        t.add_(1.0)  # the "optimizer step"
+    ck.wait_committed(s2)
+    img, _ = ck.host_image(s2)
+    want, _, _ = O.pack(before, 256, 1 << 20)
+    assert np.array_equal(img, want)
+    # Partial gate: waiting only for fragments [0, 8) protects those.
+    before = [host_bytes(t) for t in tensors]
+    ck.snapshot(step=3)
+    s4 = ck.snapshot(step=4)
+    ck.wait_captured(s4, 0, 8)
+    for t in tensors[:8]:
+        t.mul_(2.0)
+    ck.wait_committed(s4)
+    img, _ = ck.host_image(s4)
+    off = ck.offsets
+    for i in range(8):
+        o = int(off[i])
+        assert np.array_equal(img[o:o + before[i].size], before[i])
+    ck.close()
+
+
+def test_gate_negative_control_detects_the_race():
+    """Same as above without the wait: the update now lands before the
+    delayed pack, so the snapshot differs from the pre-update state.  Shows
+    the gate test can see a missing wait."""
+    tensors = _step_state(n_frag=96)
+    ck = P.Checkpointer(tensors, chunk_bytes=1 << 20)
+    before = [host_bytes(t) for t in tensors]
+    ck.snapshot(step=1)
+    s2 = ck.snapshot(step=2)
+    for t in tensors:
+        t.add_(1.0)  # no ckpt_wait: races with the delayed pack
+    ck.wait_committed(s2)
+    img, _ = ck.host_image(s2)
+    want, _, _ = O.pack(before, 256, 1 << 20)
+    assert not np.array_equal(img, want)
+    ck.close()
+
+
+def test_interrupted_snapshot_is_never_restored():
+    """Invariant I4: an offload interrupted after two chunk groups stays
+    ABORTED; restore returns the previous committed snapshot."""
+    tensors = _step_state(n_frag=16, numel=1 << 18)
+    ck = P.Checkpointer(tensors, chunk_bytes=1 << 18, group_bytes=1 << 18)
+    s1 = ck.snapshot(step=1)
+    ck.wait_committed(s1)
+    good = [host_bytes(t) for t in tensors]
+    for t in tensors:
+        t.add_(3.0)
+    P.ckpt_debug_interrupt_next(ck.ctx, 2)
+    s2 = ck.snapshot(step=2)
+    torch.cuda.synchronize()
+    assert ck.state(s2) == P.CKPT_SNAP_ABORTED
+    assert ck.state(s1) == P.CKPT_SNAP_COMMITTED
+    with pytest.raises(P.CkptError) as e:
+        ck.wait_committed(s2)
+    assert e.value.code == P.CKPT_ESTATE
+    garbage_fill(tensors)
+    assert ck.restore(0) == []
+    torch.cuda.synchronize()
+    for t, h in zip(tensors, good):
+        assert np.array_equal(host_bytes(t), h)
+    # The next snapshot reuses the aborted image, never s1's.
+    s3 = ck.snapshot(step=3)
+    ck.wait_committed(s3)
+    assert ck.state(s1) == P.CKPT_SNAP_COMMITTED and ck.state(s3) == P.CKPT_SNAP_COMMITTED
+    assert ck.restore(s1) == []
+    ck.close()
+
+
+def test_ping_pong_roles_and_busy():
+    tensors = _step_state(n_frag=64, numel=1 << 20)  # 256 MiB: copies take ~5 ms
+    ck = P.Checkpointer(tensors, chunk_bytes=1 << 22)
+    s1 = ck.snapshot(step=1)
+    s2 = ck.snapshot(step=2)
+    with pytest.raises(P.CkptError) as e:  # both images in flight
+        ck.snapshot(step=3)
+    assert e.value.code == P.CKPT_EBUSY
+    ck.wait_committed(s2)
+    assert ck.state(s1) == P.CKPT_SNAP_COMMITTED and ck.state(s2) == P.CKPT_SNAP_COMMITTED
+    s3 = ck.snapshot(step=3)  # takes s1's image
+    ck.wait_committed(s3)
+    assert ck.state(s1) == P.CKPT_SNAP_SUPERSEDED
+    with pytest.raises(P.CkptError) as e:
+        ck.restore(s1)
+    assert e.value.code == P.CKPT_ENOSNAP
+    assert ck.restore(s2) == [] and ck.restore(0) == []
+    # A corrupted newest image: the other buffer still restores cleanly.
+    img, _ = ck.host_image(s3)
+    img[12345] ^= 0x40
+    assert ck.verify(s3) == [12345 // (1 << 22)]
+    assert ck.restore(s2) == []
+    ck.close()
+
+
+def test_envelope_matches_oracle():
+    sizes = [100, 0, 4096, 33, 70_000]
+    tensors, host = random_byte_fragments(sizes, seed=51)
+    dtypes = [1, 2, 2, 0, 1]
+    classes = [0, 1, 2, 3, 0]
+    meta = b"tp=8;pp=8;dp=4;rng=" + struct.pack("<Q", 123456789)
+    ck, snap = snapshot_and_check(tensors, host, 4096, dtypes=dtypes, classes=classes, meta=meta, step=77)
+    env = ck.envelope(snap)
+    img, sums = ck.host_image(snap)
+    want = O.envelope(77, 256, 4096, ck.image_bytes, ck.offsets, sizes, dtypes, classes,
+                      O.chunk_sums(O.pack(host, 256, 4096)[0], 0, ck.image_bytes, 4096), meta)
+    assert env == want
+    ck.close()
+
+
+def test_error_codes():
+    tensors, _ = random_byte_fragments([1000], seed=61)
+    ctx = P.ckpt_create(chunk_bytes=4096)
+    with pytest.raises(P.CkptError) as e:
+        P.ckpt_snapshot_async(ctx)
+    assert e.value.code == P.CKPT_ESTATE
+    P.ckpt_register_tensors(ctx, tensors)
+    with pytest.raises(P.CkptError) as e:
+        P.ckpt_register_tensors(ctx, tensors)
+    assert e.value.code == P.CKPT_ESTATE
+    with pytest.raises(P.CkptError) as e:
+        P.ckpt_restore(ctx, 0)
+    assert e.value.code == P.CKPT_ENOSNAP
+    with pytest.raises(P.CkptError) as e:
+        P.ckpt_wait(ctx, 99, P.CKPT_WAIT_CAPTURED, None, 0, 1)
+    assert e.value.code == P.CKPT_ERANGE
+    P.ckpt_destroy(ctx)
+    with pytest.raises(P.CkptError):
+        P.ckpt_create(chunk_bytes=1000)  # not a multiple of the alignment
