@@ -1,0 +1,320 @@
+"""Benchmark of the in-memory snapshot hot path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--no-overlap] [--no-cpu]
+
+One step is one pass of the whole path over one rank's state shard (the
+24-layer, hidden-2048 GPT shard: 1168 fragments, 18.42 GB of bf16 params,
+fp32 master weights and Adam moments, 64 MiB chunks):
+  snapshot = pack + chunk sums (HBM -> HBM staging) -> chunked D2H into the
+             pinned ping-pong image -> commit         (paper Sec. V-B, VI-A)
+  gate     = the wait before the optimizer step      (paper Sec. VI-A)
+  restore  = H2D + scatter into the tensors + re-check every chunk sum
+  verify   = H2D + re-check every chunk sum
+The state is generated on the GPU before timing starts.  Prints one JSON
+line; `value` is payload bytes per second through that whole cycle.
+
+Also measured: the pack kernel against the HBM roofline (HIP events that the
+library records on its own pack stream around every launch), D2H against the
+host link's measured peak (a plain pinned 1 GiB copy in the same process),
+restore/verify rates, the step-time overhead of snapshots under a bf16 GEMM
+load (one rank of a 65B model under TP=8 x PP=8, GEMM 8192x8192x2752, timed
+per the paper's Sec. VII-A statistic), and the CPU oracle on a bounded sample.
+"""
+import argparse
+import json
+import math
+import os
+import subprocess
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "snapshot GB/s (HBM pack+checksum, D2H) + % step overhead under overlap"
+HBM_PEAK_GBPS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--no-overlap", action="store_true")
+    ap.add_argument("--overlap-steps", type=int, default=50)
+    ap.add_argument("--overlap-workload", type=int, default=3)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--cpu-sample-bytes", type=int, default=10 << 30)
+    ap.add_argument("--traffic", type=str, default="", help="JSON file with rocprofv3 FETCH/WRITE figures")
+    return ap.parse_args()
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def trimmed_mean(xs, warm=10, drop=0.05):
+    """Paper Sec. VII-A: discard the first 10 iterations, drop the slowest 5%
+    of the rest, average."""
+    xs = list(xs[warm:]) if len(xs) > warm else list(xs)
+    xs.sort()
+    keep = len(xs) - int(math.floor(len(xs) * drop))
+    xs = xs[:max(keep, 1)]
+    return sum(xs) / len(xs)
+
+
+def link_peak(torch):
+    """Plain pinned 1 GiB D2H / H2D copies: the host link's measured peak."""
+    n = 1 << 30
+    h = torch.empty(n, dtype=torch.uint8, pin_memory=True)
+    d = torch.empty(n, dtype=torch.uint8, device="cuda")
+    d.fill_(7)
+    out = {}
+    for name, fn in [("d2h", lambda: h.copy_(d, non_blocking=True)), ("h2d", lambda: d.copy_(h, non_blocking=True))]:
+        fn()
+        torch.cuda.synchronize()
+        best = 1e9
+        for _ in range(5):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            b.synchronize()
+            best = min(best, a.elapsed_time(b))
+        out[name] = n / best / 1e6
+    del h, d
+    return out
+
+
+def hbm_copy_ceiling(torch):
+    n = 4 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    best = 1e9
+    for _ in range(5):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        b.copy_(a)
+        e1.record()
+        e1.synchronize()
+        best = min(best, e0.elapsed_time(e1))
+    del a, b
+    return 2 * n / best / 1e6
+
+
+def cpu_baseline(tensors, plan, chunk, target_bytes):
+    """The oracle, single-threaded, on the first fragments of the shard up to
+    target_bytes: pack + chunk sums + restore + verify (the same cycle as one
+    GPU step, minus the host-link copies, which a CPU does not need)."""
+    import numpy as np
+    import torch
+
+    import oracle as O
+
+    frags, total = [], 0
+    for t in tensors:
+        nb = t.numel() * t.element_size()
+        if total and total + nb > target_bytes:
+            break
+        frags.append(t.detach().cpu().reshape(-1).view(torch.uint8).numpy())
+        total += nb
+    sizes = [f.size for f in frags]
+    O.lib()
+    t0 = time.perf_counter()
+    img, off, nc = O.pack(frags, 256, chunk)
+    sums = O.chunk_sums(img, 0, img.size, chunk)
+    back = O.restore_window(img, 0, img.size, off, sizes)
+    bad = O.verify(img, 0, img.size, chunk, sums)
+    dt = time.perf_counter() - t0
+    assert bad == [] and all(np.array_equal(a, b) for a, b in zip(frags[:3], back[:3]))
+    return {"value": round(total / dt / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": "first %d of %d fragments of the shard (%d bytes, %d chunks of %d MiB): pack + chunk sums "
+                      "+ restore + verify, one thread, %.1f s" % (len(frags), len(tensors), total, nc, chunk >> 20, dt)}
+
+
+def overlap_leg(torch, P, W, wid, steps):
+    """Step-time overhead of per-step snapshots under a bf16 GEMM load."""
+    tensors, plan = W.make_state(wid, device="cuda")
+    n = len(tensors)
+    M, K, N = W.OVERLAP_GEMM[wid]
+    x = torch.randn(M, K, device="cuda", dtype=torch.bfloat16)
+    w = torch.randn(K, N, device="cuda", dtype=torch.bfloat16)
+    for _ in range(5):
+        torch.matmul(x, w)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(50):
+        torch.matmul(x, w)
+    e1.record()
+    e1.synchronize()
+    t_gemm = e0.elapsed_time(e1) / 50
+    ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=W.WORKLOADS[wid]["chunk"])
+    P.ckpt_set_timing(ck.ctx, True)
+    s = ck.snapshot(step=0)
+    ck.wait_committed(s)
+    t_d2h = P.ckpt_last_timing(ck.ctx, P.CKPT_OP_SNAPSHOT)["copy_ms"]
+    P.ckpt_set_timing(ck.ctx, False)
+    R = int(math.ceil(1.5 * t_d2h / t_gemm))
+    params = [tensors[i] for i in range(0, n, 4)]
+    masters = [tensors[i] for i in range(1, n, 4)]
+    ms = [tensors[i] for i in range(2, n, 4)]
+    vs = [tensors[i] for i in range(3, n, 4)]
+
+    def optimizer():  # touches every registered fragment in place
+        torch._foreach_mul_(ms, 0.9)
+        torch._foreach_mul_(vs, 0.999)
+        torch._foreach_add_(masters, ms, alpha=-1e-3)
+        for p, m in zip(params, masters):
+            p.copy_(m)
+
+    def run(with_snap):
+        times = []
+        for k in range(steps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            snap = ck.snapshot(step=k) if with_snap else None
+            for _ in range(R):
+                torch.matmul(x, w)
+            if with_snap:
+                ck.wait_captured(snap, 0, n)
+            optimizer()
+            torch.cuda.synchronize()
+            times.append((time.perf_counter() - t0) * 1e3)
+        return times
+
+    base1 = run(False)
+    withs = run(True)
+    base2 = run(False)
+    b = trimmed_mean(base1 + base2[10:], warm=10)
+    wv = trimmed_mean(withs, warm=10)
+    ck.close()
+    del tensors, x, w
+    torch.cuda.empty_cache()
+    return {"workload": W.WORKLOADS[wid]["name"], "payload_bytes": sum(p[1] for p in plan), "gemm_mkn": [M, K, N],
+            "gemm_ms": round(t_gemm, 4), "d2h_ms": round(t_d2h, 2), "R": R, "steps": steps,
+            "base_ms": round(b, 2), "with_snapshot_ms": round(wv, 2), "overhead_pct": round(100 * (wv - b) / b, 3),
+            "statistic": "mean after dropping 10 warm-up steps and the slowest 5%"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the snapshot path has no cross-GPU step in this build "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2607_01646_amd as P
+    import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    P.lib()  # fails loudly when libckpt.so is missing
+    wid = args.workload
+    wl = W.WORKLOADS[wid]
+    log("link peak")
+    link = link_peak(torch)
+    log("hbm copy ceiling")
+    hbm_ceiling = hbm_copy_ceiling(torch)
+    log("generating workload", wl["name"])
+    tensors, plan = W.make_state(wid, device="cuda")
+    torch.cuda.synchronize()
+    S = sum(p[1] for p in plan)
+    n = len(tensors)
+    ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=wl["chunk"])
+    P.ckpt_set_timing(ck.ctx, True)
+
+    def step(k):
+        snap = ck.snapshot(step=k, meta=b"step=%d" % k)
+        ck.wait_captured(snap, 0, n)
+        ck.wait_committed(snap)
+        bad = ck.restore(snap)
+        bad += ck.verify(snap)
+        if bad:
+            raise RuntimeError("checksum mismatch in chunks %s" % bad)
+
+    log("warmup")
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+    timings = {"snapshot": [], "restore": [], "verify": []}
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(args.warmup + k)
+        timings["snapshot"].append(P.ckpt_last_timing(ck.ctx, P.CKPT_OP_SNAPSHOT))
+        timings["restore"].append(P.ckpt_last_timing(ck.ctx, P.CKPT_OP_RESTORE))
+        timings["verify"].append(P.ckpt_last_timing(ck.ctx, P.CKPT_OP_VERIFY))
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms_per_step = dt * 1e3 / args.steps
+    log("timed %d steps: %.1f ms/step" % (args.steps, ms_per_step))
+
+    def agg(kind, key):
+        return sum(t[key] for t in timings[kind])
+
+    sn = timings["snapshot"][0]
+    pack_ms = agg("snapshot", "kernel_ms")
+    launches = sum(t["kernels"] for t in timings["snapshot"])
+    pack_bytes = 2 * S * args.steps
+    pack_gbps = pack_bytes / pack_ms / 1e6
+    d2h_ms = agg("snapshot", "copy_ms")
+    d2h_gbps = sn["copy_bytes"] * args.steps / d2h_ms / 1e6 if d2h_ms > 0 else float("nan")
+    restore_gbps = sn["copy_bytes"] * args.steps / agg("restore", "total_ms") / 1e6
+    scatter_gbps = 2 * S * args.steps / agg("restore", "kernel_ms") / 1e6
+    h2d_gbps = sn["copy_bytes"] * args.steps / agg("restore", "copy_ms") / 1e6
+    verify_gbps = sn["copy_bytes"] * args.steps / agg("verify", "total_ms") / 1e6
+    verify_kernel_gbps = sn["copy_bytes"] * args.steps / agg("verify", "kernel_ms") / 1e6
+    traffic = None
+    if args.traffic and os.path.exists(args.traffic):
+        traffic = json.load(open(args.traffic)).get("pack_bytes_per_launch")
+    roofline = {"kernel": "pack_checksum (tile_kernel<PACK>)", "bound": "hbm", "achieved": round(pack_gbps, 1),
+                "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(pack_gbps / HBM_PEAK_GBPS, 4),
+                "traffic": traffic, "launches": launches, "avg_launch_ms": round(pack_ms / launches, 4),
+                "algorithmic_bytes_per_launch": int(pack_bytes / launches),
+                "frac_of_measured_copy_ceiling": round(pack_gbps / hbm_ceiling, 4)}
+    ck.close()
+    cpu = None
+    if not args.no_cpu:
+        log("cpu baseline")
+        cpu = cpu_baseline(tensors, plan, wl["chunk"], args.cpu_sample_bytes)
+    del tensors
+    torch.cuda.empty_cache()
+    overlap = None
+    if not args.no_overlap:
+        log("overlap leg")
+        overlap = overlap_leg(torch, P, W, args.overlap_workload, args.overlap_steps)
+    try:
+        sha = subprocess.run(["git", "rev-parse", "--short", "HEAD"], cwd=ROOT, capture_output=True,
+                             text=True).stdout.strip() or None
+    except Exception:
+        sha = None
+    out = {
+        "metric": METRIC, "value": round(S / (ms_per_step / 1e3) / 1e9, 3), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 2), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u64", "data": "synthetic",
+        "config": {"workload": "%s shard: %d fragments, %d payload bytes, %d MiB chunks (snapshot + gate + restore "
+                               "+ verify per step)" % (wl["name"], n, S, wl["chunk"] >> 20),
+                   "payload_bytes": S, "image_bytes": int(sn["copy_bytes"]), "chunk_bytes": wl["chunk"],
+                   "parallelism": "one rank, one GPU"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "components": {"pack_GBps": round(pack_gbps, 1), "d2h_GBps": round(d2h_gbps, 2),
+                       "d2h_link_peak_GBps": round(link["d2h"], 2), "d2h_frac_of_link": round(d2h_gbps / link["d2h"], 4),
+                       "h2d_GBps": round(h2d_gbps, 2), "h2d_link_peak_GBps": round(link["h2d"], 2),
+                       "restore_GBps": round(restore_gbps, 2), "scatter_verify_GBps": round(scatter_gbps, 1),
+                       "verify_GBps": round(verify_gbps, 2), "verify_kernel_GBps": round(verify_kernel_gbps, 1),
+                       "hbm_copy_ceiling_GBps": round(hbm_ceiling, 1)},
+        "overlap": overlap,
+        "git": sha,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

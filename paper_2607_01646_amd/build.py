@@ -18,7 +18,7 @@ DEVICE_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC",
                 "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 # The runtime has no device code: plain g++ against the HIP headers.
 HOST_CXX = os.environ.get("CXX_HOST", "g++")
-HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__",
+HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-pthread", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__",
               "-I", "/opt/rocm/include"]
 
 
@@ -45,7 +45,8 @@ def build(verbose=False):
     _run([HIPCC] + DEVICE_FLAGS + inc + ["-c", os.path.join(CSRC, "ckpt_kernels.hip"), "-o", k_obj], verbose)
     _run([HOST_CXX] + HOST_FLAGS + inc + ["-c", os.path.join(CSRC, "ckpt_runtime.cpp"), "-o", r_obj], verbose)
     tmp = LIB + ".tmp"
-    _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", k_obj, r_obj, "-o", tmp], verbose)
+    _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", k_obj, r_obj, "-o", tmp, "-L/opt/rocm/lib",
+          "-lhsa-runtime64", "-lpthread"], verbose)
     os.replace(tmp, LIB)
     return LIB
 

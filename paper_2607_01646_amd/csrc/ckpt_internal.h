@@ -25,31 +25,30 @@ struct Geometry {
     uint32_t tiles_per_chunk; // chunk_bytes >> tile_shift
 };
 
-// Per-chunk reduction state shared by the tiles of one chunk.  Both arrays
-// are zero between launches: the last tile of a chunk reads and clears them.
-struct ChunkReduce {
-    unsigned long long* acc; // n_chunks partial sums
-    unsigned int* done;      // n_chunks finished-tile counters
-};
-
 // Pack fragments into an image window and sum its chunks.
-// Tiles [t_lo, t_hi) are processed; image byte x is written to
-// dst + (x - dst_origin).  sums_out[c] receives the word-sum of chunk c.
+// Tiles [t_lo, t_hi) (whole chunks) are processed; image byte x is written to
+// dst + (x - dst_origin); partials[t] receives tile t's sum and sums_out[c]
+// the word-sum of chunk c.  Two kernel launches on stream s.
 hipError_t launch_pack(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
                        const Geometry& g, uint64_t t_lo, uint64_t t_hi, uint8_t* dst, uint64_t dst_origin,
-                       ChunkReduce red, unsigned long long* sums_out, uint32_t grid_cap, hipStream_t s);
+                       unsigned long long* partials, unsigned long long* sums_out, uint32_t grid_cap, hipStream_t s);
 
 // Scatter an image window back into the fragments, recompute chunk sums and
 // compare them with expected[]: recomputed[c] and bad[c] (1 = mismatch).
 hipError_t launch_scatter_verify(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
                                  const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src,
-                                 uint64_t src_origin, ChunkReduce red, const unsigned long long* expected,
-                                 unsigned long long* recomputed, uint8_t* bad, uint32_t grid_cap, hipStream_t s);
+                                 uint64_t src_origin, unsigned long long* partials,
+                                 const unsigned long long* expected, unsigned long long* recomputed, uint8_t* bad,
+                                 uint32_t grid_cap, hipStream_t s);
 
 // Recompute chunk sums of an image window only (no fragments touched).
 hipError_t launch_checksum_verify(const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src,
-                                  uint64_t src_origin, ChunkReduce red, const unsigned long long* expected,
-                                  unsigned long long* recomputed, uint8_t* bad, uint32_t grid_cap,
-                                  hipStream_t s);
+                                  uint64_t src_origin, unsigned long long* partials,
+                                  const unsigned long long* expected, unsigned long long* recomputed, uint8_t* bad,
+                                  uint32_t grid_cap, hipStream_t s);
+
+// Store 0 into *signal_value (an HSA signal's value) once the work enqueued
+// on s before this call has completed.
+hipError_t launch_release(int64_t* signal_value, hipStream_t s);
 
 } // namespace ckpt

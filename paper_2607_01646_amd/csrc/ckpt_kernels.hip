@@ -19,11 +19,13 @@
 // aligned 16-byte blocks and funnel-shifts them when the fragment is
 // misaligned, masks the fragment tail and writes zeros for padding.
 // Sum reduction: per lane in 64 bits, across the wave with lane shuffles,
-// across the 4 waves in LDS; then one atomic add per tile into the chunk's
-// accumulator.  The tile that finishes a chunk (a counter per chunk) reads
-// and clears the accumulator and writes the chunk result, so consecutive
-// launches need no clearing pass.  Addition modulo 2^64 is associative and
-// commutative, so any tile order gives the same bits.
+// across the 4 waves in LDS; one plain store of the tile's sum; then a small
+// second kernel adds the tile sums of each chunk (and, when checking,
+// compares with the stored sum).  The hot kernel thus has no atomics and no
+// device-scope fence: on gfx950 such a fence writes back and invalidates the
+// XCD's L2, which per tile would cost more than the tile's own traffic.
+// Addition modulo 2^64 is associative and commutative, so any order of
+// tiles gives the same bits.
 #include "ckpt_internal.h"
 
 namespace ckpt {
@@ -46,9 +48,16 @@ struct Args {
     uint64_t t_lo, t_hi;
     uint8_t* img; // PACK: destination window; SCATTER/VERIFY: source window
     uint64_t origin;
-    ChunkReduce red;
+    unsigned long long* partials; // one sum per tile
+};
+
+struct ReduceArgs {
+    const unsigned long long* partials;
+    uint64_t c_lo, c_hi; // chunks of this launch
+    uint64_t n_tiles;
+    uint32_t tiles_per_chunk;
     unsigned long long* sums_out; // PACK: chunk sums; SCATTER/VERIFY: recomputed sums
-    const unsigned long long* expected;
+    const unsigned long long* expected; // null when only summing
     uint8_t* bad;
 };
 
@@ -205,35 +214,6 @@ __device__ __forceinline__ unsigned long long block_sum(unsigned long long v, un
     return r;
 }
 
-template <int MODE>
-__device__ __forceinline__ void chunk_result(const Args& a, uint64_t c, unsigned long long s)
-{
-    a.sums_out[c] = s;
-    if (MODE != PACK) a.bad[c] = (s != a.expected[c]) ? 1 : 0;
-}
-
-// Called by thread 0 with the tile's sum.
-template <int MODE>
-__device__ void finish_tile(const Args& a, uint64_t t, unsigned long long tile_sum)
-{
-    const uint64_t c = t / a.g.tiles_per_chunk;
-    const uint32_t tiles_in =
-        (c + 1 < a.g.n_chunks) ? a.g.tiles_per_chunk : (uint32_t)(a.g.n_tiles - c * a.g.tiles_per_chunk);
-    if (tiles_in == 1) {
-        chunk_result<MODE>(a, c, tile_sum);
-        return;
-    }
-    atomicAdd(&a.red.acc[c], tile_sum);
-    __threadfence();
-    const unsigned prev = atomicAdd(&a.red.done[c], 1u);
-    if (prev + 1 == tiles_in) {
-        __threadfence();
-        const unsigned long long s = atomicExch(&a.red.acc[c], 0ull);
-        atomicExch(&a.red.done[c], 0u);
-        chunk_result<MODE>(a, c, s);
-    }
-}
-
 // Index (relative to f0) of the fragment holding image byte x: the largest k
 // with s_off[k] <= x.  Empty fragments share their offset with the next
 // fragment, so the largest such k is never an empty one.
@@ -326,47 +306,95 @@ __global__ __launch_bounds__(kBlock) void tile_kernel(Args a)
         // block_sum's barriers also retire every lane's use of s_off before
         // the next tile refills it.
         const unsigned long long tile_sum = block_sum(acc, s_red);
-        if (tid == 0) finish_tile<MODE>(a, t, tile_sum);
+        if (tid == 0) a.partials[t] = tile_sum;
+    }
+}
+
+// One workgroup per chunk: add the chunk's tile sums; when expected is given,
+// also flag a mismatch.
+__global__ __launch_bounds__(kBlock) void chunk_reduce_kernel(ReduceArgs r)
+{
+    __shared__ unsigned long long s_red[kWaves];
+    const uint64_t c = r.c_lo + blockIdx.x;
+    const uint64_t t0 = c * r.tiles_per_chunk;
+    uint64_t t1 = t0 + r.tiles_per_chunk;
+    if (t1 > r.n_tiles) t1 = r.n_tiles;
+    unsigned long long acc = 0;
+    for (uint64_t t = t0 + threadIdx.x; t < t1; t += kBlock) acc += r.partials[t];
+    const unsigned long long s = block_sum(acc, s_red);
+    if (threadIdx.x == 0) {
+        r.sums_out[c] = s;
+        if (r.expected) r.bad[c] = (s != r.expected[c]) ? 1 : 0;
     }
 }
 
 template <int MODE>
-hipError_t launch(const Args& a, uint32_t grid_cap, hipStream_t s)
+hipError_t launch(const Args& a, const Geometry& g, unsigned long long* sums_out, const unsigned long long* expected,
+                  uint8_t* bad, uint32_t grid_cap, hipStream_t s)
 {
     if (a.t_hi <= a.t_lo) return hipSuccess;
     const uint64_t n = a.t_hi - a.t_lo;
     const uint32_t grid = (uint32_t)(n < grid_cap ? n : grid_cap);
     hipLaunchKernelGGL(tile_kernel<MODE>, dim3(grid), dim3(kBlock), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // Launches cover whole chunks, so the tiles of [c_lo, c_hi) are all here.
+    ReduceArgs r;
+    r.partials = a.partials;
+    r.c_lo = a.t_lo / g.tiles_per_chunk;
+    r.c_hi = (a.t_hi + g.tiles_per_chunk - 1) / g.tiles_per_chunk;
+    r.n_tiles = g.n_tiles;
+    r.tiles_per_chunk = g.tiles_per_chunk;
+    r.sums_out = sums_out;
+    r.expected = expected;
+    r.bad = bad;
+    hipLaunchKernelGGL(chunk_reduce_kernel, dim3((uint32_t)(r.c_hi - r.c_lo)), dim3(kBlock), 0, s, r);
     return hipGetLastError();
+}
+
+// One lane: publish "this point of the stream has been reached" to a DMA
+// engine by storing 0 into an HSA signal value it polls.  The store is a
+// system-scope release; the kernels before it on the stream have finished
+// and their writes are past the L2 (the stream's kernel boundaries release
+// at device scope, which on a multi-XCD part writes the L2 back).
+__global__ void release_signal_kernel(int64_t* value)
+{
+    __hip_atomic_store(value, (int64_t)0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
 } // namespace
 
+hipError_t launch_release(int64_t* signal_value, hipStream_t s)
+{
+    hipLaunchKernelGGL(release_signal_kernel, dim3(1), dim3(1), 0, s, signal_value);
+    return hipGetLastError();
+}
+
 hipError_t launch_pack(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
                        const Geometry& g, uint64_t t_lo, uint64_t t_hi, uint8_t* dst, uint64_t dst_origin,
-                       ChunkReduce red, unsigned long long* sums_out, uint32_t grid_cap, hipStream_t s)
+                       unsigned long long* partials, unsigned long long* sums_out, uint32_t grid_cap, hipStream_t s)
 {
-    Args a{frags, tile_first, tile_last, g, t_lo, t_hi, dst, dst_origin, red, sums_out, nullptr, nullptr};
-    return launch<PACK>(a, grid_cap, s);
+    Args a{frags, tile_first, tile_last, g, t_lo, t_hi, dst, dst_origin, partials};
+    return launch<PACK>(a, g, sums_out, nullptr, nullptr, grid_cap, s);
 }
 
 hipError_t launch_scatter_verify(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
                                  const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src,
-                                 uint64_t src_origin, ChunkReduce red, const unsigned long long* expected,
-                                 unsigned long long* recomputed, uint8_t* bad, uint32_t grid_cap, hipStream_t s)
+                                 uint64_t src_origin, unsigned long long* partials,
+                                 const unsigned long long* expected, unsigned long long* recomputed, uint8_t* bad,
+                                 uint32_t grid_cap, hipStream_t s)
 {
-    Args a{frags, tile_first, tile_last, g, t_lo, t_hi, const_cast<uint8_t*>(src), src_origin, red, recomputed,
-           expected, bad};
-    return launch<SCATTER>(a, grid_cap, s);
+    Args a{frags, tile_first, tile_last, g, t_lo, t_hi, const_cast<uint8_t*>(src), src_origin, partials};
+    return launch<SCATTER>(a, g, recomputed, expected, bad, grid_cap, s);
 }
 
 hipError_t launch_checksum_verify(const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src,
-                                  uint64_t src_origin, ChunkReduce red, const unsigned long long* expected,
-                                  unsigned long long* recomputed, uint8_t* bad, uint32_t grid_cap, hipStream_t s)
+                                  uint64_t src_origin, unsigned long long* partials,
+                                  const unsigned long long* expected, unsigned long long* recomputed, uint8_t* bad,
+                                  uint32_t grid_cap, hipStream_t s)
 {
-    Args a{nullptr, nullptr, nullptr, g, t_lo, t_hi, const_cast<uint8_t*>(src), src_origin, red, recomputed,
-           expected, bad};
-    return launch<VERIFY>(a, grid_cap, s);
+    Args a{nullptr, nullptr, nullptr, g, t_lo, t_hi, const_cast<uint8_t*>(src), src_origin, partials};
+    return launch<VERIFY>(a, g, recomputed, expected, bad, grid_cap, s);
 }
 
 } // namespace ckpt

@@ -1,32 +1,49 @@
 // ckpt_runtime.cpp -- host side of libckpt (the C ABI of include/ckpt.h).
 //
-// Pipeline of one snapshot (paper Sec. V-B, D2H phase; Sec. VI-A):
-//   caller stream --event--> pack stream: for each chunk group g
-//       [wait until the copy that last read g's staging area is done]
-//       pack kernel (fragments -> staging, chunk sums)   -> event captured[g]
-//   copy stream: for each group g
-//       wait captured[g]; DMA staging -> pinned host image; event area_free
-//   copy stream: DMA chunk sums -> pinned sums; event commit
-// The two pinned host images alternate (ping-pong): a snapshot targets the
-// image that does not hold the newest live (in-flight or committed)
-// snapshot.  Because one copy stream carries every snapshot's copies in
-// order, a snapshot's first byte lands only after the previous snapshot's
-// commit event, so a committed image exists at every point (invariant I4 of
-// Sec. V-C: an unfinished snapshot is never the recovery point).
-// "Committed" is the completion of the commit event; it is queried, not
-// signalled, so the library runs no helper thread.
+// One snapshot (paper Sec. V-B, D2H phase; Sec. VI-A, ping-pong buffers and
+// the wait before the optimizer step), chunk group by chunk group g:
+//
+//   pack stream  : [wait: area_done[area(g)] >= uses of the area issued so far]
+//                  pack kernels (fragments -> staging, chunk sums)
+//                  event captured[g]            <- the gate waits on this
+//                  release kernel: dep[g] = 0
+//   SDMA engine e: (polls dep[g]) copy staging(g) -> pinned image   -> copied[g]
+//                  (after copied[g]) 8-byte copy: area_done[area(g)] = use count
+//   after the last group: release dep_sums; SDMA copies the chunk sums.
+//
+// Every copy completes into a signal of its own that starts at 1 (the
+// area-done copy of group g into flagged[g], the sums copy into `done`), so
+// the snapshot is committed exactly when `done` and every flagged[g] have
+// reached 0.
+//
+// The image copies go to the DMA engines through the HSA runtime that HIP
+// itself runs on, two engines taking alternate groups (one engine alone
+// does not fill the host link).  A plain hipMemcpyAsync D2H may instead be
+// run as a copy kernel on the compute units, competing with the pack and
+// with the training step.
+//
+// The two pinned images alternate: a snapshot takes the image that does not
+// hold the newest live (in flight or committed) snapshot.  Its copies are
+// ordered after that snapshot's (the same staging areas gate them), so a
+// committed image exists at every point, and an interrupted snapshot is
+// never the recovery point (invariant I4 of Sec. V-C).
 //
 // Recovery (Sec. V-C third stage, Sec. VI-E) reverses the path group by
 // group: DMA host image -> staging on the copy stream, then the scatter
-// kernel on the pack stream writes the fragments and checks the sums.
+// kernel on the pack stream writes the fragments and re-checks the sums.
 #include <hip/hip_runtime.h>
+#include <hsa/hsa.h>
+#include <hsa/hsa_ext_amd.h>
 
 #include <algorithm>
+#include <chrono>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "../../include/ckpt.h"
@@ -42,27 +59,33 @@ constexpr uint64_t kDefaultGroup = 1ull << 30;
 constexpr uint32_t kMaxTileShift = 16; // 64 KiB tiles at most
 constexpr uint32_t kMaxMeta = 1u << 20;
 constexpr uint32_t kDefaultGrid = 2048; // 256 CUs x 8 workgroups
+constexpr int kMaxEngines = 2;
 
 struct Frag {
     uint64_t ptr, nbytes, off;
     uint32_t dtype, cls;
 };
 
-// GPU resources of one snapshot record, recycled between snapshots.
+// GPU-side resources of one snapshot record, recycled between snapshots.
 struct RecRes {
-    std::vector<hipEvent_t> captured; // per group, on the pack stream
-    hipEvent_t commit = nullptr;      // on the copy stream, after the sums landed
+    std::vector<hipEvent_t> captured;   // per group, on the pack stream
+    std::vector<hsa_signal_t> dep;      // per group: set to 0 by the GPU once g is packed
+    std::vector<int64_t*> dep_val;      // value addresses of dep
+    std::vector<hsa_signal_t> copied;   // per group: the group's image copy finished
+    std::vector<hsa_signal_t> flagged;  // per group: the area-done copy after it finished
+    hsa_signal_t dep_sums{0}, done{0};  // sums packed; sums copied (the last copy issued)
+    int64_t* dep_sums_val = nullptr;
+    uint64_t* h_seq = nullptr;          // pinned, per group: area use number, source of the area-done copy
     unsigned long long* d_sums = nullptr;
-    // timing (only with timing on)
-    std::vector<hipEvent_t> k0, k1; // per group around the pack launch
-    hipEvent_t t0 = nullptr, c0 = nullptr, c1 = nullptr;
+    std::vector<hipEvent_t> k0, k1;     // timing: around each pack launch
+    hipEvent_t t0 = nullptr;
 };
 
 struct SnapRec {
     uint64_t id = 0, step = 0;
     int buf = -1;
     bool aborted = false;
-    bool committed = false; // cached once the commit event has completed
+    bool committed = false; // cached once `done` has reached 0
     bool timed = false;
     uint32_t groups_copied = 0;
     std::vector<uint8_t> meta;
@@ -95,18 +118,17 @@ struct ckpt_ctx {
     uint64_t n_groups = 0; // groups
     bool ring = false;
     uint64_t n_slots = 0;  // ring slots (ring mode)
-    std::vector<uint64_t> group_payload; // fragment bytes inside each group
 
     // device memory
     FragDev* d_frags = nullptr;
     uint32_t* d_tile_first = nullptr;
     uint32_t* d_tile_last = nullptr;
     uint8_t* d_staging = nullptr;
-    unsigned long long* d_acc = nullptr; // [2][n_chunks]: pack, check
-    unsigned int* d_done = nullptr;      // [2][n_chunks]
+    unsigned long long* d_partials = nullptr; // [2][n_tiles] tile sums: pack, check
     unsigned long long* d_expected = nullptr;
     unsigned long long* d_recomputed = nullptr;
     uint8_t* d_bad = nullptr;
+    uint64_t* d_area_done = nullptr;          // per staging area: number of finished copies out of it
 
     // pinned host memory
     uint8_t* h_img[2] = {nullptr, nullptr};
@@ -115,11 +137,19 @@ struct ckpt_ctx {
     uint8_t* h_bad = nullptr;
     unsigned long long* h_recomputed = nullptr;
 
+    // HSA agents and DMA engines
+    hsa_agent_t gpu_agent{0}, img_agent[2] = {{0}, {0}};
+    hsa_amd_sdma_engine_id_t d2h_engine[kMaxEngines];
+    int n_d2h_engines = 0;
+    hsa_amd_sdma_engine_id_t h2d_engine{};
+    uint64_t ts_freq = 1;
+
     // streams and events
     hipStream_t s_pack = nullptr, s_copy = nullptr;
     hipEvent_t ev_trigger = nullptr, ev_done = nullptr;
-    std::vector<hipEvent_t> area_free; // per staging area (group in full mode, slot in ring mode)
-    std::vector<hipEvent_t> ev_loaded; // per group, restore/verify
+    std::vector<uint64_t> area_seq;     // per staging area: copies issued out of it
+    std::vector<hipEvent_t> area_free;  // restore/verify: per staging area
+    std::vector<hipEvent_t> ev_loaded;  // restore/verify: per group
     std::vector<RecRes*> free_res;
     std::map<uint64_t, SnapRec> recs;
     uint64_t next_id = 1;
@@ -129,6 +159,8 @@ struct ckpt_ctx {
     bool have_last_sums = false;
     std::vector<uint64_t> last_sums;
     OpTiming op_timing[3];
+    std::vector<hipEvent_t> tk0, tk1; // restore/verify timing
+    hipEvent_t tt0 = nullptr, tc0 = nullptr, tc1 = nullptr;
 
     std::string err;
 };
@@ -153,6 +185,20 @@ ckpt_status fail(ckpt_ctx* c, ckpt_status code, const char* fmt, ...)
         hipError_t e_ = (expr);                                                                              \
         if (e_ != hipSuccess)                                                                                \
             return fail((ctx), CKPT_EHIP, "%s failed: %s (%d)", #expr, hipGetErrorString(e_), (int)e_);       \
+    } while (0)
+
+const char* hsa_text(hsa_status_t s)
+{
+    const char* t = nullptr;
+    if (hsa_status_string(s, &t) != HSA_STATUS_SUCCESS || !t) return "unknown HSA status";
+    return t;
+}
+
+#define HSACHK(ctx, expr)                                                                                    \
+    do {                                                                                                     \
+        hsa_status_t s_ = (expr);                                                                            \
+        if (s_ != HSA_STATUS_SUCCESS)                                                                        \
+            return fail((ctx), CKPT_EHIP, "%s failed: %s (%d)", #expr, hsa_text(s_), (int)s_);               \
     } while (0)
 
 bool is_pow2(uint64_t x) { return x && !(x & (x - 1)); }
@@ -225,40 +271,165 @@ ckpt_status make_event(ckpt_ctx* c, hipEvent_t* e, bool timed)
     return CKPT_OK;
 }
 
+// ---- HSA: agents and engines ------------------------------------------------
+
+struct AgentSearch {
+    uint32_t bdf;
+    uint32_t domain;
+    hsa_agent_t found;
+    bool ok;
+};
+
+hsa_status_t find_gpu_cb(hsa_agent_t a, void* data)
+{
+    AgentSearch* s = (AgentSearch*)data;
+    hsa_device_type_t type;
+    if (hsa_agent_get_info(a, HSA_AGENT_INFO_DEVICE, &type) != HSA_STATUS_SUCCESS || type != HSA_DEVICE_TYPE_GPU)
+        return HSA_STATUS_SUCCESS;
+    uint32_t bdf = 0, domain = 0;
+    hsa_agent_get_info(a, (hsa_agent_info_t)HSA_AMD_AGENT_INFO_BDFID, &bdf);
+    hsa_agent_get_info(a, (hsa_agent_info_t)HSA_AMD_AGENT_INFO_DOMAIN, &domain);
+    if (bdf == s->bdf && domain == s->domain) {
+        s->found = a;
+        s->ok = true;
+        return HSA_STATUS_INFO_BREAK;
+    }
+    return HSA_STATUS_SUCCESS;
+}
+
+// The HSA agent of the context's device (matched by PCI location) and the
+// DMA engines for device-to-host copies.
+ckpt_status setup_hsa(ckpt_ctx* c)
+{
+    static std::once_flag once;
+    static hsa_status_t init_status = HSA_STATUS_SUCCESS;
+    std::call_once(once, [] { init_status = hsa_init(); }); // reference-counted; HIP has initialized it too
+    HSACHK(c, init_status);
+    int bus = 0, dev = 0, dom = 0;
+    HIPCHK(c, hipDeviceGetAttribute(&bus, hipDeviceAttributePciBusId, c->device));
+    HIPCHK(c, hipDeviceGetAttribute(&dev, hipDeviceAttributePciDeviceId, c->device));
+    HIPCHK(c, hipDeviceGetAttribute(&dom, hipDeviceAttributePciDomainID, c->device));
+    AgentSearch s{(uint32_t)((bus << 8) | (dev << 3)), (uint32_t)dom, {0}, false};
+    hsa_status_t st = hsa_iterate_agents(find_gpu_cb, &s);
+    if (st != HSA_STATUS_SUCCESS && st != HSA_STATUS_INFO_BREAK) HSACHK(c, st);
+    if (!s.ok) return fail(c, CKPT_EHIP, "no HSA agent at PCI %04x:%02x:%02x", dom, bus, dev);
+    c->gpu_agent = s.found;
+    HSACHK(c, hsa_system_get_info(HSA_SYSTEM_INFO_TIMESTAMP_FREQUENCY, &c->ts_freq));
+    return CKPT_OK;
+}
+
+// Owner agent of a pinned host image, and the engines for copies from the
+// device into it.
+ckpt_status setup_image_agent(ckpt_ctx* c, int b)
+{
+    hsa_amd_pointer_info_t info;
+    std::memset(&info, 0, sizeof info);
+    info.size = sizeof info;
+    HSACHK(c, hsa_amd_pointer_info(c->h_img[b], &info, nullptr, nullptr, nullptr));
+    c->img_agent[b] = info.agentOwner;
+    hsa_device_type_t type = HSA_DEVICE_TYPE_GPU;
+    if (info.agentOwner.handle) hsa_agent_get_info(info.agentOwner, HSA_AGENT_INFO_DEVICE, &type);
+    if (type != HSA_DEVICE_TYPE_CPU) { // take the first CPU agent
+        hsa_status_t st = hsa_iterate_agents(
+            [](hsa_agent_t a, void* data) -> hsa_status_t {
+                hsa_device_type_t t;
+                if (hsa_agent_get_info(a, HSA_AGENT_INFO_DEVICE, &t) == HSA_STATUS_SUCCESS && t == HSA_DEVICE_TYPE_CPU) {
+                    *(hsa_agent_t*)data = a;
+                    return HSA_STATUS_INFO_BREAK;
+                }
+                return HSA_STATUS_SUCCESS;
+            },
+            &c->img_agent[b]);
+        if (st != HSA_STATUS_SUCCESS && st != HSA_STATUS_INFO_BREAK) HSACHK(c, st);
+    }
+    if (b == 0) {
+        uint32_t mask = 0;
+        HSACHK(c, hsa_amd_memory_copy_engine_status(c->img_agent[0], c->gpu_agent, &mask));
+        c->n_d2h_engines = 0;
+        for (int k = 0; k < 16 && c->n_d2h_engines < kMaxEngines; ++k)
+            if (mask & (1u << k)) c->d2h_engine[c->n_d2h_engines++] = (hsa_amd_sdma_engine_id_t)(1u << k);
+        if (c->n_d2h_engines == 0) return fail(c, CKPT_EHIP, "no DMA engine available for device-to-host copies");
+        uint32_t hmask = 0;
+        HSACHK(c, hsa_amd_memory_copy_engine_status(c->gpu_agent, c->img_agent[0], &hmask));
+        c->h2d_engine = c->d2h_engine[0];
+        for (int k = 0; k < 16; ++k)
+            if (hmask & (1u << k)) {
+                c->h2d_engine = (hsa_amd_sdma_engine_id_t)(1u << k);
+                break;
+            }
+    }
+    return CKPT_OK;
+}
+
 void destroy_res(RecRes* r)
 {
-    for (auto e : r->captured) (void)hipEventDestroy(e);
-    for (auto e : r->k0) (void)hipEventDestroy(e);
-    for (auto e : r->k1) (void)hipEventDestroy(e);
-    if (r->commit) (void)hipEventDestroy(r->commit);
+    for (auto e : r->captured)
+        if (e) (void)hipEventDestroy(e);
+    for (auto e : r->k0)
+        if (e) (void)hipEventDestroy(e);
+    for (auto e : r->k1)
+        if (e) (void)hipEventDestroy(e);
     if (r->t0) (void)hipEventDestroy(r->t0);
-    if (r->c0) (void)hipEventDestroy(r->c0);
-    if (r->c1) (void)hipEventDestroy(r->c1);
+    for (auto s : r->dep)
+        if (s.handle) hsa_signal_destroy(s);
+    for (auto s : r->copied)
+        if (s.handle) hsa_signal_destroy(s);
+    for (auto s : r->flagged)
+        if (s.handle) hsa_signal_destroy(s);
+    if (r->dep_sums.handle) hsa_signal_destroy(r->dep_sums);
+    if (r->done.handle) hsa_signal_destroy(r->done);
+    if (r->h_seq) (void)hipHostFree(r->h_seq);
     if (r->d_sums) (void)hipFree(r->d_sums);
     delete r;
 }
 
-ckpt_status get_res(ckpt_ctx* c, RecRes** out)
+ckpt_status gpu_only_signal(ckpt_ctx* c, hsa_signal_t* s, int64_t** val)
 {
-    if (!c->free_res.empty()) {
-        *out = c->free_res.back();
-        c->free_res.pop_back();
-        return CKPT_OK;
-    }
+    HSACHK(c, hsa_amd_signal_create(1, 0, nullptr, HSA_AMD_SIGNAL_AMD_GPU_ONLY, s));
+    volatile hsa_signal_value_t* p = nullptr;
+    HSACHK(c, hsa_amd_signal_value_pointer(*s, &p));
+    if (val) *val = (int64_t*)p;
+    return CKPT_OK;
+}
+
+// A signal only the GPU waits on (no interrupt event behind it); the host
+// may still read it.
+ckpt_status gpu_consumed_signal(ckpt_ctx* c, hsa_signal_t* s)
+{
+    HSACHK(c, hsa_signal_create(0, 1, &c->gpu_agent, s));
+    return CKPT_OK;
+}
+
+ckpt_status new_res(ckpt_ctx* c, RecRes** out)
+{
     RecRes* r = new RecRes();
-    r->captured.resize(c->n_groups, nullptr);
-    r->k0.resize(c->n_groups, nullptr);
-    r->k1.resize(c->n_groups, nullptr);
+    const uint64_t n = c->n_groups;
+    r->captured.assign(n, nullptr);
+    r->k0.assign(n, nullptr);
+    r->k1.assign(n, nullptr);
+    r->dep.assign(n, hsa_signal_t{0});
+    r->dep_val.assign(n, nullptr);
+    r->copied.assign(n, hsa_signal_t{0});
+    r->flagged.assign(n, hsa_signal_t{0});
     ckpt_status st = CKPT_OK;
-    for (uint64_t g = 0; g < c->n_groups && st == CKPT_OK; ++g) {
+    for (uint64_t g = 0; g < n && st == CKPT_OK; ++g) {
         st = make_event(c, &r->captured[g], false);
         if (st == CKPT_OK) st = make_event(c, &r->k0[g], true);
         if (st == CKPT_OK) st = make_event(c, &r->k1[g], true);
+        if (st == CKPT_OK) st = gpu_only_signal(c, &r->dep[g], &r->dep_val[g]);
+        if (st == CKPT_OK) st = gpu_consumed_signal(c, &r->copied[g]);
+        if (st == CKPT_OK) st = gpu_consumed_signal(c, &r->flagged[g]);
     }
-    if (st == CKPT_OK) st = make_event(c, &r->commit, false);
     if (st == CKPT_OK) st = make_event(c, &r->t0, true);
-    if (st == CKPT_OK) st = make_event(c, &r->c0, true);
-    if (st == CKPT_OK) st = make_event(c, &r->c1, true);
+    if (st == CKPT_OK) st = gpu_only_signal(c, &r->dep_sums, &r->dep_sums_val);
+    if (st == CKPT_OK && hsa_signal_create(0, 0, nullptr, &r->done) != HSA_STATUS_SUCCESS) {
+        r->done.handle = 0;
+        st = fail(c, CKPT_EHIP, "hsa_signal_create failed");
+    }
+    if (st == CKPT_OK && hipHostMalloc((void**)&r->h_seq, std::max<uint64_t>(n, 1) * 8, hipHostMallocDefault) != hipSuccess) {
+        r->h_seq = nullptr;
+        st = fail(c, CKPT_ENOMEM, "pinned use-number slots");
+    }
     if (st == CKPT_OK && hipMalloc(&r->d_sums, std::max<uint64_t>(c->n_chunks, 1) * 8) != hipSuccess) {
         r->d_sums = nullptr;
         st = fail(c, CKPT_ENOMEM, "hipMalloc of %llu chunk sums failed", (unsigned long long)c->n_chunks);
@@ -271,36 +442,60 @@ ckpt_status get_res(ckpt_ctx* c, RecRes** out)
     return CKPT_OK;
 }
 
-// Is the snapshot's commit event complete?  (Never true for an aborted one.)
-ckpt_status query_committed(ckpt_ctx* c, SnapRec& r, bool* out)
+ckpt_status get_res(ckpt_ctx* c, RecRes** out)
 {
-    if (r.aborted) {
-        *out = false;
+    if (!c->free_res.empty()) {
+        *out = c->free_res.back();
+        c->free_res.pop_back();
         return CKPT_OK;
     }
-    if (!r.committed) {
-        hipError_t q = hipEventQuery(r.res->commit);
-        if (q == hipSuccess) r.committed = true;
-        else if (q != hipErrorNotReady)
-            return fail(c, CKPT_EHIP, "hipEventQuery(commit) failed: %s", hipGetErrorString(q));
+    return new_res(c, out);
+}
+
+bool copies_done(const SnapRec& r)
+{
+    if (hsa_signal_load_scacquire(r.res->done) != 0) return false;
+    for (uint32_t g = 0; g < r.groups_copied; ++g)
+        if (hsa_signal_load_scacquire(r.res->flagged[g]) != 0) return false;
+    return true;
+}
+
+// Wait (bounded) until every copy of a snapshot has finished.
+ckpt_status wait_copies(ckpt_ctx* c, SnapRec& r)
+{
+    const uint64_t limit = 120 * c->ts_freq; // two minutes of system-timestamp ticks
+    if (hsa_signal_wait_scacquire(r.res->done, HSA_SIGNAL_CONDITION_EQ, 0, limit, HSA_WAIT_STATE_BLOCKED) != 0)
+        return fail(c, CKPT_EHIP, "snapshot %llu: chunk sums not copied after 120 s", (unsigned long long)r.id);
+    // The per-group signals have the GPU as their only waiter; the host
+    // polls their values (the engines run the groups in order, so this
+    // rarely finds one still pending once the sums have landed).
+    const auto deadline = std::chrono::steady_clock::now() + std::chrono::seconds(120);
+    for (uint32_t g = 0; g < r.groups_copied; ++g) {
+        while (hsa_signal_load_scacquire(r.res->flagged[g]) != 0) {
+            if (std::chrono::steady_clock::now() > deadline)
+                return fail(c, CKPT_EHIP, "snapshot %llu: group %u not copied after 120 s", (unsigned long long)r.id, g);
+            std::this_thread::sleep_for(std::chrono::microseconds(20));
+        }
     }
-    *out = r.committed;
     return CKPT_OK;
 }
 
-// Drop records that are neither among the newest four nor held by an image.
+// Has the snapshot committed?  (Never true for an interrupted one.)
+bool query_committed(SnapRec& r)
+{
+    if (r.aborted) return false;
+    if (!r.committed && copies_done(r)) r.committed = true;
+    return r.committed;
+}
+
+// Drop records that are neither among the newest four nor held by an image
+// and whose copies are all finished.
 void prune(ckpt_ctx* c)
 {
     for (auto it = c->recs.begin(); it != c->recs.end();) {
         SnapRec& r = it->second;
         const bool held = (c->holder[0] == r.id || c->holder[1] == r.id);
-        bool done = r.aborted || r.committed;
-        if (!done) {
-            hipError_t q = hipEventQuery(r.res->commit);
-            done = (q == hipSuccess);
-            if (done) r.committed = true;
-        }
-        if (!held && done && r.id + 4 < c->next_id) {
+        if (!held && r.id + 4 < c->next_id && copies_done(r)) {
             c->free_res.push_back(r.res);
             it = c->recs.erase(it);
         } else {
@@ -309,10 +504,15 @@ void prune(ckpt_ctx* c)
     }
 }
 
+// Wait for every enqueued kernel and copy of the context.
 ckpt_status drain(ckpt_ctx* c)
 {
     HIPCHK(c, hipStreamSynchronize(c->s_pack));
     HIPCHK(c, hipStreamSynchronize(c->s_copy));
+    for (auto& kv : c->recs) {
+        ckpt_status st = wait_copies(c, kv.second);
+        if (st) return st;
+    }
     return CKPT_OK;
 }
 
@@ -322,10 +522,7 @@ ckpt_status pick_committed(ckpt_ctx* c, uint64_t snap_id, SnapRec** out)
     SnapRec* best = nullptr;
     for (auto& kv : c->recs) {
         SnapRec& r = kv.second;
-        bool com = false;
-        ckpt_status st = query_committed(c, r, &com);
-        if (st) return st;
-        if (!com || c->holder[r.buf] != r.id) continue;
+        if (!query_committed(r) || c->holder[r.buf] != r.id) continue;
         if (snap_id != 0 && r.id != snap_id) continue;
         if (!best || r.id > best->id) best = &r;
     }
@@ -336,6 +533,22 @@ ckpt_status pick_committed(ckpt_ctx* c, uint64_t snap_id, SnapRec** out)
     }
     *out = best;
     return CKPT_OK;
+}
+
+// Zero a pinned host image from several threads, so that its pages are
+// resident before the first snapshot streams into it.
+void parallel_zero(uint8_t* p, uint64_t n)
+{
+    unsigned nt = std::thread::hardware_concurrency();
+    nt = std::max(1u, std::min(nt, 16u));
+    if (n < (64ull << 20)) nt = 1;
+    std::vector<std::thread> th;
+    const uint64_t per = (n / nt + 4095) & ~4095ull;
+    for (unsigned k = 0; k < nt; ++k) {
+        const uint64_t lo = std::min<uint64_t>(k * per, n), hi = std::min<uint64_t>(lo + per, n);
+        th.emplace_back([=] { std::memset(p + lo, 0, hi - lo); });
+    }
+    for (auto& t : th) t.join();
 }
 
 float elapsed(hipEvent_t a, hipEvent_t b)
@@ -359,38 +572,34 @@ ckpt_status run_check(ckpt_ctx* c, uint64_t snap_id, hipStream_t stream, bool sc
     if (st) return st;
     const int b = r->buf;
     const int op = scatter ? CKPT_OP_RESTORE : CKPT_OP_VERIFY;
-    RecRes* tr = nullptr; // timing events borrowed from a free record
-    if (c->timing) {
-        st = get_res(c, &tr);
-        if (st) return st;
-    }
-    ChunkReduce red{c->d_acc + c->n_chunks, c->d_done + c->n_chunks};
+    const bool timed = c->timing;
+    unsigned long long* partials = c->d_partials + c->geo.n_tiles;
     HIPCHK(c, hipMemcpyAsync(c->d_expected, c->h_sums[b], c->n_chunks * 8, hipMemcpyHostToDevice, c->s_copy));
     if (scatter) {
         HIPCHK(c, hipEventRecord(c->ev_trigger, stream));
         HIPCHK(c, hipStreamWaitEvent(c->s_pack, c->ev_trigger, 0));
     }
-    if (tr) HIPCHK(c, hipEventRecord(tr->t0, c->s_copy));
+    if (timed) HIPCHK(c, hipEventRecord(c->tt0, c->s_copy));
     for (uint64_t g = 0; g < c->n_groups; ++g) {
         const uint64_t lo = group_lo(c, g), hi = group_hi(c, g);
         HIPCHK(c, hipStreamWaitEvent(c->s_copy, c->area_free[area_of(c, g)], 0));
-        if (tr && g == 0) HIPCHK(c, hipEventRecord(tr->c0, c->s_copy));
+        if (timed && g == 0) HIPCHK(c, hipEventRecord(c->tc0, c->s_copy));
         HIPCHK(c, hipMemcpyAsync(staging_of(c, g), c->h_img[b] + lo, hi - lo, hipMemcpyHostToDevice, c->s_copy));
-        if (tr && g + 1 == c->n_groups) HIPCHK(c, hipEventRecord(tr->c1, c->s_copy));
+        if (timed && g + 1 == c->n_groups) HIPCHK(c, hipEventRecord(c->tc1, c->s_copy));
         HIPCHK(c, hipEventRecord(c->ev_loaded[g], c->s_copy));
         HIPCHK(c, hipStreamWaitEvent(c->s_pack, c->ev_loaded[g], 0));
-        if (tr) HIPCHK(c, hipEventRecord(tr->k0[g], c->s_pack));
+        if (timed) HIPCHK(c, hipEventRecord(c->tk0[g], c->s_pack));
         const uint64_t t_lo = tiles_lo(c, g), t_hi = tiles_hi(c, g);
         hipError_t e;
         if (scatter)
             e = launch_scatter_verify(c->d_frags, c->d_tile_first, c->d_tile_last, c->geo, t_lo, t_hi,
-                                      staging_of(c, g), lo, red, c->d_expected, c->d_recomputed, c->d_bad,
+                                      staging_of(c, g), lo, partials, c->d_expected, c->d_recomputed, c->d_bad,
                                       c->grid_cap, c->s_pack);
         else
-            e = launch_checksum_verify(c->geo, t_lo, t_hi, staging_of(c, g), lo, red, c->d_expected,
+            e = launch_checksum_verify(c->geo, t_lo, t_hi, staging_of(c, g), lo, partials, c->d_expected,
                                        c->d_recomputed, c->d_bad, c->grid_cap, c->s_pack);
         if (e != hipSuccess) return fail(c, CKPT_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
-        if (tr) HIPCHK(c, hipEventRecord(tr->k1[g], c->s_pack));
+        if (timed) HIPCHK(c, hipEventRecord(c->tk1[g], c->s_pack));
         HIPCHK(c, hipEventRecord(c->area_free[area_of(c, g)], c->s_pack));
     }
     HIPCHK(c, hipMemcpyAsync(c->h_bad, c->d_bad, c->n_chunks, hipMemcpyDeviceToHost, c->s_pack));
@@ -398,18 +607,17 @@ ckpt_status run_check(ckpt_ctx* c, uint64_t snap_id, hipStream_t stream, bool sc
     HIPCHK(c, hipEventRecord(c->ev_done, c->s_pack));
     if (scatter) HIPCHK(c, hipStreamWaitEvent(stream, c->ev_done, 0));
     HIPCHK(c, hipEventSynchronize(c->ev_done));
-    if (tr) {
+    if (timed) {
         ckpt_timing t{};
-        for (uint64_t g = 0; g < c->n_groups; ++g) t.kernel_ms += elapsed(tr->k0[g], tr->k1[g]);
+        for (uint64_t g = 0; g < c->n_groups; ++g) t.kernel_ms += elapsed(c->tk0[g], c->tk1[g]);
         t.kernels = (uint32_t)c->n_groups;
         t.copies = (uint32_t)c->n_groups;
-        t.copy_ms = elapsed(tr->c0, tr->c1);
-        t.total_ms = elapsed(tr->t0, tr->k1[c->n_groups - 1]);
+        t.copy_ms = elapsed(c->tc0, c->tc1);
+        t.total_ms = elapsed(c->tt0, c->tk1[c->n_groups - 1]);
         t.kernel_bytes = scatter ? 2 * c->payload : c->I;
         t.copy_bytes = c->I;
         c->op_timing[op].t = t;
         c->op_timing[op].valid = true;
-        c->free_res.push_back(tr);
     }
     c->last_sums.assign(c->h_recomputed, c->h_recomputed + c->n_chunks);
     c->have_last_sums = true;
@@ -421,8 +629,8 @@ ckpt_status run_check(ckpt_ctx* c, uint64_t snap_id, hipStream_t stream, bool sc
         }
     }
     *n_bad = nb;
-    if (nb) return fail(c, CKPT_ECORRUPT, "%u of %llu chunks failed their checksum", nb,
-                        (unsigned long long)c->n_chunks);
+    if (nb)
+        return fail(c, CKPT_ECORRUPT, "%u of %llu chunks failed their checksum", nb, (unsigned long long)c->n_chunks);
     return CKPT_OK;
 }
 
@@ -434,17 +642,19 @@ void free_ctx(ckpt_ctx* c)
     c->free_res.clear();
     for (auto e : c->area_free) (void)hipEventDestroy(e);
     for (auto e : c->ev_loaded) (void)hipEventDestroy(e);
-    if (c->ev_trigger) (void)hipEventDestroy(c->ev_trigger);
-    if (c->ev_done) (void)hipEventDestroy(c->ev_done);
+    for (auto e : c->tk0) (void)hipEventDestroy(e);
+    for (auto e : c->tk1) (void)hipEventDestroy(e);
+    for (hipEvent_t e : {c->ev_trigger, c->ev_done, c->tt0, c->tc0, c->tc1})
+        if (e) (void)hipEventDestroy(e);
     (void)hipFree(c->d_frags);
     (void)hipFree(c->d_tile_first);
     (void)hipFree(c->d_tile_last);
     (void)hipFree(c->d_staging);
-    (void)hipFree(c->d_acc);
-    (void)hipFree(c->d_done);
+    (void)hipFree(c->d_partials);
     (void)hipFree(c->d_expected);
     (void)hipFree(c->d_recomputed);
     (void)hipFree(c->d_bad);
+    (void)hipFree(c->d_area_done);
     for (int b = 0; b < 2; ++b) {
         if (c->h_img[b]) (void)hipHostFree(c->h_img[b]);
         if (c->h_sums[b]) (void)hipHostFree(c->h_sums[b]);
@@ -454,6 +664,18 @@ void free_ctx(ckpt_ctx* c)
     if (c->s_pack) (void)hipStreamDestroy(c->s_pack);
     if (c->s_copy) (void)hipStreamDestroy(c->s_copy);
 }
+
+// Issue one SDMA copy; on failure the dependency chain of the snapshot is
+// released so no engine is left polling.
+ckpt_status dma(ckpt_ctx* c, void* dst, hsa_agent_t dst_agent, const void* src, hsa_agent_t src_agent, uint64_t n,
+                const hsa_signal_t* dep, hsa_signal_t completion, hsa_amd_sdma_engine_id_t engine)
+{
+    HSACHK(c, hsa_amd_memory_async_copy_on_engine(dst, dst_agent, src, src_agent, n, dep ? 1 : 0, dep, completion,
+                                                  engine, true));
+    return CKPT_OK;
+}
+
+ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop);
 
 } // namespace
 
@@ -484,8 +706,11 @@ ckpt_status ckpt_create(const ckpt_config* cfg, ckpt_ctx** out)
         hipStreamCreateWithFlags(&c->s_pack, hipStreamNonBlocking) != hipSuccess ||
         hipStreamCreateWithFlags(&c->s_copy, hipStreamNonBlocking) != hipSuccess)
         st = CKPT_EHIP;
-    if (st == CKPT_OK) st = make_event(c, &c->ev_trigger, false);
-    if (st == CKPT_OK) st = make_event(c, &c->ev_done, false);
+    for (hipEvent_t* e : {&c->ev_trigger, &c->ev_done})
+        if (st == CKPT_OK) st = make_event(c, e, false);
+    for (hipEvent_t* e : {&c->tt0, &c->tc0, &c->tc1})
+        if (st == CKPT_OK) st = make_event(c, e, true);
+    if (st == CKPT_OK) st = setup_hsa(c);
     if (st != CKPT_OK) {
         free_ctx(c);
         delete c;
@@ -499,8 +724,7 @@ ckpt_status ckpt_destroy(ckpt_ctx* ctx)
 {
     if (!ctx) return CKPT_OK;
     (void)hipSetDevice(ctx->device);
-    if (ctx->s_pack) (void)hipStreamSynchronize(ctx->s_pack);
-    if (ctx->s_copy) (void)hipStreamSynchronize(ctx->s_copy);
+    (void)drain(ctx);
     free_ctx(ctx);
     delete ctx;
     return CKPT_OK;
@@ -512,8 +736,7 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
     if (c->registered) return fail(c, CKPT_ESTATE, "tensors already registered");
     if (!t || n == 0) return fail(c, CKPT_EINVAL, "need at least one fragment");
     HIPCHK(c, hipSetDevice(c->device));
-
-    std::vector<uint64_t> nb(n), off(n);
+    std::vector<uint64_t> nb(n);
     for (uint32_t i = 0; i < n; ++i) {
         if (t[i].nbytes && !t[i].dev_ptr) return fail(c, CKPT_EINVAL, "fragment %u: null pointer", i);
         nb[i] = t[i].nbytes;
@@ -539,14 +762,13 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
     c->geo.tiles_per_chunk = (uint32_t)(c->C >> pl.tile_shift);
     c->geo.n_tiles = pl.n_tiles;
     c->geo.n_chunks = c->n_chunks;
-    const uint32_t ts = pl.tile_shift;
 
-    // Groups: whole chunks per pack launch / DMA request; one chunk per slot in ring mode.
+    // Groups: whole chunks per pack launch and DMA request; one chunk per
+    // slot in ring mode.
     if (c->staging_cap) {
         c->ring = true;
         c->G = 1;
-        c->n_slots = std::min<uint64_t>(c->staging_cap / c->C, c->n_chunks);
-        if (c->n_slots < 1) c->n_slots = 1;
+        c->n_slots = std::max<uint64_t>(1, std::min<uint64_t>(c->staging_cap / c->C, c->n_chunks));
     } else {
         c->G = std::max<uint64_t>(1, c->group_cfg / c->C);
     }
@@ -560,20 +782,7 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
         fd[i].end = pl.end[i];
     }
     const uint64_t nt = pl.n_tiles;
-    std::vector<uint32_t>& tf = pl.tile_first;
-    std::vector<uint32_t>& tl = pl.tile_last;
-    std::vector<uint64_t> gp(c->n_groups, 0);
-    for (uint32_t i = 0; i < n; ++i) {
-        uint64_t a = fd[i].off, b = fd[i].off + fd[i].nbytes;
-        while (a < b) {
-            const uint64_t g = a / (c->G * c->C);
-            const uint64_t ge = std::min(b, (g + 1) * c->G * c->C);
-            gp[g] += ge - a;
-            a = ge;
-        }
-    }
-    c->group_payload = gp;
-    (void)ts;
+    const uint64_t n_areas = c->ring ? c->n_slots : c->n_groups;
 
 #define ALLOC(ptr, bytes)                                                                                   \
     do {                                                                                                    \
@@ -585,32 +794,34 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
     ALLOC(c->d_frags, n * sizeof(FragDev));
     ALLOC(c->d_tile_first, nt * 4);
     ALLOC(c->d_tile_last, nt * 4);
-    ALLOC(c->d_acc, 2 * c->n_chunks * 8);
-    ALLOC(c->d_done, 2 * c->n_chunks * 4);
+    ALLOC(c->d_partials, 2 * nt * 8);
     ALLOC(c->d_expected, c->n_chunks * 8);
     ALLOC(c->d_recomputed, c->n_chunks * 8);
     ALLOC(c->d_bad, c->n_chunks);
+    ALLOC(c->d_area_done, n_areas * 8);
     ALLOC(c->d_staging, c->ring ? c->n_slots * c->C : c->I);
 #undef ALLOC
     HIPCHK(c, hipMemcpy(c->d_frags, fd.data(), n * sizeof(FragDev), hipMemcpyHostToDevice));
-    HIPCHK(c, hipMemcpy(c->d_tile_first, tf.data(), nt * 4, hipMemcpyHostToDevice));
-    HIPCHK(c, hipMemcpy(c->d_tile_last, tl.data(), nt * 4, hipMemcpyHostToDevice));
-    HIPCHK(c, hipMemset(c->d_acc, 0, 2 * c->n_chunks * 8));
-    HIPCHK(c, hipMemset(c->d_done, 0, 2 * c->n_chunks * 4));
+    HIPCHK(c, hipMemcpy(c->d_tile_first, pl.tile_first.data(), nt * 4, hipMemcpyHostToDevice));
+    HIPCHK(c, hipMemcpy(c->d_tile_last, pl.tile_last.data(), nt * 4, hipMemcpyHostToDevice));
+    HIPCHK(c, hipMemset(c->d_area_done, 0, n_areas * 8));
+    c->area_seq.assign(n_areas, 0);
     for (int b = 0; b < 2; ++b) {
         if (hipHostMalloc((void**)&c->h_img[b], c->I, hipHostMallocDefault) != hipSuccess) {
             c->h_img[b] = nullptr;
             return fail(c, CKPT_ENOMEM, "pinned host image of %llu bytes", (unsigned long long)c->I);
         }
+        parallel_zero(c->h_img[b], c->I);
         if (hipHostMalloc((void**)&c->h_sums[b], c->n_chunks * 8, hipHostMallocDefault) != hipSuccess) {
             c->h_sums[b] = nullptr;
             return fail(c, CKPT_ENOMEM, "pinned sums");
         }
+        ckpt_status st = setup_image_agent(c, b);
+        if (st) return st;
     }
     if (hipHostMalloc((void**)&c->h_bad, c->n_chunks, hipHostMallocDefault) != hipSuccess ||
         hipHostMalloc((void**)&c->h_recomputed, c->n_chunks * 8, hipHostMallocDefault) != hipSuccess)
         return fail(c, CKPT_ENOMEM, "pinned result buffers");
-    const uint64_t n_areas = c->ring ? c->n_slots : c->n_groups;
     c->area_free.resize(n_areas, nullptr);
     for (auto& e : c->area_free) {
         ckpt_status st = make_event(c, &e, false);
@@ -618,8 +829,12 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
         HIPCHK(c, hipEventRecord(e, c->s_copy)); // every area starts free
     }
     c->ev_loaded.resize(c->n_groups, nullptr);
-    for (auto& e : c->ev_loaded) {
-        ckpt_status st = make_event(c, &e, false);
+    c->tk0.resize(c->n_groups, nullptr);
+    c->tk1.resize(c->n_groups, nullptr);
+    for (uint64_t g = 0; g < c->n_groups; ++g) {
+        ckpt_status st = make_event(c, &c->ev_loaded[g], false);
+        if (!st) st = make_event(c, &c->tk0[g], true);
+        if (!st) st = make_event(c, &c->tk1[g], true);
         if (st) return st;
     }
     HIPCHK(c, hipDeviceSynchronize());
@@ -642,10 +857,7 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
     for (auto& kv : c->recs) {
         SnapRec& r = kv.second;
         if (r.aborted) continue;
-        bool com = false;
-        ckpt_status st = query_committed(c, r, &com);
-        if (st) return st;
-        if (!com) ++in_flight;
+        if (!query_committed(r)) ++in_flight;
         if (!newest_live || r.id > newest_live->id) newest_live = &r;
     }
     if (in_flight >= 2) return fail(c, CKPT_EBUSY, "both host images are still being written");
@@ -658,9 +870,12 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
     r.id = id;
     r.step = step;
     r.res = res;
-    r.buf = newest_live ? 1 - newest_live->buf : (c->holder[0] == 0 ? 0 : (c->holder[1] == 0 ? 1 : 0));
-    if (!newest_live) {
-        // No live snapshot: never take an image that holds a committed one.
+    // Target: the image not holding the newest live snapshot; with no live
+    // snapshot, an image that holds nothing committed.
+    if (newest_live) {
+        r.buf = 1 - newest_live->buf;
+    } else {
+        r.buf = 0;
         for (int b = 0; b < 2; ++b) {
             auto it = c->recs.find(c->holder[b]);
             if (c->holder[b] == 0 || it == c->recs.end() || it->second.aborted) {
@@ -674,46 +889,98 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
     c->holder[r.buf] = id;
     const int32_t stop = c->interrupt_next;
     c->interrupt_next = -1;
+    const uint64_t n_copy = (stop < 0) ? c->n_groups : std::min<uint64_t>((uint64_t)stop, c->n_groups);
     hipStream_t after = (hipStream_t)after_stream;
-    uint8_t* himg = c->h_img[r.buf];
-    ChunkReduce red{c->d_acc, c->d_done};
+    // Completion signals start at 0 ("nothing pending"); each is raised to 1
+    // just before its copy is issued.
+    hsa_signal_store_screlease(res->done, 0);
+    r.groups_copied = 0;
+    if (r.timed && n_copy == 0) r.timed = false;
+    if (r.timed) hsa_amd_profiling_async_copy_enable(true);
 
-    HIPCHK(c, hipEventRecord(c->ev_trigger, after));
-    HIPCHK(c, hipStreamWaitEvent(c->s_pack, c->ev_trigger, 0));
-    if (r.timed) HIPCHK(c, hipEventRecord(res->t0, c->s_pack));
-    uint32_t copied = 0;
-    for (uint64_t g = 0; g < c->n_groups; ++g) {
-        const uint64_t lo = group_lo(c, g), hi = group_hi(c, g);
-        hipEvent_t& af = c->area_free[area_of(c, g)];
-        HIPCHK(c, hipStreamWaitEvent(c->s_pack, af, 0));
-        if (r.timed) HIPCHK(c, hipEventRecord(res->k0[g], c->s_pack));
-        hipError_t e = launch_pack(c->d_frags, c->d_tile_first, c->d_tile_last, c->geo, tiles_lo(c, g),
-                                   tiles_hi(c, g), staging_of(c, g), lo, red, res->d_sums, c->grid_cap, c->s_pack);
-        if (e != hipSuccess) return fail(c, CKPT_EHIP, "pack launch failed: %s", hipGetErrorString(e));
-        if (r.timed) HIPCHK(c, hipEventRecord(res->k1[g], c->s_pack));
-        HIPCHK(c, hipEventRecord(res->captured[g], c->s_pack));
-        if (stop < 0 || (int64_t)g < stop) {
-            HIPCHK(c, hipStreamWaitEvent(c->s_copy, res->captured[g], 0));
-            if (r.timed && g == 0) HIPCHK(c, hipEventRecord(res->c0, c->s_copy));
-            HIPCHK(c, hipMemcpyAsync(himg + lo, staging_of(c, g), hi - lo, hipMemcpyDeviceToHost, c->s_copy));
-            if (r.timed && g + 1 == c->n_groups) HIPCHK(c, hipEventRecord(res->c1, c->s_copy));
-            HIPCHK(c, hipEventRecord(af, c->s_copy));
-            ++copied;
-        } else {
-            HIPCHK(c, hipEventRecord(af, c->s_pack)); // nothing will read this area
-        }
-    }
-    r.groups_copied = copied;
-    if (stop >= 0) {
-        r.aborted = true; // interrupted offload: never committed
+    // On an error below, copies not issued never raise their signals, and
+    // the snapshot is marked interrupted.
+    st = issue_snapshot(c, r, after, n_copy, stop);
+    if (st) {
+        r.aborted = true;
         r.timed = false;
-    } else {
-        HIPCHK(c, hipMemcpyAsync(c->h_sums[r.buf], res->d_sums, c->n_chunks * 8, hipMemcpyDeviceToHost, c->s_copy));
-        HIPCHK(c, hipEventRecord(res->commit, c->s_copy));
+        *snap_id = id;
+        return st;
     }
     *snap_id = id;
     return CKPT_OK;
 }
+
+} // extern "C"
+
+namespace {
+
+ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop)
+{
+    RecRes* res = r.res;
+    uint8_t* himg = c->h_img[r.buf];
+    hsa_agent_t host = c->img_agent[r.buf];
+    ckpt_status st = CKPT_OK;
+    HIPCHK(c, hipEventRecord(c->ev_trigger, after));
+    HIPCHK(c, hipStreamWaitEvent(c->s_pack, c->ev_trigger, 0));
+    if (r.timed) HIPCHK(c, hipEventRecord(res->t0, c->s_pack));
+    for (uint64_t g = 0; g < c->n_groups; ++g) {
+        const uint64_t lo = group_lo(c, g), hi = group_hi(c, g);
+        const uint64_t area = area_of(c, g);
+        // The staging area is free once every copy issued out of it so far
+        // has finished (each finished copy bumps area_done by one).
+        if (c->area_seq[area])
+            HIPCHK(c, hipStreamWaitValue64(c->s_pack, c->d_area_done + area, c->area_seq[area],
+                                          hipStreamWaitValueGte, ~0ull));
+        if (r.timed) HIPCHK(c, hipEventRecord(res->k0[g], c->s_pack));
+        hipError_t e = launch_pack(c->d_frags, c->d_tile_first, c->d_tile_last, c->geo, tiles_lo(c, g),
+                                   tiles_hi(c, g), staging_of(c, g), lo, c->d_partials, res->d_sums, c->grid_cap,
+                                   c->s_pack);
+        if (e != hipSuccess) return fail(c, CKPT_EHIP, "pack launch failed: %s", hipGetErrorString(e));
+        if (r.timed) HIPCHK(c, hipEventRecord(res->k1[g], c->s_pack));
+        HIPCHK(c, hipEventRecord(res->captured[g], c->s_pack));
+        if (g >= n_copy) continue; // interrupted offload: this group never leaves the device
+        hsa_signal_store_screlease(res->dep[g], 1);
+        hsa_signal_store_screlease(res->copied[g], 1);
+        hsa_signal_store_screlease(res->flagged[g], 1);
+        r.groups_copied = (uint32_t)(g + 1);
+        e = launch_release(res->dep_val[g], c->s_pack);
+        if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
+        const hsa_amd_sdma_engine_id_t eng = c->d2h_engine[g % c->n_d2h_engines];
+        st = dma(c, himg + lo, host, staging_of(c, g), c->gpu_agent, hi - lo, &res->dep[g], res->copied[g], eng);
+        res->h_seq[g] = c->area_seq[area] + 1;
+        if (!st)
+            st = dma(c, c->d_area_done + area, c->gpu_agent, &res->h_seq[g], host, 8, &res->copied[g],
+                     res->flagged[g], c->h2d_engine);
+        if (st) {
+            // nothing will lower the signals of this group
+            hsa_signal_store_screlease(res->copied[g], 0);
+            hsa_signal_store_screlease(res->flagged[g], 0);
+            return st;
+        }
+        ++c->area_seq[area];
+    }
+    if (stop >= 0) {
+        r.aborted = true; // interrupted offload: never committed
+        r.timed = false;
+    } else {
+        hsa_signal_store_screlease(res->dep_sums, 1);
+        hipError_t e = launch_release(res->dep_sums_val, c->s_pack);
+        if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
+        hsa_signal_store_screlease(res->done, 1);
+        st = dma(c, c->h_sums[r.buf], host, res->d_sums, c->gpu_agent, c->n_chunks * 8, &res->dep_sums, res->done,
+                 c->d2h_engine[0]);
+        if (st) {
+            hsa_signal_store_screlease(res->done, 0);
+            return st;
+        }
+    }
+    return CKPT_OK;
+}
+
+} // namespace
+
+extern "C" {
 
 ckpt_status ckpt_wait(ckpt_ctx* c, uint64_t snap_id, uint32_t mode, void* stream, uint32_t frag_lo,
                       uint32_t frag_hi)
@@ -725,7 +992,8 @@ ckpt_status ckpt_wait(ckpt_ctx* c, uint64_t snap_id, uint32_t mode, void* stream
     HIPCHK(c, hipSetDevice(c->device));
     if (mode == CKPT_WAIT_COMMITTED) {
         if (r.aborted) return fail(c, CKPT_ESTATE, "snapshot %llu was interrupted", (unsigned long long)snap_id);
-        HIPCHK(c, hipEventSynchronize(r.res->commit));
+        ckpt_status st = wait_copies(c, r);
+        if (st) return st;
         r.committed = true;
         return CKPT_OK;
     }
@@ -756,14 +1024,8 @@ ckpt_status ckpt_snapshot_state(ckpt_ctx* c, uint64_t snap_id, uint32_t* state)
     auto it = c->recs.find(snap_id);
     if (it == c->recs.end()) return fail(c, CKPT_ERANGE, "snapshot %llu not retained", (unsigned long long)snap_id);
     SnapRec& r = it->second;
-    if (r.aborted) {
-        *state = CKPT_SNAP_ABORTED;
-        return CKPT_OK;
-    }
-    bool com = false;
-    ckpt_status st = query_committed(c, r, &com);
-    if (st) return st;
-    if (!com) *state = CKPT_SNAP_IN_FLIGHT;
+    if (r.aborted) *state = CKPT_SNAP_ABORTED;
+    else if (!query_committed(r)) *state = CKPT_SNAP_IN_FLIGHT;
     else *state = (c->holder[r.buf] == r.id) ? CKPT_SNAP_COMMITTED : CKPT_SNAP_SUPERSEDED;
     return CKPT_OK;
 }
@@ -799,27 +1061,24 @@ ckpt_status ckpt_chunk_fragments(ckpt_ctx* c, uint64_t k, uint64_t* byte_lo, uin
     if (!c->registered) return fail(c, CKPT_ESTATE, "no tensors registered");
     if (k >= c->n_chunks) return fail(c, CKPT_EINVAL, "chunk %llu out of range", (unsigned long long)k);
     const uint64_t lo = k * c->C, hi = std::min(lo + c->C, c->I);
-    // First fragment whose padded span reaches past lo; last whose offset is below hi.
     const uint32_t n = (uint32_t)c->frags.size();
-    uint32_t a = 0, b = n - 1;
-    {
-        uint32_t l = 0, h = n; // first i with end(i) > lo
-        while (l < h) {
-            uint32_t m = (l + h) / 2;
-            uint64_t end = (m + 1 < n) ? c->frags[m + 1].off : c->I;
-            if (end > lo) h = m;
-            else l = m + 1;
-        }
-        a = l;
-        l = 0;
-        h = n; // first i with off(i) >= hi
-        while (l < h) {
-            uint32_t m = (l + h) / 2;
-            if (c->frags[m].off >= hi) h = m;
-            else l = m + 1;
-        }
-        b = l ? l - 1 : 0;
+    // First fragment whose padded span ends past lo; last whose offset is below hi.
+    uint32_t l = 0, h = n;
+    while (l < h) {
+        const uint32_t m = (l + h) / 2;
+        const uint64_t end = (m + 1 < n) ? c->frags[m + 1].off : c->I;
+        if (end > lo) h = m;
+        else l = m + 1;
     }
+    const uint32_t a = l;
+    l = 0;
+    h = n;
+    while (l < h) {
+        const uint32_t m = (l + h) / 2;
+        if (c->frags[m].off >= hi) h = m;
+        else l = m + 1;
+    }
+    const uint32_t b = l ? l - 1 : 0;
     if (byte_lo) *byte_lo = lo;
     if (byte_hi) *byte_hi = hi;
     if (frag_first) *frag_first = a;
@@ -833,10 +1092,8 @@ ckpt_status ckpt_host_image(ckpt_ctx* c, uint64_t snap_id, void** image, uint64_
     auto it = c->recs.find(snap_id);
     if (it == c->recs.end()) return fail(c, CKPT_ERANGE, "snapshot %llu not retained", (unsigned long long)snap_id);
     SnapRec& r = it->second;
-    bool com = false;
-    ckpt_status st = query_committed(c, r, &com);
-    if (st) return st;
-    if (!com || c->holder[r.buf] != r.id) return fail(c, CKPT_ENOSNAP, "snapshot not committed or superseded");
+    if (!query_committed(r) || c->holder[r.buf] != r.id)
+        return fail(c, CKPT_ENOSNAP, "snapshot not committed or superseded");
     if (image) *image = c->h_img[r.buf];
     if (image_bytes) *image_bytes = c->I;
     if (sums) *sums = c->h_sums[r.buf];
@@ -858,10 +1115,8 @@ ckpt_status ckpt_envelope(ckpt_ctx* c, uint64_t snap_id, void* out, uint64_t cap
     auto it = c->recs.find(snap_id);
     if (it == c->recs.end()) return fail(c, CKPT_ERANGE, "snapshot %llu not retained", (unsigned long long)snap_id);
     SnapRec& r = it->second;
-    bool com = false;
-    ckpt_status st = query_committed(c, r, &com);
-    if (st) return st;
-    if (!com || c->holder[r.buf] != r.id) return fail(c, CKPT_ENOSNAP, "snapshot not committed or superseded");
+    if (!query_committed(r) || c->holder[r.buf] != r.id)
+        return fail(c, CKPT_ENOSNAP, "snapshot not committed or superseded");
     const uint32_t nf = (uint32_t)c->frags.size();
     const uint64_t meta_pad = round_up(r.meta.size(), 8);
     const uint64_t total = 56 + 24ull * nf + 8 * c->n_chunks + meta_pad + 8;
@@ -929,19 +1184,31 @@ ckpt_status ckpt_last_timing(ckpt_ctx* c, uint32_t which, ckpt_timing* out)
 {
     if (!c || !out || which > CKPT_OP_VERIFY) return fail(c, CKPT_EINVAL, "bad timing query");
     if (which == CKPT_OP_SNAPSHOT) {
-        // newest timed, committed snapshot
-        SnapRec* best = nullptr;
+        SnapRec* best = nullptr; // newest timed, committed snapshot
         for (auto& kv : c->recs)
             if (kv.second.timed && !kv.second.aborted && (!best || kv.first > best->id)) best = &kv.second;
         if (!best) return fail(c, CKPT_ESTATE, "no timed snapshot retained");
-        HIPCHK(c, hipEventSynchronize(best->res->commit));
+        ckpt_status st = wait_copies(c, *best);
+        if (st) return st;
         RecRes* r = best->res;
         ckpt_timing t{};
         for (uint64_t g = 0; g < c->n_groups; ++g) t.kernel_ms += elapsed(r->k0[g], r->k1[g]);
         t.kernels = (uint32_t)c->n_groups;
         t.copies = (uint32_t)c->n_groups;
-        t.copy_ms = elapsed(r->c0, r->c1);
-        t.total_ms = elapsed(r->t0, r->c1);
+        // DMA span: first image copy start to last image copy end (engine timestamps).
+        uint64_t t_start = UINT64_MAX, t_end = 0;
+        bool ok = true;
+        for (uint64_t g = 0; g < c->n_groups; ++g) {
+            hsa_amd_profiling_async_copy_time_t ct;
+            if (hsa_amd_profiling_get_async_copy_time(r->copied[g], &ct) != HSA_STATUS_SUCCESS) {
+                ok = false;
+                break;
+            }
+            t_start = std::min<uint64_t>(t_start, ct.start);
+            t_end = std::max<uint64_t>(t_end, ct.end);
+        }
+        t.copy_ms = (ok && t_end > t_start) ? (float)((double)(t_end - t_start) * 1e3 / (double)c->ts_freq) : -1.f;
+        t.total_ms = -1.f;
         t.kernel_bytes = 2 * c->payload;
         t.copy_bytes = c->I;
         *out = t;
