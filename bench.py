@@ -46,8 +46,104 @@ def parse():
     ap.add_argument("--overlap-workload", type=int, default=3)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-sample-bytes", type=int, default=10 << 30)
-    ap.add_argument("--traffic", type=str, default="", help="JSON file with rocprofv3 FETCH/WRITE figures")
+    ap.add_argument("--traffic", type=str, default=os.path.join(ROOT, "profiles", "pack_checksum_gpt1.3b_traffic.txt"),
+                    help="rocprofv3 FETCH_SIZE/WRITE_SIZE summary written by --pmc-summary")
+    ap.add_argument("--pmc-run", action="store_true",
+                    help="short run for counter collection: a 1 GiB plain copy, then two snapshots")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarize two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of --pmc-run")
+    ap.add_argument("--stats-summary", metavar="DIR", help="summarize a rocprofv3 --kernel-trace --stats run")
+    ap.add_argument("--command", default="", help="command line recorded in a summary")
     return ap.parse_args()
+
+
+PACK_KERNEL = "tile_kernel<0"  # PACK instantiation of the tile kernel
+COPY_KERNEL = "__amd_rocclr_copyBuffer"
+CALIBRATION_BYTES = 1 << 30
+
+
+def kernel_source_sha():
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in ["ckpt_kernels.hip", "ckpt_internal.h"]:
+        h.update(open(os.path.join(ROOT, "paper_2607_01646_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def read_counter_csv(d):
+    import csv
+    import glob
+
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit("no counter_collection.csv under %s" % d)
+    rows = []
+    for f in files:
+        rows += list(csv.DictReader(open(f)))
+    return rows
+
+
+def pmc_summary(fetch_dir, write_dir, command):
+    """Per-dispatch FETCH_SIZE / WRITE_SIZE of the pack kernel, scaled by the
+    same counters on a plain copy kernel of known size (1 GiB read, 1 GiB
+    written), into HBM bytes per launch."""
+    out = {"kernel_source_sha": kernel_source_sha(), "command": command}
+    for name, d in [("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)]:
+        rows = [r for r in read_counter_csv(d) if r["Counter_Name"] == name]
+        copy = [float(r["Counter_Value"]) for r in rows if COPY_KERNEL in r["Kernel_Name"]
+                and int(r["Grid_Size"]) > 1024]
+        pack = [float(r["Counter_Value"]) for r in rows if PACK_KERNEL in r["Kernel_Name"]]
+        if not copy or not pack:
+            raise SystemExit("%s: missing dispatches (copy %d, pack %d)" % (name, len(copy), len(pack)))
+        copy_kib = max(copy)  # the 1 GiB calibration copy
+        factor = CALIBRATION_BYTES / (copy_kib * 1024.0)
+        key = name.split("_")[0].lower()
+        out[key + "_kib_per_pack_dispatch"] = sum(pack) / len(pack)
+        out[key + "_pack_dispatches"] = len(pack)
+        out[key + "_kib_calibration_copy"] = copy_kib
+        out[key + "_scale"] = factor
+        out[key + "_bytes_per_pack_dispatch"] = sum(pack) / len(pack) * 1024.0 * factor
+    out["traffic_bytes_per_pack_dispatch"] = out["fetch_bytes_per_pack_dispatch"] + out["write_bytes_per_pack_dispatch"]
+    return out
+
+
+def write_summary(path, d, header):
+    with open(path, "w") as f:
+        f.write(header.rstrip() + "\n\n")
+        for k, v in d.items():
+            f.write("%s: %s\n" % (k, v))
+
+
+def read_summary(path):
+    d = {}
+    if not os.path.exists(path):
+        return d
+    for line in open(path):
+        if ": " in line and not line.startswith("#"):
+            k, v = line.rstrip("\n").split(": ", 1)
+            d[k.strip()] = v.strip()
+    return d
+
+
+def stats_summary(d, command):
+    """Markdown table of our kernels and copies from a --kernel-trace --stats run."""
+    import csv
+    import glob
+
+    ks = glob.glob(os.path.join(d, "**", "*kernel_stats.csv"), recursive=True)
+    ms = glob.glob(os.path.join(d, "**", "*memory_copy_stats.csv"), recursive=True)
+    lines = ["| name | calls | average (us) | min (us) | max (us) | total (ms) |", "|---|---|---|---|---|---|"]
+    for f in ks + ms:
+        for r in csv.DictReader(open(f)):
+            n = r["Name"]
+            if "ckpt::" in n or "MEMORY_COPY" in n or COPY_KERNEL in n:
+                short = n.replace("void ckpt::(anonymous namespace)::", "").replace("(ckpt::(anonymous namespace)::Args)", "")
+                short = short.replace("ckpt::(anonymous namespace)::", "").split("(")[0]
+                lines.append("| %s | %s | %.1f | %.1f | %.1f | %.2f |" % (
+                    short, r["Calls"], float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3,
+                    float(r["TotalDurationNs"]) / 1e6))
+    return "\n".join(lines)
 
 
 def log(*a):
@@ -203,8 +299,40 @@ def overlap_leg(torch, P, W, wid, steps):
             "statistic": "mean after dropping 10 warm-up steps and the slowest 5%"}
 
 
+def pmc_run(torch, P, W):
+    """Short run whose dispatches the counter summary reads: a 1 GiB plain
+    device copy (calibration), then two snapshots of the 1.3B GPT shard."""
+    a = torch.empty(CALIBRATION_BYTES, dtype=torch.uint8, device="cuda")
+    b = torch.empty(CALIBRATION_BYTES, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    del a, b
+    tensors, plan = W.make_state(2, device="cuda")
+    ck = P.Checkpointer(tensors, chunk_bytes=W.WORKLOADS[2]["chunk"])
+    for k in range(2):
+        s = ck.snapshot(step=k)
+        ck.wait_committed(s)
+    ck.close()
+    print("pmc run done", flush=True)
+
+
 def main():
     args = parse()
+    if args.pmc_summary:
+        d = pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.command)
+        header = ("# HBM traffic of the pack kernel (tile_kernel<PACK>) on the 24-layer hidden-2048 GPT shard\n"
+                  "# (18,421,473,280 payload bytes, 1 GiB launches), from two rocprofv3 --pmc runs of\n"
+                  "# `python bench.py --pmc-run`: FETCH_SIZE, then WRITE_SIZE (KiB per dispatch), each scaled by\n"
+                  "# the same counter on a plain 1 GiB device copy (__amd_rocclr_copyBuffer).")
+        out = args.traffic
+        write_summary(out, d, header)
+        print(open(out).read())
+        return
+    if args.stats_summary:
+        print("# rocprofv3 --kernel-trace --memory-copy-trace --stats\n\ncommand: `%s`\n" % args.command)
+        print(stats_summary(args.stats_summary, args.command))
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU: the snapshot path has no cross-GPU step in this build "
               "(--gpus %d requested)" % args.gpus, file=sys.stderr)
@@ -216,6 +344,9 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     P.lib()  # fails loudly when libckpt.so is missing
+    if args.pmc_run:
+        pmc_run(torch, P, W)
+        return
     wid = args.workload
     wl = W.WORKLOADS[wid]
     log("link peak")
@@ -270,9 +401,12 @@ def main():
     h2d_gbps = sn["copy_bytes"] * args.steps / agg("restore", "copy_ms") / 1e6
     verify_gbps = sn["copy_bytes"] * args.steps / agg("verify", "total_ms") / 1e6
     verify_kernel_gbps = sn["copy_bytes"] * args.steps / agg("verify", "kernel_ms") / 1e6
+    # HBM bytes per pack launch from the committed counter summary, unless
+    # the kernel source changed since the counters were taken.
     traffic = None
-    if args.traffic and os.path.exists(args.traffic):
-        traffic = json.load(open(args.traffic)).get("pack_bytes_per_launch")
+    summ = read_summary(args.traffic)
+    if summ.get("kernel_source_sha") == kernel_source_sha() and "traffic_bytes_per_pack_dispatch" in summ:
+        traffic = round(float(summ["traffic_bytes_per_pack_dispatch"]))
     roofline = {"kernel": "pack_checksum (tile_kernel<PACK>)", "bound": "hbm", "achieved": round(pack_gbps, 1),
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(pack_gbps / HBM_PEAK_GBPS, 4),
                 "traffic": traffic, "launches": launches, "avg_launch_ms": round(pack_ms / launches, 4),

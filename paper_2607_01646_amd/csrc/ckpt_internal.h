@@ -25,27 +25,27 @@ struct Geometry {
     uint32_t tiles_per_chunk; // chunk_bytes >> tile_shift
 };
 
-// Pack fragments into an image window and sum its chunks.
-// Tiles [t_lo, t_hi) (whole chunks) are processed; image byte x is written to
-// dst + (x - dst_origin); partials[t] receives tile t's sum and sums_out[c]
-// the word-sum of chunk c.  Two kernel launches on stream s.
+// The tile kernels.  Each covers tiles [t_lo, t_hi) and writes tile t's
+// word-sum to partials[t]; launches cover whole chunks.  grid_cap bounds the
+// workgroups (one per tile when the cap is larger).
+//   pack:     fragment bytes -> image window; image byte x goes to dst + (x - dst_origin)
+//   scatter:  image window -> fragment bytes (image byte x read at src + (x - src_origin))
+//   checksum: image window only
 hipError_t launch_pack(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
                        const Geometry& g, uint64_t t_lo, uint64_t t_hi, uint8_t* dst, uint64_t dst_origin,
-                       unsigned long long* partials, unsigned long long* sums_out, uint32_t grid_cap, hipStream_t s);
+                       unsigned long long* partials, uint32_t grid_cap, hipStream_t s);
+hipError_t launch_scatter(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
+                          const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src, uint64_t src_origin,
+                          unsigned long long* partials, uint32_t grid_cap, hipStream_t s);
+hipError_t launch_checksum(const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src, uint64_t src_origin,
+                           unsigned long long* partials, uint32_t grid_cap, hipStream_t s);
 
-// Scatter an image window back into the fragments, recompute chunk sums and
-// compare them with expected[]: recomputed[c] and bad[c] (1 = mismatch).
-hipError_t launch_scatter_verify(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
-                                 const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src,
-                                 uint64_t src_origin, unsigned long long* partials,
-                                 const unsigned long long* expected, unsigned long long* recomputed, uint8_t* bad,
-                                 uint32_t grid_cap, hipStream_t s);
-
-// Recompute chunk sums of an image window only (no fragments touched).
-hipError_t launch_checksum_verify(const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src,
-                                  uint64_t src_origin, unsigned long long* partials,
-                                  const unsigned long long* expected, unsigned long long* recomputed, uint8_t* bad,
-                                  uint32_t grid_cap, hipStream_t s);
+// Chunk sums of the chunks covered by tiles [t_lo, t_hi): sums_out[c] is the
+// sum of the chunk's tile sums.  With expected non-null, bad[c] is set to 1
+// where sums_out[c] != expected[c] (and to 0 elsewhere).
+hipError_t launch_chunk_reduce(const Geometry& g, uint64_t t_lo, uint64_t t_hi, const unsigned long long* partials,
+                               unsigned long long* sums_out, const unsigned long long* expected, uint8_t* bad,
+                               hipStream_t s);
 
 // Store 0 into *signal_value (an HSA signal's value) once the work enqueued
 // on s before this call has completed.

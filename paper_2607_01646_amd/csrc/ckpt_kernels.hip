@@ -11,9 +11,10 @@
 // floating-point instruction touches them, so NaN payloads, -0 and
 // subnormals pass unchanged.
 //
-// Work split.  The image is cut into power-of-two tiles that never cross a
-// chunk.  A workgroup of 256 lanes (4 wave64) takes tiles grid-stride; each
-// lane moves 16-byte vectors.  A tile inside one 16-byte-aligned fragment
+// Work split.  The image is cut into power-of-two tiles (16 KiB) that never
+// cross a chunk.  A workgroup of 256 lanes (4 wave64) takes one tile (or
+// tiles grid-stride when the grid is capped); each lane moves 16-byte
+// vectors, four in flight.  A tile inside one 16-byte-aligned fragment
 // takes an unrolled non-temporal stream; otherwise each vector finds its
 // fragment (binary search over the tile's fragment offsets in LDS), loads
 // aligned 16-byte blocks and funnel-shifts them when the fragment is
@@ -33,9 +34,8 @@ namespace {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kBlock = 256;
-constexpr int kWaves = kBlock / 64;
-constexpr int kLdsFrags = 1024; // fragment offsets cached per tile
+constexpr int kBlock = 256;      // lanes per workgroup (4 wave64)
+constexpr int kLdsFrags = 512;  // fragment offsets cached per tile (a 16 KiB tile holds at most 65 non-empty ones)
 constexpr int kUnroll = 4;      // 16-byte vectors in flight per lane on the streaming path
 
 enum Mode { PACK = 0, SCATTER = 1, VERIFY = 2 };
@@ -151,42 +151,58 @@ __device__ void store_general(uint64_t ptr, uint64_t nbytes, uint64_t p, u32x4 v
     }
 }
 
+template <bool NT>
+__device__ __forceinline__ u32x4 ld(const u32x4* p)
+{
+    if (NT) return __builtin_nontemporal_load(p);
+    return *p;
+}
+
+template <bool NT>
+__device__ __forceinline__ void st(u32x4 v, u32x4* p)
+{
+    if (NT) __builtin_nontemporal_store(v, p);
+    else *p = v;
+}
+
 // Streaming copy of nvec aligned 16-byte vectors with their sum.
+template <int BLOCK, int UNROLL, bool NTL, bool NTS>
 __device__ __forceinline__ unsigned long long stream_copy(const u32x4* __restrict__ s, u32x4* __restrict__ d,
                                                           uint32_t nvec, uint32_t tid)
 {
     unsigned long long acc = 0;
     uint32_t v = tid;
-    for (; v + (kUnroll - 1) * kBlock < nvec; v += kUnroll * kBlock) {
-        u32x4 r[kUnroll];
+    for (; v + (UNROLL - 1) * BLOCK < nvec; v += UNROLL * BLOCK) {
+        u32x4 r[UNROLL];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) r[u] = __builtin_nontemporal_load(s + v + u * kBlock);
+        for (int u = 0; u < UNROLL; ++u) r[u] = ld<NTL>(s + v + u * BLOCK);
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            __builtin_nontemporal_store(r[u], d + v + u * kBlock);
+        for (int u = 0; u < UNROLL; ++u) {
+            st<NTS>(r[u], d + v + u * BLOCK);
             acc += vsum(r[u]);
         }
     }
-    for (; v < nvec; v += kBlock) {
-        const u32x4 r = __builtin_nontemporal_load(s + v);
-        __builtin_nontemporal_store(r, d + v);
+    for (; v < nvec; v += BLOCK) {
+        const u32x4 r = ld<NTL>(s + v);
+        st<NTS>(r, d + v);
         acc += vsum(r);
     }
     return acc;
 }
 
+template <int BLOCK, int UNROLL, bool NTL>
 __device__ __forceinline__ unsigned long long stream_sum(const u32x4* __restrict__ s, uint32_t nvec, uint32_t tid)
 {
     unsigned long long acc = 0;
     uint32_t v = tid;
-    for (; v + (kUnroll - 1) * kBlock < nvec; v += kUnroll * kBlock) {
-        u32x4 r[kUnroll];
+    for (; v + (UNROLL - 1) * BLOCK < nvec; v += UNROLL * BLOCK) {
+        u32x4 r[UNROLL];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) r[u] = __builtin_nontemporal_load(s + v + u * kBlock);
+        for (int u = 0; u < UNROLL; ++u) r[u] = ld<NTL>(s + v + u * BLOCK);
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) acc += vsum(r[u]);
+        for (int u = 0; u < UNROLL; ++u) acc += vsum(r[u]);
     }
-    for (; v < nvec; v += kBlock) acc += vsum(__builtin_nontemporal_load(s + v));
+    for (; v < nvec; v += BLOCK) acc += vsum(ld<NTL>(s + v));
     return acc;
 }
 
@@ -198,6 +214,7 @@ __device__ __forceinline__ unsigned long long shfl_xor64(unsigned long long v, i
 }
 
 // Sum over the workgroup; the result is valid in thread 0.
+template <int BLOCK>
 __device__ __forceinline__ unsigned long long block_sum(unsigned long long v, unsigned long long* s_red)
 {
 #pragma unroll
@@ -208,7 +225,7 @@ __device__ __forceinline__ unsigned long long block_sum(unsigned long long v, un
     unsigned long long r = 0;
     if (threadIdx.x == 0) {
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) r += s_red[w];
+        for (int w = 0; w < BLOCK / 64; ++w) r += s_red[w];
     }
     __syncthreads();
     return r;
@@ -239,10 +256,10 @@ __device__ __forceinline__ uint32_t find_frag_global(const FragDev* frags, uint3
     return lo;
 }
 
-template <int MODE>
-__global__ __launch_bounds__(kBlock) void tile_kernel(Args a)
+template <int MODE, int BLOCK = kBlock, int UNROLL = kUnroll, bool NTL = true, bool NTS = true>
+__global__ __launch_bounds__(BLOCK) void tile_kernel(Args a)
 {
-    __shared__ unsigned long long s_red[kWaves];
+    __shared__ unsigned long long s_red[BLOCK / 64];
     __shared__ uint64_t s_off[kLdsFrags];
     const uint32_t tid = threadIdx.x;
     for (uint64_t t = a.t_lo + blockIdx.x; t < a.t_hi; t += gridDim.x) {
@@ -253,7 +270,7 @@ __global__ __launch_bounds__(kBlock) void tile_kernel(Args a)
         uint8_t* win = a.img + (base - a.origin);
         unsigned long long acc = 0;
         if (MODE == VERIFY) {
-            acc = stream_sum(reinterpret_cast<const u32x4*>(win), nvec, tid);
+            acc = stream_sum<BLOCK, UNROLL, NTL>(reinterpret_cast<const u32x4*>(win), nvec, tid);
         } else {
             const uint32_t f0 = a.tile_first[t], f1 = a.tile_last[t];
             if (f0 == f1) {
@@ -261,10 +278,12 @@ __global__ __launch_bounds__(kBlock) void tile_kernel(Args a)
                 const uint64_t p0 = base - F.off;
                 if ((F.ptr & 15) == 0 && p0 + (end - base) <= F.nbytes) {
                     u32x4* fr = reinterpret_cast<u32x4*>(F.ptr + p0);
-                    if (MODE == PACK) acc = stream_copy(fr, reinterpret_cast<u32x4*>(win), nvec, tid);
-                    else acc = stream_copy(reinterpret_cast<const u32x4*>(win), fr, nvec, tid);
+                    if (MODE == PACK)
+                        acc = stream_copy<BLOCK, UNROLL, NTL, NTS>(fr, reinterpret_cast<u32x4*>(win), nvec, tid);
+                    else
+                        acc = stream_copy<BLOCK, UNROLL, NTL, NTS>(reinterpret_cast<const u32x4*>(win), fr, nvec, tid);
                 } else {
-                    for (uint32_t v = tid; v < nvec; v += kBlock) {
+                    for (uint32_t v = tid; v < nvec; v += BLOCK) {
                         const uint64_t p = p0 + 16ull * v;
                         u32x4* w = reinterpret_cast<u32x4*>(win) + v;
                         if (MODE == PACK) {
@@ -282,10 +301,10 @@ __global__ __launch_bounds__(kBlock) void tile_kernel(Args a)
                 const uint32_t nf = f1 - f0 + 1;
                 const bool in_lds = nf <= (uint32_t)kLdsFrags;
                 if (in_lds) {
-                    for (uint32_t k = tid; k < nf; k += kBlock) s_off[k] = a.frags[f0 + k].off;
+                    for (uint32_t k = tid; k < nf; k += BLOCK) s_off[k] = a.frags[f0 + k].off;
                 }
                 __syncthreads();
-                for (uint32_t v = tid; v < nvec; v += kBlock) {
+                for (uint32_t v = tid; v < nvec; v += BLOCK) {
                     const uint64_t x = base + 16ull * v;
                     const uint32_t i = in_lds ? f0 + find_frag_lds(s_off, nf, x) : find_frag_global(a.frags, f0, f1, x);
                     const FragDev F = a.frags[i];
@@ -305,7 +324,7 @@ __global__ __launch_bounds__(kBlock) void tile_kernel(Args a)
         }
         // block_sum's barriers also retire every lane's use of s_off before
         // the next tile refills it.
-        const unsigned long long tile_sum = block_sum(acc, s_red);
+        const unsigned long long tile_sum = block_sum<BLOCK>(acc, s_red);
         if (tid == 0) a.partials[t] = tile_sum;
     }
 }
@@ -314,14 +333,14 @@ __global__ __launch_bounds__(kBlock) void tile_kernel(Args a)
 // also flag a mismatch.
 __global__ __launch_bounds__(kBlock) void chunk_reduce_kernel(ReduceArgs r)
 {
-    __shared__ unsigned long long s_red[kWaves];
+    __shared__ unsigned long long s_red[kBlock / 64];
     const uint64_t c = r.c_lo + blockIdx.x;
     const uint64_t t0 = c * r.tiles_per_chunk;
     uint64_t t1 = t0 + r.tiles_per_chunk;
     if (t1 > r.n_tiles) t1 = r.n_tiles;
     unsigned long long acc = 0;
     for (uint64_t t = t0 + threadIdx.x; t < t1; t += kBlock) acc += r.partials[t];
-    const unsigned long long s = block_sum(acc, s_red);
+    const unsigned long long s = block_sum<kBlock>(acc, s_red);
     if (threadIdx.x == 0) {
         r.sums_out[c] = s;
         if (r.expected) r.bad[c] = (s != r.expected[c]) ? 1 : 0;
@@ -329,26 +348,12 @@ __global__ __launch_bounds__(kBlock) void chunk_reduce_kernel(ReduceArgs r)
 }
 
 template <int MODE>
-hipError_t launch(const Args& a, const Geometry& g, unsigned long long* sums_out, const unsigned long long* expected,
-                  uint8_t* bad, uint32_t grid_cap, hipStream_t s)
+hipError_t launch_tiles(const Args& a, uint32_t grid_cap, hipStream_t s)
 {
     if (a.t_hi <= a.t_lo) return hipSuccess;
     const uint64_t n = a.t_hi - a.t_lo;
     const uint32_t grid = (uint32_t)(n < grid_cap ? n : grid_cap);
     hipLaunchKernelGGL(tile_kernel<MODE>, dim3(grid), dim3(kBlock), 0, s, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    // Launches cover whole chunks, so the tiles of [c_lo, c_hi) are all here.
-    ReduceArgs r;
-    r.partials = a.partials;
-    r.c_lo = a.t_lo / g.tiles_per_chunk;
-    r.c_hi = (a.t_hi + g.tiles_per_chunk - 1) / g.tiles_per_chunk;
-    r.n_tiles = g.n_tiles;
-    r.tiles_per_chunk = g.tiles_per_chunk;
-    r.sums_out = sums_out;
-    r.expected = expected;
-    r.bad = bad;
-    hipLaunchKernelGGL(chunk_reduce_kernel, dim3((uint32_t)(r.c_hi - r.c_lo)), dim3(kBlock), 0, s, r);
     return hipGetLastError();
 }
 
@@ -372,29 +377,43 @@ hipError_t launch_release(int64_t* signal_value, hipStream_t s)
 
 hipError_t launch_pack(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
                        const Geometry& g, uint64_t t_lo, uint64_t t_hi, uint8_t* dst, uint64_t dst_origin,
-                       unsigned long long* partials, unsigned long long* sums_out, uint32_t grid_cap, hipStream_t s)
+                       unsigned long long* partials, uint32_t grid_cap, hipStream_t s)
 {
     Args a{frags, tile_first, tile_last, g, t_lo, t_hi, dst, dst_origin, partials};
-    return launch<PACK>(a, g, sums_out, nullptr, nullptr, grid_cap, s);
+    return launch_tiles<PACK>(a, grid_cap, s);
 }
 
-hipError_t launch_scatter_verify(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
-                                 const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src,
-                                 uint64_t src_origin, unsigned long long* partials,
-                                 const unsigned long long* expected, unsigned long long* recomputed, uint8_t* bad,
-                                 uint32_t grid_cap, hipStream_t s)
+hipError_t launch_scatter(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
+                          const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src, uint64_t src_origin,
+                          unsigned long long* partials, uint32_t grid_cap, hipStream_t s)
 {
     Args a{frags, tile_first, tile_last, g, t_lo, t_hi, const_cast<uint8_t*>(src), src_origin, partials};
-    return launch<SCATTER>(a, g, recomputed, expected, bad, grid_cap, s);
+    return launch_tiles<SCATTER>(a, grid_cap, s);
 }
 
-hipError_t launch_checksum_verify(const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src,
-                                  uint64_t src_origin, unsigned long long* partials,
-                                  const unsigned long long* expected, unsigned long long* recomputed, uint8_t* bad,
-                                  uint32_t grid_cap, hipStream_t s)
+hipError_t launch_checksum(const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src, uint64_t src_origin,
+                           unsigned long long* partials, uint32_t grid_cap, hipStream_t s)
 {
     Args a{nullptr, nullptr, nullptr, g, t_lo, t_hi, const_cast<uint8_t*>(src), src_origin, partials};
-    return launch<VERIFY>(a, g, recomputed, expected, bad, grid_cap, s);
+    return launch_tiles<VERIFY>(a, grid_cap, s);
+}
+
+hipError_t launch_chunk_reduce(const Geometry& g, uint64_t t_lo, uint64_t t_hi, const unsigned long long* partials,
+                               unsigned long long* sums_out, const unsigned long long* expected, uint8_t* bad,
+                               hipStream_t s)
+{
+    if (t_hi <= t_lo) return hipSuccess;
+    ReduceArgs r;
+    r.partials = partials;
+    r.c_lo = t_lo / g.tiles_per_chunk;
+    r.c_hi = (t_hi + g.tiles_per_chunk - 1) / g.tiles_per_chunk;
+    r.n_tiles = g.n_tiles;
+    r.tiles_per_chunk = g.tiles_per_chunk;
+    r.sums_out = sums_out;
+    r.expected = expected;
+    r.bad = bad;
+    hipLaunchKernelGGL(chunk_reduce_kernel, dim3((uint32_t)(r.c_hi - r.c_lo)), dim3(kBlock), 0, s, r);
+    return hipGetLastError();
 }
 
 } // namespace ckpt

@@ -22,11 +22,11 @@ if torch.cuda.is_available():
 
 
 def snapshot_and_check(tensors, host, chunk, align=256, staging=0, group=0, dtypes=None, classes=None,
-                       meta=b"", step=3):
+                       meta=b"", step=3, grid=0):
     """Snapshot, compare image and sums with the oracle, trash the tensors,
     restore and compare them; returns the Checkpointer and snapshot id."""
     ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=chunk, align_bytes=align,
-                        device_staging_bytes=staging, group_bytes=group)
+                        device_staging_bytes=staging, group_bytes=group, grid_blocks=grid)
     snap = ck.snapshot(step=step, meta=meta)
     ck.wait_committed(snap)
     assert ck.state(snap) == P.CKPT_SNAP_COMMITTED
@@ -67,6 +67,15 @@ def test_edge_sizes_all_geometries(chunk, align, staging, group):
     ck.close()
 
 
+def test_capped_grid_walks_tiles_grid_stride():
+    """With the workgroup count capped, each workgroup loops over many tiles
+    (pack, scatter and verify)."""
+    tensors, host = random_byte_fragments(EDGE_SIZES, seed=5)
+    for grid in [1, 7, 64]:
+        ck, _ = snapshot_and_check(tensors, host, 1 << 16, grid=grid)
+        ck.close()
+
+
 def test_single_fragment_and_ragged_tail():
     for n in [1, 16, 17, 4 << 20, (4 << 20) + 3]:
         tensors, host = random_byte_fragments([n], seed=n)
@@ -75,7 +84,7 @@ def test_single_fragment_and_ragged_tail():
 
 
 def test_many_small_fragments_in_one_tile():
-    # 600 fragments of 1..40 bytes: several hundred fragments per 64 KiB tile
+    # 600 fragments of 1..40 bytes: 64 fragments per 16 KiB tile
     rng = np.random.default_rng(21)
     sizes = [int(s) for s in rng.integers(1, 41, 600)]
     tensors, host = random_byte_fragments(sizes, seed=22)
