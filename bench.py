@@ -54,6 +54,7 @@ def parse():
                     help="summarize two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of --pmc-run")
     ap.add_argument("--stats-summary", metavar="DIR", help="summarize a rocprofv3 --kernel-trace --stats run")
     ap.add_argument("--command", default="", help="command line recorded in a summary")
+    ap.add_argument("--bench-json", default="", help="with --stats-summary: the JSON line bench.py printed in that run")
     return ap.parse_args()
 
 
@@ -124,6 +125,24 @@ def read_summary(path):
             k, v = line.rstrip("\n").split(": ", 1)
             d[k.strip()] = v.strip()
     return d
+
+
+def timed_pack_average(d, bench):
+    """Average duration (ms) of the pack dispatches of the bench's timed steps,
+    from the kernel trace: workload 2 runs first, (warmup + steps) passes of
+    `launches / steps` dispatches each."""
+    import csv
+    import glob
+
+    files = glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True)
+    rows = []
+    for f in files:
+        rows += [r for r in csv.DictReader(open(f)) if PACK_KERNEL in r["Kernel_Name"]]
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    per = bench["roofline"]["launches"] // bench["steps"]
+    timed = rows[bench["warmup"] * per:(bench["warmup"] + bench["steps"]) * per]
+    durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e6 for r in timed]
+    return sum(durs) / len(durs), len(durs)
 
 
 def stats_summary(d, command):
@@ -234,7 +253,7 @@ def cpu_baseline(tensors, plan, chunk, target_bytes):
                       "+ restore + verify, one thread, %.1f s" % (len(frags), len(tensors), total, nc, chunk >> 20, dt)}
 
 
-def overlap_leg(torch, P, W, wid, steps):
+def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps):
     """Step-time overhead of per-step snapshots under a bf16 GEMM load."""
     tensors, plan = W.make_state(wid, device="cuda")
     n = len(tensors)
@@ -256,6 +275,8 @@ def overlap_leg(torch, P, W, wid, steps):
     s = ck.snapshot(step=0)
     ck.wait_committed(s)
     t_d2h = P.ckpt_last_timing(ck.ctx, P.CKPT_OP_SNAPSHOT)["copy_ms"]
+    if t_d2h <= 0:  # engine timestamps unavailable (a copy tracer owns the signals)
+        t_d2h = ck.image_bytes / link_d2h_gbps / 1e6
     P.ckpt_set_timing(ck.ctx, False)
     R = int(math.ceil(1.5 * t_d2h / t_gemm))
     params = [tensors[i] for i in range(0, n, 4)]
@@ -332,6 +353,17 @@ def main():
     if args.stats_summary:
         print("# rocprofv3 --kernel-trace --memory-copy-trace --stats\n\ncommand: `%s`\n" % args.command)
         print(stats_summary(args.stats_summary, args.command))
+        if args.bench_json:
+            b = json.loads(open(args.bench_json).read().strip().splitlines()[-1])
+            avg, n = timed_pack_average(args.stats_summary, b)
+            rl = b["roofline"]
+            print("\nPack kernel over the bench's timed steps (%d dispatches, taken from the kernel trace in order):"
+                  % n)
+            print("- rocprofv3 average duration: %.4f ms" % avg)
+            print("- bench.py HIP events on the pack stream, same run: %.4f ms (achieved %.1f GB/s, frac %.4f)"
+                  % (rl["avg_launch_ms"], rl["achieved"], rl["frac"]))
+            print("- algorithmic bytes per launch %d -> %.1f GB/s from the rocprofv3 average"
+                  % (rl["algorithmic_bytes_per_launch"], rl["algorithmic_bytes_per_launch"] / avg / 1e6))
         return
     if args.gpus != 1:
         print("bench.py measures one GPU: the snapshot path has no cross-GPU step in this build "
@@ -395,7 +427,7 @@ def main():
     pack_bytes = 2 * S * args.steps
     pack_gbps = pack_bytes / pack_ms / 1e6
     d2h_ms = agg("snapshot", "copy_ms")
-    d2h_gbps = sn["copy_bytes"] * args.steps / d2h_ms / 1e6 if d2h_ms > 0 else float("nan")
+    d2h_gbps = sn["copy_bytes"] * args.steps / d2h_ms / 1e6 if d2h_ms > 0 else None
     restore_gbps = sn["copy_bytes"] * args.steps / agg("restore", "total_ms") / 1e6
     scatter_gbps = 2 * S * args.steps / agg("restore", "kernel_ms") / 1e6
     h2d_gbps = sn["copy_bytes"] * args.steps / agg("restore", "copy_ms") / 1e6
@@ -422,7 +454,7 @@ def main():
     overlap = None
     if not args.no_overlap:
         log("overlap leg")
-        overlap = overlap_leg(torch, P, W, args.overlap_workload, args.overlap_steps)
+        overlap = overlap_leg(torch, P, W, args.overlap_workload, args.overlap_steps, link["d2h"])
     try:
         sha = subprocess.run(["git", "rev-parse", "--short", "HEAD"], cwd=ROOT, capture_output=True,
                              text=True).stdout.strip() or None
@@ -438,8 +470,9 @@ def main():
                    "parallelism": "one rank, one GPU"},
         "roofline": roofline,
         "cpu_baseline": cpu,
-        "components": {"pack_GBps": round(pack_gbps, 1), "d2h_GBps": round(d2h_gbps, 2),
-                       "d2h_link_peak_GBps": round(link["d2h"], 2), "d2h_frac_of_link": round(d2h_gbps / link["d2h"], 4),
+        "components": {"pack_GBps": round(pack_gbps, 1), "d2h_GBps": d2h_gbps and round(d2h_gbps, 2),
+                       "d2h_link_peak_GBps": round(link["d2h"], 2),
+                       "d2h_frac_of_link": d2h_gbps and round(d2h_gbps / link["d2h"], 4),
                        "h2d_GBps": round(h2d_gbps, 2), "h2d_link_peak_GBps": round(link["h2d"], 2),
                        "restore_GBps": round(restore_gbps, 2), "scatter_verify_GBps": round(scatter_gbps, 1),
                        "verify_GBps": round(verify_gbps, 2), "verify_kernel_GBps": round(verify_kernel_gbps, 1),

@@ -1,0 +1,120 @@
+"""Full-size shards against the oracle (needs an MI355X; tens of seconds each).
+
+At these sizes the oracle cannot pack the whole shard quickly, so the checks
+are: sampled chunks packed by the oracle from the live fragments and compared
+byte for byte with the committed host image; the oracle's sums of every chunk
+of the host image against the stored sums; and, where device memory allows, a
+full restore compared with device copies taken before the snapshot.
+"""
+import gc
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+from gpu_util import host_bytes
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    import paper_2607_01646_amd as P
+
+
+@pytest.fixture(autouse=True)
+def release_memory():
+    yield
+    gc.collect()
+    if torch.cuda.is_available():
+        torch.cuda.empty_cache()
+
+
+def sample_chunks(n_chunks, k=6, seed=77):
+    rng = np.random.default_rng(seed)
+    picks = {0, n_chunks - 1} | {int(x) for x in rng.integers(0, n_chunks, k)}
+    return sorted(picks)
+
+
+def oracle_window(tensors, off, sizes, lo, hi):
+    """The oracle's pack of image bytes [lo, hi), fed with the overlapping
+    slices of the live fragments (fragment i's bytes [a, b) placed at image
+    offset off[i] + a)."""
+    frags, offs = [], []
+    for i, s in enumerate(sizes):
+        o = int(off[i])
+        a, b = max(o, lo) - o, min(o + s, hi) - o
+        if b > a:
+            frags.append(tensors[i].reshape(-1).view(torch.uint8)[a:b].cpu().numpy())
+            offs.append(o + a)
+    return O.pack_window(frags, offs, lo, hi)
+
+
+def check_shard(wid, staging=0, full_restore=True, all_sums=True):
+    tensors, plan = W.make_state(wid, device="cuda")
+    sizes = [p[1] for p in plan]
+    chunk = W.WORKLOADS[wid]["chunk"]
+    torch.cuda.synchronize()
+    before = [t.clone() for t in tensors] if full_restore else None
+    ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=chunk,
+                        device_staging_bytes=staging)
+    off, I, nc = O.layout(sizes, 256, chunk)
+    assert np.array_equal(ck.offsets, off) and (ck.image_bytes, ck.n_chunks) == (I, nc)
+    snap = ck.snapshot(step=wid)
+    ck.wait_committed(snap)
+    img, sums = ck.host_image(snap)
+    for c in sample_chunks(nc):
+        lo, hi = c * chunk, min((c + 1) * chunk, I)
+        want = oracle_window(tensors, off, sizes, lo, hi)
+        assert np.array_equal(img[lo:hi], want), "chunk %d differs" % c
+        assert int(sums[c]) == int(O.chunk_sums(want, lo, hi, chunk)[0])
+    if all_sums:
+        assert np.array_equal(sums, O.chunk_sums(img, 0, I, chunk))
+    assert ck.verify(snap) == []
+    if full_restore:
+        for t in tensors:
+            t.view(-1).view(torch.uint8).fill_(0x3C)
+        assert ck.restore(snap) == []
+        torch.cuda.synchronize()
+        for i, (t, b) in enumerate(zip(tensors, before)):
+            assert torch.equal(t.view(-1).view(torch.uint8), b.view(-1).view(torch.uint8)), "fragment %d" % i
+    return ck, tensors, plan, snap
+
+
+def test_gpt_1_3b_shard():
+    """24 layers, hidden 2048: 1168 fragments, 18.42 GB, 64 MiB chunks."""
+    ck, *_ = check_shard(2)
+    assert ck.n_chunks == 275
+    ck.close()
+
+
+def test_llama65b_tp8pp8_rank_shard():
+    """One rank of a 65B LLaMA under TP=8 x PP=8: 360 fragments, 14.17 GB."""
+    ck, *_ = check_shard(3)
+    assert ck.n_chunks == 212
+    ck.close()
+
+
+def test_stress_4096_fragments_with_flips():
+    """4096 fragments (8 GiB, bf16/fp32 alternating, 1 KiB .. ~21 MiB) with 32
+    seeded single-bit flips in distinct chunks: all reported and located."""
+    ck, tensors, plan, snap = check_shard(5)
+    sizes = [p[1] for p in plan]
+    chunk = W.WORKLOADS[5]["chunk"]
+    img, sums = ck.host_image(snap)
+    stored = sums.copy()
+    ranges = [(c * chunk, min((c + 1) * chunk, img.size)) for c in range(ck.n_chunks)]
+    flips = W.flip_positions(ranges, n_flips=32, seed=2005)
+    for c, byte, bit in flips:
+        img[byte] ^= np.uint8(1 << bit)
+    bad = ck.restore(snap)
+    assert bad == sorted(c for c, _, _ in flips)
+    recomputed = P.ckpt_last_sums(ck.ctx)
+    for c, byte, bit in flips:
+        k = 8 * (byte % 8) + bit
+        was_set = (int(img[byte]) >> bit) & 1 == 0
+        assert (int(recomputed[c]) - int(stored[c])) % (1 << 64) == ((-(1 << k)) % (1 << 64) if was_set else 1 << k)
+        lo, hi, f0, f1 = ck.chunk_fragments(c)
+        (olo, ohi), ids = O.locate(c, chunk, ck.image_bytes, ck.offsets, sizes)
+        assert (lo, hi) == (olo, ohi) and ids and f0 <= min(ids) and max(ids) <= f1
+    ck.close()
