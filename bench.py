@@ -8,8 +8,10 @@ fp32 master weights and Adam moments, 64 MiB chunks):
   snapshot = pack + chunk sums (HBM -> HBM staging) -> chunked D2H into the
              pinned ping-pong image -> commit         (paper Sec. V-B, VI-A)
   gate     = the wait before the optimizer step      (paper Sec. VI-A)
+  verify   = H2D + re-check every chunk sum, of the previous step's committed
+             snapshot, while this step's snapshot streams out (the host link
+             is full duplex; the first step verifies its own snapshot)
   restore  = H2D + scatter into the tensors + re-check every chunk sum
-  verify   = H2D + re-check every chunk sum
 The state is generated on the GPU before timing starts.  Prints one JSON
 line; `value` is payload bytes per second through that whole cycle.
 
@@ -393,14 +395,22 @@ def main():
     ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=wl["chunk"])
     P.ckpt_set_timing(ck.ctx, True)
 
+    prev = [None]
+
     def step(k):
+        # Snapshot k streams out (D2H) while the previous committed snapshot
+        # is verified (H2D): the host link carries both directions at once.
         snap = ck.snapshot(step=k, meta=b"step=%d" % k)
         ck.wait_captured(snap, 0, n)
+        torch.cuda.current_stream().synchronize()  # packed: verify's kernels do not share HBM with the pack
+        bad = ck.verify(prev[0]) if prev[0] is not None else []
         ck.wait_committed(snap)
-        bad = ck.restore(snap)
-        bad += ck.verify(snap)
+        if prev[0] is None:
+            bad += ck.verify(snap)
+        bad += ck.restore(snap)
         if bad:
             raise RuntimeError("checksum mismatch in chunks %s" % bad)
+        prev[0] = snap
 
     log("warmup")
     for k in range(args.warmup):

@@ -87,7 +87,7 @@ typedef struct {
     uint64_t group_bytes;          /* full-image mode: bytes packed per kernel launch and copied per
                                       DMA request; 0 = 1 GiB (rounded to whole chunks) */
     int32_t device;                /* HIP device ordinal */
-    uint32_t grid_blocks;          /* cap on workgroups per kernel launch; 0 = one per 16 KiB tile */
+    uint32_t grid_blocks;          /* cap on workgroups per kernel launch; 0 = one per 8 KiB tile */
 } ckpt_config;
 
 typedef struct {
@@ -206,7 +206,8 @@ ckpt_status ckpt_debug_interrupt_next(ckpt_ctx* ctx, int32_t groups);
  * Errors: EINVAL (bad `which`), ESTATE (no timed operation of that kind). */
 typedef struct {
     float kernel_ms;     /* sum of the tile-kernel launches' durations (pack, scatter or
-                            checksum; the small per-chunk reduce kernel is not included) */
+                            checksum), from events recorded by the dispatch itself; the
+                            small per-chunk reduce kernel is not included */
     uint32_t kernels;    /* number of tile-kernel launches */
     uint32_t copies;     /* number of DMA copy requests (image bytes only) */
     float copy_ms;       /* first image copy start to last image copy end */

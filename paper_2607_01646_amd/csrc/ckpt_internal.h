@@ -27,18 +27,22 @@ struct Geometry {
 
 // The tile kernels.  Each covers tiles [t_lo, t_hi) and writes tile t's
 // word-sum to partials[t]; launches cover whole chunks.  grid_cap bounds the
-// workgroups (one per tile when the cap is larger).
+// workgroups (one per tile when the cap is larger).  Non-null t0/t1 are
+// timing events recorded around the dispatch itself.
 //   pack:     fragment bytes -> image window; image byte x goes to dst + (x - dst_origin)
 //   scatter:  image window -> fragment bytes (image byte x read at src + (x - src_origin))
 //   checksum: image window only
 hipError_t launch_pack(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
                        const Geometry& g, uint64_t t_lo, uint64_t t_hi, uint8_t* dst, uint64_t dst_origin,
-                       unsigned long long* partials, uint32_t grid_cap, hipStream_t s);
+                       unsigned long long* partials, uint32_t grid_cap, hipStream_t s, hipEvent_t t0 = nullptr,
+                       hipEvent_t t1 = nullptr);
 hipError_t launch_scatter(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
                           const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src, uint64_t src_origin,
-                          unsigned long long* partials, uint32_t grid_cap, hipStream_t s);
+                          unsigned long long* partials, uint32_t grid_cap, hipStream_t s, hipEvent_t t0 = nullptr,
+                          hipEvent_t t1 = nullptr);
 hipError_t launch_checksum(const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src, uint64_t src_origin,
-                           unsigned long long* partials, uint32_t grid_cap, hipStream_t s);
+                           unsigned long long* partials, uint32_t grid_cap, hipStream_t s, hipEvent_t t0 = nullptr,
+                           hipEvent_t t1 = nullptr);
 
 // Chunk sums of the chunks covered by tiles [t_lo, t_hi): sums_out[c] is the
 // sum of the chunk's tile sums.  With expected non-null, bad[c] is set to 1

@@ -11,10 +11,13 @@
 // floating-point instruction touches them, so NaN payloads, -0 and
 // subnormals pass unchanged.
 //
-// Work split.  The image is cut into power-of-two tiles (16 KiB) that never
+// Work split.  The image is cut into power-of-two tiles (8 KiB) that never
 // cross a chunk.  A workgroup of 256 lanes (4 wave64) takes one tile (or
-// tiles grid-stride when the grid is capped); each lane moves 16-byte
-// vectors, four in flight.  A tile inside one 16-byte-aligned fragment
+// tiles grid-stride when the grid is capped); each lane moves one batch of
+// two 16-byte vectors per tile, both loads issued before the stores.
+// Consecutive tiles go to consecutive workgroups, which the hardware deals
+// out round-robin over the 8 XCDs (measured faster than giving each XCD a
+// contiguous range).  A tile inside one 16-byte-aligned fragment
 // takes an unrolled non-temporal stream; otherwise each vector finds its
 // fragment (binary search over the tile's fragment offsets in LDS), loads
 // aligned 16-byte blocks and funnel-shifts them when the fragment is
@@ -27,6 +30,8 @@
 // XCD's L2, which per tile would cost more than the tile's own traffic.
 // Addition modulo 2^64 is associative and commutative, so any order of
 // tiles gives the same bits.
+#include <hip/hip_ext.h>
+
 #include "ckpt_internal.h"
 
 namespace ckpt {
@@ -35,8 +40,8 @@ namespace {
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBlock = 256;      // lanes per workgroup (4 wave64)
-constexpr int kLdsFrags = 512;  // fragment offsets cached per tile (a 16 KiB tile holds at most 65 non-empty ones)
-constexpr int kUnroll = 4;      // 16-byte vectors in flight per lane on the streaming path
+constexpr int kLdsFrags = 256;  // fragment offsets cached per tile (an 8 KiB tile holds at most 33 non-empty ones)
+constexpr int kUnroll = 2;      // 16-byte vectors per lane per batch: one batch covers an 8 KiB tile
 
 enum Mode { PACK = 0, SCATTER = 1, VERIFY = 2 };
 
@@ -256,13 +261,23 @@ __device__ __forceinline__ uint32_t find_frag_global(const FragDev* frags, uint3
     return lo;
 }
 
-template <int MODE, int BLOCK = kBlock, int UNROLL = kUnroll, bool NTL = true, bool NTS = true>
+// Workgroup b of a launch runs on XCD b % 8 (round-robin dispatch).  With
+// REMAP, workgroup b takes tile x*q + min(x, r) + b/8 (x = b % 8, n = 8q + r
+// workgroups), so each XCD streams one contiguous eighth of the launch.
+__device__ __forceinline__ uint64_t remap_block(uint32_t b, uint32_t n)
+{
+    const uint32_t q = n >> 3, r = n & 7, x = b & 7, k = b >> 3;
+    return (uint64_t)x * q + (x < r ? x : r) + k;
+}
+
+template <int MODE, int BLOCK = kBlock, int UNROLL = kUnroll, bool NTL = true, bool NTS = true, bool REMAP = false>
 __global__ __launch_bounds__(BLOCK) void tile_kernel(Args a)
 {
     __shared__ unsigned long long s_red[BLOCK / 64];
     __shared__ uint64_t s_off[kLdsFrags];
     const uint32_t tid = threadIdx.x;
-    for (uint64_t t = a.t_lo + blockIdx.x; t < a.t_hi; t += gridDim.x) {
+    const uint64_t first = REMAP ? remap_block(blockIdx.x, gridDim.x) : blockIdx.x;
+    for (uint64_t t = a.t_lo + first; t < a.t_hi; t += gridDim.x) {
         const uint64_t base = t << a.g.tile_shift;
         uint64_t end = base + (1ull << a.g.tile_shift);
         if (end > a.g.image_bytes) end = a.g.image_bytes;
@@ -347,13 +362,18 @@ __global__ __launch_bounds__(kBlock) void chunk_reduce_kernel(ReduceArgs r)
     }
 }
 
+// With timing events, the launch records them around the dispatch itself
+// (the same interval a kernel trace reports).
 template <int MODE>
-hipError_t launch_tiles(const Args& a, uint32_t grid_cap, hipStream_t s)
+hipError_t launch_tiles(const Args& a, uint32_t grid_cap, hipStream_t s, hipEvent_t t0, hipEvent_t t1)
 {
     if (a.t_hi <= a.t_lo) return hipSuccess;
     const uint64_t n = a.t_hi - a.t_lo;
     const uint32_t grid = (uint32_t)(n < grid_cap ? n : grid_cap);
-    hipLaunchKernelGGL(tile_kernel<MODE>, dim3(grid), dim3(kBlock), 0, s, a);
+    if (t0 && t1)
+        hipExtLaunchKernelGGL(tile_kernel<MODE>, dim3(grid), dim3(kBlock), 0, s, t0, t1, 0, a);
+    else
+        hipLaunchKernelGGL(tile_kernel<MODE>, dim3(grid), dim3(kBlock), 0, s, a);
     return hipGetLastError();
 }
 
@@ -377,25 +397,27 @@ hipError_t launch_release(int64_t* signal_value, hipStream_t s)
 
 hipError_t launch_pack(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
                        const Geometry& g, uint64_t t_lo, uint64_t t_hi, uint8_t* dst, uint64_t dst_origin,
-                       unsigned long long* partials, uint32_t grid_cap, hipStream_t s)
+                       unsigned long long* partials, uint32_t grid_cap, hipStream_t s, hipEvent_t t0, hipEvent_t t1)
 {
     Args a{frags, tile_first, tile_last, g, t_lo, t_hi, dst, dst_origin, partials};
-    return launch_tiles<PACK>(a, grid_cap, s);
+    return launch_tiles<PACK>(a, grid_cap, s, t0, t1);
 }
 
 hipError_t launch_scatter(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
                           const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src, uint64_t src_origin,
-                          unsigned long long* partials, uint32_t grid_cap, hipStream_t s)
+                          unsigned long long* partials, uint32_t grid_cap, hipStream_t s, hipEvent_t t0,
+                          hipEvent_t t1)
 {
     Args a{frags, tile_first, tile_last, g, t_lo, t_hi, const_cast<uint8_t*>(src), src_origin, partials};
-    return launch_tiles<SCATTER>(a, grid_cap, s);
+    return launch_tiles<SCATTER>(a, grid_cap, s, t0, t1);
 }
 
 hipError_t launch_checksum(const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src, uint64_t src_origin,
-                           unsigned long long* partials, uint32_t grid_cap, hipStream_t s)
+                           unsigned long long* partials, uint32_t grid_cap, hipStream_t s, hipEvent_t t0,
+                           hipEvent_t t1)
 {
     Args a{nullptr, nullptr, nullptr, g, t_lo, t_hi, const_cast<uint8_t*>(src), src_origin, partials};
-    return launch_tiles<VERIFY>(a, grid_cap, s);
+    return launch_tiles<VERIFY>(a, grid_cap, s, t0, t1);
 }
 
 hipError_t launch_chunk_reduce(const Geometry& g, uint64_t t_lo, uint64_t t_hi, const unsigned long long* partials,

@@ -56,13 +56,14 @@ namespace {
 constexpr uint64_t kDefaultChunk = 64ull << 20;
 constexpr uint32_t kDefaultAlign = 256;
 constexpr uint64_t kDefaultGroup = 1ull << 30;
-// 16 KiB tiles: each of a workgroup's 256 lanes moves exactly one batch of
-// four 16-byte vectors per tile (measured fastest on gfx950 for pack, scatter
-// and verify, one workgroup per tile).
-constexpr uint32_t kMaxTileShift = 14;
+// 8 KiB tiles: each of a workgroup's 256 lanes moves exactly one batch of
+// two 16-byte vectors per tile (measured fastest on gfx950 with one
+// workgroup per tile in 1 GiB launches).
+constexpr uint32_t kMaxTileShift = 13;
 constexpr uint32_t kMaxMeta = 1u << 20;
 constexpr uint32_t kDefaultGrid = 0x7fffffff; // one workgroup per tile unless capped
 constexpr int kMaxEngines = 2;
+constexpr uint64_t kVerifySlots = 2; // verify's device ring: two slots of one chunk group each
 
 struct Frag {
     uint64_t ptr, nbytes, off;
@@ -162,8 +163,15 @@ struct ckpt_ctx {
     bool have_last_sums = false;
     std::vector<uint64_t> last_sums;
     OpTiming op_timing[3];
-    std::vector<hipEvent_t> tk0, tk1; // restore/verify timing
+    std::vector<hipEvent_t> tk0, tk1; // restore timing
     hipEvent_t tt0 = nullptr, tc0 = nullptr, tc1 = nullptr;
+
+    // verify: its own ring of chunk slots and streams
+    uint8_t* d_vring = nullptr;
+    uint64_t n_vslots = 0;
+    hipStream_t s_vcopy = nullptr, s_vker = nullptr;
+    hipEvent_t ev_vdone = nullptr, vt0 = nullptr, vc0 = nullptr, vc1 = nullptr;
+    std::vector<hipEvent_t> vfree, vloaded, vk0, vk1;
 
     std::string err;
 };
@@ -232,7 +240,7 @@ bool plan(const uint64_t* nb, uint32_t n, uint64_t C, uint32_t A, Plan* p, bool 
     if (p->I == 0) return false;
     for (uint32_t i = 0; i < n; ++i) p->end[i] = (i + 1 < n) ? p->off[i + 1] : p->I;
     p->n_chunks = (p->I + C - 1) / C;
-    // Tiles: the largest power of two <= 16 KiB dividing the chunk size.
+    // Tiles: the largest power of two <= 8 KiB dividing the chunk size.
     uint32_t ts = 4;
     while (ts < kMaxTileShift && C % (1ull << (ts + 1)) == 0) ++ts;
     p->tile_shift = ts;
@@ -510,8 +518,8 @@ void prune(ckpt_ctx* c)
 // Wait for every enqueued kernel and copy of the context.
 ckpt_status drain(ckpt_ctx* c)
 {
-    HIPCHK(c, hipStreamSynchronize(c->s_pack));
-    HIPCHK(c, hipStreamSynchronize(c->s_copy));
+    for (hipStream_t st : {c->s_pack, c->s_copy, c->s_vcopy, c->s_vker})
+        if (st) HIPCHK(c, hipStreamSynchronize(st));
     for (auto& kv : c->recs) {
         ckpt_status st = wait_copies(c, kv.second);
         if (st) return st;
@@ -561,62 +569,101 @@ float elapsed(hipEvent_t a, hipEvent_t b)
     return ms;
 }
 
+// Where restore and verify stage image bytes on the device, and the streams
+// and events that order them.  Unit u covers chunks [u*G, (u+1)*G).
+struct Lane {
+    hipStream_t s_copy, s_ker;
+    uint8_t* base;   // staging: full image, or ring slots of G chunks each
+    bool ring;
+    uint64_t n_slots;
+    uint64_t G;
+    uint64_t n_units;
+    std::vector<hipEvent_t>* area_free; // per slot (ring) or per unit
+    std::vector<hipEvent_t>* loaded;    // per unit
+    std::vector<hipEvent_t>* tk0;       // per unit, timing
+    std::vector<hipEvent_t>* tk1;
+    hipEvent_t done, t0, c0, c1;
+};
+
+Lane restore_lane(ckpt_ctx* c)
+{
+    return Lane{c->s_copy, c->s_pack, c->d_staging, c->ring, c->n_slots, c->G, c->n_groups, &c->area_free,
+                &c->ev_loaded, &c->tk0, &c->tk1, c->ev_done, c->tt0, c->tc0, c->tc1};
+}
+
+Lane verify_lane(ckpt_ctx* c)
+{
+    return Lane{c->s_vcopy, c->s_vker, c->d_vring, true, c->n_vslots, c->G, c->n_groups, &c->vfree,
+                &c->vloaded, &c->vk0, &c->vk1, c->ev_vdone, c->vt0, c->vc0, c->vc1};
+}
+
 // Restore (scatter=true) or verify (scatter=false) from a committed image.
+// Restore first waits for every outstanding snapshot (it rewrites the live
+// tensors and shares the snapshot staging).  Verify only reads a committed
+// image, which no in-flight snapshot targets, through its own staging ring
+// and streams, so it may run while a newer snapshot streams out: the host
+// link is full duplex.
 ckpt_status run_check(ckpt_ctx* c, uint64_t snap_id, hipStream_t stream, bool scatter, uint32_t* bad_chunks,
                       uint32_t cap, uint32_t* n_bad)
 {
     if (!c->registered) return fail(c, CKPT_ESTATE, "no tensors registered");
     if (!n_bad || (cap && !bad_chunks)) return fail(c, CKPT_EINVAL, "null output pointer");
     HIPCHK(c, hipSetDevice(c->device));
-    ckpt_status st = drain(c);
-    if (st) return st;
+    ckpt_status st = CKPT_OK;
+    if (scatter) {
+        st = drain(c);
+        if (st) return st;
+    }
     SnapRec* r = nullptr;
     st = pick_committed(c, snap_id, &r);
     if (st) return st;
+    const Lane L = scatter ? restore_lane(c) : verify_lane(c);
     const int b = r->buf;
     const int op = scatter ? CKPT_OP_RESTORE : CKPT_OP_VERIFY;
     const bool timed = c->timing;
+    const uint64_t unit = L.G * c->C;
     unsigned long long* partials = c->d_partials + c->geo.n_tiles;
-    HIPCHK(c, hipMemcpyAsync(c->d_expected, c->h_sums[b], c->n_chunks * 8, hipMemcpyHostToDevice, c->s_copy));
+    HIPCHK(c, hipMemcpyAsync(c->d_expected, c->h_sums[b], c->n_chunks * 8, hipMemcpyHostToDevice, L.s_copy));
     if (scatter) {
         HIPCHK(c, hipEventRecord(c->ev_trigger, stream));
-        HIPCHK(c, hipStreamWaitEvent(c->s_pack, c->ev_trigger, 0));
+        HIPCHK(c, hipStreamWaitEvent(L.s_ker, c->ev_trigger, 0));
     }
-    if (timed) HIPCHK(c, hipEventRecord(c->tt0, c->s_copy));
-    for (uint64_t g = 0; g < c->n_groups; ++g) {
-        const uint64_t lo = group_lo(c, g), hi = group_hi(c, g);
-        HIPCHK(c, hipStreamWaitEvent(c->s_copy, c->area_free[area_of(c, g)], 0));
-        if (timed && g == 0) HIPCHK(c, hipEventRecord(c->tc0, c->s_copy));
-        HIPCHK(c, hipMemcpyAsync(staging_of(c, g), c->h_img[b] + lo, hi - lo, hipMemcpyHostToDevice, c->s_copy));
-        if (timed && g + 1 == c->n_groups) HIPCHK(c, hipEventRecord(c->tc1, c->s_copy));
-        HIPCHK(c, hipEventRecord(c->ev_loaded[g], c->s_copy));
-        HIPCHK(c, hipStreamWaitEvent(c->s_pack, c->ev_loaded[g], 0));
-        if (timed) HIPCHK(c, hipEventRecord(c->tk0[g], c->s_pack));
-        const uint64_t t_lo = tiles_lo(c, g), t_hi = tiles_hi(c, g);
+    if (timed) HIPCHK(c, hipEventRecord(L.t0, L.s_copy));
+    for (uint64_t u = 0; u < L.n_units; ++u) {
+        const uint64_t lo = u * unit, hi = std::min(lo + unit, c->I);
+        const uint64_t area = L.ring ? u % L.n_slots : u;
+        uint8_t* stage = L.ring ? L.base + area * unit : L.base + lo;
+        HIPCHK(c, hipStreamWaitEvent(L.s_copy, (*L.area_free)[area], 0));
+        if (timed && u == 0) HIPCHK(c, hipEventRecord(L.c0, L.s_copy));
+        HIPCHK(c, hipMemcpyAsync(stage, c->h_img[b] + lo, hi - lo, hipMemcpyHostToDevice, L.s_copy));
+        if (timed && u + 1 == L.n_units) HIPCHK(c, hipEventRecord(L.c1, L.s_copy));
+        HIPCHK(c, hipEventRecord((*L.loaded)[u], L.s_copy));
+        HIPCHK(c, hipStreamWaitEvent(L.s_ker, (*L.loaded)[u], 0));
+        const uint64_t t_lo = lo >> c->geo.tile_shift, t_hi = (hi + (1ull << c->geo.tile_shift) - 1) >> c->geo.tile_shift;
+        hipEvent_t k0 = timed ? (*L.tk0)[u] : nullptr, k1 = timed ? (*L.tk1)[u] : nullptr;
         hipError_t e;
         if (scatter)
-            e = launch_scatter(c->d_frags, c->d_tile_first, c->d_tile_last, c->geo, t_lo, t_hi, staging_of(c, g), lo,
-                               partials, c->grid_cap, c->s_pack);
+            e = launch_scatter(c->d_frags, c->d_tile_first, c->d_tile_last, c->geo, t_lo, t_hi, stage, lo, partials,
+                               c->grid_cap, L.s_ker, k0, k1);
         else
-            e = launch_checksum(c->geo, t_lo, t_hi, staging_of(c, g), lo, partials, c->grid_cap, c->s_pack);
+            e = launch_checksum(c->geo, t_lo, t_hi, stage, lo, partials, c->grid_cap, L.s_ker, k0, k1);
         if (e != hipSuccess) return fail(c, CKPT_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
-        if (timed) HIPCHK(c, hipEventRecord(c->tk1[g], c->s_pack));
-        e = launch_chunk_reduce(c->geo, t_lo, t_hi, partials, c->d_recomputed, c->d_expected, c->d_bad, c->s_pack);
+        e = launch_chunk_reduce(c->geo, t_lo, t_hi, partials, c->d_recomputed, c->d_expected, c->d_bad, L.s_ker);
         if (e != hipSuccess) return fail(c, CKPT_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
-        HIPCHK(c, hipEventRecord(c->area_free[area_of(c, g)], c->s_pack));
+        HIPCHK(c, hipEventRecord((*L.area_free)[area], L.s_ker));
     }
-    HIPCHK(c, hipMemcpyAsync(c->h_bad, c->d_bad, c->n_chunks, hipMemcpyDeviceToHost, c->s_pack));
-    HIPCHK(c, hipMemcpyAsync(c->h_recomputed, c->d_recomputed, c->n_chunks * 8, hipMemcpyDeviceToHost, c->s_pack));
-    HIPCHK(c, hipEventRecord(c->ev_done, c->s_pack));
-    if (scatter) HIPCHK(c, hipStreamWaitEvent(stream, c->ev_done, 0));
-    HIPCHK(c, hipEventSynchronize(c->ev_done));
+    HIPCHK(c, hipMemcpyAsync(c->h_bad, c->d_bad, c->n_chunks, hipMemcpyDeviceToHost, L.s_ker));
+    HIPCHK(c, hipMemcpyAsync(c->h_recomputed, c->d_recomputed, c->n_chunks * 8, hipMemcpyDeviceToHost, L.s_ker));
+    HIPCHK(c, hipEventRecord(L.done, L.s_ker));
+    if (scatter) HIPCHK(c, hipStreamWaitEvent(stream, L.done, 0));
+    HIPCHK(c, hipEventSynchronize(L.done));
     if (timed) {
         ckpt_timing t{};
-        for (uint64_t g = 0; g < c->n_groups; ++g) t.kernel_ms += elapsed(c->tk0[g], c->tk1[g]);
-        t.kernels = (uint32_t)c->n_groups;
-        t.copies = (uint32_t)c->n_groups;
-        t.copy_ms = elapsed(c->tc0, c->tc1);
-        t.total_ms = elapsed(c->tt0, c->tk1[c->n_groups - 1]);
+        for (uint64_t u = 0; u < L.n_units; ++u) t.kernel_ms += elapsed((*L.tk0)[u], (*L.tk1)[u]);
+        t.kernels = (uint32_t)L.n_units;
+        t.copies = (uint32_t)L.n_units;
+        t.copy_ms = elapsed(L.c0, L.c1);
+        t.total_ms = elapsed(L.t0, (*L.tk1)[L.n_units - 1]);
         t.kernel_bytes = scatter ? 2 * c->payload : c->I;
         t.copy_bytes = c->I;
         c->op_timing[op].t = t;
@@ -645,10 +692,11 @@ void free_ctx(ckpt_ctx* c)
     c->free_res.clear();
     for (auto e : c->area_free) (void)hipEventDestroy(e);
     for (auto e : c->ev_loaded) (void)hipEventDestroy(e);
-    for (auto e : c->tk0) (void)hipEventDestroy(e);
-    for (auto e : c->tk1) (void)hipEventDestroy(e);
-    for (hipEvent_t e : {c->ev_trigger, c->ev_done, c->tt0, c->tc0, c->tc1})
+    for (auto* v : {&c->tk0, &c->tk1, &c->vfree, &c->vloaded, &c->vk0, &c->vk1})
+        for (auto e : *v) (void)hipEventDestroy(e);
+    for (hipEvent_t e : {c->ev_trigger, c->ev_done, c->tt0, c->tc0, c->tc1, c->ev_vdone, c->vt0, c->vc0, c->vc1})
         if (e) (void)hipEventDestroy(e);
+    (void)hipFree(c->d_vring);
     (void)hipFree(c->d_frags);
     (void)hipFree(c->d_tile_first);
     (void)hipFree(c->d_tile_last);
@@ -664,8 +712,8 @@ void free_ctx(ckpt_ctx* c)
     }
     if (c->h_bad) (void)hipHostFree(c->h_bad);
     if (c->h_recomputed) (void)hipHostFree(c->h_recomputed);
-    if (c->s_pack) (void)hipStreamDestroy(c->s_pack);
-    if (c->s_copy) (void)hipStreamDestroy(c->s_copy);
+    for (hipStream_t st : {c->s_pack, c->s_copy, c->s_vcopy, c->s_vker})
+        if (st) (void)hipStreamDestroy(st);
 }
 
 // Issue one SDMA copy; on failure the dependency chain of the snapshot is
@@ -705,13 +753,13 @@ ckpt_status ckpt_create(const ckpt_config* cfg, ckpt_ctx** out)
     c->group_cfg = d.group_bytes ? d.group_bytes : kDefaultGroup;
     c->grid_cap = d.grid_blocks ? d.grid_blocks : kDefaultGrid;
     ckpt_status st = CKPT_OK;
-    if (hipSetDevice(c->device) != hipSuccess ||
-        hipStreamCreateWithFlags(&c->s_pack, hipStreamNonBlocking) != hipSuccess ||
-        hipStreamCreateWithFlags(&c->s_copy, hipStreamNonBlocking) != hipSuccess)
+    if (hipSetDevice(c->device) != hipSuccess)
         st = CKPT_EHIP;
-    for (hipEvent_t* e : {&c->ev_trigger, &c->ev_done})
+    for (hipStream_t* sp : {&c->s_pack, &c->s_copy, &c->s_vcopy, &c->s_vker})
+        if (st == CKPT_OK && hipStreamCreateWithFlags(sp, hipStreamNonBlocking) != hipSuccess) st = CKPT_EHIP;
+    for (hipEvent_t* e : {&c->ev_trigger, &c->ev_done, &c->ev_vdone})
         if (st == CKPT_OK) st = make_event(c, e, false);
-    for (hipEvent_t* e : {&c->tt0, &c->tc0, &c->tc1})
+    for (hipEvent_t* e : {&c->tt0, &c->tc0, &c->tc1, &c->vt0, &c->vc0, &c->vc1})
         if (st == CKPT_OK) st = make_event(c, e, true);
     if (st == CKPT_OK) st = setup_hsa(c);
     if (st != CKPT_OK) {
@@ -803,6 +851,8 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
     ALLOC(c->d_bad, c->n_chunks);
     ALLOC(c->d_area_done, n_areas * 8);
     ALLOC(c->d_staging, c->ring ? c->n_slots * c->C : c->I);
+    c->n_vslots = std::min<uint64_t>(kVerifySlots, c->n_groups);
+    ALLOC(c->d_vring, c->n_vslots * c->G * c->C);
 #undef ALLOC
     HIPCHK(c, hipMemcpy(c->d_frags, fd.data(), n * sizeof(FragDev), hipMemcpyHostToDevice));
     HIPCHK(c, hipMemcpy(c->d_tile_first, pl.tile_first.data(), nt * 4, hipMemcpyHostToDevice));
@@ -838,6 +888,21 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
         ckpt_status st = make_event(c, &c->ev_loaded[g], false);
         if (!st) st = make_event(c, &c->tk0[g], true);
         if (!st) st = make_event(c, &c->tk1[g], true);
+        if (st) return st;
+    }
+    c->vfree.resize(c->n_vslots, nullptr);
+    for (auto& e : c->vfree) {
+        ckpt_status st = make_event(c, &e, false);
+        if (st) return st;
+        HIPCHK(c, hipEventRecord(e, c->s_vker)); // every slot starts free
+    }
+    c->vloaded.resize(c->n_groups, nullptr);
+    c->vk0.resize(c->n_groups, nullptr);
+    c->vk1.resize(c->n_groups, nullptr);
+    for (uint64_t k = 0; k < c->n_groups; ++k) {
+        ckpt_status st = make_event(c, &c->vloaded[k], false);
+        if (!st) st = make_event(c, &c->vk0[k], true);
+        if (!st) st = make_event(c, &c->vk1[k], true);
         if (st) return st;
     }
     HIPCHK(c, hipDeviceSynchronize());
@@ -935,11 +1000,10 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
         if (c->area_seq[area])
             HIPCHK(c, hipStreamWaitValue64(c->s_pack, c->d_area_done + area, c->area_seq[area],
                                           hipStreamWaitValueGte, ~0ull));
-        if (r.timed) HIPCHK(c, hipEventRecord(res->k0[g], c->s_pack));
         hipError_t e = launch_pack(c->d_frags, c->d_tile_first, c->d_tile_last, c->geo, tiles_lo(c, g),
-                                   tiles_hi(c, g), staging_of(c, g), lo, c->d_partials, c->grid_cap, c->s_pack);
+                                   tiles_hi(c, g), staging_of(c, g), lo, c->d_partials, c->grid_cap, c->s_pack,
+                                   r.timed ? res->k0[g] : nullptr, r.timed ? res->k1[g] : nullptr);
         if (e != hipSuccess) return fail(c, CKPT_EHIP, "pack launch failed: %s", hipGetErrorString(e));
-        if (r.timed) HIPCHK(c, hipEventRecord(res->k1[g], c->s_pack));
         e = launch_chunk_reduce(c->geo, tiles_lo(c, g), tiles_hi(c, g), c->d_partials, res->d_sums, nullptr, nullptr,
                                 c->s_pack);
         if (e != hipSuccess) return fail(c, CKPT_EHIP, "reduce launch failed: %s", hipGetErrorString(e));

@@ -82,7 +82,7 @@ def test_tile_plan_brute_force(P):
         sizes[0] = 0
         sizes[-1] = 0
         tb, tf, tl = P.ckpt_debug_tile_plan(sizes, C, 256)
-        assert C % tb == 0 and tb & (tb - 1) == 0 and tb <= 16384
+        assert C % tb == 0 and tb & (tb - 1) == 0 and tb <= 8192
         off, I, nc = O.layout(sizes, 256, C)
         nonempty = [i for i, s in enumerate(sizes) if s]
 

@@ -84,7 +84,7 @@ def test_single_fragment_and_ragged_tail():
 
 
 def test_many_small_fragments_in_one_tile():
-    # 600 fragments of 1..40 bytes: 64 fragments per 16 KiB tile
+    # 600 fragments of 1..40 bytes: 32 fragments per 8 KiB tile
     rng = np.random.default_rng(21)
     sizes = [int(s) for s in rng.integers(1, 41, 600)]
     tensors, host = random_byte_fragments(sizes, seed=22)
@@ -284,6 +284,31 @@ def test_ping_pong_roles_and_busy():
     img[12345] ^= 0x40
     assert ck.verify(s3) == [12345 // (1 << 22)]
     assert ck.restore(s2) == []
+    ck.close()
+
+
+def test_verify_runs_beside_an_inflight_snapshot():
+    """Verify reads only the committed image, through its own staging ring,
+    so it runs while a newer snapshot streams into the other image; both
+    results match the oracle."""
+    tensors = _step_state(n_frag=64, numel=1 << 20)  # 256 MiB
+    ck = P.Checkpointer(tensors, chunk_bytes=1 << 22, group_bytes=1 << 24)
+    host1 = [host_bytes(t) for t in tensors]
+    s1 = ck.snapshot(step=1)
+    ck.wait_committed(s1)
+    for t in tensors:
+        t.mul_(-1.0)
+    host2 = [host_bytes(t) for t in tensors]
+    s2 = ck.snapshot(step=2)
+    assert ck.verify(s1) == []  # while s2's copies are in flight
+    want1, _, _ = O.pack(host1, 256, 1 << 22)
+    assert np.array_equal(P.ckpt_last_sums(ck.ctx), O.chunk_sums(want1, 0, want1.size, 1 << 22))
+    ck.wait_committed(s2)
+    img2, sums2 = ck.host_image(s2)
+    want2, _, _ = O.pack(host2, 256, 1 << 22)
+    assert np.array_equal(img2, want2) and np.array_equal(sums2, O.chunk_sums(want2, 0, want2.size, 1 << 22))
+    img1, _ = ck.host_image(s1)
+    assert np.array_equal(img1, want1)
     ck.close()
 
 
