@@ -46,6 +46,15 @@ def parse():
     ap.add_argument("--no-overlap", action="store_true")
     ap.add_argument("--overlap-steps", type=int, default=50)
     ap.add_argument("--overlap-workload", type=int, default=3)
+    ap.add_argument("--overlap-base-steps", type=int, default=0,
+                    help="steps of each of the two no-snapshot runs (0 = --overlap-steps)")
+    ap.add_argument("--overlap-ratios", default="1.5",
+                    help="compute window / standalone D2H time ratios to run, comma-separated (first = headline)")
+    ap.add_argument("--overlap-only", action="store_true",
+                    help="run only the overlap leg and print its JSON")
+    ap.add_argument("--bounce-bytes", type=int, default=0,
+                    help="pageable host images behind pinned bounce rings of this many bytes (0 = pinned images)")
+    ap.add_argument("--host-threads", type=int, default=0, help="bounce mode: host copy threads (0 = library default)")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-sample-bytes", type=int, default=10 << 30)
     ap.add_argument("--traffic", type=str, default=os.path.join(ROOT, "profiles", "pack_checksum_gpt1.3b_traffic.txt"),
@@ -255,8 +264,17 @@ def cpu_baseline(tensors, plan, chunk, target_bytes):
                       "+ restore + verify, one thread, %.1f s" % (len(frags), len(tensors), total, nc, chunk >> 20, dt)}
 
 
-def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps):
-    """Step-time overhead of per-step snapshots under a bf16 GEMM load."""
+def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_steps=0, bounce=0, threads=0):
+    """Step-time overhead of per-step snapshots under a bf16 GEMM load.
+
+    One step: R back-to-back GEMMs on the compute stream, the gate, then an
+    in-place "optimizer" update of every registered fragment; the snapshot
+    is issued right after the previous update.  R is fixed before measuring
+    as ceil(ratio * T_D2H / T_GEMM) from the standalone D2H time and the GEMM
+    time; the headline uses the first ratio.  Overhead compares the mean step
+    (paper Sec. VII-A statistic) with and without snapshots; the no-snapshot
+    runs bracket the snapshot run."""
+    base_steps = base_steps or steps
     tensors, plan = W.make_state(wid, device="cuda")
     n = len(tensors)
     M, K, N = W.OVERLAP_GEMM[wid]
@@ -272,15 +290,19 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps):
     e1.record()
     e1.synchronize()
     t_gemm = e0.elapsed_time(e1) / 50
-    ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=W.WORKLOADS[wid]["chunk"])
+    ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=W.WORKLOADS[wid]["chunk"],
+                        bounce_bytes=bounce, host_threads=threads)
     P.ckpt_set_timing(ck.ctx, True)
+    t0 = time.perf_counter()
     s = ck.snapshot(step=0)
     ck.wait_committed(s)
+    t_commit = (time.perf_counter() - t0) * 1e3
     t_d2h = P.ckpt_last_timing(ck.ctx, P.CKPT_OP_SNAPSHOT)["copy_ms"]
     if t_d2h <= 0:  # engine timestamps unavailable (a copy tracer owns the signals)
         t_d2h = ck.image_bytes / link_d2h_gbps / 1e6
+    if bounce:  # the snapshot is done when its last group is in the pageable image
+        t_d2h = max(t_d2h, t_commit)
     P.ckpt_set_timing(ck.ctx, False)
-    R = int(math.ceil(1.5 * t_d2h / t_gemm))
     params = [tensors[i] for i in range(0, n, 4)]
     masters = [tensors[i] for i in range(1, n, 4)]
     ms = [tensors[i] for i in range(2, n, 4)]
@@ -293,7 +315,7 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps):
         for p, m in zip(params, masters):
             p.copy_(m)
 
-    def run(with_snap):
+    def run(with_snap, R, steps):
         times = []
         for k in range(steps):
             torch.cuda.synchronize()
@@ -306,20 +328,36 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps):
             optimizer()
             torch.cuda.synchronize()
             times.append((time.perf_counter() - t0) * 1e3)
+            if (k + 1) % 10 == 0:
+                log("overlap: %s, %d/%d steps, last %.1f ms" % ("with snapshots" if with_snap else "baseline", k + 1,
+                                                                steps, times[-1]))
         return times
 
-    base1 = run(False)
-    withs = run(True)
-    base2 = run(False)
-    b = trimmed_mean(base1 + base2[10:], warm=10)
-    wv = trimmed_mean(withs, warm=10)
+    sweep = []
+    for ratio in ratios:
+        R = int(math.ceil(ratio * t_d2h / t_gemm))
+        log("overlap: ratio %.2f, R = %d GEMMs per step" % (ratio, R))
+        base1 = run(False, R, base_steps)
+        withs = run(True, R, steps)
+        base2 = run(False, R, base_steps)
+        b = trimmed_mean(base1 + base2[10:], warm=10)
+        wv = trimmed_mean(withs, warm=10)
+        sweep.append({"window_over_d2h": ratio, "R": R, "base_ms": round(b, 2), "with_snapshot_ms": round(wv, 2),
+                      "overhead_pct": round(100 * (wv - b) / b, 3),
+                      "floor_pct": round(100 * max(0.0, t_d2h - R * t_gemm) / b, 3)})
     ck.close()
     del tensors, x, w
     torch.cuda.empty_cache()
-    return {"workload": W.WORKLOADS[wid]["name"], "payload_bytes": sum(p[1] for p in plan), "gemm_mkn": [M, K, N],
-            "gemm_ms": round(t_gemm, 4), "d2h_ms": round(t_d2h, 2), "R": R, "steps": steps,
-            "base_ms": round(b, 2), "with_snapshot_ms": round(wv, 2), "overhead_pct": round(100 * (wv - b) / b, 3),
-            "statistic": "mean after dropping 10 warm-up steps and the slowest 5%"}
+    head = sweep[0]
+    out = {"workload": W.WORKLOADS[wid]["name"], "payload_bytes": sum(p[1] for p in plan), "gemm_mkn": [M, K, N],
+           "host_images": "pageable, %d-byte pinned bounce rings" % bounce if bounce else "pinned",
+           "gemm_ms": round(t_gemm, 4), "d2h_ms": round(t_d2h, 2), "R": head["R"], "steps": steps,
+           "base_steps": base_steps, "base_ms": head["base_ms"], "with_snapshot_ms": head["with_snapshot_ms"],
+           "overhead_pct": head["overhead_pct"],
+           "statistic": "mean after dropping 10 warm-up steps and the slowest 5%"}
+    if len(sweep) > 1:
+        out["sweep"] = sweep
+    return out
 
 
 def pmc_run(torch, P, W):
@@ -381,6 +419,14 @@ def main():
     if args.pmc_run:
         pmc_run(torch, P, W)
         return
+    ratios = [float(r) for r in args.overlap_ratios.split(",") if r]
+    if args.overlap_only:
+        log("link peak")
+        link = link_peak(torch)
+        ov = overlap_leg(torch, P, W, args.overlap_workload, args.overlap_steps, link["d2h"], ratios,
+                         args.overlap_base_steps, args.bounce_bytes, args.host_threads)
+        print(json.dumps({"overlap": ov, "d2h_link_peak_GBps": round(link["d2h"], 2)}), flush=True)
+        return
     wid = args.workload
     wl = W.WORKLOADS[wid]
     log("link peak")
@@ -392,7 +438,8 @@ def main():
     torch.cuda.synchronize()
     S = sum(p[1] for p in plan)
     n = len(tensors)
-    ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=wl["chunk"])
+    ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=wl["chunk"],
+                        bounce_bytes=args.bounce_bytes, host_threads=args.host_threads)
     P.ckpt_set_timing(ck.ctx, True)
 
     prev = [None]
@@ -464,7 +511,8 @@ def main():
     overlap = None
     if not args.no_overlap:
         log("overlap leg")
-        overlap = overlap_leg(torch, P, W, args.overlap_workload, args.overlap_steps, link["d2h"])
+        overlap = overlap_leg(torch, P, W, args.overlap_workload, args.overlap_steps, link["d2h"], ratios,
+                              args.overlap_base_steps, args.bounce_bytes, args.host_threads)
     try:
         sha = subprocess.run(["git", "rev-parse", "--short", "HEAD"], cwd=ROOT, capture_output=True,
                              text=True).stdout.strip() or None
@@ -477,6 +525,8 @@ def main():
         "config": {"workload": "%s shard: %d fragments, %d payload bytes, %d MiB chunks (snapshot + gate + restore "
                                "+ verify per step)" % (wl["name"], n, S, wl["chunk"] >> 20),
                    "payload_bytes": S, "image_bytes": int(sn["copy_bytes"]), "chunk_bytes": wl["chunk"],
+                   "host_images": ("pageable, %d-byte pinned bounce rings" % args.bounce_bytes
+                                   if args.bounce_bytes else "pinned"),
                    "parallelism": "one rank, one GPU"},
         "roofline": roofline,
         "cpu_baseline": cpu,

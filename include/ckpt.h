@@ -42,7 +42,8 @@
  *     void*; NULL means the device's null stream.
  *   - One host thread drives a context at a time; contexts are independent.
  *   - The library never allocates or frees the caller's tensors.  It owns
- *     its pinned host images, device staging, sums, events and streams, and
+ *     its host images (pinned, or pageable behind pinned bounce rings),
+ *     device staging, sums, events, streams and threads, and
  *     frees them in ckpt_destroy().
  */
 #ifndef CKPT_H
@@ -68,7 +69,7 @@ typedef int32_t ckpt_status;
 
 /* ckpt_wait modes */
 #define CKPT_WAIT_CAPTURED 0  /* stream-ordered: packed into device staging */
-#define CKPT_WAIT_COMMITTED 1 /* host-blocking: image and sums landed in pinned memory */
+#define CKPT_WAIT_COMMITTED 1 /* host-blocking: image and sums landed in host memory */
 
 /* ckpt_snapshot_state results */
 #define CKPT_SNAP_IN_FLIGHT 0
@@ -81,13 +82,22 @@ typedef struct ckpt_ctx ckpt_ctx;
 typedef struct {
     uint64_t chunk_bytes;          /* chunk size; 0 = 64 MiB.  Multiple of align_bytes. */
     uint32_t align_bytes;          /* fragment alignment in the image; 0 = 256.  Power of two, 16..4096. */
-    uint32_t host_buffers;         /* pinned host images; 0 = 2 (ping-pong).  Only 2 is accepted. */
+    uint32_t host_buffers;         /* host images; 0 = 2 (ping-pong).  Only 2 is accepted. */
     uint64_t device_staging_bytes; /* 0 = a full-size device image; otherwise a ring of chunk-sized
                                       slots of at most this many bytes (at least 2 chunks) */
     uint64_t group_bytes;          /* full-image mode: bytes packed per kernel launch and copied per
                                       DMA request; 0 = 1 GiB (rounded to whole chunks) */
     int32_t device;                /* HIP device ordinal */
     uint32_t grid_blocks;          /* cap on workgroups per kernel launch; 0 = one per 8 KiB tile */
+    uint64_t bounce_bytes;         /* 0 = the two host images are pinned and the DMA engines write
+                                      them directly.  > 0 = the images are ordinary pageable memory
+                                      (for states larger than the pinned memory the host grants):
+                                      DMA goes through two pinned rings of this many bytes each
+                                      (one per direction; whole chunk groups, at least two), and
+                                      host threads move every landed group between ring and image.
+                                      A snapshot then commits when its last group is in the image. */
+    uint32_t host_threads;         /* bounce mode: threads moving bytes between rings and images;
+                                      0 = 12 */
 } ckpt_config;
 
 typedef struct {
@@ -110,7 +120,8 @@ ckpt_status ckpt_destroy(ckpt_ctx* ctx);
  * layout (Sec. V-B: the state is packed into one contiguous buffer).  The
  * tensors stay owned by the caller and must stay allocated and unmoved while
  * the context lives.  Computes the layout, uploads the fragment and tile
- * tables, allocates device staging and two pinned host images.  Callable
+ * tables, allocates device staging and the two host images (pinned, or
+ * pageable plus the bounce rings; both pre-faulted).  Callable
  * once per context; a different layout needs a new context.
  * Errors: ESTATE (already registered), EINVAL (null pointer with nbytes > 0,
  * n == 0, or overlapping fragments are NOT checked), ENOMEM, EHIP. */
@@ -136,7 +147,7 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* ctx, void* after_stream, uint64_t step
  * snapshot snap_id has been packed, so the caller may overwrite those
  * fragments afterwards on `stream` (frag_hi above the fragment count is
  * clamped to it).  mode CKPT_WAIT_COMMITTED: blocks the
- * host until the snapshot's image and sums are in pinned memory (fragment
+ * host until the snapshot's image and sums are in host memory (fragment
  * range ignored).  Errors: ERANGE (unknown or expired snap_id), EINVAL,
  * ESTATE (COMMITTED on an aborted snapshot), EHIP. */
 ckpt_status ckpt_wait(ckpt_ctx* ctx, uint64_t snap_id, uint32_t mode, void* stream, uint32_t frag_lo,
@@ -176,7 +187,7 @@ ckpt_status ckpt_layout(ckpt_ctx* ctx, uint64_t* frag_off, uint64_t* image_bytes
 ckpt_status ckpt_chunk_fragments(ckpt_ctx* ctx, uint64_t c, uint64_t* byte_lo, uint64_t* byte_hi,
                                  uint32_t* frag_first, uint32_t* frag_last);
 
-/* Borrowed view of a snapshot's pinned host image and its stored sums (valid
+/* Borrowed view of a snapshot's host image and its stored sums (valid
  * until the buffer is reused or the context destroyed).  Writable: tests
  * inject bit flips through it.  Errors: ENOSNAP (not committed), ERANGE. */
 ckpt_status ckpt_host_image(ckpt_ctx* ctx, uint64_t snap_id, void** image, uint64_t* image_bytes,

@@ -42,7 +42,7 @@ _NAMES = {v: k for k, v in dict(globals()).items() if k.startswith("CKPT_E")}
 class ckpt_config(C.Structure):
     _fields_ = [("chunk_bytes", C.c_uint64), ("align_bytes", C.c_uint32), ("host_buffers", C.c_uint32),
                 ("device_staging_bytes", C.c_uint64), ("group_bytes", C.c_uint64), ("device", C.c_int32),
-                ("grid_blocks", C.c_uint32)]
+                ("grid_blocks", C.c_uint32), ("bounce_bytes", C.c_uint64), ("host_threads", C.c_uint32)]
 
 
 class ckpt_tensor(C.Structure):
@@ -126,10 +126,12 @@ def _u32p(a):
     return a.ctypes.data_as(C.POINTER(C.c_uint32))
 
 
-def ckpt_create(chunk_bytes=0, align_bytes=0, device_staging_bytes=0, group_bytes=0, device=None, grid_blocks=0):
+def ckpt_create(chunk_bytes=0, align_bytes=0, device_staging_bytes=0, group_bytes=0, device=None, grid_blocks=0,
+                bounce_bytes=0, host_threads=0):
     if device is None:
         device = torch.cuda.current_device()
-    cfg = ckpt_config(chunk_bytes, align_bytes, 0, device_staging_bytes, group_bytes, device, grid_blocks)
+    cfg = ckpt_config(chunk_bytes, align_bytes, 0, device_staging_bytes, group_bytes, device, grid_blocks,
+                      bounce_bytes, host_threads)
     ctx = C.c_void_p()
     rc = lib().ckpt_create(C.byref(cfg), C.byref(ctx))
     if rc != CKPT_OK:
@@ -312,9 +314,10 @@ class Checkpointer:
     """
 
     def __init__(self, tensors, dtypes=None, classes=None, chunk_bytes=0, align_bytes=0, device_staging_bytes=0,
-                 group_bytes=0, grid_blocks=0, device=None):
+                 group_bytes=0, grid_blocks=0, device=None, bounce_bytes=0, host_threads=0):
         self.tensors = list(tensors)
-        self.ctx = ckpt_create(chunk_bytes, align_bytes, device_staging_bytes, group_bytes, device, grid_blocks)
+        self.ctx = ckpt_create(chunk_bytes, align_bytes, device_staging_bytes, group_bytes, device, grid_blocks,
+                               bounce_bytes, host_threads)
         try:
             ckpt_register_tensors(self.ctx, self.tensors, dtypes, classes)
         except Exception:

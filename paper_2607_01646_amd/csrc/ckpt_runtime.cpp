@@ -35,11 +35,16 @@
 #include <hsa/hsa.h>
 #include <hsa/hsa_ext_amd.h>
 
+#include <sys/mman.h>
+
 #include <algorithm>
+#include <atomic>
 #include <chrono>
+#include <condition_variable>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <deque>
 #include <map>
 #include <mutex>
 #include <string>
@@ -64,6 +69,7 @@ constexpr uint32_t kMaxMeta = 1u << 20;
 constexpr uint32_t kDefaultGrid = 0x7fffffff; // one workgroup per tile unless capped
 constexpr int kMaxEngines = 2;
 constexpr uint64_t kVerifySlots = 2; // verify's device ring: two slots of one chunk group each
+constexpr uint32_t kDefaultHostThreads = 12; // bounce mode: host copy threads (measured: 8 do not keep up with the link)
 
 struct Frag {
     uint64_t ptr, nbytes, off;
@@ -83,11 +89,14 @@ struct RecRes {
     unsigned long long* d_sums = nullptr;
     std::vector<hipEvent_t> k0, k1;     // timing: around each pack launch
     hipEvent_t t0 = nullptr;
+    std::atomic<uint32_t> landed{0};    // bounce mode: groups moved from the ring into the image
+    std::atomic<bool> failed{false};    // bounce mode: a copy of this record could not be completed
 };
 
 struct SnapRec {
     uint64_t id = 0, step = 0;
     int buf = -1;
+    bool bounce = false;    // the image is pageable; groups land through the bounce ring
     bool aborted = false;
     bool committed = false; // cached once `done` has reached 0
     bool timed = false;
@@ -99,6 +108,126 @@ struct SnapRec {
 struct OpTiming {
     bool valid = false;
     ckpt_timing t{};
+};
+
+// Host threads that copy between host buffers in parallel (bounce mode).
+// copy() cuts one copy into parts, queues all but the first, runs the
+// first itself, and returns when every part is done; several threads may
+// call it at once.
+class CopyPool {
+public:
+    explicit CopyPool(unsigned n) : n_(std::max(1u, n))
+    {
+        for (unsigned k = 0; k + 1 < n_; ++k) th_.emplace_back([this] { work(); });
+    }
+    ~CopyPool()
+    {
+        {
+            std::lock_guard<std::mutex> l(m_);
+            stop_ = true;
+        }
+        cv_.notify_all();
+        for (auto& t : th_) t.join();
+    }
+    void copy(uint8_t* dst, const uint8_t* src, uint64_t n)
+    {
+        const uint64_t min_part = 4ull << 20;
+        uint64_t parts = std::min<uint64_t>(n_, std::max<uint64_t>(1, n / min_part));
+        if (parts <= 1) {
+            std::memcpy(dst, src, n);
+            return;
+        }
+        const uint64_t per = (n / parts + 4095) & ~4095ull;
+        Batch b;
+        b.left = 0;
+        {
+            std::lock_guard<std::mutex> l(m_);
+            for (uint64_t k = 1; k < parts; ++k) {
+                const uint64_t lo = std::min(k * per, n), hi = std::min(lo + per, n);
+                if (hi <= lo) continue;
+                q_.push_back(Part{dst + lo, src + lo, hi - lo, &b});
+                ++b.left;
+            }
+        }
+        cv_.notify_all();
+        std::memcpy(dst, src, std::min(per, n));
+        std::unique_lock<std::mutex> l(b.m);
+        b.cv.wait(l, [&] { return b.left == 0; });
+    }
+
+private:
+    struct Batch {
+        unsigned left;
+        std::mutex m;
+        std::condition_variable cv;
+    };
+    struct Part {
+        uint8_t* dst;
+        const uint8_t* src;
+        uint64_t n;
+        Batch* b;
+    };
+    void work()
+    {
+        for (;;) {
+            Part p;
+            {
+                std::unique_lock<std::mutex> l(m_);
+                cv_.wait(l, [&] { return stop_ || !q_.empty(); });
+                if (q_.empty()) return;
+                p = q_.front();
+                q_.pop_front();
+            }
+            std::memcpy(p.dst, p.src, p.n);
+            std::lock_guard<std::mutex> l(p.b->m);
+            if (--p.b->left == 0) p.b->cv.notify_all();
+        }
+    }
+    unsigned n_;
+    std::mutex m_;
+    std::condition_variable cv_;
+    std::deque<Part> q_;
+    bool stop_ = false;
+    std::vector<std::thread> th_;
+};
+
+// One group of a snapshot on its way through the bounce ring, or (sums)
+// the snapshot's chunk-sum copy, which follows its groups.
+struct PumpItem {
+    RecRes* res;
+    uint32_t g;
+    bool sums;               // the chunk sums: device -> pinned sums array, no ring slot
+    uint8_t* image;          // destination: pageable host image (group) or pinned sums array
+    const uint8_t* staging;  // source in device memory
+    uint64_t n;
+    uint64_t* area_done;     // group: device counter bumped once the staging area has been read
+    const uint64_t* seq;     // group: pinned, the value it is set to
+    hsa_amd_sdma_engine_id_t engine;
+};
+
+// Bounce-mode D2H (one per context).  The issuer takes snapshot groups in
+// order, waits for a free ring slot, and starts the DMA staging -> slot
+// (after the group's pack, through its dependency signal) followed by the
+// staging area's use-counter copy.  The drainer takes them in the same
+// order, waits for each DMA, copies slot -> image on the copy pool, frees
+// the slot and counts the group as landed.
+//
+// Every DMA of bounce mode is issued by the issuer, in snapshot and group
+// order.  Each engine runs its requests in order, and a request waiting for
+// a pack blocks the requests behind it; issuing the chunk-sum copy (which
+// waits for the last pack) ahead of group copies that earlier packs depend
+// on -- through the staging counters -- would stall the engine for good.
+struct Pump {
+    std::mutex m;
+    std::condition_variable cv;
+    std::deque<PumpItem> issue_q;
+    std::deque<std::pair<PumpItem, uint64_t>> drain_q;
+    std::vector<uint8_t> busy; // per ring slot
+    uint64_t next_slot = 0;
+    bool stop = false;
+    bool failed = false;
+    std::string err;
+    std::thread issuer, drainer;
 };
 
 } // namespace
@@ -165,6 +294,18 @@ struct ckpt_ctx {
     OpTiming op_timing[3];
     std::vector<hipEvent_t> tk0, tk1; // restore timing
     hipEvent_t tt0 = nullptr, tc0 = nullptr, tc1 = nullptr;
+
+    // bounce mode: pageable images behind two pinned rings of chunk groups
+    bool bounce = false;
+    uint64_t bounce_cfg = 0;
+    uint32_t host_threads = kDefaultHostThreads;
+    uint64_t n_bslots = 0;            // slots per ring
+    uint64_t img_map_bytes = 0;       // mapped length of each pageable image
+    uint8_t* h_bout = nullptr;        // device -> host ring
+    uint8_t* h_bin = nullptr;         // host -> device ring
+    std::vector<hipEvent_t> bin_done; // per host -> device slot: its last copy to the device finished
+    CopyPool* pool = nullptr;
+    Pump* pump = nullptr;
 
     // verify: its own ring of chunk slots and streams
     uint8_t* d_vring = nullptr;
@@ -329,14 +470,14 @@ ckpt_status setup_hsa(ckpt_ctx* c)
     return CKPT_OK;
 }
 
-// Owner agent of a pinned host image, and the engines for copies from the
-// device into it.
-ckpt_status setup_image_agent(ckpt_ctx* c, int b)
+// Owner agent of the pinned memory the engines write for image b (the image
+// itself, or the bounce ring), and the engines for copies from the device.
+ckpt_status setup_image_agent(ckpt_ctx* c, int b, const void* pinned)
 {
     hsa_amd_pointer_info_t info;
     std::memset(&info, 0, sizeof info);
     info.size = sizeof info;
-    HSACHK(c, hsa_amd_pointer_info(c->h_img[b], &info, nullptr, nullptr, nullptr));
+    HSACHK(c, hsa_amd_pointer_info(const_cast<void*>(pinned), &info, nullptr, nullptr, nullptr));
     c->img_agent[b] = info.agentOwner;
     hsa_device_type_t type = HSA_DEVICE_TYPE_GPU;
     if (info.agentOwner.handle) hsa_agent_get_info(info.agentOwner, HSA_AGENT_INFO_DEVICE, &type);
@@ -468,7 +609,16 @@ bool copies_done(const SnapRec& r)
     if (hsa_signal_load_scacquire(r.res->done) != 0) return false;
     for (uint32_t g = 0; g < r.groups_copied; ++g)
         if (hsa_signal_load_scacquire(r.res->flagged[g]) != 0) return false;
+    if (r.bounce && r.res->landed.load(std::memory_order_acquire) < r.groups_copied) return false;
     return true;
+}
+
+bool pump_failed(ckpt_ctx* c, std::string* why)
+{
+    if (!c->pump) return false;
+    std::lock_guard<std::mutex> l(c->pump->m);
+    if (why) *why = c->pump->err;
+    return c->pump->failed;
 }
 
 // Wait (bounded) until every copy of a snapshot has finished.
@@ -488,6 +638,16 @@ ckpt_status wait_copies(ckpt_ctx* c, SnapRec& r)
             std::this_thread::sleep_for(std::chrono::microseconds(20));
         }
     }
+    if (r.bounce) { // every group also has to reach the pageable image
+        while (r.res->landed.load(std::memory_order_acquire) < r.groups_copied) {
+            if (std::chrono::steady_clock::now() > deadline)
+                return fail(c, CKPT_EHIP, "snapshot %llu: image not written after 120 s", (unsigned long long)r.id);
+            std::this_thread::sleep_for(std::chrono::microseconds(50));
+        }
+        std::string why;
+        if (r.res->failed.load(std::memory_order_acquire) || pump_failed(c, &why))
+            return fail(c, CKPT_EHIP, "snapshot %llu: bounce copy failed: %s", (unsigned long long)r.id, why.c_str());
+    }
     return CKPT_OK;
 }
 
@@ -495,7 +655,13 @@ ckpt_status wait_copies(ckpt_ctx* c, SnapRec& r)
 bool query_committed(SnapRec& r)
 {
     if (r.aborted) return false;
-    if (!r.committed && copies_done(r)) r.committed = true;
+    if (!r.committed && copies_done(r)) {
+        if (r.res->failed.load(std::memory_order_acquire)) { // a group never reached the image
+            r.aborted = true;
+            return false;
+        }
+        r.committed = true;
+    }
     return r.committed;
 }
 
@@ -635,7 +801,15 @@ ckpt_status run_check(ckpt_ctx* c, uint64_t snap_id, hipStream_t stream, bool sc
         uint8_t* stage = L.ring ? L.base + area * unit : L.base + lo;
         HIPCHK(c, hipStreamWaitEvent(L.s_copy, (*L.area_free)[area], 0));
         if (timed && u == 0) HIPCHK(c, hipEventRecord(L.c0, L.s_copy));
-        HIPCHK(c, hipMemcpyAsync(stage, c->h_img[b] + lo, hi - lo, hipMemcpyHostToDevice, L.s_copy));
+        const uint8_t* src = c->h_img[b] + lo;
+        if (c->bounce) { // pageable image: through a pinned ring slot
+            const uint64_t slot = u % c->n_bslots;
+            if (u >= c->n_bslots) HIPCHK(c, hipEventSynchronize(c->bin_done[slot]));
+            c->pool->copy(c->h_bin + slot * unit, src, hi - lo);
+            src = c->h_bin + slot * unit;
+        }
+        HIPCHK(c, hipMemcpyAsync(stage, src, hi - lo, hipMemcpyHostToDevice, L.s_copy));
+        if (c->bounce) HIPCHK(c, hipEventRecord(c->bin_done[u % c->n_bslots], L.s_copy));
         if (timed && u + 1 == L.n_units) HIPCHK(c, hipEventRecord(L.c1, L.s_copy));
         HIPCHK(c, hipEventRecord((*L.loaded)[u], L.s_copy));
         HIPCHK(c, hipStreamWaitEvent(L.s_ker, (*L.loaded)[u], 0));
@@ -684,15 +858,20 @@ ckpt_status run_check(ckpt_ctx* c, uint64_t snap_id, hipStream_t stream, bool sc
     return CKPT_OK;
 }
 
+void stop_pump(ckpt_ctx* c);
+
 void free_ctx(ckpt_ctx* c)
 {
+    stop_pump(c);
+    delete c->pool;
+    c->pool = nullptr;
     for (auto& kv : c->recs) c->free_res.push_back(kv.second.res);
     c->recs.clear();
     for (auto r : c->free_res) destroy_res(r);
     c->free_res.clear();
     for (auto e : c->area_free) (void)hipEventDestroy(e);
     for (auto e : c->ev_loaded) (void)hipEventDestroy(e);
-    for (auto* v : {&c->tk0, &c->tk1, &c->vfree, &c->vloaded, &c->vk0, &c->vk1})
+    for (auto* v : {&c->tk0, &c->tk1, &c->vfree, &c->vloaded, &c->vk0, &c->vk1, &c->bin_done})
         for (auto e : *v) (void)hipEventDestroy(e);
     for (hipEvent_t e : {c->ev_trigger, c->ev_done, c->tt0, c->tc0, c->tc1, c->ev_vdone, c->vt0, c->vc0, c->vc1})
         if (e) (void)hipEventDestroy(e);
@@ -707,9 +886,12 @@ void free_ctx(ckpt_ctx* c)
     (void)hipFree(c->d_bad);
     (void)hipFree(c->d_area_done);
     for (int b = 0; b < 2; ++b) {
-        if (c->h_img[b]) (void)hipHostFree(c->h_img[b]);
+        if (c->h_img[b] && c->img_map_bytes) (void)munmap(c->h_img[b], c->img_map_bytes);
+        else if (c->h_img[b]) (void)hipHostFree(c->h_img[b]);
         if (c->h_sums[b]) (void)hipHostFree(c->h_sums[b]);
     }
+    if (c->h_bout) (void)hipHostFree(c->h_bout);
+    if (c->h_bin) (void)hipHostFree(c->h_bin);
     if (c->h_bad) (void)hipHostFree(c->h_bad);
     if (c->h_recomputed) (void)hipHostFree(c->h_recomputed);
     for (hipStream_t st : {c->s_pack, c->s_copy, c->s_vcopy, c->s_vker})
@@ -724,6 +906,145 @@ ckpt_status dma(ckpt_ctx* c, void* dst, hsa_agent_t dst_agent, const void* src, 
     HSACHK(c, hsa_amd_memory_async_copy_on_engine(dst, dst_agent, src, src_agent, n, dep ? 1 : 0, dep, completion,
                                                   engine, true));
     return CKPT_OK;
+}
+
+// Poll a signal that only the GPU side waits on until it reads 0.
+bool poll_zero(hsa_signal_t sig, int seconds)
+{
+    const auto deadline = std::chrono::steady_clock::now() + std::chrono::seconds(seconds);
+    while (hsa_signal_load_scacquire(sig) != 0) {
+        if (std::chrono::steady_clock::now() > deadline) return false;
+        std::this_thread::sleep_for(std::chrono::microseconds(20));
+    }
+    return true;
+}
+
+// Bounce mode, issuer thread (see Pump).
+void pump_issue(ckpt_ctx* c)
+{
+    Pump* p = c->pump;
+    const uint64_t unit = c->G * c->C;
+    for (;;) {
+        PumpItem it;
+        uint64_t slot = UINT64_MAX; // taken ring slot, if any
+        {
+            std::unique_lock<std::mutex> l(p->m);
+            p->cv.wait(l, [&] { return p->stop || !p->issue_q.empty(); });
+            if (p->issue_q.empty()) return;
+            it = p->issue_q.front();
+            p->issue_q.pop_front();
+            if (it.sums) {
+                // no ring slot: straight into the pinned sums array
+                bool ok = !p->failed;
+                l.unlock();
+                if (ok)
+                    ok = hsa_amd_memory_async_copy_on_engine(it.image, c->img_agent[0], it.staging, c->gpu_agent,
+                                                             it.n, 1, &it.res->dep_sums, it.res->done, it.engine,
+                                                             true) == HSA_STATUS_SUCCESS;
+                if (!ok) {
+                    hsa_signal_store_screlease(it.res->done, 0);
+                    it.res->failed.store(true, std::memory_order_release);
+                    l.lock();
+                    if (!p->failed) {
+                        p->failed = true;
+                        p->err = "DMA of the chunk sums could not be issued";
+                    }
+                }
+                continue;
+            }
+            const uint64_t s = p->next_slot % c->n_bslots;
+            p->cv.wait(l, [&] { return p->stop || p->failed || !p->busy[s]; });
+            if (!p->failed) {
+                if (p->busy[s]) return; // stopping
+                p->busy[s] = 1;
+                ++p->next_slot;
+                slot = s;
+            }
+        }
+        const char* what = nullptr;
+        bool issued = false, counted = false;
+        if (slot != UINT64_MAX) {
+            issued = hsa_amd_memory_async_copy_on_engine(c->h_bout + slot * unit, c->img_agent[0], it.staging,
+                                                         c->gpu_agent, it.n, 1, &it.res->dep[it.g],
+                                                         it.res->copied[it.g], it.engine, true) == HSA_STATUS_SUCCESS;
+            if (!issued) what = "DMA of a chunk group to the bounce ring could not be issued";
+            else
+                counted = hsa_amd_memory_async_copy_on_engine(it.area_done, c->gpu_agent, it.seq, c->img_agent[0], 8, 1,
+                                                              &it.res->copied[it.g], it.res->flagged[it.g],
+                                                              c->h2d_engine, true) == HSA_STATUS_SUCCESS;
+            if (issued && !counted) what = "staging counter copy could not be issued";
+        }
+        if (!issued) hsa_signal_store_screlease(it.res->copied[it.g], 0);
+        if (!counted) {
+            // Nothing bumps the staging area's use counter through the
+            // engines: once no copy reads the area, write it directly, so
+            // that no later pack waits for it forever.
+            if (!issued || poll_zero(it.res->copied[it.g], 120)) (void)hsa_memory_copy(it.area_done, it.seq, 8);
+            hsa_signal_store_screlease(it.res->flagged[it.g], 0);
+        }
+        std::lock_guard<std::mutex> l(p->m);
+        if (what && !p->failed) {
+            p->failed = true;
+            p->err = what;
+        }
+        if (!counted) it.res->failed.store(true, std::memory_order_release);
+        if (slot != UINT64_MAX && !issued) {
+            p->busy[slot] = 0;
+            slot = UINT64_MAX;
+        }
+        p->drain_q.emplace_back(it, slot);
+        p->cv.notify_all();
+    }
+}
+
+// Bounce mode, drainer thread (see Pump).
+void pump_drain(ckpt_ctx* c)
+{
+    Pump* p = c->pump;
+    const uint64_t unit = c->G * c->C;
+    for (;;) {
+        std::pair<PumpItem, uint64_t> d;
+        {
+            std::unique_lock<std::mutex> l(p->m);
+            p->cv.wait(l, [&] { return p->stop || !p->drain_q.empty(); });
+            if (p->drain_q.empty()) return;
+            d = p->drain_q.front();
+            p->drain_q.pop_front();
+        }
+        const PumpItem& it = d.first;
+        const uint64_t slot = d.second;
+        bool free_slot = slot != UINT64_MAX, ok = free_slot;
+        if (ok) {
+            ok = poll_zero(it.res->copied[it.g], 120);
+            if (ok) c->pool->copy(it.image, c->h_bout + slot * unit, it.n);
+            else free_slot = false; // the engine may still write it
+        }
+        {
+            std::lock_guard<std::mutex> l(p->m);
+            if (free_slot) p->busy[slot] = 0;
+            if (slot != UINT64_MAX && !ok && !p->failed) {
+                p->failed = true;
+                p->err = "DMA of a chunk group to the bounce ring did not finish within 120 s";
+            }
+            p->cv.notify_all();
+        }
+        if (!ok) it.res->failed.store(true, std::memory_order_release);
+        it.res->landed.fetch_add(1, std::memory_order_acq_rel);
+    }
+}
+
+void stop_pump(ckpt_ctx* c)
+{
+    if (!c->pump) return;
+    {
+        std::lock_guard<std::mutex> l(c->pump->m);
+        c->pump->stop = true;
+    }
+    c->pump->cv.notify_all();
+    if (c->pump->issuer.joinable()) c->pump->issuer.join();
+    if (c->pump->drainer.joinable()) c->pump->drainer.join();
+    delete c->pump;
+    c->pump = nullptr;
 }
 
 ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop);
@@ -743,6 +1064,8 @@ ckpt_status ckpt_create(const ckpt_config* cfg, ckpt_ctx** out)
     if (!geometry_ok(C, A)) return CKPT_EINVAL;
     if (d.host_buffers != 0 && d.host_buffers != 2) return CKPT_EINVAL;
     if (d.device_staging_bytes && d.device_staging_bytes < 2 * C) return CKPT_EINVAL;
+    if (d.bounce_bytes && d.bounce_bytes < 2 * C) return CKPT_EINVAL;
+    if (d.host_threads > 256) return CKPT_EINVAL;
     int ndev = 0;
     if (hipGetDeviceCount(&ndev) != hipSuccess || d.device < 0 || d.device >= ndev) return CKPT_EINVAL;
     ckpt_ctx* c = new ckpt_ctx();
@@ -752,6 +1075,8 @@ ckpt_status ckpt_create(const ckpt_config* cfg, ckpt_ctx** out)
     c->staging_cap = d.device_staging_bytes;
     c->group_cfg = d.group_bytes ? d.group_bytes : kDefaultGroup;
     c->grid_cap = d.grid_blocks ? d.grid_blocks : kDefaultGrid;
+    c->bounce_cfg = d.bounce_bytes;
+    c->host_threads = d.host_threads ? d.host_threads : kDefaultHostThreads;
     ckpt_status st = CKPT_OK;
     if (hipSetDevice(c->device) != hipSuccess)
         st = CKPT_EHIP;
@@ -824,6 +1149,14 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
         c->G = std::max<uint64_t>(1, c->group_cfg / c->C);
     }
     c->n_groups = (c->n_chunks + c->G - 1) / c->G;
+    const uint64_t unit = c->G * c->C; // bytes of one chunk group
+    if (c->bounce_cfg) {
+        if (c->bounce_cfg / unit < 2)
+            return fail(c, CKPT_EINVAL, "bounce ring of %llu bytes holds fewer than two chunk groups of %llu bytes",
+                        (unsigned long long)c->bounce_cfg, (unsigned long long)unit);
+        c->bounce = true;
+        c->n_bslots = std::min<uint64_t>(c->bounce_cfg / unit, std::max<uint64_t>(2, c->n_groups));
+    }
 
     std::vector<FragDev> fd(n);
     for (uint32_t i = 0; i < n; ++i) {
@@ -859,8 +1192,24 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
     HIPCHK(c, hipMemcpy(c->d_tile_last, pl.tile_last.data(), nt * 4, hipMemcpyHostToDevice));
     HIPCHK(c, hipMemset(c->d_area_done, 0, n_areas * 8));
     c->area_seq.assign(n_areas, 0);
+    if (c->bounce) {
+        for (uint8_t** ring : {&c->h_bout, &c->h_bin}) {
+            if (hipHostMalloc((void**)ring, c->n_bslots * unit, hipHostMallocDefault) != hipSuccess) {
+                *ring = nullptr;
+                return fail(c, CKPT_ENOMEM, "pinned bounce ring of %llu bytes", (unsigned long long)(c->n_bslots * unit));
+            }
+            parallel_zero(*ring, c->n_bslots * unit);
+        }
+        c->img_map_bytes = round_up(c->I, 2ull << 20);
+    }
     for (int b = 0; b < 2; ++b) {
-        if (hipHostMalloc((void**)&c->h_img[b], c->I, hipHostMallocDefault) != hipSuccess) {
+        if (c->bounce) {
+            void* m = mmap(nullptr, c->img_map_bytes, PROT_READ | PROT_WRITE, MAP_PRIVATE | MAP_ANONYMOUS, -1, 0);
+            if (m == MAP_FAILED)
+                return fail(c, CKPT_ENOMEM, "host image of %llu bytes", (unsigned long long)c->img_map_bytes);
+            c->h_img[b] = (uint8_t*)m;
+            (void)madvise(m, c->img_map_bytes, MADV_HUGEPAGE);
+        } else if (hipHostMalloc((void**)&c->h_img[b], c->I, hipHostMallocDefault) != hipSuccess) {
             c->h_img[b] = nullptr;
             return fail(c, CKPT_ENOMEM, "pinned host image of %llu bytes", (unsigned long long)c->I);
         }
@@ -869,7 +1218,7 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
             c->h_sums[b] = nullptr;
             return fail(c, CKPT_ENOMEM, "pinned sums");
         }
-        ckpt_status st = setup_image_agent(c, b);
+        ckpt_status st = setup_image_agent(c, b, c->bounce ? (const void*)c->h_bout : (const void*)c->h_img[b]);
         if (st) return st;
     }
     if (hipHostMalloc((void**)&c->h_bad, c->n_chunks, hipHostMallocDefault) != hipSuccess ||
@@ -904,6 +1253,18 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
         if (!st) st = make_event(c, &c->vk0[k], true);
         if (!st) st = make_event(c, &c->vk1[k], true);
         if (st) return st;
+    }
+    if (c->bounce) {
+        c->bin_done.resize(c->n_bslots, nullptr);
+        for (auto& e : c->bin_done) {
+            ckpt_status st = make_event(c, &e, false);
+            if (st) return st;
+        }
+        c->pool = new CopyPool(c->host_threads);
+        c->pump = new Pump();
+        c->pump->busy.assign(c->n_bslots, 0);
+        c->pump->issuer = std::thread(pump_issue, c);
+        c->pump->drainer = std::thread(pump_drain, c);
     }
     HIPCHK(c, hipDeviceSynchronize());
     c->registered = true;
@@ -954,6 +1315,9 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
     }
     r.meta.assign((const uint8_t*)meta, (const uint8_t*)meta + meta_len);
     r.timed = c->timing;
+    r.bounce = c->bounce;
+    res->landed.store(0, std::memory_order_relaxed);
+    res->failed.store(false, std::memory_order_relaxed);
     c->holder[r.buf] = id;
     const int32_t stop = c->interrupt_next;
     c->interrupt_next = -1;
@@ -1016,8 +1380,18 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
         e = launch_release(res->dep_val[g], c->s_pack);
         if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
         const hsa_amd_sdma_engine_id_t eng = c->d2h_engine[g % c->n_d2h_engines];
-        st = dma(c, himg + lo, host, staging_of(c, g), c->gpu_agent, hi - lo, &res->dep[g], res->copied[g], eng);
         res->h_seq[g] = c->area_seq[area] + 1;
+        if (r.bounce) { // the pump issues the copies once a ring slot is free
+            {
+                std::lock_guard<std::mutex> l(c->pump->m);
+                c->pump->issue_q.push_back(PumpItem{res, (uint32_t)g, false, himg + lo, staging_of(c, g), hi - lo,
+                                                    c->d_area_done + area, &res->h_seq[g], eng});
+            }
+            c->pump->cv.notify_all();
+            ++c->area_seq[area];
+            continue;
+        }
+        st = dma(c, himg + lo, host, staging_of(c, g), c->gpu_agent, hi - lo, &res->dep[g], res->copied[g], eng);
         if (!st)
             st = dma(c, c->d_area_done + area, c->gpu_agent, &res->h_seq[g], host, 8, &res->copied[g],
                      res->flagged[g], c->h2d_engine);
@@ -1037,6 +1411,16 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
         hipError_t e = launch_release(res->dep_sums_val, c->s_pack);
         if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
         hsa_signal_store_screlease(res->done, 1);
+        if (r.bounce) { // behind the snapshot's group copies
+            {
+                std::lock_guard<std::mutex> l(c->pump->m);
+                c->pump->issue_q.push_back(PumpItem{res, 0, true, (uint8_t*)c->h_sums[r.buf],
+                                                    (const uint8_t*)res->d_sums, c->n_chunks * 8, nullptr, nullptr,
+                                                    c->d2h_engine[0]});
+            }
+            c->pump->cv.notify_all();
+            return CKPT_OK;
+        }
         st = dma(c, c->h_sums[r.buf], host, res->d_sums, c->gpu_agent, c->n_chunks * 8, &res->dep_sums, res->done,
                  c->d2h_engine[0]);
         if (st) {

@@ -1,6 +1,11 @@
-"""Shared helpers of the GPU tests (inputs and host copies only)."""
+"""Shared helpers of the GPU tests: inputs, host copies, and the
+snapshot -> oracle -> restore check used across geometries."""
 import numpy as np
 import torch
+
+import oracle as O
+
+EDGE_SIZES = [1, 2, 3, 15, 16, 17, 255, 256, 257, 0, 4095, 4096, 4097, 100_003, 0, 0, 65536, 65537, 1 << 20, 7]
 
 
 def host_bytes(t):
@@ -22,3 +27,34 @@ def garbage_fill(tensors, value=0x5A):
     for t in tensors:
         if t.numel():
             t.view(-1).view(torch.uint8).fill_(value) if t.dtype != torch.uint8 else t.fill_(value)
+
+
+def snapshot_and_check(tensors, host, chunk, align=256, staging=0, group=0, dtypes=None, classes=None,
+                       meta=b"", step=3, grid=0, bounce=0, threads=0):
+    """Snapshot, compare image and sums with the oracle, trash the tensors,
+    restore and compare them; returns the Checkpointer and snapshot id."""
+    import paper_2607_01646_amd as P
+
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=chunk, align_bytes=align,
+                        device_staging_bytes=staging, group_bytes=group, grid_blocks=grid, bounce_bytes=bounce,
+                        host_threads=threads)
+    snap = ck.snapshot(step=step, meta=meta)
+    ck.wait_committed(snap)
+    assert ck.state(snap) == P.CKPT_SNAP_COMMITTED
+    img, sums = ck.host_image(snap)
+    want, off, nc = O.pack(host, align, chunk)
+    assert np.array_equal(ck.offsets, off)
+    assert (ck.image_bytes, ck.n_chunks) == (want.size, nc)
+    assert img.size == want.size
+    diff = np.flatnonzero(img != want)
+    assert diff.size == 0, "image differs at %d bytes, first at %d" % (diff.size, diff[0])
+    want_sums = O.chunk_sums(want, 0, want.size, chunk)
+    assert np.array_equal(sums, want_sums)
+    assert ck.verify(snap) == []
+    garbage_fill(tensors)
+    assert ck.restore(snap) == []
+    torch.cuda.synchronize()
+    for i, (t, h) in enumerate(zip(tensors, host)):
+        assert np.array_equal(host_bytes(t), h), "fragment %d not restored" % i
+    assert np.array_equal(P.ckpt_last_sums(ck.ctx), want_sums)
+    return ck, snap

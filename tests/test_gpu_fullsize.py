@@ -50,14 +50,14 @@ def oracle_window(tensors, off, sizes, lo, hi):
     return O.pack_window(frags, offs, lo, hi)
 
 
-def check_shard(wid, staging=0, full_restore=True, all_sums=True):
+def check_shard(wid, staging=0, full_restore=True, all_sums=True, bounce=0):
     tensors, plan = W.make_state(wid, device="cuda")
     sizes = [p[1] for p in plan]
     chunk = W.WORKLOADS[wid]["chunk"]
     torch.cuda.synchronize()
     before = [t.clone() for t in tensors] if full_restore else None
     ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=chunk,
-                        device_staging_bytes=staging)
+                        device_staging_bytes=staging, bounce_bytes=bounce)
     off, I, nc = O.layout(sizes, 256, chunk)
     assert np.array_equal(ck.offsets, off) and (ck.image_bytes, ck.n_chunks) == (I, nc)
     snap = ck.snapshot(step=wid)

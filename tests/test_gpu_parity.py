@@ -13,43 +13,12 @@ import torch
 
 import oracle as O
 import workloads as W
-from gpu_util import garbage_fill, host_bytes, random_byte_fragments
+from gpu_util import EDGE_SIZES, garbage_fill, host_bytes, random_byte_fragments, snapshot_and_check
 
 pytestmark = pytest.mark.gpu
 
 if torch.cuda.is_available():
     import paper_2607_01646_amd as P
-
-
-def snapshot_and_check(tensors, host, chunk, align=256, staging=0, group=0, dtypes=None, classes=None,
-                       meta=b"", step=3, grid=0):
-    """Snapshot, compare image and sums with the oracle, trash the tensors,
-    restore and compare them; returns the Checkpointer and snapshot id."""
-    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=chunk, align_bytes=align,
-                        device_staging_bytes=staging, group_bytes=group, grid_blocks=grid)
-    snap = ck.snapshot(step=step, meta=meta)
-    ck.wait_committed(snap)
-    assert ck.state(snap) == P.CKPT_SNAP_COMMITTED
-    img, sums = ck.host_image(snap)
-    want, off, nc = O.pack(host, align, chunk)
-    assert np.array_equal(ck.offsets, off)
-    assert (ck.image_bytes, ck.n_chunks) == (want.size, nc)
-    assert img.size == want.size
-    diff = np.flatnonzero(img != want)
-    assert diff.size == 0, "image differs at %d bytes, first at %d" % (diff.size, diff[0])
-    want_sums = O.chunk_sums(want, 0, want.size, chunk)
-    assert np.array_equal(sums, want_sums)
-    assert ck.verify(snap) == []
-    garbage_fill(tensors)
-    assert ck.restore(snap) == []
-    torch.cuda.synchronize()
-    for i, (t, h) in enumerate(zip(tensors, host)):
-        assert np.array_equal(host_bytes(t), h), "fragment %d not restored" % i
-    assert np.array_equal(P.ckpt_last_sums(ck.ctx), want_sums)
-    return ck, snap
-
-
-EDGE_SIZES = [1, 2, 3, 15, 16, 17, 255, 256, 257, 0, 4095, 4096, 4097, 100_003, 0, 0, 65536, 65537, 1 << 20, 7]
 
 
 @pytest.mark.parametrize("chunk,align,staging,group", [
