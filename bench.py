@@ -64,6 +64,9 @@ def parse():
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarize two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of --pmc-run")
     ap.add_argument("--stats-summary", metavar="DIR", help="summarize a rocprofv3 --kernel-trace --stats run")
+    ap.add_argument("--gemm-inflation", metavar="DIR",
+                    help="summarize GEMM durations of a rocprofv3 --kernel-trace --memory-copy-trace run of the "
+                         "overlap leg: beside a pack launch, beside a D2H copy, and alone")
     ap.add_argument("--command", default="", help="command line recorded in a summary")
     ap.add_argument("--bench-json", default="", help="with --stats-summary: the JSON line bench.py printed in that run")
     return ap.parse_args()
@@ -176,6 +179,57 @@ def stats_summary(d, command):
     return "\n".join(lines)
 
 
+def gemm_inflation(d, command):
+    """GEMM dispatch durations of an overlap run, split by what ran beside
+    them: a pack launch of the library, a device-to-host copy, or neither."""
+    import bisect
+    import csv
+    import glob
+    import statistics
+
+    kt = glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True)
+    mt = glob.glob(os.path.join(d, "**", "*memory_copy_trace.csv"), recursive=True)
+    gemms, packs, copies = [], [], []
+    for f in kt:
+        for r in csv.DictReader(open(f)):
+            a, b, n = int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"]
+            if PACK_KERNEL in n:
+                packs.append((a, b))
+            elif "Cijk" in n or "gemm" in n.lower():
+                gemms.append((a, b))
+    for f in mt:
+        for r in csv.DictReader(open(f)):
+            kind = " ".join(str(v) for k, v in r.items() if k and ("Direction" in k or "Kind" in k))
+            if "DEVICE_TO_HOST" in kind:
+                copies.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+
+    def overlaps(iv, lst, starts):
+        k = bisect.bisect_left(starts, iv[1])  # intervals starting before the GEMM ends
+        for j in range(max(0, k - 64), k):
+            if lst[j][1] > iv[0]:
+                return True
+        return False
+
+    packs.sort()
+    copies.sort()
+    ps, cs = [p[0] for p in packs], [c[0] for c in copies]
+    groups = {"beside_pack": [], "beside_d2h": [], "alone": []}
+    for g in gemms:
+        key = "beside_pack" if overlaps(g, packs, ps) else "beside_d2h" if overlaps(g, copies, cs) else "alone"
+        groups[key].append((g[1] - g[0]) / 1e3)
+    base = statistics.median(groups["alone"]) if groups["alone"] else float("nan")
+    lines = ["# GEMM durations under snapshots (rocprofv3 kernel + memory-copy trace)", "",
+             "command: `%s`" % command, "",
+             "%d GEMM dispatches, %d pack launches, %d device-to-host copies in the trace." % (
+                 len(gemms), len(packs), len(copies)), "",
+             "| GEMMs | count | median (us) | mean (us) | median vs alone |", "|---|---|---|---|---|"]
+    for k, v in groups.items():
+        if v:
+            lines.append("| %s | %d | %.1f | %.1f | %+.2f%% |" % (k, len(v), statistics.median(v), statistics.mean(v),
+                                                                  100 * (statistics.median(v) / base - 1)))
+    return "\n".join(lines)
+
+
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
@@ -234,10 +288,14 @@ def hbm_copy_ceiling(torch):
     return 2 * n / best / 1e6
 
 
-def cpu_baseline(tensors, plan, chunk, target_bytes):
-    """The oracle, single-threaded, on the first fragments of the shard up to
+def cpu_baseline(tensors, plan, chunk, target_bytes, threads=16):
+    """The oracle as it stands, on the first fragments of the shard up to
     target_bytes: pack + chunk sums + restore + verify (the same cycle as one
-    GPU step, minus the host-link copies, which a CPU does not need)."""
+    GPU step, minus the host-link copies, which a CPU does not need).  Timed
+    on one thread, then with the image split by whole chunks over `threads`
+    threads (the oracle's C calls run outside the interpreter lock)."""
+    from concurrent.futures import ThreadPoolExecutor
+
     import numpy as np
     import torch
 
@@ -252,16 +310,37 @@ def cpu_baseline(tensors, plan, chunk, target_bytes):
         total += nb
     sizes = [f.size for f in frags]
     O.lib()
+    off, I, nc = O.layout(sizes, 256, chunk)
+
+    def cycle(lo, hi):
+        t0 = time.perf_counter()
+        win = O.pack_window(frags, off, lo, hi)
+        sums = O.chunk_sums(win, lo, hi, chunk)
+        t1 = time.perf_counter()
+        back = O.restore_window(win, lo, hi, off, sizes)
+        bad = O.verify(win, lo, hi, chunk, sums)
+        t2 = time.perf_counter()
+        return t1 - t0, t2 - t1, bad, back
+
     t0 = time.perf_counter()
-    img, off, nc = O.pack(frags, 256, chunk)
-    sums = O.chunk_sums(img, 0, img.size, chunk)
-    back = O.restore_window(img, 0, img.size, off, sizes)
-    bad = O.verify(img, 0, img.size, chunk, sums)
-    dt = time.perf_counter() - t0
+    t_pack, t_rest, bad, back = cycle(0, I)
+    dt1 = time.perf_counter() - t0
     assert bad == [] and all(np.array_equal(a, b) for a, b in zip(frags[:3], back[:3]))
-    return {"value": round(total / dt / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+    del back
+    nthr = max(1, min(threads, os.cpu_count() or 1))
+    per = (nc + nthr - 1) // nthr
+    parts = [(k * per * chunk, min((k + 1) * per * chunk, I)) for k in range(nthr) if k * per * chunk < I]
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(nthr) as ex:
+        res = list(ex.map(lambda r: cycle(*r)[2], parts))
+    dtn = time.perf_counter() - t0
+    assert all(r == [] for r in res)
+    return {"value": round(total / dt1 / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": "first %d of %d fragments of the shard (%d bytes, %d chunks of %d MiB): pack + chunk sums "
-                      "+ restore + verify, one thread, %.1f s" % (len(frags), len(tensors), total, nc, chunk >> 20, dt)}
+                      "+ restore + verify, one thread, %.1f s" % (len(frags), len(tensors), total, nc, chunk >> 20, dt1),
+            "pack_checksum_GBps": round(2 * total / t_pack / 1e9, 3), "restore_verify_GBps": round(total / t_rest / 1e9, 3),
+            "parallel": {"value": round(total / dtn / 1e9, 3), "cores": len(parts),
+                         "split": "whole chunks, %d per thread" % per, "seconds": round(dtn, 2)}}
 
 
 def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_steps=0, bounce=0, threads=0):
@@ -389,6 +468,9 @@ def main():
         out = args.traffic
         write_summary(out, d, header)
         print(open(out).read())
+        return
+    if args.gemm_inflation:
+        print(gemm_inflation(args.gemm_inflation, args.command))
         return
     if args.stats_summary:
         print("# rocprofv3 --kernel-trace --memory-copy-trace --stats\n\ncommand: `%s`\n" % args.command)
