@@ -213,7 +213,7 @@ ckpt_status ckpt_debug_interrupt_next(ckpt_ctx* ctx, int32_t groups);
 /* GPU timing of the last operation of each kind, from HIP events recorded
  * on the library's own streams (enable with ckpt_set_timing(ctx, 1) before
  * the operation; timing adds one event pair per kernel launch and per copy
- * request).  which: 0 = snapshot, 1 = restore, 2 = verify.
+ * request).  which: 0 = snapshot, 1 = restore, 2 = verify, 3 = pack only.
  * Errors: EINVAL (bad `which`), ESTATE (no timed operation of that kind). */
 typedef struct {
     float kernel_ms;     /* sum of the tile-kernel launches' durations (pack, scatter or
@@ -230,6 +230,8 @@ typedef struct {
 #define CKPT_OP_SNAPSHOT 0
 #define CKPT_OP_RESTORE 1
 #define CKPT_OP_VERIFY 2
+#define CKPT_OP_PACK 3 /* the pack launches alone of the newest timed snapshot, committed or not
+                          (an interrupted one included); waits for its pack; copies = 0 */
 ckpt_status ckpt_set_timing(ckpt_ctx* ctx, int32_t enable);
 ckpt_status ckpt_last_timing(ckpt_ctx* ctx, uint32_t which, ckpt_timing* out);
 

@@ -35,6 +35,7 @@ CKPT_SNAP_SUPERSEDED = 3
 CKPT_OP_SNAPSHOT = 0
 CKPT_OP_RESTORE = 1
 CKPT_OP_VERIFY = 2
+CKPT_OP_PACK = 3
 
 _NAMES = {v: k for k, v in dict(globals()).items() if k.startswith("CKPT_E")}
 

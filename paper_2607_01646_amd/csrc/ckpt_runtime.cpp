@@ -1327,8 +1327,7 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
     // just before its copy is issued.
     hsa_signal_store_screlease(res->done, 0);
     r.groups_copied = 0;
-    if (r.timed && n_copy == 0) r.timed = false;
-    if (r.timed) hsa_amd_profiling_async_copy_enable(true);
+    if (r.timed && n_copy > 0) hsa_amd_profiling_async_copy_enable(true);
 
     // On an error below, copies not issued never raise their signals, and
     // the snapshot is marked interrupted.
@@ -1404,8 +1403,7 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
         ++c->area_seq[area];
     }
     if (stop >= 0) {
-        r.aborted = true; // interrupted offload: never committed
-        r.timed = false;
+        r.aborted = true; // interrupted offload: never committed (its pack timing stays readable)
     } else {
         hsa_signal_store_screlease(res->dep_sums, 1);
         hipError_t e = launch_release(res->dep_sums_val, c->s_pack);
@@ -1635,7 +1633,23 @@ ckpt_status ckpt_set_timing(ckpt_ctx* c, int32_t enable)
 
 ckpt_status ckpt_last_timing(ckpt_ctx* c, uint32_t which, ckpt_timing* out)
 {
-    if (!c || !out || which > CKPT_OP_VERIFY) return fail(c, CKPT_EINVAL, "bad timing query");
+    if (!c || !out || which > CKPT_OP_PACK) return fail(c, CKPT_EINVAL, "bad timing query");
+    if (which == CKPT_OP_PACK) {
+        SnapRec* best = nullptr; // newest timed snapshot, committed or not
+        for (auto& kv : c->recs)
+            if (kv.second.timed && (!best || kv.first > best->id)) best = &kv.second;
+        if (!best) return fail(c, CKPT_ESTATE, "no timed snapshot retained");
+        RecRes* r = best->res;
+        HIPCHK(c, hipEventSynchronize(r->k1[c->n_groups - 1])); // packs run in order on one stream
+        ckpt_timing t{};
+        for (uint64_t g = 0; g < c->n_groups; ++g) t.kernel_ms += elapsed(r->k0[g], r->k1[g]);
+        t.kernels = (uint32_t)c->n_groups;
+        t.copy_ms = -1.f;
+        t.total_ms = -1.f;
+        t.kernel_bytes = 2 * c->payload;
+        *out = t;
+        return CKPT_OK;
+    }
     if (which == CKPT_OP_SNAPSHOT) {
         SnapRec* best = nullptr; // newest timed, committed snapshot
         for (auto& kv : c->recs)
