@@ -56,6 +56,10 @@ def parse():
     ap.add_argument("--bounce-bytes", type=int, default=0,
                     help="pageable host images behind pinned bounce rings of this many bytes (0 = pinned images)")
     ap.add_argument("--host-threads", type=int, default=0, help="bounce mode: host copy threads (0 = library default)")
+    ap.add_argument("--h2h-only", action="store_true",
+                    help="run only the H2H replication leg (ring peer in this process, TCP over 127.0.0.1)")
+    ap.add_argument("--h2h-workload", type=int, default=3)
+    ap.add_argument("--h2h-steps", type=int, default=5)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-sample-bytes", type=int, default=10 << 30)
     ap.add_argument("--traffic", type=str, default=os.path.join(ROOT, "profiles", "pack_checksum_gpt1.3b_traffic.txt"),
@@ -440,6 +444,86 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
     return out
 
 
+def loopback_peak(nbytes=4 << 30, piece=256 << 20):
+    """One TCP stream over 127.0.0.1 with the library's socket settings: the
+    emulated network's own ceiling."""
+    import socket
+    import threading
+
+    ls = socket.socket(socket.AF_INET, socket.SOCK_STREAM)
+    ls.bind(("127.0.0.1", 0))
+    ls.listen(1)
+    tx = socket.create_connection(ls.getsockname())
+    rx, _ = ls.accept()
+    for s in (tx, rx):
+        s.setsockopt(socket.IPPROTO_TCP, socket.TCP_NODELAY, 1)
+        s.setsockopt(socket.SOL_SOCKET, socket.SO_SNDBUF, 16 << 20)
+        s.setsockopt(socket.SOL_SOCKET, socket.SO_RCVBUF, 16 << 20)
+    src = bytearray(piece)
+    dst = memoryview(bytearray(piece))
+
+    def send():
+        for _ in range(nbytes // piece):
+            tx.sendall(src)
+
+    t = threading.Thread(target=send)
+    t0 = time.perf_counter()
+    t.start()
+    got = 0
+    while got < nbytes:
+        k = rx.recv_into(dst[:min(piece, nbytes - got)])
+        if not k:
+            break
+        got += k
+    t.join()
+    dt = time.perf_counter() - t0
+    for s in (tx, rx, ls):
+        s.close()
+    return got / dt / 1e9
+
+
+def h2h_leg(torch, P, W, wid, steps):
+    """H2H replication (paper Sec. V-B): the optimizer-state chunks of each
+    snapshot go to a ring peer in this process over TCP on 127.0.0.1; the
+    peer re-checks every chunk sum on the GPU before it commits.  The state is
+    registered class-major so that the optimizer classes fill a run of chunks."""
+    tensors, plan = W.make_state(wid, device="cuda")
+    order = sorted(range(len(plan)), key=lambda i: (plan[i][3], i))
+    tensors = [tensors[i] for i in order]
+    dtypes, classes = [plan[i][2] for i in order], [plan[i][3] for i in order]
+    torch.cuda.synchronize()
+    mask = (1 << W.CLS_MASTER) | (1 << W.CLS_ADAM_M) | (1 << W.CLS_ADAM_V)
+    log("h2h: loopback peak")
+    loop = loopback_peak()
+    peer = P.Peer()
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=W.WORKLOADS[wid]["chunk"])
+    ck.replicate_to(peer.port, mask)
+    ids, rbytes = P.ckpt_replica_chunks(ck.ctx)
+    rows = []
+    for k in range(steps):
+        s = ck.snapshot(step=k)
+        ck.wait_replicated(s)
+        send_ms, ack_ms = P.ckpt_replica_timing(ck.ctx)
+        recv_ms, check_ms = peer.timing()
+        rows.append((send_ms, ack_ms, recv_ms, check_ms))
+        log("h2h: snapshot %d: sent in %.1f ms, acknowledged after %.1f ms (peer check %.1f ms)"
+            % (k, send_ms, ack_ms, check_ms))
+    ck.close()
+    peer.close()
+    del tensors
+    torch.cuda.empty_cache()
+    import statistics
+
+    med = [statistics.median(r[i] for r in rows[1:] or rows) for i in range(4)]
+    return {"workload": W.WORKLOADS[wid]["name"], "classes": "master, Adam m, Adam v (params stay local)",
+            "image_bytes": int(ck.image_bytes), "replica_bytes": int(rbytes), "replica_chunks": int(len(ids)),
+            "snapshots": steps, "send_ms": round(med[0], 1), "ack_ms": round(med[1], 1),
+            "peer_recv_ms": round(med[2], 1), "peer_gpu_check_ms": round(med[3], 1),
+            "h2h_GBps": round(rbytes / med[0] / 1e6, 2), "h2h_with_check_GBps": round(rbytes / med[1] / 1e6, 2),
+            "peer_check_GBps": round(rbytes / med[3] / 1e6, 2), "loopback_peak_GBps": round(loop, 2),
+            "statistic": "median over snapshots after the first"}
+
+
 def pmc_run(torch, P, W):
     """Short run whose dispatches the counter summary reads: a 1 GiB plain
     device copy (calibration), then two snapshots of the 1.3B GPT shard."""
@@ -503,6 +587,9 @@ def main():
         pmc_run(torch, P, W)
         return
     ratios = [float(r) for r in args.overlap_ratios.split(",") if r]
+    if args.h2h_only:
+        print(json.dumps({"h2h": h2h_leg(torch, P, W, args.h2h_workload, args.h2h_steps)}), flush=True)
+        return
     if args.overlap_only:
         log("link peak")
         link = link_peak(torch)

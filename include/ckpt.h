@@ -70,6 +70,7 @@ typedef int32_t ckpt_status;
 /* ckpt_wait modes */
 #define CKPT_WAIT_CAPTURED 0  /* stream-ordered: packed into device staging */
 #define CKPT_WAIT_COMMITTED 1 /* host-blocking: image and sums landed in host memory */
+#define CKPT_WAIT_REPLICATED 2 /* host-blocking: the ring peer has checked and committed the replica */
 
 /* ckpt_snapshot_state results */
 #define CKPT_SNAP_IN_FLIGHT 0
@@ -249,6 +250,77 @@ ckpt_status ckpt_plan(const uint64_t* nbytes, uint32_t n, uint64_t chunk_bytes, 
 ckpt_status ckpt_debug_tile_plan(const uint64_t* nbytes, uint32_t n, uint64_t chunk_bytes, uint32_t align_bytes,
                                  uint64_t* tile_bytes, uint64_t* n_tiles, uint32_t* tile_first,
                                  uint32_t* tile_last);
+
+/* ---- Host-to-host replication to a ring peer (Sec. V-B "Host-to-host";
+ * Sec. VI-A: the wait before the optimizer step covers the peer replica) ----
+ *
+ * ckpt_replicate_to: connect to a peer (ckpt_peer_*) listening at host:port
+ * (dotted IPv4) and start the context's H2H worker.  From then on every
+ * snapshot, once committed locally, is sent: the chunks holding a byte of a
+ * fragment whose class tag k has bit k set in cls_mask (the optimizer-state
+ * classes, in the paper), their stored sums and the snapshot's envelope.
+ * The peer re-checks every chunk sum on its GPU, commits its own ping-pong
+ * copy and answers.  ckpt_wait(CKPT_WAIT_REPLICATED) blocks until that
+ * answer: OK, ECORRUPT (the peer found bad chunks; ckpt_replica_result lists
+ * them; its previous replica stays), or EHIP (connection failed).  While a
+ * snapshot's replica is being sent its host image is held: a snapshot that
+ * would reuse it returns EBUSY.  Once per context, after registration.
+ * Errors: EINVAL (bad address or mask selecting nothing), ESTATE, EHIP. */
+ckpt_status ckpt_replicate_to(ckpt_ctx* ctx, const char* host, uint32_t port, uint64_t cls_mask);
+
+/* The replicated chunk ids (increasing; up to cap written) and their total
+ * bytes.  Errors: ESTATE (no peer). */
+ckpt_status ckpt_replica_chunks(ckpt_ctx* ctx, uint64_t* ids, uint64_t cap, uint64_t* n, uint64_t* replica_bytes);
+
+/* Non-blocking replication state of a snapshot: *state = 0 pending, 1 the
+ * peer committed it, 2 the peer found corrupt chunks (their ids in bad, up to
+ * cap; *n_bad the count), 3 failed (not sent, or no answer).
+ * Errors: ERANGE (not replicated: interrupted, or older than 64 snapshots). */
+ckpt_status ckpt_replica_result(ckpt_ctx* ctx, uint64_t snap_id, int32_t* state, uint64_t* bad, uint32_t cap,
+                                uint32_t* n_bad);
+
+/* Host wall time of the last replication, from the local commit being
+ * observed: to the last byte sent, and to the peer's answer. */
+ckpt_status ckpt_replica_timing(ckpt_ctx* ctx, double* send_ms, double* ack_ms);
+
+/* Fault injection for tests: kind 1 flips bit (b & 7) of replica byte a in
+ * the next stream (the local image is untouched); kind 2 closes the
+ * connection after a replica bytes of the next stream; 0 cancels. */
+ckpt_status ckpt_debug_h2h_fault(ckpt_ctx* ctx, int32_t kind, uint64_t a, uint64_t b);
+
+/* The receiving side: a ring peer holding its predecessor's replicas.  It
+ * listens on 127.0.0.1:port (0 = any free port; see ckpt_peer_port), takes
+ * one sender at a time, receives each snapshot's replica into the pinned
+ * buffer that does not hold its newest committed replica, re-checks every
+ * chunk sum on cfg->device with the library's checksum kernel (host->device
+ * copies through a two-slot device ring, cfg->group_bytes per slot), and
+ * commits the buffer only when every sum matches (Sec. VI-A: the buffer
+ * received from the ring predecessor alternates like the local one).  A
+ * stream cut mid-snapshot leaves the previous replica in place; the peer
+ * then waits for the next connection. */
+typedef struct ckpt_peer ckpt_peer;
+ckpt_status ckpt_peer_create(const ckpt_config* cfg, uint32_t port, ckpt_peer** out);
+ckpt_status ckpt_peer_port(const ckpt_peer* peer, uint32_t* port);
+/* Stops the receiver (closing any connection) and frees everything. */
+ckpt_status ckpt_peer_destroy(ckpt_peer* peer);
+/* Wait (up to timeout_ms) until snapshot snap_id of the sender has been
+ * handled: *result = CKPT_OK (committed), CKPT_ECORRUPT (rejected), or
+ * CKPT_EHIP (the stream broke).  Errors: ERANGE on timeout. */
+ckpt_status ckpt_peer_wait(ckpt_peer* peer, uint64_t snap_id, int32_t timeout_ms, int32_t* result);
+/* Borrowed view of the newest committed replica: sender's snapshot id and
+ * step, the replica bytes (chunks back to back), the sender's chunk ids and
+ * sums, and the envelope.  Valid until the peer starts receiving the
+ * snapshot after the next committed one (that one reuses this buffer).
+ * Errors: ENOSNAP (none committed). */
+ckpt_status ckpt_peer_replica(ckpt_peer* peer, uint64_t* snap_id, uint64_t* step, const void** data,
+                              uint64_t* bytes, const uint64_t** chunk_ids, const uint64_t** sums, uint64_t* n_chunks,
+                              const void** envelope, uint64_t* envelope_len);
+/* The sender's chunk ids that failed the check in the last rejected
+ * snapshot (up to cap; *n the count). */
+ckpt_status ckpt_peer_last_bad(ckpt_peer* peer, uint64_t* bad, uint32_t cap, uint32_t* n);
+/* Receive and GPU-check time of the last replica (ms). */
+ckpt_status ckpt_peer_timing(ckpt_peer* peer, double* recv_ms, double* check_ms);
+const char* ckpt_peer_last_error(const ckpt_peer* peer);
 
 /* Text of the context's last error ("" if none).  Valid until the next call. */
 const char* ckpt_last_error(const ckpt_ctx* ctx);

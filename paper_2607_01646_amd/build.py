@@ -18,6 +18,7 @@ DEVICE_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC",
                 "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 # The runtime has no device code: plain g++ against the HIP headers.
 HOST_CXX = os.environ.get("CXX_HOST", "g++")
+HOST_SOURCES = ["ckpt_runtime.cpp", "ckpt_peer.cpp"]
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-pthread", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__",
               "-I", "/opt/rocm/include"]
 
@@ -40,12 +41,15 @@ def build(verbose=False):
     obj_dir = os.path.join(PKG, "_build")
     os.makedirs(obj_dir, exist_ok=True)
     k_obj = os.path.join(obj_dir, "ckpt_kernels.o")
-    r_obj = os.path.join(obj_dir, "ckpt_runtime.o")
     inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
     _run([HIPCC] + DEVICE_FLAGS + inc + ["-c", os.path.join(CSRC, "ckpt_kernels.hip"), "-o", k_obj], verbose)
-    _run([HOST_CXX] + HOST_FLAGS + inc + ["-c", os.path.join(CSRC, "ckpt_runtime.cpp"), "-o", r_obj], verbose)
+    host_objs = []
+    for src in HOST_SOURCES:
+        o = os.path.join(obj_dir, src.replace(".cpp", ".o"))
+        _run([HOST_CXX] + HOST_FLAGS + inc + ["-c", os.path.join(CSRC, src), "-o", o], verbose)
+        host_objs.append(o)
     tmp = LIB + ".tmp"
-    _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", k_obj, r_obj, "-o", tmp, "-L/opt/rocm/lib",
+    _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", k_obj] + host_objs + ["-o", tmp, "-L/opt/rocm/lib",
           "-lhsa-runtime64", "-lpthread"], verbose)
     os.replace(tmp, LIB)
     return LIB

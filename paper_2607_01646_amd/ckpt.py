@@ -28,6 +28,8 @@ CKPT_EBUSY = -7
 CKPT_ERANGE = -8
 CKPT_WAIT_CAPTURED = 0
 CKPT_WAIT_COMMITTED = 1
+CKPT_WAIT_REPLICATED = 2
+REPLICA_PENDING, REPLICA_OK, REPLICA_CORRUPT, REPLICA_FAILED = 0, 1, 2, 3
 CKPT_SNAP_IN_FLIGHT = 0
 CKPT_SNAP_COMMITTED = 1
 CKPT_SNAP_ABORTED = 2
@@ -94,6 +96,20 @@ def lib():
             "ckpt_plan": ([P(u64), u32, u64, u32, P(u64), P(u64), P(u64)], i32),
             "ckpt_debug_tile_plan": ([P(u64), u32, u64, u32, P(u64), P(u64), P(u32), P(u32)], i32),
             "ckpt_last_error": ([vp], C.c_char_p),
+            "ckpt_replicate_to": ([vp, C.c_char_p, u32, u64], i32),
+            "ckpt_replica_chunks": ([vp, P(u64), u64, P(u64), P(u64)], i32),
+            "ckpt_replica_result": ([vp, u64, P(i32), P(u64), u32, P(u32)], i32),
+            "ckpt_replica_timing": ([vp, P(C.c_double), P(C.c_double)], i32),
+            "ckpt_debug_h2h_fault": ([vp, i32, u64, u64], i32),
+            "ckpt_peer_create": ([P(ckpt_config), u32, P(vp)], i32),
+            "ckpt_peer_port": ([vp, P(u32)], i32),
+            "ckpt_peer_destroy": ([vp], i32),
+            "ckpt_peer_wait": ([vp, u64, i32, P(i32)], i32),
+            "ckpt_peer_replica": ([vp, P(u64), P(u64), P(vp), P(u64), P(P(u64)), P(P(u64)), P(u64), P(vp), P(u64)],
+                                  i32),
+            "ckpt_peer_last_bad": ([vp, P(u64), u32, P(u32)], i32),
+            "ckpt_peer_timing": ([vp, P(C.c_double), P(C.c_double)], i32),
+            "ckpt_peer_last_error": ([vp], C.c_char_p),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -301,6 +317,115 @@ def ckpt_last_error(ctx):
     return (lib().ckpt_last_error(ctx) or b"").decode()
 
 
+def ckpt_replicate_to(ctx, host, port, cls_mask):
+    return _check(ctx, lib().ckpt_replicate_to(ctx, host.encode(), port, cls_mask))
+
+
+def ckpt_replica_chunks(ctx):
+    """(chunk ids uint64[m], replica bytes) of the replicated chunk set."""
+    n = C.c_uint64()
+    rb = C.c_uint64()
+    _check(ctx, lib().ckpt_replica_chunks(ctx, None, 0, C.byref(n), C.byref(rb)))
+    ids = np.zeros(max(n.value, 1), dtype=np.uint64)
+    _check(ctx, lib().ckpt_replica_chunks(ctx, _u64p(ids), n.value, C.byref(n), C.byref(rb)))
+    return ids[:n.value], rb.value
+
+
+def ckpt_replica_result(ctx, snap_id):
+    """(state, [bad chunk ids]) of a snapshot's replication."""
+    st = C.c_int32()
+    nb = C.c_uint32()
+    _check(ctx, lib().ckpt_replica_result(ctx, snap_id, C.byref(st), None, 0, C.byref(nb)))
+    bad = np.zeros(max(nb.value, 1), dtype=np.uint64)
+    _check(ctx, lib().ckpt_replica_result(ctx, snap_id, C.byref(st), _u64p(bad), nb.value, C.byref(nb)))
+    return st.value, [int(x) for x in bad[:nb.value]]
+
+
+def ckpt_replica_timing(ctx):
+    a, b = C.c_double(), C.c_double()
+    _check(ctx, lib().ckpt_replica_timing(ctx, C.byref(a), C.byref(b)))
+    return a.value, b.value
+
+
+def ckpt_debug_h2h_fault(ctx, kind, a=0, b=0):
+    return _check(ctx, lib().ckpt_debug_h2h_fault(ctx, kind, a, b))
+
+
+class PeerError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__("%s (%d): %s" % (_NAMES.get(code, "CKPT_E?"), code, msg))
+        self.code = code
+
+
+class Peer:
+    """The receiving ring peer of H2H replication (include/ckpt.h,
+    ckpt_peer_*): listens on 127.0.0.1, re-checks every received chunk sum on
+    the GPU, keeps two alternating replica buffers."""
+
+    def __init__(self, port=0, device=None, group_bytes=0):
+        if device is None:
+            device = torch.cuda.current_device()
+        cfg = ckpt_config(0, 0, 0, 0, group_bytes, device, 0, 0, 0)
+        self.p = C.c_void_p()
+        rc = lib().ckpt_peer_create(C.byref(cfg), port, C.byref(self.p))
+        if rc != CKPT_OK:
+            raise PeerError(rc, "ckpt_peer_create failed")
+        pt = C.c_uint32()
+        lib().ckpt_peer_port(self.p, C.byref(pt))
+        self.port = pt.value
+
+    def _err(self, rc):
+        return PeerError(rc, (lib().ckpt_peer_last_error(self.p) or b"").decode())
+
+    def wait(self, snap_id, timeout_ms=120_000):
+        """Result code of the sender's snapshot snap_id (CKPT_OK, CKPT_ECORRUPT,
+        CKPT_EHIP ...); raises on timeout."""
+        r = C.c_int32()
+        rc = lib().ckpt_peer_wait(self.p, snap_id, timeout_ms, C.byref(r))
+        if rc != CKPT_OK:
+            raise self._err(rc)
+        return r.value
+
+    def replica(self):
+        """Newest committed replica: dict with snap_id, step, data (uint8 view),
+        chunk_ids, sums, envelope (bytes)."""
+        sid, step, nbytes, n, elen = C.c_uint64(), C.c_uint64(), C.c_uint64(), C.c_uint64(), C.c_uint64()
+        data, env = C.c_void_p(), C.c_void_p()
+        ids, sums = C.POINTER(C.c_uint64)(), C.POINTER(C.c_uint64)()
+        rc = lib().ckpt_peer_replica(self.p, C.byref(sid), C.byref(step), C.byref(data), C.byref(nbytes),
+                                     C.byref(ids), C.byref(sums), C.byref(n), C.byref(env), C.byref(elen))
+        if rc != CKPT_OK:
+            raise self._err(rc)
+        return {"snap_id": sid.value, "step": step.value,
+                "data": np.ctypeslib.as_array(C.cast(data, C.POINTER(C.c_uint8)), shape=(nbytes.value,)),
+                "chunk_ids": np.ctypeslib.as_array(ids, shape=(n.value,)).copy(),
+                "sums": np.ctypeslib.as_array(sums, shape=(n.value,)),
+                "envelope": C.string_at(env, elen.value) if elen.value else b""}
+
+    def last_bad(self):
+        n = C.c_uint32()
+        lib().ckpt_peer_last_bad(self.p, None, 0, C.byref(n))
+        out = np.zeros(max(n.value, 1), dtype=np.uint64)
+        lib().ckpt_peer_last_bad(self.p, _u64p(out), n.value, C.byref(n))
+        return [int(x) for x in out[:n.value]]
+
+    def timing(self):
+        a, b = C.c_double(), C.c_double()
+        lib().ckpt_peer_timing(self.p, C.byref(a), C.byref(b))
+        return a.value, b.value
+
+    def close(self):
+        if self.p:
+            lib().ckpt_peer_destroy(self.p)
+            self.p = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
 class Checkpointer:
     """One rank's in-memory snapshot context over a list of device tensors.
 
@@ -354,6 +479,15 @@ class Checkpointer:
 
     def chunk_fragments(self, c):
         return ckpt_chunk_fragments(self.ctx, c)
+
+    def replicate_to(self, port, cls_mask, host="127.0.0.1"):
+        return ckpt_replicate_to(self.ctx, host, port, cls_mask)
+
+    def wait_replicated(self, snap):
+        return ckpt_wait(self.ctx, snap, CKPT_WAIT_REPLICATED)
+
+    def replica_result(self, snap):
+        return ckpt_replica_result(self.ctx, snap)
 
     def close(self):
         if self.ctx is not None:

@@ -53,6 +53,7 @@
 
 #include "../../include/ckpt.h"
 #include "ckpt_internal.h"
+#include "ckpt_wire.h"
 
 using namespace ckpt;
 
@@ -230,6 +231,46 @@ struct Pump {
     std::thread issuer, drainer;
 };
 
+// H2H replication (paper Sec. V-B, "Host-to-host"): one job per snapshot,
+// handed to the worker when the snapshot is issued.  The worker waits for
+// the local commit, sends the replicated chunks with their sums and the
+// envelope, and waits for the peer's acknowledgement.
+struct RepJob {
+    uint64_t id = 0, step = 0;
+    int buf = 0;
+    RecRes* res = nullptr;
+    uint32_t groups_copied = 0;
+    bool bounce = false;
+    std::vector<uint8_t> meta;
+};
+
+enum { REP_PENDING = 0, REP_OK = 1, REP_CORRUPT = 2, REP_FAILED = 3 };
+
+struct RepStatus {
+    int state = REP_PENDING;
+    std::vector<uint64_t> bad; // sender chunk ids the peer found corrupt
+    std::string err;
+};
+
+struct Replicator {
+    int fd = -1;
+    uint64_t cls_mask = 0;
+    std::vector<uint64_t> ids; // replicated chunks, increasing
+    uint64_t bytes = 0;        // replica bytes per snapshot
+    std::mutex m;
+    std::condition_variable cv;
+    std::deque<RepJob> q;
+    std::map<uint64_t, RepStatus> status;
+    bool busy[2] = {false, false}; // a replication still reads host image b
+    bool stop = false;
+    bool broken = false; // the connection failed: later jobs fail at once
+    std::string err;
+    int fault_kind = 0;  // debug: 1 = flip one bit of the next stream, 2 = cut the next stream
+    uint64_t fault_a = 0, fault_b = 0;
+    double last_send_ms = 0, last_ack_ms = 0; // commit -> last byte sent, commit -> acknowledgement
+    std::thread worker;
+};
+
 } // namespace
 
 struct ckpt_ctx {
@@ -306,6 +347,9 @@ struct ckpt_ctx {
     std::vector<hipEvent_t> bin_done; // per host -> device slot: its last copy to the device finished
     CopyPool* pool = nullptr;
     Pump* pump = nullptr;
+
+    // H2H replication to a ring peer
+    Replicator* rep = nullptr;
 
     // verify: its own ring of chunk slots and streams
     uint8_t* d_vring = nullptr;
@@ -604,14 +648,16 @@ ckpt_status get_res(ckpt_ctx* c, RecRes** out)
     return new_res(c, out);
 }
 
-bool copies_done(const SnapRec& r)
+bool res_done(const RecRes* res, uint32_t groups_copied, bool bounce)
 {
-    if (hsa_signal_load_scacquire(r.res->done) != 0) return false;
-    for (uint32_t g = 0; g < r.groups_copied; ++g)
-        if (hsa_signal_load_scacquire(r.res->flagged[g]) != 0) return false;
-    if (r.bounce && r.res->landed.load(std::memory_order_acquire) < r.groups_copied) return false;
+    if (hsa_signal_load_scacquire(res->done) != 0) return false;
+    for (uint32_t g = 0; g < groups_copied; ++g)
+        if (hsa_signal_load_scacquire(res->flagged[g]) != 0) return false;
+    if (bounce && res->landed.load(std::memory_order_acquire) < groups_copied) return false;
     return true;
 }
+
+bool copies_done(const SnapRec& r) { return res_done(r.res, r.groups_copied, r.bounce); }
 
 bool pump_failed(ckpt_ctx* c, std::string* why)
 {
@@ -859,9 +905,11 @@ ckpt_status run_check(ckpt_ctx* c, uint64_t snap_id, hipStream_t stream, bool sc
 }
 
 void stop_pump(ckpt_ctx* c);
+void rep_stop(ckpt_ctx* c);
 
 void free_ctx(ckpt_ctx* c)
 {
+    rep_stop(c); // reads host images and snapshot records
     stop_pump(c);
     delete c->pool;
     c->pool = nullptr;
@@ -917,6 +965,193 @@ bool poll_zero(hsa_signal_t sig, int seconds)
         std::this_thread::sleep_for(std::chrono::microseconds(20));
     }
     return true;
+}
+
+// The envelope of a snapshot (format in include/ckpt.h, ckpt_envelope).
+std::vector<uint8_t> build_envelope(const ckpt_ctx* c, uint64_t step, const std::vector<uint8_t>& meta,
+                                    const uint64_t* sums)
+{
+    const uint32_t nf = (uint32_t)c->frags.size();
+    const uint64_t meta_pad = round_up(meta.size(), 8);
+    const uint64_t total = 56 + 24ull * nf + 8 * c->n_chunks + meta_pad + 8;
+    // x86-64 and gfx950 are little-endian: fields are stored in native order.
+    std::vector<uint8_t> buf(total, 0);
+    uint8_t* p = buf.data();
+    struct __attribute__((packed)) Head {
+        char magic[8];
+        uint32_t version, align;
+        uint64_t step, chunk, image, n_chunks;
+        uint32_t n_frag, meta_len;
+    } h;
+    static_assert(sizeof(Head) == 56, "envelope header is 56 bytes");
+    std::memcpy(h.magic, "CKPTENV1", 8);
+    h.version = 1;
+    h.align = c->A;
+    h.step = step;
+    h.chunk = c->C;
+    h.image = c->I;
+    h.n_chunks = c->n_chunks;
+    h.n_frag = nf;
+    h.meta_len = (uint32_t)meta.size();
+    std::memcpy(p, &h, sizeof h);
+    p += sizeof h;
+    for (uint32_t i = 0; i < nf; ++i) {
+        struct __attribute__((packed)) Ent {
+            uint64_t off, nbytes;
+            uint32_t dtype, cls;
+        } e{c->frags[i].off, c->frags[i].nbytes, c->frags[i].dtype, c->frags[i].cls};
+        std::memcpy(p, &e, sizeof e);
+        p += sizeof e;
+    }
+    std::memcpy(p, sums, c->n_chunks * 8);
+    p += c->n_chunks * 8;
+    if (!meta.empty()) std::memcpy(p, meta.data(), meta.size());
+    p += meta_pad;
+    uint64_t s = 0;
+    for (const uint8_t* q = buf.data(); q < p; q += 8) {
+        uint64_t w;
+        std::memcpy(&w, q, 8);
+        s += w;
+    }
+    std::memcpy(p, &s, 8);
+    return buf;
+}
+
+// H2H worker thread (see Replicator).
+void rep_worker(ckpt_ctx* c)
+{
+    Replicator* R = c->rep;
+    using clock = std::chrono::steady_clock;
+    for (;;) {
+        RepJob j;
+        bool broken;
+        {
+            std::unique_lock<std::mutex> l(R->m);
+            R->cv.wait(l, [&] { return R->stop || !R->q.empty(); });
+            if (R->q.empty()) return;
+            j = std::move(R->q.front());
+            R->q.pop_front();
+            broken = R->broken;
+        }
+        RepStatus st;
+        st.state = REP_FAILED;
+        // 1. The local offload has to commit first (bounded wait).
+        const auto t_wait = clock::now();
+        bool committed = false;
+        while (!broken) {
+            if (res_done(j.res, j.groups_copied, j.bounce)) {
+                committed = !j.res->failed.load(std::memory_order_acquire);
+                break;
+            }
+            if (clock::now() - t_wait > std::chrono::seconds(120)) break;
+            {
+                std::lock_guard<std::mutex> l(R->m);
+                if (R->stop) break;
+            }
+            std::this_thread::sleep_for(std::chrono::microseconds(100));
+        }
+        if (broken) st.err = "the connection to the peer failed earlier: " + R->err;
+        else if (!committed) st.err = "the local snapshot did not commit";
+        const auto t_commit = clock::now();
+        int fault = 0;
+        uint64_t fa = 0, fb = 0;
+        if (committed) {
+            {
+                std::lock_guard<std::mutex> l(R->m);
+                fault = R->fault_kind;
+                fa = R->fault_a;
+                fb = R->fault_b;
+                R->fault_kind = 0;
+            }
+            // 2. Send head, ids, sums, envelope and the chunks.
+            const auto deadline = t_commit + std::chrono::seconds(120);
+            const uint64_t m = R->ids.size();
+            const uint64_t* sums_all = c->h_sums[j.buf];
+            std::vector<uint64_t> sums(m);
+            for (uint64_t k = 0; k < m; ++k) sums[k] = sums_all[R->ids[k]];
+            const std::vector<uint8_t> env = build_envelope(c, j.step, j.meta, sums_all);
+            WireHead h;
+            std::memcpy(h.magic, kWireMagic, 8);
+            h.snap_id = j.id;
+            h.step = j.step;
+            h.chunk_bytes = c->C;
+            h.image_bytes = c->I;
+            h.m = m;
+            h.replica_bytes = R->bytes;
+            h.env_len = env.size();
+            bool ok = send_all(R->fd, &h, sizeof h, deadline) == 0 &&
+                      send_all(R->fd, R->ids.data(), 8 * m, deadline) == 0 &&
+                      send_all(R->fd, sums.data(), 8 * m, deadline) == 0 &&
+                      send_all(R->fd, env.data(), env.size(), deadline) == 0;
+            const uint8_t* img = c->h_img[j.buf];
+            uint64_t sent = 0; // replica bytes sent so far
+            for (uint64_t k = 0; ok && k < m;) {
+                // one run of consecutive chunk ids is contiguous in the image
+                uint64_t e = k + 1;
+                while (e < m && R->ids[e] == R->ids[e - 1] + 1) ++e;
+                const uint64_t lo = R->ids[k] * c->C, hi = std::min(R->ids[e - 1] * c->C + c->C, c->I);
+                uint64_t n = hi - lo;
+                if (fault == 2 && sent + n >= fa) { // debug: cut the stream after fa replica bytes
+                    (void)send_all(R->fd, img + lo, fa - sent, deadline);
+                    ok = false;
+                    break;
+                }
+                if (fault == 1 && fa >= sent && fa < sent + n) { // debug: flip bit fb of replica byte fa
+                    const uint64_t at = fa - sent;
+                    uint8_t b = img[lo + at] ^ (uint8_t)(1u << (fb & 7));
+                    ok = send_all(R->fd, img + lo, at, deadline) == 0 && send_all(R->fd, &b, 1, deadline) == 0 &&
+                         send_all(R->fd, img + lo + at + 1, n - at - 1, deadline) == 0;
+                } else {
+                    ok = send_all(R->fd, img + lo, n, deadline) == 0;
+                }
+                sent += n;
+                k = e;
+            }
+            const auto t1 = clock::now();
+            // 3. The peer's verdict.
+            WireAck a;
+            if (ok) ok = recv_all(R->fd, &a, sizeof a, deadline) == 0 && std::memcmp(a.magic, kAckMagic, 8) == 0 &&
+                         a.snap_id == j.id && a.n_bad <= m;
+            if (ok && a.n_bad) {
+                st.bad.resize(a.n_bad);
+                ok = recv_all(R->fd, st.bad.data(), 8ull * a.n_bad, deadline) == 0;
+            }
+            const auto t2 = clock::now();
+            if (ok) {
+                st.state = a.status == CKPT_OK ? REP_OK : a.status == CKPT_ECORRUPT ? REP_CORRUPT : REP_FAILED;
+                if (st.state == REP_FAILED) st.err = "the peer reported error " + std::to_string(a.status);
+                std::lock_guard<std::mutex> l(R->m);
+                R->last_send_ms = std::chrono::duration<double, std::milli>(t1 - t_commit).count();
+                R->last_ack_ms = std::chrono::duration<double, std::milli>(t2 - t_commit).count();
+            } else {
+                st.err = fault == 2 ? "stream cut on request" : "sending to the peer failed";
+                std::lock_guard<std::mutex> l(R->m);
+                R->broken = true;
+                R->err = st.err;
+                ::shutdown(R->fd, SHUT_RDWR);
+            }
+        }
+        std::lock_guard<std::mutex> l(R->m);
+        R->status[j.id] = std::move(st);
+        R->busy[j.buf] = false;
+        R->cv.notify_all();
+    }
+}
+
+void rep_stop(ckpt_ctx* c)
+{
+    Replicator* R = c->rep;
+    if (!R) return;
+    {
+        std::lock_guard<std::mutex> l(R->m);
+        R->stop = true;
+    }
+    R->cv.notify_all();
+    if (R->fd >= 0) ::shutdown(R->fd, SHUT_RDWR);
+    if (R->worker.joinable()) R->worker.join();
+    if (R->fd >= 0) ::close(R->fd);
+    delete R;
+    c->rep = nullptr;
 }
 
 // Bounce mode, issuer thread (see Pump).
@@ -1290,6 +1525,25 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
         if (!newest_live || r.id > newest_live->id) newest_live = &r;
     }
     if (in_flight >= 2) return fail(c, CKPT_EBUSY, "both host images are still being written");
+    // Target: the image not holding the newest live snapshot; with no live
+    // snapshot, an image that holds nothing committed.
+    int buf = 0;
+    if (newest_live) {
+        buf = 1 - newest_live->buf;
+    } else {
+        for (int b = 0; b < 2; ++b) {
+            auto it = c->recs.find(c->holder[b]);
+            if (c->holder[b] == 0 || it == c->recs.end() || it->second.aborted) {
+                buf = b;
+                break;
+            }
+        }
+    }
+    if (c->rep) {
+        std::lock_guard<std::mutex> l(c->rep->m);
+        if (c->rep->busy[buf])
+            return fail(c, CKPT_EBUSY, "the snapshot in host image %d is still being sent to the peer", buf);
+    }
 
     RecRes* res = nullptr;
     ckpt_status st = get_res(c, &res);
@@ -1299,20 +1553,7 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
     r.id = id;
     r.step = step;
     r.res = res;
-    // Target: the image not holding the newest live snapshot; with no live
-    // snapshot, an image that holds nothing committed.
-    if (newest_live) {
-        r.buf = 1 - newest_live->buf;
-    } else {
-        r.buf = 0;
-        for (int b = 0; b < 2; ++b) {
-            auto it = c->recs.find(c->holder[b]);
-            if (c->holder[b] == 0 || it == c->recs.end() || it->second.aborted) {
-                r.buf = b;
-                break;
-            }
-        }
-    }
+    r.buf = buf;
     r.meta.assign((const uint8_t*)meta, (const uint8_t*)meta + meta_len);
     r.timed = c->timing;
     r.bounce = c->bounce;
@@ -1337,6 +1578,24 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
         r.timed = false;
         *snap_id = id;
         return st;
+    }
+    if (c->rep && !r.aborted) { // H2H once the offload commits
+        RepJob j;
+        j.id = id;
+        j.step = step;
+        j.buf = r.buf;
+        j.res = res;
+        j.groups_copied = r.groups_copied;
+        j.bounce = r.bounce;
+        j.meta = r.meta;
+        std::lock_guard<std::mutex> l(c->rep->m);
+        c->rep->busy[r.buf] = true;
+        while (!c->rep->status.empty() && c->rep->status.begin()->first + 64 < id &&
+               c->rep->status.begin()->second.state != REP_PENDING)
+            c->rep->status.erase(c->rep->status.begin());
+        c->rep->status[id] = RepStatus{};
+        c->rep->q.push_back(std::move(j));
+        c->rep->cv.notify_all();
     }
     *snap_id = id;
     return CKPT_OK;
@@ -1437,6 +1696,22 @@ ckpt_status ckpt_wait(ckpt_ctx* c, uint64_t snap_id, uint32_t mode, void* stream
                       uint32_t frag_hi)
 {
     if (!c) return CKPT_EINVAL;
+    if (mode == CKPT_WAIT_REPLICATED) {
+        if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
+        Replicator* R = c->rep;
+        std::unique_lock<std::mutex> l(R->m);
+        auto s = R->status.find(snap_id);
+        if (s == R->status.end())
+            return fail(c, CKPT_ERANGE, "snapshot %llu is not being replicated", (unsigned long long)snap_id);
+        if (!R->cv.wait_for(l, std::chrono::seconds(240), [&] { return s->second.state != REP_PENDING; }))
+            return fail(c, CKPT_EHIP, "snapshot %llu: no answer from the peer after 240 s", (unsigned long long)snap_id);
+        if (s->second.state == REP_OK) return CKPT_OK;
+        if (s->second.state == REP_CORRUPT)
+            return fail(c, CKPT_ECORRUPT, "the peer found %zu corrupt chunks in snapshot %llu", s->second.bad.size(),
+                        (unsigned long long)snap_id);
+        return fail(c, CKPT_EHIP, "snapshot %llu not replicated: %s", (unsigned long long)snap_id,
+                    s->second.err.c_str());
+    }
     auto it = c->recs.find(snap_id);
     if (it == c->recs.end()) return fail(c, CKPT_ERANGE, "snapshot %llu not retained", (unsigned long long)snap_id);
     SnapRec& r = it->second;
@@ -1568,52 +1843,10 @@ ckpt_status ckpt_envelope(ckpt_ctx* c, uint64_t snap_id, void* out, uint64_t cap
     SnapRec& r = it->second;
     if (!query_committed(r) || c->holder[r.buf] != r.id)
         return fail(c, CKPT_ENOSNAP, "snapshot not committed or superseded");
-    const uint32_t nf = (uint32_t)c->frags.size();
-    const uint64_t meta_pad = round_up(r.meta.size(), 8);
-    const uint64_t total = 56 + 24ull * nf + 8 * c->n_chunks + meta_pad + 8;
-    *len = total;
-    if (!out || cap < total) return fail(c, CKPT_EINVAL, "envelope needs %llu bytes", (unsigned long long)total);
-    // x86-64 and gfx950 are little-endian: fields are stored in native order.
-    std::vector<uint8_t> buf(total, 0);
-    uint8_t* p = buf.data();
-    struct __attribute__((packed)) Head {
-        char magic[8];
-        uint32_t version, align;
-        uint64_t step, chunk, image, n_chunks;
-        uint32_t n_frag, meta_len;
-    } h;
-    static_assert(sizeof(Head) == 56, "envelope header is 56 bytes");
-    std::memcpy(h.magic, "CKPTENV1", 8);
-    h.version = 1;
-    h.align = c->A;
-    h.step = r.step;
-    h.chunk = c->C;
-    h.image = c->I;
-    h.n_chunks = c->n_chunks;
-    h.n_frag = nf;
-    h.meta_len = (uint32_t)r.meta.size();
-    std::memcpy(p, &h, sizeof h);
-    p += sizeof h;
-    for (uint32_t i = 0; i < nf; ++i) {
-        struct __attribute__((packed)) Ent {
-            uint64_t off, nbytes;
-            uint32_t dtype, cls;
-        } e{c->frags[i].off, c->frags[i].nbytes, c->frags[i].dtype, c->frags[i].cls};
-        std::memcpy(p, &e, sizeof e);
-        p += sizeof e;
-    }
-    std::memcpy(p, c->h_sums[r.buf], c->n_chunks * 8);
-    p += c->n_chunks * 8;
-    if (!r.meta.empty()) std::memcpy(p, r.meta.data(), r.meta.size());
-    p += meta_pad;
-    uint64_t s = 0;
-    for (const uint8_t* q = buf.data(); q < p; q += 8) {
-        uint64_t w;
-        std::memcpy(&w, q, 8);
-        s += w;
-    }
-    std::memcpy(p, &s, 8);
-    std::memcpy(out, buf.data(), total);
+    const std::vector<uint8_t> buf = build_envelope(c, r.step, r.meta, c->h_sums[r.buf]);
+    *len = buf.size();
+    if (!out || cap < buf.size()) return fail(c, CKPT_EINVAL, "envelope needs %llu bytes", (unsigned long long)buf.size());
+    std::memcpy(out, buf.data(), buf.size());
     return CKPT_OK;
 }
 
@@ -1713,6 +1946,90 @@ ckpt_status ckpt_debug_tile_plan(const uint64_t* nbytes, uint32_t n, uint64_t ch
     if (n_tiles) *n_tiles = p.n_tiles;
     if (tile_first) std::memcpy(tile_first, p.tile_first.data(), 4 * p.n_tiles);
     if (tile_last && tile_first) std::memcpy(tile_last, p.tile_last.data(), 4 * p.n_tiles);
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_replicate_to(ckpt_ctx* c, const char* host, uint32_t port, uint64_t cls_mask)
+{
+    if (!c || !host || port == 0 || port > 65535 || cls_mask == 0) return fail(c, CKPT_EINVAL, "bad replication target");
+    if (!c->registered) return fail(c, CKPT_ESTATE, "no tensors registered");
+    if (c->rep) return fail(c, CKPT_ESTATE, "a replication peer is already set");
+    // Chunks holding a byte of a fragment of a selected class.
+    std::vector<uint8_t> pick(c->n_chunks, 0);
+    for (const Frag& f : c->frags) {
+        if (!f.nbytes || f.cls >= 64 || !((cls_mask >> f.cls) & 1)) continue;
+        for (uint64_t k = f.off / c->C; k <= (f.off + f.nbytes - 1) / c->C; ++k) pick[k] = 1;
+    }
+    std::vector<uint64_t> ids;
+    for (uint64_t k = 0; k < c->n_chunks; ++k)
+        if (pick[k]) ids.push_back(k);
+    if (ids.empty()) return fail(c, CKPT_EINVAL, "no registered fragment has a selected class");
+    sockaddr_in a{};
+    a.sin_family = AF_INET;
+    a.sin_port = htons((uint16_t)port);
+    if (inet_pton(AF_INET, host, &a.sin_addr) != 1) return fail(c, CKPT_EINVAL, "host must be a dotted IPv4 address");
+    const int fd = ::socket(AF_INET, SOCK_STREAM, 0);
+    if (fd < 0) return fail(c, CKPT_EHIP, "socket: %s", strerror(errno));
+    tune_socket(fd);
+    if (::connect(fd, (sockaddr*)&a, sizeof a) != 0) {
+        const int e = errno;
+        ::close(fd);
+        return fail(c, CKPT_EHIP, "connect to %s:%u: %s", host, port, strerror(e));
+    }
+    Replicator* R = new Replicator();
+    R->fd = fd;
+    R->cls_mask = cls_mask;
+    R->ids = std::move(ids);
+    R->bytes = replica_bytes(R->ids.data(), R->ids.size(), c->C, c->I);
+    c->rep = R;
+    R->worker = std::thread(rep_worker, c);
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_replica_chunks(ckpt_ctx* c, uint64_t* ids, uint64_t cap, uint64_t* n, uint64_t* replica_bytes_out)
+{
+    if (!c || !n) return CKPT_EINVAL;
+    if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
+    *n = c->rep->ids.size();
+    if (replica_bytes_out) *replica_bytes_out = c->rep->bytes;
+    if (ids) std::memcpy(ids, c->rep->ids.data(), 8 * std::min<uint64_t>(cap, c->rep->ids.size()));
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_replica_result(ckpt_ctx* c, uint64_t snap_id, int32_t* state, uint64_t* bad, uint32_t cap,
+                                uint32_t* n_bad)
+{
+    if (!c || !state) return CKPT_EINVAL;
+    if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
+    std::lock_guard<std::mutex> l(c->rep->m);
+    auto s = c->rep->status.find(snap_id);
+    if (s == c->rep->status.end())
+        return fail(c, CKPT_ERANGE, "snapshot %llu is not being replicated", (unsigned long long)snap_id);
+    *state = s->second.state;
+    if (n_bad) *n_bad = (uint32_t)s->second.bad.size();
+    if (bad) std::memcpy(bad, s->second.bad.data(), 8 * std::min<uint64_t>(cap, s->second.bad.size()));
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_replica_timing(ckpt_ctx* c, double* send_ms, double* ack_ms)
+{
+    if (!c || !send_ms || !ack_ms) return CKPT_EINVAL;
+    if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
+    std::lock_guard<std::mutex> l(c->rep->m);
+    *send_ms = c->rep->last_send_ms;
+    *ack_ms = c->rep->last_ack_ms;
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_debug_h2h_fault(ckpt_ctx* c, int32_t kind, uint64_t a, uint64_t b)
+{
+    if (!c || kind < 0 || kind > 2) return CKPT_EINVAL;
+    if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
+    std::lock_guard<std::mutex> l(c->rep->m);
+    if (kind && a >= c->rep->bytes) return fail(c, CKPT_EINVAL, "fault position beyond the replica");
+    c->rep->fault_kind = kind;
+    c->rep->fault_a = a;
+    c->rep->fault_b = b;
     return CKPT_OK;
 }
 

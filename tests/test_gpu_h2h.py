@@ -1,0 +1,241 @@
+"""Host-to-host replication to a ring peer, against the CPU oracle (needs an
+MI355X; sender and peer talk over TCP on 127.0.0.1).
+
+The expected replica is computed from the oracle alone: the chunks that hold
+a byte of a fragment of a selected class (oracle locate), their bytes from the
+oracle's pack, their sums, and the oracle's envelope of the snapshot.
+"""
+import multiprocessing as mp
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+from gpu_util import host_bytes
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    import paper_2607_01646_amd as P
+
+OPT = (1 << W.CLS_MASTER) | (1 << W.CLS_ADAM_M) | (1 << W.CLS_ADAM_V)
+
+
+def class_major(tensors, plan):
+    """The same state registered class by class: parameters first, then master
+    weights and the two moments, so the optimizer classes fill a run of chunks."""
+    order = sorted(range(len(plan)), key=lambda i: (plan[i][3], i))
+    return [tensors[i] for i in order], [plan[i][2] for i in order], [plan[i][3] for i in order]
+
+
+def expected_replica(host, dtypes, classes, chunk, mask, step, meta=b""):
+    sizes = [h.size for h in host]
+    img, off, nc = O.pack(host, 256, chunk)
+    I = img.size
+    ids = [c for c in range(nc) if any((mask >> classes[i]) & 1 for i in O.locate(c, chunk, I, off, sizes)[1])]
+    data = np.concatenate([img[c * chunk:min((c + 1) * chunk, I)] for c in ids])
+    sums = O.chunk_sums(img, 0, I, chunk)
+    env = O.envelope(step, 256, chunk, I, off, sizes, dtypes, classes, sums, meta)
+    return np.array(ids, dtype=np.uint64), data, sums[ids], env
+
+
+def tiny_state():
+    tensors, plan = W.make_state(1, device="cuda")
+    tensors, dtypes, classes = class_major(tensors, plan)
+    torch.cuda.synchronize()
+    return tensors, dtypes, classes
+
+
+@pytest.mark.parametrize("bounce", [0, 2 << 20])
+def test_replica_of_the_optimizer_state_matches_the_oracle(bounce):
+    """Workload 1 registered class-major, 1 MiB chunks: the peer's committed
+    replica equals the oracle's chunks, sums and envelope, and leaves out the
+    chunks that hold parameters only."""
+    tensors, dtypes, classes = tiny_state()
+    chunk = 1 << 20
+    peer = P.Peer()
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=chunk, group_bytes=chunk, bounce_bytes=bounce)
+    ck.replicate_to(peer.port, OPT)
+    host = [host_bytes(t) for t in tensors]
+    s = ck.snapshot(step=7, meta=b"rng")
+    ck.wait_replicated(s)
+    assert peer.wait(s) == P.CKPT_OK
+    ids, data, sums, env = expected_replica(host, dtypes, classes, chunk, OPT, 7, b"rng")
+    got_ids, nbytes = P.ckpt_replica_chunks(ck.ctx)
+    assert np.array_equal(got_ids, ids) and nbytes == data.size
+    assert data.size < ck.image_bytes  # parameter-only chunks stay home
+    r = peer.replica()
+    assert (r["snap_id"], r["step"]) == (s, 7)
+    assert np.array_equal(r["chunk_ids"], ids)
+    assert np.array_equal(r["data"], data)
+    assert np.array_equal(r["sums"], sums)
+    assert r["envelope"] == env
+    assert ck.replica_result(s) == (P.REPLICA_OK, [])
+    ck.close()
+    peer.close()
+
+
+def test_param_major_layout_replicates_every_mixed_chunk():
+    """Parameter-major registration interleaves classes: every chunk holding a
+    byte of master weights or moments is sent; the replica still matches."""
+    tensors, plan = W.make_state(1, device="cuda")
+    dtypes, classes = [p[2] for p in plan], [p[3] for p in plan]
+    torch.cuda.synchronize()
+    chunk = 1 << 20
+    peer = P.Peer()
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=chunk)
+    ck.replicate_to(peer.port, OPT)
+    host = [host_bytes(t) for t in tensors]
+    s = ck.snapshot(step=1)
+    ck.wait_replicated(s)
+    ids, data, sums, env = expected_replica(host, dtypes, classes, chunk, OPT, 1)
+    r = peer.replica()
+    assert np.array_equal(r["chunk_ids"], ids) and np.array_equal(r["data"], data)
+    assert np.array_equal(r["sums"], sums) and r["envelope"] == env
+    ck.close()
+    peer.close()
+
+
+def test_flip_in_transit_is_caught_and_the_previous_replica_stays():
+    tensors, dtypes, classes = tiny_state()
+    chunk = 1 << 20
+    peer = P.Peer()
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=chunk)
+    ck.replicate_to(peer.port, OPT)
+    host1 = [host_bytes(t) for t in tensors]
+    s1 = ck.snapshot(step=1)
+    ck.wait_replicated(s1)
+    for t in tensors:
+        t.mul_(2)
+    ids, _ = P.ckpt_replica_chunks(ck.ctx)
+    at = 3 * chunk + 12345  # replica byte in the fourth replicated chunk
+    P.ckpt_debug_h2h_fault(ck.ctx, 1, at, 5)
+    s2 = ck.snapshot(step=2)
+    with pytest.raises(P.CkptError) as e:
+        ck.wait_replicated(s2)
+    assert e.value.code == P.CKPT_ECORRUPT
+    assert ck.replica_result(s2) == (P.REPLICA_CORRUPT, [int(ids[3])])
+    assert peer.wait(s2) == P.CKPT_ECORRUPT and peer.last_bad() == [int(ids[3])]
+    r = peer.replica()  # still snapshot 1, byte for byte
+    want1 = expected_replica(host1, dtypes, classes, chunk, OPT, 1)
+    assert r["snap_id"] == s1 and np.array_equal(r["data"], want1[1])
+    assert ck.verify(s2) == []  # the local snapshot itself is intact
+    host3 = [host_bytes(t) for t in tensors]
+    s3 = ck.snapshot(step=3)
+    ck.wait_replicated(s3)
+    r = peer.replica()
+    assert r["snap_id"] == s3 and np.array_equal(r["data"], expected_replica(host3, dtypes, classes, chunk, OPT, 3)[1])
+    ck.close()
+    peer.close()
+
+
+def test_cut_stream_keeps_the_previous_replica():
+    tensors, dtypes, classes = tiny_state()
+    chunk = 1 << 20
+    peer = P.Peer()
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=chunk)
+    ck.replicate_to(peer.port, OPT)
+    host1 = [host_bytes(t) for t in tensors]
+    s1 = ck.snapshot(step=1)
+    ck.wait_replicated(s1)
+    P.ckpt_debug_h2h_fault(ck.ctx, 2, 5 * chunk + 7)  # stream closed 5 MiB into the replica
+    s2 = ck.snapshot(step=2)
+    with pytest.raises(P.CkptError) as e:
+        ck.wait_replicated(s2)
+    assert e.value.code == P.CKPT_EHIP
+    assert peer.wait(s2) == P.CKPT_EHIP
+    r = peer.replica()
+    assert r["snap_id"] == s1 and np.array_equal(r["data"], expected_replica(host1, dtypes, classes, chunk, OPT, 1)[1])
+    # the connection is gone: later snapshots still commit locally, replication fails fast
+    s3 = ck.snapshot(step=3)
+    ck.wait_committed(s3)
+    with pytest.raises(P.CkptError) as e:
+        ck.wait_replicated(s3)
+    assert e.value.code == P.CKPT_EHIP
+    ck.close()
+    peer.close()
+
+
+def test_ping_pong_on_the_peer_over_several_snapshots():
+    """Four snapshots of changing state, each waited for before the next
+    update (the paper's single wait before the optimizer step): the peer's
+    replica always equals the newest one."""
+    tensors, dtypes, classes = tiny_state()
+    chunk = 1 << 20
+    peer = P.Peer(group_bytes=4 << 20)
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=chunk)
+    ck.replicate_to(peer.port, OPT)
+    for step in range(4):
+        host = [host_bytes(t) for t in tensors]
+        s = ck.snapshot(step=step)
+        ck.wait_replicated(s)
+        r = peer.replica()
+        want = expected_replica(host, dtypes, classes, chunk, OPT, step)
+        assert r["snap_id"] == s and np.array_equal(r["data"], want[1]) and r["envelope"] == want[3]
+        for t in tensors:
+            t.add_(0.5)
+    ck.close()
+    peer.close()
+
+
+def _peer_process(conn, device):
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    import paper_2607_01646_amd as PP
+
+    peer = PP.Peer(device=device)
+    conn.send(peer.port)
+    snap = conn.recv()
+    rc = peer.wait(snap)
+    r = peer.replica()
+    conn.send((rc, r["snap_id"], r["chunk_ids"].tolist(), r["sums"].tolist(), bytes(r["data"]), r["envelope"]))
+    conn.recv()
+    peer.close()
+
+
+def test_peer_in_another_process():
+    """The ring peer as its own process (its own HIP context on the same GPU)."""
+    tensors, dtypes, classes = tiny_state()
+    chunk = 1 << 20
+    ctx = mp.get_context("spawn")
+    a, b = ctx.Pipe()
+    proc = ctx.Process(target=_peer_process, args=(b, torch.cuda.current_device()))
+    proc.start()
+    try:
+        port = a.recv()
+        ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=chunk)
+        ck.replicate_to(port, OPT)
+        host = [host_bytes(t) for t in tensors]
+        s = ck.snapshot(step=11)
+        a.send(s)
+        ck.wait_replicated(s)
+        rc, sid, ids, sums, data, env = a.recv()
+        want = expected_replica(host, dtypes, classes, chunk, OPT, 11)
+        assert rc == P.CKPT_OK and sid == s
+        assert ids == want[0].tolist() and sums == want[2].tolist()
+        assert np.array_equal(np.frombuffer(data, dtype=np.uint8), want[1]) and env == want[3]
+        a.send("done")
+        ck.close()
+    finally:
+        proc.join(timeout=60)
+        if proc.is_alive():
+            proc.kill()
+    assert proc.exitcode == 0
+
+
+def test_replication_errors():
+    tensors, dtypes, classes = tiny_state()
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=1 << 20)
+    with pytest.raises(P.CkptError) as e:
+        ck.wait_replicated(1)
+    assert e.value.code == P.CKPT_ESTATE
+    with pytest.raises(P.CkptError) as e:
+        ck.replicate_to(1, 1 << 9)  # no fragment has class 9
+    assert e.value.code == P.CKPT_EINVAL
+    with pytest.raises(P.CkptError) as e:
+        ck.replicate_to(1, OPT)  # nothing listens on port 1
+    assert e.value.code == P.CKPT_EHIP
+    ck.close()
