@@ -23,10 +23,12 @@
 // with the training step.
 //
 // The two pinned images alternate: a snapshot takes the image that does not
-// hold the newest live (in flight or committed) snapshot.  Its copies are
-// ordered after that snapshot's (the same staging areas gate them), so a
-// committed image exists at every point, and an interrupted snapshot is
-// never the recovery point (invariant I4 of Sec. V-C).
+// hold the newest live (in flight or committed) snapshot.  When that one has
+// not committed yet, every image copy of the new snapshot also waits for its
+// commit (its chunk-sum copy and its last staging-counter copy are listed as
+// DMA dependencies), so a committed image exists at every point once the
+// first snapshot has committed, and an interrupted snapshot is never the
+// recovery point (invariant I4 of Sec. V-C).
 //
 // Recovery (Sec. V-C third stage, Sec. VI-E) reverses the path group by
 // group: DMA host image -> staging on the copy stream, then the scatter
@@ -204,6 +206,8 @@ struct PumpItem {
     uint64_t* area_done;     // group: device counter bumped once the staging area has been read
     const uint64_t* seq;     // group: pinned, the value it is set to
     hsa_amd_sdma_engine_id_t engine;
+    const RecRes* after;     // first group: the snapshot that must have committed before this image is written
+    uint32_t after_groups;   // its group copies
 };
 
 // Bounce-mode D2H (one per context).  The issuer takes snapshot groups in
@@ -949,12 +953,21 @@ void free_ctx(ckpt_ctx* c)
 // Issue one SDMA copy; on failure the dependency chain of the snapshot is
 // released so no engine is left polling.
 ckpt_status dma(ckpt_ctx* c, void* dst, hsa_agent_t dst_agent, const void* src, hsa_agent_t src_agent, uint64_t n,
-                const hsa_signal_t* dep, hsa_signal_t completion, hsa_amd_sdma_engine_id_t engine)
+                const hsa_signal_t* dep, hsa_signal_t completion, hsa_amd_sdma_engine_id_t engine, uint32_t n_dep = 1)
 {
-    HSACHK(c, hsa_amd_memory_async_copy_on_engine(dst, dst_agent, src, src_agent, n, dep ? 1 : 0, dep, completion,
+    HSACHK(c, hsa_amd_memory_async_copy_on_engine(dst, dst_agent, src, src_agent, n, dep ? n_dep : 0, dep, completion,
                                                   engine, true));
     return CKPT_OK;
 }
+
+// The snapshot a new one must not overtake: the newest live one when it has
+// not committed yet.  Its completion signals (the chunk-sum copy and the
+// last staging-counter copy, whose engine runs them in order, so it implies
+// every earlier one) are 0 exactly when it has committed.
+struct PrevSnap {
+    const RecRes* res = nullptr;
+    uint32_t groups_copied = 0;
+};
 
 // Poll a signal that only the GPU side waits on until it reads 0.
 bool poll_zero(hsa_signal_t sig, int seconds)
@@ -1251,6 +1264,14 @@ void pump_drain(ckpt_ctx* c)
         bool free_slot = slot != UINT64_MAX, ok = free_slot;
         if (ok) {
             ok = poll_zero(it.res->copied[it.g], 120);
+            // Only once the previous snapshot has committed (all its groups,
+            // drained before this one's, its staging counters and its sums)
+            // may the older image be overwritten.
+            if (ok && it.after) {
+                const auto deadline = std::chrono::steady_clock::now() + std::chrono::seconds(120);
+                while (!res_done(it.after, it.after_groups, true) && std::chrono::steady_clock::now() < deadline)
+                    std::this_thread::sleep_for(std::chrono::microseconds(20));
+            }
             if (ok) c->pool->copy(it.image, c->h_bout + slot * unit, it.n);
             else free_slot = false; // the engine may still write it
         }
@@ -1282,7 +1303,8 @@ void stop_pump(ckpt_ctx* c)
     c->pump = nullptr;
 }
 
-ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop);
+ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop,
+                           const PrevSnap& prev);
 
 } // namespace
 
@@ -1572,7 +1594,15 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
 
     // On an error below, copies not issued never raise their signals, and
     // the snapshot is marked interrupted.
-    st = issue_snapshot(c, r, after, n_copy, stop);
+    // A committed image must exist at every point (Sec. VI-A; invariant I4):
+    // this snapshot writes the image of the older committed one, so none of
+    // its bytes may land there before the newest live snapshot has committed.
+    PrevSnap prev;
+    if (newest_live && !query_committed(*newest_live)) {
+        prev.res = newest_live->res;
+        prev.groups_copied = newest_live->groups_copied;
+    }
+    st = issue_snapshot(c, r, after, n_copy, stop, prev);
     if (st) {
         r.aborted = true;
         r.timed = false;
@@ -1605,7 +1635,8 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
 
 namespace {
 
-ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop)
+ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop,
+                           const PrevSnap& prev)
 {
     RecRes* res = r.res;
     uint8_t* himg = c->h_img[r.buf];
@@ -1643,13 +1674,20 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
             {
                 std::lock_guard<std::mutex> l(c->pump->m);
                 c->pump->issue_q.push_back(PumpItem{res, (uint32_t)g, false, himg + lo, staging_of(c, g), hi - lo,
-                                                    c->d_area_done + area, &res->h_seq[g], eng});
+                                                    c->d_area_done + area, &res->h_seq[g], eng,
+                                                    g == 0 ? prev.res : nullptr, prev.groups_copied});
             }
             c->pump->cv.notify_all();
             ++c->area_seq[area];
             continue;
         }
-        st = dma(c, himg + lo, host, staging_of(c, g), c->gpu_agent, hi - lo, &res->dep[g], res->copied[g], eng);
+        hsa_signal_t deps[3] = {res->dep[g], {0}, {0}};
+        uint32_t n_dep = 1;
+        if (prev.res) {
+            deps[n_dep++] = prev.res->done;
+            if (prev.groups_copied) deps[n_dep++] = prev.res->flagged[prev.groups_copied - 1];
+        }
+        st = dma(c, himg + lo, host, staging_of(c, g), c->gpu_agent, hi - lo, deps, res->copied[g], eng, n_dep);
         if (!st)
             st = dma(c, c->d_area_done + area, c->gpu_agent, &res->h_seq[g], host, 8, &res->copied[g],
                      res->flagged[g], c->h2d_engine);
@@ -1673,7 +1711,7 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
                 std::lock_guard<std::mutex> l(c->pump->m);
                 c->pump->issue_q.push_back(PumpItem{res, 0, true, (uint8_t*)c->h_sums[r.buf],
                                                     (const uint8_t*)res->d_sums, c->n_chunks * 8, nullptr, nullptr,
-                                                    c->d2h_engine[0]});
+                                                    c->d2h_engine[0], nullptr, 0});
             }
             c->pump->cv.notify_all();
             return CKPT_OK;

@@ -13,6 +13,7 @@ import torch
 import oracle as O
 import workloads as W
 from gpu_util import EDGE_SIZES, garbage_fill, host_bytes, random_byte_fragments, snapshot_and_check
+from test_gpu_parity import check_committed_image_survives
 
 pytestmark = pytest.mark.gpu
 
@@ -145,6 +146,11 @@ def test_verify_beside_an_inflight_bounce_snapshot():
         assert np.array_equal(img, want)
         assert np.array_equal(sums, O.chunk_sums(want, 0, want.size, chunk))
     ck.close()
+
+
+def test_a_committed_image_exists_while_two_bounce_snapshots_are_in_flight():
+    for _ in range(3):
+        check_committed_image_survives(1 << 25)
 
 
 def test_bounce_configuration_errors():
