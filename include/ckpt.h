@@ -251,6 +251,43 @@ ckpt_status ckpt_debug_tile_plan(const uint64_t* nbytes, uint32_t n, uint64_t ch
                                  uint64_t* tile_bytes, uint64_t* n_tiles, uint32_t* tile_first,
                                  uint32_t* tile_last);
 
+/* ---- Crash-surviving local snapshots (Sec. V-B: the host copy serves fast
+ * local recovery without any network transfer; Sec. V-C: a local reset
+ * re-enters as a replacement) ----
+ *
+ * ckpt_image_file, before ckpt_register_tensors and only in bounce mode
+ * (cfg.bounce_bytes > 0): keep the two host images, their chunk sums and a
+ * commit record for each in the file at path, mapped shared, so that they
+ * outlive the process (under /dev/shm: until the host reboots).  A record is
+ * written after the snapshot's last byte and its sums have landed, and is
+ * cleared before its image is rewritten, so a process that dies at any point
+ * leaves its newest committed snapshot restorable (invariant I4).
+ *   CKPT_FILE_CREATE: create or truncate the file at registration.
+ *   CKPT_FILE_ADOPT: open a file written by a context of the same layout
+ *     (same fragment sizes, dtypes and classes in the same order, chunk size
+ *     and alignment); its newest valid record becomes this context's
+ *     committed snapshot (ckpt_latest names it; ckpt_restore restores it,
+ *     re-checking every chunk sum).
+ * File format (little-endian): a head at offset 0 {char magic[8] = "CKPTFIL1";
+ * u32 version = 1; u32 align; u64 chunk_bytes; u64 image_bytes; u64 n_chunks;
+ * u32 n_frag; u32 0; u64 table_sum = sum over fragments of off + nbytes +
+ * (dtype | cls << 32) mod 2^64; u64 image_off[2]; u64 sums_off[2];
+ * u64 meta_off[2]; u64 file_bytes}; at 4096 + 512 * b the record of image b
+ * {u64 state (1 = committed); u64 seq (of two valid records the larger is the
+ * newest); u64 snap_id; u64 step; u64 meta_len; u64 rec_sum = seq + snap_id +
+ * step + meta_len + the word-sum of the image's n_chunks sums and of its blob
+ * zero-padded to 8 bytes, mod 2^64}; image b's sums at sums_off[b], its blob
+ * at meta_off[b] and its bytes at image_off[b].
+ * Errors: EINVAL (bounce mode off, bad mode), ESTATE (already registered);
+ * at registration: EINVAL (the file's layout differs), EHIP / ENOMEM (file
+ * errors). */
+#define CKPT_FILE_CREATE 0
+#define CKPT_FILE_ADOPT 1
+ckpt_status ckpt_image_file(ckpt_ctx* ctx, const char* path, uint32_t mode);
+
+/* The newest committed snapshot still held (0 if none) and its step. */
+ckpt_status ckpt_latest(ckpt_ctx* ctx, uint64_t* snap_id, uint64_t* step);
+
 /* ---- Host-to-host replication to a ring peer (Sec. V-B "Host-to-host";
  * Sec. VI-A: the wait before the optimizer step covers the peer replica) ----
  *

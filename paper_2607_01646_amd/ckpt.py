@@ -30,6 +30,8 @@ CKPT_WAIT_CAPTURED = 0
 CKPT_WAIT_COMMITTED = 1
 CKPT_WAIT_REPLICATED = 2
 REPLICA_PENDING, REPLICA_OK, REPLICA_CORRUPT, REPLICA_FAILED = 0, 1, 2, 3
+CKPT_FILE_CREATE = 0
+CKPT_FILE_ADOPT = 1
 CKPT_SNAP_IN_FLIGHT = 0
 CKPT_SNAP_COMMITTED = 1
 CKPT_SNAP_ABORTED = 2
@@ -96,6 +98,8 @@ def lib():
             "ckpt_plan": ([P(u64), u32, u64, u32, P(u64), P(u64), P(u64)], i32),
             "ckpt_debug_tile_plan": ([P(u64), u32, u64, u32, P(u64), P(u64), P(u32), P(u32)], i32),
             "ckpt_last_error": ([vp], C.c_char_p),
+            "ckpt_image_file": ([vp, C.c_char_p, u32], i32),
+            "ckpt_latest": ([vp, P(u64), P(u64)], i32),
             "ckpt_replicate_to": ([vp, C.c_char_p, u32, u64], i32),
             "ckpt_replica_chunks": ([vp, P(u64), u64, P(u64), P(u64)], i32),
             "ckpt_replica_result": ([vp, u64, P(i32), P(u64), u32, P(u32)], i32),
@@ -317,6 +321,17 @@ def ckpt_last_error(ctx):
     return (lib().ckpt_last_error(ctx) or b"").decode()
 
 
+def ckpt_image_file(ctx, path, mode=CKPT_FILE_CREATE):
+    return _check(ctx, lib().ckpt_image_file(ctx, path.encode(), mode))
+
+
+def ckpt_latest(ctx):
+    """(snapshot id, step) of the newest committed snapshot still held; id 0 if none."""
+    sid, step = C.c_uint64(), C.c_uint64()
+    _check(ctx, lib().ckpt_latest(ctx, C.byref(sid), C.byref(step)))
+    return sid.value, step.value
+
+
 def ckpt_replicate_to(ctx, host, port, cls_mask):
     return _check(ctx, lib().ckpt_replicate_to(ctx, host.encode(), port, cls_mask))
 
@@ -440,11 +455,14 @@ class Checkpointer:
     """
 
     def __init__(self, tensors, dtypes=None, classes=None, chunk_bytes=0, align_bytes=0, device_staging_bytes=0,
-                 group_bytes=0, grid_blocks=0, device=None, bounce_bytes=0, host_threads=0):
+                 group_bytes=0, grid_blocks=0, device=None, bounce_bytes=0, host_threads=0, image_file=None,
+                 image_file_mode=CKPT_FILE_CREATE):
         self.tensors = list(tensors)
         self.ctx = ckpt_create(chunk_bytes, align_bytes, device_staging_bytes, group_bytes, device, grid_blocks,
                                bounce_bytes, host_threads)
         try:
+            if image_file is not None:
+                ckpt_image_file(self.ctx, image_file, image_file_mode)
             ckpt_register_tensors(self.ctx, self.tensors, dtypes, classes)
         except Exception:
             ckpt_destroy(self.ctx)
@@ -479,6 +497,9 @@ class Checkpointer:
 
     def chunk_fragments(self, c):
         return ckpt_chunk_fragments(self.ctx, c)
+
+    def latest(self):
+        return ckpt_latest(self.ctx)
 
     def replicate_to(self, port, cls_mask, host="127.0.0.1"):
         return ckpt_replicate_to(self.ctx, host, port, cls_mask)

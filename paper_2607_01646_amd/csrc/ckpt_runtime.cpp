@@ -37,7 +37,10 @@
 #include <hsa/hsa.h>
 #include <hsa/hsa_ext_amd.h>
 
+#include <fcntl.h>
 #include <sys/mman.h>
+#include <sys/stat.h>
+#include <unistd.h>
 
 #include <algorithm>
 #include <atomic>
@@ -48,6 +51,7 @@
 #include <cstring>
 #include <deque>
 #include <map>
+#include <memory>
 #include <mutex>
 #include <string>
 #include <thread>
@@ -94,12 +98,14 @@ struct RecRes {
     hipEvent_t t0 = nullptr;
     std::atomic<uint32_t> landed{0};    // bounce mode: groups moved from the ring into the image
     std::atomic<bool> failed{false};    // bounce mode: a copy of this record could not be completed
+    std::atomic<bool> recorded{false};  // image file: the commit record has been written
 };
 
 struct SnapRec {
     uint64_t id = 0, step = 0;
     int buf = -1;
     bool bounce = false;    // the image is pageable; groups land through the bounce ring
+    bool file = false;      // the image lives in the image file: committed once its record is written
     bool aborted = false;
     bool committed = false; // cached once `done` has reached 0
     bool timed = false;
@@ -197,18 +203,45 @@ private:
 // One group of a snapshot on its way through the bounce ring, or (sums)
 // the snapshot's chunk-sum copy, which follows its groups.
 struct PumpItem {
-    RecRes* res;
-    uint32_t g;
-    bool sums;               // the chunk sums: device -> pinned sums array, no ring slot
-    uint8_t* image;          // destination: pageable host image (group) or pinned sums array
-    const uint8_t* staging;  // source in device memory
-    uint64_t n;
-    uint64_t* area_done;     // group: device counter bumped once the staging area has been read
-    const uint64_t* seq;     // group: pinned, the value it is set to
-    hsa_amd_sdma_engine_id_t engine;
-    const RecRes* after;     // first group: the snapshot that must have committed before this image is written
-    uint32_t after_groups;   // its group copies
+    RecRes* res = nullptr;
+    uint32_t g = 0;
+    bool sums = false;               // the chunk sums: device -> pinned sums array, no ring slot
+    uint8_t* image = nullptr;        // destination: pageable host image (group) or pinned sums array
+    const uint8_t* staging = nullptr; // source in device memory
+    uint64_t n = 0;
+    uint64_t* area_done = nullptr;   // group: device counter bumped once the staging area has been read
+    const uint64_t* seq = nullptr;   // group: pinned, the value it is set to
+    hsa_amd_sdma_engine_id_t engine{};
+    const RecRes* after = nullptr;   // first group: the snapshot that must have committed before this image is
+                                     // written
+    uint32_t after_groups = 0;       // group copies of that snapshot (record: of this item's own snapshot)
+    int buf = 0;                     // host image written
+    bool record = false;             // image file: write the snapshot's commit record (no copy)
+    uint64_t need_rec = 0;           // sums: records of image buf that must be written before its sums array is reused
+    uint64_t snap_id = 0, step = 0;
+    std::shared_ptr<const std::vector<uint8_t>> meta;
 };
+
+// Image file (ckpt_image_file): the two images, their sums and commit
+// records in one shared mapping.  Layout: FileHead at 0, FileRec b at
+// kRecOff + 512 * b, then per image its sums, its caller blob area and (2 MiB
+// aligned) its bytes.
+struct FileHead {
+    char magic[8]; // "CKPTFIL1"
+    uint32_t version, align;
+    uint64_t chunk, image_bytes, n_chunks;
+    uint32_t n_frag, pad;
+    uint64_t table_sum; // word-sum of the fragment table (offset, bytes, dtype, class per fragment)
+    uint64_t image_off[2], sums_off[2], meta_off[2];
+    uint64_t file_bytes;
+};
+struct FileRec {
+    uint64_t state;   // 1 = committed; stored last, 0 before the image is rewritten
+    uint64_t seq;     // commit number: of two valid records the larger is the newest
+    uint64_t snap_id, step, meta_len;
+    uint64_t rec_sum; // word-sum of seq, snap_id, step, meta_len, the chunk sums and the zero-padded blob
+};
+constexpr uint64_t kRecOff = 4096;
 
 // Bounce-mode D2H (one per context).  The issuer takes snapshot groups in
 // order, waits for a free ring slot, and starts the DMA staging -> slot
@@ -229,6 +262,7 @@ struct Pump {
     std::deque<std::pair<PumpItem, uint64_t>> drain_q;
     std::vector<uint8_t> busy; // per ring slot
     uint64_t next_slot = 0;
+    uint64_t rec_pushed[2] = {0, 0}, rec_done[2] = {0, 0}; // image-file commit records per host image
     bool stop = false;
     bool failed = false;
     std::string err;
@@ -354,6 +388,14 @@ struct ckpt_ctx {
 
     // H2H replication to a ring peer
     Replicator* rep = nullptr;
+
+    // image file (crash-surviving images; bounce mode only)
+    std::string file_path;
+    int file_mode = -1; // -1 none, else CKPT_FILE_CREATE / CKPT_FILE_ADOPT
+    int file_fd = -1;
+    uint8_t* file_map = nullptr;
+    FileHead fhead{};
+    uint64_t file_seq = 0; // last commit number written (drainer thread after registration)
 
     // verify: its own ring of chunk slots and streams
     uint8_t* d_vring = nullptr;
@@ -661,7 +703,13 @@ bool res_done(const RecRes* res, uint32_t groups_copied, bool bounce)
     return true;
 }
 
-bool copies_done(const SnapRec& r) { return res_done(r.res, r.groups_copied, r.bounce); }
+bool copies_done(const SnapRec& r)
+{
+    // an interrupted or failed snapshot never gets a record
+    return res_done(r.res, r.groups_copied, r.bounce) &&
+           (!r.file || r.aborted || r.res->failed.load(std::memory_order_acquire) ||
+            r.res->recorded.load(std::memory_order_acquire));
+}
 
 bool pump_failed(ckpt_ctx* c, std::string* why)
 {
@@ -697,6 +745,11 @@ ckpt_status wait_copies(ckpt_ctx* c, SnapRec& r)
         std::string why;
         if (r.res->failed.load(std::memory_order_acquire) || pump_failed(c, &why))
             return fail(c, CKPT_EHIP, "snapshot %llu: bounce copy failed: %s", (unsigned long long)r.id, why.c_str());
+        while (r.file && !r.aborted && !r.res->recorded.load(std::memory_order_acquire)) {
+            if (std::chrono::steady_clock::now() > deadline)
+                return fail(c, CKPT_EHIP, "snapshot %llu: commit record not written after 120 s", (unsigned long long)r.id);
+            std::this_thread::sleep_for(std::chrono::microseconds(50));
+        }
     }
     return CKPT_OK;
 }
@@ -938,10 +991,17 @@ void free_ctx(ckpt_ctx* c)
     (void)hipFree(c->d_bad);
     (void)hipFree(c->d_area_done);
     for (int b = 0; b < 2; ++b) {
-        if (c->h_img[b] && c->img_map_bytes) (void)munmap(c->h_img[b], c->img_map_bytes);
-        else if (c->h_img[b]) (void)hipHostFree(c->h_img[b]);
+        if (c->file_map) {
+            // part of the file mapping
+        } else if (c->h_img[b] && c->img_map_bytes) {
+            (void)munmap(c->h_img[b], c->img_map_bytes);
+        } else if (c->h_img[b]) {
+            (void)hipHostFree(c->h_img[b]);
+        }
         if (c->h_sums[b]) (void)hipHostFree(c->h_sums[b]);
     }
+    if (c->file_map) (void)munmap(c->file_map, c->fhead.file_bytes);
+    if (c->file_fd >= 0) (void)::close(c->file_fd);
     if (c->h_bout) (void)hipHostFree(c->h_bout);
     if (c->h_bin) (void)hipHostFree(c->h_bin);
     if (c->h_bad) (void)hipHostFree(c->h_bad);
@@ -1167,6 +1227,114 @@ void rep_stop(ckpt_ctx* c)
     c->rep = nullptr;
 }
 
+// ---- image file (ckpt_image_file) ----
+
+uint64_t word_sum(const uint8_t* p, uint64_t n) // n a multiple of 8
+{
+    uint64_t s = 0;
+    for (uint64_t k = 0; k < n; k += 8) {
+        uint64_t w;
+        std::memcpy(&w, p + k, 8);
+        s += w;
+    }
+    return s;
+}
+
+FileRec* file_rec(const ckpt_ctx* c, int b) { return (FileRec*)(c->file_map + kRecOff + 512 * b); }
+
+void file_layout(const ckpt_ctx* c, FileHead* h)
+{
+    std::memset(h, 0, sizeof *h);
+    std::memcpy(h->magic, "CKPTFIL1", 8);
+    h->version = 1;
+    h->align = c->A;
+    h->chunk = c->C;
+    h->image_bytes = c->I;
+    h->n_chunks = c->n_chunks;
+    h->n_frag = (uint32_t)c->frags.size();
+    for (const Frag& f : c->frags) h->table_sum += f.off + f.nbytes + (f.dtype | ((uint64_t)f.cls << 32));
+    uint64_t o = kRecOff + 1024;
+    for (int b = 0; b < 2; ++b) {
+        h->sums_off[b] = round_up(o, 4096);
+        h->meta_off[b] = h->sums_off[b] + round_up(8 * c->n_chunks, 4096);
+        o = h->meta_off[b] + kMaxMeta;
+    }
+    for (int b = 0; b < 2; ++b) {
+        h->image_off[b] = round_up(o, 2ull << 20);
+        o = h->image_off[b] + round_up(c->I, 2ull << 20);
+    }
+    h->file_bytes = o;
+}
+
+uint64_t rec_checksum(const ckpt_ctx* c, const FileRec& r, int b)
+{
+    return r.seq + r.snap_id + r.step + r.meta_len + word_sum(c->file_map + c->fhead.sums_off[b], 8 * c->n_chunks) +
+           word_sum(c->file_map + c->fhead.meta_off[b], round_up(r.meta_len, 8));
+}
+
+bool rec_valid(const ckpt_ctx* c, int b)
+{
+    const FileRec* r = file_rec(c, b);
+    return __atomic_load_n(&r->state, __ATOMIC_ACQUIRE) == 1 && r->meta_len <= kMaxMeta &&
+           rec_checksum(c, *r, b) == r->rec_sum;
+}
+
+// Before image b is rewritten its record stops naming a snapshot.
+void file_invalidate(ckpt_ctx* c, int b) { __atomic_store_n(&file_rec(c, b)->state, (uint64_t)0, __ATOMIC_RELEASE); }
+
+// After the snapshot's last byte and its sums have landed: sums, caller
+// blob, then the record, its state last.
+void file_commit(ckpt_ctx* c, const PumpItem& it)
+{
+    const int b = it.buf;
+    std::memcpy(c->file_map + c->fhead.sums_off[b], c->h_sums[b], 8 * c->n_chunks);
+    const uint64_t len = it.meta ? it.meta->size() : 0;
+    uint8_t* meta = c->file_map + c->fhead.meta_off[b];
+    if (len) std::memcpy(meta, it.meta->data(), len);
+    std::memset(meta + len, 0, round_up(len, 8) - len);
+    FileRec* r = file_rec(c, b);
+    r->seq = ++c->file_seq;
+    r->snap_id = it.snap_id;
+    r->step = it.step;
+    r->meta_len = len;
+    r->rec_sum = rec_checksum(c, *r, b);
+    __atomic_store_n(&r->state, (uint64_t)1, __ATOMIC_RELEASE);
+}
+
+// Map the image file at registration (bounce mode): create it, or check an
+// existing one against this context's layout.
+ckpt_status open_image_file(ckpt_ctx* c)
+{
+    file_layout(c, &c->fhead);
+    const bool create = c->file_mode == CKPT_FILE_CREATE;
+    c->file_fd = ::open(c->file_path.c_str(), create ? (O_RDWR | O_CREAT | O_TRUNC) : O_RDWR, 0600);
+    if (c->file_fd < 0) return fail(c, CKPT_EHIP, "open %s: %s", c->file_path.c_str(), strerror(errno));
+    if (create) {
+        if (::ftruncate(c->file_fd, (off_t)c->fhead.file_bytes) != 0)
+            return fail(c, CKPT_ENOMEM, "ftruncate %s: %s", c->file_path.c_str(), strerror(errno));
+    } else {
+        struct stat st;
+        if (::fstat(c->file_fd, &st) != 0 || (uint64_t)st.st_size != c->fhead.file_bytes)
+            return fail(c, CKPT_EINVAL, "%s does not hold images of this layout", c->file_path.c_str());
+    }
+    void* m = ::mmap(nullptr, c->fhead.file_bytes, PROT_READ | PROT_WRITE, MAP_SHARED, c->file_fd, 0);
+    if (m == MAP_FAILED) return fail(c, CKPT_ENOMEM, "mmap %s: %s", c->file_path.c_str(), strerror(errno));
+    c->file_map = (uint8_t*)m;
+    (void)madvise(m, c->fhead.file_bytes, MADV_HUGEPAGE);
+    if (create) {
+        std::memcpy(c->file_map, &c->fhead, sizeof c->fhead);
+        std::memset(c->file_map + kRecOff, 0, 1024);
+    } else if (std::memcmp(c->file_map, &c->fhead, sizeof c->fhead) != 0) {
+        return fail(c, CKPT_EINVAL, "%s holds images of another layout (fragments, chunk or alignment differ)",
+                    c->file_path.c_str());
+    }
+    for (int b = 0; b < 2; ++b) {
+        c->h_img[b] = c->file_map + c->fhead.image_off[b];
+        if (create) parallel_zero(c->h_img[b], c->I); // fault the pages in now
+    }
+    return CKPT_OK;
+}
+
 // Bounce mode, issuer thread (see Pump).
 void pump_issue(ckpt_ctx* c)
 {
@@ -1181,9 +1349,16 @@ void pump_issue(ckpt_ctx* c)
             if (p->issue_q.empty()) return;
             it = p->issue_q.front();
             p->issue_q.pop_front();
+            if (it.record) { // no copy: handled by the drainer in order
+                p->drain_q.emplace_back(it, UINT64_MAX);
+                p->cv.notify_all();
+                continue;
+            }
             if (it.sums) {
-                // no ring slot: straight into the pinned sums array
-                bool ok = !p->failed;
+                // no ring slot: straight into the pinned sums array, once the
+                // drainer has written every earlier record that reads it
+                p->cv.wait(l, [&] { return p->stop || p->failed || p->rec_done[it.buf] >= it.need_rec; });
+                bool ok = !p->failed && !p->stop;
                 l.unlock();
                 if (ok)
                     ok = hsa_amd_memory_async_copy_on_engine(it.image, c->img_agent[0], it.staging, c->gpu_agent,
@@ -1261,6 +1436,19 @@ void pump_drain(ckpt_ctx* c)
         }
         const PumpItem& it = d.first;
         const uint64_t slot = d.second;
+        if (it.record) { // the snapshot's commit record in the image file
+            const auto deadline = std::chrono::steady_clock::now() + std::chrono::seconds(120);
+            while (!res_done(it.res, it.after_groups, true) && std::chrono::steady_clock::now() < deadline)
+                std::this_thread::sleep_for(std::chrono::microseconds(20));
+            if (res_done(it.res, it.after_groups, true) && !it.res->failed.load(std::memory_order_acquire)) {
+                file_commit(c, it);
+                it.res->recorded.store(true, std::memory_order_release);
+            }
+            std::lock_guard<std::mutex> l(p->m);
+            ++p->rec_done[it.buf];
+            p->cv.notify_all();
+            continue;
+        }
         bool free_slot = slot != UINT64_MAX, ok = free_slot;
         if (ok) {
             ok = poll_zero(it.res->copied[it.g], 120);
@@ -1272,6 +1460,9 @@ void pump_drain(ckpt_ctx* c)
                 while (!res_done(it.after, it.after_groups, true) && std::chrono::steady_clock::now() < deadline)
                     std::this_thread::sleep_for(std::chrono::microseconds(20));
             }
+            // The image's record (an older snapshot's) stops counting before
+            // the first byte of a new one lands.
+            if (ok && it.g == 0 && c->file_map) file_invalidate(c, it.buf);
             if (ok) c->pool->copy(it.image, c->h_bout + slot * unit, it.n);
             else free_slot = false; // the engine may still write it
         }
@@ -1459,8 +1650,14 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
         }
         c->img_map_bytes = round_up(c->I, 2ull << 20);
     }
+    if (c->file_mode >= 0) {
+        ckpt_status st = open_image_file(c);
+        if (st) return st;
+    }
     for (int b = 0; b < 2; ++b) {
-        if (c->bounce) {
+        if (c->file_map) {
+            // images live in the file
+        } else if (c->bounce) {
             void* m = mmap(nullptr, c->img_map_bytes, PROT_READ | PROT_WRITE, MAP_PRIVATE | MAP_ANONYMOUS, -1, 0);
             if (m == MAP_FAILED)
                 return fail(c, CKPT_ENOMEM, "host image of %llu bytes", (unsigned long long)c->img_map_bytes);
@@ -1470,7 +1667,7 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
             c->h_img[b] = nullptr;
             return fail(c, CKPT_ENOMEM, "pinned host image of %llu bytes", (unsigned long long)c->I);
         }
-        parallel_zero(c->h_img[b], c->I);
+        if (!c->file_map) parallel_zero(c->h_img[b], c->I);
         if (hipHostMalloc((void**)&c->h_sums[b], c->n_chunks * 8, hipHostMallocDefault) != hipSuccess) {
             c->h_sums[b] = nullptr;
             return fail(c, CKPT_ENOMEM, "pinned sums");
@@ -1525,6 +1722,35 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
     }
     HIPCHK(c, hipDeviceSynchronize());
     c->registered = true;
+    if (c->file_mode == CKPT_FILE_ADOPT) {
+        // The file's newest valid record becomes this context's committed snapshot.
+        int best = -1;
+        for (int b = 0; b < 2; ++b) {
+            if (!rec_valid(c, b)) continue;
+            c->file_seq = std::max(c->file_seq, file_rec(c, b)->seq);
+            if (best < 0 || file_rec(c, b)->seq > file_rec(c, best)->seq) best = b;
+        }
+        if (best >= 0) {
+            RecRes* res = nullptr;
+            ckpt_status st = get_res(c, &res);
+            if (st) return st;
+            const FileRec* fr = file_rec(c, best);
+            const uint64_t id = c->next_id++;
+            SnapRec& r = c->recs[id];
+            r.id = id;
+            r.step = fr->step;
+            r.buf = best;
+            r.res = res;
+            r.bounce = true;
+            r.file = true;
+            res->recorded.store(true, std::memory_order_relaxed);
+            r.committed = true; // nothing in flight: its signals are all 0
+            const uint8_t* meta = c->file_map + c->fhead.meta_off[best];
+            r.meta.assign(meta, meta + fr->meta_len);
+            std::memcpy(c->h_sums[best], c->file_map + c->fhead.sums_off[best], 8 * c->n_chunks);
+            c->holder[best] = id;
+        }
+    }
     return CKPT_OK;
 }
 
@@ -1579,8 +1805,10 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
     r.meta.assign((const uint8_t*)meta, (const uint8_t*)meta + meta_len);
     r.timed = c->timing;
     r.bounce = c->bounce;
+    r.file = c->file_map != nullptr;
     res->landed.store(0, std::memory_order_relaxed);
     res->failed.store(false, std::memory_order_relaxed);
+    res->recorded.store(false, std::memory_order_relaxed);
     c->holder[r.buf] = id;
     const int32_t stop = c->interrupt_next;
     c->interrupt_next = -1;
@@ -1673,9 +1901,19 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
         if (r.bounce) { // the pump issues the copies once a ring slot is free
             {
                 std::lock_guard<std::mutex> l(c->pump->m);
-                c->pump->issue_q.push_back(PumpItem{res, (uint32_t)g, false, himg + lo, staging_of(c, g), hi - lo,
-                                                    c->d_area_done + area, &res->h_seq[g], eng,
-                                                    g == 0 ? prev.res : nullptr, prev.groups_copied});
+                PumpItem it;
+                it.res = res;
+                it.g = (uint32_t)g;
+                it.image = himg + lo;
+                it.staging = staging_of(c, g);
+                it.n = hi - lo;
+                it.area_done = c->d_area_done + area;
+                it.seq = &res->h_seq[g];
+                it.engine = eng;
+                it.after = g == 0 ? prev.res : nullptr;
+                it.after_groups = prev.groups_copied;
+                it.buf = r.buf;
+                c->pump->issue_q.push_back(it);
             }
             c->pump->cv.notify_all();
             ++c->area_seq[area];
@@ -1709,9 +1947,28 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
         if (r.bounce) { // behind the snapshot's group copies
             {
                 std::lock_guard<std::mutex> l(c->pump->m);
-                c->pump->issue_q.push_back(PumpItem{res, 0, true, (uint8_t*)c->h_sums[r.buf],
-                                                    (const uint8_t*)res->d_sums, c->n_chunks * 8, nullptr, nullptr,
-                                                    c->d2h_engine[0], nullptr, 0});
+                PumpItem sums;
+                sums.res = res;
+                sums.sums = true;
+                sums.image = (uint8_t*)c->h_sums[r.buf];
+                sums.staging = (const uint8_t*)res->d_sums;
+                sums.n = c->n_chunks * 8;
+                sums.engine = c->d2h_engine[0];
+                sums.buf = r.buf;
+                sums.need_rec = c->pump->rec_pushed[r.buf];
+                c->pump->issue_q.push_back(sums);
+                if (c->file_map) { // then the commit record, once all of it has landed
+                    ++c->pump->rec_pushed[r.buf];
+                    PumpItem rec;
+                    rec.res = res;
+                    rec.after_groups = r.groups_copied;
+                    rec.buf = r.buf;
+                    rec.record = true;
+                    rec.snap_id = r.id;
+                    rec.step = r.step;
+                    rec.meta = std::make_shared<const std::vector<uint8_t>>(r.meta);
+                    c->pump->issue_q.push_back(std::move(rec));
+                }
             }
             c->pump->cv.notify_all();
             return CKPT_OK;
@@ -1984,6 +2241,30 @@ ckpt_status ckpt_debug_tile_plan(const uint64_t* nbytes, uint32_t n, uint64_t ch
     if (n_tiles) *n_tiles = p.n_tiles;
     if (tile_first) std::memcpy(tile_first, p.tile_first.data(), 4 * p.n_tiles);
     if (tile_last && tile_first) std::memcpy(tile_last, p.tile_last.data(), 4 * p.n_tiles);
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_image_file(ckpt_ctx* c, const char* path, uint32_t mode)
+{
+    if (!c || !path || !*path || mode > CKPT_FILE_ADOPT) return fail(c, CKPT_EINVAL, "bad image file arguments");
+    if (c->registered) return fail(c, CKPT_ESTATE, "tensors already registered");
+    if (!c->bounce_cfg) return fail(c, CKPT_EINVAL, "an image file needs bounce mode (bounce_bytes > 0)");
+    c->file_path = path;
+    c->file_mode = (int)mode;
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_latest(ckpt_ctx* c, uint64_t* snap_id, uint64_t* step)
+{
+    if (!c || !snap_id) return CKPT_EINVAL;
+    *snap_id = 0;
+    for (auto& kv : c->recs) {
+        SnapRec& r = kv.second;
+        if (query_committed(r) && c->holder[r.buf] == r.id && r.id > *snap_id) {
+            *snap_id = r.id;
+            if (step) *step = r.step;
+        }
+    }
     return CKPT_OK;
 }
 
