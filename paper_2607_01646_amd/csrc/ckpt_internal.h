@@ -25,10 +25,15 @@ struct Geometry {
     uint32_t tiles_per_chunk; // chunk_bytes >> tile_shift
 };
 
+// Partial sums per tile: each wave of a tile's workgroup sums its own slice.
+constexpr uint32_t kTileParts = 4;
+
 // The tile kernels.  Each covers tiles [t_lo, t_hi) and writes tile t's
-// word-sum to partials[t]; launches cover whole chunks.  grid_cap bounds the
-// workgroups (one per tile when the cap is larger).  Non-null t0/t1 are
-// timing events recorded around the dispatch itself.
+// word-sums to partials[t * kTileParts ...] (one per wave slice; partials
+// holds kTileParts entries per tile of the image); launches cover whole
+// chunks.  grid_cap bounds the workgroups (one per tile when the cap is
+// larger).  Non-null t0/t1 are timing events recorded around the dispatch
+// itself.
 //   pack:     fragment bytes -> image window; image byte x goes to dst + (x - dst_origin)
 //   scatter:  image window -> fragment bytes (image byte x read at src + (x - src_origin))
 //   checksum: image window only
@@ -45,7 +50,7 @@ hipError_t launch_checksum(const Geometry& g, uint64_t t_lo, uint64_t t_hi, cons
                            hipEvent_t t1 = nullptr);
 
 // Chunk sums of the chunks covered by tiles [t_lo, t_hi): sums_out[c] is the
-// sum of the chunk's tile sums.  With expected non-null, bad[c] is set to 1
+// sum of the partial sums of the chunk's tiles.  With expected non-null, bad[c] is set to 1
 // where sums_out[c] != expected[c] (and to 0 elsewhere).
 hipError_t launch_chunk_reduce(const Geometry& g, uint64_t t_lo, uint64_t t_hi, const unsigned long long* partials,
                                unsigned long long* sums_out, const unsigned long long* expected, uint8_t* bad,

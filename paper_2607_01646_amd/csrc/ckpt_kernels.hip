@@ -13,21 +13,23 @@
 //
 // Work split.  The image is cut into power-of-two tiles (8 KiB) that never
 // cross a chunk.  A workgroup of 256 lanes (4 wave64) takes one tile (or
-// tiles grid-stride when the grid is capped); each lane moves one batch of
-// two 16-byte vectors per tile, both loads issued before the stores.
-// Consecutive tiles go to consecutive workgroups, which the hardware deals
-// out round-robin over the 8 XCDs (measured faster than giving each XCD a
-// contiguous range).  A tile inside one 16-byte-aligned fragment
-// takes an unrolled non-temporal stream; otherwise each vector finds its
-// fragment (binary search over the tile's fragment offsets in LDS), loads
-// aligned 16-byte blocks and funnel-shifts them when the fragment is
-// misaligned, masks the fragment tail and writes zeros for padding.
-// Sum reduction: per lane in 64 bits, across the wave with lane shuffles,
-// across the 4 waves in LDS; one plain store of the tile's sum; then a small
-// second kernel adds the tile sums of each chunk (and, when checking,
-// compares with the stored sum).  The hot kernel thus has no atomics and no
-// device-scope fence: on gfx950 such a fence writes back and invalidates the
-// XCD's L2, which per tile would cost more than the tile's own traffic.
+// tiles grid-stride when the grid is capped); each wave owns a contiguous
+// quarter of it (2 KiB) and each lane moves two 16-byte vectors of that
+// slice, both loads issued before the stores.  Consecutive tiles go to
+// consecutive workgroups, which the hardware deals out round-robin over the
+// 8 XCDs (measured faster than giving each XCD a contiguous range).  A tile
+// inside one 16-byte-aligned fragment takes an unrolled non-temporal stream;
+// otherwise each vector finds its fragment (binary search over the tile's
+// fragment offsets in LDS), loads aligned 16-byte blocks and funnel-shifts
+// them when the fragment is misaligned, masks the fragment tail and writes
+// zeros for padding.
+// Sum reduction: per lane in 64 bits, across the wave with lane shuffles;
+// each wave stores its slice's sum (four partial sums per tile), with no
+// workgroup barrier on the streaming path.  A small second kernel adds the
+// partial sums of each chunk (and, when checking, compares with the stored
+// sum).  The hot kernel thus has no atomics and no device-scope fence: on
+// gfx950 such a fence writes back and invalidates the XCD's L2, which per
+// tile would cost more than the tile's own traffic.
 // Addition modulo 2^64 is associative and commutative, so any order of
 // tiles gives the same bits.
 #include <hip/hip_ext.h>
@@ -170,24 +172,26 @@ __device__ __forceinline__ void st(u32x4 v, u32x4* p)
     else *p = v;
 }
 
-// Streaming copy of nvec aligned 16-byte vectors with their sum.
-template <int BLOCK, int UNROLL, bool NTL, bool NTS>
-__device__ __forceinline__ unsigned long long stream_copy(const u32x4* __restrict__ s, u32x4* __restrict__ d,
-                                                          uint32_t nvec, uint32_t tid)
+// Streaming copy of the aligned 16-byte vectors [v0, v1) with their sum:
+// lane l takes v0 + l, v0 + l + 64, ..., UNROLL loads in flight before the
+// stores, so each wave moves contiguous 1 KiB runs.
+template <int UNROLL, bool NTL, bool NTS>
+__device__ __forceinline__ unsigned long long slice_copy(const u32x4* __restrict__ s, u32x4* __restrict__ d,
+                                                         uint32_t v0, uint32_t v1, uint32_t lane)
 {
     unsigned long long acc = 0;
-    uint32_t v = tid;
-    for (; v + (UNROLL - 1) * BLOCK < nvec; v += UNROLL * BLOCK) {
+    uint32_t v = v0 + lane;
+    for (; v + (UNROLL - 1) * 64 < v1; v += UNROLL * 64) {
         u32x4 r[UNROLL];
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u) r[u] = ld<NTL>(s + v + u * BLOCK);
+        for (int u = 0; u < UNROLL; ++u) r[u] = ld<NTL>(s + v + u * 64);
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u) {
-            st<NTS>(r[u], d + v + u * BLOCK);
+            st<NTS>(r[u], d + v + u * 64);
             acc += vsum(r[u]);
         }
     }
-    for (; v < nvec; v += BLOCK) {
+    for (; v < v1; v += 64) {
         const u32x4 r = ld<NTL>(s + v);
         st<NTS>(r, d + v);
         acc += vsum(r);
@@ -195,19 +199,20 @@ __device__ __forceinline__ unsigned long long stream_copy(const u32x4* __restric
     return acc;
 }
 
-template <int BLOCK, int UNROLL, bool NTL>
-__device__ __forceinline__ unsigned long long stream_sum(const u32x4* __restrict__ s, uint32_t nvec, uint32_t tid)
+template <int UNROLL, bool NTL>
+__device__ __forceinline__ unsigned long long slice_sum(const u32x4* __restrict__ s, uint32_t v0, uint32_t v1,
+                                                        uint32_t lane)
 {
     unsigned long long acc = 0;
-    uint32_t v = tid;
-    for (; v + (UNROLL - 1) * BLOCK < nvec; v += UNROLL * BLOCK) {
+    uint32_t v = v0 + lane;
+    for (; v + (UNROLL - 1) * 64 < v1; v += UNROLL * 64) {
         u32x4 r[UNROLL];
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u) r[u] = ld<NTL>(s + v + u * BLOCK);
+        for (int u = 0; u < UNROLL; ++u) r[u] = ld<NTL>(s + v + u * 64);
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u) acc += vsum(r[u]);
     }
-    for (; v < nvec; v += BLOCK) acc += vsum(ld<NTL>(s + v));
+    for (; v < v1; v += 64) acc += vsum(ld<NTL>(s + v));
     return acc;
 }
 
@@ -218,12 +223,19 @@ __device__ __forceinline__ unsigned long long shfl_xor64(unsigned long long v, i
     return ((unsigned long long)hi << 32) | lo;
 }
 
+// Sum over one wave; every lane gets the result.
+__device__ __forceinline__ unsigned long long wave_sum(unsigned long long v)
+{
+#pragma unroll
+    for (int m = 32; m > 0; m >>= 1) v += shfl_xor64(v, m);
+    return v;
+}
+
 // Sum over the workgroup; the result is valid in thread 0.
 template <int BLOCK>
 __device__ __forceinline__ unsigned long long block_sum(unsigned long long v, unsigned long long* s_red)
 {
-#pragma unroll
-    for (int m = 32; m > 0; m >>= 1) v += shfl_xor64(v, m);
+    v = wave_sum(v);
     const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     if (lane == 0) s_red[wave] = v;
     __syncthreads();
@@ -273,19 +285,25 @@ __device__ __forceinline__ uint64_t remap_block(uint32_t b, uint32_t n)
 template <int MODE, int BLOCK = kBlock, int UNROLL = kUnroll, bool NTL = true, bool NTS = true, bool REMAP = false>
 __global__ __launch_bounds__(BLOCK) void tile_kernel(Args a)
 {
-    __shared__ unsigned long long s_red[BLOCK / 64];
+    static_assert(BLOCK / 64 == kTileParts, "one partial sum per wave");
+    constexpr uint32_t WAVES = BLOCK / 64;
     __shared__ uint64_t s_off[kLdsFrags];
-    const uint32_t tid = threadIdx.x;
+    const uint32_t tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const uint64_t first = REMAP ? remap_block(blockIdx.x, gridDim.x) : blockIdx.x;
+    // Wave w owns vectors [w * slice, (w + 1) * slice) of the tile.
+    const uint32_t tile_vecs = 1u << (a.g.tile_shift - 4);
+    const uint32_t slice = (tile_vecs + WAVES - 1) / WAVES;
     for (uint64_t t = a.t_lo + first; t < a.t_hi; t += gridDim.x) {
         const uint64_t base = t << a.g.tile_shift;
         uint64_t end = base + (1ull << a.g.tile_shift);
         if (end > a.g.image_bytes) end = a.g.image_bytes;
         const uint32_t nvec = (uint32_t)((end - base) >> 4);
+        const uint32_t v0 = w * slice;
+        const uint32_t v1 = v0 + slice < nvec ? v0 + slice : nvec;
         uint8_t* win = a.img + (base - a.origin);
         unsigned long long acc = 0;
         if (MODE == VERIFY) {
-            acc = stream_sum<BLOCK, UNROLL, NTL>(reinterpret_cast<const u32x4*>(win), nvec, tid);
+            acc = slice_sum<UNROLL, NTL>(reinterpret_cast<const u32x4*>(win), v0, v1, lane);
         } else {
             const uint32_t f0 = a.tile_first[t], f1 = a.tile_last[t];
             if (f0 == f1) {
@@ -294,53 +312,55 @@ __global__ __launch_bounds__(BLOCK) void tile_kernel(Args a)
                 if ((F.ptr & 15) == 0 && p0 + (end - base) <= F.nbytes) {
                     u32x4* fr = reinterpret_cast<u32x4*>(F.ptr + p0);
                     if (MODE == PACK)
-                        acc = stream_copy<BLOCK, UNROLL, NTL, NTS>(fr, reinterpret_cast<u32x4*>(win), nvec, tid);
+                        acc = slice_copy<UNROLL, NTL, NTS>(fr, reinterpret_cast<u32x4*>(win), v0, v1, lane);
                     else
-                        acc = stream_copy<BLOCK, UNROLL, NTL, NTS>(reinterpret_cast<const u32x4*>(win), fr, nvec, tid);
+                        acc = slice_copy<UNROLL, NTL, NTS>(reinterpret_cast<const u32x4*>(win), fr, v0, v1, lane);
                 } else {
-                    for (uint32_t v = tid; v < nvec; v += BLOCK) {
+                    for (uint32_t v = v0 + lane; v < v1; v += 64) {
                         const uint64_t p = p0 + 16ull * v;
-                        u32x4* w = reinterpret_cast<u32x4*>(win) + v;
+                        u32x4* wv = reinterpret_cast<u32x4*>(win) + v;
                         if (MODE == PACK) {
                             const u32x4 r = fetch_general(F.ptr, F.nbytes, p);
-                            __builtin_nontemporal_store(r, w);
+                            __builtin_nontemporal_store(r, wv);
                             acc += vsum(r);
                         } else {
-                            const u32x4 r = __builtin_nontemporal_load(w);
+                            const u32x4 r = __builtin_nontemporal_load(wv);
                             store_general(F.ptr, F.nbytes, p, r);
                             acc += vsum(r);
                         }
                     }
                 }
             } else {
+                // Several fragments: their offsets go to LDS for the search.
+                // Both barriers are workgroup-uniform (f0, f1 depend on t only);
+                // the first keeps the previous tile's readers ahead of the refill.
                 const uint32_t nf = f1 - f0 + 1;
                 const bool in_lds = nf <= (uint32_t)kLdsFrags;
+                __syncthreads();
                 if (in_lds) {
                     for (uint32_t k = tid; k < nf; k += BLOCK) s_off[k] = a.frags[f0 + k].off;
                 }
                 __syncthreads();
-                for (uint32_t v = tid; v < nvec; v += BLOCK) {
+                for (uint32_t v = v0 + lane; v < v1; v += 64) {
                     const uint64_t x = base + 16ull * v;
                     const uint32_t i = in_lds ? f0 + find_frag_lds(s_off, nf, x) : find_frag_global(a.frags, f0, f1, x);
                     const FragDev F = a.frags[i];
                     const uint64_t p = x - F.off;
-                    u32x4* w = reinterpret_cast<u32x4*>(win) + v;
+                    u32x4* wv = reinterpret_cast<u32x4*>(win) + v;
                     if (MODE == PACK) {
                         const u32x4 r = fetch_general(F.ptr, F.nbytes, p);
-                        __builtin_nontemporal_store(r, w);
+                        __builtin_nontemporal_store(r, wv);
                         acc += vsum(r);
                     } else {
-                        const u32x4 r = __builtin_nontemporal_load(w);
+                        const u32x4 r = __builtin_nontemporal_load(wv);
                         store_general(F.ptr, F.nbytes, p, r);
                         acc += vsum(r);
                     }
                 }
             }
         }
-        // block_sum's barriers also retire every lane's use of s_off before
-        // the next tile refills it.
-        const unsigned long long tile_sum = block_sum<BLOCK>(acc, s_red);
-        if (tid == 0) a.partials[t] = tile_sum;
+        acc = wave_sum(acc);
+        if (lane == 0) a.partials[t * WAVES + w] = acc;
     }
 }
 
@@ -354,7 +374,7 @@ __global__ __launch_bounds__(kBlock) void chunk_reduce_kernel(ReduceArgs r)
     uint64_t t1 = t0 + r.tiles_per_chunk;
     if (t1 > r.n_tiles) t1 = r.n_tiles;
     unsigned long long acc = 0;
-    for (uint64_t t = t0 + threadIdx.x; t < t1; t += kBlock) acc += r.partials[t];
+    for (uint64_t k = t0 * kTileParts + threadIdx.x; k < t1 * kTileParts; k += kBlock) acc += r.partials[k];
     const unsigned long long s = block_sum<kBlock>(acc, s_red);
     if (threadIdx.x == 0) {
         r.sums_out[c] = s;

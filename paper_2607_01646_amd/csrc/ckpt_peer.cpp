@@ -144,7 +144,7 @@ bool setup_geometry(ckpt_peer* p, const WireHead& h, const std::vector<uint64_t>
     }
     ok = ok && hipHostMalloc((void**)&p->h_bad, p->n, hipHostMallocDefault) == hipSuccess &&
          hipMalloc((void**)&p->d_ring, 2 * std::min(unit, p->R)) == hipSuccess &&
-         hipMalloc((void**)&p->d_partials, 8 * p->geo.n_tiles) == hipSuccess &&
+         hipMalloc((void**)&p->d_partials, 8 * kTileParts * p->geo.n_tiles) == hipSuccess &&
          hipMalloc((void**)&p->d_expected, 8 * p->n) == hipSuccess &&
          hipMalloc((void**)&p->d_recomputed, 8 * p->n) == hipSuccess && hipMalloc((void**)&p->d_bad, p->n) == hipSuccess &&
          hipStreamCreateWithFlags(&p->s_copy, hipStreamNonBlocking) == hipSuccess &&

@@ -336,7 +336,7 @@ struct ckpt_ctx {
     uint32_t* d_tile_first = nullptr;
     uint32_t* d_tile_last = nullptr;
     uint8_t* d_staging = nullptr;
-    unsigned long long* d_partials = nullptr; // [2][n_tiles] tile sums: pack, check
+    unsigned long long* d_partials = nullptr; // [2][n_tiles * kTileParts] tile partial sums: pack, check
     unsigned long long* d_expected = nullptr;
     unsigned long long* d_recomputed = nullptr;
     uint8_t* d_bad = nullptr;
@@ -891,7 +891,7 @@ ckpt_status run_check(ckpt_ctx* c, uint64_t snap_id, hipStream_t stream, bool sc
     const int op = scatter ? CKPT_OP_RESTORE : CKPT_OP_VERIFY;
     const bool timed = c->timing;
     const uint64_t unit = L.G * c->C;
-    unsigned long long* partials = c->d_partials + c->geo.n_tiles;
+    unsigned long long* partials = c->d_partials + c->geo.n_tiles * kTileParts;
     HIPCHK(c, hipMemcpyAsync(c->d_expected, c->h_sums[b], c->n_chunks * 8, hipMemcpyHostToDevice, L.s_copy));
     if (scatter) {
         HIPCHK(c, hipEventRecord(c->ev_trigger, stream));
@@ -1626,7 +1626,7 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
     ALLOC(c->d_frags, n * sizeof(FragDev));
     ALLOC(c->d_tile_first, nt * 4);
     ALLOC(c->d_tile_last, nt * 4);
-    ALLOC(c->d_partials, 2 * nt * 8);
+    ALLOC(c->d_partials, 2 * nt * kTileParts * 8);
     ALLOC(c->d_expected, c->n_chunks * 8);
     ALLOC(c->d_recomputed, c->n_chunks * 8);
     ALLOC(c->d_bad, c->n_chunks);
