@@ -401,10 +401,14 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
 
     def run(with_snap, R, steps):
         times = []
+        snap = None
         for k in range(steps):
             torch.cuda.synchronize()
             t0 = time.perf_counter()
-            snap = ck.snapshot(step=k) if with_snap else None
+            if with_snap:
+                if snap is not None:  # one snapshot in flight: a D2H longer than the step shows up here
+                    ck.wait_committed(snap)
+                snap = ck.snapshot(step=k)
             for _ in range(R):
                 torch.matmul(x, w)
             if with_snap:

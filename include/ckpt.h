@@ -64,7 +64,7 @@ typedef int32_t ckpt_status;
 #define CKPT_EHIP (-4)     /* a HIP runtime call failed; see ckpt_last_error() */
 #define CKPT_ECORRUPT (-5) /* one or more chunk sums did not match; list filled */
 #define CKPT_ENOSNAP (-6)  /* no committed snapshot (or the requested one is gone) */
-#define CKPT_EBUSY (-7)    /* both host buffers are still in flight */
+#define CKPT_EBUSY (-7)    /* the previous snapshot has not committed (or its replica is being sent) */
 #define CKPT_ERANGE (-8)   /* snapshot id unknown or no longer retained */
 
 /* ckpt_wait modes */
@@ -132,13 +132,17 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* ctx, const ckpt_tensor* t, uint32_t 
  * after all work already enqueued on after_stream (call it right after the
  * previous optimizer step).  Packs every fragment with its chunk sums into
  * device staging on the library's side stream, then copies the image and the
- * sums chunk group by chunk group into the pinned host buffer that does not
- * hold the newest committed snapshot.  Returns at once with *snap_id
+ * sums chunk group by chunk group into the host image that does not hold
+ * the newest committed snapshot.  One image always holds the newest
+ * committed snapshot and the other receives the one in flight, so a
+ * snapshot starts only once the previous one has committed (the caller's
+ * wait before the optimizer step, Sec. VI-A, normally ensures that; with
+ * CKPT_WAIT_COMMITTED it can wait explicitly).  Returns at once with *snap_id
  * (increasing from 1).  meta (may be NULL when meta_len == 0) is the caller's
  * envelope blob -- parallel configuration, RNG states -- copied before the
  * call returns; at most 1 MiB.
- * Errors: ESTATE (nothing registered), EBUSY (two earlier snapshots are
- * both still uncommitted), EINVAL, EHIP. */
+ * Errors: ESTATE (nothing registered), EBUSY (the previous snapshot has
+ * not committed yet), EINVAL, EHIP. */
 ckpt_status ckpt_snapshot_async(ckpt_ctx* ctx, void* after_stream, uint64_t step, const void* meta,
                                 uint32_t meta_len, uint64_t* snap_id);
 

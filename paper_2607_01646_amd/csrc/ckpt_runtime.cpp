@@ -22,13 +22,12 @@
 // run as a copy kernel on the compute units, competing with the pack and
 // with the training step.
 //
-// The two pinned images alternate: a snapshot takes the image that does not
-// hold the newest live (in flight or committed) snapshot.  When that one has
-// not committed yet, every image copy of the new snapshot also waits for its
-// commit (its chunk-sum copy and its last staging-counter copy are listed as
-// DMA dependencies), so a committed image exists at every point once the
-// first snapshot has committed, and an interrupted snapshot is never the
-// recovery point (invariant I4 of Sec. V-C).
+// The two images alternate: one holds the newest committed snapshot, the
+// other receives the snapshot in flight, and a new snapshot may start only
+// once the previous one has committed (CKPT_EBUSY otherwise).  So a
+// committed image exists at every point once the first snapshot has
+// committed, and an interrupted snapshot is never the recovery point
+// (invariant I4 of Sec. V-C).
 //
 // Recovery (Sec. V-C third stage, Sec. VI-E) reverses the path group by
 // group: DMA host image -> staging on the copy stream, then the scatter
@@ -212,9 +211,7 @@ struct PumpItem {
     uint64_t* area_done = nullptr;   // group: device counter bumped once the staging area has been read
     const uint64_t* seq = nullptr;   // group: pinned, the value it is set to
     hsa_amd_sdma_engine_id_t engine{};
-    const RecRes* after = nullptr;   // first group: the snapshot that must have committed before this image is
-                                     // written
-    uint32_t after_groups = 0;       // group copies of that snapshot (record: of this item's own snapshot)
+    uint32_t groups = 0;             // record: the snapshot's group copies
     int buf = 0;                     // host image written
     bool record = false;             // image file: write the snapshot's commit record (no copy)
     uint64_t need_rec = 0;           // sums: records of image buf that must be written before its sums array is reused
@@ -722,13 +719,15 @@ bool pump_failed(ckpt_ctx* c, std::string* why)
 // Wait (bounded) until every copy of a snapshot has finished.
 ckpt_status wait_copies(ckpt_ctx* c, SnapRec& r)
 {
-    const uint64_t limit = 120 * c->ts_freq; // two minutes of system-timestamp ticks
-    if (hsa_signal_wait_scacquire(r.res->done, HSA_SIGNAL_CONDITION_EQ, 0, limit, HSA_WAIT_STATE_BLOCKED) != 0)
-        return fail(c, CKPT_EHIP, "snapshot %llu: chunk sums not copied after 120 s", (unsigned long long)r.id);
+    // The wait's timeout is only a hint (in system-timestamp ticks): wait in
+    // one-second slices against our own deadline.
+    const auto deadline = std::chrono::steady_clock::now() + std::chrono::seconds(120);
+    while (hsa_signal_wait_scacquire(r.res->done, HSA_SIGNAL_CONDITION_EQ, 0, c->ts_freq, HSA_WAIT_STATE_BLOCKED) != 0)
+        if (std::chrono::steady_clock::now() > deadline)
+            return fail(c, CKPT_EHIP, "snapshot %llu: chunk sums not copied after 120 s", (unsigned long long)r.id);
     // The per-group signals have the GPU as their only waiter; the host
     // polls their values (the engines run the groups in order, so this
     // rarely finds one still pending once the sums have landed).
-    const auto deadline = std::chrono::steady_clock::now() + std::chrono::seconds(120);
     for (uint32_t g = 0; g < r.groups_copied; ++g) {
         while (hsa_signal_load_scacquire(r.res->flagged[g]) != 0) {
             if (std::chrono::steady_clock::now() > deadline)
@@ -1013,21 +1012,12 @@ void free_ctx(ckpt_ctx* c)
 // Issue one SDMA copy; on failure the dependency chain of the snapshot is
 // released so no engine is left polling.
 ckpt_status dma(ckpt_ctx* c, void* dst, hsa_agent_t dst_agent, const void* src, hsa_agent_t src_agent, uint64_t n,
-                const hsa_signal_t* dep, hsa_signal_t completion, hsa_amd_sdma_engine_id_t engine, uint32_t n_dep = 1)
+                const hsa_signal_t* dep, hsa_signal_t completion, hsa_amd_sdma_engine_id_t engine)
 {
-    HSACHK(c, hsa_amd_memory_async_copy_on_engine(dst, dst_agent, src, src_agent, n, dep ? n_dep : 0, dep, completion,
+    HSACHK(c, hsa_amd_memory_async_copy_on_engine(dst, dst_agent, src, src_agent, n, dep ? 1 : 0, dep, completion,
                                                   engine, true));
     return CKPT_OK;
 }
-
-// The snapshot a new one must not overtake: the newest live one when it has
-// not committed yet.  Its completion signals (the chunk-sum copy and the
-// last staging-counter copy, whose engine runs them in order, so it implies
-// every earlier one) are 0 exactly when it has committed.
-struct PrevSnap {
-    const RecRes* res = nullptr;
-    uint32_t groups_copied = 0;
-};
 
 // Poll a signal that only the GPU side waits on until it reads 0.
 bool poll_zero(hsa_signal_t sig, int seconds)
@@ -1310,8 +1300,11 @@ ckpt_status open_image_file(ckpt_ctx* c)
     c->file_fd = ::open(c->file_path.c_str(), create ? (O_RDWR | O_CREAT | O_TRUNC) : O_RDWR, 0600);
     if (c->file_fd < 0) return fail(c, CKPT_EHIP, "open %s: %s", c->file_path.c_str(), strerror(errno));
     if (create) {
-        if (::ftruncate(c->file_fd, (off_t)c->fhead.file_bytes) != 0)
-            return fail(c, CKPT_ENOMEM, "ftruncate %s: %s", c->file_path.c_str(), strerror(errno));
+        // Reserve the space now: a sparse file on a full tmpfs would fault
+        // (SIGBUS) on first write instead of failing here.
+        const int e = ::posix_fallocate(c->file_fd, 0, (off_t)c->fhead.file_bytes);
+        if (e != 0) return fail(c, CKPT_ENOMEM, "reserving %llu bytes for %s: %s",
+                                (unsigned long long)c->fhead.file_bytes, c->file_path.c_str(), strerror(e));
     } else {
         struct stat st;
         if (::fstat(c->file_fd, &st) != 0 || (uint64_t)st.st_size != c->fhead.file_bytes)
@@ -1438,9 +1431,9 @@ void pump_drain(ckpt_ctx* c)
         const uint64_t slot = d.second;
         if (it.record) { // the snapshot's commit record in the image file
             const auto deadline = std::chrono::steady_clock::now() + std::chrono::seconds(120);
-            while (!res_done(it.res, it.after_groups, true) && std::chrono::steady_clock::now() < deadline)
+            while (!res_done(it.res, it.groups, true) && std::chrono::steady_clock::now() < deadline)
                 std::this_thread::sleep_for(std::chrono::microseconds(20));
-            if (res_done(it.res, it.after_groups, true) && !it.res->failed.load(std::memory_order_acquire)) {
+            if (res_done(it.res, it.groups, true) && !it.res->failed.load(std::memory_order_acquire)) {
                 file_commit(c, it);
                 it.res->recorded.store(true, std::memory_order_release);
             }
@@ -1452,14 +1445,6 @@ void pump_drain(ckpt_ctx* c)
         bool free_slot = slot != UINT64_MAX, ok = free_slot;
         if (ok) {
             ok = poll_zero(it.res->copied[it.g], 120);
-            // Only once the previous snapshot has committed (all its groups,
-            // drained before this one's, its staging counters and its sums)
-            // may the older image be overwritten.
-            if (ok && it.after) {
-                const auto deadline = std::chrono::steady_clock::now() + std::chrono::seconds(120);
-                while (!res_done(it.after, it.after_groups, true) && std::chrono::steady_clock::now() < deadline)
-                    std::this_thread::sleep_for(std::chrono::microseconds(20));
-            }
             // The image's record (an older snapshot's) stops counting before
             // the first byte of a new one lands.
             if (ok && it.g == 0 && c->file_map) file_invalidate(c, it.buf);
@@ -1494,8 +1479,7 @@ void stop_pump(ckpt_ctx* c)
     c->pump = nullptr;
 }
 
-ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop,
-                           const PrevSnap& prev);
+ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop);
 
 } // namespace
 
@@ -1772,7 +1756,10 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
         if (!query_committed(r)) ++in_flight;
         if (!newest_live || r.id > newest_live->id) newest_live = &r;
     }
-    if (in_flight >= 2) return fail(c, CKPT_EBUSY, "both host images are still being written");
+    // One image always holds the newest committed snapshot and the other
+    // receives the one in flight (Sec. VI-A): a snapshot may start only once
+    // the previous one has committed.
+    if (in_flight >= 1) return fail(c, CKPT_EBUSY, "the previous snapshot has not committed yet");
     // Target: the image not holding the newest live snapshot; with no live
     // snapshot, an image that holds nothing committed.
     int buf = 0;
@@ -1822,15 +1809,7 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
 
     // On an error below, copies not issued never raise their signals, and
     // the snapshot is marked interrupted.
-    // A committed image must exist at every point (Sec. VI-A; invariant I4):
-    // this snapshot writes the image of the older committed one, so none of
-    // its bytes may land there before the newest live snapshot has committed.
-    PrevSnap prev;
-    if (newest_live && !query_committed(*newest_live)) {
-        prev.res = newest_live->res;
-        prev.groups_copied = newest_live->groups_copied;
-    }
-    st = issue_snapshot(c, r, after, n_copy, stop, prev);
+    st = issue_snapshot(c, r, after, n_copy, stop);
     if (st) {
         r.aborted = true;
         r.timed = false;
@@ -1863,8 +1842,7 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
 
 namespace {
 
-ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop,
-                           const PrevSnap& prev)
+ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop)
 {
     RecRes* res = r.res;
     uint8_t* himg = c->h_img[r.buf];
@@ -1910,8 +1888,6 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
                 it.area_done = c->d_area_done + area;
                 it.seq = &res->h_seq[g];
                 it.engine = eng;
-                it.after = g == 0 ? prev.res : nullptr;
-                it.after_groups = prev.groups_copied;
                 it.buf = r.buf;
                 c->pump->issue_q.push_back(it);
             }
@@ -1919,13 +1895,7 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
             ++c->area_seq[area];
             continue;
         }
-        hsa_signal_t deps[3] = {res->dep[g], {0}, {0}};
-        uint32_t n_dep = 1;
-        if (prev.res) {
-            deps[n_dep++] = prev.res->done;
-            if (prev.groups_copied) deps[n_dep++] = prev.res->flagged[prev.groups_copied - 1];
-        }
-        st = dma(c, himg + lo, host, staging_of(c, g), c->gpu_agent, hi - lo, deps, res->copied[g], eng, n_dep);
+        st = dma(c, himg + lo, host, staging_of(c, g), c->gpu_agent, hi - lo, &res->dep[g], res->copied[g], eng);
         if (!st)
             st = dma(c, c->d_area_done + area, c->gpu_agent, &res->h_seq[g], host, 8, &res->copied[g],
                      res->flagged[g], c->h2d_engine);
@@ -1961,7 +1931,7 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
                     ++c->pump->rec_pushed[r.buf];
                     PumpItem rec;
                     rec.res = res;
-                    rec.after_groups = r.groups_copied;
+                    rec.groups = r.groups_copied;
                     rec.buf = r.buf;
                     rec.record = true;
                     rec.snap_id = r.id;

@@ -43,9 +43,10 @@ def test_large_groups_use_the_copy_pool():
 
 
 def test_consecutive_snapshots_reuse_slots_and_images():
-    """Six snapshots of changing state, two in flight at a time, through a
-    two-slot ring: each committed image equals the oracle's pack of the state
-    it captured, and the older image keeps its own snapshot."""
+    """Six snapshots of changing state through a two-slot ring, each issued
+    right after the previous one committed: each committed image equals the
+    oracle's pack of the state it captured, and the older image keeps its own
+    snapshot."""
     torch.manual_seed(5)
     tensors = [torch.randn(n, device="cuda") for n in (70_001, 1 << 18, 3, 1 << 19, 12_345)]
     chunk = 1 << 16
@@ -58,8 +59,8 @@ def test_consecutive_snapshots_reuse_slots_and_images():
         for t in tensors:
             t.mul_(-1.5).add_(0.25)
         snaps.append(s)
+        ck.wait_committed(s)
         if step % 2 == 1:
-            ck.wait_committed(s)
             for k in (step - 1, step):
                 img, sums = ck.host_image(snaps[k])
                 want, _, _ = O.pack(states[k], 256, chunk)
@@ -148,9 +149,8 @@ def test_verify_beside_an_inflight_bounce_snapshot():
     ck.close()
 
 
-def test_a_committed_image_exists_while_two_bounce_snapshots_are_in_flight():
-    for _ in range(3):
-        check_committed_image_survives(1 << 25)
+def test_a_committed_image_exists_while_a_bounce_snapshot_is_in_flight():
+    check_committed_image_survives(1 << 25)
 
 
 def test_bounce_configuration_errors():

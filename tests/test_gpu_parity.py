@@ -149,54 +149,83 @@ def _step_state(n_frag=48, numel=1 << 20, seed=41):
     return [torch.randn(numel, generator=g, device="cuda") for _ in range(n_frag)]
 
 
+def _hold(stream, ms=40.0):
+    """Keep `stream` busy for about `ms` milliseconds (a chain of fp32
+    matmuls), so that a snapshot triggered after it starts packing late."""
+    a = torch.randn(4096, 4096, device="cuda")
+    with torch.cuda.stream(stream):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        b = a @ a
+        e1.record()
+    e1.synchronize()
+    n = max(1, int(ms / max(e0.elapsed_time(e1), 1e-3)))
+    with torch.cuda.stream(stream):
+        for _ in range(n):
+            b = a @ b
+    return b
+
+
 def test_gate_orders_optimizer_after_capture():
-    """The wait before the optimizer step: an in-place update launched right
-    after ckpt_wait(CAPTURED) must not leak into the snapshot.  A first
-    snapshot keeps the copy engine busy so the second snapshot's pack is
-    delayed behind it -- the window in which an ungated update would win."""
+    """The wait before the optimizer step: an in-place update launched on
+    another stream right after ckpt_wait(CAPTURED) must not leak into the
+    snapshot, although the snapshot's trigger sits behind ~40 ms of work on
+    the training stream, so its pack starts long after the update could."""
     tensors = _step_state(n_frag=96)
     ck = P.Checkpointer(tensors, chunk_bytes=1 << 20)
-    before = [host_bytes(t) for t in tensors]  # values at both snapshots
-    ck.snapshot(step=1)
-    s2 = ck.snapshot(step=2)  # its pack waits for snapshot 1's copies (~7 ms)
-    ck.wait_captured(s2, 0, len(tensors))
-    for t in tensors:
-        t.add_(1.0)  # the "optimizer step"
-    ck.wait_committed(s2)
-    img, _ = ck.host_image(s2)
+    main, side = torch.cuda.current_stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    before = [host_bytes(t) for t in tensors]
+    keep = _hold(main)
+    s = ck.snapshot(step=1, stream=main)
+    ck.wait_captured(s, 0, len(tensors), stream=side)
+    with torch.cuda.stream(side):
+        for t in tensors:
+            t.add_(1.0)  # the "optimizer step"
+    ck.wait_committed(s)
+    img, _ = ck.host_image(s)
     want, _, _ = O.pack(before, 256, 1 << 20)
     assert np.array_equal(img, want)
     # Partial gate: waiting only for fragments [0, 8) protects those.
+    torch.cuda.synchronize()
     before = [host_bytes(t) for t in tensors]
-    ck.snapshot(step=3)
-    s4 = ck.snapshot(step=4)
-    ck.wait_captured(s4, 0, 8)
-    for t in tensors[:8]:
-        t.mul_(2.0)
-    ck.wait_committed(s4)
-    img, _ = ck.host_image(s4)
+    keep = _hold(main)
+    s = ck.snapshot(step=2, stream=main)
+    ck.wait_captured(s, 0, 8, stream=side)
+    with torch.cuda.stream(side):
+        for t in tensors[:8]:
+            t.mul_(2.0)
+    ck.wait_committed(s)
+    img, _ = ck.host_image(s)
     off = ck.offsets
     for i in range(8):
         o = int(off[i])
         assert np.array_equal(img[o:o + before[i].size], before[i])
+    torch.cuda.synchronize()
+    del keep
     ck.close()
 
 
 def test_gate_negative_control_detects_the_race():
-    """Same as above without the wait: the update now lands before the
-    delayed pack, so the snapshot differs from the pre-update state.  Shows
-    the gate test can see a missing wait."""
+    """Same without the wait: the update on the other stream runs while the
+    pack still waits for its trigger, so the snapshot holds updated values.
+    Shows the gate test can see a missing wait."""
     tensors = _step_state(n_frag=96)
     ck = P.Checkpointer(tensors, chunk_bytes=1 << 20)
+    main, side = torch.cuda.current_stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
     before = [host_bytes(t) for t in tensors]
-    ck.snapshot(step=1)
-    s2 = ck.snapshot(step=2)
-    for t in tensors:
-        t.add_(1.0)  # no ckpt_wait: races with the delayed pack
-    ck.wait_committed(s2)
-    img, _ = ck.host_image(s2)
+    keep = _hold(main)
+    s = ck.snapshot(step=1, stream=main)
+    with torch.cuda.stream(side):
+        for t in tensors:
+            t.add_(1.0)  # no ckpt_wait: runs before the delayed pack
+    ck.wait_committed(s)
+    img, _ = ck.host_image(s)
     want, _, _ = O.pack(before, 256, 1 << 20)
     assert not np.array_equal(img, want)
+    torch.cuda.synchronize()
+    del keep
     ck.close()
 
 
@@ -235,10 +264,11 @@ def test_ping_pong_roles_and_busy():
     tensors = _step_state(n_frag=64, numel=1 << 20)  # 256 MiB: copies take ~5 ms
     ck = P.Checkpointer(tensors, chunk_bytes=1 << 22)
     s1 = ck.snapshot(step=1)
-    s2 = ck.snapshot(step=2)
-    with pytest.raises(P.CkptError) as e:  # both images in flight
-        ck.snapshot(step=3)
+    with pytest.raises(P.CkptError) as e:  # one snapshot in flight at a time
+        ck.snapshot(step=2)
     assert e.value.code == P.CKPT_EBUSY
+    ck.wait_committed(s1)
+    s2 = ck.snapshot(step=2)  # the other image
     ck.wait_committed(s2)
     assert ck.state(s1) == P.CKPT_SNAP_COMMITTED and ck.state(s2) == P.CKPT_SNAP_COMMITTED
     s3 = ck.snapshot(step=3)  # takes s1's image
@@ -257,43 +287,34 @@ def test_ping_pong_roles_and_busy():
 
 
 def check_committed_image_survives(bounce):
-    """Invariant I4 / the ping-pong guarantee with two snapshots in flight:
-    the third snapshot writes the image of the first, and must not land a byte
-    there before the second has committed."""
+    """The ping-pong guarantee (Sec. VI-A; invariant I4): while a snapshot is
+    in flight the newest committed one stays in its own image, restorable and
+    verify-clean, and a further snapshot is refused until the first commits."""
     tensors = _step_state(n_frag=256, numel=1 << 20)  # 1 GiB: ~19 ms of D2H
     ck = P.Checkpointer(tensors, chunk_bytes=1 << 22, group_bytes=1 << 24, bounce_bytes=bounce)
     s1 = ck.snapshot(step=1)
     ck.wait_committed(s1)
-    img1, _ = ck.host_image(s1)  # borrowed view; s3 will reuse this image
-    watch = 2 << 24  # the first group on each of the two DMA engines
+    img1, _ = ck.host_image(s1)
+    watch = 2 << 24
     head = img1[:watch].copy()
     for t in tensors:
         t.mul_(-1.0)
     s2 = ck.snapshot(step=2)
-    ck.wait_captured(s2)
-    for t in tensors:
-        t.add_(1.0)
-    s3 = ck.snapshot(step=3)
+    with pytest.raises(P.CkptError) as e:
+        ck.snapshot(step=3)
+    assert e.value.code == P.CKPT_EBUSY
     polls = 0
-    while True:
-        # Look at the bytes first, then at the state: a change seen here must
-        # come from a copy that started after snapshot 2 had committed.
-        same = np.array_equal(img1[:watch], head)
-        committed = ck.state(s2) == P.CKPT_SNAP_COMMITTED
-        assert same or committed, "snapshot 3 overwrote the only committed image"
+    while ck.state(s2) != P.CKPT_SNAP_COMMITTED:
+        assert ck.latest() == (s1, 1) and ck.state(s1) == P.CKPT_SNAP_COMMITTED
+        assert np.array_equal(img1[:watch], head)
         polls += 1
-        if committed:
-            break
-    ck.wait_committed(s3)
-    assert polls >= 2
+    assert polls >= 1
+    assert ck.verify(s1) == [] and ck.latest() == (s2, 2)
     ck.close()
 
 
-def test_a_committed_image_exists_while_two_snapshots_are_in_flight():
-    # The unguarded window is narrow (each engine runs its queue in order); a
-    # build without the ordering showed it in about one run of five.
-    for _ in range(3):
-        check_committed_image_survives(0)
+def test_a_committed_image_exists_while_a_snapshot_is_in_flight():
+    check_committed_image_survives(0)
 
 
 def test_verify_runs_beside_an_inflight_snapshot():
