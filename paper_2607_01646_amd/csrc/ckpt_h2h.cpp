@@ -1,0 +1,235 @@
+// ckpt_h2h.cpp -- host-to-host replication to a ring peer (paper Sec. V-B,
+// "Host-to-host"): the sending side.  After each local commit the context's
+// worker streams the selected classes' chunks, their stored sums and the
+// envelope to the peer (wire format in ckpt_wire.h) and waits for its
+// verdict; the receiving side is ckpt_peer.cpp.
+#include "ckpt_host.h"
+
+namespace ckpt {
+
+// H2H worker thread (see Replicator).
+void rep_worker(ckpt_ctx* c)
+{
+    Replicator* R = c->rep;
+    using clock = std::chrono::steady_clock;
+    for (;;) {
+        RepJob j;
+        bool broken;
+        {
+            std::unique_lock<std::mutex> l(R->m);
+            R->cv.wait(l, [&] { return R->stop || !R->q.empty(); });
+            if (R->q.empty()) return;
+            j = std::move(R->q.front());
+            R->q.pop_front();
+            broken = R->broken;
+        }
+        RepStatus st;
+        st.state = REP_FAILED;
+        // 1. The local offload has to commit first (bounded wait).
+        const auto t_wait = clock::now();
+        bool committed = false;
+        while (!broken) {
+            if (res_done(j.res, j.groups_copied, j.bounce)) {
+                committed = !j.res->failed.load(std::memory_order_acquire);
+                break;
+            }
+            if (clock::now() - t_wait > std::chrono::seconds(120)) break;
+            {
+                std::lock_guard<std::mutex> l(R->m);
+                if (R->stop) break;
+            }
+            std::this_thread::sleep_for(std::chrono::microseconds(100));
+        }
+        if (broken) st.err = "the connection to the peer failed earlier: " + R->err;
+        else if (!committed) st.err = "the local snapshot did not commit";
+        const auto t_commit = clock::now();
+        int fault = 0;
+        uint64_t fa = 0, fb = 0;
+        if (committed) {
+            {
+                std::lock_guard<std::mutex> l(R->m);
+                fault = R->fault_kind;
+                fa = R->fault_a;
+                fb = R->fault_b;
+                R->fault_kind = 0;
+            }
+            // 2. Send head, ids, sums, envelope and the chunks.
+            const auto deadline = t_commit + std::chrono::seconds(120);
+            const uint64_t m = R->ids.size();
+            const uint64_t* sums_all = c->h_sums[j.buf];
+            std::vector<uint64_t> sums(m);
+            for (uint64_t k = 0; k < m; ++k) sums[k] = sums_all[R->ids[k]];
+            const std::vector<uint8_t> env = build_envelope(c, j.step, j.meta, sums_all);
+            WireHead h;
+            std::memcpy(h.magic, kWireMagic, 8);
+            h.snap_id = j.id;
+            h.step = j.step;
+            h.chunk_bytes = c->C;
+            h.image_bytes = c->I;
+            h.m = m;
+            h.replica_bytes = R->bytes;
+            h.env_len = env.size();
+            bool ok = send_all(R->fd, &h, sizeof h, deadline) == 0 &&
+                      send_all(R->fd, R->ids.data(), 8 * m, deadline) == 0 &&
+                      send_all(R->fd, sums.data(), 8 * m, deadline) == 0 &&
+                      send_all(R->fd, env.data(), env.size(), deadline) == 0;
+            const uint8_t* img = c->h_img[j.buf];
+            uint64_t sent = 0; // replica bytes sent so far
+            for (uint64_t k = 0; ok && k < m;) {
+                // one run of consecutive chunk ids is contiguous in the image
+                uint64_t e = k + 1;
+                while (e < m && R->ids[e] == R->ids[e - 1] + 1) ++e;
+                const uint64_t lo = R->ids[k] * c->C, hi = std::min(R->ids[e - 1] * c->C + c->C, c->I);
+                uint64_t n = hi - lo;
+                if (fault == 2 && sent + n >= fa) { // debug: cut the stream after fa replica bytes
+                    (void)send_all(R->fd, img + lo, fa - sent, deadline);
+                    ok = false;
+                    break;
+                }
+                if (fault == 1 && fa >= sent && fa < sent + n) { // debug: flip bit fb of replica byte fa
+                    const uint64_t at = fa - sent;
+                    uint8_t b = img[lo + at] ^ (uint8_t)(1u << (fb & 7));
+                    ok = send_all(R->fd, img + lo, at, deadline) == 0 && send_all(R->fd, &b, 1, deadline) == 0 &&
+                         send_all(R->fd, img + lo + at + 1, n - at - 1, deadline) == 0;
+                } else {
+                    ok = send_all(R->fd, img + lo, n, deadline) == 0;
+                }
+                sent += n;
+                k = e;
+            }
+            const auto t1 = clock::now();
+            // 3. The peer's verdict.
+            WireAck a;
+            if (ok) ok = recv_all(R->fd, &a, sizeof a, deadline) == 0 && std::memcmp(a.magic, kAckMagic, 8) == 0 &&
+                         a.snap_id == j.id && a.n_bad <= m;
+            if (ok && a.n_bad) {
+                st.bad.resize(a.n_bad);
+                ok = recv_all(R->fd, st.bad.data(), 8ull * a.n_bad, deadline) == 0;
+            }
+            const auto t2 = clock::now();
+            if (ok) {
+                st.state = a.status == CKPT_OK ? REP_OK : a.status == CKPT_ECORRUPT ? REP_CORRUPT : REP_FAILED;
+                if (st.state == REP_FAILED) st.err = "the peer reported error " + std::to_string(a.status);
+                std::lock_guard<std::mutex> l(R->m);
+                R->last_send_ms = std::chrono::duration<double, std::milli>(t1 - t_commit).count();
+                R->last_ack_ms = std::chrono::duration<double, std::milli>(t2 - t_commit).count();
+            } else {
+                st.err = fault == 2 ? "stream cut on request" : "sending to the peer failed";
+                std::lock_guard<std::mutex> l(R->m);
+                R->broken = true;
+                R->err = st.err;
+                ::shutdown(R->fd, SHUT_RDWR);
+            }
+        }
+        std::lock_guard<std::mutex> l(R->m);
+        R->status[j.id] = std::move(st);
+        R->busy[j.buf] = false;
+        R->cv.notify_all();
+    }
+}
+
+void rep_stop(ckpt_ctx* c)
+{
+    Replicator* R = c->rep;
+    if (!R) return;
+    {
+        std::lock_guard<std::mutex> l(R->m);
+        R->stop = true;
+    }
+    R->cv.notify_all();
+    if (R->fd >= 0) ::shutdown(R->fd, SHUT_RDWR);
+    if (R->worker.joinable()) R->worker.join();
+    if (R->fd >= 0) ::close(R->fd);
+    delete R;
+    c->rep = nullptr;
+}
+
+} // namespace ckpt
+
+extern "C" {
+
+ckpt_status ckpt_replicate_to(ckpt_ctx* c, const char* host, uint32_t port, uint64_t cls_mask)
+{
+    if (!c || !host || port == 0 || port > 65535 || cls_mask == 0) return fail(c, CKPT_EINVAL, "bad replication target");
+    if (!c->registered) return fail(c, CKPT_ESTATE, "no tensors registered");
+    if (c->rep) return fail(c, CKPT_ESTATE, "a replication peer is already set");
+    // Chunks holding a byte of a fragment of a selected class.
+    std::vector<uint8_t> pick(c->n_chunks, 0);
+    for (const Frag& f : c->frags) {
+        if (!f.nbytes || f.cls >= 64 || !((cls_mask >> f.cls) & 1)) continue;
+        for (uint64_t k = f.off / c->C; k <= (f.off + f.nbytes - 1) / c->C; ++k) pick[k] = 1;
+    }
+    std::vector<uint64_t> ids;
+    for (uint64_t k = 0; k < c->n_chunks; ++k)
+        if (pick[k]) ids.push_back(k);
+    if (ids.empty()) return fail(c, CKPT_EINVAL, "no registered fragment has a selected class");
+    sockaddr_in a{};
+    a.sin_family = AF_INET;
+    a.sin_port = htons((uint16_t)port);
+    if (inet_pton(AF_INET, host, &a.sin_addr) != 1) return fail(c, CKPT_EINVAL, "host must be a dotted IPv4 address");
+    const int fd = ::socket(AF_INET, SOCK_STREAM, 0);
+    if (fd < 0) return fail(c, CKPT_EHIP, "socket: %s", strerror(errno));
+    tune_socket(fd);
+    if (::connect(fd, (sockaddr*)&a, sizeof a) != 0) {
+        const int e = errno;
+        ::close(fd);
+        return fail(c, CKPT_EHIP, "connect to %s:%u: %s", host, port, strerror(e));
+    }
+    Replicator* R = new Replicator();
+    R->fd = fd;
+    R->cls_mask = cls_mask;
+    R->ids = std::move(ids);
+    R->bytes = replica_bytes(R->ids.data(), R->ids.size(), c->C, c->I);
+    c->rep = R;
+    R->worker = std::thread(rep_worker, c);
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_replica_chunks(ckpt_ctx* c, uint64_t* ids, uint64_t cap, uint64_t* n, uint64_t* replica_bytes_out)
+{
+    if (!c || !n) return CKPT_EINVAL;
+    if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
+    *n = c->rep->ids.size();
+    if (replica_bytes_out) *replica_bytes_out = c->rep->bytes;
+    if (ids) std::memcpy(ids, c->rep->ids.data(), 8 * std::min<uint64_t>(cap, c->rep->ids.size()));
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_replica_result(ckpt_ctx* c, uint64_t snap_id, int32_t* state, uint64_t* bad, uint32_t cap,
+                                uint32_t* n_bad)
+{
+    if (!c || !state) return CKPT_EINVAL;
+    if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
+    std::lock_guard<std::mutex> l(c->rep->m);
+    auto s = c->rep->status.find(snap_id);
+    if (s == c->rep->status.end())
+        return fail(c, CKPT_ERANGE, "snapshot %llu is not being replicated", (unsigned long long)snap_id);
+    *state = s->second.state;
+    if (n_bad) *n_bad = (uint32_t)s->second.bad.size();
+    if (bad) std::memcpy(bad, s->second.bad.data(), 8 * std::min<uint64_t>(cap, s->second.bad.size()));
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_replica_timing(ckpt_ctx* c, double* send_ms, double* ack_ms)
+{
+    if (!c || !send_ms || !ack_ms) return CKPT_EINVAL;
+    if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
+    std::lock_guard<std::mutex> l(c->rep->m);
+    *send_ms = c->rep->last_send_ms;
+    *ack_ms = c->rep->last_ack_ms;
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_debug_h2h_fault(ckpt_ctx* c, int32_t kind, uint64_t a, uint64_t b)
+{
+    if (!c || kind < 0 || kind > 2) return CKPT_EINVAL;
+    if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
+    std::lock_guard<std::mutex> l(c->rep->m);
+    if (kind && a >= c->rep->bytes) return fail(c, CKPT_EINVAL, "fault position beyond the replica");
+    c->rep->fault_kind = kind;
+    c->rep->fault_a = a;
+    c->rep->fault_b = b;
+    return CKPT_OK;
+}
+
+} // extern "C"

@@ -32,379 +32,14 @@
 // Recovery (Sec. V-C third stage, Sec. VI-E) reverses the path group by
 // group: DMA host image -> staging on the copy stream, then the scatter
 // kernel on the pack stream writes the fragments and re-checks the sums.
-#include <hip/hip_runtime.h>
-#include <hsa/hsa.h>
-#include <hsa/hsa_ext_amd.h>
-
-#include <fcntl.h>
-#include <sys/mman.h>
-#include <sys/stat.h>
-#include <unistd.h>
-
-#include <algorithm>
-#include <atomic>
-#include <chrono>
-#include <condition_variable>
-#include <cstdarg>
-#include <cstdio>
-#include <cstring>
-#include <deque>
-#include <map>
-#include <memory>
-#include <mutex>
-#include <string>
-#include <thread>
-#include <vector>
-
-#include "../../include/ckpt.h"
-#include "ckpt_internal.h"
-#include "ckpt_wire.h"
-
-using namespace ckpt;
-
-namespace {
-
-constexpr uint64_t kDefaultChunk = 64ull << 20;
-constexpr uint32_t kDefaultAlign = 256;
-constexpr uint64_t kDefaultGroup = 1ull << 30;
-// 8 KiB tiles: each of a workgroup's 256 lanes moves exactly one batch of
-// two 16-byte vectors per tile (measured fastest on gfx950 with one
-// workgroup per tile in 1 GiB launches).
-constexpr uint32_t kMaxTileShift = 13;
-constexpr uint32_t kMaxMeta = 1u << 20;
-constexpr uint32_t kDefaultGrid = 0x7fffffff; // one workgroup per tile unless capped
-constexpr int kMaxEngines = 2;
-constexpr uint64_t kVerifySlots = 2; // verify's device ring: two slots of one chunk group each
-constexpr uint32_t kDefaultHostThreads = 12; // bounce mode: host copy threads (measured: 8 do not keep up with the link)
-
-struct Frag {
-    uint64_t ptr, nbytes, off;
-    uint32_t dtype, cls;
-};
-
-// GPU-side resources of one snapshot record, recycled between snapshots.
-struct RecRes {
-    std::vector<hipEvent_t> captured;   // per group, on the pack stream
-    std::vector<hsa_signal_t> dep;      // per group: set to 0 by the GPU once g is packed
-    std::vector<int64_t*> dep_val;      // value addresses of dep
-    std::vector<hsa_signal_t> copied;   // per group: the group's image copy finished
-    std::vector<hsa_signal_t> flagged;  // per group: the area-done copy after it finished
-    hsa_signal_t dep_sums{0}, done{0};  // sums packed; sums copied (the last copy issued)
-    int64_t* dep_sums_val = nullptr;
-    uint64_t* h_seq = nullptr;          // pinned, per group: area use number, source of the area-done copy
-    unsigned long long* d_sums = nullptr;
-    std::vector<hipEvent_t> k0, k1;     // timing: around each pack launch
-    hipEvent_t t0 = nullptr;
-    std::atomic<uint32_t> landed{0};    // bounce mode: groups moved from the ring into the image
-    std::atomic<bool> failed{false};    // bounce mode: a copy of this record could not be completed
-    std::atomic<bool> recorded{false};  // image file: the commit record has been written
-};
-
-struct SnapRec {
-    uint64_t id = 0, step = 0;
-    int buf = -1;
-    bool bounce = false;    // the image is pageable; groups land through the bounce ring
-    bool file = false;      // the image lives in the image file: committed once its record is written
-    bool aborted = false;
-    bool committed = false; // cached once `done` has reached 0
-    bool timed = false;
-    uint32_t groups_copied = 0;
-    std::vector<uint8_t> meta;
-    RecRes* res = nullptr;
-};
-
-struct OpTiming {
-    bool valid = false;
-    ckpt_timing t{};
-};
-
-// Host threads that copy between host buffers in parallel (bounce mode).
-// copy() cuts one copy into parts, queues all but the first, runs the
-// first itself, and returns when every part is done; several threads may
-// call it at once.
-class CopyPool {
-public:
-    explicit CopyPool(unsigned n) : n_(std::max(1u, n))
-    {
-        for (unsigned k = 0; k + 1 < n_; ++k) th_.emplace_back([this] { work(); });
-    }
-    ~CopyPool()
-    {
-        {
-            std::lock_guard<std::mutex> l(m_);
-            stop_ = true;
-        }
-        cv_.notify_all();
-        for (auto& t : th_) t.join();
-    }
-    void copy(uint8_t* dst, const uint8_t* src, uint64_t n)
-    {
-        const uint64_t min_part = 4ull << 20;
-        uint64_t parts = std::min<uint64_t>(n_, std::max<uint64_t>(1, n / min_part));
-        if (parts <= 1) {
-            std::memcpy(dst, src, n);
-            return;
-        }
-        const uint64_t per = (n / parts + 4095) & ~4095ull;
-        Batch b;
-        b.left = 0;
-        {
-            std::lock_guard<std::mutex> l(m_);
-            for (uint64_t k = 1; k < parts; ++k) {
-                const uint64_t lo = std::min(k * per, n), hi = std::min(lo + per, n);
-                if (hi <= lo) continue;
-                q_.push_back(Part{dst + lo, src + lo, hi - lo, &b});
-                ++b.left;
-            }
-        }
-        cv_.notify_all();
-        std::memcpy(dst, src, std::min(per, n));
-        std::unique_lock<std::mutex> l(b.m);
-        b.cv.wait(l, [&] { return b.left == 0; });
-    }
-
-private:
-    struct Batch {
-        unsigned left;
-        std::mutex m;
-        std::condition_variable cv;
-    };
-    struct Part {
-        uint8_t* dst;
-        const uint8_t* src;
-        uint64_t n;
-        Batch* b;
-    };
-    void work()
-    {
-        for (;;) {
-            Part p;
-            {
-                std::unique_lock<std::mutex> l(m_);
-                cv_.wait(l, [&] { return stop_ || !q_.empty(); });
-                if (q_.empty()) return;
-                p = q_.front();
-                q_.pop_front();
-            }
-            std::memcpy(p.dst, p.src, p.n);
-            std::lock_guard<std::mutex> l(p.b->m);
-            if (--p.b->left == 0) p.b->cv.notify_all();
-        }
-    }
-    unsigned n_;
-    std::mutex m_;
-    std::condition_variable cv_;
-    std::deque<Part> q_;
-    bool stop_ = false;
-    std::vector<std::thread> th_;
-};
-
-// One group of a snapshot on its way through the bounce ring, or (sums)
-// the snapshot's chunk-sum copy, which follows its groups.
-struct PumpItem {
-    RecRes* res = nullptr;
-    uint32_t g = 0;
-    bool sums = false;               // the chunk sums: device -> pinned sums array, no ring slot
-    uint8_t* image = nullptr;        // destination: pageable host image (group) or pinned sums array
-    const uint8_t* staging = nullptr; // source in device memory
-    uint64_t n = 0;
-    uint64_t* area_done = nullptr;   // group: device counter bumped once the staging area has been read
-    const uint64_t* seq = nullptr;   // group: pinned, the value it is set to
-    hsa_amd_sdma_engine_id_t engine{};
-    uint32_t groups = 0;             // record: the snapshot's group copies
-    int buf = 0;                     // host image written
-    bool record = false;             // image file: write the snapshot's commit record (no copy)
-    uint64_t need_rec = 0;           // sums: records of image buf that must be written before its sums array is reused
-    uint64_t snap_id = 0, step = 0;
-    std::shared_ptr<const std::vector<uint8_t>> meta;
-};
-
-// Image file (ckpt_image_file): the two images, their sums and commit
-// records in one shared mapping.  Layout: FileHead at 0, FileRec b at
-// kRecOff + 512 * b, then per image its sums, its caller blob area and (2 MiB
-// aligned) its bytes.
-struct FileHead {
-    char magic[8]; // "CKPTFIL1"
-    uint32_t version, align;
-    uint64_t chunk, image_bytes, n_chunks;
-    uint32_t n_frag, pad;
-    uint64_t table_sum; // word-sum of the fragment table (offset, bytes, dtype, class per fragment)
-    uint64_t image_off[2], sums_off[2], meta_off[2];
-    uint64_t file_bytes;
-};
-struct FileRec {
-    uint64_t state;   // 1 = committed; stored last, 0 before the image is rewritten
-    uint64_t seq;     // commit number: of two valid records the larger is the newest
-    uint64_t snap_id, step, meta_len;
-    uint64_t rec_sum; // word-sum of seq, snap_id, step, meta_len, the chunk sums and the zero-padded blob
-};
-constexpr uint64_t kRecOff = 4096;
-
-// Bounce-mode D2H (one per context).  The issuer takes snapshot groups in
-// order, waits for a free ring slot, and starts the DMA staging -> slot
-// (after the group's pack, through its dependency signal) followed by the
-// staging area's use-counter copy.  The drainer takes them in the same
-// order, waits for each DMA, copies slot -> image on the copy pool, frees
-// the slot and counts the group as landed.
 //
-// Every DMA of bounce mode is issued by the issuer, in snapshot and group
-// order.  Each engine runs its requests in order, and a request waiting for
-// a pack blocks the requests behind it; issuing the chunk-sum copy (which
-// waits for the last pack) ahead of group copies that earlier packs depend
-// on -- through the staging counters -- would stall the engine for good.
-struct Pump {
-    std::mutex m;
-    std::condition_variable cv;
-    std::deque<PumpItem> issue_q;
-    std::deque<std::pair<PumpItem, uint64_t>> drain_q;
-    std::vector<uint8_t> busy; // per ring slot
-    uint64_t next_slot = 0;
-    uint64_t rec_pushed[2] = {0, 0}, rec_done[2] = {0, 0}; // image-file commit records per host image
-    bool stop = false;
-    bool failed = false;
-    std::string err;
-    std::thread issuer, drainer;
-};
+// Also here: registration, restore and verify, and the accessors.  The
+// bounce-mode pump, the image file and replication have files of their own
+// (ckpt_bounce.cpp, ckpt_file.cpp, ckpt_h2h.cpp); ckpt_host.h holds what
+// they share.
+#include "ckpt_host.h"
 
-// H2H replication (paper Sec. V-B, "Host-to-host"): one job per snapshot,
-// handed to the worker when the snapshot is issued.  The worker waits for
-// the local commit, sends the replicated chunks with their sums and the
-// envelope, and waits for the peer's acknowledgement.
-struct RepJob {
-    uint64_t id = 0, step = 0;
-    int buf = 0;
-    RecRes* res = nullptr;
-    uint32_t groups_copied = 0;
-    bool bounce = false;
-    std::vector<uint8_t> meta;
-};
-
-enum { REP_PENDING = 0, REP_OK = 1, REP_CORRUPT = 2, REP_FAILED = 3 };
-
-struct RepStatus {
-    int state = REP_PENDING;
-    std::vector<uint64_t> bad; // sender chunk ids the peer found corrupt
-    std::string err;
-};
-
-struct Replicator {
-    int fd = -1;
-    uint64_t cls_mask = 0;
-    std::vector<uint64_t> ids; // replicated chunks, increasing
-    uint64_t bytes = 0;        // replica bytes per snapshot
-    std::mutex m;
-    std::condition_variable cv;
-    std::deque<RepJob> q;
-    std::map<uint64_t, RepStatus> status;
-    bool busy[2] = {false, false}; // a replication still reads host image b
-    bool stop = false;
-    bool broken = false; // the connection failed: later jobs fail at once
-    std::string err;
-    int fault_kind = 0;  // debug: 1 = flip one bit of the next stream, 2 = cut the next stream
-    uint64_t fault_a = 0, fault_b = 0;
-    double last_send_ms = 0, last_ack_ms = 0; // commit -> last byte sent, commit -> acknowledgement
-    std::thread worker;
-};
-
-} // namespace
-
-struct ckpt_ctx {
-    // configuration
-    int device = 0;
-    uint64_t C = kDefaultChunk;
-    uint32_t A = kDefaultAlign;
-    uint64_t staging_cap = 0; // 0 = full image
-    uint64_t group_cfg = kDefaultGroup;
-    uint32_t grid_cap = kDefaultGrid;
-    bool timing = false;
-
-    // layout
-    bool registered = false;
-    std::vector<Frag> frags;
-    uint64_t I = 0, n_chunks = 0, payload = 0;
-    Geometry geo{};
-    uint64_t G = 1;        // chunks per group
-    uint64_t n_groups = 0; // groups
-    bool ring = false;
-    uint64_t n_slots = 0;  // ring slots (ring mode)
-
-    // device memory
-    FragDev* d_frags = nullptr;
-    uint32_t* d_tile_first = nullptr;
-    uint32_t* d_tile_last = nullptr;
-    uint8_t* d_staging = nullptr;
-    unsigned long long* d_partials = nullptr; // [2][n_tiles * kTileParts] tile partial sums: pack, check
-    unsigned long long* d_expected = nullptr;
-    unsigned long long* d_recomputed = nullptr;
-    uint8_t* d_bad = nullptr;
-    uint64_t* d_area_done = nullptr;          // per staging area: number of finished copies out of it
-
-    // pinned host memory
-    uint8_t* h_img[2] = {nullptr, nullptr};
-    uint64_t* h_sums[2] = {nullptr, nullptr};
-    uint64_t holder[2] = {0, 0}; // snapshot id whose bytes each image holds (0 = none)
-    uint8_t* h_bad = nullptr;
-    unsigned long long* h_recomputed = nullptr;
-
-    // HSA agents and DMA engines
-    hsa_agent_t gpu_agent{0}, img_agent[2] = {{0}, {0}};
-    hsa_amd_sdma_engine_id_t d2h_engine[kMaxEngines];
-    int n_d2h_engines = 0;
-    hsa_amd_sdma_engine_id_t h2d_engine{};
-    uint64_t ts_freq = 1;
-
-    // streams and events
-    hipStream_t s_pack = nullptr, s_copy = nullptr;
-    hipEvent_t ev_trigger = nullptr, ev_done = nullptr;
-    std::vector<uint64_t> area_seq;     // per staging area: copies issued out of it
-    std::vector<hipEvent_t> area_free;  // restore/verify: per staging area
-    std::vector<hipEvent_t> ev_loaded;  // restore/verify: per group
-    std::vector<RecRes*> free_res;
-    std::map<uint64_t, SnapRec> recs;
-    uint64_t next_id = 1;
-    int32_t interrupt_next = -1;
-
-    // results of the last restore / verify
-    bool have_last_sums = false;
-    std::vector<uint64_t> last_sums;
-    OpTiming op_timing[3];
-    std::vector<hipEvent_t> tk0, tk1; // restore timing
-    hipEvent_t tt0 = nullptr, tc0 = nullptr, tc1 = nullptr;
-
-    // bounce mode: pageable images behind two pinned rings of chunk groups
-    bool bounce = false;
-    uint64_t bounce_cfg = 0;
-    uint32_t host_threads = kDefaultHostThreads;
-    uint64_t n_bslots = 0;            // slots per ring
-    uint64_t img_map_bytes = 0;       // mapped length of each pageable image
-    uint8_t* h_bout = nullptr;        // device -> host ring
-    uint8_t* h_bin = nullptr;         // host -> device ring
-    std::vector<hipEvent_t> bin_done; // per host -> device slot: its last copy to the device finished
-    CopyPool* pool = nullptr;
-    Pump* pump = nullptr;
-
-    // H2H replication to a ring peer
-    Replicator* rep = nullptr;
-
-    // image file (crash-surviving images; bounce mode only)
-    std::string file_path;
-    int file_mode = -1; // -1 none, else CKPT_FILE_CREATE / CKPT_FILE_ADOPT
-    int file_fd = -1;
-    uint8_t* file_map = nullptr;
-    FileHead fhead{};
-    uint64_t file_seq = 0; // last commit number written (drainer thread after registration)
-
-    // verify: its own ring of chunk slots and streams
-    uint8_t* d_vring = nullptr;
-    uint64_t n_vslots = 0;
-    hipStream_t s_vcopy = nullptr, s_vker = nullptr;
-    hipEvent_t ev_vdone = nullptr, vt0 = nullptr, vc0 = nullptr, vc1 = nullptr;
-    std::vector<hipEvent_t> vfree, vloaded, vk0, vk1;
-
-    std::string err;
-};
-
-namespace {
+namespace ckpt {
 
 ckpt_status fail(ckpt_ctx* c, ckpt_status code, const char* fmt, ...)
 {
@@ -419,26 +54,12 @@ ckpt_status fail(ckpt_ctx* c, ckpt_status code, const char* fmt, ...)
     return code;
 }
 
-#define HIPCHK(ctx, expr)                                                                                    \
-    do {                                                                                                     \
-        hipError_t e_ = (expr);                                                                              \
-        if (e_ != hipSuccess)                                                                                \
-            return fail((ctx), CKPT_EHIP, "%s failed: %s (%d)", #expr, hipGetErrorString(e_), (int)e_);       \
-    } while (0)
-
 const char* hsa_text(hsa_status_t s)
 {
     const char* t = nullptr;
     if (hsa_status_string(s, &t) != HSA_STATUS_SUCCESS || !t) return "unknown HSA status";
     return t;
 }
-
-#define HSACHK(ctx, expr)                                                                                    \
-    do {                                                                                                     \
-        hsa_status_t s_ = (expr);                                                                            \
-        if (s_ != HSA_STATUS_SUCCESS)                                                                        \
-            return fail((ctx), CKPT_EHIP, "%s failed: %s (%d)", #expr, hsa_text(s_), (int)s_);               \
-    } while (0)
 
 bool is_pow2(uint64_t x) { return x && !(x & (x - 1)); }
 uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
@@ -960,9 +581,6 @@ ckpt_status run_check(ckpt_ctx* c, uint64_t snap_id, hipStream_t stream, bool sc
     return CKPT_OK;
 }
 
-void stop_pump(ckpt_ctx* c);
-void rep_stop(ckpt_ctx* c);
-
 void free_ctx(ckpt_ctx* c)
 {
     rep_stop(c); // reads host images and snapshot records
@@ -1019,17 +637,6 @@ ckpt_status dma(ckpt_ctx* c, void* dst, hsa_agent_t dst_agent, const void* src, 
     return CKPT_OK;
 }
 
-// Poll a signal that only the GPU side waits on until it reads 0.
-bool poll_zero(hsa_signal_t sig, int seconds)
-{
-    const auto deadline = std::chrono::steady_clock::now() + std::chrono::seconds(seconds);
-    while (hsa_signal_load_scacquire(sig) != 0) {
-        if (std::chrono::steady_clock::now() > deadline) return false;
-        std::this_thread::sleep_for(std::chrono::microseconds(20));
-    }
-    return true;
-}
-
 // The envelope of a snapshot (format in include/ckpt.h, ckpt_envelope).
 std::vector<uint8_t> build_envelope(const ckpt_ctx* c, uint64_t step, const std::vector<uint8_t>& meta,
                                     const uint64_t* sums)
@@ -1080,408 +687,9 @@ std::vector<uint8_t> build_envelope(const ckpt_ctx* c, uint64_t step, const std:
     return buf;
 }
 
-// H2H worker thread (see Replicator).
-void rep_worker(ckpt_ctx* c)
-{
-    Replicator* R = c->rep;
-    using clock = std::chrono::steady_clock;
-    for (;;) {
-        RepJob j;
-        bool broken;
-        {
-            std::unique_lock<std::mutex> l(R->m);
-            R->cv.wait(l, [&] { return R->stop || !R->q.empty(); });
-            if (R->q.empty()) return;
-            j = std::move(R->q.front());
-            R->q.pop_front();
-            broken = R->broken;
-        }
-        RepStatus st;
-        st.state = REP_FAILED;
-        // 1. The local offload has to commit first (bounded wait).
-        const auto t_wait = clock::now();
-        bool committed = false;
-        while (!broken) {
-            if (res_done(j.res, j.groups_copied, j.bounce)) {
-                committed = !j.res->failed.load(std::memory_order_acquire);
-                break;
-            }
-            if (clock::now() - t_wait > std::chrono::seconds(120)) break;
-            {
-                std::lock_guard<std::mutex> l(R->m);
-                if (R->stop) break;
-            }
-            std::this_thread::sleep_for(std::chrono::microseconds(100));
-        }
-        if (broken) st.err = "the connection to the peer failed earlier: " + R->err;
-        else if (!committed) st.err = "the local snapshot did not commit";
-        const auto t_commit = clock::now();
-        int fault = 0;
-        uint64_t fa = 0, fb = 0;
-        if (committed) {
-            {
-                std::lock_guard<std::mutex> l(R->m);
-                fault = R->fault_kind;
-                fa = R->fault_a;
-                fb = R->fault_b;
-                R->fault_kind = 0;
-            }
-            // 2. Send head, ids, sums, envelope and the chunks.
-            const auto deadline = t_commit + std::chrono::seconds(120);
-            const uint64_t m = R->ids.size();
-            const uint64_t* sums_all = c->h_sums[j.buf];
-            std::vector<uint64_t> sums(m);
-            for (uint64_t k = 0; k < m; ++k) sums[k] = sums_all[R->ids[k]];
-            const std::vector<uint8_t> env = build_envelope(c, j.step, j.meta, sums_all);
-            WireHead h;
-            std::memcpy(h.magic, kWireMagic, 8);
-            h.snap_id = j.id;
-            h.step = j.step;
-            h.chunk_bytes = c->C;
-            h.image_bytes = c->I;
-            h.m = m;
-            h.replica_bytes = R->bytes;
-            h.env_len = env.size();
-            bool ok = send_all(R->fd, &h, sizeof h, deadline) == 0 &&
-                      send_all(R->fd, R->ids.data(), 8 * m, deadline) == 0 &&
-                      send_all(R->fd, sums.data(), 8 * m, deadline) == 0 &&
-                      send_all(R->fd, env.data(), env.size(), deadline) == 0;
-            const uint8_t* img = c->h_img[j.buf];
-            uint64_t sent = 0; // replica bytes sent so far
-            for (uint64_t k = 0; ok && k < m;) {
-                // one run of consecutive chunk ids is contiguous in the image
-                uint64_t e = k + 1;
-                while (e < m && R->ids[e] == R->ids[e - 1] + 1) ++e;
-                const uint64_t lo = R->ids[k] * c->C, hi = std::min(R->ids[e - 1] * c->C + c->C, c->I);
-                uint64_t n = hi - lo;
-                if (fault == 2 && sent + n >= fa) { // debug: cut the stream after fa replica bytes
-                    (void)send_all(R->fd, img + lo, fa - sent, deadline);
-                    ok = false;
-                    break;
-                }
-                if (fault == 1 && fa >= sent && fa < sent + n) { // debug: flip bit fb of replica byte fa
-                    const uint64_t at = fa - sent;
-                    uint8_t b = img[lo + at] ^ (uint8_t)(1u << (fb & 7));
-                    ok = send_all(R->fd, img + lo, at, deadline) == 0 && send_all(R->fd, &b, 1, deadline) == 0 &&
-                         send_all(R->fd, img + lo + at + 1, n - at - 1, deadline) == 0;
-                } else {
-                    ok = send_all(R->fd, img + lo, n, deadline) == 0;
-                }
-                sent += n;
-                k = e;
-            }
-            const auto t1 = clock::now();
-            // 3. The peer's verdict.
-            WireAck a;
-            if (ok) ok = recv_all(R->fd, &a, sizeof a, deadline) == 0 && std::memcmp(a.magic, kAckMagic, 8) == 0 &&
-                         a.snap_id == j.id && a.n_bad <= m;
-            if (ok && a.n_bad) {
-                st.bad.resize(a.n_bad);
-                ok = recv_all(R->fd, st.bad.data(), 8ull * a.n_bad, deadline) == 0;
-            }
-            const auto t2 = clock::now();
-            if (ok) {
-                st.state = a.status == CKPT_OK ? REP_OK : a.status == CKPT_ECORRUPT ? REP_CORRUPT : REP_FAILED;
-                if (st.state == REP_FAILED) st.err = "the peer reported error " + std::to_string(a.status);
-                std::lock_guard<std::mutex> l(R->m);
-                R->last_send_ms = std::chrono::duration<double, std::milli>(t1 - t_commit).count();
-                R->last_ack_ms = std::chrono::duration<double, std::milli>(t2 - t_commit).count();
-            } else {
-                st.err = fault == 2 ? "stream cut on request" : "sending to the peer failed";
-                std::lock_guard<std::mutex> l(R->m);
-                R->broken = true;
-                R->err = st.err;
-                ::shutdown(R->fd, SHUT_RDWR);
-            }
-        }
-        std::lock_guard<std::mutex> l(R->m);
-        R->status[j.id] = std::move(st);
-        R->busy[j.buf] = false;
-        R->cv.notify_all();
-    }
-}
-
-void rep_stop(ckpt_ctx* c)
-{
-    Replicator* R = c->rep;
-    if (!R) return;
-    {
-        std::lock_guard<std::mutex> l(R->m);
-        R->stop = true;
-    }
-    R->cv.notify_all();
-    if (R->fd >= 0) ::shutdown(R->fd, SHUT_RDWR);
-    if (R->worker.joinable()) R->worker.join();
-    if (R->fd >= 0) ::close(R->fd);
-    delete R;
-    c->rep = nullptr;
-}
-
-// ---- image file (ckpt_image_file) ----
-
-uint64_t word_sum(const uint8_t* p, uint64_t n) // n a multiple of 8
-{
-    uint64_t s = 0;
-    for (uint64_t k = 0; k < n; k += 8) {
-        uint64_t w;
-        std::memcpy(&w, p + k, 8);
-        s += w;
-    }
-    return s;
-}
-
-FileRec* file_rec(const ckpt_ctx* c, int b) { return (FileRec*)(c->file_map + kRecOff + 512 * b); }
-
-void file_layout(const ckpt_ctx* c, FileHead* h)
-{
-    std::memset(h, 0, sizeof *h);
-    std::memcpy(h->magic, "CKPTFIL1", 8);
-    h->version = 1;
-    h->align = c->A;
-    h->chunk = c->C;
-    h->image_bytes = c->I;
-    h->n_chunks = c->n_chunks;
-    h->n_frag = (uint32_t)c->frags.size();
-    for (const Frag& f : c->frags) h->table_sum += f.off + f.nbytes + (f.dtype | ((uint64_t)f.cls << 32));
-    uint64_t o = kRecOff + 1024;
-    for (int b = 0; b < 2; ++b) {
-        h->sums_off[b] = round_up(o, 4096);
-        h->meta_off[b] = h->sums_off[b] + round_up(8 * c->n_chunks, 4096);
-        o = h->meta_off[b] + kMaxMeta;
-    }
-    for (int b = 0; b < 2; ++b) {
-        h->image_off[b] = round_up(o, 2ull << 20);
-        o = h->image_off[b] + round_up(c->I, 2ull << 20);
-    }
-    h->file_bytes = o;
-}
-
-uint64_t rec_checksum(const ckpt_ctx* c, const FileRec& r, int b)
-{
-    return r.seq + r.snap_id + r.step + r.meta_len + word_sum(c->file_map + c->fhead.sums_off[b], 8 * c->n_chunks) +
-           word_sum(c->file_map + c->fhead.meta_off[b], round_up(r.meta_len, 8));
-}
-
-bool rec_valid(const ckpt_ctx* c, int b)
-{
-    const FileRec* r = file_rec(c, b);
-    return __atomic_load_n(&r->state, __ATOMIC_ACQUIRE) == 1 && r->meta_len <= kMaxMeta &&
-           rec_checksum(c, *r, b) == r->rec_sum;
-}
-
-// Before image b is rewritten its record stops naming a snapshot.
-void file_invalidate(ckpt_ctx* c, int b) { __atomic_store_n(&file_rec(c, b)->state, (uint64_t)0, __ATOMIC_RELEASE); }
-
-// After the snapshot's last byte and its sums have landed: sums, caller
-// blob, then the record, its state last.
-void file_commit(ckpt_ctx* c, const PumpItem& it)
-{
-    const int b = it.buf;
-    std::memcpy(c->file_map + c->fhead.sums_off[b], c->h_sums[b], 8 * c->n_chunks);
-    const uint64_t len = it.meta ? it.meta->size() : 0;
-    uint8_t* meta = c->file_map + c->fhead.meta_off[b];
-    if (len) std::memcpy(meta, it.meta->data(), len);
-    std::memset(meta + len, 0, round_up(len, 8) - len);
-    FileRec* r = file_rec(c, b);
-    r->seq = ++c->file_seq;
-    r->snap_id = it.snap_id;
-    r->step = it.step;
-    r->meta_len = len;
-    r->rec_sum = rec_checksum(c, *r, b);
-    __atomic_store_n(&r->state, (uint64_t)1, __ATOMIC_RELEASE);
-}
-
-// Map the image file at registration (bounce mode): create it, or check an
-// existing one against this context's layout.
-ckpt_status open_image_file(ckpt_ctx* c)
-{
-    file_layout(c, &c->fhead);
-    const bool create = c->file_mode == CKPT_FILE_CREATE;
-    c->file_fd = ::open(c->file_path.c_str(), create ? (O_RDWR | O_CREAT | O_TRUNC) : O_RDWR, 0600);
-    if (c->file_fd < 0) return fail(c, CKPT_EHIP, "open %s: %s", c->file_path.c_str(), strerror(errno));
-    if (create) {
-        // Reserve the space now: a sparse file on a full tmpfs would fault
-        // (SIGBUS) on first write instead of failing here.
-        const int e = ::posix_fallocate(c->file_fd, 0, (off_t)c->fhead.file_bytes);
-        if (e != 0) return fail(c, CKPT_ENOMEM, "reserving %llu bytes for %s: %s",
-                                (unsigned long long)c->fhead.file_bytes, c->file_path.c_str(), strerror(e));
-    } else {
-        struct stat st;
-        if (::fstat(c->file_fd, &st) != 0 || (uint64_t)st.st_size != c->fhead.file_bytes)
-            return fail(c, CKPT_EINVAL, "%s does not hold images of this layout", c->file_path.c_str());
-    }
-    void* m = ::mmap(nullptr, c->fhead.file_bytes, PROT_READ | PROT_WRITE, MAP_SHARED, c->file_fd, 0);
-    if (m == MAP_FAILED) return fail(c, CKPT_ENOMEM, "mmap %s: %s", c->file_path.c_str(), strerror(errno));
-    c->file_map = (uint8_t*)m;
-    (void)madvise(m, c->fhead.file_bytes, MADV_HUGEPAGE);
-    if (create) {
-        std::memcpy(c->file_map, &c->fhead, sizeof c->fhead);
-        std::memset(c->file_map + kRecOff, 0, 1024);
-    } else if (std::memcmp(c->file_map, &c->fhead, sizeof c->fhead) != 0) {
-        return fail(c, CKPT_EINVAL, "%s holds images of another layout (fragments, chunk or alignment differ)",
-                    c->file_path.c_str());
-    }
-    for (int b = 0; b < 2; ++b) {
-        c->h_img[b] = c->file_map + c->fhead.image_off[b];
-        if (create) parallel_zero(c->h_img[b], c->I); // fault the pages in now
-    }
-    return CKPT_OK;
-}
-
-// Bounce mode, issuer thread (see Pump).
-void pump_issue(ckpt_ctx* c)
-{
-    Pump* p = c->pump;
-    const uint64_t unit = c->G * c->C;
-    for (;;) {
-        PumpItem it;
-        uint64_t slot = UINT64_MAX; // taken ring slot, if any
-        {
-            std::unique_lock<std::mutex> l(p->m);
-            p->cv.wait(l, [&] { return p->stop || !p->issue_q.empty(); });
-            if (p->issue_q.empty()) return;
-            it = p->issue_q.front();
-            p->issue_q.pop_front();
-            if (it.record) { // no copy: handled by the drainer in order
-                p->drain_q.emplace_back(it, UINT64_MAX);
-                p->cv.notify_all();
-                continue;
-            }
-            if (it.sums) {
-                // no ring slot: straight into the pinned sums array, once the
-                // drainer has written every earlier record that reads it
-                p->cv.wait(l, [&] { return p->stop || p->failed || p->rec_done[it.buf] >= it.need_rec; });
-                bool ok = !p->failed && !p->stop;
-                l.unlock();
-                if (ok)
-                    ok = hsa_amd_memory_async_copy_on_engine(it.image, c->img_agent[0], it.staging, c->gpu_agent,
-                                                             it.n, 1, &it.res->dep_sums, it.res->done, it.engine,
-                                                             true) == HSA_STATUS_SUCCESS;
-                if (!ok) {
-                    hsa_signal_store_screlease(it.res->done, 0);
-                    it.res->failed.store(true, std::memory_order_release);
-                    l.lock();
-                    if (!p->failed) {
-                        p->failed = true;
-                        p->err = "DMA of the chunk sums could not be issued";
-                    }
-                }
-                continue;
-            }
-            const uint64_t s = p->next_slot % c->n_bslots;
-            p->cv.wait(l, [&] { return p->stop || p->failed || !p->busy[s]; });
-            if (!p->failed) {
-                if (p->busy[s]) return; // stopping
-                p->busy[s] = 1;
-                ++p->next_slot;
-                slot = s;
-            }
-        }
-        const char* what = nullptr;
-        bool issued = false, counted = false;
-        if (slot != UINT64_MAX) {
-            issued = hsa_amd_memory_async_copy_on_engine(c->h_bout + slot * unit, c->img_agent[0], it.staging,
-                                                         c->gpu_agent, it.n, 1, &it.res->dep[it.g],
-                                                         it.res->copied[it.g], it.engine, true) == HSA_STATUS_SUCCESS;
-            if (!issued) what = "DMA of a chunk group to the bounce ring could not be issued";
-            else
-                counted = hsa_amd_memory_async_copy_on_engine(it.area_done, c->gpu_agent, it.seq, c->img_agent[0], 8, 1,
-                                                              &it.res->copied[it.g], it.res->flagged[it.g],
-                                                              c->h2d_engine, true) == HSA_STATUS_SUCCESS;
-            if (issued && !counted) what = "staging counter copy could not be issued";
-        }
-        if (!issued) hsa_signal_store_screlease(it.res->copied[it.g], 0);
-        if (!counted) {
-            // Nothing bumps the staging area's use counter through the
-            // engines: once no copy reads the area, write it directly, so
-            // that no later pack waits for it forever.
-            if (!issued || poll_zero(it.res->copied[it.g], 120)) (void)hsa_memory_copy(it.area_done, it.seq, 8);
-            hsa_signal_store_screlease(it.res->flagged[it.g], 0);
-        }
-        std::lock_guard<std::mutex> l(p->m);
-        if (what && !p->failed) {
-            p->failed = true;
-            p->err = what;
-        }
-        if (!counted) it.res->failed.store(true, std::memory_order_release);
-        if (slot != UINT64_MAX && !issued) {
-            p->busy[slot] = 0;
-            slot = UINT64_MAX;
-        }
-        p->drain_q.emplace_back(it, slot);
-        p->cv.notify_all();
-    }
-}
-
-// Bounce mode, drainer thread (see Pump).
-void pump_drain(ckpt_ctx* c)
-{
-    Pump* p = c->pump;
-    const uint64_t unit = c->G * c->C;
-    for (;;) {
-        std::pair<PumpItem, uint64_t> d;
-        {
-            std::unique_lock<std::mutex> l(p->m);
-            p->cv.wait(l, [&] { return p->stop || !p->drain_q.empty(); });
-            if (p->drain_q.empty()) return;
-            d = p->drain_q.front();
-            p->drain_q.pop_front();
-        }
-        const PumpItem& it = d.first;
-        const uint64_t slot = d.second;
-        if (it.record) { // the snapshot's commit record in the image file
-            const auto deadline = std::chrono::steady_clock::now() + std::chrono::seconds(120);
-            while (!res_done(it.res, it.groups, true) && std::chrono::steady_clock::now() < deadline)
-                std::this_thread::sleep_for(std::chrono::microseconds(20));
-            if (res_done(it.res, it.groups, true) && !it.res->failed.load(std::memory_order_acquire)) {
-                file_commit(c, it);
-                it.res->recorded.store(true, std::memory_order_release);
-            }
-            std::lock_guard<std::mutex> l(p->m);
-            ++p->rec_done[it.buf];
-            p->cv.notify_all();
-            continue;
-        }
-        bool free_slot = slot != UINT64_MAX, ok = free_slot;
-        if (ok) {
-            ok = poll_zero(it.res->copied[it.g], 120);
-            // The image's record (an older snapshot's) stops counting before
-            // the first byte of a new one lands.
-            if (ok && it.g == 0 && c->file_map) file_invalidate(c, it.buf);
-            if (ok) c->pool->copy(it.image, c->h_bout + slot * unit, it.n);
-            else free_slot = false; // the engine may still write it
-        }
-        {
-            std::lock_guard<std::mutex> l(p->m);
-            if (free_slot) p->busy[slot] = 0;
-            if (slot != UINT64_MAX && !ok && !p->failed) {
-                p->failed = true;
-                p->err = "DMA of a chunk group to the bounce ring did not finish within 120 s";
-            }
-            p->cv.notify_all();
-        }
-        if (!ok) it.res->failed.store(true, std::memory_order_release);
-        it.res->landed.fetch_add(1, std::memory_order_acq_rel);
-    }
-}
-
-void stop_pump(ckpt_ctx* c)
-{
-    if (!c->pump) return;
-    {
-        std::lock_guard<std::mutex> l(c->pump->m);
-        c->pump->stop = true;
-    }
-    c->pump->cv.notify_all();
-    if (c->pump->issuer.joinable()) c->pump->issuer.join();
-    if (c->pump->drainer.joinable()) c->pump->drainer.join();
-    delete c->pump;
-    c->pump = nullptr;
-}
-
 ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop);
 
-} // namespace
+} // namespace ckpt
 
 extern "C" {
 
@@ -1707,33 +915,8 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
     HIPCHK(c, hipDeviceSynchronize());
     c->registered = true;
     if (c->file_mode == CKPT_FILE_ADOPT) {
-        // The file's newest valid record becomes this context's committed snapshot.
-        int best = -1;
-        for (int b = 0; b < 2; ++b) {
-            if (!rec_valid(c, b)) continue;
-            c->file_seq = std::max(c->file_seq, file_rec(c, b)->seq);
-            if (best < 0 || file_rec(c, b)->seq > file_rec(c, best)->seq) best = b;
-        }
-        if (best >= 0) {
-            RecRes* res = nullptr;
-            ckpt_status st = get_res(c, &res);
-            if (st) return st;
-            const FileRec* fr = file_rec(c, best);
-            const uint64_t id = c->next_id++;
-            SnapRec& r = c->recs[id];
-            r.id = id;
-            r.step = fr->step;
-            r.buf = best;
-            r.res = res;
-            r.bounce = true;
-            r.file = true;
-            res->recorded.store(true, std::memory_order_relaxed);
-            r.committed = true; // nothing in flight: its signals are all 0
-            const uint8_t* meta = c->file_map + c->fhead.meta_off[best];
-            r.meta.assign(meta, meta + fr->meta_len);
-            std::memcpy(c->h_sums[best], c->file_map + c->fhead.sums_off[best], 8 * c->n_chunks);
-            c->holder[best] = id;
-        }
+        ckpt_status st = adopt_image_file(c);
+        if (st) return st;
     }
     return CKPT_OK;
 }
@@ -1840,7 +1023,7 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
 
 } // extern "C"
 
-namespace {
+namespace ckpt {
 
 ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop)
 {
@@ -1953,7 +1136,7 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
     return CKPT_OK;
 }
 
-} // namespace
+} // namespace ckpt
 
 extern "C" {
 
@@ -2213,17 +1396,6 @@ ckpt_status ckpt_debug_tile_plan(const uint64_t* nbytes, uint32_t n, uint64_t ch
     if (tile_last && tile_first) std::memcpy(tile_last, p.tile_last.data(), 4 * p.n_tiles);
     return CKPT_OK;
 }
-
-ckpt_status ckpt_image_file(ckpt_ctx* c, const char* path, uint32_t mode)
-{
-    if (!c || !path || !*path || mode > CKPT_FILE_ADOPT) return fail(c, CKPT_EINVAL, "bad image file arguments");
-    if (c->registered) return fail(c, CKPT_ESTATE, "tensors already registered");
-    if (!c->bounce_cfg) return fail(c, CKPT_EINVAL, "an image file needs bounce mode (bounce_bytes > 0)");
-    c->file_path = path;
-    c->file_mode = (int)mode;
-    return CKPT_OK;
-}
-
 ckpt_status ckpt_latest(ckpt_ctx* c, uint64_t* snap_id, uint64_t* step)
 {
     if (!c || !snap_id) return CKPT_EINVAL;
@@ -2237,91 +1409,6 @@ ckpt_status ckpt_latest(ckpt_ctx* c, uint64_t* snap_id, uint64_t* step)
     }
     return CKPT_OK;
 }
-
-ckpt_status ckpt_replicate_to(ckpt_ctx* c, const char* host, uint32_t port, uint64_t cls_mask)
-{
-    if (!c || !host || port == 0 || port > 65535 || cls_mask == 0) return fail(c, CKPT_EINVAL, "bad replication target");
-    if (!c->registered) return fail(c, CKPT_ESTATE, "no tensors registered");
-    if (c->rep) return fail(c, CKPT_ESTATE, "a replication peer is already set");
-    // Chunks holding a byte of a fragment of a selected class.
-    std::vector<uint8_t> pick(c->n_chunks, 0);
-    for (const Frag& f : c->frags) {
-        if (!f.nbytes || f.cls >= 64 || !((cls_mask >> f.cls) & 1)) continue;
-        for (uint64_t k = f.off / c->C; k <= (f.off + f.nbytes - 1) / c->C; ++k) pick[k] = 1;
-    }
-    std::vector<uint64_t> ids;
-    for (uint64_t k = 0; k < c->n_chunks; ++k)
-        if (pick[k]) ids.push_back(k);
-    if (ids.empty()) return fail(c, CKPT_EINVAL, "no registered fragment has a selected class");
-    sockaddr_in a{};
-    a.sin_family = AF_INET;
-    a.sin_port = htons((uint16_t)port);
-    if (inet_pton(AF_INET, host, &a.sin_addr) != 1) return fail(c, CKPT_EINVAL, "host must be a dotted IPv4 address");
-    const int fd = ::socket(AF_INET, SOCK_STREAM, 0);
-    if (fd < 0) return fail(c, CKPT_EHIP, "socket: %s", strerror(errno));
-    tune_socket(fd);
-    if (::connect(fd, (sockaddr*)&a, sizeof a) != 0) {
-        const int e = errno;
-        ::close(fd);
-        return fail(c, CKPT_EHIP, "connect to %s:%u: %s", host, port, strerror(e));
-    }
-    Replicator* R = new Replicator();
-    R->fd = fd;
-    R->cls_mask = cls_mask;
-    R->ids = std::move(ids);
-    R->bytes = replica_bytes(R->ids.data(), R->ids.size(), c->C, c->I);
-    c->rep = R;
-    R->worker = std::thread(rep_worker, c);
-    return CKPT_OK;
-}
-
-ckpt_status ckpt_replica_chunks(ckpt_ctx* c, uint64_t* ids, uint64_t cap, uint64_t* n, uint64_t* replica_bytes_out)
-{
-    if (!c || !n) return CKPT_EINVAL;
-    if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
-    *n = c->rep->ids.size();
-    if (replica_bytes_out) *replica_bytes_out = c->rep->bytes;
-    if (ids) std::memcpy(ids, c->rep->ids.data(), 8 * std::min<uint64_t>(cap, c->rep->ids.size()));
-    return CKPT_OK;
-}
-
-ckpt_status ckpt_replica_result(ckpt_ctx* c, uint64_t snap_id, int32_t* state, uint64_t* bad, uint32_t cap,
-                                uint32_t* n_bad)
-{
-    if (!c || !state) return CKPT_EINVAL;
-    if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
-    std::lock_guard<std::mutex> l(c->rep->m);
-    auto s = c->rep->status.find(snap_id);
-    if (s == c->rep->status.end())
-        return fail(c, CKPT_ERANGE, "snapshot %llu is not being replicated", (unsigned long long)snap_id);
-    *state = s->second.state;
-    if (n_bad) *n_bad = (uint32_t)s->second.bad.size();
-    if (bad) std::memcpy(bad, s->second.bad.data(), 8 * std::min<uint64_t>(cap, s->second.bad.size()));
-    return CKPT_OK;
-}
-
-ckpt_status ckpt_replica_timing(ckpt_ctx* c, double* send_ms, double* ack_ms)
-{
-    if (!c || !send_ms || !ack_ms) return CKPT_EINVAL;
-    if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
-    std::lock_guard<std::mutex> l(c->rep->m);
-    *send_ms = c->rep->last_send_ms;
-    *ack_ms = c->rep->last_ack_ms;
-    return CKPT_OK;
-}
-
-ckpt_status ckpt_debug_h2h_fault(ckpt_ctx* c, int32_t kind, uint64_t a, uint64_t b)
-{
-    if (!c || kind < 0 || kind > 2) return CKPT_EINVAL;
-    if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
-    std::lock_guard<std::mutex> l(c->rep->m);
-    if (kind && a >= c->rep->bytes) return fail(c, CKPT_EINVAL, "fault position beyond the replica");
-    c->rep->fault_kind = kind;
-    c->rep->fault_a = a;
-    c->rep->fault_b = b;
-    return CKPT_OK;
-}
-
 const char* ckpt_last_error(const ckpt_ctx* c) { return c ? c->err.c_str() : "null context"; }
 
 } // extern "C"

@@ -40,21 +40,27 @@ def build():
             "-L", lib_dir, "-lckpt", "-Wl,-rpath," + lib_dir, "-L/opt/rocm/lib", "-lamdhip64",
             "-Wl,-rpath,/opt/rocm/lib"])
     os.replace(ROUNDTRIP + ".tmp", ROUNDTRIP)
-    # sanitized host runtime + the existing kernel object
-    r_san = os.path.join(obj, "ckpt_runtime_san.o")
-    _run(["g++", "-O1", "-g", "-std=c++17", "-fPIC", "-pthread", "-D__HIP_PLATFORM_AMD__"] + SAN
-         + INC + ["-I", os.path.join(PKG, "csrc"), "-c", os.path.join(PKG, "csrc", "ckpt_runtime.cpp"), "-o", r_san])
+    # sanitized host runtime (every host source of the library) + the existing kernel object
+    sys.path.insert(0, ROOT)
+    from paper_2607_01646_amd.build import HOST_SOURCES
+
+    r_san = []
+    for src in HOST_SOURCES:
+        o = os.path.join(obj, src.replace(".cpp", "_san.o"))
+        _run(["g++", "-O1", "-g", "-std=c++17", "-fPIC", "-pthread", "-D__HIP_PLATFORM_AMD__"] + SAN
+             + INC + ["-I", os.path.join(PKG, "csrc"), "-c", os.path.join(PKG, "csrc", src), "-o", o])
+        r_san.append(o)
     _run(["gcc", "-O1", "-g", "-std=c11"] + SAN + INC
          + ["-c", os.path.join(HERE, "plan_fuzz.c"), "-o", os.path.join(obj, "plan_fuzz.o")])
     _run(["gcc", "-O1", "-g", "-std=c11", "-c", ORACLE_C, "-o", os.path.join(obj, "oracle_c.o")])
-    _run(["g++"] + SAN + [os.path.join(obj, "plan_fuzz.o"), os.path.join(obj, "oracle_c.o"), r_san,
-                          os.path.join(obj, "ckpt_kernels.o"), "-o", PLAN_FUZZ + ".tmp", "-pthread",
+    _run(["g++"] + SAN + [os.path.join(obj, "plan_fuzz.o"), os.path.join(obj, "oracle_c.o")] + r_san
+         + [os.path.join(obj, "ckpt_kernels.o"), "-o", PLAN_FUZZ + ".tmp", "-pthread",
                           "-L/opt/rocm/lib", "-lamdhip64", "-lhsa-runtime64", "-Wl,-rpath,/opt/rocm/lib"])
     os.replace(PLAN_FUZZ + ".tmp", PLAN_FUZZ)
     _run(["gcc", "-O1", "-g", "-std=c11", "-D__HIP_PLATFORM_AMD__"] + SAN + INC
          + ["-c", os.path.join(HERE, "abi_roundtrip.c"), "-o", os.path.join(obj, "abi_roundtrip_san.o")])
-    _run(["g++"] + SAN + [os.path.join(obj, "abi_roundtrip_san.o"), os.path.join(obj, "oracle_c.o"), r_san,
-                          os.path.join(obj, "ckpt_kernels.o"), "-o", ROUNDTRIP_SAN + ".tmp", "-pthread",
+    _run(["g++"] + SAN + [os.path.join(obj, "abi_roundtrip_san.o"), os.path.join(obj, "oracle_c.o")] + r_san
+         + [os.path.join(obj, "ckpt_kernels.o"), "-o", ROUNDTRIP_SAN + ".tmp", "-pthread",
                           "-L/opt/rocm/lib", "-lamdhip64", "-lhsa-runtime64", "-Wl,-rpath,/opt/rocm/lib"])
     os.replace(ROUNDTRIP_SAN + ".tmp", ROUNDTRIP_SAN)
     return ROUNDTRIP, PLAN_FUZZ, ROUNDTRIP_SAN
