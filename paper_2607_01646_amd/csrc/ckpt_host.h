@@ -38,10 +38,6 @@ namespace ckpt {
 constexpr uint64_t kDefaultChunk = 64ull << 20;
 constexpr uint32_t kDefaultAlign = 256;
 constexpr uint64_t kDefaultGroup = 1ull << 30;
-// 8 KiB tiles: each of a workgroup's 256 lanes moves exactly one batch of
-// two 16-byte vectors per tile (measured fastest on gfx950 with one
-// workgroup per tile in 1 GiB launches).
-constexpr uint32_t kMaxTileShift = 13;
 constexpr uint32_t kMaxMeta = 1u << 20;
 constexpr uint32_t kDefaultGrid = 0x7fffffff; // one workgroup per tile unless capped
 constexpr int kMaxEngines = 2;

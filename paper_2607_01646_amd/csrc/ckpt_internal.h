@@ -28,6 +28,10 @@ struct Geometry {
 // Partial sums per tile: each wave of a tile's workgroup sums its own slice.
 constexpr uint32_t kTileParts = 4;
 
+// Tiles are at most 1 << kMaxTileShift = 8 KiB: each wave's slice of a tile
+// is at most one batch of two 16-byte vectors per lane.
+constexpr uint32_t kMaxTileShift = 13;
+
 // The tile kernels.  Each covers tiles [t_lo, t_hi) and writes tile t's
 // word-sums to partials[t * kTileParts ...] (one per wave slice; partials
 // holds kTileParts entries per tile of the image); launches cover whole

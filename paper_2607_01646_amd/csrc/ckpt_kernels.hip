@@ -11,11 +11,12 @@
 // floating-point instruction touches them, so NaN payloads, -0 and
 // subnormals pass unchanged.
 //
-// Work split.  The image is cut into power-of-two tiles (8 KiB) that never
-// cross a chunk.  A workgroup of 256 lanes (4 wave64) takes one tile (or
-// tiles grid-stride when the grid is capped); each wave owns a contiguous
-// quarter of it (2 KiB) and each lane moves two 16-byte vectors of that
-// slice, both loads issued before the stores.  Consecutive tiles go to
+// Work split.  The image is cut into power-of-two tiles of at most 8 KiB
+// that never cross a chunk.  A workgroup of 256 lanes (4 wave64) takes one
+// tile (a separate instantiation strides over tiles when the grid is
+// capped).  Wave w owns the tile's 2 KiB slice w, and each lane moves two
+// 16-byte vectors of it, both loads issued before the stores; a tile shorter
+// than 8 KiB leaves its last waves idle.  Consecutive tiles go to
 // consecutive workgroups, which the hardware deals out round-robin over the
 // 8 XCDs (measured faster than giving each XCD a contiguous range).  A tile
 // inside one 16-byte-aligned fragment takes an unrolled non-temporal stream;
@@ -172,47 +173,26 @@ __device__ __forceinline__ void st(u32x4 v, u32x4* p)
     else *p = v;
 }
 
-// Streaming copy of the aligned 16-byte vectors [v0, v1) with their sum:
-// lane l takes v0 + l, v0 + l + 64, ..., UNROLL loads in flight before the
-// stores, so each wave moves contiguous 1 KiB runs.
-template <int UNROLL, bool NTL, bool NTS>
-__device__ __forceinline__ unsigned long long slice_copy(const u32x4* __restrict__ s, u32x4* __restrict__ d,
-                                                         uint32_t v0, uint32_t v1, uint32_t lane)
+// One wave's slice of a tile inside one 16-byte-aligned span: the n <= 64 *
+// UNROLL vectors at s (copied to d unless d is null) and their sum.  Lane l
+// takes vectors l, l + 64, ...; every guarded load is issued before the
+// first store, each a contiguous 1 KiB run per wave.  Written out without
+// a loop: a runtime trip count here measured ~1.5% slower.
+template <int UNROLL, bool NTL, bool NTS, bool STORE>
+__device__ __forceinline__ unsigned long long slice_stream(const u32x4* __restrict__ s, u32x4* __restrict__ d,
+                                                           uint32_t n, uint32_t lane)
 {
+    u32x4 r[UNROLL];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u)
+        if (lane + u * 64 < n) r[u] = ld<NTL>(s + lane + u * 64);
     unsigned long long acc = 0;
-    uint32_t v = v0 + lane;
-    for (; v + (UNROLL - 1) * 64 < v1; v += UNROLL * 64) {
-        u32x4 r[UNROLL];
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u) r[u] = ld<NTL>(s + v + u * 64);
-#pragma unroll
-        for (int u = 0; u < UNROLL; ++u) {
-            st<NTS>(r[u], d + v + u * 64);
+    for (int u = 0; u < UNROLL; ++u)
+        if (lane + u * 64 < n) {
+            if (STORE) st<NTS>(r[u], d + lane + u * 64);
             acc += vsum(r[u]);
         }
-    }
-    for (; v < v1; v += 64) {
-        const u32x4 r = ld<NTL>(s + v);
-        st<NTS>(r, d + v);
-        acc += vsum(r);
-    }
-    return acc;
-}
-
-template <int UNROLL, bool NTL>
-__device__ __forceinline__ unsigned long long slice_sum(const u32x4* __restrict__ s, uint32_t v0, uint32_t v1,
-                                                        uint32_t lane)
-{
-    unsigned long long acc = 0;
-    uint32_t v = v0 + lane;
-    for (; v + (UNROLL - 1) * 64 < v1; v += UNROLL * 64) {
-        u32x4 r[UNROLL];
-#pragma unroll
-        for (int u = 0; u < UNROLL; ++u) r[u] = ld<NTL>(s + v + u * 64);
-#pragma unroll
-        for (int u = 0; u < UNROLL; ++u) acc += vsum(r[u]);
-    }
-    for (; v < v1; v += 64) acc += vsum(ld<NTL>(s + v));
     return acc;
 }
 
@@ -282,39 +262,40 @@ __device__ __forceinline__ uint64_t remap_block(uint32_t b, uint32_t n)
     return (uint64_t)x * q + (x < r ? x : r) + k;
 }
 
-template <int MODE, int BLOCK = kBlock, int UNROLL = kUnroll, bool NTL = true, bool NTS = true, bool REMAP = false>
-__global__ __launch_bounds__(BLOCK) void tile_kernel(Args a)
+// One tile: wave w owns vectors [w * slice, (w + 1) * slice) of it and
+// stores that slice's sum to partials[t * WAVES + w].
+template <int MODE, int BLOCK, int UNROLL, bool NTL, bool NTS>
+__device__ __forceinline__ void do_tile(const Args& a, uint64_t t, uint64_t* s_off)
 {
     static_assert(BLOCK / 64 == kTileParts, "one partial sum per wave");
+    static_assert(BLOCK * UNROLL * 16 == (1u << kMaxTileShift), "one batch per lane covers the largest tile");
     constexpr uint32_t WAVES = BLOCK / 64;
-    __shared__ uint64_t s_off[kLdsFrags];
+    constexpr uint32_t kSlice = 64 * UNROLL; // vectors per wave slice
     const uint32_t tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const uint64_t first = REMAP ? remap_block(blockIdx.x, gridDim.x) : blockIdx.x;
-    // Wave w owns vectors [w * slice, (w + 1) * slice) of the tile.
-    const uint32_t tile_vecs = 1u << (a.g.tile_shift - 4);
-    const uint32_t slice = (tile_vecs + WAVES - 1) / WAVES;
-    for (uint64_t t = a.t_lo + first; t < a.t_hi; t += gridDim.x) {
+    {
         const uint64_t base = t << a.g.tile_shift;
         uint64_t end = base + (1ull << a.g.tile_shift);
         if (end > a.g.image_bytes) end = a.g.image_bytes;
         const uint32_t nvec = (uint32_t)((end - base) >> 4);
-        const uint32_t v0 = w * slice;
-        const uint32_t v1 = v0 + slice < nvec ? v0 + slice : nvec;
+        // Wave w owns vectors [v0, v1) of the tile (empty past a short tile's end).
+        const uint32_t v0 = w * kSlice;
+        const uint32_t v1 = v0 + kSlice < nvec ? v0 + kSlice : (nvec > v0 ? nvec : v0);
         uint8_t* win = a.img + (base - a.origin);
         unsigned long long acc = 0;
         if (MODE == VERIFY) {
-            acc = slice_sum<UNROLL, NTL>(reinterpret_cast<const u32x4*>(win), v0, v1, lane);
+            acc = slice_stream<UNROLL, NTL, NTS, false>(reinterpret_cast<const u32x4*>(win) + v0, nullptr, v1 - v0, lane);
         } else {
             const uint32_t f0 = a.tile_first[t], f1 = a.tile_last[t];
             if (f0 == f1) {
                 const FragDev F = a.frags[f0];
                 const uint64_t p0 = base - F.off;
                 if ((F.ptr & 15) == 0 && p0 + (end - base) <= F.nbytes) {
-                    u32x4* fr = reinterpret_cast<u32x4*>(F.ptr + p0);
+                    u32x4* fr = reinterpret_cast<u32x4*>(F.ptr + p0) + v0;
+                    u32x4* wv = reinterpret_cast<u32x4*>(win) + v0;
                     if (MODE == PACK)
-                        acc = slice_copy<UNROLL, NTL, NTS>(fr, reinterpret_cast<u32x4*>(win), v0, v1, lane);
+                        acc = slice_stream<UNROLL, NTL, NTS, true>(fr, wv, v1 - v0, lane);
                     else
-                        acc = slice_copy<UNROLL, NTL, NTS>(reinterpret_cast<const u32x4*>(win), fr, v0, v1, lane);
+                        acc = slice_stream<UNROLL, NTL, NTS, true>(wv, fr, v1 - v0, lane);
                 } else {
                     for (uint32_t v = v0 + lane; v < v1; v += 64) {
                         const uint64_t p = p0 + 16ull * v;
@@ -364,18 +345,49 @@ __global__ __launch_bounds__(BLOCK) void tile_kernel(Args a)
     }
 }
 
-// One workgroup per chunk: add the chunk's tile sums; when expected is given,
-// also flag a mismatch.
-__global__ __launch_bounds__(kBlock) void chunk_reduce_kernel(ReduceArgs r)
+// Without LOOP the grid has one workgroup per tile and each takes exactly
+// one (a grid-stride loop around the same body measured ~3% slower on the
+// default launch); with LOOP a capped grid strides over the tiles.
+template <int MODE, bool LOOP, int BLOCK = kBlock, int UNROLL = kUnroll, bool NTL = true, bool NTS = true,
+          bool REMAP = false>
+__global__ __launch_bounds__(BLOCK) void tile_kernel(Args a)
 {
-    __shared__ unsigned long long s_red[kBlock / 64];
+    __shared__ uint64_t s_off[kLdsFrags];
+    const uint64_t first = REMAP ? remap_block(blockIdx.x, gridDim.x) : blockIdx.x;
+    if (LOOP) {
+        for (uint64_t t = a.t_lo + first; t < a.t_hi; t += gridDim.x) do_tile<MODE, BLOCK, UNROLL, NTL, NTS>(a, t, s_off);
+    } else {
+        const uint64_t t = a.t_lo + first;
+        if (t < a.t_hi) do_tile<MODE, BLOCK, UNROLL, NTL, NTS>(a, t, s_off);
+    }
+}
+
+// One workgroup per chunk: add the chunk's tile sums; when expected is given,
+// also flag a mismatch.  A 64 MiB chunk has 32768 partial sums; each lane
+// keeps eight independent loads in flight (a plain strided loop with one
+// load at a time took ~70 us per 1 GiB of chunks).
+constexpr int kReduceBlock = 1024;
+constexpr int kReduceUnroll = 8;
+
+__global__ __launch_bounds__(kReduceBlock) void chunk_reduce_kernel(ReduceArgs r)
+{
+    __shared__ unsigned long long s_red[kReduceBlock / 64];
     const uint64_t c = r.c_lo + blockIdx.x;
     const uint64_t t0 = c * r.tiles_per_chunk;
     uint64_t t1 = t0 + r.tiles_per_chunk;
     if (t1 > r.n_tiles) t1 = r.n_tiles;
+    const uint64_t end = t1 * kTileParts;
+    uint64_t k = t0 * kTileParts + threadIdx.x;
     unsigned long long acc = 0;
-    for (uint64_t k = t0 * kTileParts + threadIdx.x; k < t1 * kTileParts; k += kBlock) acc += r.partials[k];
-    const unsigned long long s = block_sum<kBlock>(acc, s_red);
+    for (; k + (kReduceUnroll - 1) * kReduceBlock < end; k += kReduceUnroll * kReduceBlock) {
+        unsigned long long v[kReduceUnroll];
+#pragma unroll
+        for (int u = 0; u < kReduceUnroll; ++u) v[u] = r.partials[k + u * kReduceBlock];
+#pragma unroll
+        for (int u = 0; u < kReduceUnroll; ++u) acc += v[u];
+    }
+    for (; k < end; k += kReduceBlock) acc += r.partials[k];
+    const unsigned long long s = block_sum<kReduceBlock>(acc, s_red);
     if (threadIdx.x == 0) {
         r.sums_out[c] = s;
         if (r.expected) r.bad[c] = (s != r.expected[c]) ? 1 : 0;
@@ -390,10 +402,11 @@ hipError_t launch_tiles(const Args& a, uint32_t grid_cap, hipStream_t s, hipEven
     if (a.t_hi <= a.t_lo) return hipSuccess;
     const uint64_t n = a.t_hi - a.t_lo;
     const uint32_t grid = (uint32_t)(n < grid_cap ? n : grid_cap);
+    void (*kern)(Args) = grid == n ? tile_kernel<MODE, false> : tile_kernel<MODE, true>;
     if (t0 && t1)
-        hipExtLaunchKernelGGL(tile_kernel<MODE>, dim3(grid), dim3(kBlock), 0, s, t0, t1, 0, a);
+        hipExtLaunchKernelGGL(kern, dim3(grid), dim3(kBlock), 0, s, t0, t1, 0, a);
     else
-        hipLaunchKernelGGL(tile_kernel<MODE>, dim3(grid), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL(kern, dim3(grid), dim3(kBlock), 0, s, a);
     return hipGetLastError();
 }
 
@@ -454,7 +467,7 @@ hipError_t launch_chunk_reduce(const Geometry& g, uint64_t t_lo, uint64_t t_hi, 
     r.sums_out = sums_out;
     r.expected = expected;
     r.bad = bad;
-    hipLaunchKernelGGL(chunk_reduce_kernel, dim3((uint32_t)(r.c_hi - r.c_lo)), dim3(kBlock), 0, s, r);
+    hipLaunchKernelGGL(chunk_reduce_kernel, dim3((uint32_t)(r.c_hi - r.c_lo)), dim3(kReduceBlock), 0, s, r);
     return hipGetLastError();
 }
 

@@ -128,7 +128,7 @@ bool setup_geometry(ckpt_peer* p, const WireHead& h, const std::vector<uint64_t>
     p->R = h.replica_bytes;
     p->ids = ids;
     uint32_t ts = 0;
-    while (ts < 13 && (C >> (ts + 1)) << (ts + 1) == C) ++ts; // largest power of two <= 8 KiB dividing C
+    while (ts < kMaxTileShift && (C >> (ts + 1)) << (ts + 1) == C) ++ts; // largest power of two <= 8 KiB dividing C
     p->geo.image_bytes = p->R;
     p->geo.tile_shift = ts;
     p->geo.tiles_per_chunk = (uint32_t)(C >> ts);

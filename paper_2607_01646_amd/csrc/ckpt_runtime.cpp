@@ -4,9 +4,10 @@
 // the wait before the optimizer step), chunk group by chunk group g:
 //
 //   pack stream  : [wait: area_done[area(g)] >= uses of the area issued so far]
-//                  pack kernels (fragments -> staging, chunk sums)
+//                  pack kernel (fragments -> staging, tile sums)
 //                  event captured[g]            <- the gate waits on this
 //                  release kernel: dep[g] = 0
+//                  reduce kernel (tile sums -> chunk sums)
 //   SDMA engine e: (polls dep[g]) copy staging(g) -> pinned image   -> copied[g]
 //                  (after copied[g]) 8-byte copy: area_done[area(g)] = use count
 //   after the last group: release dep_sums; SDMA copies the chunk sums.
@@ -1046,17 +1047,21 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
                                    tiles_hi(c, g), staging_of(c, g), lo, c->d_partials, c->grid_cap, c->s_pack,
                                    r.timed ? res->k0[g] : nullptr, r.timed ? res->k1[g] : nullptr);
         if (e != hipSuccess) return fail(c, CKPT_EHIP, "pack launch failed: %s", hipGetErrorString(e));
+        // The gate and the group's copy need the packed bytes only; the chunk
+        // sums of the group are added up behind them.
+        HIPCHK(c, hipEventRecord(res->captured[g], c->s_pack));
+        if (g < n_copy) {
+            hsa_signal_store_screlease(res->dep[g], 1);
+            e = launch_release(res->dep_val[g], c->s_pack);
+            if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
+        }
         e = launch_chunk_reduce(c->geo, tiles_lo(c, g), tiles_hi(c, g), c->d_partials, res->d_sums, nullptr, nullptr,
                                 c->s_pack);
         if (e != hipSuccess) return fail(c, CKPT_EHIP, "reduce launch failed: %s", hipGetErrorString(e));
-        HIPCHK(c, hipEventRecord(res->captured[g], c->s_pack));
         if (g >= n_copy) continue; // interrupted offload: this group never leaves the device
-        hsa_signal_store_screlease(res->dep[g], 1);
         hsa_signal_store_screlease(res->copied[g], 1);
         hsa_signal_store_screlease(res->flagged[g], 1);
         r.groups_copied = (uint32_t)(g + 1);
-        e = launch_release(res->dep_val[g], c->s_pack);
-        if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
         const hsa_amd_sdma_engine_id_t eng = c->d2h_engine[g % c->n_d2h_engines];
         res->h_seq[g] = c->area_seq[area] + 1;
         if (r.bounce) { // the pump issues the copies once a ring slot is free
