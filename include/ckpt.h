@@ -334,11 +334,15 @@ ckpt_status ckpt_debug_h2h_fault(ckpt_ctx* ctx, int32_t kind, uint64_t a, uint64
  * one sender at a time, receives each snapshot's replica into the pinned
  * buffer that does not hold its newest committed replica, re-checks every
  * chunk sum on cfg->device with the library's checksum kernel (host->device
- * copies through a two-slot device ring, cfg->group_bytes per slot), and
+ * copies through a two-slot device ring, cfg->group_bytes per slot, each
+ * slot checked while the next one is received), and
  * commits the buffer only when every sum matches (Sec. VI-A: the buffer
  * received from the ring predecessor alternates like the local one).  A
  * stream cut mid-snapshot leaves the previous replica in place; the peer
- * then waits for the next connection. */
+ * then waits for the next connection.  A replacement rank's fetch
+ * (ckpt_restore_from_peer) is answered on a connection of its own, also
+ * between two snapshots of a connected sender; a second sender is refused
+ * while one is connected. */
 typedef struct ckpt_peer ckpt_peer;
 ckpt_status ckpt_peer_create(const ckpt_config* cfg, uint32_t port, ckpt_peer** out);
 ckpt_status ckpt_peer_port(const ckpt_peer* peer, uint32_t* port);
@@ -359,9 +363,55 @@ ckpt_status ckpt_peer_replica(ckpt_peer* peer, uint64_t* snap_id, uint64_t* step
 /* The sender's chunk ids that failed the check in the last rejected
  * snapshot (up to cap; *n the count). */
 ckpt_status ckpt_peer_last_bad(ckpt_peer* peer, uint64_t* bad, uint32_t cap, uint32_t* n);
-/* Receive and GPU-check time of the last replica (ms). */
+/* Host wall time of the last replica (ms): from its header to the last byte
+ * received (recv_ms), and from there to the end of the GPU check (check_ms;
+ * the check of each unit overlaps the receipt of the next). */
 ckpt_status ckpt_peer_timing(ckpt_peer* peer, double* recv_ms, double* check_ms);
 const char* ckpt_peer_last_error(const ckpt_peer* peer);
+
+/* ---- A replacement rank's optimizer state from its ring peer (Sec. V-C,
+ * third recovery stage: the optimizer shard comes back from the replica the
+ * peer kept in memory; the parameter shard comes from the ranks that share
+ * the failed rank's partition, which this library does not do) ----
+ *
+ * ckpt_restore_from_peer: ctx belongs to the replacement and is registered
+ * with the failed rank's layout (the same fragment sizes, dtypes and
+ * classes in the same order, chunk size and alignment).  Connects to the
+ * peer at host:port (dotted IPv4; ckpt_peer_*), fetches the newest replica
+ * the peer has committed, and checks that the replica's envelope describes
+ * this layout byte for byte (rebuilt from the context's fragment table with
+ * the envelope's step, sums and blob) and that its chunk sums agree with
+ * the envelope.  The replicated chunks are received into the host image
+ * that the next snapshot would fill, at their image offsets; a snapshot
+ * held there is no longer restorable (ckpt_snapshot_state: SUPERSEDED).
+ * As ckpt_restore but for those chunks only, each run of chunks as soon as
+ * it has arrived: every fragment byte they hold is written back to the
+ * registered tensors (parameter bytes sharing a chunk with optimizer bytes
+ * included), each chunk's sum is recomputed on the GPU and compared with the
+ * sum stored at pack time, and `stream` waits for the writes.  Fragment
+ * bytes outside the replicated chunks are left as they are.  *snap_id / *step (may be NULL): the failed rank's snapshot id
+ * and step.  Blocks until done (a 300 s limit on the transfer).  Does not
+ * change ckpt_last_sums or the restore timing.
+ * Errors: EINVAL (bad argument, or the reply does not match this layout:
+ * nothing written), ESTATE (not registered), EBUSY (a snapshot has not
+ * committed, or the target image is being sent to this context's own peer),
+ * ENOSNAP (the peer holds no committed replica), EHIP (connection or HIP
+ * failure; a transfer that breaks midway leaves the chunks before the break
+ * written), ECORRUPT (chunks failed their sum: their ids in bad_chunks up to
+ * cap, *n_bad the count; every replicated chunk was still written). */
+ckpt_status ckpt_restore_from_peer(ckpt_ctx* ctx, const char* host, uint32_t port, void* stream, uint64_t* snap_id,
+                                   uint64_t* step, uint32_t* bad_chunks, uint32_t cap, uint32_t* n_bad);
+
+/* What the last ckpt_restore_from_peer received (each output may be NULL):
+ * the chunk ids it wrote (increasing; up to cap; *n_ids the count), the
+ * replica's envelope (the format of ckpt_envelope, including the caller
+ * blob of the failed rank's snapshot; nothing is written and EINVAL is
+ * returned when env_cap is smaller than *env_len), and host wall times in
+ * ms: connect to the last replica byte received (fetch_ms), and from there
+ * to the end of the restore and check (check_ms).  Errors: ESTATE (none
+ * yet), EINVAL. */
+ckpt_status ckpt_peer_restore_info(ckpt_ctx* ctx, uint64_t* ids, uint64_t cap, uint64_t* n_ids, void* envelope,
+                                   uint64_t env_cap, uint64_t* env_len, double* fetch_ms, double* check_ms);
 
 /* Text of the context's last error ("" if none).  Valid until the next call. */
 const char* ckpt_last_error(const ckpt_ctx* ctx);

@@ -114,6 +114,9 @@ def lib():
             "ckpt_peer_last_bad": ([vp, P(u64), u32, P(u32)], i32),
             "ckpt_peer_timing": ([vp, P(C.c_double), P(C.c_double)], i32),
             "ckpt_peer_last_error": ([vp], C.c_char_p),
+            "ckpt_restore_from_peer": ([vp, C.c_char_p, u32, vp, P(u64), P(u64), P(u32), u32, P(u32)], i32),
+            "ckpt_peer_restore_info": ([vp, P(u64), u64, P(u64), vp, u64, P(u64), P(C.c_double), P(C.c_double)],
+                                       i32),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -366,6 +369,32 @@ def ckpt_debug_h2h_fault(ctx, kind, a=0, b=0):
     return _check(ctx, lib().ckpt_debug_h2h_fault(ctx, kind, a, b))
 
 
+def ckpt_restore_from_peer(ctx, host, port, stream=None):
+    """A replacement rank's restore from its ring peer's newest committed
+    replica: (snap_id, step, [chunk ids whose sum failed])."""
+    _, _, nc = ckpt_layout(ctx, offsets=False)
+    s = _stream(stream)
+    sid, step = C.c_uint64(), C.c_uint64()
+    bad = _bad_list_call(ctx, lambda b, cap, n: lib().ckpt_restore_from_peer(ctx, host.encode(), port, s,
+                                                                              C.byref(sid), C.byref(step), b, cap,
+                                                                              n), nc)
+    return sid.value, step.value, bad
+
+
+def ckpt_peer_restore_info(ctx):
+    """What the last restore from a peer received: {"chunk_ids", "envelope",
+    "fetch_ms", "check_ms"}."""
+    n, elen = C.c_uint64(), C.c_uint64()
+    fetch, check = C.c_double(), C.c_double()
+    _check(ctx, lib().ckpt_peer_restore_info(ctx, None, 0, C.byref(n), None, 0, C.byref(elen), None, None))
+    ids = np.zeros(max(n.value, 1), dtype=np.uint64)
+    env = C.create_string_buffer(max(elen.value, 1))
+    _check(ctx, lib().ckpt_peer_restore_info(ctx, _u64p(ids), n.value, C.byref(n), env, elen.value, C.byref(elen),
+                                             C.byref(fetch), C.byref(check)))
+    return {"chunk_ids": ids[:n.value], "envelope": env.raw[:elen.value], "fetch_ms": fetch.value,
+            "check_ms": check.value}
+
+
 class PeerError(RuntimeError):
     def __init__(self, code, msg):
         super().__init__("%s (%d): %s" % (_NAMES.get(code, "CKPT_E?"), code, msg))
@@ -509,6 +538,14 @@ class Checkpointer:
 
     def replica_result(self, snap):
         return ckpt_replica_result(self.ctx, snap)
+
+    def restore_from_peer(self, port, host="127.0.0.1", stream=None):
+        """Take the failed rank's replicated chunks back from its ring peer:
+        (snap_id, step, [bad chunk ids])."""
+        return ckpt_restore_from_peer(self.ctx, host, port, stream)
+
+    def peer_restore_info(self):
+        return ckpt_peer_restore_info(self.ctx)
 
     def close(self):
         if self.ctx is not None:

@@ -163,17 +163,10 @@ ckpt_status ckpt_replicate_to(ckpt_ctx* c, const char* host, uint32_t port, uint
     for (uint64_t k = 0; k < c->n_chunks; ++k)
         if (pick[k]) ids.push_back(k);
     if (ids.empty()) return fail(c, CKPT_EINVAL, "no registered fragment has a selected class");
-    sockaddr_in a{};
-    a.sin_family = AF_INET;
-    a.sin_port = htons((uint16_t)port);
-    if (inet_pton(AF_INET, host, &a.sin_addr) != 1) return fail(c, CKPT_EINVAL, "host must be a dotted IPv4 address");
-    const int fd = ::socket(AF_INET, SOCK_STREAM, 0);
-    if (fd < 0) return fail(c, CKPT_EHIP, "socket: %s", strerror(errno));
-    tune_socket(fd);
-    if (::connect(fd, (sockaddr*)&a, sizeof a) != 0) {
-        const int e = errno;
-        ::close(fd);
-        return fail(c, CKPT_EHIP, "connect to %s:%u: %s", host, port, strerror(e));
+    const int fd = dial(host, port);
+    if (fd < 0) {
+        if (errno == EINVAL) return fail(c, CKPT_EINVAL, "host must be a dotted IPv4 address");
+        return fail(c, CKPT_EHIP, "connect to %s:%u: %s", host, port, strerror(errno));
     }
     Replicator* R = new Replicator();
     R->fd = fd;

@@ -22,6 +22,7 @@
 #include <cstdio>
 #include <cstring>
 #include <deque>
+#include <functional>
 #include <map>
 #include <memory>
 #include <mutex>
@@ -273,6 +274,15 @@ struct Replicator {
     std::thread worker;
 };
 
+// What the last ckpt_restore_from_peer fetched.
+struct PeerRestore {
+    bool valid = false;
+    uint64_t snap_id = 0, step = 0;
+    std::vector<uint64_t> ids; // chunks written
+    std::vector<uint8_t> envelope;
+    double fetch_ms = 0, check_ms = 0;
+};
+
 } // namespace ckpt
 
 using namespace ckpt;
@@ -355,6 +365,9 @@ struct ckpt_ctx {
     // H2H replication to a ring peer
     Replicator* rep = nullptr;
 
+    // the last restore from a ring peer's replica
+    PeerRestore peer_restore;
+
     // image file (crash-surviving images; bounce mode only)
     std::string file_path;
     int file_mode = -1; // -1 none, else CKPT_FILE_CREATE / CKPT_FILE_ADOPT
@@ -397,6 +410,21 @@ uint64_t round_up(uint64_t x, uint64_t a);
 
 // Snapshot records (ckpt_runtime.cpp)
 ckpt_status get_res(ckpt_ctx* c, RecRes** out);
+// Wait until every snapshot's copies have finished and the library's
+// streams are idle.
+ckpt_status drain(ckpt_ctx* c);
+// The host image the next snapshot would fill (EBUSY while a snapshot is
+// uncommitted or that image is being sent to the peer).
+ckpt_status pick_target_image(ckpt_ctx* c, int* out);
+// Restore (scatter) or verify host image b against h_sums[b]: all chunks,
+// or only `ids` (increasing).  Fills the bad list like ckpt_restore.  With
+// `fill`, each span [lo, hi) of image bytes is first handed to fill, which
+// puts them in place (the host -> device work of earlier spans runs
+// meanwhile); false from fill ends the operation with EHIP once the work
+// already issued has finished (the caller records the error text).
+ckpt_status check_image(ckpt_ctx* c, int b, hipStream_t stream, bool scatter, const std::vector<uint64_t>* ids,
+                        uint32_t* bad_chunks, uint32_t cap, uint32_t* n_bad,
+                        const std::function<bool(uint64_t, uint64_t)>& fill = nullptr);
 bool res_done(const RecRes* res, uint32_t groups_copied, bool bounce);
 void parallel_zero(uint8_t* p, uint64_t n);
 std::vector<uint8_t> build_envelope(const ckpt_ctx* c, uint64_t step, const std::vector<uint8_t>& meta,

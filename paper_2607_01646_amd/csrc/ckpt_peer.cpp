@@ -9,8 +9,12 @@
 // committed replica, re-check every chunk sum on the GPU (host -> device
 // copies through a two-slot device ring, then the library's checksum and
 // chunk-reduce kernels over the replica laid out as an image of its own
-// chunks), commit only if every sum matches, and answer the sender.  A
+// chunks; each unit is checked while the next one arrives), commit only if
+// every sum matches, and answer the sender.  A
 // stream that breaks mid-snapshot leaves the previous replica in place.
+// A replacement rank (Sec. V-C, third recovery stage) fetches the newest
+// committed replica on a connection of its own, also between two snapshots
+// of a connected sender.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -162,8 +166,12 @@ bool setup_geometry(ckpt_peer* p, const WireHead& h, const std::vector<uint64_t>
 }
 
 // Re-check every chunk sum of replica buffer b on the GPU; fills bad with
-// the sender's ids of the chunks that differ.  Returns false on a HIP error.
-bool check_on_gpu(ckpt_peer* p, int b, std::vector<uint64_t>& bad)
+// the sender's ids of the chunks that differ.  fill(lo, hi) first puts
+// replica bytes [lo, hi) in place (received from the sender while the
+// earlier units are copied and checked).  Returns false when fill fails or
+// on a HIP error, after the work already issued has finished.
+template <class Fill>
+bool check_on_gpu(ckpt_peer* p, int b, std::vector<uint64_t>& bad, Fill fill)
 {
     const uint64_t unit = std::min(p->G * p->C, p->R);
     const uint64_t tile = 1ull << p->geo.tile_shift;
@@ -172,7 +180,7 @@ bool check_on_gpu(ckpt_peer* p, int b, std::vector<uint64_t>& bad)
         const uint64_t hi = std::min(lo + unit, p->R);
         const int slot = (int)(u & 1);
         uint8_t* stage = p->d_ring + slot * unit;
-        ok = hipStreamWaitEvent(p->s_copy, p->ev_free[slot], 0) == hipSuccess &&
+        ok = fill(lo, hi) && hipStreamWaitEvent(p->s_copy, p->ev_free[slot], 0) == hipSuccess &&
              hipMemcpyAsync(stage, p->h_buf[b] + lo, hi - lo, hipMemcpyHostToDevice, p->s_copy) == hipSuccess &&
              hipEventRecord(p->ev_loaded[slot], p->s_copy) == hipSuccess &&
              hipStreamWaitEvent(p->s_ker, p->ev_loaded[slot], 0) == hipSuccess;
@@ -184,23 +192,80 @@ bool check_on_gpu(ckpt_peer* p, int b, std::vector<uint64_t>& bad)
     }
     ok = ok && hipMemcpyAsync(p->h_bad, p->d_bad, p->n, hipMemcpyDeviceToHost, p->s_ker) == hipSuccess &&
          hipStreamSynchronize(p->s_ker) == hipSuccess;
-    if (!ok) return false;
+    if (!ok) {
+        (void)hipStreamSynchronize(p->s_copy);
+        (void)hipStreamSynchronize(p->s_ker);
+        return false;
+    }
     bad.clear();
     for (uint64_t j = 0; j < p->n; ++j)
         if (p->h_bad[j]) bad.push_back(p->ids[j]);
     return true;
 }
 
-// Wait until fd is readable or the peer is stopping.
-bool wait_readable(ckpt_peer* p, int fd)
+// Wait until the sender's fd or the listening socket is readable: 1 = the
+// sender, 2 = a new connection, 0 = stopping or a poll error.
+int wait_readable(ckpt_peer* p, int fd)
 {
     while (!p->stop.load()) {
-        pollfd q{fd, POLLIN, 0};
-        const int r = ::poll(&q, 1, 200);
-        if (r > 0) return true;
-        if (r < 0 && errno != EINTR) return false;
+        pollfd q[2] = {{fd, POLLIN, 0}, {p->lfd, POLLIN, 0}};
+        const int r = ::poll(q, 2, 200);
+        if (r > 0) return (q[0].revents & (POLLIN | POLLHUP | POLLERR)) ? 1 : 2;
+        if (r < 0 && errno != EINTR) return 0;
     }
-    return false;
+    return 0;
+}
+
+// Answer a replacement rank's fetch (its magic already read): the newest
+// committed replica in the sender's stream format.  Runs on the peer thread,
+// so no snapshot can be received into that buffer meanwhile.
+void serve_fetch(ckpt_peer* p, int fd)
+{
+    const auto deadline = std::chrono::steady_clock::now() + std::chrono::seconds(120);
+    WireFetch f;
+    if (recv_all(fd, reinterpret_cast<char*>(&f) + 8, sizeof f - 8, deadline)) return;
+    int b;
+    {
+        std::lock_guard<std::mutex> l(p->m);
+        b = p->committed;
+    }
+    WireAck a;
+    std::memcpy(a.magic, kAckMagic, 8);
+    a.snap_id = b >= 0 ? p->snap[b] : 0;
+    a.status = b >= 0 ? CKPT_OK : CKPT_ENOSNAP;
+    a.n_bad = 0;
+    a.reserved = 0;
+    if (send_all(fd, &a, sizeof a, deadline) || b < 0) return;
+    WireHead h;
+    std::memcpy(h.magic, kWireMagic, 8);
+    h.snap_id = p->snap[b];
+    h.step = p->step[b];
+    h.chunk_bytes = p->C;
+    h.image_bytes = p->I;
+    h.m = p->n;
+    h.replica_bytes = p->R;
+    h.env_len = p->env[b].size();
+    const bool sent = send_all(fd, &h, sizeof h, deadline) == 0 &&
+                      send_all(fd, p->ids.data(), 8 * p->n, deadline) == 0 &&
+                      send_all(fd, p->h_sums[b], 8 * p->n, deadline) == 0 &&
+                      send_all(fd, p->env[b].data(), p->env[b].size(), deadline) == 0 &&
+                      send_all(fd, p->h_buf[b], p->R, deadline) == 0;
+    if (!sent) set_err(p, "fetch of replica %llu: connection broke", (unsigned long long)h.snap_id);
+}
+
+// A connection accepted while a sender is being served: answer a fetch,
+// refuse a second sender.
+void side_connection(ckpt_peer* p)
+{
+    const int fd = ::accept(p->lfd, nullptr, nullptr);
+    if (fd < 0) return;
+    tune_socket(fd);
+    char magic[8];
+    if (recv_all(fd, magic, 8, std::chrono::steady_clock::now() + std::chrono::seconds(10)) == 0) {
+        if (std::memcmp(magic, kFetchMagic, 8) == 0) serve_fetch(p, fd);
+        else set_err(p, "refused a connection while a sender is connected");
+    }
+    ::close(fd);
 }
 
 void finish(ckpt_peer* p, uint64_t id, int32_t result)
@@ -211,16 +276,27 @@ void finish(ckpt_peer* p, uint64_t id, int32_t result)
     p->cv.notify_all();
 }
 
-// Handle one sender connection until it closes or breaks.
+// Handle one sender connection (the first snapshot's magic already read)
+// until it closes or breaks; between snapshots, answer fetches on other
+// connections.
 void serve(ckpt_peer* p, int fd)
 {
     using clock = std::chrono::steady_clock;
-    for (;;) {
-        if (!wait_readable(p, fd)) return;
+    for (bool first = true;; first = false) {
+        if (!first) {
+            const int w = wait_readable(p, fd);
+            if (w == 0) return;
+            if (w == 2) {
+                side_connection(p);
+                continue;
+            }
+        }
         const auto t0 = clock::now();
         const auto deadline = t0 + std::chrono::seconds(120);
         WireHead h;
-        if (recv_all(fd, &h, sizeof h, deadline)) return; // closed between snapshots
+        if (!first && recv_all(fd, h.magic, 8, deadline)) return; // closed between snapshots
+        if (first) std::memcpy(h.magic, kWireMagic, 8);
+        if (recv_all(fd, reinterpret_cast<char*>(&h) + 8, sizeof h - 8, deadline)) return;
         if (std::memcmp(h.magic, kWireMagic, 8) != 0 || h.m == 0 || h.m > (1ull << 32) || h.env_len > kMaxEnvelope) {
             set_err(p, "malformed replica header");
             return;
@@ -250,16 +326,27 @@ void serve(ckpt_peer* p, int fd)
         }
         std::vector<uint8_t> env(h.env_len);
         const bool got = recv_all(fd, p->h_sums[target], 8 * h.m, deadline) == 0 &&
-                         recv_all(fd, env.data(), h.env_len, deadline) == 0 &&
-                         recv_all(fd, p->h_buf[target], h.replica_bytes, deadline) == 0;
-        if (!got) { // stream broken mid-snapshot: nothing committed
+                         recv_all(fd, env.data(), h.env_len, deadline) == 0;
+        // The replica bytes arrive unit by unit, each checked on the GPU
+        // while the next one is received.
+        bool broke = !got;
+        auto t1 = t0;
+        auto fill = [&](uint64_t lo, uint64_t hi) {
+            if (recv_all(fd, p->h_buf[target] + lo, hi - lo, deadline)) {
+                broke = true;
+                return false;
+            }
+            if (hi == h.replica_bytes) t1 = clock::now();
+            return true;
+        };
+        std::vector<uint64_t> bad;
+        const bool checked = got && check_on_gpu(p, target, bad, fill);
+        if (broke) { // stream broken mid-snapshot: nothing committed
             set_err(p, "stream broke while receiving snapshot %llu", (unsigned long long)h.snap_id);
             finish(p, h.snap_id, CKPT_EHIP);
             return;
         }
-        const auto t1 = clock::now();
-        std::vector<uint64_t> bad;
-        if (!check_on_gpu(p, target, bad)) {
+        if (!checked) {
             set_err(p, "GPU check failed");
             finish(p, h.snap_id, CKPT_EHIP);
             return;
@@ -306,7 +393,12 @@ void peer_main(ckpt_peer* p)
             std::lock_guard<std::mutex> l(p->m);
             p->cfd = fd;
         }
-        serve(p, fd);
+        char magic[8];
+        if (recv_all(fd, magic, 8, std::chrono::steady_clock::now() + std::chrono::seconds(10)) == 0) {
+            if (std::memcmp(magic, kFetchMagic, 8) == 0) serve_fetch(p, fd);
+            else if (std::memcmp(magic, kWireMagic, 8) == 0) serve(p, fd);
+            else set_err(p, "unknown request on a new connection");
+        }
         {
             std::lock_guard<std::mutex> l(p->m);
             p->cfd = -1;

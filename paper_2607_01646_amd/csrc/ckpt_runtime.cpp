@@ -418,6 +418,44 @@ ckpt_status drain(ckpt_ctx* c)
 }
 
 // Resolve snap_id (0 = newest committed) to a committed, still-held record.
+ckpt_status pick_target_image(ckpt_ctx* c, int* out)
+{
+    // At most one uncommitted snapshot; find the newest live one.
+    int in_flight = 0;
+    SnapRec* newest_live = nullptr;
+    for (auto& kv : c->recs) {
+        SnapRec& r = kv.second;
+        if (r.aborted) continue;
+        if (!query_committed(r)) ++in_flight;
+        if (!newest_live || r.id > newest_live->id) newest_live = &r;
+    }
+    // One image always holds the newest committed snapshot and the other
+    // receives the one in flight (Sec. VI-A): a snapshot may start only once
+    // the previous one has committed.
+    if (in_flight >= 1) return fail(c, CKPT_EBUSY, "the previous snapshot has not committed yet");
+    // Target: the image not holding the newest live snapshot; with no live
+    // snapshot, an image that holds nothing committed.
+    int buf = 0;
+    if (newest_live) {
+        buf = 1 - newest_live->buf;
+    } else {
+        for (int b = 0; b < 2; ++b) {
+            auto it = c->recs.find(c->holder[b]);
+            if (c->holder[b] == 0 || it == c->recs.end() || it->second.aborted) {
+                buf = b;
+                break;
+            }
+        }
+    }
+    if (c->rep) {
+        std::lock_guard<std::mutex> l(c->rep->m);
+        if (c->rep->busy[buf])
+            return fail(c, CKPT_EBUSY, "the snapshot in host image %d is still being sent to the peer", buf);
+    }
+    *out = buf;
+    return CKPT_OK;
+}
+
 ckpt_status pick_committed(ckpt_ctx* c, uint64_t snap_id, SnapRec** out)
 {
     SnapRec* best = nullptr;
@@ -487,31 +525,34 @@ Lane verify_lane(ckpt_ctx* c)
                 &c->vloaded, &c->vk0, &c->vk1, c->ev_vdone, c->vt0, c->vc0, c->vc1};
 }
 
-// Restore (scatter=true) or verify (scatter=false) from a committed image.
-// Restore first waits for every outstanding snapshot (it rewrites the live
-// tensors and shares the snapshot staging).  Verify only reads a committed
-// image, which no in-flight snapshot targets, through its own staging ring
-// and streams, so it may run while a newer snapshot streams out: the host
-// link is full duplex.
-ckpt_status run_check(ckpt_ctx* c, uint64_t snap_id, hipStream_t stream, bool scatter, uint32_t* bad_chunks,
-                      uint32_t cap, uint32_t* n_bad)
+// Restore (scatter=true) or verify (scatter=false) the chunks of host image
+// b against the sums in h_sums[b]: every chunk, or only the chunks `ids`
+// (increasing) when given.  The caller has checked the arguments and, for a
+// restore, drained every snapshot.
+ckpt_status check_image(ckpt_ctx* c, int b, hipStream_t stream, bool scatter, const std::vector<uint64_t>* ids,
+                        uint32_t* bad_chunks, uint32_t cap, uint32_t* n_bad,
+                        const std::function<bool(uint64_t, uint64_t)>& fill)
 {
-    if (!c->registered) return fail(c, CKPT_ESTATE, "no tensors registered");
-    if (!n_bad || (cap && !bad_chunks)) return fail(c, CKPT_EINVAL, "null output pointer");
-    HIPCHK(c, hipSetDevice(c->device));
-    ckpt_status st = CKPT_OK;
-    if (scatter) {
-        st = drain(c);
-        if (st) return st;
-    }
-    SnapRec* r = nullptr;
-    st = pick_committed(c, snap_id, &r);
-    if (st) return st;
     const Lane L = scatter ? restore_lane(c) : verify_lane(c);
-    const int b = r->buf;
     const int op = scatter ? CKPT_OP_RESTORE : CKPT_OP_VERIFY;
-    const bool timed = c->timing;
     const uint64_t unit = L.G * c->C;
+    // Byte spans to move, each within one unit's size: whole units, or the
+    // runs of consecutive chunk ids cut at that size.
+    std::vector<std::pair<uint64_t, uint64_t>> spans;
+    if (!ids) {
+        for (uint64_t u = 0; u < L.n_units; ++u) spans.emplace_back(u * unit, std::min((u + 1) * unit, c->I));
+    } else {
+        for (size_t j = 0; j < ids->size();) {
+            size_t k = j + 1;
+            while (k < ids->size() && (*ids)[k] == (*ids)[k - 1] + 1 && k - j < L.G) ++k;
+            spans.emplace_back((*ids)[j] * c->C, std::min(((*ids)[k - 1] + 1) * c->C, c->I));
+            j = k;
+        }
+    }
+    const uint64_t n_spans = spans.size();
+    // Per-span events are reused round-robin past the unit count; timing is
+    // kept for whole-image operations only.
+    const bool timed = c->timing && !ids;
     unsigned long long* partials = c->d_partials + c->geo.n_tiles * kTileParts;
     HIPCHK(c, hipMemcpyAsync(c->d_expected, c->h_sums[b], c->n_chunks * 8, hipMemcpyHostToDevice, L.s_copy));
     if (scatter) {
@@ -519,12 +560,18 @@ ckpt_status run_check(ckpt_ctx* c, uint64_t snap_id, hipStream_t stream, bool sc
         HIPCHK(c, hipStreamWaitEvent(L.s_ker, c->ev_trigger, 0));
     }
     if (timed) HIPCHK(c, hipEventRecord(L.t0, L.s_copy));
-    for (uint64_t u = 0; u < L.n_units; ++u) {
-        const uint64_t lo = u * unit, hi = std::min(lo + unit, c->I);
-        const uint64_t area = L.ring ? u % L.n_slots : u;
+    for (uint64_t u = 0; u < n_spans; ++u) {
+        const uint64_t lo = spans[u].first, hi = spans[u].second;
+        const uint64_t ev = u % L.n_units;
+        const uint64_t area = L.ring ? u % L.n_slots : ev;
         uint8_t* stage = L.ring ? L.base + area * unit : L.base + lo;
         HIPCHK(c, hipStreamWaitEvent(L.s_copy, (*L.area_free)[area], 0));
         if (timed && u == 0) HIPCHK(c, hipEventRecord(L.c0, L.s_copy));
+        if (fill && !fill(lo, hi)) { // the span's bytes did not arrive: let the issued work finish, then fail
+            (void)hipStreamSynchronize(L.s_copy);
+            (void)hipStreamSynchronize(L.s_ker);
+            return CKPT_EHIP;
+        }
         const uint8_t* src = c->h_img[b] + lo;
         if (c->bounce) { // pageable image: through a pinned ring slot
             const uint64_t slot = u % c->n_bslots;
@@ -534,9 +581,9 @@ ckpt_status run_check(ckpt_ctx* c, uint64_t snap_id, hipStream_t stream, bool sc
         }
         HIPCHK(c, hipMemcpyAsync(stage, src, hi - lo, hipMemcpyHostToDevice, L.s_copy));
         if (c->bounce) HIPCHK(c, hipEventRecord(c->bin_done[u % c->n_bslots], L.s_copy));
-        if (timed && u + 1 == L.n_units) HIPCHK(c, hipEventRecord(L.c1, L.s_copy));
-        HIPCHK(c, hipEventRecord((*L.loaded)[u], L.s_copy));
-        HIPCHK(c, hipStreamWaitEvent(L.s_ker, (*L.loaded)[u], 0));
+        if (timed && u + 1 == n_spans) HIPCHK(c, hipEventRecord(L.c1, L.s_copy));
+        HIPCHK(c, hipEventRecord((*L.loaded)[ev], L.s_copy));
+        HIPCHK(c, hipStreamWaitEvent(L.s_ker, (*L.loaded)[ev], 0));
         const uint64_t t_lo = lo >> c->geo.tile_shift, t_hi = (hi + (1ull << c->geo.tile_shift) - 1) >> c->geo.tile_shift;
         hipEvent_t k0 = timed ? (*L.tk0)[u] : nullptr, k1 = timed ? (*L.tk1)[u] : nullptr;
         hipError_t e;
@@ -567,19 +614,47 @@ ckpt_status run_check(ckpt_ctx* c, uint64_t snap_id, hipStream_t stream, bool sc
         c->op_timing[op].t = t;
         c->op_timing[op].valid = true;
     }
-    c->last_sums.assign(c->h_recomputed, c->h_recomputed + c->n_chunks);
-    c->have_last_sums = true;
     uint32_t nb = 0;
-    for (uint64_t k = 0; k < c->n_chunks; ++k) {
-        if (c->h_bad[k]) {
-            if (nb < cap) bad_chunks[nb] = (uint32_t)k;
-            ++nb;
-        }
+    auto flag = [&](uint64_t k) {
+        if (!c->h_bad[k]) return;
+        if (nb < cap) bad_chunks[nb] = (uint32_t)k;
+        ++nb;
+    };
+    if (ids) {
+        for (uint64_t k : *ids) flag(k);
+    } else {
+        c->last_sums.assign(c->h_recomputed, c->h_recomputed + c->n_chunks);
+        c->have_last_sums = true;
+        for (uint64_t k = 0; k < c->n_chunks; ++k) flag(k);
     }
     *n_bad = nb;
     if (nb)
-        return fail(c, CKPT_ECORRUPT, "%u of %llu chunks failed their checksum", nb, (unsigned long long)c->n_chunks);
+        return fail(c, CKPT_ECORRUPT, "%u of %llu chunks failed their checksum", nb,
+                    (unsigned long long)(ids ? ids->size() : c->n_chunks));
     return CKPT_OK;
+}
+
+// Restore (scatter=true) or verify (scatter=false) from a committed image.
+// Restore first waits for every outstanding snapshot (it rewrites the live
+// tensors and shares the snapshot staging).  Verify only reads a committed
+// image, which no in-flight snapshot targets, through its own staging ring
+// and streams, so it may run while a newer snapshot streams out: the host
+// link is full duplex.
+ckpt_status run_check(ckpt_ctx* c, uint64_t snap_id, hipStream_t stream, bool scatter, uint32_t* bad_chunks,
+                      uint32_t cap, uint32_t* n_bad)
+{
+    if (!c->registered) return fail(c, CKPT_ESTATE, "no tensors registered");
+    if (!n_bad || (cap && !bad_chunks)) return fail(c, CKPT_EINVAL, "null output pointer");
+    HIPCHK(c, hipSetDevice(c->device));
+    ckpt_status st = CKPT_OK;
+    if (scatter) {
+        st = drain(c);
+        if (st) return st;
+    }
+    SnapRec* r = nullptr;
+    st = pick_committed(c, snap_id, &r);
+    if (st) return st;
+    return check_image(c, r->buf, stream, scatter, nullptr, bad_chunks, cap, n_bad);
 }
 
 void free_ctx(ckpt_ctx* c)
@@ -931,41 +1006,12 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
     if (meta_len > kMaxMeta) return fail(c, CKPT_EINVAL, "meta blob larger than 1 MiB");
     HIPCHK(c, hipSetDevice(c->device));
     prune(c);
-    // At most two uncommitted snapshots; find the newest live one.
-    int in_flight = 0;
-    SnapRec* newest_live = nullptr;
-    for (auto& kv : c->recs) {
-        SnapRec& r = kv.second;
-        if (r.aborted) continue;
-        if (!query_committed(r)) ++in_flight;
-        if (!newest_live || r.id > newest_live->id) newest_live = &r;
-    }
-    // One image always holds the newest committed snapshot and the other
-    // receives the one in flight (Sec. VI-A): a snapshot may start only once
-    // the previous one has committed.
-    if (in_flight >= 1) return fail(c, CKPT_EBUSY, "the previous snapshot has not committed yet");
-    // Target: the image not holding the newest live snapshot; with no live
-    // snapshot, an image that holds nothing committed.
     int buf = 0;
-    if (newest_live) {
-        buf = 1 - newest_live->buf;
-    } else {
-        for (int b = 0; b < 2; ++b) {
-            auto it = c->recs.find(c->holder[b]);
-            if (c->holder[b] == 0 || it == c->recs.end() || it->second.aborted) {
-                buf = b;
-                break;
-            }
-        }
-    }
-    if (c->rep) {
-        std::lock_guard<std::mutex> l(c->rep->m);
-        if (c->rep->busy[buf])
-            return fail(c, CKPT_EBUSY, "the snapshot in host image %d is still being sent to the peer", buf);
-    }
+    ckpt_status st = pick_target_image(c, &buf);
+    if (st) return st;
 
     RecRes* res = nullptr;
-    ckpt_status st = get_res(c, &res);
+    st = get_res(c, &res);
     if (st) return st;
     const uint64_t id = c->next_id++;
     SnapRec& r = c->recs[id];

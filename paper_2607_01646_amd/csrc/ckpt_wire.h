@@ -15,6 +15,17 @@
 // peer -> sender:
 //   WireAck                        (32 bytes)
 //   u64 bad_chunk_id[n_bad]        (sender's ids of chunks whose sum failed)
+//
+// A replacement rank fetching its predecessor's state (Sec. V-C, third
+// recovery stage) opens a connection of its own:
+// replacement -> peer:
+//   WireFetch                      (32 bytes)
+// peer -> replacement:
+//   WireAck                        (status CKPT_OK, or CKPT_ENOSNAP when the
+//                                   peer holds no committed replica; snap_id)
+//   then, with CKPT_OK, the newest committed replica in the per-snapshot
+//   format above (WireHead, ids, sums, envelope, data); the peer then
+//   closes the connection.
 #pragma once
 
 #include <arpa/inet.h>
@@ -34,6 +45,7 @@ namespace ckpt {
 
 constexpr char kWireMagic[8] = {'C', 'K', 'P', 'T', 'H', '2', 'H', '1'};
 constexpr char kAckMagic[8] = {'C', 'K', 'P', 'T', 'A', 'C', 'K', '1'};
+constexpr char kFetchMagic[8] = {'C', 'K', 'P', 'T', 'G', 'E', 'T', '1'};
 
 struct WireHead {
     char magic[8];
@@ -55,6 +67,12 @@ struct WireAck {
     uint64_t reserved;
 };
 static_assert(sizeof(WireAck) == 32, "wire ack is 32 bytes");
+
+struct WireFetch {
+    char magic[8];
+    uint64_t reserved[3];
+};
+static_assert(sizeof(WireFetch) == 32, "fetch request is 32 bytes");
 
 // Replica bytes of m chunks of chunk_bytes each, the last one possibly the
 // image's short last chunk.
@@ -121,6 +139,29 @@ inline void tune_socket(int fd)
     int buf = 16 << 20;
     (void)setsockopt(fd, SOL_SOCKET, SO_SNDBUF, &buf, sizeof buf);
     (void)setsockopt(fd, SOL_SOCKET, SO_RCVBUF, &buf, sizeof buf);
+}
+
+// Connect to a dotted IPv4 address.  Returns the socket, or -1 with errno
+// set (EINVAL for an address that does not parse).
+inline int dial(const char* host, uint32_t port)
+{
+    sockaddr_in a{};
+    a.sin_family = AF_INET;
+    a.sin_port = htons((uint16_t)port);
+    if (inet_pton(AF_INET, host, &a.sin_addr) != 1) {
+        errno = EINVAL;
+        return -1;
+    }
+    const int fd = ::socket(AF_INET, SOCK_STREAM, 0);
+    if (fd < 0) return -1;
+    tune_socket(fd);
+    if (::connect(fd, (sockaddr*)&a, sizeof a) != 0) {
+        const int e = errno;
+        ::close(fd);
+        errno = e;
+        return -1;
+    }
+    return fd;
 }
 
 } // namespace ckpt

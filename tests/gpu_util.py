@@ -58,3 +58,23 @@ def snapshot_and_check(tensors, host, chunk, align=256, staging=0, group=0, dtyp
         assert np.array_equal(host_bytes(t), h), "fragment %d not restored" % i
     assert np.array_equal(P.ckpt_last_sums(ck.ctx), want_sums)
     return ck, snap
+
+
+def class_major(tensors, plan):
+    """The same state registered class by class: parameters first, then master
+    weights and the two moments, so the optimizer classes fill a run of chunks."""
+    order = sorted(range(len(plan)), key=lambda i: (plan[i][3], i))
+    return [tensors[i] for i in order], [plan[i][2] for i in order], [plan[i][3] for i in order]
+
+
+def expected_replica(host, dtypes, classes, chunk, mask, step, meta=b""):
+    """From the oracle alone: the chunk ids holding a byte of a fragment of a
+    class in mask, their bytes, their sums, and the snapshot's envelope."""
+    sizes = [h.size for h in host]
+    img, off, nc = O.pack(host, 256, chunk)
+    I = img.size
+    ids = [c for c in range(nc) if any((mask >> classes[i]) & 1 for i in O.locate(c, chunk, I, off, sizes)[1])]
+    data = np.concatenate([img[c * chunk:min((c + 1) * chunk, I)] for c in ids])
+    sums = O.chunk_sums(img, 0, I, chunk)
+    env = O.envelope(step, 256, chunk, I, off, sizes, dtypes, classes, sums, meta)
+    return np.array(ids, dtype=np.uint64), data, sums[ids], env

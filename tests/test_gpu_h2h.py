@@ -13,9 +13,8 @@ import numpy as np
 import pytest
 import torch
 
-import oracle as O
 import workloads as W
-from gpu_util import host_bytes
+from gpu_util import class_major, expected_replica, host_bytes
 
 pytestmark = pytest.mark.gpu
 
@@ -23,24 +22,6 @@ if torch.cuda.is_available():
     import paper_2607_01646_amd as P
 
 OPT = (1 << W.CLS_MASTER) | (1 << W.CLS_ADAM_M) | (1 << W.CLS_ADAM_V)
-
-
-def class_major(tensors, plan):
-    """The same state registered class by class: parameters first, then master
-    weights and the two moments, so the optimizer classes fill a run of chunks."""
-    order = sorted(range(len(plan)), key=lambda i: (plan[i][3], i))
-    return [tensors[i] for i in order], [plan[i][2] for i in order], [plan[i][3] for i in order]
-
-
-def expected_replica(host, dtypes, classes, chunk, mask, step, meta=b""):
-    sizes = [h.size for h in host]
-    img, off, nc = O.pack(host, 256, chunk)
-    I = img.size
-    ids = [c for c in range(nc) if any((mask >> classes[i]) & 1 for i in O.locate(c, chunk, I, off, sizes)[1])]
-    data = np.concatenate([img[c * chunk:min((c + 1) * chunk, I)] for c in ids])
-    sums = O.chunk_sums(img, 0, I, chunk)
-    env = O.envelope(step, 256, chunk, I, off, sizes, dtypes, classes, sums, meta)
-    return np.array(ids, dtype=np.uint64), data, sums[ids], env
 
 
 def tiny_state():
