@@ -60,6 +60,8 @@ def parse():
                     help="run only the H2H replication leg (ring peer in this process, TCP over 127.0.0.1)")
     ap.add_argument("--h2h-workload", type=int, default=3)
     ap.add_argument("--h2h-steps", type=int, default=5)
+    ap.add_argument("--h2h-peers", type=int, default=1,
+                    help="replicate each snapshot to this many peers (k of Sec. V-C), all in this process")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-sample-bytes", type=int, default=10 << 30)
     ap.add_argument("--traffic", type=str, default=os.path.join(ROOT, "profiles", "pack_checksum_gpt1.3b_traffic.txt"),
@@ -486,11 +488,12 @@ def loopback_peak(nbytes=4 << 30, piece=256 << 20):
     return got / dt / 1e9
 
 
-def h2h_leg(torch, P, W, wid, steps):
+def h2h_leg(torch, P, W, wid, steps, n_peers=1, bounce_bytes=0, host_threads=0):
     """H2H replication (paper Sec. V-B): the optimizer-state chunks of each
-    snapshot go to a ring peer in this process over TCP on 127.0.0.1; the
-    peer re-checks every chunk sum on the GPU before it commits.  The state is
-    registered class-major so that the optimizer classes fill a run of chunks."""
+    snapshot go to n_peers ring peers (k of Sec. V-C) in this process over
+    TCP on 127.0.0.1; each peer re-checks every chunk sum on the GPU before it
+    commits.  The state is registered class-major so that the optimizer
+    classes fill a run of chunks."""
     tensors, plan = W.make_state(wid, device="cuda")
     order = sorted(range(len(plan)), key=lambda i: (plan[i][3], i))
     tensors = [tensors[i] for i in order]
@@ -499,9 +502,14 @@ def h2h_leg(torch, P, W, wid, steps):
     mask = (1 << W.CLS_MASTER) | (1 << W.CLS_ADAM_M) | (1 << W.CLS_ADAM_V)
     log("h2h: loopback peak")
     loop = loopback_peak()
-    peer = P.Peer()
-    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=W.WORKLOADS[wid]["chunk"])
-    ck.replicate_to(peer.port, mask)
+    peers = [P.Peer() for _ in range(n_peers)]
+    peer = peers[0]
+    # (pageable images behind bounce rings keep the pinned total under the
+    # host's limit when several peers hold pinned replicas)
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=W.WORKLOADS[wid]["chunk"], bounce_bytes=bounce_bytes,
+                        host_threads=host_threads)
+    for p in peers:
+        ck.replicate_to(p.port, mask)
     ids, rbytes = P.ckpt_replica_chunks(ck.ctx)
     rows = []
     for k in range(steps):
@@ -521,7 +529,8 @@ def h2h_leg(torch, P, W, wid, steps):
     for t in fresh:
         t.view(-1).view(torch.uint8).fill_(0x3C)
     torch.cuda.synchronize()
-    rk = P.Checkpointer(fresh, dtypes, classes, chunk_bytes=W.WORKLOADS[wid]["chunk"])
+    rk = P.Checkpointer(fresh, dtypes, classes, chunk_bytes=W.WORKLOADS[wid]["chunk"], bounce_bytes=bounce_bytes,
+                        host_threads=host_threads)
     rest = []
     for k in range(3):
         sid, step, bad = rk.restore_from_peer(peer.port)
@@ -537,7 +546,8 @@ def h2h_leg(torch, P, W, wid, steps):
                                                 tensors[i].view(-1).view(torch.uint8)):
             raise RuntimeError("peer restore: fragment %d differs from the lost rank's" % i)
     rk.close()
-    peer.close()
+    for p in peers:
+        p.close()
     del tensors, fresh
     torch.cuda.empty_cache()
     import statistics
@@ -547,11 +557,15 @@ def h2h_leg(torch, P, W, wid, steps):
     c_ms = statistics.median(r[1] for r in rest)
     t_ms = statistics.median(r[0] + r[1] for r in rest)
     return {"workload": W.WORKLOADS[wid]["name"], "classes": "master, Adam m, Adam v (params stay local)",
-            "image_bytes": image_bytes, "replica_bytes": int(rbytes), "replica_chunks": int(len(ids)),
+            "peers": n_peers, "host_images": "pageable + bounce" if bounce_bytes else "pinned",
+            "image_bytes": image_bytes, "replica_bytes": int(rbytes),
+            "replica_chunks": int(len(ids)),
             "snapshots": steps, "send_ms": round(med[0], 1), "ack_ms": round(med[1], 1),
             "peer_recv_ms": round(med[2], 1), "peer_check_after_last_byte_ms": round(med[3], 1),
-            "h2h_GBps": round(rbytes / med[0] / 1e6, 2), "h2h_with_check_GBps": round(rbytes / med[1] / 1e6, 2),
-            "loopback_peak_GBps": round(loop, 2), "statistic": "median over snapshots after the first",
+            "h2h_GBps": round(n_peers * rbytes / med[0] / 1e6, 2),
+            "h2h_with_check_GBps": round(n_peers * rbytes / med[1] / 1e6, 2),
+            "loopback_peak_GBps": round(loop, 2),
+            "statistic": "median over snapshots after the first; rates count the bytes sent to all peers",
             "replacement_restore": {"to_last_byte_ms": round(f_ms, 1), "after_last_byte_ms": round(c_ms, 1),
                                     "total_ms": round(t_ms, 1), "total_GBps": round(rbytes / t_ms / 1e6, 2),
                                     "runs": len(rest), "statistic": "median of the runs"}}
@@ -621,7 +635,8 @@ def main():
         return
     ratios = [float(r) for r in args.overlap_ratios.split(",") if r]
     if args.h2h_only:
-        print(json.dumps({"h2h": h2h_leg(torch, P, W, args.h2h_workload, args.h2h_steps)}), flush=True)
+        print(json.dumps({"h2h": h2h_leg(torch, P, W, args.h2h_workload, args.h2h_steps, args.h2h_peers,
+                                         args.bounce_bytes, args.host_threads)}), flush=True)
         return
     if args.overlap_only:
         log("link peak")

@@ -292,41 +292,60 @@ ckpt_status ckpt_image_file(ckpt_ctx* ctx, const char* path, uint32_t mode);
 /* The newest committed snapshot still held (0 if none) and its step. */
 ckpt_status ckpt_latest(ckpt_ctx* ctx, uint64_t* snap_id, uint64_t* step);
 
-/* ---- Host-to-host replication to a ring peer (Sec. V-B "Host-to-host";
- * Sec. VI-A: the wait before the optimizer step covers the peer replica) ----
+/* ---- Host-to-host replication to ring peers (Sec. V-B "Host-to-host";
+ * Sec. VI-A: the wait before the optimizer step covers the peer replica;
+ * Sec. V-C: k distinct peers tolerate k concurrent failures) ----
  *
  * ckpt_replicate_to: connect to a peer (ckpt_peer_*) listening at host:port
- * (dotted IPv4) and start the context's H2H worker.  From then on every
- * snapshot, once committed locally, is sent: the chunks holding a byte of a
+ * (dotted IPv4) and start a worker for it.  From then on every snapshot,
+ * once committed locally, is sent to it: the chunks holding a byte of a
  * fragment whose class tag k has bit k set in cls_mask (the optimizer-state
  * classes, in the paper), their stored sums and the snapshot's envelope.
  * The peer re-checks every chunk sum on its GPU, commits its own ping-pong
- * copy and answers.  ckpt_wait(CKPT_WAIT_REPLICATED) blocks until that
- * answer: OK, ECORRUPT (the peer found bad chunks; ckpt_replica_result lists
- * them; its previous replica stays), or EHIP (connection failed).  While a
+ * copy and answers.  Call it again (after registration, up to 8 times, with
+ * the same cls_mask, while no replication is in progress) to add further
+ * peers; each receives the snapshots issued after it was added, and the
+ * streams to the k peers run at the same time.
+ * ckpt_wait(CKPT_WAIT_REPLICATED) blocks until every peer has answered: OK
+ * when all committed the replica; ECORRUPT when a peer found bad chunks (that
+ * peer keeps its previous replica; ckpt_replica_result lists them); EHIP
+ * when a connection failed (the failure wins over corruption).  While a
  * snapshot's replica is being sent its host image is held: a snapshot that
- * would reuse it returns EBUSY.  Once per context, after registration.
- * Errors: EINVAL (bad address or mask selecting nothing), ESTATE, EHIP. */
+ * would reuse it returns EBUSY.
+ * Errors: EINVAL (bad address, mask selecting nothing, a mask other than
+ * the first peer's, more than 8 peers), ESTATE, EBUSY (adding a peer while
+ * a replication is in progress), EHIP. */
 ckpt_status ckpt_replicate_to(ckpt_ctx* ctx, const char* host, uint32_t port, uint64_t cls_mask);
 
 /* The replicated chunk ids (increasing; up to cap written) and their total
- * bytes.  Errors: ESTATE (no peer). */
+ * bytes (the same for every peer).  Errors: ESTATE (no peer). */
 ckpt_status ckpt_replica_chunks(ckpt_ctx* ctx, uint64_t* ids, uint64_t cap, uint64_t* n, uint64_t* replica_bytes);
 
-/* Non-blocking replication state of a snapshot: *state = 0 pending, 1 the
- * peer committed it, 2 the peer found corrupt chunks (their ids in bad, up to
- * cap; *n_bad the count), 3 failed (not sent, or no answer).
+/* Non-blocking replication state of a snapshot over all its peers: *state =
+ * 0 while any peer is pending, else 3 when any failed (not sent, or no
+ * answer), else 2 when any found corrupt chunks (the union of their ids in
+ * bad, up to cap; *n_bad the count), else 1 (every peer committed it).
  * Errors: ERANGE (not replicated: interrupted, or older than 64 snapshots). */
 ckpt_status ckpt_replica_result(ckpt_ctx* ctx, uint64_t snap_id, int32_t* state, uint64_t* bad, uint32_t cap,
                                 uint32_t* n_bad);
 
+/* The same for peer `peer` alone (0-based, in the order the peers were added).
+ * Errors: ESTATE (no such peer), ERANGE. */
+ckpt_status ckpt_replica_peer_result(ckpt_ctx* ctx, uint32_t peer, uint64_t snap_id, int32_t* state, uint64_t* bad,
+                                     uint32_t cap, uint32_t* n_bad);
+
+/* Number of replication peers. */
+ckpt_status ckpt_replica_peers(ckpt_ctx* ctx, uint32_t* n);
+
 /* Host wall time of the last replication, from the local commit being
- * observed: to the last byte sent, and to the peer's answer. */
+ * observed: to the last byte sent, and to the answer (the slowest peer). */
 ckpt_status ckpt_replica_timing(ckpt_ctx* ctx, double* send_ms, double* ack_ms);
 
 /* Fault injection for tests: kind 1 flips bit (b & 7) of replica byte a in
- * the next stream (the local image is untouched); kind 2 closes the
- * connection after a replica bytes of the next stream; 0 cancels. */
+ * the next stream to peer `peer` (the local image is untouched); kind 2
+ * closes that peer's connection after a replica bytes of its next stream;
+ * 0 cancels.  ckpt_debug_h2h_fault acts on the first peer. */
+ckpt_status ckpt_debug_h2h_fault_peer(ckpt_ctx* ctx, uint32_t peer, int32_t kind, uint64_t a, uint64_t b);
 ckpt_status ckpt_debug_h2h_fault(ckpt_ctx* ctx, int32_t kind, uint64_t a, uint64_t b);
 
 /* The receiving side: a ring peer holding its predecessor's replicas.  It

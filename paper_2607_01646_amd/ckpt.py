@@ -105,6 +105,9 @@ def lib():
             "ckpt_replica_result": ([vp, u64, P(i32), P(u64), u32, P(u32)], i32),
             "ckpt_replica_timing": ([vp, P(C.c_double), P(C.c_double)], i32),
             "ckpt_debug_h2h_fault": ([vp, i32, u64, u64], i32),
+            "ckpt_debug_h2h_fault_peer": ([vp, u32, i32, u64, u64], i32),
+            "ckpt_replica_peer_result": ([vp, u32, u64, P(i32), P(u64), u32, P(u32)], i32),
+            "ckpt_replica_peers": ([vp, P(u32)], i32),
             "ckpt_peer_create": ([P(ckpt_config), u32, P(vp)], i32),
             "ckpt_peer_port": ([vp, P(u32)], i32),
             "ckpt_peer_destroy": ([vp], i32),
@@ -359,6 +362,26 @@ def ckpt_replica_result(ctx, snap_id):
     return st.value, [int(x) for x in bad[:nb.value]]
 
 
+def ckpt_replica_peer_result(ctx, peer, snap_id):
+    """(state, [bad chunk ids]) of a snapshot's replication to one peer."""
+    st = C.c_int32()
+    nb = C.c_uint32()
+    _check(ctx, lib().ckpt_replica_peer_result(ctx, peer, snap_id, C.byref(st), None, 0, C.byref(nb)))
+    bad = np.zeros(max(nb.value, 1), dtype=np.uint64)
+    _check(ctx, lib().ckpt_replica_peer_result(ctx, peer, snap_id, C.byref(st), _u64p(bad), nb.value, C.byref(nb)))
+    return st.value, [int(x) for x in bad[:nb.value]]
+
+
+def ckpt_replica_peers(ctx):
+    n = C.c_uint32()
+    _check(ctx, lib().ckpt_replica_peers(ctx, C.byref(n)))
+    return n.value
+
+
+def ckpt_debug_h2h_fault_peer(ctx, peer, kind, a=0, b=0):
+    return _check(ctx, lib().ckpt_debug_h2h_fault_peer(ctx, peer, kind, a, b))
+
+
 def ckpt_replica_timing(ctx):
     a, b = C.c_double(), C.c_double()
     _check(ctx, lib().ckpt_replica_timing(ctx, C.byref(a), C.byref(b)))
@@ -538,6 +561,9 @@ class Checkpointer:
 
     def replica_result(self, snap):
         return ckpt_replica_result(self.ctx, snap)
+
+    def replica_peer_result(self, peer, snap):
+        return ckpt_replica_peer_result(self.ctx, peer, snap)
 
     def restore_from_peer(self, port, host="127.0.0.1", stream=None):
         """Take the failed rank's replicated chunks back from its ring peer:

@@ -1,16 +1,17 @@
-// ckpt_h2h.cpp -- host-to-host replication to a ring peer (paper Sec. V-B,
-// "Host-to-host"): the sending side.  After each local commit the context's
-// worker streams the selected classes' chunks, their stored sums and the
-// envelope to the peer (wire format in ckpt_wire.h) and waits for its
-// verdict; the receiving side is ckpt_peer.cpp.
+// ckpt_h2h.cpp -- host-to-host replication to ring peers (paper Sec. V-B,
+// "Host-to-host"; Sec. V-C, replication to k distinct peers against
+// concurrent failures): the sending side.  After each local commit, one
+// worker per peer streams the selected classes' chunks, their stored sums
+// and the envelope to its peer (wire format in ckpt_wire.h) and waits for
+// the verdict; the k streams run at once.  The receiving side is
+// ckpt_peer.cpp.
 #include "ckpt_host.h"
 
 namespace ckpt {
 
-// H2H worker thread (see Replicator).
-void rep_worker(ckpt_ctx* c)
+// H2H worker thread of one peer (see Replicator).
+void rep_worker(ckpt_ctx* c, Replicator* R)
 {
-    Replicator* R = c->rep;
     using clock = std::chrono::steady_clock;
     for (;;) {
         RepJob j;
@@ -130,18 +131,29 @@ void rep_worker(ckpt_ctx* c)
 
 void rep_stop(ckpt_ctx* c)
 {
-    Replicator* R = c->rep;
-    if (!R) return;
-    {
-        std::lock_guard<std::mutex> l(R->m);
-        R->stop = true;
+    for (Replicator* R : c->reps) {
+        {
+            std::lock_guard<std::mutex> l(R->m);
+            R->stop = true;
+        }
+        R->cv.notify_all();
+        if (R->fd >= 0) ::shutdown(R->fd, SHUT_RDWR);
     }
-    R->cv.notify_all();
-    if (R->fd >= 0) ::shutdown(R->fd, SHUT_RDWR);
-    if (R->worker.joinable()) R->worker.join();
-    if (R->fd >= 0) ::close(R->fd);
-    delete R;
-    c->rep = nullptr;
+    for (Replicator* R : c->reps) {
+        if (R->worker.joinable()) R->worker.join();
+        if (R->fd >= 0) ::close(R->fd);
+        delete R;
+    }
+    c->reps.clear();
+}
+
+bool rep_busy(ckpt_ctx* c, int b)
+{
+    for (Replicator* R : c->reps) {
+        std::lock_guard<std::mutex> l(R->m);
+        if (R->busy[b]) return true;
+    }
+    return false;
 }
 
 } // namespace ckpt
@@ -152,7 +164,16 @@ ckpt_status ckpt_replicate_to(ckpt_ctx* c, const char* host, uint32_t port, uint
 {
     if (!c || !host || port == 0 || port > 65535 || cls_mask == 0) return fail(c, CKPT_EINVAL, "bad replication target");
     if (!c->registered) return fail(c, CKPT_ESTATE, "no tensors registered");
-    if (c->rep) return fail(c, CKPT_ESTATE, "a replication peer is already set");
+    if (c->reps.size() >= kMaxPeers) return fail(c, CKPT_EINVAL, "at most %zu replication peers", kMaxPeers);
+    if (!c->reps.empty() && c->reps[0]->cls_mask != cls_mask)
+        return fail(c, CKPT_EINVAL, "every peer receives the same classes");
+    // Snapshots already issued are not sent to a peer added now: adding one
+    // while a snapshot is in flight or being sent would leave it behind.
+    for (Replicator* R : c->reps) {
+        std::lock_guard<std::mutex> l(R->m);
+        if (!R->q.empty() || R->busy[0] || R->busy[1])
+            return fail(c, CKPT_EBUSY, "a replication is in progress");
+    }
     // Chunks holding a byte of a fragment of a selected class.
     std::vector<uint8_t> pick(c->n_chunks, 0);
     for (const Frag& f : c->frags) {
@@ -173,29 +194,32 @@ ckpt_status ckpt_replicate_to(ckpt_ctx* c, const char* host, uint32_t port, uint
     R->cls_mask = cls_mask;
     R->ids = std::move(ids);
     R->bytes = replica_bytes(R->ids.data(), R->ids.size(), c->C, c->I);
-    c->rep = R;
-    R->worker = std::thread(rep_worker, c);
+    R->first_id = c->next_id;
+    c->reps.push_back(R);
+    R->worker = std::thread(rep_worker, c, R);
     return CKPT_OK;
 }
 
 ckpt_status ckpt_replica_chunks(ckpt_ctx* c, uint64_t* ids, uint64_t cap, uint64_t* n, uint64_t* replica_bytes_out)
 {
     if (!c || !n) return CKPT_EINVAL;
-    if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
-    *n = c->rep->ids.size();
-    if (replica_bytes_out) *replica_bytes_out = c->rep->bytes;
-    if (ids) std::memcpy(ids, c->rep->ids.data(), 8 * std::min<uint64_t>(cap, c->rep->ids.size()));
+    if (c->reps.empty()) return fail(c, CKPT_ESTATE, "no replication peer");
+    const Replicator* R = c->reps[0]; // every peer receives the same chunks
+    *n = R->ids.size();
+    if (replica_bytes_out) *replica_bytes_out = R->bytes;
+    if (ids) std::memcpy(ids, R->ids.data(), 8 * std::min<uint64_t>(cap, R->ids.size()));
     return CKPT_OK;
 }
 
-ckpt_status ckpt_replica_result(ckpt_ctx* c, uint64_t snap_id, int32_t* state, uint64_t* bad, uint32_t cap,
-                                uint32_t* n_bad)
+ckpt_status ckpt_replica_peer_result(ckpt_ctx* c, uint32_t peer, uint64_t snap_id, int32_t* state, uint64_t* bad,
+                                     uint32_t cap, uint32_t* n_bad)
 {
     if (!c || !state) return CKPT_EINVAL;
-    if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
-    std::lock_guard<std::mutex> l(c->rep->m);
-    auto s = c->rep->status.find(snap_id);
-    if (s == c->rep->status.end())
+    if (peer >= c->reps.size()) return fail(c, CKPT_ESTATE, "no replication peer %u", peer);
+    Replicator* R = c->reps[peer];
+    std::lock_guard<std::mutex> l(R->m);
+    auto s = R->status.find(snap_id);
+    if (s == R->status.end())
         return fail(c, CKPT_ERANGE, "snapshot %llu is not being replicated", (unsigned long long)snap_id);
     *state = s->second.state;
     if (n_bad) *n_bad = (uint32_t)s->second.bad.size();
@@ -203,25 +227,68 @@ ckpt_status ckpt_replica_result(ckpt_ctx* c, uint64_t snap_id, int32_t* state, u
     return CKPT_OK;
 }
 
+ckpt_status ckpt_replica_result(ckpt_ctx* c, uint64_t snap_id, int32_t* state, uint64_t* bad, uint32_t cap,
+                                uint32_t* n_bad)
+{
+    if (!c || !state) return CKPT_EINVAL;
+    if (c->reps.empty()) return fail(c, CKPT_ESTATE, "no replication peer");
+    // Pending while any peer is; then failed, corrupt (the union of the bad
+    // chunks) or OK.
+    bool pending = false, failed = false;
+    std::vector<uint64_t> all;
+    for (Replicator* R : c->reps) {
+        if (snap_id < R->first_id && R != c->reps[0]) continue; // added after this snapshot
+        std::lock_guard<std::mutex> l(R->m);
+        auto s = R->status.find(snap_id);
+        if (s == R->status.end())
+            return fail(c, CKPT_ERANGE, "snapshot %llu is not being replicated", (unsigned long long)snap_id);
+        pending |= s->second.state == REP_PENDING;
+        failed |= s->second.state == REP_FAILED;
+        all.insert(all.end(), s->second.bad.begin(), s->second.bad.end());
+    }
+    std::sort(all.begin(), all.end());
+    all.erase(std::unique(all.begin(), all.end()), all.end());
+    *state = pending ? REP_PENDING : failed ? REP_FAILED : all.empty() ? REP_OK : REP_CORRUPT;
+    if (n_bad) *n_bad = (uint32_t)all.size();
+    if (bad) std::memcpy(bad, all.data(), 8 * std::min<uint64_t>(cap, all.size()));
+    return CKPT_OK;
+}
+
 ckpt_status ckpt_replica_timing(ckpt_ctx* c, double* send_ms, double* ack_ms)
 {
     if (!c || !send_ms || !ack_ms) return CKPT_EINVAL;
-    if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
-    std::lock_guard<std::mutex> l(c->rep->m);
-    *send_ms = c->rep->last_send_ms;
-    *ack_ms = c->rep->last_ack_ms;
+    if (c->reps.empty()) return fail(c, CKPT_ESTATE, "no replication peer");
+    *send_ms = *ack_ms = 0;
+    for (Replicator* R : c->reps) { // the slowest peer's
+        std::lock_guard<std::mutex> l(R->m);
+        *send_ms = std::max(*send_ms, R->last_send_ms);
+        *ack_ms = std::max(*ack_ms, R->last_ack_ms);
+    }
+    return CKPT_OK;
+}
+
+ckpt_status ckpt_debug_h2h_fault_peer(ckpt_ctx* c, uint32_t peer, int32_t kind, uint64_t a, uint64_t b)
+{
+    if (!c || kind < 0 || kind > 2) return CKPT_EINVAL;
+    if (peer >= c->reps.size()) return fail(c, CKPT_ESTATE, "no replication peer %u", peer);
+    Replicator* R = c->reps[peer];
+    std::lock_guard<std::mutex> l(R->m);
+    if (kind && a >= R->bytes) return fail(c, CKPT_EINVAL, "fault position beyond the replica");
+    R->fault_kind = kind;
+    R->fault_a = a;
+    R->fault_b = b;
     return CKPT_OK;
 }
 
 ckpt_status ckpt_debug_h2h_fault(ckpt_ctx* c, int32_t kind, uint64_t a, uint64_t b)
 {
-    if (!c || kind < 0 || kind > 2) return CKPT_EINVAL;
-    if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
-    std::lock_guard<std::mutex> l(c->rep->m);
-    if (kind && a >= c->rep->bytes) return fail(c, CKPT_EINVAL, "fault position beyond the replica");
-    c->rep->fault_kind = kind;
-    c->rep->fault_a = a;
-    c->rep->fault_b = b;
+    return ckpt_debug_h2h_fault_peer(c, 0, kind, a, b);
+}
+
+ckpt_status ckpt_replica_peers(ckpt_ctx* c, uint32_t* n)
+{
+    if (!c || !n) return CKPT_EINVAL;
+    *n = (uint32_t)c->reps.size();
     return CKPT_OK;
 }
 

@@ -257,6 +257,7 @@ struct RepStatus {
 
 struct Replicator {
     int fd = -1;
+    uint64_t first_id = 0; // the first snapshot this peer receives (peers may be added later)
     uint64_t cls_mask = 0;
     std::vector<uint64_t> ids; // replicated chunks, increasing
     uint64_t bytes = 0;        // replica bytes per snapshot
@@ -362,8 +363,8 @@ struct ckpt_ctx {
     CopyPool* pool = nullptr;
     Pump* pump = nullptr;
 
-    // H2H replication to a ring peer
-    Replicator* rep = nullptr;
+    // H2H replication to ring peers (k distinct peers, in the order they were added)
+    std::vector<Replicator*> reps;
 
     // the last restore from a ring peer's replica
     PeerRestore peer_restore;
@@ -442,7 +443,10 @@ ckpt_status adopt_image_file(ckpt_ctx* c);
 void file_invalidate(ckpt_ctx* c, int b);
 void file_commit(ckpt_ctx* c, const PumpItem& it);
 
-// Replication to a ring peer (ckpt_h2h.cpp)
+// Replication to ring peers (ckpt_h2h.cpp)
+constexpr size_t kMaxPeers = 8;
 void rep_stop(ckpt_ctx* c);
+// Whether a replication still reads host image b.
+bool rep_busy(ckpt_ctx* c, int b);
 
 } // namespace ckpt

@@ -447,11 +447,8 @@ ckpt_status pick_target_image(ckpt_ctx* c, int* out)
             }
         }
     }
-    if (c->rep) {
-        std::lock_guard<std::mutex> l(c->rep->m);
-        if (c->rep->busy[buf])
-            return fail(c, CKPT_EBUSY, "the snapshot in host image %d is still being sent to the peer", buf);
-    }
+    if (rep_busy(c, buf))
+        return fail(c, CKPT_EBUSY, "the snapshot in host image %d is still being sent to a peer", buf);
     *out = buf;
     return CKPT_OK;
 }
@@ -1046,7 +1043,8 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
         *snap_id = id;
         return st;
     }
-    if (c->rep && !r.aborted) { // H2H once the offload commits
+    for (Replicator* R : c->reps) { // H2H once the offload commits, to every peer
+        if (r.aborted) break;
         RepJob j;
         j.id = id;
         j.step = step;
@@ -1055,14 +1053,14 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
         j.groups_copied = r.groups_copied;
         j.bounce = r.bounce;
         j.meta = r.meta;
-        std::lock_guard<std::mutex> l(c->rep->m);
-        c->rep->busy[r.buf] = true;
-        while (!c->rep->status.empty() && c->rep->status.begin()->first + 64 < id &&
-               c->rep->status.begin()->second.state != REP_PENDING)
-            c->rep->status.erase(c->rep->status.begin());
-        c->rep->status[id] = RepStatus{};
-        c->rep->q.push_back(std::move(j));
-        c->rep->cv.notify_all();
+        std::lock_guard<std::mutex> l(R->m);
+        R->busy[r.buf] = true;
+        while (!R->status.empty() && R->status.begin()->first + 64 < id &&
+               R->status.begin()->second.state != REP_PENDING)
+            R->status.erase(R->status.begin());
+        R->status[id] = RepStatus{};
+        R->q.push_back(std::move(j));
+        R->cv.notify_all();
     }
     *snap_id = id;
     return CKPT_OK;
@@ -1196,20 +1194,34 @@ ckpt_status ckpt_wait(ckpt_ctx* c, uint64_t snap_id, uint32_t mode, void* stream
 {
     if (!c) return CKPT_EINVAL;
     if (mode == CKPT_WAIT_REPLICATED) {
-        if (!c->rep) return fail(c, CKPT_ESTATE, "no replication peer");
-        Replicator* R = c->rep;
-        std::unique_lock<std::mutex> l(R->m);
-        auto s = R->status.find(snap_id);
-        if (s == R->status.end())
-            return fail(c, CKPT_ERANGE, "snapshot %llu is not being replicated", (unsigned long long)snap_id);
-        if (!R->cv.wait_for(l, std::chrono::seconds(240), [&] { return s->second.state != REP_PENDING; }))
-            return fail(c, CKPT_EHIP, "snapshot %llu: no answer from the peer after 240 s", (unsigned long long)snap_id);
-        if (s->second.state == REP_OK) return CKPT_OK;
-        if (s->second.state == REP_CORRUPT)
-            return fail(c, CKPT_ECORRUPT, "the peer found %zu corrupt chunks in snapshot %llu", s->second.bad.size(),
-                        (unsigned long long)snap_id);
-        return fail(c, CKPT_EHIP, "snapshot %llu not replicated: %s", (unsigned long long)snap_id,
-                    s->second.err.c_str());
+        if (c->reps.empty()) return fail(c, CKPT_ESTATE, "no replication peer");
+        // Every peer's answer; the worst one decides (failed, then corrupt).
+        const auto deadline = std::chrono::steady_clock::now() + std::chrono::seconds(240);
+        ckpt_status worst = CKPT_OK;
+        std::string why;
+        for (size_t k = 0; k < c->reps.size(); ++k) {
+            Replicator* R = c->reps[k];
+            if (k && snap_id < R->first_id) continue; // this peer was added after the snapshot
+            std::unique_lock<std::mutex> l(R->m);
+            auto s = R->status.find(snap_id);
+            if (s == R->status.end())
+                return fail(c, CKPT_ERANGE, "snapshot %llu is not being replicated", (unsigned long long)snap_id);
+            if (!R->cv.wait_until(l, deadline, [&] { return s->second.state != REP_PENDING; }))
+                return fail(c, CKPT_EHIP, "snapshot %llu: no answer from peer %zu after 240 s",
+                            (unsigned long long)snap_id, k);
+            if (s->second.state == REP_FAILED) {
+                worst = CKPT_EHIP;
+                why = "peer " + std::to_string(k) + ": " + s->second.err;
+            } else if (s->second.state == REP_CORRUPT && worst == CKPT_OK) {
+                worst = CKPT_ECORRUPT;
+                why = "peer " + std::to_string(k) + " found " + std::to_string(s->second.bad.size()) +
+                      " corrupt chunks";
+            }
+        }
+        if (worst == CKPT_OK) return CKPT_OK;
+        if (worst == CKPT_ECORRUPT)
+            return fail(c, CKPT_ECORRUPT, "snapshot %llu: %s", (unsigned long long)snap_id, why.c_str());
+        return fail(c, CKPT_EHIP, "snapshot %llu not replicated: %s", (unsigned long long)snap_id, why.c_str());
     }
     auto it = c->recs.find(snap_id);
     if (it == c->recs.end()) return fail(c, CKPT_ERANGE, "snapshot %llu not retained", (unsigned long long)snap_id);

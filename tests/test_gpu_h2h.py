@@ -220,3 +220,95 @@ def test_replication_errors():
         ck.replicate_to(1, OPT)  # nothing listens on port 1
     assert e.value.code == P.CKPT_EHIP
     ck.close()
+
+
+def test_two_peers_hold_the_same_replica_and_fail_separately():
+    """k = 2 (Sec. V-C): both peers commit the oracle's replica; a bit flipped
+    on the way to the first peer only is reported by that peer, the second
+    commits, and the combined result lists the chunk."""
+    tensors, dtypes, classes = tiny_state()
+    chunk = 1 << 20
+    peers = [P.Peer(), P.Peer()]
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=chunk)
+    for p in peers:
+        ck.replicate_to(p.port, OPT)
+    assert P.ckpt_replica_peers(ck.ctx) == 2
+    host1 = [host_bytes(t) for t in tensors]
+    s1 = ck.snapshot(step=4, meta=b"k2")
+    ck.wait_replicated(s1)
+    want1 = expected_replica(host1, dtypes, classes, chunk, OPT, 4, b"k2")
+    for k, p in enumerate(peers):
+        r = p.replica()
+        assert r["snap_id"] == s1 and np.array_equal(r["data"], want1[1]) and r["envelope"] == want1[3]
+        assert np.array_equal(r["sums"], want1[2])
+        assert ck.replica_peer_result(k, s1) == (P.REPLICA_OK, [])
+    for t in tensors:
+        t.mul_(3)
+    host2 = [host_bytes(t) for t in tensors]
+    ids = want1[0]
+    P.ckpt_debug_h2h_fault_peer(ck.ctx, 0, 1, 5 * chunk + 99, 2)
+    s2 = ck.snapshot(step=5)
+    with pytest.raises(P.CkptError) as e:
+        ck.wait_replicated(s2)
+    assert e.value.code == P.CKPT_ECORRUPT
+    assert ck.replica_peer_result(0, s2) == (P.REPLICA_CORRUPT, [int(ids[5])])
+    assert ck.replica_peer_result(1, s2) == (P.REPLICA_OK, [])
+    assert ck.replica_result(s2) == (P.REPLICA_CORRUPT, [int(ids[5])])
+    assert peers[0].replica()["snap_id"] == s1  # kept its previous replica
+    r = peers[1].replica()
+    assert r["snap_id"] == s2 and np.array_equal(r["data"], expected_replica(host2, dtypes, classes, chunk, OPT, 5)[1])
+    ck.close()
+    for p in peers:
+        p.close()
+
+
+def test_peer_added_later_gets_the_following_snapshots():
+    tensors, dtypes, classes = tiny_state()
+    chunk = 1 << 20
+    a, b = P.Peer(), P.Peer()
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=chunk)
+    ck.replicate_to(a.port, OPT)
+    s1 = ck.snapshot(step=1)
+    ck.wait_replicated(s1)
+    ck.replicate_to(b.port, OPT)
+    with pytest.raises(P.PeerError):
+        b.replica()  # nothing yet
+    host2 = [host_bytes(t) for t in tensors]
+    s2 = ck.snapshot(step=2)
+    ck.wait_replicated(s2)
+    ck.wait_replicated(s1)  # s1 went to the first peer only, and still counts as replicated
+    assert ck.replica_result(s1) == (P.REPLICA_OK, [])
+    want = expected_replica(host2, dtypes, classes, chunk, OPT, 2)
+    for p in (a, b):
+        assert p.replica()["snap_id"] == s2 and np.array_equal(p.replica()["data"], want[1])
+    with pytest.raises(P.CkptError) as e:
+        ck.replica_peer_result(1, s1)
+    assert e.value.code == P.CKPT_ERANGE
+    ck.close()
+    a.close()
+    b.close()
+
+
+def test_peer_list_errors():
+    tensors, dtypes, classes = tiny_state()
+    peers = [P.Peer() for _ in range(9)]
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=1 << 20)
+    ck.replicate_to(peers[0].port, OPT)
+    with pytest.raises(P.CkptError) as e:
+        ck.replicate_to(peers[1].port, 1 << W.CLS_MASTER)  # another class mask
+    assert e.value.code == P.CKPT_EINVAL
+    for p in peers[1:8]:
+        ck.replicate_to(p.port, OPT)
+    assert P.ckpt_replica_peers(ck.ctx) == 8
+    with pytest.raises(P.CkptError) as e:
+        ck.replicate_to(peers[8].port, OPT)  # a ninth
+    assert e.value.code == P.CKPT_EINVAL
+    with pytest.raises(P.CkptError) as e:
+        ck.replica_peer_result(8, 1)
+    assert e.value.code == P.CKPT_ESTATE
+    s = ck.snapshot(step=1)
+    ck.wait_replicated(s)
+    assert all(p.wait(s) == P.CKPT_OK for p in peers[:8])
+    ck.close()
+    for p in peers:
+        p.close()

@@ -381,3 +381,30 @@ def test_malformed_replies_are_refused_before_anything_is_written():
     th.join(timeout=30)
     assert_tensors(fresh, expected_after(host, before, classes, ids))
     b.close()
+
+
+def test_owner_and_one_replica_holder_lost_the_other_serves():
+    """k = 2: the owner and its first replica holder fail in the same step;
+    the replacement restores from the second holder."""
+    tensors, dtypes, classes = state()
+    peers = [P.Peer(), P.Peer()]
+    a = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=CHUNK)
+    for p in peers:
+        a.replicate_to(p.port, OPT)
+    failed_host = [host_bytes(t) for t in tensors]
+    s = a.snapshot(step=13, meta=b"two")
+    a.wait_replicated(s)
+    fresh = replacement_like(tensors)
+    a.close()
+    peers[0].close()  # the first holder is gone too
+    before = [host_bytes(t) for t in fresh]
+    b = P.Checkpointer(fresh, dtypes, classes, chunk_bytes=CHUNK)
+    with pytest.raises(P.CkptError) as e:
+        b.restore_from_peer(peers[0].port)  # nobody listens there any more
+    assert e.value.code == P.CKPT_EHIP
+    assert b.restore_from_peer(peers[1].port) == (s, 13, [])
+    ids, _, _, env = expected_replica(failed_host, dtypes, classes, CHUNK, OPT, 13, b"two")
+    assert_tensors(fresh, expected_after(failed_host, before, classes, ids))
+    assert b.peer_restore_info()["envelope"] == env
+    b.close()
+    peers[1].close()
