@@ -63,7 +63,7 @@ def test_plan_matches_oracle_layout(P):
 def test_plan_workload_sizes(P):
     import workloads as W
 
-    for wid in [1, 2, 3, 5]:
+    for wid in [1, 2, 3, 5, 6]:
         plan = W.fragment_plan(wid)
         sizes = [p[1] for p in plan]
         C = W.WORKLOADS[wid]["chunk"]

@@ -95,6 +95,16 @@ def test_llama65b_tp8pp8_rank_shard():
     ck.close()
 
 
+def test_llama65b_rank_shard_in_full_precision():
+    """The same rank with every tensor in fp32, the paper's training setting:
+    360 fragments, 16.19 GB (16 bytes per parameter)."""
+    ck, tensors, plan, _ = check_shard(6)
+    assert ck.n_chunks == 242 and sum(p[1] for p in plan) == 16_192_634_880
+    assert all(p[2] == W.DT_FP32 for p in plan)
+    assert torch.equal(tensors[0], tensors[1])  # the parameter equals its master copy
+    ck.close()
+
+
 def test_stress_4096_fragments_with_flips():
     """4096 fragments (8 GiB, bf16/fp32 alternating, 1 KiB .. ~21 MiB) with 32
     seeded single-bit flips in distinct chunks: all reported and located."""

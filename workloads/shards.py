@@ -8,12 +8,14 @@ Values: master ~ N(0, 0.02^2), parameter = bf16(master) (round to nearest
 even), m ~ N(0, 1e-3^2), v = (N(0, 1e-3^2))^2; every fragment draws from its
 own generator seeded from (1000 + workload id, fragment index).
 
-Workloads (ids 1-5):
+Workloads (ids 1-6):
   1  4-layer GPT, hidden 512, FFN 2048, vocab 8192, 512 positions (17.07M params), 4 MiB chunks
   2  24-layer GPT, hidden 2048, FFN 8192, vocab 50304, 2048 positions (1.316B params), 64 MiB chunks
   3  one rank of a 65B LLaMA under TP=8 x PP=8: 10 layers, hidden 8192, FFN 22016/8 (1.012B params)
   4  7B LLaMA: 32 layers, hidden 4096, FFN 11008, vocab 32000 (6.738B params)
   5  4096 fragments, log-uniform sizes rescaled to 8 GiB in total, bf16/fp32 alternating
+  6  workload 3 in full precision, the paper's training setting (Sec. VII): the parameter is fp32 too
+     (equal to its master copy), 16 bytes per parameter
 """
 import math
 
@@ -40,10 +42,12 @@ WORKLOADS = {
             embed=True, head=True, chunk=64 * MiB),
     5: dict(name="stress-4096-frag-8GiB", kind="stress", n=4096, total=8 * GiB, lo=1024, hi=64 * MiB,
             chunk=64 * MiB),
+    6: dict(name="llama65B-tp8pp8-rank-10L-h8192-fp32", kind="llama", layers=10, hidden=8192, ffn=22016,
+            vocab=32000, tp=8, embed=False, head=False, chunk=64 * MiB, fp32=True),
 }
 
 # bf16 GEMM that stands in for forward/backward compute in the overlap runs
-OVERLAP_GEMM = {3: (8192, 8192, 2752), 4: (8192, 4096, 11008)}
+OVERLAP_GEMM = {3: (8192, 8192, 2752), 4: (8192, 4096, 11008), 6: (8192, 8192, 2752)}
 
 
 def gpt_param_shapes(layers, hidden, ffn, vocab, seq):
@@ -127,11 +131,12 @@ def fragment_plan(wid):
         return [("frag%d" % i, s, dt, CLS_MASTER if dt == DT_FP32 else CLS_PARAM)
                 for i, (s, dt) in enumerate(zip(sizes, dts))]
     plan = []
+    fp32 = WORKLOADS[wid].get("fp32", False)
     for name, shape in param_shapes(wid):
         numel = math.prod(shape)
         for cls, suffix in [(CLS_PARAM, ""), (CLS_MASTER, ".master"), (CLS_ADAM_M, ".exp_avg"),
                             (CLS_ADAM_V, ".exp_avg_sq")]:
-            dt = CLASS_DTYPE[cls]
+            dt = DT_FP32 if fp32 else CLASS_DTYPE[cls]
             plan.append((name + suffix, numel * ELEM_BYTES[dt], dt, cls))
     return plan
 
@@ -161,10 +166,10 @@ def make_state(wid, device="cuda"):
             out.append(t)
         return out, plan
     for i in range(0, len(plan), 4):
-        numel = plan[i][1] // 2
+        numel = plan[i][1] // ELEM_BYTES[plan[i][2]]
         g = torch.Generator(device=device).manual_seed(fragment_seed(wid, i))
         master = torch.randn(numel, generator=g, device=device) * 0.02
-        param = master.to(torch.bfloat16)
+        param = master.clone() if plan[i][2] == DT_FP32 else master.to(torch.bfloat16)
         g = torch.Generator(device=device).manual_seed(fragment_seed(wid, i + 2))
         m = torch.randn(numel, generator=g, device=device) * 1e-3
         g = torch.Generator(device=device).manual_seed(fragment_seed(wid, i + 3))
