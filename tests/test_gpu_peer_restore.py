@@ -64,8 +64,8 @@ def assert_tensors(tensors, want):
         assert np.array_equal(host_bytes(t), w), "fragment %d differs" % i
 
 
-@pytest.mark.parametrize("bounce", [0, 2 << 20])
-def test_replacement_takes_the_optimizer_state_back(bounce):
+@pytest.mark.parametrize("bounce, staging", [(0, 0), (2 << 20, 0), (0, 3 << 20)])
+def test_replacement_takes_the_optimizer_state_back(bounce, staging):
     """Rank A replicates snapshot (step 7) to the peer and is lost; replacement
     B, registered with A's layout, restores from the peer: the optimizer
     fragments equal A's at step 7, parameter-only fragments keep B's bytes."""
@@ -82,7 +82,8 @@ def test_replacement_takes_the_optimizer_state_back(bounce):
     ids, _, _, env = expected_replica(failed_host, dtypes, classes, CHUNK, OPT, 7, b"rng")
 
     before = [host_bytes(t) for t in fresh]
-    b = P.Checkpointer(fresh, dtypes, classes, chunk_bytes=CHUNK, group_bytes=CHUNK, bounce_bytes=bounce)
+    b = P.Checkpointer(fresh, dtypes, classes, chunk_bytes=CHUNK, group_bytes=CHUNK, bounce_bytes=bounce,
+                       device_staging_bytes=staging)
     sid, step, bad = b.restore_from_peer(peer.port)
     assert (sid, step, bad) == (s, 7, [])
     assert_tensors(fresh, expected_after(failed_host, before, classes, ids))
