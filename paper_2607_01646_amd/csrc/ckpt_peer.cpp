@@ -52,7 +52,8 @@ struct ckpt_peer {
 
     std::mutex m; // guards everything below that the API reads
     std::condition_variable cv;
-    int cfd = -1;
+    int cfd = -1; // the connection being served
+    int sfd = -1; // a fetch answered beside a connected sender
 
     // geometry, fixed by the first snapshot received
     bool ready = false;
@@ -260,10 +261,18 @@ void side_connection(ckpt_peer* p)
     const int fd = ::accept(p->lfd, nullptr, nullptr);
     if (fd < 0) return;
     tune_socket(fd);
+    {
+        std::lock_guard<std::mutex> l(p->m);
+        p->sfd = fd;
+    }
     char magic[8];
     if (recv_all(fd, magic, 8, std::chrono::steady_clock::now() + std::chrono::seconds(10)) == 0) {
         if (std::memcmp(magic, kFetchMagic, 8) == 0) serve_fetch(p, fd);
         else set_err(p, "refused a connection while a sender is connected");
+    }
+    {
+        std::lock_guard<std::mutex> l(p->m);
+        p->sfd = -1;
     }
     ::close(fd);
 }
@@ -458,6 +467,7 @@ ckpt_status ckpt_peer_destroy(ckpt_peer* p)
     {
         std::lock_guard<std::mutex> l(p->m);
         if (p->cfd >= 0) ::shutdown(p->cfd, SHUT_RDWR);
+        if (p->sfd >= 0) ::shutdown(p->sfd, SHUT_RDWR);
     }
     if (p->th.joinable()) p->th.join();
     ::close(p->lfd);
