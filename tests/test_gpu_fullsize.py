@@ -128,3 +128,45 @@ def test_stress_4096_fragments_with_flips():
         (olo, ohi), ids = O.locate(c, chunk, ck.image_bytes, ck.offsets, sizes)
         assert (lo, hi) == (olo, ohi) and ids and f0 <= min(ids) and max(ids) <= f1
     ck.close()
+
+
+@pytest.mark.parametrize("shift", [0, 3])
+def test_fragment_beyond_4_gib(shift):
+    """One 4.5 GiB fragment (16-byte aligned, or a view 3 bytes into its
+    buffer) between two small ones: image offsets, tile offsets and the
+    funnel-shifted reads all pass 2^32 bytes within the fragment."""
+    n = (9 << 29) + 5  # 4.5 GiB + 5 bytes
+    flat = torch.empty(n + 16, dtype=torch.uint8, device="cuda")
+    g = torch.Generator(device="cuda").manual_seed(4242)
+    flat.copy_(torch.randint(0, 256, (n + 16,), generator=g, device="cuda", dtype=torch.uint8))
+    small_a = torch.arange(777, dtype=torch.int32, device="cuda")
+    small_b = torch.full((1001,), 0xA7, dtype=torch.uint8, device="cuda")
+    tensors = [small_a, flat[shift:shift + n], small_b]
+    sizes = [777 * 4, n, 1001]
+    chunk = 64 << 20
+    torch.cuda.synchronize()
+    before = [t.clone() for t in tensors]
+    outside = torch.cat([flat[:shift], flat[shift + n:]]).clone()  # bytes of the buffer outside the view
+    ck = P.Checkpointer(tensors, chunk_bytes=chunk)
+    off, I, nc = O.layout(sizes, 256, chunk)
+    assert np.array_equal(ck.offsets, off) and (ck.image_bytes, ck.n_chunks) == (I, nc)
+    snap = ck.snapshot(step=1)
+    ck.wait_committed(snap)
+    img, sums = ck.host_image(snap)
+    x = int(off[1]) + (1 << 32)  # image byte of the big fragment's byte 2^32
+    picks = sorted({0, (x - 8) // chunk, x // chunk, (int(off[1]) + n - 1) // chunk, nc - 1})
+    for c in picks:
+        lo, hi = c * chunk, min((c + 1) * chunk, I)
+        want = oracle_window(tensors, off, sizes, lo, hi)
+        assert np.array_equal(img[lo:hi], want), "chunk %d differs" % c
+    assert np.array_equal(sums, O.chunk_sums(img, 0, I, chunk))
+    assert ck.verify(snap) == []
+    for t in tensors:
+        t.view(-1).view(torch.uint8).fill_(0x3C)
+    assert ck.restore(snap) == []
+    torch.cuda.synchronize()
+    for i, (t, b) in enumerate(zip(tensors, before)):
+        assert torch.equal(t.view(-1).view(torch.uint8), b.view(-1).view(torch.uint8)), "fragment %d" % i
+    # the scatter never writes outside the view
+    assert torch.equal(torch.cat([flat[:shift], flat[shift + n:]]), outside)
+    ck.close()
