@@ -56,6 +56,8 @@ def parse():
     ap.add_argument("--bounce-bytes", type=int, default=0,
                     help="pageable host images behind pinned bounce rings of this many bytes (0 = pinned images)")
     ap.add_argument("--host-threads", type=int, default=0, help="bounce mode: host copy threads (0 = library default)")
+    ap.add_argument("--grid-blocks", type=int, default=0,
+                    help="overlap leg: cap on the tile kernels' workgroups per launch (0 = one per tile)")
     ap.add_argument("--h2h-only", action="store_true",
                     help="run only the H2H replication leg (ring peer in this process, TCP over 127.0.0.1)")
     ap.add_argument("--h2h-workload", type=int, default=3)
@@ -350,7 +352,8 @@ def cpu_baseline(tensors, plan, chunk, target_bytes, threads=16):
                          "split": "whole chunks, %d per thread" % per, "seconds": round(dtn, 2)}}
 
 
-def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_steps=0, bounce=0, threads=0):
+def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_steps=0, bounce=0, threads=0,
+                grid_blocks=0):
     """Step-time overhead of per-step snapshots under a bf16 GEMM load.
 
     One step: R back-to-back GEMMs on the compute stream, the gate, then an
@@ -377,7 +380,7 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
     e1.synchronize()
     t_gemm = e0.elapsed_time(e1) / 50
     ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=W.WORKLOADS[wid]["chunk"],
-                        bounce_bytes=bounce, host_threads=threads)
+                        bounce_bytes=bounce, host_threads=threads, grid_blocks=grid_blocks)
     P.ckpt_set_timing(ck.ctx, True)
     t0 = time.perf_counter()
     s = ck.snapshot(step=0)
@@ -441,6 +444,7 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
     head = sweep[0]
     out = {"workload": W.WORKLOADS[wid]["name"], "payload_bytes": sum(p[1] for p in plan), "gemm_mkn": [M, K, N],
            "host_images": "pageable, %d-byte pinned bounce rings" % bounce if bounce else "pinned",
+           "tile_kernel_workgroups": grid_blocks or "one per tile",
            "gemm_ms": round(t_gemm, 4), "d2h_ms": round(t_d2h, 2), "R": head["R"], "steps": steps,
            "base_steps": base_steps, "base_ms": head["base_ms"], "with_snapshot_ms": head["with_snapshot_ms"],
            "overhead_pct": head["overhead_pct"],
@@ -642,7 +646,7 @@ def main():
         log("link peak")
         link = link_peak(torch)
         ov = overlap_leg(torch, P, W, args.overlap_workload, args.overlap_steps, link["d2h"], ratios,
-                         args.overlap_base_steps, args.bounce_bytes, args.host_threads)
+                         args.overlap_base_steps, args.bounce_bytes, args.host_threads, args.grid_blocks)
         print(json.dumps({"overlap": ov, "d2h_link_peak_GBps": round(link["d2h"], 2)}), flush=True)
         return
     wid = args.workload
@@ -743,7 +747,7 @@ def main():
     if not args.no_overlap:
         log("overlap leg")
         overlap = overlap_leg(torch, P, W, args.overlap_workload, args.overlap_steps, link["d2h"], ratios,
-                              args.overlap_base_steps, args.bounce_bytes, args.host_threads)
+                              args.overlap_base_steps, args.bounce_bytes, args.host_threads, args.grid_blocks)
     try:
         sha = subprocess.run(["git", "rev-parse", "--short", "HEAD"], cwd=ROOT, capture_output=True,
                              text=True).stdout.strip() or None
