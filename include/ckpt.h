@@ -317,6 +317,14 @@ ckpt_status ckpt_latest(ckpt_ctx* ctx, uint64_t* snap_id, uint64_t* step);
  * a replication is in progress), EHIP. */
 ckpt_status ckpt_replicate_to(ckpt_ctx* ctx, const char* host, uint32_t port, uint64_t cls_mask);
 
+/* Drop peer `peer` (0-based; later peers move down one place): its worker
+ * stops, a replica it is sending fails, its connection closes.  For ring
+ * repair after the peer's node is lost (Sec. V-C): drop it, then add the
+ * replacement's peer with ckpt_replicate_to.  Snapshots sent only to dropped
+ * peers count as not replicated (ERANGE from ckpt_wait(REPLICATED)).
+ * Errors: ESTATE (no such peer). */
+ckpt_status ckpt_replicate_remove(ckpt_ctx* ctx, uint32_t peer);
+
 /* The replicated chunk ids (increasing; up to cap written) and their total
  * bytes (the same for every peer).  Errors: ESTATE (no peer). */
 ckpt_status ckpt_replica_chunks(ckpt_ctx* ctx, uint64_t* ids, uint64_t cap, uint64_t* n, uint64_t* replica_bytes);

@@ -108,6 +108,7 @@ def lib():
             "ckpt_debug_h2h_fault_peer": ([vp, u32, i32, u64, u64], i32),
             "ckpt_replica_peer_result": ([vp, u32, u64, P(i32), P(u64), u32, P(u32)], i32),
             "ckpt_replica_peers": ([vp, P(u32)], i32),
+            "ckpt_replicate_remove": ([vp, u32], i32),
             "ckpt_peer_create": ([P(ckpt_config), u32, P(vp)], i32),
             "ckpt_peer_port": ([vp, P(u32)], i32),
             "ckpt_peer_destroy": ([vp], i32),
@@ -372,6 +373,10 @@ def ckpt_replica_peer_result(ctx, peer, snap_id):
     return st.value, [int(x) for x in bad[:nb.value]]
 
 
+def ckpt_replicate_remove(ctx, peer):
+    return _check(ctx, lib().ckpt_replicate_remove(ctx, peer))
+
+
 def ckpt_replica_peers(ctx):
     n = C.c_uint32()
     _check(ctx, lib().ckpt_replica_peers(ctx, C.byref(n)))
@@ -564,6 +569,9 @@ class Checkpointer:
 
     def replica_peer_result(self, peer, snap):
         return ckpt_replica_peer_result(self.ctx, peer, snap)
+
+    def replicate_remove(self, peer):
+        return ckpt_replicate_remove(self.ctx, peer)
 
     def restore_from_peer(self, port, host="127.0.0.1", stream=None):
         """Take the failed rank's replicated chunks back from its ring peer:

@@ -129,9 +129,23 @@ void rep_worker(ckpt_ctx* c, Replicator* R)
     }
 }
 
+// Stop one peer's worker (a job it is sending fails) and free it.
+void rep_free(Replicator* R)
+{
+    {
+        std::lock_guard<std::mutex> l(R->m);
+        R->stop = true;
+    }
+    R->cv.notify_all();
+    if (R->fd >= 0) ::shutdown(R->fd, SHUT_RDWR);
+    if (R->worker.joinable()) R->worker.join();
+    if (R->fd >= 0) ::close(R->fd);
+    delete R;
+}
+
 void rep_stop(ckpt_ctx* c)
 {
-    for (Replicator* R : c->reps) {
+    for (Replicator* R : c->reps) { // interrupt every peer first, then join them one by one
         {
             std::lock_guard<std::mutex> l(R->m);
             R->stop = true;
@@ -139,11 +153,7 @@ void rep_stop(ckpt_ctx* c)
         R->cv.notify_all();
         if (R->fd >= 0) ::shutdown(R->fd, SHUT_RDWR);
     }
-    for (Replicator* R : c->reps) {
-        if (R->worker.joinable()) R->worker.join();
-        if (R->fd >= 0) ::close(R->fd);
-        delete R;
-    }
+    for (Replicator* R : c->reps) rep_free(R);
     c->reps.clear();
 }
 
@@ -200,6 +210,16 @@ ckpt_status ckpt_replicate_to(ckpt_ctx* c, const char* host, uint32_t port, uint
     return CKPT_OK;
 }
 
+ckpt_status ckpt_replicate_remove(ckpt_ctx* c, uint32_t peer)
+{
+    if (!c) return CKPT_EINVAL;
+    if (peer >= c->reps.size()) return fail(c, CKPT_ESTATE, "no replication peer %u", peer);
+    Replicator* R = c->reps[peer];
+    c->reps.erase(c->reps.begin() + peer);
+    rep_free(R);
+    return CKPT_OK;
+}
+
 ckpt_status ckpt_replica_chunks(ckpt_ctx* c, uint64_t* ids, uint64_t cap, uint64_t* n, uint64_t* replica_bytes_out)
 {
     if (!c || !n) return CKPT_EINVAL;
@@ -235,9 +255,11 @@ ckpt_status ckpt_replica_result(ckpt_ctx* c, uint64_t snap_id, int32_t* state, u
     // Pending while any peer is; then failed, corrupt (the union of the bad
     // chunks) or OK.
     bool pending = false, failed = false;
+    size_t asked = 0;
     std::vector<uint64_t> all;
     for (Replicator* R : c->reps) {
-        if (snap_id < R->first_id && R != c->reps[0]) continue; // added after this snapshot
+        if (snap_id < R->first_id) continue; // added after this snapshot
+        ++asked;
         std::lock_guard<std::mutex> l(R->m);
         auto s = R->status.find(snap_id);
         if (s == R->status.end())
@@ -246,6 +268,8 @@ ckpt_status ckpt_replica_result(ckpt_ctx* c, uint64_t snap_id, int32_t* state, u
         failed |= s->second.state == REP_FAILED;
         all.insert(all.end(), s->second.bad.begin(), s->second.bad.end());
     }
+    if (!asked)
+        return fail(c, CKPT_ERANGE, "snapshot %llu was not sent to any current peer", (unsigned long long)snap_id);
     std::sort(all.begin(), all.end());
     all.erase(std::unique(all.begin(), all.end()), all.end());
     *state = pending ? REP_PENDING : failed ? REP_FAILED : all.empty() ? REP_OK : REP_CORRUPT;

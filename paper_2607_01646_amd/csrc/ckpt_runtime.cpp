@@ -1199,9 +1199,11 @@ ckpt_status ckpt_wait(ckpt_ctx* c, uint64_t snap_id, uint32_t mode, void* stream
         const auto deadline = std::chrono::steady_clock::now() + std::chrono::seconds(240);
         ckpt_status worst = CKPT_OK;
         std::string why;
+        size_t asked = 0;
         for (size_t k = 0; k < c->reps.size(); ++k) {
             Replicator* R = c->reps[k];
-            if (k && snap_id < R->first_id) continue; // this peer was added after the snapshot
+            if (snap_id < R->first_id) continue; // this peer was added after the snapshot
+            ++asked;
             std::unique_lock<std::mutex> l(R->m);
             auto s = R->status.find(snap_id);
             if (s == R->status.end())
@@ -1218,6 +1220,8 @@ ckpt_status ckpt_wait(ckpt_ctx* c, uint64_t snap_id, uint32_t mode, void* stream
                       " corrupt chunks";
             }
         }
+        if (!asked)
+            return fail(c, CKPT_ERANGE, "snapshot %llu was not sent to any current peer", (unsigned long long)snap_id);
         if (worst == CKPT_OK) return CKPT_OK;
         if (worst == CKPT_ECORRUPT)
             return fail(c, CKPT_ECORRUPT, "snapshot %llu: %s", (unsigned long long)snap_id, why.c_str());

@@ -78,3 +78,19 @@ def expected_replica(host, dtypes, classes, chunk, mask, step, meta=b""):
     sums = O.chunk_sums(img, 0, I, chunk)
     env = O.envelope(step, 256, chunk, I, off, sizes, dtypes, classes, sums, meta)
     return np.array(ids, dtype=np.uint64), data, sums[ids], env
+
+
+def expected_after_restore(failed_host, before_host, ids, chunk):
+    """A replacement's fragments after restoring the chunks `ids` of the
+    failed rank's image (oracle pack of failed_host): the image bytes inside
+    those chunks, the replacement's own bytes (before_host) elsewhere."""
+    sizes = [h.size for h in failed_host]
+    img, off, _ = O.pack(failed_host, 256, chunk)
+    out = [b.copy() for b in before_host]
+    for c in ids:
+        lo, hi = int(c) * chunk, min((int(c) + 1) * chunk, img.size)
+        for i, o in enumerate(off):
+            a, b = max(lo, int(o)), min(hi, int(o) + sizes[i])
+            if a < b:
+                out[i][a - int(o):b - int(o)] = img[a:b]
+    return out

@@ -262,7 +262,7 @@ def test_two_peers_hold_the_same_replica_and_fail_separately():
         p.close()
 
 
-def test_peer_added_later_gets_the_following_snapshots():
+def test_peer_added_later_and_removed():
     tensors, dtypes, classes = tiny_state()
     chunk = 1 << 20
     a, b = P.Peer(), P.Peer()
@@ -284,6 +284,19 @@ def test_peer_added_later_gets_the_following_snapshots():
     with pytest.raises(P.CkptError) as e:
         ck.replica_peer_result(1, s1)
     assert e.value.code == P.CKPT_ERANGE
+    # dropping the first peer: s1 went to it alone and no longer counts as replicated
+    ck.replicate_remove(0)
+    assert P.ckpt_replica_peers(ck.ctx) == 1
+    with pytest.raises(P.CkptError) as e:
+        ck.wait_replicated(s1)
+    assert e.value.code == P.CKPT_ERANGE
+    ck.wait_replicated(s2)
+    s3 = ck.snapshot(step=3)
+    ck.wait_replicated(s3)
+    assert b.replica()["snap_id"] == s3 and a.replica()["snap_id"] == s2
+    with pytest.raises(P.CkptError) as e:
+        ck.replicate_remove(1)
+    assert e.value.code == P.CKPT_ESTATE
     ck.close()
     a.close()
     b.close()

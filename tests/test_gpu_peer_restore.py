@@ -17,7 +17,7 @@ import torch
 
 import oracle as O
 import workloads as W
-from gpu_util import class_major, expected_replica, garbage_fill, host_bytes
+from gpu_util import class_major, expected_after_restore, expected_replica, garbage_fill, host_bytes
 
 pytestmark = pytest.mark.gpu
 
@@ -44,18 +44,7 @@ def replacement_like(tensors, value=0x3C):
 
 
 def expected_after(failed_host, before_host, classes, ids):
-    """Each fragment: the failed rank's image bytes inside the replicated
-    chunks, the replacement's own bytes elsewhere."""
-    sizes = [h.size for h in failed_host]
-    img, off, _ = O.pack(failed_host, 256, CHUNK)
-    out = [b.copy() for b in before_host]
-    for c in ids:
-        lo, hi = int(c) * CHUNK, min((int(c) + 1) * CHUNK, img.size)
-        for i, o in enumerate(off):
-            a, b = max(lo, int(o)), min(hi, int(o) + sizes[i])
-            if a < b:
-                out[i][a - int(o):b - int(o)] = img[a:b]
-    return out
+    return expected_after_restore(failed_host, before_host, ids, CHUNK)
 
 
 def assert_tensors(tensors, want):
