@@ -404,6 +404,8 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
         for p, m in zip(params, masters):
             p.copy_(m)
 
+    calls = []  # host time of each snapshot call
+
     def run(with_snap, R, steps):
         times = []
         snap = None
@@ -413,7 +415,9 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
             if with_snap:
                 if snap is not None:  # one snapshot in flight: a D2H longer than the step shows up here
                     ck.wait_committed(snap)
+                tc = time.perf_counter()
                 snap = ck.snapshot(step=k)
+                calls.append((time.perf_counter() - tc) * 1e3)
             for _ in range(R):
                 torch.matmul(x, w)
             if with_snap:
@@ -448,6 +452,7 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
            "gemm_ms": round(t_gemm, 4), "d2h_ms": round(t_d2h, 2), "R": head["R"], "steps": steps,
            "base_steps": base_steps, "base_ms": head["base_ms"], "with_snapshot_ms": head["with_snapshot_ms"],
            "overhead_pct": head["overhead_pct"],
+           "snapshot_call_ms": round(sorted(calls)[len(calls) // 2], 3) if calls else None,
            "statistic": "mean after dropping 10 warm-up steps and the slowest 5%"}
     if len(sweep) > 1:
         out["sweep"] = sweep
