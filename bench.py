@@ -168,6 +168,36 @@ def timed_pack_average(d, bench):
     return sum(durs) / len(durs), len(durs)
 
 
+def timed_d2h_from_trace(d, bench):
+    """Per timed snapshot of the bench's workload-2 steps: image bytes / (last
+    group copy's end - first group copy's start), from the memory-copy trace.
+    The group copies are the device-to-host copies longer than 1 ms, in time
+    order: (warmup + steps) snapshots of `launches / steps` copies each come
+    first (the calibration copies before them are blit kernels, not copies)."""
+    import csv
+    import glob
+    import statistics
+
+    copies = []
+    for f in glob.glob(os.path.join(d, "**", "*memory_copy_trace.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            kind = " ".join(str(v) for k, v in r.items() if k and ("Direction" in k or "Kind" in k))
+            a, b = int(r["Start_Timestamp"]), int(r["End_Timestamp"])
+            if "DEVICE_TO_HOST" in kind and b - a > 1_000_000:
+                copies.append((a, b))
+    copies.sort()
+    per = bench["roofline"]["launches"] // bench["steps"]
+    image = bench["config"]["image_bytes"]
+    rates = []
+    for k in range(bench["warmup"], bench["warmup"] + bench["steps"]):
+        grp = copies[k * per:(k + 1) * per]
+        if len(grp) < per:
+            break
+        span = max(b for _, b in grp) - min(a for a, _ in grp)
+        rates.append(image / span)  # bytes per ns = GB/s
+    return rates, (statistics.median(rates) if rates else float("nan"))
+
+
 def stats_summary(d, command):
     """Markdown table of our kernels and copies from a --kernel-trace --stats run."""
     import csv
@@ -627,6 +657,16 @@ def main():
                   % (rl["avg_launch_ms"], rl["achieved"], rl["frac"]))
             print("- algorithmic bytes per launch %d -> %.1f GB/s from the rocprofv3 average"
                   % (rl["algorithmic_bytes_per_launch"], rl["algorithmic_bytes_per_launch"] / avg / 1e6))
+            rates, med = timed_d2h_from_trace(args.stats_summary, b)
+            c = b["components"]
+            print("\nD2H of the bench's timed snapshots (image bytes / first group copy start to last group copy end, "
+                  "from the memory-copy trace):")
+            print("- per snapshot: %s GB/s; median %.2f GB/s = %.1f%% of the link measured in the run (%.2f GB/s)"
+                  % (", ".join("%.2f" % x for x in rates), med, 100 * med / c["d2h_link_peak_GBps"],
+                     c["d2h_link_peak_GBps"]))
+            print("- bench.py's own figure from the engines' completion timestamps, same run: %s"
+                  % ("%.2f GB/s" % c["d2h_GBps"] if c["d2h_GBps"] else "not available (the copy tracer owns the "
+                     "completion signals)"))
         return
     if args.gpus != 1:
         print("bench.py measures one GPU: the snapshot path has no cross-GPU step in this build "
