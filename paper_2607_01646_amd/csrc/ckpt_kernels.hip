@@ -253,15 +253,6 @@ __device__ __forceinline__ uint32_t find_frag_global(const FragDev* frags, uint3
     return lo;
 }
 
-// Workgroup b of a launch runs on XCD b % 8 (round-robin dispatch).  With
-// REMAP, workgroup b takes tile x*q + min(x, r) + b/8 (x = b % 8, n = 8q + r
-// workgroups), so each XCD streams one contiguous eighth of the launch.
-__device__ __forceinline__ uint64_t remap_block(uint32_t b, uint32_t n)
-{
-    const uint32_t q = n >> 3, r = n & 7, x = b & 7, k = b >> 3;
-    return (uint64_t)x * q + (x < r ? x : r) + k;
-}
-
 // One tile: wave w owns vectors [w * slice, (w + 1) * slice) of it and
 // stores that slice's sum to partials[t * WAVES + w].
 template <int MODE, int BLOCK, int UNROLL, bool NTL, bool NTS>
@@ -348,12 +339,11 @@ __device__ __forceinline__ void do_tile(const Args& a, uint64_t t, uint64_t* s_o
 // Without LOOP the grid has one workgroup per tile and each takes exactly
 // one (a grid-stride loop around the same body measured ~3% slower on the
 // default launch); with LOOP a capped grid strides over the tiles.
-template <int MODE, bool LOOP, int BLOCK = kBlock, int UNROLL = kUnroll, bool NTL = true, bool NTS = true,
-          bool REMAP = false>
+template <int MODE, bool LOOP, int BLOCK = kBlock, int UNROLL = kUnroll, bool NTL = true, bool NTS = true>
 __global__ __launch_bounds__(BLOCK) void tile_kernel(Args a)
 {
     __shared__ uint64_t s_off[kLdsFrags];
-    const uint64_t first = REMAP ? remap_block(blockIdx.x, gridDim.x) : blockIdx.x;
+    const uint64_t first = blockIdx.x;
     if (LOOP) {
         for (uint64_t t = a.t_lo + first; t < a.t_hi; t += gridDim.x) do_tile<MODE, BLOCK, UNROLL, NTL, NTS>(a, t, s_off);
     } else {
