@@ -27,6 +27,10 @@
  * before the optimizer step is refined to chunk granularity: it covers only
  * the chunks holding the fragments the caller is about to overwrite.
  *
+ * Further sections below: crash-surviving image files, host-to-host
+ * replication of the optimizer chunks to k ring peers (and the receiving
+ * peer), and a replacement rank's restore from a peer's replica.
+ *
  * Image layout.  Fragments keep registration order.  off[0] = 0,
  * off[i] = align_up(off[i-1] + nbytes[i-1], align); the image is
  * align_up(off[n-1] + nbytes[n-1], align) bytes; padding bytes are zero and
