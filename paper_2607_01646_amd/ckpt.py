@@ -509,6 +509,11 @@ class Checkpointer:
         ... forward / backward ...
         ck.wait_captured(snap, lo, hi)      # before overwriting fragments [lo, hi)
         ... optimizer step ...
+
+    Recovery: ck.restore() (newest committed snapshot) or ck.verify().
+    Replication: ck.replicate_to(port, cls_mask) once per peer, then
+    ck.wait_replicated(snap).  A replacement rank registered with the same
+    layout calls restore_from_peer(port) on the peer holding its replica.
     """
 
     def __init__(self, tensors, dtypes=None, classes=None, chunk_bytes=0, align_bytes=0, device_staging_bytes=0,
