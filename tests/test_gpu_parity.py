@@ -29,6 +29,8 @@ if torch.cuda.is_available():
     (65536, 16, 0, 65536),             # 16-byte alignment, one chunk per group
     (8192, 256, 4 * 8192, 0),          # ring of four device slots
     (1 << 16, 4096, 2 * (1 << 16), 0), # ring of two slots, 4 KiB alignment
+    (16, 16, 0, 0),                    # chunk = alignment = one 16-byte vector: 16-byte tiles
+    (48, 16, 0, 1 << 16),              # three-vector chunks, 1365 per group
 ])
 def test_edge_sizes_all_geometries(chunk, align, staging, group):
     tensors, host = random_byte_fragments(EDGE_SIZES, seed=chunk + align)
