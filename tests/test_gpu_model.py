@@ -1,0 +1,155 @@
+"""A seeded random walk over the library's operations, checked against a
+model of the ping-pong images (needs an MI355X).
+
+Operations: change the tensors, snapshot and commit, snapshot with the
+offload cut after a random number of groups (invariant I4: never committed),
+restore the newest or the older held snapshot, verify, and flip a bit in a
+committed host image.  The model holds, per host image, which snapshot it
+keeps and the tensor bytes of that snapshot; a snapshot goes to the image
+that does not hold the newest committed one (Sec. VI-A).  After every
+operation the library's snapshot states and newest snapshot must match the
+model; every restore must give back the model's bytes; every committed image
+must equal the oracle's pack of those bytes, with the oracle's sums.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+from gpu_util import garbage_fill, host_bytes
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    import paper_2607_01646_amd as P
+
+CHUNK = 1 << 20
+GROUP = 2 << 20
+
+
+class Image:
+    def __init__(self, snap, step, data):
+        self.snap, self.step, self.data = snap, step, data  # data None: interrupted
+
+
+@pytest.mark.parametrize("bounce, staging", [(0, 0), (4 << 20, 0), (0, 3 * GROUP)])
+def test_random_walk_against_the_ping_pong_model(bounce, staging):
+    rng = np.random.default_rng(1234 + bounce + staging)
+    tensors, plan = W.make_state(1, device="cuda")
+    tensors, plan = tensors[:72], plan[:72]  # the first 18 parameter tensors with their optimizer state
+    torch.cuda.synchronize()
+    sizes = [p[1] for p in plan]
+    ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=CHUNK, group_bytes=GROUP,
+                        bounce_bytes=bounce, device_staging_bytes=staging)
+    _, I, nc = O.layout(sizes, 256, CHUNK)
+    n_groups = -(-I // GROUP)
+    hold = [None, None]
+    newest = None  # index of the image holding the newest committed snapshot
+    seen = {}      # snap id -> (image index, committed?)
+    step = 0
+
+    def current():
+        torch.cuda.synchronize()
+        return [host_bytes(t) for t in tensors]
+
+    def target():
+        if newest is not None:
+            return 1 - newest
+        for b in (0, 1):
+            if hold[b] is None or hold[b].data is None:
+                return b
+        raise AssertionError("unreachable")
+
+    def check_states():
+        for sid, (b, committed) in seen.items():
+            try:
+                st = ck.state(sid)
+            except P.CkptError as e:  # old records may be dropped
+                assert e.code == P.CKPT_ERANGE
+                continue
+            if not committed:
+                assert st == P.CKPT_SNAP_ABORTED, (sid, st)
+            elif hold[b] is not None and hold[b].snap == sid:
+                assert st == P.CKPT_SNAP_COMMITTED, (sid, st)
+            else:
+                assert st == P.CKPT_SNAP_SUPERSEDED, (sid, st)
+        if newest is None:
+            assert ck.latest()[0] == 0
+        else:
+            assert ck.latest() == (hold[newest].snap, hold[newest].step)
+
+    def assert_tensors(data):
+        torch.cuda.synchronize()
+        for i, (t, d) in enumerate(zip(tensors, data)):
+            assert np.array_equal(host_bytes(t), d), "fragment %d" % i
+
+    ops = ["mutate", "commit", "commit", "abort", "restore", "restore_older", "verify", "flip"]
+    done = {op: 0 for op in ops}
+    for it in range(120):
+        op = ops[int(rng.integers(0, len(ops)))]
+        done[op] += 1
+        if op == "mutate":
+            for i in rng.choice(len(tensors), size=8, replace=False):
+                t = tensors[int(i)]
+                if rng.random() < 0.5:
+                    t.add_(float(rng.integers(1, 9)))
+                else:
+                    u = t.view(-1).view(torch.uint8)
+                    u.copy_(torch.randint(0, 256, u.shape, dtype=torch.uint8, device=u.device))
+        elif op == "commit":
+            step += 1
+            data = current()
+            b = target()
+            s = ck.snapshot(step=step, meta=b"walk %d" % it)
+            ck.wait_committed(s)
+            hold[b] = Image(s, step, data)
+            newest = b
+            seen[s] = (b, True)
+            img, sums = ck.host_image(s)
+            want, _, _ = O.pack(data, 256, CHUNK)
+            assert np.array_equal(img, want), "image of snapshot %d" % s
+            assert np.array_equal(sums, O.chunk_sums(want, 0, I, CHUNK))
+        elif op == "abort":
+            step += 1
+            b = target()
+            P.ckpt_debug_interrupt_next(ck.ctx, int(rng.integers(0, n_groups)))
+            s = ck.snapshot(step=step)
+            torch.cuda.synchronize()
+            assert ck.state(s) == P.CKPT_SNAP_ABORTED
+            hold[b] = Image(s, step, None)
+            seen[s] = (b, False)
+        elif op == "restore":
+            garbage_fill(tensors, int(rng.integers(0, 256)))
+            if newest is None:
+                with pytest.raises(P.CkptError) as e:
+                    ck.restore(0)
+                assert e.value.code == P.CKPT_ENOSNAP
+                continue
+            assert ck.restore(0) == []
+            assert_tensors(hold[newest].data)
+        elif op == "restore_older":
+            older = None if newest is None else hold[1 - newest]
+            if older is None or older.data is None:
+                continue
+            garbage_fill(tensors, 0x42)
+            assert ck.restore(older.snap) == []
+            assert_tensors(older.data)
+        elif op == "verify":
+            for img in hold:
+                if img is not None and img.data is not None:
+                    assert ck.verify(img.snap) == []
+        elif op == "flip":
+            if newest is None:
+                continue
+            s = hold[newest].snap
+            img, _ = ck.host_image(s)
+            x = int(rng.integers(0, I))
+            bit = 1 << int(rng.integers(0, 8))
+            img[x] ^= bit
+            assert ck.verify(s) == [x // CHUNK]
+            img[x] ^= bit
+            assert ck.verify(s) == []
+        check_states()
+    assert min(done.values()) >= 5, done  # every kind of operation ran several times
+    ck.close()
