@@ -402,8 +402,13 @@ void peer_main(ckpt_peer* p)
             std::lock_guard<std::mutex> l(p->m);
             p->cfd = fd;
         }
+        // A sender may connect long before its first snapshot: wait for the
+        // first bytes without a deadline, answering fetches on other
+        // connections meanwhile.
+        int w;
+        while ((w = wait_readable(p, fd)) == 2) side_connection(p);
         char magic[8];
-        if (recv_all(fd, magic, 8, std::chrono::steady_clock::now() + std::chrono::seconds(10)) == 0) {
+        if (w == 1 && recv_all(fd, magic, 8, std::chrono::steady_clock::now() + std::chrono::seconds(10)) == 0) {
             if (std::memcmp(magic, kFetchMagic, 8) == 0) serve_fetch(p, fd);
             else if (std::memcmp(magic, kWireMagic, 8) == 0) serve(p, fd);
             else set_err(p, "unknown request on a new connection");

@@ -325,3 +325,27 @@ def test_peer_list_errors():
     ck.close()
     for p in peers:
         p.close()
+
+
+def test_sender_idle_after_connecting_keeps_its_connection():
+    """A sender may connect long before its first snapshot; meanwhile the peer
+    answers a fetch on another connection (regression: the peer used to drop
+    a connection that sent nothing for 10 s)."""
+    import time
+
+    tensors, dtypes, classes = tiny_state()
+    peer = P.Peer()
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=1 << 20)
+    ck.replicate_to(peer.port, OPT)
+    other = P.Checkpointer([torch.empty_like(t) for t in tensors], dtypes, classes, chunk_bytes=1 << 20)
+    with pytest.raises(P.CkptError) as e:
+        other.restore_from_peer(peer.port)  # answered while the sender is still silent
+    assert e.value.code == P.CKPT_ENOSNAP
+    time.sleep(11)
+    host = [host_bytes(t) for t in tensors]
+    s = ck.snapshot(step=1)
+    ck.wait_replicated(s)
+    assert np.array_equal(peer.replica()["data"], expected_replica(host, dtypes, classes, 1 << 20, OPT, 1)[1])
+    other.close()
+    ck.close()
+    peer.close()

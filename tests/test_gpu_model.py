@@ -153,3 +153,81 @@ def test_random_walk_against_the_ping_pong_model(bounce, staging):
         check_states()
     assert min(done.values()) >= 5, done  # every kind of operation ran several times
     ck.close()
+
+
+def test_random_walk_with_a_peer():
+    """The same walk with replication to a peer: every committed snapshot is
+    replicated and waited for; some streams carry a flipped bit (the peer
+    rejects them and keeps its previous replica); a replacement context
+    restores from the peer now and then and must get exactly the replica the
+    model says the peer holds."""
+    from gpu_util import class_major, expected_after_restore
+
+    opt = (1 << W.CLS_MASTER) | (1 << W.CLS_ADAM_M) | (1 << W.CLS_ADAM_V)
+    rng = np.random.default_rng(99)
+    full, plan = W.make_state(1, device="cuda")
+    tensors, dtypes, classes = class_major(full[:72], plan[:72])
+    del full
+    torch.cuda.synchronize()
+    sizes = [int(t.numel() * t.element_size()) for t in tensors]
+    _, I, nc = O.layout(sizes, 256, CHUNK)
+    peer = P.Peer()
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=CHUNK, group_bytes=GROUP)
+    ck.replicate_to(peer.port, opt)
+    ids, rbytes = P.ckpt_replica_chunks(ck.ctx)
+    fresh = [torch.empty_like(t) for t in tensors]
+    rk = P.Checkpointer(fresh, dtypes, classes, chunk_bytes=CHUNK, group_bytes=GROUP)
+    peer_state = None  # (snap, step, tensor bytes) of the peer's committed replica
+    step = 0
+    ops = ["mutate", "replicate", "replicate", "replicate_flip", "abort", "fetch"]
+    done = {op: 0 for op in ops}
+    for it in range(60):
+        op = ops[int(rng.integers(0, len(ops)))]
+        done[op] += 1
+        if op == "mutate":
+            for i in rng.choice(len(tensors), size=6, replace=False):
+                tensors[int(i)].add_(float(rng.integers(1, 9)))
+        elif op in ("replicate", "replicate_flip"):
+            step += 1
+            torch.cuda.synchronize()
+            data = [host_bytes(t) for t in tensors]
+            if op == "replicate_flip":
+                at = int(rng.integers(0, rbytes))
+                P.ckpt_debug_h2h_fault(ck.ctx, 1, at, int(rng.integers(0, 8)))
+            s = ck.snapshot(step=step)
+            ck.wait_committed(s)
+            if op == "replicate":
+                ck.wait_replicated(s)
+                peer_state = (s, step, data)
+            else:
+                with pytest.raises(P.CkptError) as e:
+                    ck.wait_replicated(s)
+                assert e.value.code == P.CKPT_ECORRUPT
+                assert ck.replica_result(s) == (P.REPLICA_CORRUPT, [int(ids[at // CHUNK])])
+        elif op == "abort":
+            step += 1
+            P.ckpt_debug_interrupt_next(ck.ctx, int(rng.integers(0, -(-I // GROUP))))
+            ck.snapshot(step=step)
+            torch.cuda.synchronize()
+        elif op == "fetch":
+            garbage_fill(fresh, int(rng.integers(0, 256)))
+            torch.cuda.synchronize()
+            before = [host_bytes(t) for t in fresh]
+            if peer_state is None:
+                with pytest.raises(P.CkptError) as e:
+                    rk.restore_from_peer(peer.port)
+                assert e.value.code == P.CKPT_ENOSNAP
+                continue
+            s, st, data = peer_state
+            assert rk.restore_from_peer(peer.port) == (s, st, [])
+            want = expected_after_restore(data, before, ids, CHUNK)
+            torch.cuda.synchronize()
+            for i, t in enumerate(fresh):
+                assert np.array_equal(host_bytes(t), want[i]), "fragment %d" % i
+        if peer_state is not None:
+            r = peer.replica()
+            assert (r["snap_id"], r["step"]) == peer_state[:2]
+    assert min(done.values()) >= 4, done
+    rk.close()
+    ck.close()
+    peer.close()
