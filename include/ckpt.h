@@ -310,7 +310,10 @@ ckpt_status ckpt_latest(ckpt_ctx* ctx, uint64_t* snap_id, uint64_t* step);
  * the same cls_mask, while no replication is in progress) to add further
  * peers; each receives the snapshots issued after it was added, and the
  * streams to the k peers run at the same time.
- * ckpt_wait(CKPT_WAIT_REPLICATED) blocks until every peer has answered: OK
+ * ckpt_wait(CKPT_WAIT_REPLICATED) blocks until every peer has answered (a
+ * transfer may take as long as it needs while bytes flow; one that makes no
+ * progress for 30 s, or whose local snapshot does not commit within 120 s,
+ * fails with EHIP): OK
  * when all committed the replica; ECORRUPT when a peer found bad chunks (that
  * peer keeps its previous replica; ckpt_replica_result lists them); EHIP
  * when a connection failed (the failure wins over corruption).  While a
@@ -421,8 +424,8 @@ const char* ckpt_peer_last_error(const ckpt_peer* peer);
  * included), each chunk's sum is recomputed on the GPU and compared with the
  * sum stored at pack time, and `stream` waits for the writes.  Fragment
  * bytes outside the replicated chunks are left as they are.  *snap_id / *step (may be NULL): the failed rank's snapshot id
- * and step.  Blocks until done (a 300 s limit on the transfer).  Does not
- * change ckpt_last_sums or the restore timing.
+ * and step.  Blocks until done (the transfer fails with EHIP once it makes no
+ * progress for 30 s).  Does not change ckpt_last_sums or the restore timing.
  * Errors: EINVAL (bad argument, or the reply does not match this layout:
  * nothing written), ESTATE (not registered), EBUSY (a snapshot has not
  * committed, or the target image is being sent to this context's own peer),

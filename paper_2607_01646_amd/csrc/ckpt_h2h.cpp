@@ -54,8 +54,9 @@ void rep_worker(ckpt_ctx* c, Replicator* R)
                 fb = R->fault_b;
                 R->fault_kind = 0;
             }
-            // 2. Send head, ids, sums, envelope and the chunks.
-            const auto deadline = t_commit + std::chrono::seconds(120);
+            // 2. Send head, ids, sums, envelope and the chunks (the deadline
+            // moves on while bytes flow: only a stalled connection fails).
+            auto deadline = t_commit + std::chrono::seconds(120);
             const uint64_t m = R->ids.size();
             const uint64_t* sums_all = c->h_sums[j.buf];
             std::vector<uint64_t> sums(m);

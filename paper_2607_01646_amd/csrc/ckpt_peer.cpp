@@ -222,7 +222,7 @@ int wait_readable(ckpt_peer* p, int fd)
 // so no snapshot can be received into that buffer meanwhile.
 void serve_fetch(ckpt_peer* p, int fd)
 {
-    const auto deadline = std::chrono::steady_clock::now() + std::chrono::seconds(120);
+    auto deadline = std::chrono::steady_clock::now() + std::chrono::seconds(120);
     WireFetch f;
     if (recv_all(fd, reinterpret_cast<char*>(&f) + 8, sizeof f - 8, deadline)) return;
     int b;
@@ -301,7 +301,7 @@ void serve(ckpt_peer* p, int fd)
             }
         }
         const auto t0 = clock::now();
-        const auto deadline = t0 + std::chrono::seconds(120);
+        auto deadline = t0 + std::chrono::seconds(120);
         WireHead h;
         if (!first && recv_all(fd, h.magic, 8, deadline)) return; // closed between snapshots
         if (first) std::memcpy(h.magic, kWireMagic, 8);

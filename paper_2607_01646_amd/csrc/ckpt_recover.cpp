@@ -78,7 +78,7 @@ ckpt_status ckpt_restore_from_peer(ckpt_ctx* c, const char* host, uint32_t port,
     if (st) return st;
 
     const auto t0 = clock::now();
-    const auto deadline = t0 + std::chrono::seconds(300);
+    auto deadline = t0 + std::chrono::seconds(300);
     const int fd = dial(host, port);
     if (fd < 0) {
         if (errno == EINVAL) return fail(c, CKPT_EINVAL, "host must be a dotted IPv4 address");

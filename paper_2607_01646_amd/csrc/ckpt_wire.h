@@ -84,8 +84,14 @@ inline uint64_t replica_bytes(const uint64_t* ids, uint64_t m, uint64_t chunk_by
     return (m - 1) * chunk_bytes + last_len;
 }
 
-// Blocking send / receive of exactly n bytes with an overall deadline.
-// Return 0 on success, -1 on error or timeout, -2 when the other side closed.
+// Blocking send / receive of exactly n bytes.  Return 0 on success, -1 on
+// error or timeout, -2 when the other side closed.  `deadline` bounds the
+// wait for progress: every piece moved pushes it to at least kWireGrace from
+// now, so a transfer may take as long as it needs while data flows and only a
+// stalled connection times out.  The caller's deadline variable is updated,
+// so a sequence of calls shares it.
+constexpr auto kWireGrace = std::chrono::seconds(30);
+
 inline int wire_wait(int fd, short ev, std::chrono::steady_clock::time_point deadline)
 {
     for (;;) {
@@ -99,7 +105,12 @@ inline int wire_wait(int fd, short ev, std::chrono::steady_clock::time_point dea
     }
 }
 
-inline int send_all(int fd, const void* buf, uint64_t n, std::chrono::steady_clock::time_point deadline)
+inline void wire_progress(std::chrono::steady_clock::time_point& deadline)
+{
+    deadline = std::max(deadline, std::chrono::steady_clock::now() + kWireGrace);
+}
+
+inline int send_all(int fd, const void* buf, uint64_t n, std::chrono::steady_clock::time_point& deadline)
 {
     const uint8_t* p = (const uint8_t*)buf;
     while (n) {
@@ -111,11 +122,12 @@ inline int send_all(int fd, const void* buf, uint64_t n, std::chrono::steady_clo
         }
         p += k;
         n -= (uint64_t)k;
+        wire_progress(deadline);
     }
     return 0;
 }
 
-inline int recv_all(int fd, void* buf, uint64_t n, std::chrono::steady_clock::time_point deadline)
+inline int recv_all(int fd, void* buf, uint64_t n, std::chrono::steady_clock::time_point& deadline)
 {
     uint8_t* p = (uint8_t*)buf;
     while (n) {
@@ -128,8 +140,22 @@ inline int recv_all(int fd, void* buf, uint64_t n, std::chrono::steady_clock::ti
         }
         p += k;
         n -= (uint64_t)k;
+        wire_progress(deadline);
     }
     return 0;
+}
+
+// One-off calls with a deadline of their own.
+inline int send_all(int fd, const void* buf, uint64_t n, std::chrono::steady_clock::time_point&& deadline)
+{
+    auto d = deadline;
+    return send_all(fd, buf, n, d);
+}
+
+inline int recv_all(int fd, void* buf, uint64_t n, std::chrono::steady_clock::time_point&& deadline)
+{
+    auto d = deadline;
+    return recv_all(fd, buf, n, d);
 }
 
 inline void tune_socket(int fd)
