@@ -33,15 +33,17 @@ class Image:
         self.snap, self.step, self.data = snap, step, data  # data None: interrupted
 
 
-@pytest.mark.parametrize("bounce, staging", [(0, 0), (4 << 20, 0), (0, 3 * GROUP)])
-def test_random_walk_against_the_ping_pong_model(bounce, staging):
-    rng = np.random.default_rng(1234 + bounce + staging)
+@pytest.mark.parametrize("bounce, staging, file", [(0, 0, False), (4 << 20, 0, False), (0, 3 * GROUP, False),
+                                                   (4 << 20, 3 * GROUP, False), (4 << 20, 0, True)])
+def test_random_walk_against_the_ping_pong_model(bounce, staging, file, tmp_path):
+    rng = np.random.default_rng(1234 + bounce + staging + file)
     tensors, plan = W.make_state(1, device="cuda")
     tensors, plan = tensors[:72], plan[:72]  # the first 18 parameter tensors with their optimizer state
     torch.cuda.synchronize()
     sizes = [p[1] for p in plan]
     ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=CHUNK, group_bytes=GROUP,
-                        bounce_bytes=bounce, device_staging_bytes=staging)
+                        bounce_bytes=bounce, device_staging_bytes=staging,
+                        image_file=str(tmp_path / "images") if file else None)
     _, I, nc = O.layout(sizes, 256, CHUNK)
     n_groups = -(-I // GROUP)
     hold = [None, None]
@@ -85,6 +87,8 @@ def test_random_walk_against_the_ping_pong_model(bounce, staging):
             assert np.array_equal(host_bytes(t), d), "fragment %d" % i
 
     ops = ["mutate", "commit", "commit", "abort", "restore", "restore_older", "verify", "flip"]
+    if file:
+        ops.append("reopen")
     done = {op: 0 for op in ops}
     for it in range(120):
         op = ops[int(rng.integers(0, len(ops)))]
@@ -139,6 +143,21 @@ def test_random_walk_against_the_ping_pong_model(bounce, staging):
             for img in hold:
                 if img is not None and img.data is not None:
                     assert ck.verify(img.snap) == []
+        elif op == "reopen":  # a restarted process adopts the image file: the newest committed snapshot survives
+            ck.close()
+            ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=CHUNK,
+                                group_bytes=GROUP, bounce_bytes=bounce, device_staging_bytes=staging,
+                                image_file=str(tmp_path / "images"), image_file_mode=P.CKPT_FILE_ADOPT)
+            seen = {}
+            if newest is None:
+                hold = [None, None]
+            else:
+                sid, st = ck.latest()
+                assert st == hold[newest].step
+                kept = Image(sid, st, hold[newest].data)
+                hold = [None, None]
+                hold[newest] = kept
+                seen[sid] = (newest, True)
         elif op == "flip":
             if newest is None:
                 continue
