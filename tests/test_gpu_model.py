@@ -250,3 +250,101 @@ def test_random_walk_with_a_peer():
     rk.close()
     ck.close()
     peer.close()
+
+
+def test_random_walk_with_changing_peers():
+    """Peers join and leave (1 to 3 at a time, Sec. V-C k-peer replication and
+    ring repair); a flipped bit goes to one chosen peer only; fetches go to a
+    random live peer.  The model keeps each peer's committed replica: a peer
+    takes only snapshots issued after it joined, and keeps its previous
+    replica when it rejects one."""
+    from gpu_util import class_major, expected_after_restore
+
+    opt = (1 << W.CLS_MASTER) | (1 << W.CLS_ADAM_M) | (1 << W.CLS_ADAM_V)
+    rng = np.random.default_rng(7)
+    full, plan = W.make_state(1, device="cuda")
+    tensors, dtypes, classes = class_major(full[:72], plan[:72])
+    del full
+    torch.cuda.synchronize()
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=CHUNK, group_bytes=GROUP)
+    fresh = [torch.empty_like(t) for t in tensors]
+    rk = P.Checkpointer(fresh, dtypes, classes, chunk_bytes=CHUNK, group_bytes=GROUP)
+    peers = []  # [Peer, committed replica (snap, step, bytes) or None], in the order added
+    retired = []
+    ids = rbytes = None
+    step = 0
+
+    def add_peer():
+        nonlocal ids, rbytes
+        p = P.Peer()
+        ck.replicate_to(p.port, opt)
+        peers.append([p, None])
+        ids, rbytes = P.ckpt_replica_chunks(ck.ctx)
+
+    add_peer()
+    ops = ["mutate", "snap", "snap", "snap_flip", "add", "remove", "fetch"]
+    done = {op: 0 for op in ops}
+    for it in range(80):
+        op = ops[int(rng.integers(0, len(ops)))]
+        if op == "add" and len(peers) >= 3 or op == "remove" and len(peers) <= 1:
+            continue
+        done[op] += 1
+        if op == "mutate":
+            for i in rng.choice(len(tensors), size=6, replace=False):
+                tensors[int(i)].add_(float(rng.integers(1, 9)))
+        elif op == "add":
+            add_peer()
+        elif op == "remove":
+            j = int(rng.integers(0, len(peers)))
+            ck.replicate_remove(j)
+            retired.append(peers.pop(j)[0])  # its node stays up; it just leaves the ring
+            assert P.ckpt_replica_peers(ck.ctx) == len(peers)
+        elif op in ("snap", "snap_flip"):
+            step += 1
+            torch.cuda.synchronize()
+            data = [host_bytes(t) for t in tensors]
+            bad_peer = None
+            if op == "snap_flip":
+                bad_peer = int(rng.integers(0, len(peers)))
+                at = int(rng.integers(0, rbytes))
+                P.ckpt_debug_h2h_fault_peer(ck.ctx, bad_peer, 1, at, int(rng.integers(0, 8)))
+            s = ck.snapshot(step=step)
+            if bad_peer is None:
+                ck.wait_replicated(s)
+            else:
+                with pytest.raises(P.CkptError) as e:
+                    ck.wait_replicated(s)
+                assert e.value.code == P.CKPT_ECORRUPT
+                assert ck.replica_result(s) == (P.REPLICA_CORRUPT, [int(ids[at // CHUNK])])
+            for j, entry in enumerate(peers):
+                want_state = P.REPLICA_CORRUPT if j == bad_peer else P.REPLICA_OK
+                assert ck.replica_peer_result(j, s)[0] == want_state
+                if j != bad_peer:
+                    entry[1] = (s, step, data)
+        elif op == "fetch":
+            j = int(rng.integers(0, len(peers)))
+            p, rep = peers[j]
+            garbage_fill(fresh, int(rng.integers(0, 256)))
+            torch.cuda.synchronize()
+            before = [host_bytes(t) for t in fresh]
+            if rep is None:
+                with pytest.raises(P.CkptError) as e:
+                    rk.restore_from_peer(p.port)
+                assert e.value.code == P.CKPT_ENOSNAP
+                continue
+            assert rk.restore_from_peer(p.port) == (rep[0], rep[1], [])
+            want = expected_after_restore(rep[2], before, ids, CHUNK)
+            torch.cuda.synchronize()
+            for i, t in enumerate(fresh):
+                assert np.array_equal(host_bytes(t), want[i]), "fragment %d" % i
+        for p, rep in peers:
+            if rep is not None:
+                r = p.replica()
+                assert (r["snap_id"], r["step"]) == rep[:2]
+    assert min(done.values()) >= 4, done
+    rk.close()
+    ck.close()
+    for p, _ in peers:
+        p.close()
+    for p in retired:
+        p.close()
