@@ -56,6 +56,8 @@ def parse():
     ap.add_argument("--bounce-bytes", type=int, default=0,
                     help="pageable host images behind pinned bounce rings of this many bytes (0 = pinned images)")
     ap.add_argument("--host-threads", type=int, default=0, help="bounce mode: host copy threads (0 = library default)")
+    ap.add_argument("--image-file", default="",
+                    help="bounce mode: keep the host images in this file (crash-surviving; removed at the end)")
     ap.add_argument("--grid-blocks", type=int, default=0,
                     help="overlap leg: cap on the tile kernels' workgroups per launch (0 = one per tile)")
     ap.add_argument("--h2h-only", action="store_true",
@@ -706,7 +708,8 @@ def main():
     S = sum(p[1] for p in plan)
     n = len(tensors)
     ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=wl["chunk"],
-                        bounce_bytes=args.bounce_bytes, host_threads=args.host_threads)
+                        bounce_bytes=args.bounce_bytes, host_threads=args.host_threads,
+                        image_file=args.image_file or None)
     P.ckpt_set_timing(ck.ctx, True)
 
     prev = [None]
@@ -782,6 +785,8 @@ def main():
         alone_n += t["kernels"]
     pack_alone_gbps = 2 * S * 3 / alone_ms / 1e6
     ck.close()
+    if args.image_file and os.path.exists(args.image_file):
+        os.unlink(args.image_file)
     cpu = None
     if not args.no_cpu:
         log("cpu baseline")
@@ -805,7 +810,10 @@ def main():
         "config": {"workload": "%s shard: %d fragments, %d payload bytes, %d MiB chunks (snapshot + gate + restore "
                                "+ verify per step)" % (wl["name"], n, S, wl["chunk"] >> 20),
                    "payload_bytes": S, "image_bytes": int(sn["copy_bytes"]), "chunk_bytes": wl["chunk"],
-                   "host_images": ("pageable, %d-byte pinned bounce rings" % args.bounce_bytes
+                   "host_images": ("image file %s behind %d-byte pinned bounce rings" % (args.image_file,
+                                                                                          args.bounce_bytes)
+                                   if args.image_file else
+                                   "pageable, %d-byte pinned bounce rings" % args.bounce_bytes
                                    if args.bounce_bytes else "pinned"),
                    "parallelism": "one rank, one GPU"},
         "roofline": roofline,
