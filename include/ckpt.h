@@ -383,8 +383,16 @@ ckpt_status ckpt_peer_port(const ckpt_peer* peer, uint32_t* port);
 /* Stops the receiver (closing any connection) and frees everything. */
 ckpt_status ckpt_peer_destroy(ckpt_peer* peer);
 /* Wait (up to timeout_ms) until snapshot snap_id of the sender has been
- * handled: *result = CKPT_OK (committed), CKPT_ECORRUPT (rejected), or
- * CKPT_EHIP (the stream broke).  Errors: ERANGE on timeout. */
+ * handled: *result = CKPT_OK (committed), CKPT_ECORRUPT (rejected),
+ * CKPT_EHIP (the stream broke), CKPT_EINVAL (a chunk list out of order or
+ * out of the image, a replica size that does not match it, or a geometry
+ * other than the first snapshot's) or CKPT_ENOMEM (no room for the
+ * replica buffers).  The header is checked before anything is allocated
+ * for it (chunk size a multiple of 256, image at most 2^48 bytes, m chunks
+ * within the image, replica size within those m chunks) and the chunk ids
+ * as they arrive; a malformed header ends the connection with no result.
+ * Either way the peer drops that sender and keeps its newest committed
+ * replica.  Errors: ERANGE on timeout. */
 ckpt_status ckpt_peer_wait(ckpt_peer* peer, uint64_t snap_id, int32_t timeout_ms, int32_t* result);
 /* Borrowed view of the newest committed replica: sender's snapshot id and
  * step, the replica bytes (chunks back to back), the sender's chunk ids and

@@ -486,6 +486,10 @@ class Peer:
         lib().ckpt_peer_timing(self.p, C.byref(a), C.byref(b))
         return a.value, b.value
 
+    def last_error(self):
+        """Text of the receiver's last error ("" if none)."""
+        return (lib().ckpt_peer_last_error(self.p) or b"").decode()
+
     def close(self):
         if self.p:
             lib().ckpt_peer_destroy(self.p)

@@ -25,6 +25,7 @@
 #include <cstdio>
 #include <cstring>
 #include <map>
+#include <new>
 #include <mutex>
 #include <string>
 #include <thread>
@@ -119,14 +120,11 @@ void free_geometry(ckpt_peer* p)
     p->s_copy = p->s_ker = nullptr;
 }
 
-// Allocate buffers for the sender's geometry (first snapshot only).
+// Allocate buffers for the sender's geometry (first snapshot only; the
+// header and the ids have been checked).
 bool setup_geometry(ckpt_peer* p, const WireHead& h, const std::vector<uint64_t>& ids)
 {
     const uint64_t C = h.chunk_bytes;
-    if (C == 0 || C % 256 || h.m == 0 || h.image_bytes == 0 || h.image_bytes % 16) return false;
-    for (uint64_t k = 0; k < h.m; ++k)
-        if (ids[k] * C >= h.image_bytes || (k && ids[k] <= ids[k - 1])) return false;
-    if (replica_bytes(ids.data(), h.m, C, h.image_bytes) != h.replica_bytes) return false;
     p->C = C;
     p->I = h.image_bytes;
     p->n = h.m;
@@ -285,6 +283,39 @@ void finish(ckpt_peer* p, uint64_t id, int32_t result)
     p->cv.notify_all();
 }
 
+// Header fields that hold for any sender: chunk size a multiple of 256,
+// an image of at most 2^48 bytes, 1 <= m <= the image's chunk count, and a
+// replica of m chunks of which only the last may be short.  Checked before
+// anything is allocated for the snapshot.
+bool head_ok(const WireHead& h)
+{
+    const uint64_t C = h.chunk_bytes, I = h.image_bytes;
+    if (std::memcmp(h.magic, kWireMagic, 8) != 0 || C == 0 || C % 256 || I == 0 || I % 16 || I > (1ull << 48) ||
+        h.env_len > kMaxEnvelope)
+        return false;
+    const uint64_t img_chunks = I / C + (I % C != 0);
+    return h.m != 0 && h.m <= img_chunks && h.replica_bytes > (h.m - 1) * C && h.replica_bytes <= h.m * C;
+}
+
+// Receive the header's m chunk ids in pieces, each checked as it arrives
+// (increasing, inside the sender's image), so that memory grows only with
+// valid ids actually received.  0 = received, -1 = the connection failed,
+// -2 = an id out of order or out of range.
+int recv_ids(int fd, const WireHead& h, std::vector<uint64_t>& ids, std::chrono::steady_clock::time_point& deadline)
+{
+    const uint64_t img_chunks = h.image_bytes / h.chunk_bytes + (h.image_bytes % h.chunk_bytes != 0);
+    const uint64_t piece = 1ull << 17;
+    ids.clear();
+    while (ids.size() < h.m) {
+        const uint64_t k0 = ids.size(), k = std::min<uint64_t>(piece, h.m - k0);
+        ids.resize(k0 + k);
+        if (recv_all(fd, ids.data() + k0, 8 * k, deadline)) return -1;
+        for (uint64_t j = k0; j < k0 + k; ++j)
+            if (ids[j] >= img_chunks || (j && ids[j] <= ids[j - 1])) return -2;
+    }
+    return 0;
+}
+
 // Handle one sender connection (the first snapshot's magic already read)
 // until it closes or breaks; between snapshots, answer fetches on other
 // connections.
@@ -306,26 +337,35 @@ void serve(ckpt_peer* p, int fd)
         if (!first && recv_all(fd, h.magic, 8, deadline)) return; // closed between snapshots
         if (first) std::memcpy(h.magic, kWireMagic, 8);
         if (recv_all(fd, reinterpret_cast<char*>(&h) + 8, sizeof h - 8, deadline)) return;
-        if (std::memcmp(h.magic, kWireMagic, 8) != 0 || h.m == 0 || h.m > (1ull << 32) || h.env_len > kMaxEnvelope) {
+        if (!head_ok(h)) {
             set_err(p, "malformed replica header");
             return;
         }
-        std::vector<uint64_t> ids(h.m);
-        if (recv_all(fd, ids.data(), 8 * h.m, deadline)) {
+        if (p->ready && (h.chunk_bytes != p->C || h.image_bytes != p->I || h.m != p->n || h.replica_bytes != p->R)) {
+            set_err(p, "replica geometry changed");
+            finish(p, h.snap_id, CKPT_EINVAL);
+            return;
+        }
+        std::vector<uint64_t> ids;
+        const int got_ids = recv_ids(fd, h, ids, deadline);
+        if (got_ids == -1) {
             finish(p, h.snap_id, CKPT_EHIP);
             return;
         }
-        if (!p->ready) {
-            if (!setup_geometry(p, h, ids)) {
-                set_err(p, "cannot take a replica of %llu bytes in %llu chunks", (unsigned long long)h.replica_bytes,
-                        (unsigned long long)h.m);
-                finish(p, h.snap_id, CKPT_ENOMEM);
-                return;
-            }
-        } else if (h.chunk_bytes != p->C || h.image_bytes != p->I || h.m != p->n || h.replica_bytes != p->R ||
-                   ids != p->ids) {
-            set_err(p, "replica geometry changed");
+        const char* why = got_ids == -2 ? "malformed replica chunk list"
+                          : p->ready    ? (ids != p->ids ? "replica geometry changed" : nullptr)
+                          : replica_bytes(ids.data(), h.m, h.chunk_bytes, h.image_bytes) != h.replica_bytes
+                              ? "malformed replica size"
+                              : nullptr;
+        if (why) {
+            set_err(p, "%s", why);
             finish(p, h.snap_id, CKPT_EINVAL);
+            return;
+        }
+        if (!p->ready && !setup_geometry(p, h, ids)) {
+            set_err(p, "cannot take a replica of %llu bytes in %llu chunks", (unsigned long long)h.replica_bytes,
+                    (unsigned long long)h.m);
+            finish(p, h.snap_id, CKPT_ENOMEM);
             return;
         }
         int target;
@@ -410,7 +450,13 @@ void peer_main(ckpt_peer* p)
         char magic[8];
         if (w == 1 && recv_all(fd, magic, 8, std::chrono::steady_clock::now() + std::chrono::seconds(10)) == 0) {
             if (std::memcmp(magic, kFetchMagic, 8) == 0) serve_fetch(p, fd);
-            else if (std::memcmp(magic, kWireMagic, 8) == 0) serve(p, fd);
+            else if (std::memcmp(magic, kWireMagic, 8) == 0) {
+                try {
+                    serve(p, fd);
+                } catch (const std::bad_alloc&) { // a sender's sizes this host cannot hold
+                    set_err(p, "out of host memory while receiving a replica");
+                }
+            }
             else set_err(p, "unknown request on a new connection");
         }
         {

@@ -349,3 +349,75 @@ def test_sender_idle_after_connecting_keeps_its_connection():
     other.close()
     ck.close()
     peer.close()
+
+
+def _raw_stream(port, data):
+    import socket
+
+    s = socket.create_connection(("127.0.0.1", port))
+    s.sendall(data)
+    return s
+
+
+def _await_error(peer, text, timeout=30.0):
+    import time
+
+    end = time.time() + timeout
+    while time.time() < end:
+        if text in peer.last_error():
+            return
+        time.sleep(0.05)
+    raise AssertionError("peer error %r, expected %r" % (peer.last_error(), text))
+
+
+def test_malformed_sender_streams_are_dropped_and_the_peer_keeps_serving():
+    """Streams no sender writes are refused before the peer allocates anything
+    for them, and a real sender is served afterwards (regression: a header
+    claiming 2^32 chunks made the peer allocate room for their ids up front)."""
+    import struct
+
+    C = 1 << 20
+
+    def head(snap, chunk, image, m, replica, env_len=0):
+        return struct.pack("<8s7Q", b"CKPTH2H1", snap, 1, chunk, image, m, replica, env_len)
+
+    def ids(*k):
+        return np.array(k, dtype=np.uint64).tobytes()
+
+    peer = P.Peer()
+    # 2^32 chunks of 256 bytes in a 1 TiB image: consistent, but the ids never come
+    s = _raw_stream(peer.port, head(1, 256, 1 << 40, 1 << 32, 1 << 40))
+    s.close()
+    assert peer.wait(1, 30_000) == P.CKPT_EHIP
+    cases = [
+        (head(2, 100, 4 * C, 2, 2 * C), None, "malformed replica header"),  # chunk not a multiple of 256
+        (head(3, C, 4 * C, 2, 2 * C) + ids(1, 0), P.CKPT_EINVAL, "malformed replica chunk list"),  # out of order
+        (head(4, C, 4 * C, 5, 5 * C), None, "malformed replica header"),  # more chunks than the image has
+        (head(5, C, 4 * C, 2, 2 * C) + ids(3, 4), P.CKPT_EINVAL, "malformed replica chunk list"),  # beyond the image
+        (head(6, C, 4 * C, 2, 2 * C - 256) + ids(0, 1), P.CKPT_EINVAL, "malformed replica size"),
+        (head(7, C, 1 << 50, 2, 2 * C), None, "malformed replica header"),  # image above 2^48 bytes
+    ]
+    for data, result, text in cases:
+        s = _raw_stream(peer.port, data)
+        if result is not None:
+            snap = struct.unpack_from("<Q", data, 8)[0]
+            assert peer.wait(snap, 30_000) == result
+        _await_error(peer, text)
+        s.close()
+    with pytest.raises(P.PeerError) as e:
+        peer.replica()
+    assert e.value.code == P.CKPT_ENOSNAP
+
+    tensors, dtypes, classes = tiny_state()
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=C)
+    ck.replicate_to(peer.port, OPT)
+    host = [host_bytes(t) for t in tensors]
+    s = ck.snapshot(step=9, meta=b"after")
+    ck.wait_replicated(s)
+    ids_want, data_want, _, env_want = expected_replica(host, dtypes, classes, C, OPT, 9, b"after")
+    rep = peer.replica()
+    assert (rep["snap_id"], rep["step"]) == (s, 9)
+    assert np.array_equal(rep["chunk_ids"], ids_want) and np.array_equal(rep["data"], data_want)
+    assert rep["envelope"] == env_want
+    ck.close()
+    peer.close()
