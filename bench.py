@@ -56,6 +56,9 @@ def parse():
     ap.add_argument("--bounce-bytes", type=int, default=0,
                     help="pageable host images behind pinned bounce rings of this many bytes (0 = pinned images)")
     ap.add_argument("--host-threads", type=int, default=0, help="bounce mode: host copy threads (0 = library default)")
+    ap.add_argument("--staging-bytes", type=int, default=0,
+                    help="device staging: 0 = a full-size image (default); else a ring of chunk-sized slots of at "
+                         "most this many bytes, the next pack of a slot waiting for its copy (main and overlap legs)")
     ap.add_argument("--image-file", default="",
                     help="bounce mode: keep the host images in this file (crash-surviving; removed at the end)")
     ap.add_argument("--grid-blocks", type=int, default=0,
@@ -385,7 +388,7 @@ def cpu_baseline(tensors, plan, chunk, target_bytes, threads=16):
 
 
 def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_steps=0, bounce=0, threads=0,
-                grid_blocks=0):
+                grid_blocks=0, staging=0):
     """Step-time overhead of per-step snapshots under a bf16 GEMM load.
 
     One step: R back-to-back GEMMs on the compute stream, the gate, then an
@@ -412,7 +415,8 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
     e1.synchronize()
     t_gemm = e0.elapsed_time(e1) / 50
     ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=W.WORKLOADS[wid]["chunk"],
-                        bounce_bytes=bounce, host_threads=threads, grid_blocks=grid_blocks)
+                        bounce_bytes=bounce, host_threads=threads, grid_blocks=grid_blocks,
+                        device_staging_bytes=staging)
     P.ckpt_set_timing(ck.ctx, True)
     t0 = time.perf_counter()
     s = ck.snapshot(step=0)
@@ -480,6 +484,7 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
     head = sweep[0]
     out = {"workload": W.WORKLOADS[wid]["name"], "payload_bytes": sum(p[1] for p in plan), "gemm_mkn": [M, K, N],
            "host_images": "pageable, %d-byte pinned bounce rings" % bounce if bounce else "pinned",
+           "device_staging": staging_text(staging, W.WORKLOADS[wid]["chunk"]),
            "tile_kernel_workgroups": grid_blocks or "one per tile",
            "gemm_ms": round(t_gemm, 4), "d2h_ms": round(t_d2h, 2), "R": head["R"], "steps": steps,
            "base_steps": base_steps, "base_ms": head["base_ms"], "with_snapshot_ms": head["with_snapshot_ms"],
@@ -489,6 +494,10 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
     if len(sweep) > 1:
         out["sweep"] = sweep
     return out
+
+
+def staging_text(staging, chunk):
+    return "full image" if not staging else "ring of %d chunk slots" % max(1, staging // chunk)
 
 
 def loopback_peak(nbytes=4 << 30, piece=256 << 20):
@@ -693,7 +702,8 @@ def main():
         log("link peak")
         link = link_peak(torch)
         ov = overlap_leg(torch, P, W, args.overlap_workload, args.overlap_steps, link["d2h"], ratios,
-                         args.overlap_base_steps, args.bounce_bytes, args.host_threads, args.grid_blocks)
+                         args.overlap_base_steps, args.bounce_bytes, args.host_threads, args.grid_blocks,
+                         args.staging_bytes)
         print(json.dumps({"overlap": ov, "d2h_link_peak_GBps": round(link["d2h"], 2)}), flush=True)
         return
     wid = args.workload
@@ -709,7 +719,7 @@ def main():
     n = len(tensors)
     ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=wl["chunk"],
                         bounce_bytes=args.bounce_bytes, host_threads=args.host_threads,
-                        image_file=args.image_file or None)
+                        image_file=args.image_file or None, device_staging_bytes=args.staging_bytes)
     P.ckpt_set_timing(ck.ctx, True)
 
     prev = [None]
@@ -797,7 +807,8 @@ def main():
     if not args.no_overlap:
         log("overlap leg")
         overlap = overlap_leg(torch, P, W, args.overlap_workload, args.overlap_steps, link["d2h"], ratios,
-                              args.overlap_base_steps, args.bounce_bytes, args.host_threads, args.grid_blocks)
+                              args.overlap_base_steps, args.bounce_bytes, args.host_threads, args.grid_blocks,
+                              args.staging_bytes)
     try:
         sha = subprocess.run(["git", "rev-parse", "--short", "HEAD"], cwd=ROOT, capture_output=True,
                              text=True).stdout.strip() or None
@@ -815,6 +826,7 @@ def main():
                                    if args.image_file else
                                    "pageable, %d-byte pinned bounce rings" % args.bounce_bytes
                                    if args.bounce_bytes else "pinned"),
+                   "device_staging": staging_text(args.staging_bytes, wl["chunk"]),
                    "parallelism": "one rank, one GPU"},
         "roofline": roofline,
         "cpu_baseline": cpu,
