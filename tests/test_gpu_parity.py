@@ -68,6 +68,48 @@ def test_many_small_fragments_in_one_tile():
     ck.close()
 
 
+@pytest.mark.parametrize("align", [256, 16])
+def test_dense_tiny_fragments_at_odd_offsets(align):
+    """60,000 fragments of 1..1199 bytes at arbitrary byte offsets in one
+    buffer: nearly every tile holds several fragments with misaligned sources,
+    so the multi-fragment path of pack and scatter carries the whole image.
+    The restore must write every fragment back and leave the gaps between
+    them untouched."""
+    rng = np.random.default_rng(4242 + align)
+    n = 60_000
+    sizes = rng.integers(1, 1200, n)
+    gaps = rng.integers(0, 64, n)
+    offs = np.cumsum(gaps + np.concatenate(([0], sizes[:-1])))
+    total = int(offs[-1] + sizes[-1] + 64)
+    host_all = rng.integers(0, 256, total, dtype=np.uint8)
+    dev_all = torch.from_numpy(host_all.copy()).cuda()
+    frags = [dev_all[int(o):int(o) + int(z)] for o, z in zip(offs, sizes)]
+    host = [host_all[int(o):int(o) + int(z)] for o, z in zip(offs, sizes)]
+    chunk = 1 << 20
+    ck = P.Checkpointer(frags, chunk_bytes=chunk, align_bytes=align)
+    snap = ck.snapshot(step=1)
+    ck.wait_committed(snap)
+    img, sums = ck.host_image(snap)
+    want, off, nc = O.pack(host, align, chunk)
+    assert np.array_equal(ck.offsets, off) and img.size == want.size
+    diff = np.flatnonzero(img != want)
+    assert diff.size == 0, "image differs at %d bytes, first at %d" % (diff.size, diff[0])
+    assert np.array_equal(sums, O.chunk_sums(want, 0, want.size, chunk))
+    dev_all.fill_(0x5A)
+    assert ck.restore(snap) == []
+    torch.cuda.synchronize()
+    got = dev_all.cpu().numpy()
+    in_frag = np.zeros(total, dtype=bool)
+    starts, ends = offs, offs + sizes
+    marks = np.zeros(total + 1, dtype=np.int64)
+    np.add.at(marks, starts, 1)
+    np.add.at(marks, ends, -1)
+    in_frag = np.cumsum(marks[:-1]) > 0
+    assert np.array_equal(got[in_frag], host_all[in_frag]), "a fragment byte was not restored"
+    assert np.all(got[~in_frag] == 0x5A), "the restore wrote outside the fragments"
+    ck.close()
+
+
 def test_tiny_gpt_shard_bit_exact():
     """Workload 1: 4-layer GPT shard (208 fragments, 238.9 MB), 4 MiB chunks."""
     tensors, plan = W.make_state(1, device="cuda")
