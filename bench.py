@@ -680,8 +680,8 @@ def main():
                      "completion signals)"))
         return
     if args.gpus != 1:
-        print("bench.py measures one GPU: the snapshot path has no cross-GPU step in this build "
-              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        print("bench.py measures one GPU: each rank packs and offloads its own shard, with no step across GPUs, "
+              "so more GPUs would only repeat the one-GPU figure (--gpus %d requested)" % args.gpus, file=sys.stderr)
         sys.exit(2)
     import torch
 

@@ -3,7 +3,7 @@
 Test infrastructure only: the definitions it implements (layout, pack,
 checksum, restore, verify, locate, envelope) are stated in the header of
 ckpt_oracle.c, following Sec. V-B (D2H paragraph) and Sec. VI-A of the paper
-plus the word-sum integrity check this project adds.  Arrays are numpy;
+plus a per-chunk word-sum integrity check, which the paper does not have.  Arrays are numpy;
 fragment bytes are numpy uint8 arrays or bytes objects.
 """
 import ctypes as C
