@@ -56,9 +56,13 @@ def parse():
     ap.add_argument("--bounce-bytes", type=int, default=0,
                     help="pageable host images behind pinned bounce rings of this many bytes (0 = pinned images)")
     ap.add_argument("--host-threads", type=int, default=0, help="bounce mode: host copy threads (0 = library default)")
+    ap.add_argument("--group-bytes", type=int, default=0,
+                    help="bytes per pack launch and DMA request (whole chunks); 0 = the library default (1 GiB, or "
+                         "one chunk per ring slot)")
     ap.add_argument("--staging-bytes", type=int, default=0,
-                    help="device staging: 0 = a full-size image (default); else a ring of chunk-sized slots of at "
-                         "most this many bytes, the next pack of a slot waiting for its copy (main and overlap legs)")
+                    help="device staging: 0 = a full-size image (default); else a ring of slots of one chunk group "
+                         "each, at most this many bytes in all, the next pack of a slot waiting for its copy (main "
+                         "and overlap legs)")
     ap.add_argument("--image-file", default="",
                     help="bounce mode: keep the host images in this file (crash-surviving; removed at the end)")
     ap.add_argument("--grid-blocks", type=int, default=0,
@@ -388,7 +392,7 @@ def cpu_baseline(tensors, plan, chunk, target_bytes, threads=16):
 
 
 def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_steps=0, bounce=0, threads=0,
-                grid_blocks=0, staging=0):
+                grid_blocks=0, staging=0, group=0):
     """Step-time overhead of per-step snapshots under a bf16 GEMM load.
 
     One step: R back-to-back GEMMs on the compute stream, the gate, then an
@@ -416,17 +420,26 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
     t_gemm = e0.elapsed_time(e1) / 50
     ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=W.WORKLOADS[wid]["chunk"],
                         bounce_bytes=bounce, host_threads=threads, grid_blocks=grid_blocks,
-                        device_staging_bytes=staging)
+                        device_staging_bytes=staging, group_bytes=group)
     P.ckpt_set_timing(ck.ctx, True)
-    t0 = time.perf_counter()
-    s = ck.snapshot(step=0)
-    ck.wait_committed(s)
-    t_commit = (time.perf_counter() - t0) * 1e3
-    t_d2h = P.ckpt_last_timing(ck.ctx, P.CKPT_OP_SNAPSHOT)["copy_ms"]
-    if t_d2h <= 0:  # engine timestamps unavailable (a copy tracer owns the signals)
-        t_d2h = ck.image_bytes / link_d2h_gbps / 1e6
-    if bounce:  # the snapshot is done when its last group is in the pageable image
-        t_d2h = max(t_d2h, t_commit)
+    # Standalone D2H: the median of three snapshots after one warm-up snapshot
+    # (the first snapshot of a context also sets up its records).
+    d2h_runs = []
+    for k in range(4):
+        t0 = time.perf_counter()
+        s = ck.snapshot(step=k)
+        ck.wait_committed(s)
+        t_commit = (time.perf_counter() - t0) * 1e3
+        tm = P.ckpt_last_timing(ck.ctx, P.CKPT_OP_SNAPSHOT)
+        ck_groups = tm["kernels"]
+        t = tm["copy_ms"]
+        if t <= 0:  # engine timestamps unavailable (a copy tracer owns the signals)
+            t = ck.image_bytes / link_d2h_gbps / 1e6
+        if bounce:  # the snapshot is done when its last group is in the pageable image
+            t = max(t, t_commit)
+        if k:
+            d2h_runs.append(t)
+    t_d2h = sorted(d2h_runs)[1]
     P.ckpt_set_timing(ck.ctx, False)
     params = [tensors[i] for i in range(0, n, 4)]
     masters = [tensors[i] for i in range(1, n, 4)]
@@ -485,8 +498,10 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
     out = {"workload": W.WORKLOADS[wid]["name"], "payload_bytes": sum(p[1] for p in plan), "gemm_mkn": [M, K, N],
            "host_images": "pageable, %d-byte pinned bounce rings" % bounce if bounce else "pinned",
            "device_staging": staging_text(staging, W.WORKLOADS[wid]["chunk"]),
+           "groups_per_snapshot": ck_groups,
            "tile_kernel_workgroups": grid_blocks or "one per tile",
-           "gemm_ms": round(t_gemm, 4), "d2h_ms": round(t_d2h, 2), "R": head["R"], "steps": steps,
+           "gemm_ms": round(t_gemm, 4), "d2h_ms": round(t_d2h, 2), "d2h_runs_ms": [round(t, 2) for t in d2h_runs],
+           "R": head["R"], "steps": steps,
            "base_steps": base_steps, "base_ms": head["base_ms"], "with_snapshot_ms": head["with_snapshot_ms"],
            "overhead_pct": head["overhead_pct"],
            "snapshot_call_ms": round(sorted(calls)[len(calls) // 2], 3) if calls else None,
@@ -497,7 +512,7 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
 
 
 def staging_text(staging, chunk):
-    return "full image" if not staging else "ring of %d chunk slots" % max(1, staging // chunk)
+    return "full image" if not staging else "ring of at most %d bytes (%d chunks)" % (staging, staging // chunk)
 
 
 def loopback_peak(nbytes=4 << 30, piece=256 << 20):
@@ -703,7 +718,7 @@ def main():
         link = link_peak(torch)
         ov = overlap_leg(torch, P, W, args.overlap_workload, args.overlap_steps, link["d2h"], ratios,
                          args.overlap_base_steps, args.bounce_bytes, args.host_threads, args.grid_blocks,
-                         args.staging_bytes)
+                         args.staging_bytes, args.group_bytes)
         print(json.dumps({"overlap": ov, "d2h_link_peak_GBps": round(link["d2h"], 2)}), flush=True)
         return
     wid = args.workload
@@ -719,7 +734,8 @@ def main():
     n = len(tensors)
     ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=wl["chunk"],
                         bounce_bytes=args.bounce_bytes, host_threads=args.host_threads,
-                        image_file=args.image_file or None, device_staging_bytes=args.staging_bytes)
+                        image_file=args.image_file or None, device_staging_bytes=args.staging_bytes,
+                        group_bytes=args.group_bytes)
     P.ckpt_set_timing(ck.ctx, True)
 
     prev = [None]
@@ -808,7 +824,7 @@ def main():
         log("overlap leg")
         overlap = overlap_leg(torch, P, W, args.overlap_workload, args.overlap_steps, link["d2h"], ratios,
                               args.overlap_base_steps, args.bounce_bytes, args.host_threads, args.grid_blocks,
-                              args.staging_bytes)
+                              args.staging_bytes, args.group_bytes)
     try:
         sha = subprocess.run(["git", "rev-parse", "--short", "HEAD"], cwd=ROOT, capture_output=True,
                              text=True).stdout.strip() or None
@@ -827,6 +843,7 @@ def main():
                                    "pageable, %d-byte pinned bounce rings" % args.bounce_bytes
                                    if args.bounce_bytes else "pinned"),
                    "device_staging": staging_text(args.staging_bytes, wl["chunk"]),
+                   "groups_per_snapshot": int(sn["kernels"]),
                    "parallelism": "one rank, one GPU"},
         "roofline": roofline,
         "cpu_baseline": cpu,

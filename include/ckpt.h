@@ -88,10 +88,13 @@ typedef struct {
     uint64_t chunk_bytes;          /* chunk size; 0 = 64 MiB.  Multiple of align_bytes. */
     uint32_t align_bytes;          /* fragment alignment in the image; 0 = 256.  Power of two, 16..4096. */
     uint32_t host_buffers;         /* host images; 0 = 2 (ping-pong).  Only 2 is accepted. */
-    uint64_t device_staging_bytes; /* 0 = a full-size device image; otherwise a ring of chunk-sized
-                                      slots of at most this many bytes (at least 2 chunks) */
-    uint64_t group_bytes;          /* full-image mode: bytes packed per kernel launch and copied per
-                                      DMA request; 0 = 1 GiB (rounded to whole chunks) */
+    uint64_t device_staging_bytes; /* 0 = a full-size device image; otherwise a ring of slots of at
+                                      most this many bytes in all (at least 2 chunks); each slot
+                                      holds one chunk group */
+    uint64_t group_bytes;          /* bytes packed per kernel launch and copied per DMA request,
+                                      rounded down to whole chunks.  Full-image mode: 0 = 1 GiB.
+                                      Ring mode: 0 = one chunk per slot; larger groups are capped at
+                                      half the ring, so that it always has two slots or more */
     int32_t device;                /* HIP device ordinal */
     uint32_t grid_blocks;          /* cap on workgroups per kernel launch; 0 = one per 8 KiB tile */
     uint64_t bounce_bytes;         /* 0 = the two host images are pinned and the DMA engines write

@@ -295,6 +295,7 @@ struct ckpt_ctx {
     uint32_t A = kDefaultAlign;
     uint64_t staging_cap = 0; // 0 = full image
     uint64_t group_cfg = kDefaultGroup;
+    bool group_set = false; // group_bytes given explicitly (ring mode: slots of that many bytes)
     uint32_t grid_cap = kDefaultGrid;
     bool timing = false;
 
@@ -306,7 +307,7 @@ struct ckpt_ctx {
     uint64_t G = 1;        // chunks per group
     uint64_t n_groups = 0; // groups
     bool ring = false;
-    uint64_t n_slots = 0;  // ring slots (ring mode)
+    uint64_t n_slots = 0;  // ring slots of G chunks each (ring mode)
 
     // device memory
     FragDev* d_frags = nullptr;

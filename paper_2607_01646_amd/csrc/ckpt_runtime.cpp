@@ -123,7 +123,7 @@ uint64_t tiles_hi(const ckpt_ctx* c, uint64_t g)
 uint64_t area_of(const ckpt_ctx* c, uint64_t g) { return c->ring ? g % c->n_slots : g; }
 uint8_t* staging_of(const ckpt_ctx* c, uint64_t g)
 {
-    return c->ring ? c->d_staging + (g % c->n_slots) * c->C : c->d_staging + group_lo(c, g);
+    return c->ring ? c->d_staging + (g % c->n_slots) * c->G * c->C : c->d_staging + group_lo(c, g);
 }
 
 ckpt_status make_event(ckpt_ctx* c, hipEvent_t* e, bool timed)
@@ -210,13 +210,24 @@ ckpt_status setup_image_agent(ckpt_ctx* c, int b, const void* pinned)
         for (int k = 0; k < 16 && c->n_d2h_engines < kMaxEngines; ++k)
             if (mask & (1u << k)) c->d2h_engine[c->n_d2h_engines++] = (hsa_amd_sdma_engine_id_t)(1u << k);
         if (c->n_d2h_engines == 0) return fail(c, CKPT_EHIP, "no DMA engine available for device-to-host copies");
-        uint32_t hmask = 0;
+        // The 8-byte staging-counter copies (host -> device) get an engine
+        // that carries no image copy when there is one: an engine runs its
+        // requests in order, so a counter copy queued behind another group's
+        // image copy would hold back the next pack of that staging area.
+        uint32_t hmask = 0, used = 0;
         HSACHK(c, hsa_amd_memory_copy_engine_status(c->gpu_agent, c->img_agent[0], &hmask));
+        for (int k = 0; k < c->n_d2h_engines; ++k) used |= (uint32_t)c->d2h_engine[k];
         c->h2d_engine = c->d2h_engine[0];
-        for (int k = 0; k < 16; ++k)
+        bool own = false;
+        for (int k = 0; k < 16 && !own; ++k)
+            if ((hmask & (1u << k)) && !(used & (1u << k))) {
+                c->h2d_engine = (hsa_amd_sdma_engine_id_t)(1u << k);
+                own = true;
+            }
+        for (int k = 0; k < 16 && !own; ++k)
             if (hmask & (1u << k)) {
                 c->h2d_engine = (hsa_amd_sdma_engine_id_t)(1u << k);
-                break;
+                own = true;
             }
     }
     return CKPT_OK;
@@ -787,6 +798,7 @@ ckpt_status ckpt_create(const ckpt_config* cfg, ckpt_ctx** out)
     c->A = A;
     c->staging_cap = d.device_staging_bytes;
     c->group_cfg = d.group_bytes ? d.group_bytes : kDefaultGroup;
+    c->group_set = d.group_bytes != 0;
     c->grid_cap = d.grid_blocks ? d.grid_blocks : kDefaultGrid;
     c->bounce_cfg = d.bounce_bytes;
     c->host_threads = d.host_threads ? d.host_threads : kDefaultHostThreads;
@@ -852,16 +864,18 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
     c->geo.n_tiles = pl.n_tiles;
     c->geo.n_chunks = c->n_chunks;
 
-    // Groups: whole chunks per pack launch and DMA request; one chunk per
-    // slot in ring mode.
+    // Groups: whole chunks per pack launch and DMA request.  In ring mode a
+    // group fills one slot: one chunk unless group_bytes asks for more, and
+    // never more than half the ring, so that at least two slots exist.
     if (c->staging_cap) {
         c->ring = true;
-        c->G = 1;
-        c->n_slots = std::max<uint64_t>(1, std::min<uint64_t>(c->staging_cap / c->C, c->n_chunks));
+        const uint64_t want = c->group_set ? std::max<uint64_t>(1, c->group_cfg / c->C) : 1;
+        c->G = std::max<uint64_t>(1, std::min<uint64_t>(want, c->staging_cap / (2 * c->C)));
     } else {
         c->G = std::max<uint64_t>(1, c->group_cfg / c->C);
     }
     c->n_groups = (c->n_chunks + c->G - 1) / c->G;
+    if (c->ring) c->n_slots = std::max<uint64_t>(1, std::min<uint64_t>(c->staging_cap / (c->G * c->C), c->n_groups));
     const uint64_t unit = c->G * c->C; // bytes of one chunk group
     if (c->bounce_cfg) {
         if (c->bounce_cfg / unit < 2)
@@ -896,7 +910,7 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
     ALLOC(c->d_recomputed, c->n_chunks * 8);
     ALLOC(c->d_bad, c->n_chunks);
     ALLOC(c->d_area_done, n_areas * 8);
-    ALLOC(c->d_staging, c->ring ? c->n_slots * c->C : c->I);
+    ALLOC(c->d_staging, c->ring ? c->n_slots * c->G * c->C : c->I);
     c->n_vslots = std::min<uint64_t>(kVerifySlots, c->n_groups);
     ALLOC(c->d_vring, c->n_vslots * c->G * c->C);
 #undef ALLOC

@@ -28,6 +28,8 @@ if torch.cuda.is_available():
     (1 << 20, 256, 0, 0),              # chunk larger than most fragments
     (65536, 16, 0, 65536),             # 16-byte alignment, one chunk per group
     (8192, 256, 4 * 8192, 0),          # ring of four device slots
+    (4096, 256, 12 * 4096, 3 * 4096),  # ring of four slots of three chunks each
+    (4096, 256, 4 * 4096, 8 * 4096),   # ring slot size capped at half the ring: two slots of two chunks
     (1 << 16, 4096, 2 * (1 << 16), 0), # ring of two slots, 4 KiB alignment
     (16, 16, 0, 0),                    # chunk = alignment = one 16-byte vector: 16-byte tiles
     (48, 16, 0, 1 << 16),              # three-vector chunks, 1365 per group
