@@ -91,6 +91,8 @@ def parse():
 
 
 PACK_KERNEL = "tile_kernel<0"  # PACK instantiation of the tile kernel
+SCATTER_KERNEL = "tile_kernel<1"
+VERIFY_KERNEL = "tile_kernel<2"
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 CALIBRATION_BYTES = 1 << 30
 
@@ -122,6 +124,7 @@ def pmc_summary(fetch_dir, write_dir, command):
     same counters on a plain copy kernel of known size (1 GiB read, 1 GiB
     written), into HBM bytes per launch."""
     out = {"kernel_source_sha": kernel_source_sha(), "command": command}
+    others = {"scatter": SCATTER_KERNEL, "verify": VERIFY_KERNEL}
     for name, d in [("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)]:
         rows = [r for r in read_counter_csv(d) if r["Counter_Name"] == name]
         copy = [float(r["Counter_Value"]) for r in rows if COPY_KERNEL in r["Kernel_Name"]
@@ -137,7 +140,16 @@ def pmc_summary(fetch_dir, write_dir, command):
         out[key + "_kib_calibration_copy"] = copy_kib
         out[key + "_scale"] = factor
         out[key + "_bytes_per_pack_dispatch"] = sum(pack) / len(pack) * 1024.0 * factor
+        for kind, kname in others.items():  # restore and verify passes of the same run, when present
+            v = [float(r["Counter_Value"]) for r in rows if kname in r["Kernel_Name"]]
+            if v:
+                out["%s_%s_dispatches" % (key, kind)] = len(v)
+                out["%s_bytes_per_%s_dispatch" % (key, kind)] = sum(v) / len(v) * 1024.0 * factor
     out["traffic_bytes_per_pack_dispatch"] = out["fetch_bytes_per_pack_dispatch"] + out["write_bytes_per_pack_dispatch"]
+    for kind in others:
+        f, w = out.get("fetch_bytes_per_%s_dispatch" % kind), out.get("write_bytes_per_%s_dispatch" % kind)
+        if f is not None and w is not None:
+            out["traffic_bytes_per_%s_dispatch" % kind] = f + w
     return out
 
 
@@ -650,6 +662,8 @@ def pmc_run(torch, P, W):
     for k in range(2):
         s = ck.snapshot(step=k)
         ck.wait_committed(s)
+    if ck.restore(s) or ck.verify(s):  # one pass of the scatter and of the verify kernel
+        raise SystemExit("checksum mismatch in the counter run")
     ck.close()
     print("pmc run done", flush=True)
 
@@ -661,7 +675,10 @@ def main():
         header = ("# HBM traffic of the pack kernel (tile_kernel<PACK>) on the 24-layer hidden-2048 GPT shard\n"
                   "# (18,421,473,280 payload bytes, 1 GiB launches), from two rocprofv3 --pmc runs of\n"
                   "# `python bench.py --pmc-run`: FETCH_SIZE, then WRITE_SIZE (KiB per dispatch), each scaled by\n"
-                  "# the same counter on a plain 1 GiB device copy (__amd_rocclr_copyBuffer).")
+                  "# the same counter on a plain 1 GiB device copy (__amd_rocclr_copyBuffer).  The same run's\n"
+                  "# restore (tile_kernel<SCATTER>) and verify (tile_kernel<VERIFY>) passes are summarized too.\n"
+                  "# Algorithmic bytes per dispatch (18 per pass, the last one short): pack and scatter\n"
+                  "# 2,046,830,364 (read + write of the image's 1 GiB windows), verify 1,023,415,182 (read).")
         out = args.traffic
         write_summary(out, d, header)
         print(open(out).read())
