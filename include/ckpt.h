@@ -131,8 +131,13 @@ ckpt_status ckpt_destroy(ckpt_ctx* ctx);
  * tables, allocates device staging and the two host images (pinned, or
  * pageable plus the bounce rings; both pre-faulted).  Callable
  * once per context; a different layout needs a new context.
- * Errors: ESTATE (already registered), EINVAL (null pointer with nbytes > 0,
- * n == 0, or overlapping fragments are NOT checked), ENOMEM, EHIP. */
+ * Every non-empty fragment must be device (or managed) memory of the
+ * context's GPU and lie inside one allocation; this is checked here, so a
+ * wrong pointer or size fails now instead of faulting the first pack.
+ * Overlapping fragments are not checked.
+ * Errors: ESTATE (already registered), EINVAL (n == 0, a null pointer with
+ * nbytes > 0, memory that is not this GPU's device memory, or nbytes running
+ * past the end of the fragment's allocation), ENOMEM, EHIP. */
 ckpt_status ckpt_register_tensors(ckpt_ctx* ctx, const ckpt_tensor* t, uint32_t n);
 
 /* Start snapshot `step` (Sec. V-B D2H; Sec. VI-A ping-pong).  Stream-ordered

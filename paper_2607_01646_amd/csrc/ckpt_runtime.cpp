@@ -841,6 +841,32 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
     for (uint32_t i = 0; i < n; ++i) {
         if (t[i].nbytes && !t[i].dev_ptr) return fail(c, CKPT_EINVAL, "fragment %u: null pointer", i);
         nb[i] = t[i].nbytes;
+        if (!nb[i]) continue;
+        // The kernels dereference every fragment byte: the fragment has to be
+        // memory of this context's GPU and lie inside one allocation, or the
+        // first pack would fault instead of this call failing.
+        hipPointerAttribute_t pa;
+        std::memset(&pa, 0, sizeof pa);
+        if (hipPointerGetAttributes(&pa, t[i].dev_ptr) != hipSuccess) {
+            (void)hipGetLastError(); // leave no error behind for the next call to report
+            return fail(c, CKPT_EINVAL, "fragment %u: %p is not memory the GPU runtime knows", i, t[i].dev_ptr);
+        }
+        if (pa.type != hipMemoryTypeDevice && !pa.isManaged)
+            return fail(c, CKPT_EINVAL, "fragment %u: %p is not device memory (memory type %d)", i, t[i].dev_ptr,
+                        (int)pa.type);
+        if (pa.type == hipMemoryTypeDevice && pa.device != c->device)
+            return fail(c, CKPT_EINVAL, "fragment %u: memory of device %d, the context is on device %d", i, pa.device,
+                        c->device);
+        hipDeviceptr_t base = nullptr;
+        size_t size = 0;
+        if (hipMemGetAddressRange(&base, &size, (hipDeviceptr_t)t[i].dev_ptr) == hipSuccess) {
+            const uint64_t lo = (uint64_t)(uintptr_t)t[i].dev_ptr, b = (uint64_t)(uintptr_t)base;
+            if (lo < b || nb[i] > size || lo - b > size - nb[i])
+                return fail(c, CKPT_EINVAL, "fragment %u: %llu bytes at %p run past the end of its allocation", i,
+                            (unsigned long long)nb[i], t[i].dev_ptr);
+        } else {
+            (void)hipGetLastError();
+        }
     }
     Plan pl;
     if (!plan(nb.data(), n, c->C, c->A, &pl)) return fail(c, CKPT_EINVAL, "all fragments are empty");

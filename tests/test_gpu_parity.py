@@ -422,3 +422,34 @@ def test_error_codes():
     P.ckpt_destroy(ctx)
     with pytest.raises(P.CkptError):
         P.ckpt_create(chunk_bytes=1000)  # not a multiple of the alignment
+
+
+def test_registration_rejects_memory_the_kernels_cannot_read():
+    """Only device memory of the context's GPU, inside one allocation, can be
+    registered; anything else fails at registration (no kernel runs here)."""
+    import ctypes as C
+
+    def register_raw(ptr, nbytes):
+        ctx = P.ckpt_create(chunk_bytes=1 << 20)
+        arr = (P.ckpt_tensor * 1)()
+        arr[0].dev_ptr = ptr
+        arr[0].nbytes = nbytes
+        rc = P.lib().ckpt_register_tensors(ctx, arr, 1)
+        msg = P.ckpt_last_error(ctx)
+        P.ckpt_destroy(ctx)
+        return rc, msg
+
+    host = np.zeros(1 << 16, dtype=np.uint8)  # pageable host memory
+    rc, msg = register_raw(host.ctypes.data, host.size)
+    assert rc == P.CKPT_EINVAL, msg
+    pinned = torch.zeros(1 << 16, dtype=torch.uint8, pin_memory=True)  # host memory the GPU can reach
+    rc, msg = register_raw(pinned.data_ptr(), pinned.numel())
+    assert rc == P.CKPT_EINVAL and "not device memory" in msg, msg
+    dev = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
+    rc, msg = register_raw(dev.data_ptr(), 1 << 40)  # far past the end of its allocation
+    assert rc == P.CKPT_EINVAL and "past the end" in msg, msg
+    rc, msg = register_raw(dev.data_ptr() + 4096, (1 << 20) - 4096)  # a view inside the allocation
+    assert rc == P.CKPT_OK, msg
+    rc, msg = register_raw(dev.data_ptr(), 1 << 20)
+    assert rc == P.CKPT_OK, msg
+    torch.cuda.synchronize()
