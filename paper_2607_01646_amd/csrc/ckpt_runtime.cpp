@@ -7,10 +7,10 @@
 //                  pack kernel (fragments -> staging, tile sums)
 //                  event captured[g]            <- the gate waits on this
 //                  release kernel: dep[g] = 0
-//                  reduce kernel (tile sums -> chunk sums)
 //   SDMA engine e: (polls dep[g]) copy staging(g) -> pinned image   -> copied[g]
-//                  (after copied[g]) 8-byte copy: area_done[area(g)] = use count
-//   after the last group: release dep_sums; SDMA copies the chunk sums.
+//   counter engine: (after copied[g]) 8-byte copy: area_done[area(g)] = use count
+//   after the last group: one reduce kernel (tile sums -> chunk sums), release
+//   dep_sums; SDMA copies the chunk sums.
 //
 // Every copy completes into a signal of its own that starts at 1 (the
 // area-done copy of group g into flagged[g], the sums copy into `done`), so
@@ -1132,16 +1132,13 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
                                    r.timed ? res->k0[g] : nullptr, r.timed ? res->k1[g] : nullptr);
         if (e != hipSuccess) return fail(c, CKPT_EHIP, "pack launch failed: %s", hipGetErrorString(e));
         // The gate and the group's copy need the packed bytes only; the chunk
-        // sums of the group are added up behind them.
+        // sums are added up once, after the last group (below).
         HIPCHK(c, hipEventRecord(res->captured[g], c->s_pack));
         if (g < n_copy) {
             hsa_signal_store_screlease(res->dep[g], 1);
             e = launch_release(res->dep_val[g], c->s_pack);
             if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
         }
-        e = launch_chunk_reduce(c->geo, tiles_lo(c, g), tiles_hi(c, g), c->d_partials, res->d_sums, nullptr, nullptr,
-                                c->s_pack);
-        if (e != hipSuccess) return fail(c, CKPT_EHIP, "reduce launch failed: %s", hipGetErrorString(e));
         if (g >= n_copy) continue; // interrupted offload: this group never leaves the device
         hsa_signal_store_screlease(res->copied[g], 1);
         hsa_signal_store_screlease(res->flagged[g], 1);
@@ -1182,8 +1179,14 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
     if (stop >= 0) {
         r.aborted = true; // interrupted offload: never committed (its pack timing stays readable)
     } else {
+        // Every chunk's sum from its tiles' partial sums, in one launch: only
+        // the sums copy below needs them, and one launch per group would cost
+        // the caller host time per group.
+        hipError_t e = launch_chunk_reduce(c->geo, 0, c->geo.n_tiles, c->d_partials, res->d_sums, nullptr, nullptr,
+                                           c->s_pack);
+        if (e != hipSuccess) return fail(c, CKPT_EHIP, "reduce launch failed: %s", hipGetErrorString(e));
         hsa_signal_store_screlease(res->dep_sums, 1);
-        hipError_t e = launch_release(res->dep_sums_val, c->s_pack);
+        e = launch_release(res->dep_sums_val, c->s_pack);
         if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
         hsa_signal_store_screlease(res->done, 1);
         if (r.bounce) { // behind the snapshot's group copies
