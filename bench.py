@@ -58,7 +58,7 @@ def parse():
     ap.add_argument("--host-threads", type=int, default=0, help="bounce mode: host copy threads (0 = library default)")
     ap.add_argument("--group-bytes", type=int, default=0,
                     help="bytes per pack launch and DMA request (whole chunks); 0 = the library default (1 GiB, or "
-                         "one chunk per ring slot)")
+                         "a quarter of the staging ring)")
     ap.add_argument("--staging-bytes", type=int, default=0,
                     help="device staging: 0 = a full-size image (default); else a ring of slots of one chunk group "
                          "each, at most this many bytes in all, the next pack of a slot waiting for its copy (main "

@@ -93,8 +93,9 @@ typedef struct {
                                       holds one chunk group */
     uint64_t group_bytes;          /* bytes packed per kernel launch and copied per DMA request,
                                       rounded down to whole chunks.  Full-image mode: 0 = 1 GiB.
-                                      Ring mode: 0 = one chunk per slot; larger groups are capped at
-                                      half the ring, so that it always has two slots or more */
+                                      Ring mode: 0 = a quarter of the ring (at least one chunk);
+                                      groups are capped at half the ring, so that it always has
+                                      two slots or more */
     int32_t device;                /* HIP device ordinal */
     uint32_t grid_blocks;          /* cap on workgroups per kernel launch; 0 = one per 8 KiB tile */
     uint64_t bounce_bytes;         /* 0 = the two host images are pinned and the DMA engines write

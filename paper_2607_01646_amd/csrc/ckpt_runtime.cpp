@@ -891,11 +891,12 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
     c->geo.n_chunks = c->n_chunks;
 
     // Groups: whole chunks per pack launch and DMA request.  In ring mode a
-    // group fills one slot: one chunk unless group_bytes asks for more, and
-    // never more than half the ring, so that at least two slots exist.
+    // group fills one slot: group_bytes when given, else a quarter of the
+    // ring (four slots; fewer groups cost less host time per snapshot), at
+    // least one chunk and never more than half the ring.
     if (c->staging_cap) {
         c->ring = true;
-        const uint64_t want = c->group_set ? std::max<uint64_t>(1, c->group_cfg / c->C) : 1;
+        const uint64_t want = std::max<uint64_t>(1, (c->group_set ? c->group_cfg : c->staging_cap / 4) / c->C);
         c->G = std::max<uint64_t>(1, std::min<uint64_t>(want, c->staging_cap / (2 * c->C)));
     } else {
         c->G = std::max<uint64_t>(1, c->group_cfg / c->C);
