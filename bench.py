@@ -305,25 +305,42 @@ def trimmed_mean(xs, warm=10, drop=0.05):
 
 
 def link_peak(torch):
-    """Plain pinned 1 GiB D2H / H2D copies: the host link's measured peak."""
+    """Plain pinned 1 GiB D2H / H2D copies: the host link's measured peak,
+    the best of one 1 GiB copy and of 2 or 4 concurrent copies of its parts
+    on their own streams (wall time from the first start to the last end)."""
     n = 1 << 30
     h = torch.empty(n, dtype=torch.uint8, pin_memory=True)
     d = torch.empty(n, dtype=torch.uint8, device="cuda")
     d.fill_(7)
+    streams = [torch.cuda.Stream() for _ in range(4)]
     out = {}
-    for name, fn in [("d2h", lambda: h.copy_(d, non_blocking=True)), ("h2d", lambda: d.copy_(h, non_blocking=True))]:
-        fn()
-        torch.cuda.synchronize()
+    for name in ("d2h", "h2d"):
         best = 1e9
-        for _ in range(5):
-            a = torch.cuda.Event(enable_timing=True)
-            b = torch.cuda.Event(enable_timing=True)
-            a.record()
-            fn()
-            b.record()
-            b.synchronize()
-            best = min(best, a.elapsed_time(b))
+        for parts in (1, 2, 4):
+            per = n // parts
+            dst, src = (h, d) if name == "d2h" else (d, h)
+
+            def run():
+                start = torch.cuda.Event(enable_timing=True)
+                start.record()
+                ends = []
+                for k in range(parts):
+                    st = streams[k]
+                    st.wait_event(start)
+                    with torch.cuda.stream(st):
+                        dst[k * per:(k + 1) * per].copy_(src[k * per:(k + 1) * per], non_blocking=True)
+                        e = torch.cuda.Event(enable_timing=True)
+                        e.record(st)
+                        ends.append(e)
+                for e in ends:
+                    e.synchronize()
+                return max(start.elapsed_time(e) for e in ends)
+
+            run()
+            for _ in range(5):
+                best = min(best, run())
         out[name] = n / best / 1e6
+    torch.cuda.synchronize()
     del h, d
     return out
 
