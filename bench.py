@@ -627,7 +627,7 @@ def h2h_leg(torch, P, W, wid, steps, n_peers=1, bounce_bytes=0, host_threads=0):
                         host_threads=host_threads)
     rest = []
     for k in range(3):
-        sid, step, bad = rk.restore_from_peer(peer.port)
+        _, _, bad = rk.restore_from_peer(peer.port)
         torch.cuda.synchronize()
         if bad:
             raise RuntimeError("peer restore: chunks %s failed their sums" % bad)
@@ -674,7 +674,7 @@ def pmc_run(torch, P, W):
     b.copy_(a)
     torch.cuda.synchronize()
     del a, b
-    tensors, plan = W.make_state(2, device="cuda")
+    tensors, _ = W.make_state(2, device="cuda")
     ck = P.Checkpointer(tensors, chunk_bytes=W.WORKLOADS[2]["chunk"])
     for k in range(2):
         s = ck.snapshot(step=k)
@@ -834,7 +834,7 @@ def main():
     # Pack-only passes (outside the timed steps): snapshots whose offload is
     # cut before their first copy, so the kernels run with the host link
     # idle; such a snapshot is aborted and never committed.
-    alone_ms, alone_n = 0.0, 0
+    alone_ms = 0.0
     for k in range(3):
         P.ckpt_debug_interrupt_next(ck.ctx, 0)
         s_cut = ck.snapshot(step=10_000 + k)
@@ -842,7 +842,6 @@ def main():
         torch.cuda.current_stream().synchronize()
         t = P.ckpt_last_timing(ck.ctx, P.CKPT_OP_PACK)
         alone_ms += t["kernel_ms"]
-        alone_n += t["kernels"]
     pack_alone_gbps = 2 * S * 3 / alone_ms / 1e6
     # The same pack-only passes, each issued right after an optimizer-like
     # update (every fragment read and written in place, values unchanged):
