@@ -14,7 +14,6 @@ import torch
 
 import oracle as O
 import workloads as W
-from gpu_util import host_bytes
 
 pytestmark = pytest.mark.gpu
 

@@ -5,7 +5,6 @@ byte order, a dropped word, a missing alignment, a wrong index, a salted
 start value ...), builds the copy with gcc and runs every pin against it.
 A mutant that passes all pins would mean the pins cannot see that mistake.
 """
-import os
 import subprocess
 
 import pytest
