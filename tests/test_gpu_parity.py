@@ -30,6 +30,7 @@ if torch.cuda.is_available():
     (8192, 256, 4 * 8192, 0),          # ring of four device slots
     (4096, 256, 12 * 4096, 3 * 4096),  # ring of four slots of three chunks each
     (4096, 256, 4 * 4096, 8 * 4096),   # ring slot size capped at half the ring: two slots of two chunks
+    (4096, 256, 16 * 4096, 0),         # default ring slots: a quarter of the ring, four slots of four chunks
     (1 << 16, 4096, 2 * (1 << 16), 0), # ring of two slots, 4 KiB alignment
     (16, 16, 0, 0),                    # chunk = alignment = one 16-byte vector: 16-byte tiles
     (48, 16, 0, 1 << 16),              # three-vector chunks, 1365 per group
