@@ -20,7 +20,7 @@ library records on its own pack stream around every launch), D2H against the
 host link's measured peak (a plain pinned 1 GiB copy in the same process),
 restore/verify rates, the step-time overhead of snapshots under a bf16 GEMM
 load (one rank of a 65B model under TP=8 x PP=8, GEMM 8192x8192x2752, timed
-per the paper's Sec. VII-A statistic), and the CPU oracle on a bounded sample.
+per the paper's Sec. VII-B per-iteration statistic), and the CPU oracle on a bounded sample.
 """
 import argparse
 import json
@@ -295,7 +295,7 @@ def log(*a):
 
 
 def trimmed_mean(xs, warm=10, drop=0.05):
-    """Paper Sec. VII-A: discard the first 10 iterations, drop the slowest 5%
+    """Paper Sec. VII-B (per-iteration overhead): discard the first 10 iterations, drop the slowest 5%
     of the rest, average."""
     xs = list(xs[warm:]) if len(xs) > warm else list(xs)
     xs.sort()
@@ -429,7 +429,7 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
     is issued right after the previous update.  R is fixed before measuring
     as ceil(ratio * T_D2H / T_GEMM) from the standalone D2H time and the GEMM
     time; the headline uses the first ratio.  Overhead compares the mean step
-    (paper Sec. VII-A statistic) with and without snapshots; the no-snapshot
+    (paper Sec. VII-B per-iteration statistic) with and without snapshots; the no-snapshot
     runs bracket the snapshot run."""
     base_steps = base_steps or steps
     tensors, plan = W.make_state(wid, device="cuda")

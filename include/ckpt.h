@@ -8,7 +8,7 @@
  *     state (optimizer shard, parameter shard, metadata envelope with the
  *     step index, parallel configuration and RNG states) is packed into one
  *     contiguous buffer and copied asynchronously to pinned host memory on a
- *     dedicated stream, so that local recovery needs no network transfer.
+ *     dedicated stream, so that a rank can recover from host memory alone.
  *   - Sec. VI-A: two host buffers alternate roles -- one holds the committed
  *     snapshot of the previous iteration, the other receives the current one
  *     -- so an interrupted offload never destroys the last good snapshot.
@@ -268,8 +268,8 @@ ckpt_status ckpt_debug_tile_plan(const uint64_t* nbytes, uint32_t n, uint64_t ch
                                  uint64_t* tile_bytes, uint64_t* n_tiles, uint32_t* tile_first,
                                  uint32_t* tile_last);
 
-/* ---- Crash-surviving local snapshots (Sec. V-B: the host copy serves fast
- * local recovery without any network transfer; Sec. V-C: a local reset
+/* ---- Crash-surviving local snapshots (Sec. V-B: the host copy lets a
+ * rank come back from its own host memory alone; Sec. V-C: a local reset
  * re-enters as a replacement) ----
  *
  * ckpt_image_file, before ckpt_register_tensors and only in bounce mode
