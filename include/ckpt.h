@@ -107,6 +107,13 @@ typedef struct {
                                       A snapshot then commits when its last group is in the image. */
     uint32_t host_threads;         /* bounce mode: threads moving bytes between rings and images;
                                       0 = 12 */
+    void* side_stream;             /* the dedicated stream of Sec. V-B: a hipStream_t of `device`
+                                      on which the snapshot's pack, chunk-sum and release kernels
+                                      (and the restore's scatter kernels) run.  NULL = the library
+                                      creates its own (non-blocking, default priority).  A caller's
+                                      stream stays the caller's: it must stay valid until
+                                      ckpt_destroy, which does not destroy it, and other work
+                                      queued on it delays the pack.  Ignored by ckpt_peer_create. */
 } ckpt_config;
 
 typedef struct {

@@ -336,6 +336,7 @@ struct ckpt_ctx {
 
     // streams and events
     hipStream_t s_pack = nullptr, s_copy = nullptr;
+    bool own_pack = true; // false: s_pack is the caller's side stream (never destroyed here)
     hipEvent_t ev_trigger = nullptr, ev_done = nullptr;
     std::vector<uint64_t> area_seq;     // per staging area: copies issued out of it
     std::vector<hipEvent_t> area_free;  // restore/verify: per staging area

@@ -707,6 +707,7 @@ void free_ctx(ckpt_ctx* c)
     if (c->h_bin) (void)hipHostFree(c->h_bin);
     if (c->h_bad) (void)hipHostFree(c->h_bad);
     if (c->h_recomputed) (void)hipHostFree(c->h_recomputed);
+    if (!c->own_pack) c->s_pack = nullptr; // the caller's stream
     for (hipStream_t st : {c->s_pack, c->s_copy, c->s_vcopy, c->s_vker})
         if (st) (void)hipStreamDestroy(st);
 }
@@ -805,8 +806,12 @@ ckpt_status ckpt_create(const ckpt_config* cfg, ckpt_ctx** out)
     ckpt_status st = CKPT_OK;
     if (hipSetDevice(c->device) != hipSuccess)
         st = CKPT_EHIP;
+    if (d.side_stream) { // the caller's dedicated stream carries the pack
+        c->s_pack = (hipStream_t)d.side_stream;
+        c->own_pack = false;
+    }
     for (hipStream_t* sp : {&c->s_pack, &c->s_copy, &c->s_vcopy, &c->s_vker})
-        if (st == CKPT_OK && hipStreamCreateWithFlags(sp, hipStreamNonBlocking) != hipSuccess) st = CKPT_EHIP;
+        if (st == CKPT_OK && !*sp && hipStreamCreateWithFlags(sp, hipStreamNonBlocking) != hipSuccess) st = CKPT_EHIP;
     for (hipEvent_t* e : {&c->ev_trigger, &c->ev_done, &c->ev_vdone})
         if (st == CKPT_OK) st = make_event(c, e, false);
     for (hipEvent_t* e : {&c->tt0, &c->tc0, &c->tc1, &c->vt0, &c->vc0, &c->vc1})

@@ -94,3 +94,104 @@ def expected_after_restore(failed_host, before_host, ids, chunk):
             if a < b:
                 out[i][a - int(o):b - int(o)] = img[a:b]
     return out
+
+
+def assert_located(ck, c, chunk, sizes):
+    """Locate (definition 5): the library's byte range of chunk c and its
+    fragment range [f0, f1] must give exactly the oracle's list -- the
+    non-empty fragments inside the range are the fragments overlapping the
+    chunk, no more and no fewer."""
+    lo, hi, f0, f1 = ck.chunk_fragments(c)
+    (olo, ohi), ids = O.locate(c, chunk, ck.image_bytes, ck.offsets, sizes)
+    assert (lo, hi) == (olo, ohi), "chunk %d: byte range %s, oracle %s" % (c, (lo, hi), (olo, ohi))
+    got = [i for i in range(f0, f1 + 1) if sizes[i]]
+    assert got == ids, "chunk %d: fragments %s, oracle %s" % (c, got, ids)
+    return ids
+
+
+def window_slices(tensors, off, sizes, lo, hi):
+    """Host copies of the live fragments' bytes that fall in image bytes
+    [lo, hi), with their image offsets (fragment i's bytes [a, b) sit at
+    image offset off[i] + a).  Copied by torch, outside the library."""
+    import bisect
+
+    offs = [int(o) for o in off]
+    frags, at = [], []
+    i = max(0, bisect.bisect_right(offs, lo) - 1)
+    while i < len(sizes) and offs[i] < hi:
+        o, s = offs[i], int(sizes[i])
+        a, b = max(o, lo) - o, min(o + s, hi) - o
+        if b > a:
+            frags.append(tensors[i].reshape(-1).view(torch.uint8)[a:b].cpu().numpy())
+            at.append(o + a)
+        i += 1
+    return frags, at
+
+
+def check_image_against_oracle(tensors, off, sizes, img, sums, chunk, threads=16):
+    """Every chunk of a committed host image, byte for byte, against the
+    oracle's pack of the live fragments, and every stored sum against the
+    oracle's sum of that chunk.  Streams chunk by chunk (the main thread
+    copies the fragment bytes of a chunk to the host, a pool of threads runs
+    the oracle and compares; the oracle's C calls release the interpreter
+    lock), so it needs no second copy of a shard of tens of GB.  Returns the
+    number of chunks checked."""
+    import os
+    from concurrent.futures import ThreadPoolExecutor
+
+    I = img.size
+    nc = (I + chunk - 1) // chunk
+    assert sums.size == nc
+
+    def check(c, frags, at):
+        lo, hi = c * chunk, min((c + 1) * chunk, I)
+        want = O.pack_window(frags, at, lo, hi)
+        if not np.array_equal(img[lo:hi], want):
+            d = np.flatnonzero(img[lo:hi] != want)
+            return "chunk %d differs from the oracle at %d bytes, first at image byte %d" % (c, d.size, lo + d[0])
+        s = int(O.chunk_sums(want, lo, hi, chunk)[0])
+        if s != int(sums[c]):
+            return "chunk %d: stored sum %#x, oracle %#x" % (c, int(sums[c]), s)
+        return None
+
+    workers = max(1, min(threads, os.cpu_count() or 1))
+    pending = []
+    errors = []
+    with ThreadPoolExecutor(workers) as ex:
+        for c in range(nc):
+            lo, hi = c * chunk, min((c + 1) * chunk, I)
+            frags, at = window_slices(tensors, off, sizes, lo, hi)
+            pending.append(ex.submit(check, c, frags, at))
+            if len(pending) >= 2 * workers:  # bound the host memory in flight
+                r = pending.pop(0).result()
+                if r:
+                    errors.append(r)
+        errors += [r for r in (f.result() for f in pending) if r]
+    assert not errors, "%d chunks wrong; %s" % (len(errors), "; ".join(errors[:4]))
+    return nc
+
+
+def fragment_digests(tensors, piece=1 << 26):
+    """Per-fragment digest computed by torch on the GPU (independent of the
+    library): byte count, the sum of the fragment's 32-bit words (bytes when
+    its length is not a multiple of 4) and their sum weighted by position
+    (weights 1..65521, so moved or swapped words change it).  int64
+    arithmetic wraps the same way every time, so equal bytes give equal
+    digests."""
+    out = []
+    for t in tensors:
+        b = t.reshape(-1).view(torch.uint8)
+        n = b.numel()
+        if n == 0:
+            out.append((0, 0, 0))
+            continue
+        w = b.view(torch.int32) if n % 4 == 0 else b
+        s1 = torch.zeros((), dtype=torch.int64, device=b.device)
+        s2 = torch.zeros((), dtype=torch.int64, device=b.device)
+        for k in range(0, w.numel(), piece):
+            x = w[k:k + piece].to(torch.int64)
+            pos = torch.arange(k, k + x.numel(), dtype=torch.int64, device=b.device) % 65521 + 1
+            s1 += x.sum()
+            s2 += (x * pos).sum()
+        out.append((n, int(s1), int(s2)))
+    return out

@@ -1,10 +1,11 @@
 """Full-size shards against the oracle (needs an MI355X; tens of seconds each).
 
-At these sizes the oracle cannot pack the whole shard quickly, so the checks
-are: sampled chunks packed by the oracle from the live fragments and compared
-byte for byte with the committed host image; the oracle's sums of every chunk
-of the host image against the stored sums; and, where device memory allows, a
-full restore compared with device copies taken before the snapshot.
+Every chunk of the committed host image is compared byte for byte with the
+oracle's pack of the live fragments, and every stored sum with the oracle's
+sum of that chunk, streamed chunk by chunk over a pool of host threads
+(gpu_util.check_image_against_oracle).  The restore is compared with device
+copies taken before the snapshot where device memory allows, else with
+per-fragment digests taken by torch before the snapshot.
 """
 import gc
 
@@ -14,6 +15,7 @@ import torch
 
 import oracle as O
 import workloads as W
+from gpu_util import assert_located, check_image_against_oracle, fragment_digests
 
 pytestmark = pytest.mark.gpu
 
@@ -29,32 +31,17 @@ def release_memory():
         torch.cuda.empty_cache()
 
 
-def sample_chunks(n_chunks, k=6, seed=77):
-    rng = np.random.default_rng(seed)
-    picks = {0, n_chunks - 1} | {int(x) for x in rng.integers(0, n_chunks, k)}
-    return sorted(picks)
-
-
-def oracle_window(tensors, off, sizes, lo, hi):
-    """The oracle's pack of image bytes [lo, hi), fed with the overlapping
-    slices of the live fragments (fragment i's bytes [a, b) placed at image
-    offset off[i] + a)."""
-    frags, offs = [], []
-    for i, s in enumerate(sizes):
-        o = int(off[i])
-        a, b = max(o, lo) - o, min(o + s, hi) - o
-        if b > a:
-            frags.append(tensors[i].reshape(-1).view(torch.uint8)[a:b].cpu().numpy())
-            offs.append(o + a)
-    return O.pack_window(frags, offs, lo, hi)
-
-
-def check_shard(wid, staging=0, full_restore=True, all_sums=True, bounce=0):
+def check_shard(wid, staging=0, full_restore=True, bounce=0, digests=False):
+    """Snapshot workload wid, check every chunk and sum against the oracle,
+    verify, then trash the tensors, restore and check every fragment: against
+    device copies (full_restore) or against torch digests taken before the
+    snapshot (digests; for shards too large to copy on the device)."""
     tensors, plan = W.make_state(wid, device="cuda")
     sizes = [p[1] for p in plan]
     chunk = W.WORKLOADS[wid]["chunk"]
     torch.cuda.synchronize()
     before = [t.clone() for t in tensors] if full_restore else None
+    dig = fragment_digests(tensors) if digests else None
     ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=chunk,
                         device_staging_bytes=staging, bounce_bytes=bounce)
     off, I, nc = O.layout(sizes, 256, chunk)
@@ -62,21 +49,20 @@ def check_shard(wid, staging=0, full_restore=True, all_sums=True, bounce=0):
     snap = ck.snapshot(step=wid)
     ck.wait_committed(snap)
     img, sums = ck.host_image(snap)
-    for c in sample_chunks(nc):
-        lo, hi = c * chunk, min((c + 1) * chunk, I)
-        want = oracle_window(tensors, off, sizes, lo, hi)
-        assert np.array_equal(img[lo:hi], want), "chunk %d differs" % c
-        assert int(sums[c]) == int(O.chunk_sums(want, lo, hi, chunk)[0])
-    if all_sums:
-        assert np.array_equal(sums, O.chunk_sums(img, 0, I, chunk))
+    assert check_image_against_oracle(tensors, off, sizes, img, sums, chunk) == nc
     assert ck.verify(snap) == []
-    if full_restore:
+    if full_restore or digests:
         for t in tensors:
             t.view(-1).view(torch.uint8).fill_(0x3C)
         assert ck.restore(snap) == []
         torch.cuda.synchronize()
+    if full_restore:
         for i, (t, b) in enumerate(zip(tensors, before)):
             assert torch.equal(t.view(-1).view(torch.uint8), b.view(-1).view(torch.uint8)), "fragment %d" % i
+    if digests:
+        after = fragment_digests(tensors)
+        wrong = [i for i, (a, b) in enumerate(zip(dig, after)) if a != b]
+        assert not wrong, "%d fragments not restored, first %d" % (len(wrong), wrong[0])
     return ck, tensors, plan, snap
 
 
@@ -123,9 +109,7 @@ def test_stress_4096_fragments_with_flips():
         k = 8 * (byte % 8) + bit
         was_set = (int(img[byte]) >> bit) & 1 == 0
         assert (int(recomputed[c]) - int(stored[c])) % (1 << 64) == ((-(1 << k)) % (1 << 64) if was_set else 1 << k)
-        lo, hi, f0, f1 = ck.chunk_fragments(c)
-        (olo, ohi), ids = O.locate(c, chunk, ck.image_bytes, ck.offsets, sizes)
-        assert (lo, hi) == (olo, ohi) and ids and f0 <= min(ids) and max(ids) <= f1
+        assert assert_located(ck, c, chunk, sizes)
     ck.close()
 
 
@@ -152,13 +136,8 @@ def test_fragment_beyond_4_gib(shift):
     snap = ck.snapshot(step=1)
     ck.wait_committed(snap)
     img, sums = ck.host_image(snap)
-    x = int(off[1]) + (1 << 32)  # image byte of the big fragment's byte 2^32
-    picks = sorted({0, (x - 8) // chunk, x // chunk, (int(off[1]) + n - 1) // chunk, nc - 1})
-    for c in picks:
-        lo, hi = c * chunk, min((c + 1) * chunk, I)
-        want = oracle_window(tensors, off, sizes, lo, hi)
-        assert np.array_equal(img[lo:hi], want), "chunk %d differs" % c
-    assert np.array_equal(sums, O.chunk_sums(img, 0, I, chunk))
+    # every chunk, including those around the big fragment's byte 2^32
+    assert check_image_against_oracle(tensors, off, sizes, img, sums, chunk) == nc
     assert ck.verify(snap) == []
     for t in tensors:
         t.view(-1).view(torch.uint8).fill_(0x3C)

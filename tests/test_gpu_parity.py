@@ -13,7 +13,8 @@ import torch
 
 import oracle as O
 import workloads as W
-from gpu_util import EDGE_SIZES, garbage_fill, host_bytes, random_byte_fragments, snapshot_and_check
+from gpu_util import (EDGE_SIZES, assert_located, garbage_fill, host_bytes, random_byte_fragments,
+                      snapshot_and_check)
 
 pytestmark = pytest.mark.gpu
 
@@ -179,9 +180,7 @@ def test_single_bit_flips_are_reported_and_located():
         was_set = (int(flipped[byte]) >> bit) & 1 == 0  # bit value before the flip
         delta = (int(recomputed[c]) - int(stored[c])) % (1 << 64)
         assert delta == ((-(1 << k)) % (1 << 64) if was_set else (1 << k))
-        lo, hi, f0, f1 = ck.chunk_fragments(c)
-        (olo, ohi), ids = O.locate(c, chunk, ck.image_bytes, ck.offsets, sizes)
-        assert (lo, hi) == (olo, ohi) and f0 <= min(ids) and max(ids) <= f1
+        assert assert_located(ck, c, chunk, sizes)
     garbage_fill(tensors)
     assert ck.restore(snap) == want_bad  # every byte is still written back
     torch.cuda.synchronize()
@@ -213,13 +212,23 @@ def _hold(stream, ms=40.0):
     return b
 
 
-def test_gate_orders_optimizer_after_capture():
+# Staging modes of the gate tests: the full device image (the gate waits for
+# the pack only) and a ring of four 4 MiB slots over the 384 MiB state (each
+# slot is reused only after its previous group has been copied to the host,
+# so the capture of the later chunks is paced by the D2H).
+GATE_STAGING = [0, 16 << 20]
+GATE_CHUNK = 1 << 20
+
+
+@pytest.mark.parametrize("staging", GATE_STAGING)
+def test_gate_orders_optimizer_after_capture(staging):
     """The wait before the optimizer step: an in-place update launched on
     another stream right after ckpt_wait(CAPTURED) must not leak into the
     snapshot, although the snapshot's trigger sits behind ~40 ms of work on
-    the training stream, so its pack starts long after the update could."""
+    the training stream, so its pack starts long after the update could.
+    Whole range, then a partial range [0, 8) that protects only those."""
     tensors = _step_state(n_frag=96)
-    ck = P.Checkpointer(tensors, chunk_bytes=1 << 20)
+    ck = P.Checkpointer(tensors, chunk_bytes=GATE_CHUNK, device_staging_bytes=staging)
     main, side = torch.cuda.current_stream(), torch.cuda.Stream()
     torch.cuda.synchronize()
     before = [host_bytes(t) for t in tensors]
@@ -230,10 +239,10 @@ def test_gate_orders_optimizer_after_capture():
         for t in tensors:
             t.add_(1.0)  # the "optimizer step"
     ck.wait_committed(s)
-    img, _ = ck.host_image(s)
-    want, _, _ = O.pack(before, 256, 1 << 20)
+    img, sums = ck.host_image(s)
+    want, _, _ = O.pack(before, 256, GATE_CHUNK)
     assert np.array_equal(img, want)
-    # Partial gate: waiting only for fragments [0, 8) protects those.
+    assert np.array_equal(sums, O.chunk_sums(want, 0, want.size, GATE_CHUNK))
     torch.cuda.synchronize()
     before = [host_bytes(t) for t in tensors]
     keep = _hold(main)
@@ -253,12 +262,13 @@ def test_gate_orders_optimizer_after_capture():
     ck.close()
 
 
-def test_gate_negative_control_detects_the_race():
+@pytest.mark.parametrize("staging", GATE_STAGING)
+def test_gate_negative_control_detects_the_race(staging):
     """Same without the wait: the update on the other stream runs while the
     pack still waits for its trigger, so the snapshot holds updated values.
     Shows the gate test can see a missing wait."""
     tensors = _step_state(n_frag=96)
-    ck = P.Checkpointer(tensors, chunk_bytes=1 << 20)
+    ck = P.Checkpointer(tensors, chunk_bytes=GATE_CHUNK, device_staging_bytes=staging)
     main, side = torch.cuda.current_stream(), torch.cuda.Stream()
     torch.cuda.synchronize()
     before = [host_bytes(t) for t in tensors]
@@ -269,11 +279,129 @@ def test_gate_negative_control_detects_the_race():
             t.add_(1.0)  # no ckpt_wait: runs before the delayed pack
     ck.wait_committed(s)
     img, _ = ck.host_image(s)
-    want, _, _ = O.pack(before, 256, 1 << 20)
+    want, _, _ = O.pack(before, 256, GATE_CHUNK)
     assert not np.array_equal(img, want)
     torch.cuda.synchronize()
     del keep
     ck.close()
+
+
+def test_ring_gate_covers_only_its_range():
+    """Ring staging: the capture of the last chunks waits for ring slots to
+    come back from the host link, so a wait on fragments [0, 8) (captured
+    first) does not cover the last eight fragments.  Updating those after
+    that wait races the D2H-paced pack and reaches the image; updating them
+    after a wait on their own range does not.  Shows that in ring mode the
+    gate's range decides what is protected."""
+    tensors = _step_state(n_frag=96)
+    ck = P.Checkpointer(tensors, chunk_bytes=GATE_CHUNK, device_staging_bytes=16 << 20)
+    side = torch.cuda.Stream()
+    n = len(tensors)
+    for lo, hi, leaks in [(0, 8, True), (n - 8, n, False)]:
+        torch.cuda.synchronize()
+        before = [host_bytes(t) for t in tensors]
+        s = ck.snapshot(step=lo)
+        ck.wait_captured(s, lo, hi, stream=side)
+        with torch.cuda.stream(side):
+            for t in tensors[n - 8:]:
+                t.add_(1.0)
+        ck.wait_committed(s)
+        torch.cuda.synchronize()
+        img, _ = ck.host_image(s)
+        off = ck.offsets
+        same = all(np.array_equal(img[int(off[i]):int(off[i]) + before[i].size], before[i]) for i in range(n - 8, n))
+        assert same != leaks, "gate on [%d, %d): last fragments %s" % (lo, hi, "protected" if same else "updated")
+        # the chunks before the updated fragments hold the state of the trigger either way
+        o = int(off[n - 8])
+        want, _, _ = O.pack(before, 256, GATE_CHUNK)
+        assert np.array_equal(img[:o], want[:o])
+    ck.close()
+
+
+@pytest.mark.parametrize("staging", GATE_STAGING)
+def test_trigger_captures_writes_queued_before_it(staging):
+    """The trigger (row a2): a snapshot issued on after_stream is ordered after
+    the work already enqueued there.  An in-place update of every registered
+    tensor is queued on the training stream behind ~40 ms of other work; the
+    snapshot call returns while that update is still pending, and the
+    committed image must equal the oracle's pack of the updated bytes."""
+    tensors = _step_state(n_frag=96)
+    ck = P.Checkpointer(tensors, chunk_bytes=GATE_CHUNK, device_staging_bytes=staging)
+    main = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+    before = [host_bytes(t) for t in tensors]
+    keep = _hold(main)
+    for t in tensors:
+        t.add_(1.0)  # queued on main behind the hold
+    updated = torch.cuda.Event()
+    updated.record(main)
+    s = ck.snapshot(step=1, stream=main)
+    assert not updated.query(), "the update ran before the snapshot call returned; the test proves nothing"
+    ck.wait_committed(s)
+    torch.cuda.synchronize()
+    after = [host_bytes(t) for t in tensors]
+    img, sums = ck.host_image(s)
+    want, _, _ = O.pack(after, 256, GATE_CHUNK)
+    assert np.array_equal(img, want)
+    assert np.array_equal(sums, O.chunk_sums(want, 0, want.size, GATE_CHUNK))
+    assert not np.array_equal(want, O.pack(before, 256, GATE_CHUNK)[0])
+    del keep
+    ck.close()
+
+
+def test_trigger_negative_control_on_an_idle_stream():
+    """Same, with the snapshot issued on an idle stream: nothing orders it
+    after the update pending on the training stream, so it packs the bytes
+    from before the update.  Shows the trigger test can see a missing order."""
+    tensors = _step_state(n_frag=96)
+    ck = P.Checkpointer(tensors, chunk_bytes=GATE_CHUNK)
+    main, idle = torch.cuda.current_stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    before = [host_bytes(t) for t in tensors]
+    keep = _hold(main)
+    for t in tensors:
+        t.add_(1.0)
+    s = ck.snapshot(step=1, stream=idle)
+    ck.wait_committed(s)
+    img, _ = ck.host_image(s)
+    want, _, _ = O.pack(before, 256, GATE_CHUNK)
+    assert np.array_equal(img, want)
+    torch.cuda.synchronize()
+    del keep
+    ck.close()
+
+
+def test_side_stream_carries_the_pack():
+    """ckpt_config.side_stream: the pack runs on the caller's stream, behind
+    what the caller queued there.  With ~40 ms of work on that stream, the
+    pack comes after an (ungated) update queued 5 ms later on the training
+    stream, so the image holds the updated bytes; with the library's own
+    stream the pack ran at once and holds the bytes from before.  The
+    caller's stream outlives the context."""
+    tensors = _step_state(n_frag=48)
+    main = torch.cuda.current_stream()
+    for use_side in (False, True):
+        side = torch.cuda.Stream()
+        ck = P.Checkpointer(tensors, chunk_bytes=GATE_CHUNK, side_stream=side if use_side else None)
+        torch.cuda.synchronize()
+        before = [host_bytes(t) for t in tensors]
+        keep_side = _hold(side)
+        s = ck.snapshot(step=1, stream=main)
+        keep_main = _hold(main, 5.0)
+        for t in tensors:
+            t.add_(1.0)  # not gated: ordered only by where the pack runs
+        ck.wait_committed(s)
+        torch.cuda.synchronize()
+        after = [host_bytes(t) for t in tensors]
+        img, sums = ck.host_image(s)
+        want, _, _ = O.pack(after if use_side else before, 256, GATE_CHUNK)
+        assert np.array_equal(img, want), "side stream %s" % use_side
+        assert np.array_equal(sums, O.chunk_sums(want, 0, want.size, GATE_CHUNK))
+        ck.close()
+        with torch.cuda.stream(side):  # still the caller's
+            keep_side = keep_side + 1.0
+        side.synchronize()
+        del keep_side, keep_main
 
 
 def test_interrupted_snapshot_is_never_restored():
