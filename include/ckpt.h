@@ -471,7 +471,46 @@ ckpt_status ckpt_restore_from_peer(ckpt_ctx* ctx, const char* host, uint32_t por
 ckpt_status ckpt_peer_restore_info(ckpt_ctx* ctx, uint64_t* ids, uint64_t cap, uint64_t* n_ids, void* envelope,
                                    uint64_t env_cap, uint64_t* env_len, double* fetch_ms, double* check_ms);
 
-/* Text of the context's last error ("" if none).  Valid until the next call. */
+/* ---- Allocation-free pack, for callers that cannot allocate (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc) ----
+ *
+ * ckpt_pack_noalloc: the pack and per-chunk sums of ckpt_snapshot_async --
+ * the same kernels, layout and sums -- into a device image the caller owns,
+ * with no context and no allocation: no hipMalloc, hipFree, pinned or
+ * pageable allocation of any kind.  Nothing is copied to the host.
+ *   t, n          fragment descriptors in layout order (host array; read
+ *                 before the call returns); each non-empty one must be
+ *                 memory of `device` inside one allocation.
+ *   chunk_bytes, align_bytes   as in ckpt_config (0 = 64 MiB / 256).
+ *   device        HIP device ordinal; the caller's current device is
+ *                 restored before the call returns.
+ *   image         device memory of `device`, 16-byte aligned, image_cap
+ *                 bytes; receives image bytes [0, *image_bytes) (fragment
+ *                 bytes and zero padding); bytes past that are not touched.
+ *   sums          device memory of `device`, 8-byte aligned, sums_cap
+ *                 entries; receives the *n_chunks chunk sums.
+ *   stream        hipStream_t of `device` (NULL = null stream); the work is
+ *                 enqueued on it and the call returns without waiting.
+ *   image_bytes, n_chunks      host outputs (may be NULL), also set when the
+ *                 capacities are too small.
+ * The library keeps the fragment table, the tile table and the partial sums
+ * in one fixed 7 MiB device array per GPU (held until the process ends).
+ * Limits: at most 65536 fragments, chunks of at most 1 GiB (at 8 KiB tiles);
+ * the image may be any size (it is packed in groups of at most 1 GiB that
+ * reuse the array).  Every call on a GPU uses that GPU's array: calls whose
+ * work overlaps on one GPU (different streams, not ordered by events) race
+ * and give wrong sums; order them, e.g. one stream.
+ * Errors: EINVAL (null pointer, n == 0 or above 65536, bad geometry, chunk
+ * above the limit, image_cap / sums_cap too small, misaligned image or sums,
+ * or memory that is not `device`'s or runs past its allocation; nothing is
+ * enqueued), EHIP (a launch failed).  Text: ckpt_last_error(NULL) on the
+ * same thread. */
+ckpt_status ckpt_pack_noalloc(const ckpt_tensor* t, uint32_t n, uint64_t chunk_bytes, uint32_t align_bytes,
+                              int32_t device, void* image, uint64_t image_cap, uint64_t* sums, uint64_t sums_cap,
+                              void* stream, uint64_t* image_bytes, uint64_t* n_chunks);
+
+/* Text of the context's last error ("" if none).  Valid until the next call.
+ * With NULL: the text of this thread's last failed ckpt_pack_noalloc. */
 const char* ckpt_last_error(const ckpt_ctx* ctx);
 
 #ifdef __cplusplus

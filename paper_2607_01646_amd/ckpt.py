@@ -122,6 +122,7 @@ def lib():
             "ckpt_restore_from_peer": ([vp, C.c_char_p, u32, vp, P(u64), P(u64), P(u32), u32, P(u32)], i32),
             "ckpt_peer_restore_info": ([vp, P(u64), u64, P(u64), vp, u64, P(u64), P(C.c_double), P(C.c_double)],
                                        i32),
+            "ckpt_pack_noalloc": ([P(ckpt_tensor), u32, u64, u32, i32, vp, u64, vp, u64, vp, P(u64), P(u64)], i32),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -424,6 +425,29 @@ def ckpt_peer_restore_info(ctx):
                                              C.byref(fetch), C.byref(check)))
     return {"chunk_ids": ids[:n.value], "envelope": env.raw[:elen.value], "fetch_ms": fetch.value,
             "check_ms": check.value}
+
+
+def ckpt_pack_noalloc(tensors, image, sums, chunk_bytes=0, align_bytes=0, stream=None, device=None):
+    """Allocation-free pack of `tensors` into the device tensors `image`
+    (uint8) and `sums` (int64/uint64, one per chunk) on `stream`; returns
+    (image_bytes, n_chunks).  Asynchronous like a kernel launch."""
+    if device is None:
+        device = torch.cuda.current_device()
+    n = len(tensors)
+    arr = (ckpt_tensor * max(n, 1))()
+    for i, t in enumerate(tensors):
+        if not t.is_cuda:
+            raise ValueError("fragment %d is not a device tensor" % i)
+        nb = tensor_bytes(t)
+        arr[i].dev_ptr = t.data_ptr() if nb else None
+        arr[i].nbytes = nb
+    ib, nc = C.c_uint64(), C.c_uint64()
+    rc = lib().ckpt_pack_noalloc(arr, n, chunk_bytes, align_bytes, device, C.c_void_p(image.data_ptr()),
+                                 image.numel() * image.element_size(), C.c_void_p(sums.data_ptr()),
+                                 sums.numel() * sums.element_size() // 8, _stream(stream), C.byref(ib), C.byref(nc))
+    if rc != CKPT_OK:
+        raise CkptError(rc, (lib().ckpt_last_error(None) or b"").decode())
+    return ib.value, nc.value
 
 
 class PeerError(RuntimeError):

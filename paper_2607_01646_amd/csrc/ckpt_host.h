@@ -410,6 +410,9 @@ const char* hsa_text(hsa_status_t s);
     } while (0)
 
 uint64_t round_up(uint64_t x, uint64_t a);
+bool geometry_ok(uint64_t C, uint32_t A);
+// Text of this thread's last failed ckpt_pack_noalloc ("" if none).
+const char* noalloc_error();
 
 // Snapshot records (ckpt_runtime.cpp)
 ckpt_status get_res(ckpt_ctx* c, RecRes** out);

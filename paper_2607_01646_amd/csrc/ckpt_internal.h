@@ -64,4 +64,47 @@ hipError_t launch_chunk_reduce(const Geometry& g, uint64_t t_lo, uint64_t t_hi, 
 // on s before this call has completed.
 hipError_t launch_release(int64_t* signal_value, hipStream_t s);
 
+// ---- The allocation-free pack (ckpt_pack_noalloc) ----
+// Its tables and partial sums live in a fixed device array of the kernel
+// file (one per GPU, held until the process ends), laid out as: the fragment
+// table (at most kNoallocMaxFrags entries), then the first- and
+// last-fragment tables of one group of at most kNoallocGroupTiles tiles, then
+// that group's partial sums.  Groups are whole chunks and are packed one
+// after another on the caller's stream, reusing the tables.
+constexpr uint32_t kNoallocMaxFrags = 65536;
+constexpr uint64_t kNoallocGroupTiles = 131072; // 1 GiB of 8 KiB tiles
+constexpr uint64_t kNoallocFragsOff = 0;
+constexpr uint64_t kNoallocFirstOff = kNoallocFragsOff + (uint64_t)kNoallocMaxFrags * sizeof(FragDev);
+constexpr uint64_t kNoallocLastOff = kNoallocFirstOff + kNoallocGroupTiles * 4;
+constexpr uint64_t kNoallocPartialsOff = kNoallocLastOff + kNoallocGroupTiles * 4;
+constexpr uint64_t kNoallocScratchBytes = kNoallocPartialsOff + kNoallocGroupTiles * kTileParts * 8; // 7 MiB
+// Fragment descriptors per upload launch (they travel as kernel arguments).
+constexpr uint32_t kUploadBatch = 96;
+
+// Device address of the current device's scratch array, looked up once per
+// device with that device current (the array's host-side name is only a
+// handle, never a device address).
+hipError_t noalloc_scratch(uint8_t** ptr);
+
+// Write descriptors src[0, count) (host memory, count <= kUploadBatch) to
+// dst[0, count) on the device, in stream order, through kernel arguments.
+hipError_t launch_frag_upload(FragDev* dst, const FragDev* src, uint32_t count, hipStream_t s);
+
+// Tile table of tiles [t_lo, t_hi) over the n fragments in frags (device):
+// first[t - t_lo] / last[t - t_lo] = first / last fragment holding a byte of
+// tile t (the first fragment whose padded span ends past the tile's first /
+// last byte; the last fragment when none does), as the runtime's host planner
+// computes it.
+hipError_t launch_tile_table(const FragDev* frags, uint32_t n, const Geometry& g, uint64_t t_lo, uint64_t t_hi,
+                             uint32_t* first, uint32_t* last, hipStream_t s);
+
+// Tile size rule shared by the planners: the largest power of two no larger
+// than 1 << kMaxTileShift (and at least 16) that divides the chunk size.
+inline uint32_t tile_shift_for(uint64_t chunk_bytes)
+{
+    uint32_t ts = 4;
+    while (ts < kMaxTileShift && chunk_bytes % (1ull << (ts + 1)) == 0) ++ts;
+    return ts;
+}
+
 } // namespace ckpt

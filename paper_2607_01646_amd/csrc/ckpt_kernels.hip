@@ -35,6 +35,8 @@
 // tiles gives the same bits.
 #include <hip/hip_ext.h>
 
+#include <mutex>
+
 #include "ckpt_internal.h"
 
 namespace ckpt {
@@ -424,7 +426,93 @@ __global__ void release_signal_kernel(int64_t* value)
     __hip_atomic_store(value, (int64_t)0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
+// ---- allocation-free pack: scratch, table upload, tile table ----
+
+struct FragBatch {
+    uint32_t count;
+    FragDev f[kUploadBatch];
+};
+
+__global__ __launch_bounds__(128) void frag_upload_kernel(FragDev* dst, FragBatch b)
+{
+    const uint32_t k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k < b.count) dst[k] = b.f[k];
+}
+
+// One lane per tile: binary search for the first fragment whose padded span
+// [off, end) ends past the tile's first byte, and for the first one ending
+// past its last byte (end[] never decreases; empty fragments have empty spans).
+__global__ __launch_bounds__(256) void tile_table_kernel(const FragDev* frags, uint32_t n, Geometry g, uint64_t t_lo,
+                                                         uint64_t t_hi, uint32_t* first, uint32_t* last)
+{
+    const uint64_t t = t_lo + (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= t_hi) return;
+    const uint64_t x0 = t << g.tile_shift;
+    uint64_t x1 = x0 + (1ull << g.tile_shift);
+    if (x1 > g.image_bytes) x1 = g.image_bytes;
+    --x1;
+    uint32_t r[2];
+    const uint64_t xs[2] = {x0, x1};
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        uint32_t lo = 0, hi = n - 1; // the answer lies in [lo, hi]; n - 1 when no span ends past x
+        while (lo < hi) {
+            const uint32_t mid = lo + ((hi - lo) >> 1);
+            if (frags[mid].end > xs[k]) hi = mid;
+            else lo = mid + 1;
+        }
+        r[k] = lo;
+    }
+    first[t - t_lo] = r[0];
+    last[t - t_lo] = r[1];
+}
+
+// The scratch of ckpt_pack_noalloc (layout in ckpt_internal.h).  Host code
+// reaches it only through the address noalloc_scratch() looks up.
+static __device__ __align__(256) uint8_t scratch[kNoallocScratchBytes];
+
 } // namespace
+
+hipError_t noalloc_scratch(uint8_t** ptr)
+{
+    constexpr int kMaxDevices = 64;
+    static std::mutex m;
+    static uint8_t* addr[kMaxDevices] = {};
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> l(m);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[dev] = (uint8_t*)p;
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
+}
+
+hipError_t launch_frag_upload(FragDev* dst, const FragDev* src, uint32_t count, hipStream_t s)
+{
+    if (count == 0) return hipSuccess;
+    if (count > kUploadBatch) return hipErrorInvalidValue;
+    FragBatch b;
+    b.count = count;
+    for (uint32_t k = 0; k < count; ++k) b.f[k] = src[k];
+    hipLaunchKernelGGL(frag_upload_kernel, dim3(1), dim3(128), 0, s, dst, b);
+    return hipGetLastError();
+}
+
+hipError_t launch_tile_table(const FragDev* frags, uint32_t n, const Geometry& g, uint64_t t_lo, uint64_t t_hi,
+                             uint32_t* first, uint32_t* last, hipStream_t s)
+{
+    if (t_hi <= t_lo || n == 0) return hipSuccess;
+    const uint64_t nt = t_hi - t_lo;
+    hipLaunchKernelGGL(tile_table_kernel, dim3((uint32_t)((nt + 255) / 256)), dim3(256), 0, s, frags, n, g, t_lo, t_hi,
+                       first, last);
+    return hipGetLastError();
+}
 
 hipError_t launch_release(int64_t* signal_value, hipStream_t s)
 {

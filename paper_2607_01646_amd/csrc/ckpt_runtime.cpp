@@ -91,8 +91,7 @@ bool plan(const uint64_t* nb, uint32_t n, uint64_t C, uint32_t A, Plan* p, bool 
     for (uint32_t i = 0; i < n; ++i) p->end[i] = (i + 1 < n) ? p->off[i + 1] : p->I;
     p->n_chunks = (p->I + C - 1) / C;
     // Tiles: the largest power of two <= 8 KiB dividing the chunk size.
-    uint32_t ts = 4;
-    while (ts < kMaxTileShift && C % (1ull << (ts + 1)) == 0) ++ts;
+    const uint32_t ts = tile_shift_for(C);
     p->tile_shift = ts;
     p->n_tiles = (p->I + (1ull << ts) - 1) >> ts;
     if (!tiles) return true;
@@ -1525,6 +1524,6 @@ ckpt_status ckpt_latest(ckpt_ctx* c, uint64_t* snap_id, uint64_t* step)
     }
     return CKPT_OK;
 }
-const char* ckpt_last_error(const ckpt_ctx* c) { return c ? c->err.c_str() : "null context"; }
+const char* ckpt_last_error(const ckpt_ctx* c) { return c ? c->err.c_str() : noalloc_error(); }
 
 } // extern "C"

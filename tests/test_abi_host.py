@@ -113,3 +113,46 @@ def test_create_without_gpu_fails_cleanly(P):
         pytest.skip("a GPU is present")
     with pytest.raises(P.CkptError):
         P.ckpt_create(device=0)
+
+
+def test_noalloc_pack_sizes_its_image_like_the_oracle(P):
+    """ckpt_pack_noalloc computes its layout in two passes without any table;
+    with capacities of zero it stops before touching a device and reports
+    the image size and chunk count, which must be the oracle's."""
+    import ctypes as C
+
+    rng = np.random.default_rng(11)
+    fake = 0x10000  # never dereferenced: the call returns before any device work
+    for A, Cb in [(256, 4 << 20), (256, 768), (16, 64), (4096, 8192)]:
+        for _ in range(10):
+            n = int(rng.integers(1, 200))
+            sizes = [int(s) for s in rng.integers(0, 9000, n)]
+            sizes[0] = max(sizes[0], 1)
+            arr = (P.ckpt_tensor * n)()
+            for i, s in enumerate(sizes):
+                arr[i].dev_ptr = fake if s else None
+                arr[i].nbytes = s
+            ib, nc = C.c_uint64(), C.c_uint64()
+            rc = P.lib().ckpt_pack_noalloc(arr, n, Cb, A, 0, C.c_void_p(fake), 0, C.c_void_p(fake), 0, None,
+                                           C.byref(ib), C.byref(nc))
+            assert rc == P.CKPT_EINVAL and b"needs" in P.lib().ckpt_last_error(None)
+            _, I, n_chunks = O.layout(sizes, A, Cb)
+            assert (ib.value, nc.value) == (I, n_chunks)
+
+
+def test_noalloc_pack_refuses_what_exceeds_its_scratch(P):
+    import ctypes as C
+
+    fake = 0x10000
+    arr = (P.ckpt_tensor * 65537)()
+    ib, nc = C.c_uint64(), C.c_uint64()
+    args = (C.c_void_p(fake), 1 << 40, C.c_void_p(fake), 1 << 30, None, C.byref(ib), C.byref(nc))
+    assert P.lib().ckpt_pack_noalloc(arr, 65537, 0, 0, 0, *args) == P.CKPT_EINVAL
+    assert b"at most 65536" in P.lib().ckpt_last_error(None)
+    arr[0].dev_ptr, arr[0].nbytes = fake, 100
+    assert P.lib().ckpt_pack_noalloc(arr, 1, 2 << 30, 0, 0, *args) == P.CKPT_EINVAL
+    assert b"1 GiB" in P.lib().ckpt_last_error(None)
+    assert P.lib().ckpt_pack_noalloc(arr, 1, 1000, 256, 0, *args) == P.CKPT_EINVAL  # chunk not a multiple of 256
+    assert P.lib().ckpt_pack_noalloc(arr, 1, 0, 0, 0, C.c_void_p(fake + 8), 1 << 40, C.c_void_p(fake), 1 << 30, None,
+                                     C.byref(ib), C.byref(nc)) == P.CKPT_EINVAL
+    assert b"aligned" in P.lib().ckpt_last_error(None)
