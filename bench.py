@@ -1,26 +1,35 @@
 """Benchmark of the in-memory snapshot hot path on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--no-overlap] [--no-cpu]
+    python bench.py [--steps K] [--warmup W] [--no-overlap] [--no-cpu] [--gating]
 
-One step is one pass of the whole path over one rank's state shard (the
-24-layer, hidden-2048 GPT shard: 1168 fragments, 18.42 GB of bf16 params,
-fp32 master weights and Adam moments, 64 MiB chunks):
-  snapshot = pack + chunk sums (HBM -> HBM staging) -> chunked D2H into the
-             pinned ping-pong image -> commit         (paper Sec. V-B, VI-A)
-  gate     = the wait before the optimizer step      (paper Sec. VI-A)
-  verify   = H2D + re-check every chunk sum, of the previous step's committed
-             snapshot, while this step's snapshot streams out (the host link
-             is full duplex; the first step verifies its own snapshot)
+One step is one pass of the whole path over one rank's state shard -- by
+default the 7B LLaMA shard (32 layers, hidden 4096, FFN 11008: 1164
+fragments, 94.3 GB of bf16 params, fp32 master weights and Adam moments,
+64 MiB chunks), whose two host images are pageable memory behind 8 GiB
+pinned bounce rings:
+  update   = an optimizer-like update of every fragment, in buckets, each
+             behind the wait on exactly the chunks it overwrites
+                                                        (paper Sec. VI-A)
+  snapshot = triggered right after the update: pack + chunk sums (HBM ->
+             HBM staging) -> chunked D2H -> commit     (paper Sec. V-B, VI-A)
+  verify   = H2D + re-check every chunk sum, of the previous step's
+             committed snapshot, while this step's snapshot streams out (the
+             host link is full duplex; the first step verifies its own)
   restore  = H2D + scatter into the tensors + re-check every chunk sum
 The state is generated on the GPU before timing starts.  Prints one JSON
-line; `value` is payload bytes per second through that whole cycle.
+line; `value` is the snapshot rate: payload bytes over the trigger-to-commit
+time of the timed steps' snapshots.
 
 Also measured: the pack kernel against the HBM roofline (HIP events that the
-library records on its own pack stream around every launch), D2H against the
-host link's measured peak (a plain pinned 1 GiB copy in the same process),
-restore/verify rates, the step-time overhead of snapshots under a bf16 GEMM
-load (one rank of a 65B model under TP=8 x PP=8, GEMM 8192x8192x2752, timed
-per the paper's Sec. VII-B per-iteration statistic), and the CPU oracle on a bounded sample.
+library records on its own pack stream around every launch) and against the
+same kernel over one contiguous fragment; the pack stream's whole span (pack
+launches, release kernels, chunk-sum reduce); D2H against the host link's
+measured peak (plain pinned 1 GiB copies in the same process);
+restore/verify rates; the step-time overhead of a snapshot every step for 50
+steps under the shard's bf16 GEMM load (8192x4096x11008), timed per the
+paper's Sec. VII-B per-iteration statistic; and the CPU oracle on a bounded
+sample.  --gating adds the comparison of per-bucket and whole-range waits
+with a staging ring (one rank of a 65B model under TP=8 x PP=8).
 """
 import argparse
 import json
@@ -40,21 +49,36 @@ HBM_PEAK_GBPS = 8000.0
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", type=int, default=4,
+                    help="shard of the timed steps (default 4: the 7B LLaMA shard, the largest single-GPU one)")
     ap.add_argument("--no-overlap", action="store_true")
     ap.add_argument("--overlap-steps", type=int, default=50)
-    ap.add_argument("--overlap-workload", type=int, default=3)
-    ap.add_argument("--overlap-base-steps", type=int, default=0,
+    ap.add_argument("--overlap-workload", type=int, default=0, help="0 = the --workload shard (its context reused)")
+    ap.add_argument("--overlap-base-steps", type=int, default=20,
                     help="steps of each of the two no-snapshot runs (0 = --overlap-steps)")
     ap.add_argument("--overlap-ratios", default="1.5",
-                    help="compute window / standalone D2H time ratios to run, comma-separated (first = headline); "
-                         "each entry also gives the floor max(0, T_D2H - base step) / base step")
+                    help="compute window / standalone snapshot time ratios to run, comma-separated (first = "
+                         "headline); each entry also gives the floor max(0, T_snapshot - base step) / base step")
+    ap.add_argument("--overlap-gating", choices=["buckets", "whole"], default="buckets",
+                    help="the update's gate: one ckpt_wait per optimizer bucket on its own fragments, or one wait "
+                         "on every fragment")
     ap.add_argument("--overlap-only", action="store_true",
                     help="run only the overlap leg and print its JSON")
-    ap.add_argument("--bounce-bytes", type=int, default=0,
-                    help="pageable host images behind pinned bounce rings of this many bytes (0 = pinned images)")
+    ap.add_argument("--gating", action="store_true",
+                    help="also run the gate-granularity comparison (per-bucket against whole-range waits with a "
+                         "staging ring)")
+    ap.add_argument("--gating-only", action="store_true", help="run only the gate-granularity comparison")
+    ap.add_argument("--gating-workload", type=int, default=3)
+    ap.add_argument("--gating-ratios", default="0.5,0.75,1.0,1.5")
+    ap.add_argument("--gating-steps", type=int, default=25)
+    ap.add_argument("--gating-base-steps", type=int, default=15)
+    ap.add_argument("--gating-staging-bytes", type=int, default=1 << 30)
+    ap.add_argument("--bounce-bytes", type=int, default=-1,
+                    help="pageable host images behind pinned bounce rings of this many bytes; 0 = pinned images; "
+                         "-1 = 8 GiB rings for workload 4 (two 94.3 GB images exceed the pinned memory the host "
+                         "grants), pinned otherwise")
     ap.add_argument("--host-threads", type=int, default=0, help="bounce mode: host copy threads (0 = library default)")
     ap.add_argument("--group-bytes", type=int, default=0,
                     help="bytes per pack launch and DMA request (whole chunks); 0 = the library default (1 GiB, or "
@@ -63,6 +87,8 @@ def parse():
                     help="device staging: 0 = a full-size image (default); else a ring of slots of one chunk group "
                          "each, at most this many bytes in all, the next pack of a slot waiting for its copy (main "
                          "and overlap legs)")
+    ap.add_argument("--ceiling-bytes", type=int, default=8 << 30,
+                    help="size of the contiguous fragment the pack ceiling is measured on")
     ap.add_argument("--image-file", default="",
                     help="bounce mode: keep the host images in this file (crash-surviving; removed at the end)")
     ap.add_argument("--grid-blocks", type=int, default=0,
@@ -75,10 +101,11 @@ def parse():
                     help="replicate each snapshot to this many peers (k of Sec. V-C), all in this process")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-sample-bytes", type=int, default=10 << 30)
-    ap.add_argument("--traffic", type=str, default=os.path.join(ROOT, "profiles", "pack_checksum_gpt1.3b_traffic.txt"),
+    ap.add_argument("--traffic", type=str, default=os.path.join(ROOT, "profiles", "pack_checksum_llama7b_traffic.txt"),
                     help="rocprofv3 FETCH_SIZE/WRITE_SIZE summary written by --pmc-summary")
     ap.add_argument("--pmc-run", action="store_true",
-                    help="short run for counter collection: a 1 GiB plain copy, then two snapshots")
+                    help="short run for counter collection: a 1 GiB plain copy, then two snapshots of --workload, "
+                         "a restore and a verify")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarize two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of --pmc-run")
     ap.add_argument("--stats-summary", metavar="DIR", help="summarize a rocprofv3 --kernel-trace --stats run")
@@ -88,6 +115,9 @@ def parse():
     ap.add_argument("--command", default="", help="command line recorded in a summary")
     ap.add_argument("--bench-json", default="", help="with --stats-summary: the JSON line bench.py printed in that run")
     return ap.parse_args()
+
+
+DEFAULT_BOUNCE = 8 << 30
 
 
 PACK_KERNEL = "tile_kernel<0"  # PACK instantiation of the tile kernel
@@ -173,8 +203,8 @@ def read_summary(path):
 
 def timed_pack_average(d, bench):
     """Average duration (ms) of the pack dispatches of the bench's timed steps,
-    from the kernel trace: workload 2 runs first, (warmup + steps) passes of
-    `launches / steps` dispatches each."""
+    from the kernel trace: after the ceiling's passes, (warmup + steps)
+    passes of `launches / steps` dispatches each."""
     import csv
     import glob
 
@@ -183,6 +213,7 @@ def timed_pack_average(d, bench):
     for f in files:
         rows += [r for r in csv.DictReader(open(f)) if PACK_KERNEL in r["Kernel_Name"]]
     rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    rows = rows[bench["components"]["pack_ceiling"]["launches_total"]:]  # the ceiling's passes come first
     per = bench["roofline"]["launches"] // bench["steps"]
     timed = rows[bench["warmup"] * per:(bench["warmup"] + bench["steps"]) * per]
     durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e6 for r in timed]
@@ -290,8 +321,11 @@ def gemm_inflation(d, command):
     return "\n".join(lines)
 
 
+_T0 = time.perf_counter()
+
+
 def log(*a):
-    print("[bench]", *a, file=sys.stderr, flush=True)
+    print("[bench +%.0fs]" % (time.perf_counter() - _T0), *a, file=sys.stderr, flush=True)
 
 
 def trimmed_mean(xs, warm=10, drop=0.05):
@@ -345,32 +379,39 @@ def link_peak(torch):
     return out
 
 
-def hbm_copy_ceiling(torch):
-    n = 4 << 30
-    a = torch.empty(n, dtype=torch.uint8, device="cuda")
-    b = torch.empty(n, dtype=torch.uint8, device="cuda")
-    a.fill_(1)
-    b.copy_(a)
-    torch.cuda.synchronize()
-    best = 1e9
-    for _ in range(5):
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record()
-        b.copy_(a)
-        e1.record()
-        e1.synchronize()
-        best = min(best, e0.elapsed_time(e1))
-    del a, b
-    return 2 * n / best / 1e6
+def host_cpus():
+    """Cores the oracle may use here (this process's CPU affinity, capped by a
+    cgroup CPU quota when one is set) and what the host reports about itself."""
+    aff = len(os.sched_getaffinity(0))
+    quota = None
+    try:
+        q, per = open("/sys/fs/cgroup/cpu.max").read().split()
+        if q != "max":
+            quota = int(q) / int(per)
+    except (OSError, ValueError):
+        pass
+    usable = aff if quota is None else max(1, min(aff, int(quota)))
+    topo = {}
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            k, _, v = line.partition(":")
+            if k.strip() in ("Model name", "Socket(s)", "Core(s) per socket", "Thread(s) per core", "CPU(s)",
+                             "NUMA node(s)"):
+                topo[k.strip()] = v.strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    return usable, {"os_cpu_count": os.cpu_count(), "affinity_cpus": aff, "cgroup_quota_cpus": quota,
+                    "threads_used": usable, "lscpu": topo}
 
 
-def cpu_baseline(tensors, plan, chunk, target_bytes, threads=16):
+def cpu_baseline(tensors, chunk, target_bytes):
     """The oracle as it stands, on the first fragments of the shard up to
-    target_bytes: pack + chunk sums + restore + verify (the same cycle as one
-    GPU step, minus the host-link copies, which a CPU does not need).  Timed
-    on one thread, then with the image split by whole chunks over `threads`
-    threads (the oracle's C calls run outside the interpreter lock)."""
+    target_bytes: pack + chunk sums + restore + verify (the GPU step's
+    kernels' work, without the host-link copies a CPU does not need).  Timed
+    with the image split by whole chunks over every core this process may use
+    (the oracle's C calls run outside the interpreter lock), and on one
+    thread."""
     from concurrent.futures import ThreadPoolExecutor
 
     import numpy as np
@@ -399,40 +440,124 @@ def cpu_baseline(tensors, plan, chunk, target_bytes, threads=16):
         t2 = time.perf_counter()
         return t1 - t0, t2 - t1, bad, back
 
+    nthr, host = host_cpus()
+    per = (nc + nthr - 1) // nthr
+    parts = [(k * per * chunk, min((k + 1) * per * chunk, I)) for k in range(nthr) if k * per * chunk < I]
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(len(parts)) as ex:
+        res = list(ex.map(lambda r: cycle(*r)[2], parts))
+    dtn = time.perf_counter() - t0
+    assert all(r == [] for r in res)
     t0 = time.perf_counter()
     t_pack, t_rest, bad, back = cycle(0, I)
     dt1 = time.perf_counter() - t0
     assert bad == [] and all(np.array_equal(a, b) for a, b in zip(frags[:3], back[:3]))
     del back
-    nthr = max(1, min(threads, os.cpu_count() or 1))
-    per = (nc + nthr - 1) // nthr
-    parts = [(k * per * chunk, min((k + 1) * per * chunk, I)) for k in range(nthr) if k * per * chunk < I]
-    t0 = time.perf_counter()
-    with ThreadPoolExecutor(nthr) as ex:
-        res = list(ex.map(lambda r: cycle(*r)[2], parts))
-    dtn = time.perf_counter() - t0
-    assert all(r == [] for r in res)
-    return {"value": round(total / dt1 / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": "first %d of %d fragments of the shard (%d bytes, %d chunks of %d MiB): pack + chunk sums "
-                      "+ restore + verify, one thread, %.1f s" % (len(frags), len(tensors), total, nc, chunk >> 20, dt1),
-            "pack_checksum_GBps": round(2 * total / t_pack / 1e9, 3), "restore_verify_GBps": round(total / t_rest / 1e9, 3),
-            "parallel": {"value": round(total / dtn / 1e9, 3), "cores": len(parts),
-                         "split": "whole chunks, %d per thread" % per, "seconds": round(dtn, 2)}}
+    return {"value": round(total / dtn / 1e9, 3), "unit": "GB/s", "cores": len(parts), "kind": "oracle",
+            "sample": "first %d of %d fragments of the shard (%d bytes, %d chunks of %d MiB): pack + chunk sums + "
+                      "restore + verify, split by whole chunks over %d threads (%.2f s), and on one thread (%.1f s)"
+                      % (len(frags), len(tensors), total, nc, chunk >> 20, len(parts), dtn, dt1),
+            "host": host,
+            "single_thread": {"value": round(total / dt1 / 1e9, 3), "cores": 1, "seconds": round(dt1, 2),
+                              "pack_checksum_GBps": round(2 * total / t_pack / 1e9, 3),
+                              "restore_verify_GBps": round(total / t_rest / 1e9, 3)}}
+
+
+def buckets_of(plan, n_buckets):
+    """Contiguous runs of whole parameters (4 fragments each: param, master,
+    m, v) of about equal bytes: the optimizer's buckets, in registration order."""
+    sizes = [sum(p[1] for p in plan[i:i + 4]) for i in range(0, len(plan), 4)]
+    total, out, lo, acc = sum(sizes), [], 0, 0
+    for j, z in enumerate(sizes):
+        acc += z
+        if acc >= total * (len(out) + 1) / n_buckets or j == len(sizes) - 1:
+            out.append((lo * 4, (j + 1) * 4))
+            lo = j + 1
+    return out
+
+
+class Optimizer:
+    """An in-place optimizer-like update of every registered fragment (read
+    and write of all 14 bytes per parameter, like an Adam step): m *= 0.9,
+    v *= 0.999, master -= 1e-3 * m, param = master.  update(lo, hi) touches
+    fragments [lo, hi) only; each bucket can be gated by ckpt_wait(CAPTURED)
+    on exactly the fragments it overwrites."""
+
+    def __init__(self, torch, tensors):
+        self.torch = torch
+        self.t = tensors
+
+    def update(self, lo, hi):
+        T = self.torch
+        p, w, m, v = self.t[lo:hi:4], self.t[lo + 1:hi:4], self.t[lo + 2:hi:4], self.t[lo + 3:hi:4]
+        T._foreach_mul_(m, 0.9)
+        T._foreach_mul_(v, 0.999)
+        T._foreach_add_(w, m, alpha=-1e-3)
+        for a, b in zip(p, w):
+            a.copy_(b)
+
+
+def pack_ceiling(torch, P, nbytes, chunk):
+    """The same pack kernel over one contiguous, 16-byte-aligned fragment of
+    nbytes (1 GiB launches, as for the shard): pack-only passes (the offload
+    is cut before its first copy, so the link stays idle), each right after
+    an in-place update of the fragment (as a snapshot follows the optimizer
+    step), and each after a host synchronisation with the GPU idle."""
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    buf.view(torch.int32).random_()
+    ck = P.Checkpointer([buf], chunk_bytes=chunk)
+    P.ckpt_set_timing(ck.ctx, True)
+
+    def one(update):
+        if update:
+            buf.view(torch.int32).add_(0)
+        else:
+            torch.cuda.synchronize()
+        P.ckpt_debug_interrupt_next(ck.ctx, 0)
+        s = ck.snapshot()
+        ck.wait_captured(s, 0, 1)
+        torch.cuda.current_stream().synchronize()
+        return P.ckpt_last_timing(ck.ctx, P.CKPT_OP_PACK)
+
+    one(True)
+    out = {}
+    for name, update in (("after_update", True), ("idle", False)):
+        ts = [one(update) for _ in range(3)]
+        ms = sum(t["kernel_ms"] for t in ts)
+        out[name + "_GBps"] = round(2 * nbytes * 3 / ms / 1e6, 1)
+        out[name + "_avg_launch_ms"] = round(ms / sum(t["kernels"] for t in ts), 4)
+    out["bytes"] = nbytes
+    out["launches_per_pass"] = ts[0]["kernels"]
+    out["launches_total"] = 7 * ts[0]["kernels"]  # the first pass, then three after an update and three idle
+    ck.close()
+    del buf
+    torch.cuda.empty_cache()
+    return out
 
 
 def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_steps=0, bounce=0, threads=0,
-                grid_blocks=0, staging=0, group=0):
+                grid_blocks=0, staging=0, group=0, shared=None, gating="buckets", n_buckets=8):
     """Step-time overhead of per-step snapshots under a bf16 GEMM load.
 
-    One step: R back-to-back GEMMs on the compute stream, the gate, then an
-    in-place "optimizer" update of every registered fragment; the snapshot
-    is issued right after the previous update.  R is fixed before measuring
-    as ceil(ratio * T_D2H / T_GEMM) from the standalone D2H time and the GEMM
-    time; the headline uses the first ratio.  Overhead compares the mean step
-    (paper Sec. VII-B per-iteration statistic) with and without snapshots; the no-snapshot
-    runs bracket the snapshot run."""
+    One step: R back-to-back GEMMs on the compute stream, then the optimizer
+    update in buckets, each gated by ckpt_wait(CAPTURED) on exactly the
+    fragments it overwrites (gating="buckets"; "whole": one wait on every
+    fragment before the first bucket); the snapshot is issued right after
+    the previous update.  R is fixed before measuring as
+    ceil(ratio * T_D2H / T_GEMM) from the standalone snapshot time (trigger
+    to commit) and the GEMM time; the headline uses the first ratio.
+    Overhead compares the mean step (paper Sec. VII-B per-iteration
+    statistic) with and without snapshots; the no-snapshot runs bracket the
+    snapshot run.  shared = (tensors, plan, checkpointer) reuses a registered
+    state instead of making one."""
     base_steps = base_steps or steps
-    tensors, plan = W.make_state(wid, device="cuda")
+    if shared is None:
+        tensors, plan = W.make_state(wid, device="cuda")
+        ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan],
+                            chunk_bytes=W.WORKLOADS[wid]["chunk"], bounce_bytes=bounce, host_threads=threads,
+                            grid_blocks=grid_blocks, device_staging_bytes=staging, group_bytes=group)
+    else:
+        tensors, plan, ck = shared
     n = len(tensors)
     M, K, N = W.OVERLAP_GEMM[wid]
     x = torch.randn(M, K, device="cuda", dtype=torch.bfloat16)
@@ -447,44 +572,29 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
     e1.record()
     e1.synchronize()
     t_gemm = e0.elapsed_time(e1) / 50
-    ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=W.WORKLOADS[wid]["chunk"],
-                        bounce_bytes=bounce, host_threads=threads, grid_blocks=grid_blocks,
-                        device_staging_bytes=staging, group_bytes=group)
     P.ckpt_set_timing(ck.ctx, True)
-    # Standalone D2H: the median of three snapshots after one warm-up snapshot
-    # (the first snapshot of a context also sets up its records).
-    d2h_runs = []
+    # Standalone snapshot (trigger to commit): the median of three after a
+    # warm-up snapshot (the first snapshot of a context also sets up its
+    # records).
+    d2h_runs, copy_runs = [], []
     for k in range(4):
-        t0 = time.perf_counter()
         s = ck.snapshot(step=k)
         ck.wait_committed(s)
-        t_commit = (time.perf_counter() - t0) * 1e3
         tm = P.ckpt_last_timing(ck.ctx, P.CKPT_OP_SNAPSHOT)
         ck_groups = tm["kernels"]
-        t = tm["copy_ms"]
+        t = tm["total_ms"]
         if t <= 0:  # engine timestamps unavailable (a copy tracer owns the signals)
             t = ck.image_bytes / link_d2h_gbps / 1e6
-        if bounce:  # the snapshot is done when its last group is in the pageable image
-            t = max(t, t_commit)
         if k:
             d2h_runs.append(t)
+            copy_runs.append(tm["copy_ms"])
     t_d2h = sorted(d2h_runs)[1]
     P.ckpt_set_timing(ck.ctx, False)
-    params = [tensors[i] for i in range(0, n, 4)]
-    masters = [tensors[i] for i in range(1, n, 4)]
-    ms = [tensors[i] for i in range(2, n, 4)]
-    vs = [tensors[i] for i in range(3, n, 4)]
-
-    def optimizer():  # touches every registered fragment in place
-        torch._foreach_mul_(ms, 0.9)
-        torch._foreach_mul_(vs, 0.999)
-        torch._foreach_add_(masters, ms, alpha=-1e-3)
-        for p, m in zip(params, masters):
-            p.copy_(m)
-
+    opt = Optimizer(torch, tensors)
+    bks = buckets_of(plan, n_buckets)
     calls = []  # host time of each snapshot call
 
-    def run(with_snap, R, steps):
+    def run(with_snap, R, steps, mode):
         times = []
         snap = None
         for k in range(steps):
@@ -498,30 +608,35 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
                 calls.append((time.perf_counter() - tc) * 1e3)
             for _ in range(R):
                 torch.matmul(x, w)
-            if with_snap:
+            if with_snap and mode == "whole":
                 ck.wait_captured(snap, 0, n)
-            optimizer()
+            for lo, hi in bks:
+                if with_snap and mode == "buckets":
+                    ck.wait_captured(snap, lo, hi)
+                opt.update(lo, hi)
             torch.cuda.synchronize()
             times.append((time.perf_counter() - t0) * 1e3)
             if (k + 1) % 10 == 0:
-                log("overlap: %s, %d/%d steps, last %.1f ms" % ("with snapshots" if with_snap else "baseline", k + 1,
-                                                                steps, times[-1]))
+                log("overlap: %s, %d/%d steps, last %.1f ms" % (
+                    ("snapshots, %s gating" % mode) if with_snap else "baseline", k + 1, steps, times[-1]))
         return times
 
     sweep = []
     for ratio in ratios:
         R = int(math.ceil(ratio * t_d2h / t_gemm))
         log("overlap: ratio %.2f, R = %d GEMMs per step" % (ratio, R))
-        base1 = run(False, R, base_steps)
-        withs = run(True, R, steps)
-        base2 = run(False, R, base_steps)
+        base1 = run(False, R, base_steps, None)
+        withs = run(True, R, steps, gating)
+        base2 = run(False, R, base_steps, None)
         b = trimmed_mean(base1 + base2[10:], warm=10)
         wv = trimmed_mean(withs, warm=10)
         sweep.append({"window_over_d2h": ratio, "R": R, "base_ms": round(b, 2), "with_snapshot_ms": round(wv, 2),
                       "overhead_pct": round(100 * (wv - b) / b, 3),
                       "floor_pct": round(100 * max(0.0, t_d2h - b) / b, 3)})
-    ck.close()
-    del tensors, x, w
+    if shared is None:
+        ck.close()
+        del tensors
+    del x, w
     torch.cuda.empty_cache()
     head = sweep[0]
     out = {"workload": W.WORKLOADS[wid]["name"], "payload_bytes": sum(p[1] for p in plan), "gemm_mkn": [M, K, N],
@@ -529,15 +644,60 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
            "device_staging": staging_text(staging, W.WORKLOADS[wid]["chunk"]),
            "groups_per_snapshot": ck_groups,
            "tile_kernel_workgroups": grid_blocks or "one per tile",
-           "gemm_ms": round(t_gemm, 4), "d2h_ms": round(t_d2h, 2), "d2h_runs_ms": [round(t, 2) for t in d2h_runs],
+           "gating": "%d buckets, each behind ckpt_wait(CAPTURED) on its own fragments" % len(bks)
+                     if gating == "buckets" else "one ckpt_wait(CAPTURED) on every fragment",
+           "gemm_ms": round(t_gemm, 4), "snapshot_ms": round(t_d2h, 2),
+           "snapshot_runs_ms": [round(t, 2) for t in d2h_runs],
+           "snapshot_alone_GBps": round(sum(p[1] for p in plan) / t_d2h / 1e6, 2),
+           "d2h_alone_GBps": round(ck.image_bytes / sorted(copy_runs)[1] / 1e6, 2) if min(copy_runs) > 0 else None,
+           "d2h_link_peak_GBps": round(link_d2h_gbps, 2),
            "R": head["R"], "steps": steps,
            "base_steps": base_steps, "base_ms": head["base_ms"], "with_snapshot_ms": head["with_snapshot_ms"],
            "overhead_pct": head["overhead_pct"],
            "snapshot_call_ms": round(sorted(calls)[len(calls) // 2], 3) if calls else None,
            "statistic": "mean after dropping 10 warm-up steps and the slowest 5%"}
+    if out["d2h_alone_GBps"]:
+        out["d2h_alone_frac_of_link"] = round(out["d2h_alone_GBps"] / link_d2h_gbps, 4)
     if len(sweep) > 1:
         out["sweep"] = sweep
     return out
+
+
+def gating_leg(torch, P, W, wid, ratios, steps, base_steps, staging, n_buckets=8):
+    """Does waiting only on the chunks each bucket overwrites pay?  With a
+    staging ring the capture of the later chunks is paced by the D2H, so a
+    single wait on every fragment holds the whole update back until the last
+    chunk is packed, while per-bucket waits let each bucket go as soon as its
+    own chunks are.  Same loop as the overlap leg, for each window/D2H ratio:
+    no snapshots, snapshots with one whole-range wait, snapshots with
+    per-bucket waits (each run on the same registered state)."""
+    tensors, plan = W.make_state(wid, device="cuda")
+    ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=W.WORKLOADS[wid]["chunk"],
+                        device_staging_bytes=staging)
+    shared = (tensors, plan, ck)
+    rows = []
+    link = link_peak(torch)["d2h"]
+    for ratio in ratios:
+        res = {}
+        for mode in ("whole", "buckets"):
+            res[mode] = overlap_leg(torch, P, W, wid, steps, link, (ratio,), base_steps, shared=shared, gating=mode,
+                                    n_buckets=n_buckets)
+        rows.append({"window_over_d2h": ratio, "R": res["whole"]["R"],
+                     "base_ms": res["whole"]["base_ms"],
+                     "whole_range_ms": res["whole"]["with_snapshot_ms"],
+                     "whole_range_overhead_pct": res["whole"]["overhead_pct"],
+                     "per_bucket_base_ms": res["buckets"]["base_ms"],
+                     "per_bucket_ms": res["buckets"]["with_snapshot_ms"],
+                     "per_bucket_overhead_pct": res["buckets"]["overhead_pct"],
+                     "snapshot_ms": res["whole"]["snapshot_ms"]})
+        log("gating: ratio %.2f: whole range %+.2f%%, per bucket %+.2f%%" % (
+            ratio, rows[-1]["whole_range_overhead_pct"], rows[-1]["per_bucket_overhead_pct"]))
+    ck.close()
+    del tensors, shared
+    torch.cuda.empty_cache()
+    return {"workload": W.WORKLOADS[wid]["name"], "payload_bytes": sum(p[1] for p in plan),
+            "device_staging": staging_text(staging, W.WORKLOADS[wid]["chunk"]), "buckets": n_buckets,
+            "gemm_mkn": list(W.OVERLAP_GEMM[wid]), "steps": steps, "base_steps": base_steps, "rows": rows}
 
 
 def staging_text(staging, chunk):
@@ -665,37 +825,50 @@ def h2h_leg(torch, P, W, wid, steps, n_peers=1, bounce_bytes=0, host_threads=0):
                                     "runs": len(rest), "statistic": "median of the runs"}}
 
 
-def pmc_run(torch, P, W):
+def pmc_run(torch, P, W, wid, bounce):
     """Short run whose dispatches the counter summary reads: a 1 GiB plain
-    device copy (calibration), then two snapshots of the 1.3B GPT shard."""
+    device copy (calibration), then two snapshots of workload wid, one
+    restore and one verify."""
     a = torch.empty(CALIBRATION_BYTES, dtype=torch.uint8, device="cuda")
     b = torch.empty(CALIBRATION_BYTES, dtype=torch.uint8, device="cuda")
     a.fill_(1)
     b.copy_(a)
     torch.cuda.synchronize()
     del a, b
-    tensors, _ = W.make_state(2, device="cuda")
-    ck = P.Checkpointer(tensors, chunk_bytes=W.WORKLOADS[2]["chunk"])
+    tensors, plan = W.make_state(wid, device="cuda")
+    ck = P.Checkpointer(tensors, chunk_bytes=W.WORKLOADS[wid]["chunk"], bounce_bytes=bounce)
     for k in range(2):
         s = ck.snapshot(step=k)
         ck.wait_committed(s)
+        print("pmc run: snapshot %d committed" % k, flush=True)
     if ck.restore(s) or ck.verify(s):  # one pass of the scatter and of the verify kernel
         raise SystemExit("checksum mismatch in the counter run")
+    print("pmc run done: %s, %d payload bytes, %d-byte image" % (W.WORKLOADS[wid]["name"], sum(p[1] for p in plan),
+                                                                  ck.image_bytes), flush=True)
     ck.close()
-    print("pmc run done", flush=True)
 
 
 def main():
     args = parse()
     if args.pmc_summary:
         d = pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.command)
-        header = ("# HBM traffic of the pack kernel (tile_kernel<PACK>) on the 24-layer hidden-2048 GPT shard\n"
-                  "# (18,421,473,280 payload bytes, 1 GiB launches), from two rocprofv3 --pmc runs of\n"
+        import workloads as W
+
+        wid = args.workload
+        plan = W.fragment_plan(wid)
+        S = sum(p[1] for p in plan)
+        import oracle as O
+
+        _, I, _ = O.layout([p[1] for p in plan], 256, W.WORKLOADS[wid]["chunk"])
+        per = (I + (1 << 30) - 1) >> 30
+        header = ("# HBM traffic of the pack kernel (tile_kernel<PACK>) on the %s shard\n"
+                  "# (%d payload bytes, 1 GiB launches), from two rocprofv3 --pmc runs of\n"
                   "# `python bench.py --pmc-run`: FETCH_SIZE, then WRITE_SIZE (KiB per dispatch), each scaled by\n"
                   "# the same counter on a plain 1 GiB device copy (__amd_rocclr_copyBuffer).  The same run's\n"
                   "# restore (tile_kernel<SCATTER>) and verify (tile_kernel<VERIFY>) passes are summarized too.\n"
-                  "# Algorithmic bytes per dispatch (18 per pass, the last one short): pack and scatter\n"
-                  "# 2,046,830,364 (read + write of the image's 1 GiB windows), verify 1,023,415,182 (read).")
+                  "# Algorithmic bytes per dispatch (%d per pass, the last one short): pack and scatter\n"
+                  "# %d (read + write), verify %d (read)." % (W.WORKLOADS[wid]["name"], S, per, 2 * S // per,
+                                                               I // per))
         out = args.traffic
         write_summary(out, d, header)
         print(open(out).read())
@@ -740,51 +913,75 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     P.lib()  # fails loudly when libckpt.so is missing
     if args.pmc_run:
-        pmc_run(torch, P, W)
+        wid = args.workload
+        pmc_run(torch, P, W, wid, args.bounce_bytes if args.bounce_bytes >= 0 else (DEFAULT_BOUNCE if wid == 4 else 0))
         return
     ratios = [float(r) for r in args.overlap_ratios.split(",") if r]
+    wid = args.workload
+    bounce = args.bounce_bytes if args.bounce_bytes >= 0 else (DEFAULT_BOUNCE if wid == 4 else 0)
+    owid = args.overlap_workload or wid
     if args.h2h_only:
         print(json.dumps({"h2h": h2h_leg(torch, P, W, args.h2h_workload, args.h2h_steps, args.h2h_peers,
-                                         args.bounce_bytes, args.host_threads)}), flush=True)
+                                         max(args.bounce_bytes, 0), args.host_threads)}), flush=True)
+        return
+    if args.gating_only:
+        g = gating_leg(torch, P, W, args.gating_workload, [float(r) for r in args.gating_ratios.split(",") if r],
+                       args.gating_steps, args.gating_base_steps, args.gating_staging_bytes)
+        print(json.dumps({"gating": g}), flush=True)
         return
     if args.overlap_only:
         log("link peak")
         link = link_peak(torch)
-        ov = overlap_leg(torch, P, W, args.overlap_workload, args.overlap_steps, link["d2h"], ratios,
-                         args.overlap_base_steps, args.bounce_bytes, args.host_threads, args.grid_blocks,
-                         args.staging_bytes, args.group_bytes)
+        ob = bounce if owid == wid else max(args.bounce_bytes, 0)
+        ov = overlap_leg(torch, P, W, owid, args.overlap_steps, link["d2h"], ratios, args.overlap_base_steps, ob,
+                         args.host_threads, args.grid_blocks, args.staging_bytes, args.group_bytes,
+                         gating=args.overlap_gating)
         print(json.dumps({"overlap": ov, "d2h_link_peak_GBps": round(link["d2h"], 2)}), flush=True)
         return
-    wid = args.workload
     wl = W.WORKLOADS[wid]
     log("link peak")
     link = link_peak(torch)
-    log("hbm copy ceiling")
-    hbm_ceiling = hbm_copy_ceiling(torch)
+    log("pack ceiling: one contiguous %d-byte fragment" % args.ceiling_bytes)
+    ceiling = pack_ceiling(torch, P, args.ceiling_bytes, wl["chunk"])
     log("generating workload", wl["name"])
     tensors, plan = W.make_state(wid, device="cuda")
     torch.cuda.synchronize()
     S = sum(p[1] for p in plan)
     n = len(tensors)
+    cpu = None
+    if not args.no_cpu:  # before the host images take their share of host memory
+        log("cpu baseline")
+        cpu = cpu_baseline(tensors, wl["chunk"], args.cpu_sample_bytes)
+    log("registering %d fragments (%d payload bytes; host images %s)" % (
+        n, S, "pageable behind %d-byte bounce rings" % bounce if bounce else "pinned"))
     ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=wl["chunk"],
-                        bounce_bytes=args.bounce_bytes, host_threads=args.host_threads,
+                        bounce_bytes=bounce, host_threads=args.host_threads,
                         image_file=args.image_file or None, device_staging_bytes=args.staging_bytes,
                         group_bytes=args.group_bytes)
     P.ckpt_set_timing(ck.ctx, True)
-
+    opt = Optimizer(torch, tensors)
+    bks = buckets_of(plan, 8)
+    compute = torch.cuda.current_stream()
     prev = [None]
 
     def step(k):
-        # Snapshot k streams out (D2H) while the previous committed snapshot
-        # is verified (H2D): the host link carries both directions at once.
+        # Optimizer step k-1: each bucket waits (on the compute stream) only
+        # for the previous snapshot's capture of the chunks it overwrites.
+        for lo, hi in bks:
+            if prev[0] is not None:
+                ck.wait_captured(prev[0], lo, hi)
+            opt.update(lo, hi)
+        # Snapshot k, triggered on the compute stream right after the update;
+        # while it streams out (D2H), the previous committed snapshot is
+        # verified (H2D): the host link carries both directions at once.
         snap = ck.snapshot(step=k, meta=b"step=%d" % k)
         ck.wait_captured(snap, 0, n)
-        torch.cuda.current_stream().synchronize()  # packed: verify's kernels do not share HBM with the pack
+        compute.synchronize()  # packed: verify's kernels do not share HBM with the pack
         bad = ck.verify(prev[0]) if prev[0] is not None else []
         ck.wait_committed(snap)
         if prev[0] is None:
             bad += ck.verify(snap)
-        bad += ck.restore(snap)
+        bad += ck.restore(snap)  # the tensors already hold these bytes: every chunk must check
         if bad:
             raise RuntimeError("checksum mismatch in chunks %s" % bad)
         prev[0] = snap
@@ -809,17 +1006,19 @@ def main():
         return sum(t[key] for t in timings[kind])
 
     sn = timings["snapshot"][0]
+    K = args.steps
+    snap_ms = agg("snapshot", "total_ms") / K  # trigger to commit
     pack_ms = agg("snapshot", "kernel_ms")
     launches = sum(t["kernels"] for t in timings["snapshot"])
-    pack_bytes = 2 * S * args.steps
-    pack_gbps = pack_bytes / pack_ms / 1e6
+    pack_gbps = 2 * S * K / pack_ms / 1e6
+    span_gbps = 2 * S * K / agg("snapshot", "span_ms") / 1e6
     d2h_ms = agg("snapshot", "copy_ms")
-    d2h_gbps = sn["copy_bytes"] * args.steps / d2h_ms / 1e6 if d2h_ms > 0 else None
-    restore_gbps = sn["copy_bytes"] * args.steps / agg("restore", "total_ms") / 1e6
-    scatter_gbps = 2 * S * args.steps / agg("restore", "kernel_ms") / 1e6
-    h2d_gbps = sn["copy_bytes"] * args.steps / agg("restore", "copy_ms") / 1e6
-    verify_gbps = sn["copy_bytes"] * args.steps / agg("verify", "total_ms") / 1e6
-    verify_kernel_gbps = sn["copy_bytes"] * args.steps / agg("verify", "kernel_ms") / 1e6
+    d2h_gbps = sn["copy_bytes"] * K / d2h_ms / 1e6 if d2h_ms > 0 else None
+    restore_gbps = sn["copy_bytes"] * K / agg("restore", "total_ms") / 1e6
+    scatter_gbps = 2 * S * K / agg("restore", "kernel_ms") / 1e6
+    h2d_gbps = sn["copy_bytes"] * K / agg("restore", "copy_ms") / 1e6
+    verify_gbps = sn["copy_bytes"] * K / agg("verify", "total_ms") / 1e6
+    verify_kernel_gbps = sn["copy_bytes"] * K / agg("verify", "kernel_ms") / 1e6
     # HBM bytes per pack launch from the committed counter summary, unless
     # the kernel source changed since the counters were taken.
     traffic = None
@@ -829,83 +1028,94 @@ def main():
     roofline = {"kernel": "pack_checksum (tile_kernel<PACK>)", "bound": "hbm", "achieved": round(pack_gbps, 1),
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(pack_gbps / HBM_PEAK_GBPS, 4),
                 "traffic": traffic, "launches": launches, "avg_launch_ms": round(pack_ms / launches, 4),
-                "algorithmic_bytes_per_launch": int(pack_bytes / launches),
-                "frac_of_measured_copy_ceiling": round(pack_gbps / hbm_ceiling, 4)}
-    # Pack-only passes (outside the timed steps): snapshots whose offload is
-    # cut before their first copy, so the kernels run with the host link
-    # idle; such a snapshot is aborted and never committed.
-    alone_ms = 0.0
-    for k in range(3):
-        P.ckpt_debug_interrupt_next(ck.ctx, 0)
-        s_cut = ck.snapshot(step=10_000 + k)
-        ck.wait_captured(s_cut, 0, n)
-        torch.cuda.current_stream().synchronize()
-        t = P.ckpt_last_timing(ck.ctx, P.CKPT_OP_PACK)
-        alone_ms += t["kernel_ms"]
-    pack_alone_gbps = 2 * S * 3 / alone_ms / 1e6
-    # The same pack-only passes, each issued right after an optimizer-like
-    # update (every fragment read and written in place, values unchanged):
-    # where a training loop issues its snapshot.  Informational; the
-    # headline stays the pipelined figure above.
-    upd_ms = 0.0
-    for k in range(3):
-        torch._foreach_mul_(tensors, 1.0)
-        P.ckpt_debug_interrupt_next(ck.ctx, 0)
-        s_cut = ck.snapshot(step=20_000 + k)
-        ck.wait_captured(s_cut, 0, n)
-        torch.cuda.current_stream().synchronize()
-        upd_ms += P.ckpt_last_timing(ck.ctx, P.CKPT_OP_PACK)["kernel_ms"]
-    pack_after_update_gbps = 2 * S * 3 / upd_ms / 1e6
-    ck.close()
-    if args.image_file and os.path.exists(args.image_file):
-        os.unlink(args.image_file)
-    cpu = None
-    if not args.no_cpu:
-        log("cpu baseline")
-        cpu = cpu_baseline(tensors, plan, wl["chunk"], args.cpu_sample_bytes)
-    del tensors
-    torch.cuda.empty_cache()
+                "algorithmic_bytes_per_launch": int(2 * S * K / launches),
+                "ceiling": "the same kernel over one contiguous 16-byte-aligned %d-byte fragment, right after an "
+                           "in-place update of it: %.1f GB/s" % (ceiling["bytes"], ceiling["after_update_GBps"]),
+                "frac_of_ceiling": round(pack_gbps / ceiling["after_update_GBps"], 4),
+                "a3_span_GBps": round(span_gbps, 1), "a3_span_frac": round(span_gbps / HBM_PEAK_GBPS, 4)}
+    # Pack-only passes over the shard (outside the timed steps): snapshots
+    # whose offload is cut before their first copy, so the kernels run with
+    # the host link idle; each right after the optimizer update, and each
+    # after a host synchronisation with the GPU idle.  Such a snapshot is
+    # aborted and never committed.
+    def pack_only(update, reps=3):
+        ms, cnt = 0.0, 0
+        for k in range(reps):
+            if update:
+                for lo, hi in bks:
+                    opt.update(lo, hi)
+            else:
+                torch.cuda.synchronize()
+            P.ckpt_debug_interrupt_next(ck.ctx, 0)
+            s_cut = ck.snapshot(step=10_000 + k)
+            ck.wait_captured(s_cut, 0, n)
+            compute.synchronize()
+            t = P.ckpt_last_timing(ck.ctx, P.CKPT_OP_PACK)
+            ms += t["kernel_ms"]
+        return 2 * S * reps / ms / 1e6
+
+    pack_after_update_gbps = pack_only(True)
+    pack_idle_gbps = pack_only(False)
     overlap = None
     if not args.no_overlap:
         log("overlap leg")
-        overlap = overlap_leg(torch, P, W, args.overlap_workload, args.overlap_steps, link["d2h"], ratios,
-                              args.overlap_base_steps, args.bounce_bytes, args.host_threads, args.grid_blocks,
-                              args.staging_bytes, args.group_bytes)
+        shared = (tensors, plan, ck) if owid == wid else None
+        overlap = overlap_leg(torch, P, W, owid, args.overlap_steps, link["d2h"], ratios, args.overlap_base_steps,
+                              bounce if owid == wid else 0, args.host_threads, args.grid_blocks, args.staging_bytes,
+                              args.group_bytes, shared=shared, gating=args.overlap_gating)
+    ck.close()
+    if args.image_file and os.path.exists(args.image_file):
+        os.unlink(args.image_file)
+    del tensors
+    torch.cuda.empty_cache()
+    gating = None
+    if args.gating:
+        log("gating leg")
+        gating = gating_leg(torch, P, W, args.gating_workload, [float(r) for r in args.gating_ratios.split(",") if r],
+                            args.gating_steps, args.gating_base_steps, args.gating_staging_bytes)
     try:
         sha = subprocess.run(["git", "rev-parse", "--short", "HEAD"], cwd=ROOT, capture_output=True,
                              text=True).stdout.strip() or None
     except Exception:
         sha = None
     out = {
-        "metric": METRIC, "value": round(S / (ms_per_step / 1e3) / 1e9, 3), "unit": "GB/s", "n_gpus": 1,
+        "metric": METRIC, "value": round(S / snap_ms / 1e6, 3), "unit": "GB/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 2), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "u64", "data": "synthetic",
-        "config": {"workload": "%s shard: %d fragments, %d payload bytes, %d MiB chunks (snapshot + gate + restore "
-                               "+ verify per step)" % (wl["name"], n, S, wl["chunk"] >> 20),
+        "config": {"workload": "%s shard: %d fragments, %d payload bytes, %d MiB chunks; per step: optimizer update "
+                               "(per-bucket gate), snapshot (pack + sums + D2H + commit) with verify of the previous "
+                               "snapshot beside it, restore" % (wl["name"], n, S, wl["chunk"] >> 20),
+                   "value": "snapshot GB/s: payload bytes / trigger-to-commit time of the timed steps' snapshots "
+                            "(pack + chunk sums + D2H into host memory + commit)",
                    "payload_bytes": S, "image_bytes": int(sn["copy_bytes"]), "chunk_bytes": wl["chunk"],
-                   "host_images": ("image file %s behind %d-byte pinned bounce rings" % (args.image_file,
-                                                                                          args.bounce_bytes)
+                   "host_images": ("image file %s behind %d-byte pinned bounce rings" % (args.image_file, bounce)
                                    if args.image_file else
-                                   "pageable, %d-byte pinned bounce rings" % args.bounce_bytes
-                                   if args.bounce_bytes else "pinned"),
+                                   "pageable, %d-byte pinned bounce rings" % bounce if bounce else "pinned"),
                    "device_staging": staging_text(args.staging_bytes, wl["chunk"]),
                    "groups_per_snapshot": int(sn["kernels"]),
                    "parallelism": "one rank, one GPU"},
         "roofline": roofline,
         "cpu_baseline": cpu,
-        "components": {"pack_GBps": round(pack_gbps, 1),
-                       "pack_alone_GBps": round(pack_alone_gbps, 1),
-                       "pack_alone_frac": round(pack_alone_gbps / HBM_PEAK_GBPS, 4),
+        "components": {"snapshot_ms": round(snap_ms, 2),
+                       "cycle_GBps": round(S / ms_per_step / 1e6, 3),
+                       "pack_GBps": round(pack_gbps, 1),
+                       "pack_ceiling": ceiling,
                        "pack_after_update_GBps": round(pack_after_update_gbps, 1),
                        "pack_after_update_frac": round(pack_after_update_gbps / HBM_PEAK_GBPS, 4),
+                       "pack_after_update_frac_of_ceiling": round(pack_after_update_gbps
+                                                                  / ceiling["after_update_GBps"], 4),
+                       "pack_idle_GBps": round(pack_idle_gbps, 1),
+                       "pack_idle_frac": round(pack_idle_gbps / HBM_PEAK_GBPS, 4),
                        "d2h_GBps": d2h_gbps and round(d2h_gbps, 2),
                        "d2h_link_peak_GBps": round(link["d2h"], 2),
                        "d2h_frac_of_link": d2h_gbps and round(d2h_gbps / link["d2h"], 4),
+                       "d2h_note": "DMA span of the timed snapshots, with the previous snapshot's verify (H2D) "
+                                   "running beside it",
                        "h2d_GBps": round(h2d_gbps, 2), "h2d_link_peak_GBps": round(link["h2d"], 2),
                        "restore_GBps": round(restore_gbps, 2), "scatter_verify_GBps": round(scatter_gbps, 1),
-                       "verify_GBps": round(verify_gbps, 2), "verify_kernel_GBps": round(verify_kernel_gbps, 1),
-                       "hbm_copy_ceiling_GBps": round(hbm_ceiling, 1)},
+                       "verify_GBps": round(verify_gbps, 2), "verify_kernel_GBps": round(verify_kernel_gbps, 1)},
         "overlap": overlap,
+        "gating": gating,
         "git": sha,
     }
     print(json.dumps(out), flush=True)

@@ -247,10 +247,17 @@ typedef struct {
     uint32_t kernels;    /* number of tile-kernel launches */
     uint32_t copies;     /* number of DMA copy requests (image bytes only) */
     float copy_ms;       /* first image copy start to last image copy end */
-    float total_ms;      /* operation start (after the trigger) to its last event */
+    float total_ms;      /* operation start (after the trigger) to its last event; for a
+                            snapshot: to its commit (image and sums in host memory; with
+                            pageable images, the last group landed in the image) */
     uint64_t kernel_bytes; /* algorithmic HBM bytes of the kernels: 2*payload (pack,
                               scatter) or image bytes (verify) */
     uint64_t copy_bytes;   /* image bytes moved over the host link */
+    float span_ms;         /* snapshot / pack: the first pack launch's start to the end of the
+                              pack stream's work -- every pack launch, the release kernels
+                              between them, the chunk-sum reduce and its release, gaps
+                              included (an interrupted snapshot: to its last pack launch);
+                              -1 for restore and verify */
 } ckpt_timing;
 #define CKPT_OP_SNAPSHOT 0
 #define CKPT_OP_RESTORE 1

@@ -57,7 +57,8 @@ class ckpt_tensor(C.Structure):
 
 class ckpt_timing(C.Structure):
     _fields_ = [("kernel_ms", C.c_float), ("kernels", C.c_uint32), ("copies", C.c_uint32), ("copy_ms", C.c_float),
-                ("total_ms", C.c_float), ("kernel_bytes", C.c_uint64), ("copy_bytes", C.c_uint64)]
+                ("total_ms", C.c_float), ("kernel_bytes", C.c_uint64), ("copy_bytes", C.c_uint64),
+                ("span_ms", C.c_float)]
 
 
 class CkptError(RuntimeError):

@@ -124,6 +124,9 @@ void pump_drain(ckpt_ctx* c)
                 std::this_thread::sleep_for(std::chrono::microseconds(20));
             if (res_done(it.res, it.groups, true) && !it.res->failed.load(std::memory_order_acquire)) {
                 file_commit(c, it);
+                uint64_t ts = 0;
+                (void)hsa_system_get_info(HSA_SYSTEM_INFO_TIMESTAMP, &ts);
+                it.res->recorded_ts.store(ts, std::memory_order_relaxed);
                 it.res->recorded.store(true, std::memory_order_release);
             }
             std::lock_guard<std::mutex> l(p->m);
@@ -150,6 +153,11 @@ void pump_drain(ckpt_ctx* c)
             p->cv.notify_all();
         }
         if (!ok) it.res->failed.store(true, std::memory_order_release);
+        if (ok && it.g + 1 == c->n_groups) { // the image's last byte has landed (groups drain in order)
+            uint64_t ts = 0;
+            (void)hsa_system_get_info(HSA_SYSTEM_INFO_TIMESTAMP, &ts);
+            it.res->landed_ts.store(ts, std::memory_order_relaxed);
+        }
         it.res->landed.fetch_add(1, std::memory_order_acq_rel);
     }
 }

@@ -63,9 +63,15 @@ struct RecRes {
     unsigned long long* d_sums = nullptr;
     std::vector<hipEvent_t> k0, k1;     // timing: around each pack launch
     hipEvent_t t0 = nullptr;
+    hipEvent_t t_red = nullptr;         // timing: after the chunk-sum reduce and its release
     std::atomic<uint32_t> landed{0};    // bounce mode: groups moved from the ring into the image
     std::atomic<bool> failed{false};    // bounce mode: a copy of this record could not be completed
     std::atomic<bool> recorded{false};  // image file: the commit record has been written
+    // Timing, in the HSA system timestamp domain (that of the DMA engines'
+    // copy timestamps): when the last group landed in the pageable image,
+    // and when the commit record was written (0 = not yet).
+    std::atomic<uint64_t> landed_ts{0};
+    std::atomic<uint64_t> recorded_ts{0};
 };
 
 struct SnapRec {

@@ -241,6 +241,7 @@ void destroy_res(RecRes* r)
     for (auto e : r->k1)
         if (e) (void)hipEventDestroy(e);
     if (r->t0) (void)hipEventDestroy(r->t0);
+    if (r->t_red) (void)hipEventDestroy(r->t_red);
     for (auto s : r->dep)
         if (s.handle) hsa_signal_destroy(s);
     for (auto s : r->copied)
@@ -292,6 +293,7 @@ ckpt_status new_res(ckpt_ctx* c, RecRes** out)
         if (st == CKPT_OK) st = gpu_consumed_signal(c, &r->flagged[g]);
     }
     if (st == CKPT_OK) st = make_event(c, &r->t0, true);
+    if (st == CKPT_OK) st = make_event(c, &r->t_red, true);
     if (st == CKPT_OK) st = gpu_only_signal(c, &r->dep_sums, &r->dep_sums_val);
     if (st == CKPT_OK && hsa_signal_create(0, 0, nullptr, &r->done) != HSA_STATUS_SUCCESS) {
         r->done.handle = 0;
@@ -618,6 +620,7 @@ ckpt_status check_image(ckpt_ctx* c, int b, hipStream_t stream, bool scatter, co
         t.total_ms = elapsed(L.t0, (*L.tk1)[L.n_units - 1]);
         t.kernel_bytes = scatter ? 2 * c->payload : c->I;
         t.copy_bytes = c->I;
+        t.span_ms = -1.f;
         c->op_timing[op].t = t;
         c->op_timing[op].valid = true;
     }
@@ -1066,6 +1069,8 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
     r.bounce = c->bounce;
     r.file = c->file_map != nullptr;
     res->landed.store(0, std::memory_order_relaxed);
+    res->landed_ts.store(0, std::memory_order_relaxed);
+    res->recorded_ts.store(0, std::memory_order_relaxed);
     res->failed.store(false, std::memory_order_relaxed);
     res->recorded.store(false, std::memory_order_relaxed);
     c->holder[r.buf] = id;
@@ -1193,6 +1198,7 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
         hsa_signal_store_screlease(res->dep_sums, 1);
         e = launch_release(res->dep_sums_val, c->s_pack);
         if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
+        if (r.timed) HIPCHK(c, hipEventRecord(res->t_red, c->s_pack));
         hsa_signal_store_screlease(res->done, 1);
         if (r.bounce) { // behind the snapshot's group copies
             {
@@ -1427,6 +1433,18 @@ ckpt_status ckpt_set_timing(ckpt_ctx* c, int32_t enable)
     return CKPT_OK;
 }
 
+namespace ckpt {
+// First pack launch's start to the end of the pack stream's snapshot work:
+// every pack launch, the release kernels between them, the chunk-sum reduce
+// and its release (an interrupted snapshot has no reduce: to its last pack).
+float pack_span(ckpt_ctx* c, const SnapRec& r)
+{
+    hipEvent_t end = r.aborted ? r.res->k1[c->n_groups - 1] : r.res->t_red;
+    if (hipEventSynchronize(end) != hipSuccess) return -1.f;
+    return elapsed(r.res->k0[0], end);
+}
+} // namespace ckpt
+
 ckpt_status ckpt_last_timing(ckpt_ctx* c, uint32_t which, ckpt_timing* out)
 {
     if (!c || !out || which > CKPT_OP_PACK) return fail(c, CKPT_EINVAL, "bad timing query");
@@ -1443,6 +1461,7 @@ ckpt_status ckpt_last_timing(ckpt_ctx* c, uint32_t which, ckpt_timing* out)
         t.copy_ms = -1.f;
         t.total_ms = -1.f;
         t.kernel_bytes = 2 * c->payload;
+        t.span_ms = pack_span(c, *best);
         *out = t;
         return CKPT_OK;
     }
@@ -1458,6 +1477,7 @@ ckpt_status ckpt_last_timing(ckpt_ctx* c, uint32_t which, ckpt_timing* out)
         for (uint64_t g = 0; g < c->n_groups; ++g) t.kernel_ms += elapsed(r->k0[g], r->k1[g]);
         t.kernels = (uint32_t)c->n_groups;
         t.copies = (uint32_t)c->n_groups;
+        t.span_ms = pack_span(c, *best);
         // DMA span: first image copy start to last image copy end (engine timestamps).
         uint64_t t_start = UINT64_MAX, t_end = 0;
         bool ok = true;
@@ -1471,7 +1491,20 @@ ckpt_status ckpt_last_timing(ckpt_ctx* c, uint32_t which, ckpt_timing* out)
             t_end = std::max<uint64_t>(t_end, ct.end);
         }
         t.copy_ms = (ok && t_end > t_start) ? (float)((double)(t_end - t_start) * 1e3 / (double)c->ts_freq) : -1.f;
+        // Trigger to commit: the first group's pack, then from its copy's
+        // start to the commit -- the last of: the last group copy's end, the
+        // sums copy's end and, with pageable images, the last group landing in
+        // the image (and the file record).  One clock throughout except the
+        // first pack (HIP events); the first copy starts right after it.
         t.total_ms = -1.f;
+        hsa_amd_profiling_async_copy_time_t cs;
+        if (ok && t_end > t_start && hsa_amd_profiling_get_async_copy_time(r->done, &cs) == HSA_STATUS_SUCCESS) {
+            uint64_t commit = std::max<uint64_t>(t_end, cs.end);
+            if (best->bounce) commit = std::max<uint64_t>(commit, r->landed_ts.load(std::memory_order_relaxed));
+            if (best->file) commit = std::max<uint64_t>(commit, r->recorded_ts.load(std::memory_order_relaxed));
+            const float k0 = elapsed(r->k0[0], r->k1[0]);
+            if (k0 >= 0.f) t.total_ms = k0 + (float)((double)(commit - t_start) * 1e3 / (double)c->ts_freq);
+        }
         t.kernel_bytes = 2 * c->payload;
         t.copy_bytes = c->I;
         *out = t;
