@@ -87,6 +87,8 @@ def parse():
                     help="device staging: 0 = a full-size image (default); else a ring of slots of one chunk group "
                          "each, at most this many bytes in all, the next pack of a slot waiting for its copy (main "
                          "and overlap legs)")
+    ap.add_argument("--pack-launch-bytes", type=int, default=0,
+                    help="full-image staging: bytes per pack launch (whole groups); 0 = the library default (one group)")
     ap.add_argument("--ceiling-bytes", type=int, default=8 << 30,
                     help="size of the contiguous fragment the pack ceiling is measured on")
     ap.add_argument("--image-file", default="",
@@ -497,7 +499,7 @@ class Optimizer:
             a.copy_(b)
 
 
-def pack_ceiling(torch, P, nbytes, chunk):
+def pack_ceiling(torch, P, nbytes, chunk, launch=0):
     """The same pack kernel over one contiguous, 16-byte-aligned fragment of
     nbytes (1 GiB launches, as for the shard): pack-only passes (the offload
     is cut before its first copy, so the link stays idle), each right after
@@ -505,7 +507,7 @@ def pack_ceiling(torch, P, nbytes, chunk):
     step), and each after a host synchronisation with the GPU idle."""
     buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
     buf.view(torch.int32).random_()
-    ck = P.Checkpointer([buf], chunk_bytes=chunk)
+    ck = P.Checkpointer([buf], chunk_bytes=chunk, pack_launch_bytes=launch)
     P.ckpt_set_timing(ck.ctx, True)
 
     def one(update):
@@ -536,7 +538,7 @@ def pack_ceiling(torch, P, nbytes, chunk):
 
 
 def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_steps=0, bounce=0, threads=0,
-                grid_blocks=0, staging=0, group=0, shared=None, gating="buckets", n_buckets=8):
+                grid_blocks=0, staging=0, group=0, shared=None, gating="buckets", n_buckets=8, launch=0):
     """Step-time overhead of per-step snapshots under a bf16 GEMM load.
 
     One step: R back-to-back GEMMs on the compute stream, then the optimizer
@@ -555,7 +557,8 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
         tensors, plan = W.make_state(wid, device="cuda")
         ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan],
                             chunk_bytes=W.WORKLOADS[wid]["chunk"], bounce_bytes=bounce, host_threads=threads,
-                            grid_blocks=grid_blocks, device_staging_bytes=staging, group_bytes=group)
+                            grid_blocks=grid_blocks, device_staging_bytes=staging, group_bytes=group,
+                            pack_launch_bytes=launch)
     else:
         tensors, plan, ck = shared
     n = len(tensors)
@@ -581,7 +584,7 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
         s = ck.snapshot(step=k)
         ck.wait_committed(s)
         tm = P.ckpt_last_timing(ck.ctx, P.CKPT_OP_SNAPSHOT)
-        ck_groups = tm["kernels"]
+        ck_groups = tm["kernels"]  # pack launches
         t = tm["total_ms"]
         if t <= 0:  # engine timestamps unavailable (a copy tracer owns the signals)
             t = ck.image_bytes / link_d2h_gbps / 1e6
@@ -642,7 +645,7 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
     out = {"workload": W.WORKLOADS[wid]["name"], "payload_bytes": sum(p[1] for p in plan), "gemm_mkn": [M, K, N],
            "host_images": "pageable, %d-byte pinned bounce rings" % bounce if bounce else "pinned",
            "device_staging": staging_text(staging, W.WORKLOADS[wid]["chunk"]),
-           "groups_per_snapshot": ck_groups,
+           "pack_launches_per_snapshot": ck_groups,
            "tile_kernel_workgroups": grid_blocks or "one per tile",
            "gating": "%d buckets, each behind ckpt_wait(CAPTURED) on its own fragments" % len(bks)
                      if gating == "buckets" else "one ckpt_wait(CAPTURED) on every fragment",
@@ -935,14 +938,14 @@ def main():
         ob = bounce if owid == wid else max(args.bounce_bytes, 0)
         ov = overlap_leg(torch, P, W, owid, args.overlap_steps, link["d2h"], ratios, args.overlap_base_steps, ob,
                          args.host_threads, args.grid_blocks, args.staging_bytes, args.group_bytes,
-                         gating=args.overlap_gating)
+                         gating=args.overlap_gating, launch=args.pack_launch_bytes)
         print(json.dumps({"overlap": ov, "d2h_link_peak_GBps": round(link["d2h"], 2)}), flush=True)
         return
     wl = W.WORKLOADS[wid]
     log("link peak")
     link = link_peak(torch)
     log("pack ceiling: one contiguous %d-byte fragment" % args.ceiling_bytes)
-    ceiling = pack_ceiling(torch, P, args.ceiling_bytes, wl["chunk"])
+    ceiling = pack_ceiling(torch, P, args.ceiling_bytes, wl["chunk"], args.pack_launch_bytes)
     log("generating workload", wl["name"])
     tensors, plan = W.make_state(wid, device="cuda")
     torch.cuda.synchronize()
@@ -957,7 +960,7 @@ def main():
     ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=wl["chunk"],
                         bounce_bytes=bounce, host_threads=args.host_threads,
                         image_file=args.image_file or None, device_staging_bytes=args.staging_bytes,
-                        group_bytes=args.group_bytes)
+                        group_bytes=args.group_bytes, pack_launch_bytes=args.pack_launch_bytes)
     P.ckpt_set_timing(ck.ctx, True)
     opt = Optimizer(torch, tensors)
     bks = buckets_of(plan, 8)
@@ -1062,7 +1065,8 @@ def main():
         shared = (tensors, plan, ck) if owid == wid else None
         overlap = overlap_leg(torch, P, W, owid, args.overlap_steps, link["d2h"], ratios, args.overlap_base_steps,
                               bounce if owid == wid else 0, args.host_threads, args.grid_blocks, args.staging_bytes,
-                              args.group_bytes, shared=shared, gating=args.overlap_gating)
+                              args.group_bytes, shared=shared, gating=args.overlap_gating,
+                              launch=args.pack_launch_bytes)
     ck.close()
     if args.image_file and os.path.exists(args.image_file):
         os.unlink(args.image_file)
@@ -1092,7 +1096,7 @@ def main():
                                    if args.image_file else
                                    "pageable, %d-byte pinned bounce rings" % bounce if bounce else "pinned"),
                    "device_staging": staging_text(args.staging_bytes, wl["chunk"]),
-                   "groups_per_snapshot": int(sn["kernels"]),
+                   "groups_per_snapshot": int(sn["copies"]), "pack_launches_per_snapshot": int(sn["kernels"]),
                    "parallelism": "one rank, one GPU"},
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -114,6 +114,12 @@ typedef struct {
                                       stream stays the caller's: it must stay valid until
                                       ckpt_destroy, which does not destroy it, and other work
                                       queued on it delays the pack.  Ignored by ckpt_peer_create. */
+    uint64_t pack_launch_bytes;    /* full-image staging: bytes packed per kernel launch, whole chunk
+                                      groups (each group still has its own DMA request); 0 = one
+                                      group per launch.  Larger launches spend less time between
+                                      launches (a snapshot's pack phase is shorter with the GPU
+                                      otherwise idle) but slow concurrent training kernels more.
+                                      Ring mode packs one group per launch. */
 } ckpt_config;
 
 typedef struct {
@@ -244,7 +250,8 @@ typedef struct {
     float kernel_ms;     /* sum of the tile-kernel launches' durations (pack, scatter or
                             checksum), from events recorded by the dispatch itself; the
                             small per-chunk reduce kernel is not included */
-    uint32_t kernels;    /* number of tile-kernel launches */
+    uint32_t kernels;    /* number of tile-kernel launches (a snapshot's pack launches cover
+                            pack_launch_bytes each) */
     uint32_t copies;     /* number of DMA copy requests (image bytes only) */
     float copy_ms;       /* first image copy start to last image copy end */
     float total_ms;      /* operation start (after the trigger) to its last event; for a

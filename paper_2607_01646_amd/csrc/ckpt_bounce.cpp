@@ -70,7 +70,7 @@ void pump_issue(ckpt_ctx* c)
         bool issued = false, counted = false;
         if (slot != UINT64_MAX) {
             issued = hsa_amd_memory_async_copy_on_engine(c->h_bout + slot * unit, c->img_agent[0], it.staging,
-                                                         c->gpu_agent, it.n, 1, &it.res->dep[it.g],
+                                                         c->gpu_agent, it.n, 1, &it.res->dep[it.g / c->LG * c->LG],
                                                          it.res->copied[it.g], it.engine, true) == HSA_STATUS_SUCCESS;
             if (!issued) what = "DMA of a chunk group to the bounce ring could not be issued";
             else

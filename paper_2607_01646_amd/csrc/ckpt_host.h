@@ -39,6 +39,7 @@ namespace ckpt {
 constexpr uint64_t kDefaultChunk = 64ull << 20;
 constexpr uint32_t kDefaultAlign = 256;
 constexpr uint64_t kDefaultGroup = 1ull << 30;
+constexpr uint64_t kDefaultLaunch = 0; // full-image staging: bytes per pack launch (0 = one group)
 constexpr uint32_t kMaxMeta = 1u << 20;
 constexpr uint32_t kDefaultGrid = 0x7fffffff; // one workgroup per tile unless capped
 constexpr int kMaxEngines = 2;
@@ -312,6 +313,9 @@ struct ckpt_ctx {
     Geometry geo{};
     uint64_t G = 1;        // chunks per group
     uint64_t n_groups = 0; // groups
+    uint64_t launch_cfg = kDefaultLaunch;
+    uint64_t LG = 1;         // groups per pack launch (1 in ring mode)
+    uint64_t n_launches = 0; // pack launches per snapshot
     bool ring = false;
     uint64_t n_slots = 0;  // ring slots of G chunks each (ring mode)
 

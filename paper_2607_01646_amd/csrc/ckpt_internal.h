@@ -38,13 +38,15 @@ constexpr uint32_t kMaxTileShift = 13;
 // chunks.  grid_cap bounds the workgroups (one per tile when the cap is
 // larger).  Non-null t0/t1 are timing events recorded around the dispatch
 // itself.
-//   pack:     fragment bytes -> image window; image byte x goes to dst + (x - dst_origin)
+//   pack:     fragment bytes -> image window; image byte x goes to dst + (x - dst_origin);
+//             a non-null release is an HSA signal value the launch sets to 0
+//             as it starts (after the stream's previous kernel finished)
 //   scatter:  image window -> fragment bytes (image byte x read at src + (x - src_origin))
 //   checksum: image window only
 hipError_t launch_pack(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
                        const Geometry& g, uint64_t t_lo, uint64_t t_hi, uint8_t* dst, uint64_t dst_origin,
                        unsigned long long* partials, uint32_t grid_cap, hipStream_t s, hipEvent_t t0 = nullptr,
-                       hipEvent_t t1 = nullptr);
+                       hipEvent_t t1 = nullptr, int64_t* release = nullptr);
 hipError_t launch_scatter(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
                           const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src, uint64_t src_origin,
                           unsigned long long* partials, uint32_t grid_cap, hipStream_t s, hipEvent_t t0 = nullptr,
@@ -55,10 +57,11 @@ hipError_t launch_checksum(const Geometry& g, uint64_t t_lo, uint64_t t_hi, cons
 
 // Chunk sums of the chunks covered by tiles [t_lo, t_hi): sums_out[c] is the
 // sum of the partial sums of the chunk's tiles.  With expected non-null, bad[c] is set to 1
-// where sums_out[c] != expected[c] (and to 0 elsewhere).
+// where sums_out[c] != expected[c] (and to 0 elsewhere).  A non-null release
+// is set to 0 as the launch starts, as for the pack.
 hipError_t launch_chunk_reduce(const Geometry& g, uint64_t t_lo, uint64_t t_hi, const unsigned long long* partials,
                                unsigned long long* sums_out, const unsigned long long* expected, uint8_t* bad,
-                               hipStream_t s);
+                               hipStream_t s, int64_t* release = nullptr);
 
 // Store 0 into *signal_value (an HSA signal's value) once the work enqueued
 // on s before this call has completed.

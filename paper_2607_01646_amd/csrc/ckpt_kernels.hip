@@ -59,6 +59,7 @@ struct Args {
     uint8_t* img; // PACK: destination window; SCATTER/VERIFY: source window
     uint64_t origin;
     unsigned long long* partials; // one sum per tile
+    int64_t* release;             // PACK: an HSA signal value to set to 0 at the start (or null)
 };
 
 struct ReduceArgs {
@@ -69,7 +70,23 @@ struct ReduceArgs {
     unsigned long long* sums_out; // PACK: chunk sums; SCATTER/VERIFY: recomputed sums
     const unsigned long long* expected; // null when only summing
     uint8_t* bad;
+    int64_t* release; // an HSA signal value to set to 0 at the start (or null)
 };
+
+// Lane 0 of workgroup 0 stores 0 into *release: a system-scope release of
+// "the kernels before this one on the stream have finished".  A kernel
+// starts only once the previous kernel of its stream has completed, and a
+// kernel's completion releases its writes at device scope (on a multi-XCD
+// part that writes the L2 back), so a DMA engine waiting for the signal
+// reads that kernel's bytes.  Carried by the next launch, it saves a
+// one-lane kernel and a dispatch gap per chunk group.  The tile kernel does
+// it after workgroup 0's tile: ahead of the tile, the test of the pointer
+// put a second dependent argument load in front of every workgroup's work.
+__device__ __forceinline__ void release_signal(int64_t* release)
+{
+    if (release && blockIdx.x == 0 && threadIdx.x == 0)
+        __hip_atomic_store(release, (int64_t)0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+}
 
 __device__ __forceinline__ unsigned long long vsum(u32x4 v)
 {
@@ -366,6 +383,7 @@ __global__ __launch_bounds__(BLOCK) void tile_kernel(Args a)
         const uint64_t t = a.t_lo + first;
         if (t < a.t_hi) do_tile<MODE, BLOCK, UNROLL, NTL, NTS>(a, t, s_off);
     }
+    if (MODE == PACK) release_signal(a.release);
 }
 
 // One workgroup per chunk: add the chunk's tile sums; when expected is given,
@@ -378,6 +396,7 @@ constexpr int kReduceUnroll = 8;
 __global__ __launch_bounds__(kReduceBlock) void chunk_reduce_kernel(ReduceArgs r)
 {
     __shared__ unsigned long long s_red[kReduceBlock / 64];
+    release_signal(r.release);
     const uint64_t c = r.c_lo + blockIdx.x;
     const uint64_t t0 = c * r.tiles_per_chunk;
     uint64_t t1 = t0 + r.tiles_per_chunk;
@@ -522,9 +541,10 @@ hipError_t launch_release(int64_t* signal_value, hipStream_t s)
 
 hipError_t launch_pack(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
                        const Geometry& g, uint64_t t_lo, uint64_t t_hi, uint8_t* dst, uint64_t dst_origin,
-                       unsigned long long* partials, uint32_t grid_cap, hipStream_t s, hipEvent_t t0, hipEvent_t t1)
+                       unsigned long long* partials, uint32_t grid_cap, hipStream_t s, hipEvent_t t0, hipEvent_t t1,
+                       int64_t* release)
 {
-    Args a{frags, tile_first, tile_last, g, t_lo, t_hi, dst, dst_origin, partials};
+    Args a{frags, tile_first, tile_last, g, t_lo, t_hi, dst, dst_origin, partials, release};
     return launch_tiles<PACK>(a, grid_cap, s, t0, t1);
 }
 
@@ -533,7 +553,7 @@ hipError_t launch_scatter(const FragDev* frags, const uint32_t* tile_first, cons
                           unsigned long long* partials, uint32_t grid_cap, hipStream_t s, hipEvent_t t0,
                           hipEvent_t t1)
 {
-    Args a{frags, tile_first, tile_last, g, t_lo, t_hi, const_cast<uint8_t*>(src), src_origin, partials};
+    Args a{frags, tile_first, tile_last, g, t_lo, t_hi, const_cast<uint8_t*>(src), src_origin, partials, nullptr};
     return launch_tiles<SCATTER>(a, grid_cap, s, t0, t1);
 }
 
@@ -541,13 +561,13 @@ hipError_t launch_checksum(const Geometry& g, uint64_t t_lo, uint64_t t_hi, cons
                            unsigned long long* partials, uint32_t grid_cap, hipStream_t s, hipEvent_t t0,
                            hipEvent_t t1)
 {
-    Args a{nullptr, nullptr, nullptr, g, t_lo, t_hi, const_cast<uint8_t*>(src), src_origin, partials};
+    Args a{nullptr, nullptr, nullptr, g, t_lo, t_hi, const_cast<uint8_t*>(src), src_origin, partials, nullptr};
     return launch_tiles<VERIFY>(a, grid_cap, s, t0, t1);
 }
 
 hipError_t launch_chunk_reduce(const Geometry& g, uint64_t t_lo, uint64_t t_hi, const unsigned long long* partials,
                                unsigned long long* sums_out, const unsigned long long* expected, uint8_t* bad,
-                               hipStream_t s)
+                               hipStream_t s, int64_t* release)
 {
     if (t_hi <= t_lo) return hipSuccess;
     ReduceArgs r;
@@ -559,6 +579,7 @@ hipError_t launch_chunk_reduce(const Geometry& g, uint64_t t_lo, uint64_t t_hi, 
     r.sums_out = sums_out;
     r.expected = expected;
     r.bad = bad;
+    r.release = release;
     hipLaunchKernelGGL(chunk_reduce_kernel, dim3((uint32_t)(r.c_hi - r.c_lo)), dim3(kReduceBlock), 0, s, r);
     return hipGetLastError();
 }

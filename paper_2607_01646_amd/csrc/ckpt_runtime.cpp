@@ -804,6 +804,7 @@ ckpt_status ckpt_create(const ckpt_config* cfg, ckpt_ctx** out)
     c->group_set = d.group_bytes != 0;
     c->grid_cap = d.grid_blocks ? d.grid_blocks : kDefaultGrid;
     c->bounce_cfg = d.bounce_bytes;
+    if (d.pack_launch_bytes) c->launch_cfg = d.pack_launch_bytes;
     c->host_threads = d.host_threads ? d.host_threads : kDefaultHostThreads;
     ckpt_status st = CKPT_OK;
     if (hipSetDevice(c->device) != hipSuccess)
@@ -909,6 +910,12 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
         c->G = std::max<uint64_t>(1, c->group_cfg / c->C);
     }
     c->n_groups = (c->n_chunks + c->G - 1) / c->G;
+    // Pack launches of whole groups (full-image staging): a larger launch
+    // spends less time in the gaps between launches, but slows concurrent
+    // training kernels more, so the default is one group per launch; each
+    // group keeps its own DMA request.  In ring mode a launch fills one slot.
+    c->LG = (c->ring || !c->launch_cfg) ? 1 : std::max<uint64_t>(1, c->launch_cfg / (c->G * c->C));
+    c->n_launches = (c->n_groups + c->LG - 1) / c->LG;
     if (c->ring) c->n_slots = std::max<uint64_t>(1, std::min<uint64_t>(c->staging_cap / (c->G * c->C), c->n_groups));
     const uint64_t unit = c->G * c->C; // bytes of one chunk group
     if (c->bounce_cfg) {
@@ -1120,7 +1127,11 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
 
 namespace ckpt {
 
-ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop)
+// The body of issue_snapshot.  `carried` is the signal of a group whose DMA
+// has been issued while the launch that will release it has not yet been
+// enqueued; on an error return the caller releases it from the host.
+ckpt_status issue_groups(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop,
+                         hsa_signal_t& carried)
 {
     RecRes* res = r.res;
     uint8_t* himg = c->h_img[r.buf];
@@ -1129,25 +1140,51 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
     HIPCHK(c, hipEventRecord(c->ev_trigger, after));
     HIPCHK(c, hipStreamWaitEvent(c->s_pack, c->ev_trigger, 0));
     if (r.timed) HIPCHK(c, hipEventRecord(res->t0, c->s_pack));
+    // Each launch packs LG groups; each copied group's DMA waits for the
+    // signal of its launch's first group to drop to 0.  With a full-size
+    // image the next launch on the pack stream (the next pack, or the
+    // chunk-sum reduce after the last) sets it, which happens only after this
+    // launch's pack has finished; in ring mode the next pack may first wait
+    // for a slot, so a one-lane kernel releases the group right after its
+    // pack instead.
+    const bool carry = !c->ring;
+    int64_t* pending = nullptr; // the previous launch's release, carried by the next launch
     for (uint64_t g = 0; g < c->n_groups; ++g) {
         const uint64_t lo = group_lo(c, g), hi = group_hi(c, g);
         const uint64_t area = area_of(c, g);
-        // The staging area is free once every copy issued out of it so far
-        // has finished (each finished copy bumps area_done by one).
-        if (c->area_seq[area])
-            HIPCHK(c, hipStreamWaitValue64(c->s_pack, c->d_area_done + area, c->area_seq[area],
-                                          hipStreamWaitValueGte, ~0ull));
-        hipError_t e = launch_pack(c->d_frags, c->d_tile_first, c->d_tile_last, c->geo, tiles_lo(c, g),
-                                   tiles_hi(c, g), staging_of(c, g), lo, c->d_partials, c->grid_cap, c->s_pack,
-                                   r.timed ? res->k0[g] : nullptr, r.timed ? res->k1[g] : nullptr);
-        if (e != hipSuccess) return fail(c, CKPT_EHIP, "pack launch failed: %s", hipGetErrorString(e));
-        // The gate and the group's copy need the packed bytes only; the chunk
-        // sums are added up once, after the last group (below).
-        HIPCHK(c, hipEventRecord(res->captured[g], c->s_pack));
-        if (g < n_copy) {
-            hsa_signal_store_screlease(res->dep[g], 1);
-            e = launch_release(res->dep_val[g], c->s_pack);
-            if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
+        const uint64_t j = g / c->LG;      // this group's launch
+        const uint64_t g0 = j * c->LG;     // its first group
+        const uint64_t g1 = std::min(g0 + c->LG, c->n_groups);
+        if (g == g0) {
+            // A staging area is free once every copy issued out of it so far
+            // has finished (each finished copy bumps area_done by one); the
+            // launch writes the areas of all its groups.
+            for (uint64_t h = g0; h < g1; ++h) {
+                const uint64_t a = area_of(c, h);
+                if (c->area_seq[a])
+                    HIPCHK(c, hipStreamWaitValue64(c->s_pack, c->d_area_done + a, c->area_seq[a],
+                                                  hipStreamWaitValueGte, ~0ull));
+            }
+            hipError_t e = launch_pack(c->d_frags, c->d_tile_first, c->d_tile_last, c->geo, tiles_lo(c, g0),
+                                       tiles_hi(c, g1 - 1), staging_of(c, g0), lo, c->d_partials, c->grid_cap,
+                                       c->s_pack, r.timed ? res->k0[j] : nullptr, r.timed ? res->k1[j] : nullptr,
+                                       pending);
+            if (e != hipSuccess) return fail(c, CKPT_EHIP, "pack launch failed: %s", hipGetErrorString(e));
+            pending = nullptr; // enqueued: the GPU releases it
+            carried.handle = 0;
+            // The gate and the launch's copies need the packed bytes only; the
+            // chunk sums are added up once, after the last launch (below).
+            HIPCHK(c, hipEventRecord(res->captured[g1 - 1], c->s_pack));
+            if (g0 < n_copy) {
+                hsa_signal_store_screlease(res->dep[g0], 1); // before any copy is issued or a launch clears it
+                if (carry) {
+                    pending = res->dep_val[g0];
+                    carried = res->dep[g0];
+                } else {
+                    e = launch_release(res->dep_val[g0], c->s_pack);
+                    if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
+                }
+            }
         }
         if (g >= n_copy) continue; // interrupted offload: this group never leaves the device
         hsa_signal_store_screlease(res->copied[g], 1);
@@ -1174,7 +1211,7 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
             ++c->area_seq[area];
             continue;
         }
-        st = dma(c, himg + lo, host, staging_of(c, g), c->gpu_agent, hi - lo, &res->dep[g], res->copied[g], eng);
+        st = dma(c, himg + lo, host, staging_of(c, g), c->gpu_agent, hi - lo, &res->dep[g0], res->copied[g], eng);
         if (!st)
             st = dma(c, c->d_area_done + area, c->gpu_agent, &res->h_seq[g], host, 8, &res->copied[g],
                      res->flagged[g], c->h2d_engine);
@@ -1188,13 +1225,19 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
     }
     if (stop >= 0) {
         r.aborted = true; // interrupted offload: never committed (its pack timing stays readable)
+        if (pending) {    // the last copied group was the last group
+            hipError_t e = launch_release(pending, c->s_pack);
+            if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
+            carried.handle = 0;
+        }
     } else {
         // Every chunk's sum from its tiles' partial sums, in one launch: only
         // the sums copy below needs them, and one launch per group would cost
-        // the caller host time per group.
+        // the caller host time per group.  It also releases the last group.
         hipError_t e = launch_chunk_reduce(c->geo, 0, c->geo.n_tiles, c->d_partials, res->d_sums, nullptr, nullptr,
-                                           c->s_pack);
+                                           c->s_pack, pending);
         if (e != hipSuccess) return fail(c, CKPT_EHIP, "reduce launch failed: %s", hipGetErrorString(e));
+        carried.handle = 0;
         hsa_signal_store_screlease(res->dep_sums, 1);
         e = launch_release(res->dep_sums_val, c->s_pack);
         if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
@@ -1237,6 +1280,16 @@ ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t 
         }
     }
     return CKPT_OK;
+}
+
+ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop)
+{
+    hsa_signal_t carried{0};
+    const ckpt_status st = issue_groups(c, r, after, n_copy, stop, carried);
+    // A DMA whose release never got enqueued would wait forever: let it run
+    // (the snapshot is marked interrupted and is never restored).
+    if (st && carried.handle) hsa_signal_store_screlease(carried, 0);
+    return st;
 }
 
 } // namespace ckpt
@@ -1309,7 +1362,8 @@ ckpt_status ckpt_wait(ckpt_ctx* c, uint64_t snap_id, uint32_t mode, void* stream
     }
     if (!any) return CKPT_OK; // only empty fragments: nothing to protect
     const uint64_t g = last / (c->G * c->C);
-    HIPCHK(c, hipStreamWaitEvent((hipStream_t)stream, r.res->captured[g], 0));
+    const uint64_t gl = std::min((g / c->LG + 1) * c->LG, c->n_groups) - 1; // its launch's last group
+    HIPCHK(c, hipStreamWaitEvent((hipStream_t)stream, r.res->captured[gl], 0));
     return CKPT_OK;
 }
 
@@ -1439,7 +1493,7 @@ namespace ckpt {
 // and its release (an interrupted snapshot has no reduce: to its last pack).
 float pack_span(ckpt_ctx* c, const SnapRec& r)
 {
-    hipEvent_t end = r.aborted ? r.res->k1[c->n_groups - 1] : r.res->t_red;
+    hipEvent_t end = r.aborted ? r.res->k1[c->n_launches - 1] : r.res->t_red;
     if (hipEventSynchronize(end) != hipSuccess) return -1.f;
     return elapsed(r.res->k0[0], end);
 }
@@ -1454,10 +1508,10 @@ ckpt_status ckpt_last_timing(ckpt_ctx* c, uint32_t which, ckpt_timing* out)
             if (kv.second.timed && (!best || kv.first > best->id)) best = &kv.second;
         if (!best) return fail(c, CKPT_ESTATE, "no timed snapshot retained");
         RecRes* r = best->res;
-        HIPCHK(c, hipEventSynchronize(r->k1[c->n_groups - 1])); // packs run in order on one stream
+        HIPCHK(c, hipEventSynchronize(r->k1[c->n_launches - 1])); // packs run in order on one stream
         ckpt_timing t{};
-        for (uint64_t g = 0; g < c->n_groups; ++g) t.kernel_ms += elapsed(r->k0[g], r->k1[g]);
-        t.kernels = (uint32_t)c->n_groups;
+        for (uint64_t j = 0; j < c->n_launches; ++j) t.kernel_ms += elapsed(r->k0[j], r->k1[j]);
+        t.kernels = (uint32_t)c->n_launches;
         t.copy_ms = -1.f;
         t.total_ms = -1.f;
         t.kernel_bytes = 2 * c->payload;
@@ -1474,8 +1528,8 @@ ckpt_status ckpt_last_timing(ckpt_ctx* c, uint32_t which, ckpt_timing* out)
         if (st) return st;
         RecRes* r = best->res;
         ckpt_timing t{};
-        for (uint64_t g = 0; g < c->n_groups; ++g) t.kernel_ms += elapsed(r->k0[g], r->k1[g]);
-        t.kernels = (uint32_t)c->n_groups;
+        for (uint64_t j = 0; j < c->n_launches; ++j) t.kernel_ms += elapsed(r->k0[j], r->k1[j]);
+        t.kernels = (uint32_t)c->n_launches;
         t.copies = (uint32_t)c->n_groups;
         t.span_ms = pack_span(c, *best);
         // DMA span: first image copy start to last image copy end (engine timestamps).
@@ -1491,7 +1545,7 @@ ckpt_status ckpt_last_timing(ckpt_ctx* c, uint32_t which, ckpt_timing* out)
             t_end = std::max<uint64_t>(t_end, ct.end);
         }
         t.copy_ms = (ok && t_end > t_start) ? (float)((double)(t_end - t_start) * 1e3 / (double)c->ts_freq) : -1.f;
-        // Trigger to commit: the first group's pack, then from its copy's
+        // Trigger to commit: the first launch's pack, then from its copy's
         // start to the commit -- the last of: the last group copy's end, the
         // sums copy's end and, with pageable images, the last group landing in
         // the image (and the file record).  One clock throughout except the

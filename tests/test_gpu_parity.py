@@ -22,6 +22,17 @@ if torch.cuda.is_available():
     import paper_2607_01646_amd as P
 
 
+@pytest.mark.parametrize("chunk,align,staging,group,launch", [
+    (4096, 256, 0, 4096, 3 * 4096),    # pack launches of three one-chunk groups, each group its own copy
+    (8192, 256, 0, 2 * 8192, 5 * 8192),  # launch size rounded down to two groups of two chunks
+    (4096, 16, 0, 4096, 1),            # launch smaller than a group: one group per launch
+])
+def test_edge_sizes_multi_group_launches(chunk, align, staging, group, launch):
+    tensors, host = random_byte_fragments(EDGE_SIZES, seed=chunk + launch)
+    ck, _ = snapshot_and_check(tensors, host, chunk, align, staging, group, launch=launch)
+    ck.close()
+
+
 @pytest.mark.parametrize("chunk,align,staging,group", [
     (4096, 256, 0, 0),                 # many chunks, one launch
     (4096, 256, 0, 3 * 4096),          # three chunks per launch and copy
@@ -220,6 +231,37 @@ GATE_STAGING = [0, 16 << 20]
 GATE_CHUNK = 1 << 20
 
 
+@pytest.mark.parametrize("launch", [3 << 20, 8 << 20])
+def test_gate_with_multi_group_launches(launch):
+    """Full-image staging with one-chunk groups packed several per launch:
+    the gate on fragments [0, 8) waits for the launch holding their last
+    chunk; an update of those fragments right after it stays out of the
+    image, and so does an update of everything after a whole-range wait."""
+    tensors = _step_state(n_frag=96)
+    ck = P.Checkpointer(tensors, chunk_bytes=GATE_CHUNK, group_bytes=GATE_CHUNK, pack_launch_bytes=launch)
+    main, side = torch.cuda.current_stream(), torch.cuda.Stream()
+    for lo, hi in [(0, 8), (0, len(tensors))]:
+        torch.cuda.synchronize()
+        before = [host_bytes(t) for t in tensors]
+        keep = _hold(main)
+        s = ck.snapshot(step=hi, stream=main)
+        ck.wait_captured(s, lo, hi, stream=side)
+        with torch.cuda.stream(side):
+            for t in tensors[lo:hi]:
+                t.mul_(-1.0)
+        ck.wait_committed(s)
+        img, sums = ck.host_image(s)
+        want, _, _ = O.pack(before, 256, GATE_CHUNK)
+        off = ck.offsets
+        end = int(off[hi - 1]) + before[hi - 1].size
+        assert np.array_equal(img[:end], want[:end])
+        if hi == len(tensors):
+            assert np.array_equal(sums, O.chunk_sums(want, 0, want.size, GATE_CHUNK))
+        torch.cuda.synchronize()
+        del keep
+    ck.close()
+
+
 @pytest.mark.parametrize("staging", GATE_STAGING)
 def test_gate_orders_optimizer_after_capture(staging):
     """The wait before the optimizer step: an in-place update launched on
@@ -404,11 +446,13 @@ def test_side_stream_carries_the_pack():
         del keep_side, keep_main
 
 
-def test_interrupted_snapshot_is_never_restored():
+@pytest.mark.parametrize("launch", [0, 3 << 18])
+def test_interrupted_snapshot_is_never_restored(launch):
     """Invariant I4: an offload interrupted after two chunk groups stays
-    ABORTED; restore returns the previous committed snapshot."""
+    ABORTED; restore returns the previous committed snapshot.  With three
+    groups per pack launch the interruption falls inside a launch."""
     tensors = _step_state(n_frag=16, numel=1 << 18)
-    ck = P.Checkpointer(tensors, chunk_bytes=1 << 18, group_bytes=1 << 18)
+    ck = P.Checkpointer(tensors, chunk_bytes=1 << 18, group_bytes=1 << 18, pack_launch_bytes=launch)
     s1 = ck.snapshot(step=1)
     ck.wait_committed(s1)
     good = [host_bytes(t) for t in tensors]
