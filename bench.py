@@ -1,6 +1,6 @@
 """Benchmark of the in-memory snapshot hot path on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--no-overlap] [--no-cpu] [--gating]
+    python bench.py [--steps K] [--warmup W] [--no-overlap] [--no-cpu] [--no-gating]
 
 One step is one pass of the whole path over one rank's state shard -- by
 default the 7B LLaMA shard (32 layers, hidden 4096, FFN 11008: 1164
@@ -28,8 +28,8 @@ measured peak (plain pinned 1 GiB copies in the same process);
 restore/verify rates; the step-time overhead of a snapshot every step for 50
 steps under the shard's bf16 GEMM load (8192x4096x11008), timed per the
 paper's Sec. VII-B per-iteration statistic; and the CPU oracle on a bounded
-sample.  --gating adds the comparison of per-bucket and whole-range waits
-with a staging ring (one rank of a 65B model under TP=8 x PP=8).
+sample, and the comparison of per-bucket and whole-range waits before the
+update with a staging ring (one rank of a 65B model under TP=8 x PP=8).
 """
 import argparse
 import json
@@ -66,15 +66,18 @@ def parse():
                          "on every fragment")
     ap.add_argument("--overlap-only", action="store_true",
                     help="run only the overlap leg and print its JSON")
-    ap.add_argument("--gating", action="store_true",
-                    help="also run the gate-granularity comparison (per-bucket against whole-range waits with a "
+    ap.add_argument("--no-gating", action="store_true",
+                    help="skip the gate-granularity comparison (per-bucket against whole-range waits with a "
                          "staging ring)")
     ap.add_argument("--gating-only", action="store_true", help="run only the gate-granularity comparison")
     ap.add_argument("--gating-workload", type=int, default=3)
-    ap.add_argument("--gating-ratios", default="0.5,0.75,1.0,1.5")
-    ap.add_argument("--gating-steps", type=int, default=25)
-    ap.add_argument("--gating-base-steps", type=int, default=15)
-    ap.add_argument("--gating-staging-bytes", type=int, default=1 << 30)
+    ap.add_argument("--gating-ratios", default="0.75",
+                    help="compute window / snapshot time ratios of the gate comparison (the full sweep: "
+                         "0.5,0.75,1.0,1.5)")
+    ap.add_argument("--gating-steps", type=int, default=20)
+    ap.add_argument("--gating-base-steps", type=int, default=12)
+    ap.add_argument("--gating-staging-bytes", type=int, default=256 << 20,
+                    help="staging ring of the gate comparison (default: four one-chunk slots)")
     ap.add_argument("--bounce-bytes", type=int, default=-1,
                     help="pageable host images behind pinned bounce rings of this many bytes; 0 = pinned images; "
                          "-1 = 8 GiB rings for workload 4 (two 94.3 GB images exceed the pinned memory the host "
@@ -685,7 +688,8 @@ def gating_leg(torch, P, W, wid, ratios, steps, base_steps, staging, n_buckets=8
         for mode in ("whole", "buckets"):
             res[mode] = overlap_leg(torch, P, W, wid, steps, link, (ratio,), base_steps, shared=shared, gating=mode,
                                     n_buckets=n_buckets)
-        rows.append({"window_over_d2h": ratio, "R": res["whole"]["R"],
+        rows.append({"window_over_d2h": ratio, "R": res["whole"]["R"], "gemm_ms": res["whole"]["gemm_ms"],
+                     "update_ms": round(res["whole"]["base_ms"] - res["whole"]["R"] * res["whole"]["gemm_ms"], 2),
                      "base_ms": res["whole"]["base_ms"],
                      "whole_range_ms": res["whole"]["with_snapshot_ms"],
                      "whole_range_overhead_pct": res["whole"]["overhead_pct"],
@@ -1073,7 +1077,7 @@ def main():
     del tensors
     torch.cuda.empty_cache()
     gating = None
-    if args.gating:
+    if not args.no_gating:
         log("gating leg")
         gating = gating_leg(torch, P, W, args.gating_workload, [float(r) for r in args.gating_ratios.split(",") if r],
                             args.gating_steps, args.gating_base_steps, args.gating_staging_bytes)
