@@ -540,8 +540,30 @@ def pack_ceiling(torch, P, nbytes, chunk, launch=0):
     return out
 
 
+def standalone_snapshot(P, ck, link_d2h_gbps, runs=3, warm=1):
+    """Snapshot time alone, trigger to commit: the median of `runs` snapshots
+    after `warm` warm-up snapshots (the first snapshots of a context also set
+    up its records).  Returns (median ms, [runs ms], [DMA spans ms], pack
+    launches per snapshot)."""
+    P.ckpt_set_timing(ck.ctx, True)
+    t_runs, copy_runs = [], []
+    for k in range(warm + runs):
+        s = ck.snapshot(step=k)
+        ck.wait_committed(s)
+        tm = P.ckpt_last_timing(ck.ctx, P.CKPT_OP_SNAPSHOT)
+        t = tm["total_ms"]
+        if t <= 0:  # engine timestamps unavailable (a copy tracer owns the signals)
+            t = ck.image_bytes / link_d2h_gbps / 1e6
+        if k >= warm:
+            t_runs.append(t)
+            copy_runs.append(tm["copy_ms"])
+    P.ckpt_set_timing(ck.ctx, False)
+    return sorted(t_runs)[len(t_runs) // 2], t_runs, copy_runs, tm["kernels"]
+
+
 def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_steps=0, bounce=0, threads=0,
-                grid_blocks=0, staging=0, group=0, shared=None, gating="buckets", n_buckets=8, launch=0):
+                grid_blocks=0, staging=0, group=0, shared=None, gating="buckets", n_buckets=8, launch=0,
+                snap=None):
     """Step-time overhead of per-step snapshots under a bf16 GEMM load.
 
     One step: R back-to-back GEMMs on the compute stream, then the optimizer
@@ -578,24 +600,8 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
     e1.record()
     e1.synchronize()
     t_gemm = e0.elapsed_time(e1) / 50
-    P.ckpt_set_timing(ck.ctx, True)
-    # Standalone snapshot (trigger to commit): the median of three after a
-    # warm-up snapshot (the first snapshot of a context also sets up its
-    # records).
-    d2h_runs, copy_runs = [], []
-    for k in range(4):
-        s = ck.snapshot(step=k)
-        ck.wait_committed(s)
-        tm = P.ckpt_last_timing(ck.ctx, P.CKPT_OP_SNAPSHOT)
-        ck_groups = tm["kernels"]  # pack launches
-        t = tm["total_ms"]
-        if t <= 0:  # engine timestamps unavailable (a copy tracer owns the signals)
-            t = ck.image_bytes / link_d2h_gbps / 1e6
-        if k:
-            d2h_runs.append(t)
-            copy_runs.append(tm["copy_ms"])
-    t_d2h = sorted(d2h_runs)[1]
-    P.ckpt_set_timing(ck.ctx, False)
+    # Standalone snapshot (trigger to commit), unless the caller measured it
+    t_d2h, d2h_runs, copy_runs, ck_groups = snap or standalone_snapshot(P, ck, link_d2h_gbps)
     opt = Optimizer(torch, tensors)
     bks = buckets_of(plan, n_buckets)
     calls = []  # host time of each snapshot call
@@ -683,11 +689,12 @@ def gating_leg(torch, P, W, wid, ratios, steps, base_steps, staging, n_buckets=8
     shared = (tensors, plan, ck)
     rows = []
     link = link_peak(torch)["d2h"]
+    snap = standalone_snapshot(P, ck, link, runs=3, warm=2)  # one R for both modes
     for ratio in ratios:
         res = {}
         for mode in ("whole", "buckets"):
             res[mode] = overlap_leg(torch, P, W, wid, steps, link, (ratio,), base_steps, shared=shared, gating=mode,
-                                    n_buckets=n_buckets)
+                                    n_buckets=n_buckets, snap=snap)
         rows.append({"window_over_d2h": ratio, "R": res["whole"]["R"], "gemm_ms": res["whole"]["gemm_ms"],
                      "update_ms": round(res["whole"]["base_ms"] - res["whole"]["R"] * res["whole"]["gemm_ms"], 2),
                      "base_ms": res["whole"]["base_ms"],
@@ -696,6 +703,8 @@ def gating_leg(torch, P, W, wid, ratios, steps, base_steps, staging, n_buckets=8
                      "per_bucket_base_ms": res["buckets"]["base_ms"],
                      "per_bucket_ms": res["buckets"]["with_snapshot_ms"],
                      "per_bucket_overhead_pct": res["buckets"]["overhead_pct"],
+                     "per_bucket_saves_ms": round(res["whole"]["with_snapshot_ms"]
+                                                  - res["buckets"]["with_snapshot_ms"], 2),
                      "snapshot_ms": res["whole"]["snapshot_ms"]})
         log("gating: ratio %.2f: whole range %+.2f%%, per bucket %+.2f%%" % (
             ratio, rows[-1]["whole_range_overhead_pct"], rows[-1]["per_bucket_overhead_pct"]))
