@@ -92,6 +92,8 @@ def parse():
                          "and overlap legs)")
     ap.add_argument("--pack-launch-bytes", type=int, default=0,
                     help="full-image staging: bytes per pack launch (whole groups); 0 = the library default (one group)")
+    ap.add_argument("--d2h-engines", type=int, default=0, help="DMA engines of the snapshot copies (0 = library default)")
+    ap.add_argument("--overlap-R", type=int, default=0, help="overlap leg: GEMMs per step (0 = from the ratio)")
     ap.add_argument("--ceiling-bytes", type=int, default=8 << 30,
                     help="size of the contiguous fragment the pack ceiling is measured on")
     ap.add_argument("--image-file", default="",
@@ -563,7 +565,7 @@ def standalone_snapshot(P, ck, link_d2h_gbps, runs=3, warm=1):
 
 def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_steps=0, bounce=0, threads=0,
                 grid_blocks=0, staging=0, group=0, shared=None, gating="buckets", n_buckets=8, launch=0,
-                snap=None):
+                snap=None, engines=0, fixed_R=0):
     """Step-time overhead of per-step snapshots under a bf16 GEMM load.
 
     One step: R back-to-back GEMMs on the compute stream, then the optimizer
@@ -583,7 +585,7 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
         ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan],
                             chunk_bytes=W.WORKLOADS[wid]["chunk"], bounce_bytes=bounce, host_threads=threads,
                             grid_blocks=grid_blocks, device_staging_bytes=staging, group_bytes=group,
-                            pack_launch_bytes=launch)
+                            pack_launch_bytes=launch, d2h_engines=engines)
     else:
         tensors, plan, ck = shared
     n = len(tensors)
@@ -635,7 +637,7 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
 
     sweep = []
     for ratio in ratios:
-        R = int(math.ceil(ratio * t_d2h / t_gemm))
+        R = fixed_R or int(math.ceil(ratio * t_d2h / t_gemm))
         log("overlap: ratio %.2f, R = %d GEMMs per step" % (ratio, R))
         base1 = run(False, R, base_steps, None)
         withs = run(True, R, steps, gating)
@@ -951,7 +953,8 @@ def main():
         ob = bounce if owid == wid else max(args.bounce_bytes, 0)
         ov = overlap_leg(torch, P, W, owid, args.overlap_steps, link["d2h"], ratios, args.overlap_base_steps, ob,
                          args.host_threads, args.grid_blocks, args.staging_bytes, args.group_bytes,
-                         gating=args.overlap_gating, launch=args.pack_launch_bytes)
+                         gating=args.overlap_gating, launch=args.pack_launch_bytes, engines=args.d2h_engines,
+                         fixed_R=args.overlap_R)
         print(json.dumps({"overlap": ov, "d2h_link_peak_GBps": round(link["d2h"], 2)}), flush=True)
         return
     wl = W.WORKLOADS[wid]
@@ -973,7 +976,8 @@ def main():
     ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=wl["chunk"],
                         bounce_bytes=bounce, host_threads=args.host_threads,
                         image_file=args.image_file or None, device_staging_bytes=args.staging_bytes,
-                        group_bytes=args.group_bytes, pack_launch_bytes=args.pack_launch_bytes)
+                        group_bytes=args.group_bytes, pack_launch_bytes=args.pack_launch_bytes,
+                        d2h_engines=args.d2h_engines)
     P.ckpt_set_timing(ck.ctx, True)
     opt = Optimizer(torch, tensors)
     bks = buckets_of(plan, 8)
@@ -1082,7 +1086,7 @@ def main():
         overlap = overlap_leg(torch, P, W, owid, args.overlap_steps, link["d2h"], ratios, args.overlap_base_steps,
                               bounce if owid == wid else 0, args.host_threads, args.grid_blocks, args.staging_bytes,
                               args.group_bytes, shared=shared, gating=args.overlap_gating,
-                              launch=args.pack_launch_bytes)
+                              launch=args.pack_launch_bytes, engines=args.d2h_engines, fixed_R=args.overlap_R)
     ck.close()
     if args.image_file and os.path.exists(args.image_file):
         os.unlink(args.image_file)

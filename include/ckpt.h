@@ -120,6 +120,10 @@ typedef struct {
                                       launches (a snapshot's pack phase is shorter with the GPU
                                       otherwise idle) but slow concurrent training kernels more.
                                       Ring mode packs one group per launch. */
+    uint32_t d2h_engines;          /* DMA engines the snapshot's group copies alternate over; 0 = all
+                                      the device offers for device-to-host copies (up to 2).  One
+                                      engine reaches ~41 GB/s on the MI355X, two the host link's
+                                      ~57 GB/s. */
 } ckpt_config;
 
 typedef struct {

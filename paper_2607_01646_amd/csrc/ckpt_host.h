@@ -341,6 +341,7 @@ struct ckpt_ctx {
     hsa_agent_t gpu_agent{0}, img_agent[2] = {{0}, {0}};
     hsa_amd_sdma_engine_id_t d2h_engine[kMaxEngines];
     int n_d2h_engines = 0;
+    uint32_t d2h_engines_cfg = 0; // 0 = all available (up to kMaxEngines)
     hsa_amd_sdma_engine_id_t h2d_engine{};
     uint64_t ts_freq = 1;
 

@@ -206,7 +206,8 @@ ckpt_status setup_image_agent(ckpt_ctx* c, int b, const void* pinned)
         uint32_t mask = 0;
         HSACHK(c, hsa_amd_memory_copy_engine_status(c->img_agent[0], c->gpu_agent, &mask));
         c->n_d2h_engines = 0;
-        for (int k = 0; k < 16 && c->n_d2h_engines < kMaxEngines; ++k)
+        const int cap = c->d2h_engines_cfg ? std::min<int>((int)c->d2h_engines_cfg, kMaxEngines) : kMaxEngines;
+        for (int k = 0; k < 16 && c->n_d2h_engines < cap; ++k)
             if (mask & (1u << k)) c->d2h_engine[c->n_d2h_engines++] = (hsa_amd_sdma_engine_id_t)(1u << k);
         if (c->n_d2h_engines == 0) return fail(c, CKPT_EHIP, "no DMA engine available for device-to-host copies");
         // The 8-byte staging-counter copies (host -> device) get an engine
@@ -805,6 +806,7 @@ ckpt_status ckpt_create(const ckpt_config* cfg, ckpt_ctx** out)
     c->grid_cap = d.grid_blocks ? d.grid_blocks : kDefaultGrid;
     c->bounce_cfg = d.bounce_bytes;
     if (d.pack_launch_bytes) c->launch_cfg = d.pack_launch_bytes;
+    c->d2h_engines_cfg = d.d2h_engines;
     c->host_threads = d.host_threads ? d.host_threads : kDefaultHostThreads;
     ckpt_status st = CKPT_OK;
     if (hipSetDevice(c->device) != hipSuccess)
