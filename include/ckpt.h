@@ -124,7 +124,15 @@ typedef struct {
                                       the device offers for device-to-host copies (up to 2).  One
                                       engine reaches ~41 GB/s on the MI355X, two the host link's
                                       ~57 GB/s. */
+    uint32_t poison;               /* debug check: nonzero = before a staging area is packed again
+                                      (after its previous copy has left the device), fill it with the
+                                      16-byte canary CKPT_CANARY; with correct ordering the pack
+                                      overwrites every byte first, so the canary never reaches a
+                                      host image.  Costs one extra write of the staging per snapshot. */
 } ckpt_config;
+
+/* The canary of ckpt_config.poison: these 16 bytes, repeated. */
+#define CKPT_CANARY "\xde\xad\xc0\xde\x5a\x5a\xa5\xa5" "CKPTPOIS"
 
 typedef struct {
     const void* dev_ptr; /* device address of the fragment's first byte; any alignment */

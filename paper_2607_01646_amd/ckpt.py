@@ -40,6 +40,7 @@ CKPT_OP_SNAPSHOT = 0
 CKPT_OP_RESTORE = 1
 CKPT_OP_VERIFY = 2
 CKPT_OP_PACK = 3
+CKPT_CANARY = bytes([0xDE, 0xAD, 0xC0, 0xDE, 0x5A, 0x5A, 0xA5, 0xA5]) + b"CKPTPOIS"
 
 _NAMES = {v: k for k, v in dict(globals()).items() if k.startswith("CKPT_E")}
 
@@ -48,7 +49,8 @@ class ckpt_config(C.Structure):
     _fields_ = [("chunk_bytes", C.c_uint64), ("align_bytes", C.c_uint32), ("host_buffers", C.c_uint32),
                 ("device_staging_bytes", C.c_uint64), ("group_bytes", C.c_uint64), ("device", C.c_int32),
                 ("grid_blocks", C.c_uint32), ("bounce_bytes", C.c_uint64), ("host_threads", C.c_uint32),
-                ("side_stream", C.c_void_p), ("pack_launch_bytes", C.c_uint64), ("d2h_engines", C.c_uint32)]
+                ("side_stream", C.c_void_p), ("pack_launch_bytes", C.c_uint64), ("d2h_engines", C.c_uint32),
+                ("poison", C.c_uint32)]
 
 
 class ckpt_tensor(C.Structure):
@@ -158,14 +160,14 @@ def _u32p(a):
 
 
 def ckpt_create(chunk_bytes=0, align_bytes=0, device_staging_bytes=0, group_bytes=0, device=None, grid_blocks=0,
-                bounce_bytes=0, host_threads=0, side_stream=None, pack_launch_bytes=0, d2h_engines=0):
+                bounce_bytes=0, host_threads=0, side_stream=None, pack_launch_bytes=0, d2h_engines=0, poison=False):
     """side_stream: a torch stream (or raw handle) for the pack kernels; None =
     the library's own.  The caller keeps it alive while the context lives."""
     if device is None:
         device = torch.cuda.current_device()
     cfg = ckpt_config(chunk_bytes, align_bytes, 0, device_staging_bytes, group_bytes, device, grid_blocks,
                       bounce_bytes, host_threads, _stream(side_stream).value if side_stream is not None else None,
-                      pack_launch_bytes, d2h_engines)
+                      pack_launch_bytes, d2h_engines, 1 if poison else 0)
     ctx = C.c_void_p()
     rc = lib().ckpt_create(C.byref(cfg), C.byref(ctx))
     if rc != CKPT_OK:
@@ -466,7 +468,7 @@ class Peer:
     def __init__(self, port=0, device=None, group_bytes=0):
         if device is None:
             device = torch.cuda.current_device()
-        cfg = ckpt_config(0, 0, 0, 0, group_bytes, device, 0, 0, 0, None, 0, 0)
+        cfg = ckpt_config(0, 0, 0, 0, group_bytes, device, 0, 0, 0, None, 0, 0, 0)
         self.p = C.c_void_p()
         rc = lib().ckpt_peer_create(C.byref(cfg), port, C.byref(self.p))
         if rc != CKPT_OK:
@@ -551,11 +553,12 @@ class Checkpointer:
 
     def __init__(self, tensors, dtypes=None, classes=None, chunk_bytes=0, align_bytes=0, device_staging_bytes=0,
                  group_bytes=0, grid_blocks=0, device=None, bounce_bytes=0, host_threads=0, image_file=None,
-                 image_file_mode=CKPT_FILE_CREATE, side_stream=None, pack_launch_bytes=0, d2h_engines=0):
+                 image_file_mode=CKPT_FILE_CREATE, side_stream=None, pack_launch_bytes=0, d2h_engines=0,
+                 poison=False):
         self.tensors = list(tensors)
         self.side_stream = side_stream  # kept alive with the context
         self.ctx = ckpt_create(chunk_bytes, align_bytes, device_staging_bytes, group_bytes, device, grid_blocks,
-                               bounce_bytes, host_threads, side_stream, pack_launch_bytes, d2h_engines)
+                               bounce_bytes, host_threads, side_stream, pack_launch_bytes, d2h_engines, poison)
         try:
             if image_file is not None:
                 ckpt_image_file(self.ctx, image_file, image_file_mode)

@@ -342,6 +342,7 @@ struct ckpt_ctx {
     hsa_amd_sdma_engine_id_t d2h_engine[kMaxEngines];
     int n_d2h_engines = 0;
     uint32_t d2h_engines_cfg = 0; // 0 = all available (up to kMaxEngines)
+    bool poison = false;          // fill each staging area with the canary before it is packed again
     hsa_amd_sdma_engine_id_t h2d_engine{};
     uint64_t ts_freq = 1;
 

@@ -67,6 +67,10 @@ hipError_t launch_chunk_reduce(const Geometry& g, uint64_t t_lo, uint64_t t_hi, 
 // on s before this call has completed.
 hipError_t launch_release(int64_t* signal_value, hipStream_t s);
 
+// Fill [p, p + n) (p 16-byte aligned, n a multiple of 16) with the 16-byte
+// pattern w (the staging canary of ckpt_config.poison).
+hipError_t launch_fill16(uint8_t* p, uint64_t n, const uint32_t w[4], hipStream_t s);
+
 // ---- The allocation-free pack (ckpt_pack_noalloc) ----
 // Its tables and partial sums live in a fixed device array of the kernel
 // file (one per GPU, held until the process ends), laid out as: the fragment

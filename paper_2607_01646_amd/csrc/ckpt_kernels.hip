@@ -35,6 +35,7 @@
 // tiles gives the same bits.
 #include <hip/hip_ext.h>
 
+#include <algorithm>
 #include <mutex>
 
 #include "ckpt_internal.h"
@@ -445,6 +446,12 @@ __global__ void release_signal_kernel(int64_t* value)
     __hip_atomic_store(value, (int64_t)0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
+__global__ __launch_bounds__(256) void fill16_kernel(u32x4* p, uint64_t n16, u32x4 w)
+{
+    for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n16; k += (uint64_t)gridDim.x * blockDim.x)
+        p[k] = w;
+}
+
 // ---- allocation-free pack: scratch, table upload, tile table ----
 
 struct FragBatch {
@@ -510,6 +517,21 @@ hipError_t noalloc_scratch(uint8_t** ptr)
     }
     *ptr = addr[dev];
     return hipSuccess;
+}
+
+hipError_t launch_fill16(uint8_t* p, uint64_t n, const uint32_t w[4], hipStream_t s)
+{
+    if (n == 0) return hipSuccess;
+    if (((uintptr_t)p & 15) || (n & 15)) return hipErrorInvalidValue;
+    u32x4 v;
+    v.x = w[0];
+    v.y = w[1];
+    v.z = w[2];
+    v.w = w[3];
+    const uint64_t n16 = n >> 4;
+    const uint64_t blocks = std::min<uint64_t>((n16 + 255) / 256, 8192);
+    hipLaunchKernelGGL(fill16_kernel, dim3((uint32_t)blocks), dim3(256), 0, s, reinterpret_cast<u32x4*>(p), n16, v);
+    return hipGetLastError();
 }
 
 hipError_t launch_frag_upload(FragDev* dst, const FragDev* src, uint32_t count, hipStream_t s)

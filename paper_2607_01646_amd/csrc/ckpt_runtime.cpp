@@ -807,6 +807,7 @@ ckpt_status ckpt_create(const ckpt_config* cfg, ckpt_ctx** out)
     c->bounce_cfg = d.bounce_bytes;
     if (d.pack_launch_bytes) c->launch_cfg = d.pack_launch_bytes;
     c->d2h_engines_cfg = d.d2h_engines;
+    c->poison = d.poison != 0;
     c->host_threads = d.host_threads ? d.host_threads : kDefaultHostThreads;
     ckpt_status st = CKPT_OK;
     if (hipSetDevice(c->device) != hipSuccess)
@@ -1166,6 +1167,12 @@ ckpt_status issue_groups(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_
                 if (c->area_seq[a])
                     HIPCHK(c, hipStreamWaitValue64(c->s_pack, c->d_area_done + a, c->area_seq[a],
                                                   hipStreamWaitValueGte, ~0ull));
+            }
+            if (c->poison) { // debug check: the canary, then the pack over it (stream order)
+                uint32_t w[4];
+                std::memcpy(w, CKPT_CANARY, 16);
+                hipError_t e = launch_fill16(staging_of(c, g0), group_hi(c, g1 - 1) - lo, w, c->s_pack);
+                if (e != hipSuccess) return fail(c, CKPT_EHIP, "canary fill failed: %s", hipGetErrorString(e));
             }
             hipError_t e = launch_pack(c->d_frags, c->d_tile_first, c->d_tile_last, c->geo, tiles_lo(c, g0),
                                        tiles_hi(c, g1 - 1), staging_of(c, g0), lo, c->d_partials, c->grid_cap,

@@ -156,3 +156,12 @@ def test_noalloc_pack_refuses_what_exceeds_its_scratch(P):
     assert P.lib().ckpt_pack_noalloc(arr, 1, 0, 0, 0, C.c_void_p(fake + 8), 1 << 40, C.c_void_p(fake), 1 << 30, None,
                                      C.byref(ib), C.byref(nc)) == P.CKPT_EINVAL
     assert b"aligned" in P.lib().ckpt_last_error(None)
+
+
+def test_canary_of_the_header_and_the_binding_agree(P):
+    import codecs
+
+    line = [l for l in open(HEADER) if l.startswith("#define CKPT_CANARY")][0]
+    pieces = re.findall(r'"((?:[^"\\]|\\.)*)"', line)
+    value = b"".join(codecs.escape_decode(p.encode())[0] for p in pieces)
+    assert value == P.CKPT_CANARY and len(value) == 16

@@ -413,6 +413,35 @@ def test_trigger_negative_control_on_an_idle_stream():
     ck.close()
 
 
+@pytest.mark.parametrize("staging,bounce", [(16 << 20, 0), (0, 0), (16 << 20, 8 << 20)])
+def test_poison_canary_never_reaches_an_image(staging, bounce):
+    """ckpt_config.poison: each staging area is filled with the canary after
+    its previous copy and before it is packed again.  Over several snapshots
+    (each gated update changing every fragment) every committed image equals
+    the oracle's pack and holds no 16-byte-aligned copy of the canary: the
+    pack always overwrites the canary before a copy reads the area.  Ring
+    staging (pinned and pageable images) and the full-size image."""
+    tensors = _step_state(n_frag=96)
+    ck = P.Checkpointer(tensors, chunk_bytes=GATE_CHUNK, device_staging_bytes=staging, bounce_bytes=bounce,
+                        poison=True)
+    canary = np.frombuffer(P.CKPT_CANARY, dtype=np.uint8)
+    for k in range(3):
+        torch.cuda.synchronize()
+        before = [host_bytes(t) for t in tensors]
+        s = ck.snapshot(step=k)
+        ck.wait_captured(s, 0, len(tensors))
+        for t in tensors:
+            t.mul_(-1.0)  # the gated update
+        ck.wait_committed(s)
+        img, sums = ck.host_image(s)
+        want, _, _ = O.pack(before, 256, GATE_CHUNK)
+        assert np.array_equal(img, want), "snapshot %d" % k
+        assert np.array_equal(sums, O.chunk_sums(want, 0, want.size, GATE_CHUNK))
+        assert not np.any(np.all(img.reshape(-1, 16) == canary, axis=1))
+        assert ck.verify(s) == []
+    ck.close()
+
+
 def test_side_stream_carries_the_pack():
     """ckpt_config.side_stream: the pack runs on the caller's stream, behind
     what the caller queued there.  With ~40 ms of work on that stream, the
