@@ -958,6 +958,11 @@ def main():
         print(json.dumps({"overlap": ov, "d2h_link_peak_GBps": round(link["d2h"], 2)}), flush=True)
         return
     wl = W.WORKLOADS[wid]
+    gating = None
+    if not args.no_gating:  # first: its host memory is freed again before the shard's images are made
+        log("gating leg")
+        gating = gating_leg(torch, P, W, args.gating_workload, [float(r) for r in args.gating_ratios.split(",") if r],
+                            args.gating_steps, args.gating_base_steps, args.gating_staging_bytes)
     log("link peak")
     link = link_peak(torch)
     log("pack ceiling: one contiguous %d-byte fragment" % args.ceiling_bytes)
@@ -1056,6 +1061,7 @@ def main():
                            "in-place update of it: %.1f GB/s" % (ceiling["bytes"], ceiling["after_update_GBps"]),
                 "frac_of_ceiling": round(pack_gbps / ceiling["after_update_GBps"], 4),
                 "a3_span_GBps": round(span_gbps, 1), "a3_span_frac": round(span_gbps / HBM_PEAK_GBPS, 4)}
+
     # Pack-only passes over the shard (outside the timed steps): snapshots
     # whose offload is cut before their first copy, so the kernels run with
     # the host link idle; each right after the optimizer update, and each
@@ -1079,6 +1085,31 @@ def main():
 
     pack_after_update_gbps = pack_only(True)
     pack_idle_gbps = pack_only(False)
+    # The pack stream's span without the per-launch timing events (which
+    # lengthen the gaps between launches): snapshots like the timed steps'
+    # (update, then snapshot, verify beside it), timed around the first
+    # launch and after the chunk-sum reduce only.
+    P.ckpt_set_timing(ck.ctx, 2)
+    spans = []
+    for k in range(3):
+        for lo, hi in bks:
+            opt.update(lo, hi)
+        s_k = ck.snapshot(step=30_000 + k)
+        ck.wait_captured(s_k, 0, n)
+        compute.synchronize()
+        if ck.verify(prev[0]):
+            raise RuntimeError("verify failed beside the span snapshots")
+        ck.wait_committed(s_k)
+        spans.append(P.ckpt_last_timing(ck.ctx, P.CKPT_OP_SNAPSHOT)["span_ms"])
+        prev[0] = s_k
+    P.ckpt_set_timing(ck.ctx, True)
+    span_plain_gbps = 2 * S * len(spans) / sum(spans) / 1e6
+    roofline["a3_span_without_launch_events_GBps"] = round(span_plain_gbps, 1)
+    roofline["a3_span_without_launch_events_frac"] = round(span_plain_gbps / HBM_PEAK_GBPS, 4)
+    roofline["a3_span_note"] = ("2 x payload over the pack stream's whole span: every pack launch, the release "
+                                "kernel, the chunk-sum reduce and the gaps between them; in the timed steps (with an "
+                                "event pair around every launch) and in three more such snapshots timed around the "
+                                "first launch and the end only")
     overlap = None
     if not args.no_overlap:
         log("overlap leg")
@@ -1092,11 +1123,6 @@ def main():
         os.unlink(args.image_file)
     del tensors
     torch.cuda.empty_cache()
-    gating = None
-    if not args.no_gating:
-        log("gating leg")
-        gating = gating_leg(torch, P, W, args.gating_workload, [float(r) for r in args.gating_ratios.split(",") if r],
-                            args.gating_steps, args.gating_base_steps, args.gating_staging_bytes)
     try:
         sha = subprocess.run(["git", "rev-parse", "--short", "HEAD"], cwd=ROOT, capture_output=True,
                              text=True).stdout.strip() or None

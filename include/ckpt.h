@@ -256,7 +256,11 @@ ckpt_status ckpt_debug_interrupt_next(ckpt_ctx* ctx, int32_t groups);
 /* GPU timing of the last operation of each kind, from HIP events recorded
  * on the library's own streams (enable with ckpt_set_timing(ctx, 1) before
  * the operation; timing adds one event pair per kernel launch and per copy
- * request).  which: 0 = snapshot, 1 = restore, 2 = verify, 3 = pack only.
+ * request, which lengthens the gaps between a snapshot's pack launches;
+ * ckpt_set_timing(ctx, 2) times snapshots with events around the first pack
+ * launch and after the pack stream's last kernel only: span_ms, total_ms and
+ * copy_ms as at level 1, kernel_ms = -1, and no CKPT_OP_PACK result).
+ * which: 0 = snapshot, 1 = restore, 2 = verify, 3 = pack only.
  * Errors: EINVAL (bad `which`), ESTATE (no timed operation of that kind). */
 typedef struct {
     float kernel_ms;     /* sum of the tile-kernel launches' durations (pack, scatter or

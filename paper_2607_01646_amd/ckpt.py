@@ -300,7 +300,10 @@ def ckpt_debug_interrupt_next(ctx, groups):
 
 
 def ckpt_set_timing(ctx, enable=True):
-    return _check(ctx, lib().ckpt_set_timing(ctx, 1 if enable else 0))
+    """enable: False/0 off, True/1 events around every launch and copy, 2 a
+    snapshot's first pack launch and pack-stream end only."""
+    level = 2 if enable == 2 and not isinstance(enable, bool) else (1 if enable else 0)
+    return _check(ctx, lib().ckpt_set_timing(ctx, level))
 
 
 def ckpt_last_timing(ctx, which=CKPT_OP_SNAPSHOT):

@@ -83,6 +83,7 @@ struct SnapRec {
     bool aborted = false;
     bool committed = false; // cached once `done` has reached 0
     bool timed = false;
+    bool per_launch = false; // timed with events around every pack launch (else around the first only)
     uint32_t groups_copied = 0;
     std::vector<uint8_t> meta;
     RecRes* res = nullptr;
@@ -305,6 +306,7 @@ struct ckpt_ctx {
     bool group_set = false; // group_bytes given explicitly (ring mode: slots of that many bytes)
     uint32_t grid_cap = kDefaultGrid;
     bool timing = false;
+    bool timing_span = false; // timing level 2: a snapshot's first launch and pack-stream end only
 
     // layout
     bool registered = false;

@@ -1076,6 +1076,7 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
     r.buf = buf;
     r.meta.assign((const uint8_t*)meta, (const uint8_t*)meta + meta_len);
     r.timed = c->timing;
+    r.per_launch = c->timing && !c->timing_span;
     r.bounce = c->bounce;
     r.file = c->file_map != nullptr;
     res->landed.store(0, std::memory_order_relaxed);
@@ -1176,7 +1177,8 @@ ckpt_status issue_groups(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_
             }
             hipError_t e = launch_pack(c->d_frags, c->d_tile_first, c->d_tile_last, c->geo, tiles_lo(c, g0),
                                        tiles_hi(c, g1 - 1), staging_of(c, g0), lo, c->d_partials, c->grid_cap,
-                                       c->s_pack, r.timed ? res->k0[j] : nullptr, r.timed ? res->k1[j] : nullptr,
+                                       c->s_pack, r.timed && (r.per_launch || j == 0) ? res->k0[j] : nullptr,
+                                       r.timed && (r.per_launch || j == 0) ? res->k1[j] : nullptr,
                                        pending);
             if (e != hipSuccess) return fail(c, CKPT_EHIP, "pack launch failed: %s", hipGetErrorString(e));
             pending = nullptr; // enqueued: the GPU releases it
@@ -1493,6 +1495,7 @@ ckpt_status ckpt_set_timing(ckpt_ctx* c, int32_t enable)
 {
     if (!c) return CKPT_EINVAL;
     c->timing = enable != 0;
+    c->timing_span = enable == 2;
     return CKPT_OK;
 }
 
@@ -1502,6 +1505,7 @@ namespace ckpt {
 // and its release (an interrupted snapshot has no reduce: to its last pack).
 float pack_span(ckpt_ctx* c, const SnapRec& r)
 {
+    if (r.aborted && !r.per_launch) return -1.f; // its last launch carries no event
     hipEvent_t end = r.aborted ? r.res->k1[c->n_launches - 1] : r.res->t_red;
     if (hipEventSynchronize(end) != hipSuccess) return -1.f;
     return elapsed(r.res->k0[0], end);
@@ -1517,6 +1521,7 @@ ckpt_status ckpt_last_timing(ckpt_ctx* c, uint32_t which, ckpt_timing* out)
             if (kv.second.timed && (!best || kv.first > best->id)) best = &kv.second;
         if (!best) return fail(c, CKPT_ESTATE, "no timed snapshot retained");
         RecRes* r = best->res;
+        if (!best->per_launch) return fail(c, CKPT_ESTATE, "the newest timed snapshot has no per-launch events");
         HIPCHK(c, hipEventSynchronize(r->k1[c->n_launches - 1])); // packs run in order on one stream
         ckpt_timing t{};
         for (uint64_t j = 0; j < c->n_launches; ++j) t.kernel_ms += elapsed(r->k0[j], r->k1[j]);
@@ -1537,7 +1542,11 @@ ckpt_status ckpt_last_timing(ckpt_ctx* c, uint32_t which, ckpt_timing* out)
         if (st) return st;
         RecRes* r = best->res;
         ckpt_timing t{};
-        for (uint64_t j = 0; j < c->n_launches; ++j) t.kernel_ms += elapsed(r->k0[j], r->k1[j]);
+        if (best->per_launch) {
+            for (uint64_t j = 0; j < c->n_launches; ++j) t.kernel_ms += elapsed(r->k0[j], r->k1[j]);
+        } else {
+            t.kernel_ms = -1.f;
+        }
         t.kernels = (uint32_t)c->n_launches;
         t.copies = (uint32_t)c->n_groups;
         t.span_ms = pack_span(c, *best);

@@ -655,3 +655,30 @@ def test_registration_rejects_memory_the_kernels_cannot_read():
     rc, msg = register_raw(dev.data_ptr(), 1 << 20)
     assert rc == P.CKPT_OK, msg
     torch.cuda.synchronize()
+
+
+def test_timing_levels():
+    """ckpt_set_timing: level 1 times every pack launch; level 2 only the
+    first launch and the pack stream's end (span and trigger-to-commit
+    still reported, per-launch sums not), and the image is the same."""
+    tensors = _step_state(n_frag=32)
+    ck = P.Checkpointer(tensors, chunk_bytes=GATE_CHUNK, group_bytes=4 * GATE_CHUNK)
+    host = [host_bytes(t) for t in tensors]
+    want, _, _ = O.pack(host, 256, GATE_CHUNK)
+    for level in (1, 2):
+        P.ckpt_set_timing(ck.ctx, level)
+        s = ck.snapshot(step=level)
+        ck.wait_committed(s)
+        t = P.ckpt_last_timing(ck.ctx, P.CKPT_OP_SNAPSHOT)
+        assert t["kernels"] == t["copies"] == ck.n_chunks // 4
+        assert t["span_ms"] > 0 and t["total_ms"] > t["copy_ms"] > 0
+        assert np.array_equal(ck.host_image(s)[0], want)
+        if level == 1:
+            assert 0 < t["kernel_ms"] <= t["span_ms"]
+            assert P.ckpt_last_timing(ck.ctx, P.CKPT_OP_PACK)["kernel_ms"] > 0
+        else:
+            assert t["kernel_ms"] == -1
+            with pytest.raises(P.CkptError) as e:
+                P.ckpt_last_timing(ck.ctx, P.CKPT_OP_PACK)
+            assert e.value.code == P.CKPT_ESTATE
+    ck.close()
