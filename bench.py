@@ -70,6 +70,9 @@ def parse():
                     help="skip the gate-granularity comparison (per-bucket against whole-range waits with a "
                          "staging ring)")
     ap.add_argument("--gating-only", action="store_true", help="run only the gate-granularity comparison")
+    ap.add_argument("--gemm-beside-only", action="store_true",
+                    help="time the load's GEMM alone, beside host-to-device copies and beside a snapshot's "
+                         "device-to-host copies (workload 3)")
     ap.add_argument("--gating-workload", type=int, default=3)
     ap.add_argument("--gating-ratios", default="0.75",
                     help="compute window / snapshot time ratios of the gate comparison (the full sweep: "
@@ -677,6 +680,64 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
     return out
 
 
+def gemm_beside_leg(torch, P, W, wid=3, reps=5):
+    """Where the step overhead under snapshots comes from: the load's GEMM
+    timed alone, beside host -> device copies on the DMA engines (torch's
+    pinned copies, 3 x 8 GiB), and beside a snapshot's device -> host copies
+    (the library, after its pack).  Alternating, median of the middle runs."""
+    M, K, N = W.OVERLAP_GEMM[wid]
+    x = torch.randn(M, K, device="cuda", dtype=torch.bfloat16)
+    w = torch.randn(K, N, device="cuda", dtype=torch.bfloat16)
+    tensors, plan = W.make_state(wid, device="cuda")
+    ck = P.Checkpointer(tensors, chunk_bytes=W.WORKLOADS[wid]["chunk"])
+    for k in range(2):
+        s = ck.snapshot(step=k)
+        ck.wait_committed(s)
+    host = torch.empty(8 << 30, dtype=torch.uint8, pin_memory=True)
+    dev = torch.empty(8 << 30, dtype=torch.uint8, device="cuda")
+    side = torch.cuda.Stream()
+
+    def gemms(n):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            torch.matmul(x, w)
+        e1.record()
+        e1.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    gemms(50)
+    res = {"alone": [], "beside_h2d": [], "beside_d2h": []}
+    for rep in range(reps):
+        torch.cuda.synchronize()
+        res["alone"].append(gemms(300))
+        torch.cuda.synchronize()
+        with torch.cuda.stream(side):
+            for _ in range(3):
+                dev.copy_(host, non_blocking=True)
+        res["beside_h2d"].append(gemms(300))
+        torch.cuda.synchronize()
+        s = ck.snapshot(step=10 + rep)
+        time.sleep(0.01)  # past the pack (a few ms), into the copies (~250 ms)
+        res["beside_d2h"].append(gemms(250))
+        ck.wait_committed(s)
+        log("gemm beside: rep %d" % rep)
+    ck.close()
+    del tensors, host, dev, x, w
+    torch.cuda.empty_cache()
+
+    def mid(v):
+        v = sorted(v)
+        return sum(v[1:-1]) / len(v[1:-1])
+
+    a = mid(res["alone"])
+    return {"workload": W.WORKLOADS[wid]["name"], "gemm_mkn": [M, K, N],
+            "gemm_ms": {k: [round(t, 4) for t in v] for k, v in res.items()},
+            "beside_h2d_pct": round(100 * (mid(res["beside_h2d"]) / a - 1), 2),
+            "beside_d2h_pct": round(100 * (mid(res["beside_d2h"]) / a - 1), 2),
+            "statistic": "mean of the runs left after dropping the fastest and the slowest"}
+
+
 def gating_leg(torch, P, W, wid, ratios, steps, base_steps, staging, n_buckets=8):
     """Does waiting only on the chunks each bucket overwrites pay?  With a
     staging ring the capture of the later chunks is paced by the D2H, so a
@@ -941,6 +1002,9 @@ def main():
     if args.h2h_only:
         print(json.dumps({"h2h": h2h_leg(torch, P, W, args.h2h_workload, args.h2h_steps, args.h2h_peers,
                                          max(args.bounce_bytes, 0), args.host_threads)}), flush=True)
+        return
+    if args.gemm_beside_only:
+        print(json.dumps({"gemm_beside": gemm_beside_leg(torch, P, W)}), flush=True)
         return
     if args.gating_only:
         g = gating_leg(torch, P, W, args.gating_workload, [float(r) for r in args.gating_ratios.split(",") if r],
