@@ -122,6 +122,12 @@ def parse():
     ap.add_argument("--gemm-inflation", metavar="DIR",
                     help="summarize GEMM durations of a rocprofv3 --kernel-trace --memory-copy-trace run of the "
                          "overlap leg: beside a pack launch, beside a D2H copy, and alone")
+    ap.add_argument("--gemm-pmc-run", action="store_true",
+                    help="short run for the GEMM counter study: phases of the load's GEMM alone and beside a "
+                         "snapshot's device-to-host copies (workload 3); prints the phases as JSON")
+    ap.add_argument("--counters-summary", nargs="+", metavar=("KIND", "DIR"),
+                    help="KIND pack|gemm, then rocprofv3 --pmc --kernel-trace output folders of --pmc-run (pack) or "
+                         "--gemm-pmc-run (gemm; each folder also holds that run's printed JSON as run.json)")
     ap.add_argument("--command", default="", help="command line recorded in a summary")
     ap.add_argument("--bench-json", default="", help="with --stats-summary: the JSON line bench.py printed in that run")
     return ap.parse_args()
@@ -329,6 +335,240 @@ def gemm_inflation(d, command):
             lines.append("| %s | %d | %.1f | %.1f | %+.2f%% |" % (k, len(v), statistics.median(v), statistics.mean(v),
                                                                   100 * (statistics.median(v) / base - 1)))
     return "\n".join(lines)
+
+
+def counter_dispatches(d):
+    """Per-dispatch counters of one rocprofv3 --pmc --kernel-trace run:
+    {dispatch_id: {"name", "grid", "ns", counter: value}} (duration from the
+    kernel trace, else from the counter file's own timestamps)."""
+    import csv
+    import glob
+
+    out = {}
+    for r in read_counter_csv(d):
+        k = int(r["Dispatch_Id"])
+        e = out.setdefault(k, {"name": r["Kernel_Name"], "grid": int(r["Grid_Size"]), "ns": 0})
+        e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        if r.get("Start_Timestamp") and r.get("End_Timestamp"):
+            e["ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+    for f in glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            k = int(r["Dispatch_Id"])
+            if k in out:
+                out[k]["ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+    return out
+
+
+def counter_totals(rows):
+    """Sum of every counter and of the durations over a list of dispatches."""
+    t = {"dispatches": len(rows), "ns": sum(r["ns"] for r in rows)}
+    for r in rows:
+        for k, v in r.items():
+            if k not in ("name", "grid", "ns"):
+                t[k] = t.get(k, 0.0) + v
+    return t
+
+
+def counter_readings(t):
+    """Derived figures of a class of dispatches whose counters may come from
+    several runs (each counter from the run that collected it; every run
+    repeats the same dispatches).  Ratios of counters of one clock domain:
+    the TCC's (L2 channel) counters among themselves, GRBM among itself."""
+    g = t.get
+    n = t["dispatches"]
+    out = {"dispatches": n, "mean duration (us)": t["ns"] / n / 1e3}
+    if g("clock"):
+        out["GRBM_COUNT per ns (clock, summed over the counter's instances)"] = t["clock"]
+    if g("GRBM_GUI_ACTIVE") and g("GRBM_COUNT"):
+        out["GRBM_GUI_ACTIVE / GRBM_COUNT"] = t["GRBM_GUI_ACTIVE"] / t["GRBM_COUNT"]
+    if g("TCC_EA0_RDREQ_sum") and g("TCC_EA0_RDREQ_128B_sum") is not None and g("TCC_EA0_RDREQ_64B_sum") is not None:
+        n32 = g("TCC_EA0_RDREQ_32B_sum", 0.0)
+        by_size = 32 * n32 + 64 * t["TCC_EA0_RDREQ_64B_sum"] + 128 * t["TCC_EA0_RDREQ_128B_sum"]
+        out["read requests per dispatch (32/64/128 B)"] = "%.0f / %.0f / %.0f" % (
+            n32 / n, t["TCC_EA0_RDREQ_64B_sum"] / n, t["TCC_EA0_RDREQ_128B_sum"] / n)
+        out["read bytes per dispatch from request sizes"] = by_size / n
+        out["read requests not of 32/64/128 B"] = (t["TCC_EA0_RDREQ_sum"] - n32 - t["TCC_EA0_RDREQ_64B_sum"]
+                                                    - t["TCC_EA0_RDREQ_128B_sum"]) / n
+    if g("TCC_BUBBLE_sum") is not None and g("TCC_EA0_RDREQ_sum") and g("TCC_EA0_RDREQ_32B_sum") is not None:
+        b, rq, n32 = t["TCC_BUBBLE_sum"], t["TCC_EA0_RDREQ_sum"], t["TCC_EA0_RDREQ_32B_sum"]
+        out["TCC_BUBBLE (128-byte requests by FETCH_SIZE's count) per dispatch"] = b / n
+        out["read bytes per dispatch by FETCH_SIZE's formula"] = (128 * b + 64 * (rq - b - n32) + 32 * n32) / n
+    if g("TCC_EA0_WRREQ_sum") and g("TCC_EA0_WRREQ_64B_sum") is not None:
+        w, w64 = t["TCC_EA0_WRREQ_sum"], t["TCC_EA0_WRREQ_64B_sum"]
+        out["write bytes per dispatch (WRITE_SIZE's formula)"] = (64 * w64 + 32 * (w - w64)) / n
+    if g("TCC_EA0_RDREQ_LEVEL_sum") and g("TCC_EA0_RDREQ_sum"):
+        out["EA read latency (TCC cycles, in-flight level / requests)"] = (t["TCC_EA0_RDREQ_LEVEL_sum"]
+                                                                           / t["TCC_EA0_RDREQ_sum"])
+    if g("TCC_EA0_WRREQ_LEVEL_sum") and g("TCC_EA0_WRREQ_sum"):
+        out["EA write latency (TCC cycles)"] = t["TCC_EA0_WRREQ_LEVEL_sum"] / t["TCC_EA0_WRREQ_sum"]
+    busy = g("TCC_BUSY_sum")
+    if busy:
+        if g("TCC_BUSY_avr"):
+            out["TCC channels (TCC_BUSY_sum / TCC_BUSY_avr)"] = busy / t["TCC_BUSY_avr"]
+        for k, label in [("TCC_EA0_RDREQ_LEVEL_sum", "reads in flight per channel per busy cycle"),
+                         ("TCC_EA0_WRREQ_LEVEL_sum", "writes in flight per channel per busy cycle"),
+                         ("TCC_EA0_RDREQ_DRAM_CREDIT_STALL_sum", "read DRAM-credit stall cycles / busy cycles"),
+                         ("TCC_EA0_WRREQ_DRAM_CREDIT_STALL_sum", "write DRAM-credit stall cycles / busy cycles"),
+                         ("TCC_EA0_WRREQ_STALL_sum", "write-request stall cycles / busy cycles"),
+                         ("TCC_TAG_STALL_sum", "tag stall cycles / busy cycles")]:
+            if g(k) is not None:
+                out[label] = t[k] / busy
+        if g("TCC_WRREQ_STALL_max") is not None and g("TCC_EA0_WRREQ_STALL_sum") and g("TCC_BUSY_avr"):
+            ch = busy / t["TCC_BUSY_avr"]
+            out["write stalls: busiest channel / channel mean"] = t["TCC_WRREQ_STALL_max"] / (
+                t["TCC_EA0_WRREQ_STALL_sum"] / ch)
+    if g("TCC_HIT_sum") is not None and g("TCC_MISS_sum") is not None and t["TCC_HIT_sum"] + t["TCC_MISS_sum"] > 0:
+        out["L2 hit rate"] = t["TCC_HIT_sum"] / (t["TCC_HIT_sum"] + t["TCC_MISS_sum"])
+    if g("TCC_EA0_RDREQ_sum"):
+        out["EA read requests per dispatch"] = t["TCC_EA0_RDREQ_sum"] / n
+    if g("TCC_EA0_RDREQ_DRAM_sum") is not None and g("TCC_EA0_RDREQ_sum"):
+        out["read requests to DRAM / all read requests"] = t["TCC_EA0_RDREQ_DRAM_sum"] / t["TCC_EA0_RDREQ_sum"]
+    if g("TCC_EA0_WRREQ_DRAM_sum") is not None and g("TCC_EA0_WRREQ_sum"):
+        out["write requests to DRAM / all write requests"] = t["TCC_EA0_WRREQ_DRAM_sum"] / t["TCC_EA0_WRREQ_sum"]
+    if g("TA_BUSY_avr") and g("TA_BUSY_max"):
+        # (the least busy TA belongs to a compute unit that the part does not enable, so it reads 0)
+        out["TA busy: mean / busiest instance"] = t["TA_BUSY_avr"] / t["TA_BUSY_max"]
+    if g("TA_BUSY_avr") and g("GRBM_GUI_ACTIVE"):
+        out["TA_BUSY_avr per dispatch (cycles)"] = t["TA_BUSY_avr"] / n
+    if g("TD_TD_BUSY_sum"):
+        out["TD_TD_BUSY_sum per dispatch (cycles)"] = t["TD_TD_BUSY_sum"] / n
+    if g("TCP_TCC_READ_REQ_LATENCY_sum") and g("TCP_TCC_READ_REQ_sum"):
+        out["TCP->TCC read latency (cycles)"] = t["TCP_TCC_READ_REQ_LATENCY_sum"] / t["TCP_TCC_READ_REQ_sum"]
+    if g("TCP_PENDING_STALL_CYCLES_sum") is not None:
+        out["TCP_PENDING_STALL_CYCLES_sum per dispatch"] = t["TCP_PENDING_STALL_CYCLES_sum"] / n
+    if g("TCP_TCR_TCP_STALL_CYCLES_sum") is not None:
+        out["TCP_TCR_TCP_STALL_CYCLES_sum per dispatch"] = t["TCP_TCR_TCP_STALL_CYCLES_sum"] / n
+    for k, label in [("SQ_BUSY_CYCLES", "SQ_BUSY_CYCLES per dispatch"),
+                     ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_VALU_MFMA_BUSY_CYCLES per dispatch"),
+                     ("SQ_WAVE_CYCLES", "SQ_WAVE_CYCLES per dispatch"),
+                     ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_INSTS_VALU_MFMA_MOPS_BF16 per dispatch"),
+                     ("GRBM_GUI_ACTIVE", "GRBM_GUI_ACTIVE per dispatch")]:
+        if g(k) is not None:
+            out[label] = t[k] / n
+    if g("SQ_VALU_MFMA_BUSY_CYCLES") and g("GRBM_GUI_ACTIVE"):
+        out["SQ_VALU_MFMA_BUSY_CYCLES / GRBM_GUI_ACTIVE"] = t["SQ_VALU_MFMA_BUSY_CYCLES"] / t["GRBM_GUI_ACTIVE"]
+    return out
+
+
+def merge_totals(parts):
+    """One class's totals from several runs: each counter from the first run
+    that collected it, scaled to the first run's dispatch count (a GEMM
+    phase's length differs between runs), and the durations from the first
+    run.  The clock comes from the run that counted GRBM_COUNT, over that
+    run's own durations."""
+    t = dict(parts[0])
+    for p in parts[1:]:
+        for k, v in p.items():
+            if k not in ("dispatches", "ns") and k not in t:
+                t[k] = v * t["dispatches"] / p["dispatches"]
+    for p in parts:
+        if p.get("GRBM_COUNT") and p["ns"]:
+            t["clock"] = p["GRBM_COUNT"] / p["ns"]
+            break
+    return t
+
+
+def pack_classes(disp):
+    """The pack run's dispatches by kernel: the 1 GiB calibration copy, the
+    pack, scatter and verify tile kernels."""
+    rows = [disp[k] for k in sorted(disp)]
+    copies = [r for r in rows if COPY_KERNEL in r["name"] and r["grid"] > 1024]  # the run's first large copy
+    return {"calibration copy (1 GiB)": copies[:1],
+            "pack": [r for r in rows if PACK_KERNEL in r["name"]],
+            "scatter": [r for r in rows if SCATTER_KERNEL in r["name"]],
+            "verify": [r for r in rows if VERIFY_KERNEL in r["name"]]}
+
+
+def gemm_classes(d, disp):
+    """The GEMM run's dispatches by phase, from the phase list the run
+    printed (run.json in the same folder): the GEMM kernel's dispatches in
+    order, cut by the phases' counts."""
+    lines = [x for x in open(os.path.join(d, "run.json")).read().splitlines() if x.startswith('{"workload"')]
+    phases = json.loads(lines[-1])["phases"]
+    names = {}
+    for r in disp.values():
+        names[r["name"]] = names.get(r["name"], 0) + 1
+    gemm = max(names, key=names.get)
+    rows = [disp[k] for k in sorted(disp) if disp[k]["name"] == gemm]
+    if len(rows) != sum(c for _, c in phases):
+        raise SystemExit("%s: %d GEMM dispatches, phases list %d" % (d, len(rows), sum(c for _, c in phases)))
+    out, i = {}, 0
+    for name, c in phases:
+        out.setdefault(name, []).extend(rows[i:i + c])
+        i += c
+    out.pop("warmup", None)
+    return out
+
+
+def counters_summary(kind, dirs, command):
+    """Markdown table of counter readings per kernel class (pack run) or per
+    phase (GEMM run), over one or more rocprofv3 --pmc runs."""
+    per_dir = []
+    for d in dirs:
+        disp = counter_dispatches(d)
+        cls = pack_classes(disp) if kind == "pack" else gemm_classes(d, disp)
+        per_dir.append({k: counter_totals(v) for k, v in cls.items() if v})
+    names = [k for k in per_dir[0]]
+    tables = {k: counter_readings(merge_totals([p[k] for p in per_dir if k in p])) for k in names}
+    # GEMM phases: also each phase against the GEMMs alone
+    rel = [c for c in names if c != "alone"] if "alone" in tables else []
+    keys = list(tables[names[0]])
+    keys += sorted({k for c in names for k in tables[c]} - set(keys))
+    rows = []
+    for k in keys:
+        vals = []
+        for c in names:
+            v = tables[c].get(k)
+            vals.append("" if v is None else v if isinstance(v, str) else "%.4g" % v)
+        for c in rel:
+            a, v = tables["alone"].get(k), tables[c].get(k)
+            ok = isinstance(a, float) and isinstance(v, float) and a != 0 and k != "dispatches"
+            vals.append("%+.2f%%" % (100 * (v / a - 1)) if ok else "")
+        rows.append("| %s | %s |" % (k, " | ".join(vals)))
+    cols = names + ["%s vs alone" % c for c in rel]
+    head = ["command: `%s`" % command, "", "| | %s |" % " | ".join(cols), "|---|%s" % ("---|" * len(cols))]
+    return "\n".join(head + rows)
+
+
+def gemm_pmc_run(torch, P, W, wid=3, reps=3):
+    """Short run for the counter study of the load's GEMM: phases of GEMMs
+    alone and beside a snapshot's device-to-host copies after its pack has
+    finished.  GEMMs go in batches of 10 with a host synchronisation after
+    each, and the 'beside' phase stops once the snapshot has committed: every
+    GEMM of that phase but those of its last batch ran beside the copies, also
+    when a counter tool serializes the dispatches.  Prints the phases (name,
+    GEMM dispatches) as JSON."""
+    M, K, N = W.OVERLAP_GEMM[wid]
+    x = torch.randn(M, K, device="cuda", dtype=torch.bfloat16)
+    w = torch.randn(K, N, device="cuda", dtype=torch.bfloat16)
+    tensors, plan = W.make_state(wid, device="cuda")
+    ck = P.Checkpointer(tensors, chunk_bytes=W.WORKLOADS[wid]["chunk"])
+    for k in range(2):
+        s = ck.snapshot(step=k)
+        ck.wait_committed(s)
+    phases = []
+
+    def run(name, busy, cap):
+        n = 0
+        while n < cap and busy():
+            for _ in range(10):
+                torch.matmul(x, w)
+            torch.cuda.synchronize()
+            n += 10
+        phases.append([name, n])
+        return n
+
+    run("warmup", lambda: True, 20)
+    for rep in range(reps):
+        run("alone", lambda: True, 200)
+        s = ck.snapshot(step=10 + rep)
+        ck.wait_captured(s)
+        torch.cuda.synchronize()  # the pack has finished; the copies run
+        run("beside_d2h", lambda: ck.state(s) == P.CKPT_SNAP_IN_FLIGHT, 2000)
+        ck.wait_committed(s)
+        log("gemm pmc run: rep %d, phases %s" % (rep, phases[-2:]))
+    ck.close()
+    print(json.dumps({"workload": W.WORKLOADS[wid]["name"], "gemm_mkn": [M, K, N], "phases": phases}), flush=True)
 
 
 _T0 = time.perf_counter()
@@ -680,6 +920,74 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
     return out
 
 
+class ClockSampler:
+    """Background reader of the GPU's own telemetry (amdsmi GPU metrics, read
+    only): graphics clock per XCD, socket power and memory clock, every
+    `period` s, so that a phase's GEMM durations can be set against the
+    clock they ran at.  `error` holds the reason when the metrics cannot be
+    read; the phases then report no telemetry."""
+
+    def __init__(self, torch, period=0.01):
+        import threading
+
+        self.samples, self.error, self.period = [], None, period
+        self._stop = threading.Event()
+        try:
+            import amdsmi
+
+            amdsmi.amdsmi_init()
+            self._smi = amdsmi
+            p = torch.cuda.get_device_properties(torch.cuda.current_device())
+            want = "%04x:%02x:%02x" % (p.pci_domain_id, p.pci_bus_id, p.pci_device_id)
+            handles = amdsmi.amdsmi_get_processor_handles()
+            match = [h for h in handles if amdsmi.amdsmi_get_gpu_device_bdf(h).lower().startswith(want)]
+            if not match and len(handles) != 1:
+                raise RuntimeError("no amdsmi device at %s among %d" % (want, len(handles)))
+            self._h = (match or handles)[0]
+            self._read()
+        except Exception as e:  # telemetry is optional: the timing stands without it
+            self.error = "%s: %s" % (type(e).__name__, e)
+            return
+        self._t = threading.Thread(target=self._run, daemon=True)
+        self._t.start()
+
+    def _read(self):
+        m = self._smi.amdsmi_get_gpu_metrics_info(self._h)
+        clks = [c for c in (m.get("current_gfxclks") or []) if isinstance(c, (int, float)) and c > 0]
+        num = lambda k: m.get(k) if isinstance(m.get(k), (int, float)) else None  # noqa: E731
+        return {"t": time.perf_counter(), "gfxclk": sum(clks) / len(clks) if clks else num("current_gfxclk"),
+                "power": num("current_socket_power"), "uclk": num("current_uclk"),
+                "throttle": m.get("indep_throttle_status")}
+
+    def _run(self):
+        while not self._stop.is_set():
+            try:
+                self.samples.append(self._read())
+            except Exception as e:
+                self.error = "%s: %s" % (type(e).__name__, e)
+                return
+            self._stop.wait(self.period)
+
+    def stop(self):
+        self._stop.set()
+        if self.error is None:
+            self._t.join()
+            try:
+                self._smi.amdsmi_shut_down()
+            except Exception:
+                pass
+
+    def window(self, t0, t1):
+        """Mean clock (MHz), socket power (W) and memory clock over [t0, t1]."""
+        s = [x for x in self.samples if t0 <= x["t"] <= t1]
+        out = {"samples": len(s)}
+        for k in ("gfxclk", "power", "uclk"):
+            v = [x[k] for x in s if x[k] is not None]
+            out[k] = sum(v) / len(v) if v else None
+        out["throttled_samples"] = sum(1 for x in s if x["throttle"] not in (None, 0, False, "N/A"))
+        return out
+
+
 def gemm_beside_leg(torch, P, W, wid=3, reps=5):
     """Where the step overhead under snapshots comes from: the load's GEMM
     timed alone, beside host -> device copies on the DMA engines (torch's
@@ -708,20 +1016,29 @@ def gemm_beside_leg(torch, P, W, wid=3, reps=5):
 
     gemms(50)
     res = {"alone": [], "beside_h2d": [], "beside_d2h": []}
+    clock = ClockSampler(torch)
+    windows = {k: [] for k in res}
+
+    def timed(kind, n):
+        t0 = time.perf_counter()
+        res[kind].append(gemms(n))
+        windows[kind].append((t0, time.perf_counter()))
+
     for rep in range(reps):
         torch.cuda.synchronize()
-        res["alone"].append(gemms(300))
+        timed("alone", 300)
         torch.cuda.synchronize()
         with torch.cuda.stream(side):
             for _ in range(3):
                 dev.copy_(host, non_blocking=True)
-        res["beside_h2d"].append(gemms(300))
+        timed("beside_h2d", 300)
         torch.cuda.synchronize()
         s = ck.snapshot(step=10 + rep)
         time.sleep(0.01)  # past the pack (a few ms), into the copies (~250 ms)
-        res["beside_d2h"].append(gemms(250))
+        timed("beside_d2h", 250)
         ck.wait_committed(s)
         log("gemm beside: rep %d" % rep)
+    clock.stop()
     ck.close()
     del tensors, host, dev, x, w
     torch.cuda.empty_cache()
@@ -730,12 +1047,29 @@ def gemm_beside_leg(torch, P, W, wid=3, reps=5):
         v = sorted(v)
         return sum(v[1:-1]) / len(v[1:-1])
 
+    def telemetry(kind):  # sample-weighted over every window of the phase
+        parts = [clock.window(a, b) for a, b in windows[kind]]
+        out = {"samples": sum(p["samples"] for p in parts),
+               "throttled_samples": sum(p["throttled_samples"] for p in parts)}
+        for k in ("gfxclk", "power", "uclk"):
+            num = sum(p[k] * p["samples"] for p in parts if p[k] is not None)
+            den = sum(p["samples"] for p in parts if p[k] is not None)
+            out[k] = round(num / den, 1) if den else None
+        return out
+
     a = mid(res["alone"])
-    return {"workload": W.WORKLOADS[wid]["name"], "gemm_mkn": [M, K, N],
-            "gemm_ms": {k: [round(t, 4) for t in v] for k, v in res.items()},
-            "beside_h2d_pct": round(100 * (mid(res["beside_h2d"]) / a - 1), 2),
-            "beside_d2h_pct": round(100 * (mid(res["beside_d2h"]) / a - 1), 2),
-            "statistic": "mean of the runs left after dropping the fastest and the slowest"}
+    out = {"workload": W.WORKLOADS[wid]["name"], "gemm_mkn": [M, K, N],
+           "gemm_ms": {k: [round(t, 4) for t in v] for k, v in res.items()},
+           "beside_h2d_pct": round(100 * (mid(res["beside_h2d"]) / a - 1), 2),
+           "beside_d2h_pct": round(100 * (mid(res["beside_d2h"]) / a - 1), 2),
+           "statistic": "mean of the runs left after dropping the fastest and the slowest"}
+    if clock.error:
+        out["telemetry_error"] = clock.error
+    else:
+        out["telemetry"] = {k: telemetry(k) for k in res}
+        out["telemetry_note"] = ("amdsmi GPU metrics sampled every 10 ms during each phase: graphics clock (MHz, "
+                                 "mean over the XCDs), socket power (W), memory clock (MHz)")
+    return out
 
 
 def gating_leg(torch, P, W, wid, ratios, steps, base_steps, staging, n_buckets=8):
@@ -952,6 +1286,9 @@ def main():
         write_summary(out, d, header)
         print(open(out).read())
         return
+    if args.counters_summary:
+        print(counters_summary(args.counters_summary[0], args.counters_summary[1:], args.command))
+        return
     if args.gemm_inflation:
         print(gemm_inflation(args.gemm_inflation, args.command))
         return
@@ -1002,6 +1339,9 @@ def main():
     if args.h2h_only:
         print(json.dumps({"h2h": h2h_leg(torch, P, W, args.h2h_workload, args.h2h_steps, args.h2h_peers,
                                          max(args.bounce_bytes, 0), args.host_threads)}), flush=True)
+        return
+    if args.gemm_pmc_run:
+        gemm_pmc_run(torch, P, W)
         return
     if args.gemm_beside_only:
         print(json.dumps({"gemm_beside": gemm_beside_leg(torch, P, W)}), flush=True)
