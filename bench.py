@@ -96,6 +96,9 @@ def parse():
     ap.add_argument("--pack-launch-bytes", type=int, default=0,
                     help="full-image staging: bytes per pack launch (whole groups); 0 = the library default (one group)")
     ap.add_argument("--d2h-engines", type=int, default=0, help="DMA engines of the snapshot copies (0 = library default)")
+    ap.add_argument("--direct", action="store_true",
+                    help="direct D2H (ckpt_config.direct_d2h): no device staging, the DMA engines copy the fragments "
+                         "and the kernels only sum (timed steps and overlap leg)")
     ap.add_argument("--overlap-R", type=int, default=0, help="overlap leg: GEMMs per step (0 = from the ratio)")
     ap.add_argument("--ceiling-bytes", type=int, default=8 << 30,
                     help="size of the contiguous fragment the pack ceiling is measured on")
@@ -808,7 +811,7 @@ def standalone_snapshot(P, ck, link_d2h_gbps, runs=3, warm=1):
 
 def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_steps=0, bounce=0, threads=0,
                 grid_blocks=0, staging=0, group=0, shared=None, gating="buckets", n_buckets=8, launch=0,
-                snap=None, engines=0, fixed_R=0):
+                snap=None, engines=0, fixed_R=0, direct=False):
     """Step-time overhead of per-step snapshots under a bf16 GEMM load.
 
     One step: R back-to-back GEMMs on the compute stream, then the optimizer
@@ -828,7 +831,7 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
         ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan],
                             chunk_bytes=W.WORKLOADS[wid]["chunk"], bounce_bytes=bounce, host_threads=threads,
                             grid_blocks=grid_blocks, device_staging_bytes=staging, group_bytes=group,
-                            pack_launch_bytes=launch, d2h_engines=engines)
+                            pack_launch_bytes=launch, d2h_engines=engines, direct=direct)
     else:
         tensors, plan, ck = shared
     n = len(tensors)
@@ -898,7 +901,9 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
     head = sweep[0]
     out = {"workload": W.WORKLOADS[wid]["name"], "payload_bytes": sum(p[1] for p in plan), "gemm_mkn": [M, K, N],
            "host_images": "pageable, %d-byte pinned bounce rings" % bounce if bounce else "pinned",
-           "device_staging": staging_text(staging, W.WORKLOADS[wid]["chunk"]),
+           "device_staging": ("none (direct D2H: the engines copy the fragments, the kernels only sum)"
+                              if direct
+                              else staging_text(staging, W.WORKLOADS[wid]["chunk"])),
            "pack_launches_per_snapshot": ck_groups,
            "tile_kernel_workgroups": grid_blocks or "one per tile",
            "gating": "%d buckets, each behind ckpt_wait(CAPTURED) on its own fragments" % len(bks)
@@ -1358,7 +1363,7 @@ def main():
         ov = overlap_leg(torch, P, W, owid, args.overlap_steps, link["d2h"], ratios, args.overlap_base_steps, ob,
                          args.host_threads, args.grid_blocks, args.staging_bytes, args.group_bytes,
                          gating=args.overlap_gating, launch=args.pack_launch_bytes, engines=args.d2h_engines,
-                         fixed_R=args.overlap_R)
+                         fixed_R=args.overlap_R, direct=args.direct)
         print(json.dumps({"overlap": ov, "d2h_link_peak_GBps": round(link["d2h"], 2)}), flush=True)
         return
     wl = W.WORKLOADS[wid]
@@ -1386,7 +1391,7 @@ def main():
                         bounce_bytes=bounce, host_threads=args.host_threads,
                         image_file=args.image_file or None, device_staging_bytes=args.staging_bytes,
                         group_bytes=args.group_bytes, pack_launch_bytes=args.pack_launch_bytes,
-                        d2h_engines=args.d2h_engines)
+                        d2h_engines=args.d2h_engines, direct=args.direct)
     P.ckpt_set_timing(ck.ctx, True)
     opt = Optimizer(torch, tensors)
     bks = buckets_of(plan, 8)
@@ -1442,8 +1447,9 @@ def main():
     snap_ms = None if traced else agg("snapshot", "total_ms") / K
     pack_ms = agg("snapshot", "kernel_ms")
     launches = sum(t["kernels"] for t in timings["snapshot"])
-    pack_gbps = 2 * S * K / pack_ms / 1e6
-    span_gbps = 2 * S * K / agg("snapshot", "span_ms") / 1e6
+    KB = sn["kernel_bytes"]  # algorithmic bytes of a snapshot's kernels: 2 S (pack), S (direct D2H: sums)
+    pack_gbps = KB * K / pack_ms / 1e6
+    span_gbps = KB * K / agg("snapshot", "span_ms") / 1e6
     d2h_ms = agg("snapshot", "copy_ms")
     d2h_gbps = sn["copy_bytes"] * K / d2h_ms / 1e6 if d2h_ms > 0 else None
     restore_gbps = sn["copy_bytes"] * K / agg("restore", "total_ms") / 1e6
@@ -1455,12 +1461,14 @@ def main():
     # the kernel source changed since the counters were taken.
     traffic = None
     summ = read_summary(args.traffic)
-    if summ.get("kernel_source_sha") == kernel_source_sha() and "traffic_bytes_per_pack_dispatch" in summ:
+    if (not args.direct and summ.get("kernel_source_sha") == kernel_source_sha()
+            and "traffic_bytes_per_pack_dispatch" in summ):
         traffic = round(float(summ["traffic_bytes_per_pack_dispatch"]))
-    roofline = {"kernel": "pack_checksum (tile_kernel<PACK>)", "bound": "hbm", "achieved": round(pack_gbps, 1),
+    roofline = {"kernel": "sums (tile_kernel<SUMS>, direct D2H)" if args.direct else "pack_checksum (tile_kernel<PACK>)",
+                "bound": "hbm", "achieved": round(pack_gbps, 1),
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(pack_gbps / HBM_PEAK_GBPS, 4),
                 "traffic": traffic, "launches": launches, "avg_launch_ms": round(pack_ms / launches, 4),
-                "algorithmic_bytes_per_launch": int(2 * S * K / launches),
+                "algorithmic_bytes_per_launch": int(KB * K / launches),
                 "ceiling": "the same kernel over one contiguous 16-byte-aligned %d-byte fragment, right after an "
                            "in-place update of it: %.1f GB/s" % (ceiling["bytes"], ceiling["after_update_GBps"]),
                 "frac_of_ceiling": round(pack_gbps / ceiling["after_update_GBps"], 4),
@@ -1485,7 +1493,7 @@ def main():
             compute.synchronize()
             t = P.ckpt_last_timing(ck.ctx, P.CKPT_OP_PACK)
             ms += t["kernel_ms"]
-        return 2 * S * reps / ms / 1e6
+        return KB * reps / ms / 1e6
 
     pack_after_update_gbps = pack_only(True)
     pack_idle_gbps = pack_only(False)
@@ -1507,7 +1515,7 @@ def main():
         spans.append(P.ckpt_last_timing(ck.ctx, P.CKPT_OP_SNAPSHOT)["span_ms"])
         prev[0] = s_k
     P.ckpt_set_timing(ck.ctx, True)
-    span_plain_gbps = 2 * S * len(spans) / sum(spans) / 1e6
+    span_plain_gbps = KB * len(spans) / sum(spans) / 1e6
     roofline["a3_span_without_launch_events_GBps"] = round(span_plain_gbps, 1)
     roofline["a3_span_without_launch_events_frac"] = round(span_plain_gbps / HBM_PEAK_GBPS, 4)
     roofline["a3_span_note"] = ("2 x payload over the pack stream's whole span: every pack launch, the release "
@@ -1521,7 +1529,8 @@ def main():
         overlap = overlap_leg(torch, P, W, owid, args.overlap_steps, link["d2h"], ratios, args.overlap_base_steps,
                               bounce if owid == wid else 0, args.host_threads, args.grid_blocks, args.staging_bytes,
                               args.group_bytes, shared=shared, gating=args.overlap_gating,
-                              launch=args.pack_launch_bytes, engines=args.d2h_engines, fixed_R=args.overlap_R)
+                              launch=args.pack_launch_bytes, engines=args.d2h_engines, fixed_R=args.overlap_R,
+                              direct=args.direct)
     ck.close()
     if args.image_file and os.path.exists(args.image_file):
         os.unlink(args.image_file)
@@ -1545,7 +1554,8 @@ def main():
                    "host_images": ("image file %s behind %d-byte pinned bounce rings" % (args.image_file, bounce)
                                    if args.image_file else
                                    "pageable, %d-byte pinned bounce rings" % bounce if bounce else "pinned"),
-                   "device_staging": staging_text(args.staging_bytes, wl["chunk"]),
+                   "device_staging": ("none (direct D2H)" if args.direct
+                                      else staging_text(args.staging_bytes, wl["chunk"])),
                    "groups_per_snapshot": int(sn["copies"]), "pack_launches_per_snapshot": int(sn["kernels"]),
                    "parallelism": "one rank, one GPU"},
         "roofline": roofline,

@@ -129,6 +129,19 @@ typedef struct {
                                       16-byte canary CKPT_CANARY; with correct ordering the pack
                                       overwrites every byte first, so the canary never reaches a
                                       host image.  Costs one extra write of the staging per snapshot. */
+    uint32_t direct_d2h;           /* nonzero = no device staging for snapshots: the DMA engines copy
+                                      each fragment from the live tensors straight into its place in
+                                      the host image (or the bounce ring), the padding between
+                                      fragments is zeroed on the host, and the snapshot's kernels
+                                      only compute the chunk sums (reading the fragments once: half
+                                      the HBM traffic of pack + copy, and no device image).  The
+                                      gate (ckpt_wait CAPTURED) then also waits for the copies of
+                                      the chunk groups it covers, so an update issued before the
+                                      copies finish waits for the host link.  Restore stages through
+                                      a device ring of up to four chunk groups.  Not combinable with
+                                      device_staging_bytes or poison; pack_launch_bytes is ignored.
+                                      At most 65536 fragment pieces (fragments cut at group
+                                      boundaries). */
 } ckpt_config;
 
 /* The canary of ckpt_config.poison: these 16 bytes, repeated. */
@@ -171,7 +184,8 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* ctx, const ckpt_tensor* t, uint32_t 
  * previous optimizer step).  Packs every fragment with its chunk sums into
  * device staging on the library's side stream, then copies the image and the
  * sums chunk group by chunk group into the host image that does not hold
- * the newest committed snapshot.  One image always holds the newest
+ * the newest committed snapshot (with direct_d2h: sums the fragments in place
+ * and copies them straight into that image).  One image always holds the newest
  * committed snapshot and the other receives the one in flight, so a
  * snapshot starts only once the previous one has committed (the caller's
  * wait before the optimizer step, Sec. VI-A, normally ensures that; with
@@ -187,7 +201,8 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* ctx, void* after_stream, uint64_t step
 /* The synchronization point before the optimizer step (Sec. VI-A), refined to
  * chunk granularity.  mode CKPT_WAIT_CAPTURED: makes `stream` wait (no host
  * block) until every chunk holding bytes of fragments [frag_lo, frag_hi) of
- * snapshot snap_id has been packed, so the caller may overwrite those
+ * snapshot snap_id has been packed (with direct_d2h: summed and copied to
+ * host memory), so the caller may overwrite those
  * fragments afterwards on `stream` (frag_hi above the fragment count is
  * clamped to it).  mode CKPT_WAIT_COMMITTED: blocks the
  * host until the snapshot's image and sums are in host memory (fragment

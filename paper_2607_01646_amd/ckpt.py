@@ -50,7 +50,7 @@ class ckpt_config(C.Structure):
                 ("device_staging_bytes", C.c_uint64), ("group_bytes", C.c_uint64), ("device", C.c_int32),
                 ("grid_blocks", C.c_uint32), ("bounce_bytes", C.c_uint64), ("host_threads", C.c_uint32),
                 ("side_stream", C.c_void_p), ("pack_launch_bytes", C.c_uint64), ("d2h_engines", C.c_uint32),
-                ("poison", C.c_uint32)]
+                ("poison", C.c_uint32), ("direct_d2h", C.c_uint32)]
 
 
 class ckpt_tensor(C.Structure):
@@ -160,14 +160,16 @@ def _u32p(a):
 
 
 def ckpt_create(chunk_bytes=0, align_bytes=0, device_staging_bytes=0, group_bytes=0, device=None, grid_blocks=0,
-                bounce_bytes=0, host_threads=0, side_stream=None, pack_launch_bytes=0, d2h_engines=0, poison=False):
+                bounce_bytes=0, host_threads=0, side_stream=None, pack_launch_bytes=0, d2h_engines=0, poison=False,
+                direct=False):
     """side_stream: a torch stream (or raw handle) for the pack kernels; None =
-    the library's own.  The caller keeps it alive while the context lives."""
+    the library's own.  The caller keeps it alive while the context lives.
+    direct: ckpt_config.direct_d2h."""
     if device is None:
         device = torch.cuda.current_device()
     cfg = ckpt_config(chunk_bytes, align_bytes, 0, device_staging_bytes, group_bytes, device, grid_blocks,
                       bounce_bytes, host_threads, _stream(side_stream).value if side_stream is not None else None,
-                      pack_launch_bytes, d2h_engines, 1 if poison else 0)
+                      pack_launch_bytes, d2h_engines, 1 if poison else 0, 1 if direct else 0)
     ctx = C.c_void_p()
     rc = lib().ckpt_create(C.byref(cfg), C.byref(ctx))
     if rc != CKPT_OK:
@@ -557,11 +559,12 @@ class Checkpointer:
     def __init__(self, tensors, dtypes=None, classes=None, chunk_bytes=0, align_bytes=0, device_staging_bytes=0,
                  group_bytes=0, grid_blocks=0, device=None, bounce_bytes=0, host_threads=0, image_file=None,
                  image_file_mode=CKPT_FILE_CREATE, side_stream=None, pack_launch_bytes=0, d2h_engines=0,
-                 poison=False):
+                 poison=False, direct=False):
         self.tensors = list(tensors)
         self.side_stream = side_stream  # kept alive with the context
         self.ctx = ckpt_create(chunk_bytes, align_bytes, device_staging_bytes, group_bytes, device, grid_blocks,
-                               bounce_bytes, host_threads, side_stream, pack_launch_bytes, d2h_engines, poison)
+                               bounce_bytes, host_threads, side_stream, pack_launch_bytes, d2h_engines, poison,
+                               direct)
         try:
             if image_file is not None:
                 ckpt_image_file(self.ctx, image_file, image_file_mode)

@@ -69,11 +69,25 @@ void pump_issue(ckpt_ctx* c)
         const char* what = nullptr;
         bool issued = false, counted = false;
         if (slot != UINT64_MAX) {
-            issued = hsa_amd_memory_async_copy_on_engine(c->h_bout + slot * unit, c->img_agent[0], it.staging,
-                                                         c->gpu_agent, it.n, 1, &it.res->dep[it.g / c->LG * c->LG],
-                                                         it.res->copied[it.g], it.engine, true) == HSA_STATUS_SUCCESS;
-            if (!issued) what = "DMA of a chunk group to the bounce ring could not be issued";
-            else
+            if (c->direct) { // the group's fragment pieces, straight from the tensors into the slot
+                const uint64_t want = c->piece_first[it.g + 1] - c->piece_first[it.g];
+                const uint64_t got = issue_pieces(c, it.res, it.g, c->h_bout + slot * unit, c->img_agent[0],
+                                                  &it.res->dep[it.g], it.engine);
+                issued = got == want;
+                if (!issued) {
+                    // the pieces already issued must have finished before the slot is reused
+                    if (got) (void)poll_zero(it.res->piece_done[c->piece_first[it.g] + got - 1], 120);
+                    what = "DMA of a fragment piece to the bounce ring could not be issued";
+                }
+            } else {
+                issued = hsa_amd_memory_async_copy_on_engine(c->h_bout + slot * unit, c->img_agent[0], it.staging,
+                                                             c->gpu_agent, it.n, 1,
+                                                             &it.res->dep[it.g / c->LG * c->LG],
+                                                             it.res->copied[it.g], it.engine,
+                                                             true) == HSA_STATUS_SUCCESS;
+                if (!issued) what = "DMA of a chunk group to the bounce ring could not be issued";
+            }
+            if (issued)
                 counted = hsa_amd_memory_async_copy_on_engine(it.area_done, c->gpu_agent, it.seq, c->img_agent[0], 8, 1,
                                                               &it.res->copied[it.g], it.res->flagged[it.g],
                                                               c->h2d_engine, true) == HSA_STATUS_SUCCESS;

@@ -51,6 +51,17 @@ struct Frag {
     uint32_t dtype, cls;
 };
 
+// Direct D2H: the bytes of one fragment inside one chunk group (the DMA
+// engines copy each piece straight from the tensor), or one run of image
+// padding inside a group (zeroed on the host before the group's copies).
+struct Piece {
+    uint64_t src; // device address (pieces); unused for padding
+    uint64_t off; // image offset
+    uint64_t n;
+};
+constexpr uint64_t kMaxDirectPieces = 65536;
+constexpr uint64_t kDirectRestoreSlots = 4; // restore's device ring in direct mode, in chunk groups
+
 // GPU-side resources of one snapshot record, recycled between snapshots.
 struct RecRes {
     std::vector<hipEvent_t> captured;   // per group, on the pack stream
@@ -58,6 +69,8 @@ struct RecRes {
     std::vector<int64_t*> dep_val;      // value addresses of dep
     std::vector<hsa_signal_t> copied;   // per group: the group's image copy finished
     std::vector<hsa_signal_t> flagged;  // per group: the area-done copy after it finished
+    std::vector<hsa_signal_t> piece_done; // direct D2H, per piece but each group's last (whose copy
+                                          // signals `copied`): the piece's copy finished
     hsa_signal_t dep_sums{0}, done{0};  // sums packed; sums copied (the last copy issued)
     int64_t* dep_sums_val = nullptr;
     uint64_t* h_seq = nullptr;          // pinned, per group: area use number, source of the area-done copy
@@ -182,7 +195,8 @@ struct PumpItem {
     uint32_t g = 0;
     bool sums = false;               // the chunk sums: device -> pinned sums array, no ring slot
     uint8_t* image = nullptr;        // destination: pageable host image (group) or pinned sums array
-    const uint8_t* staging = nullptr; // source in device memory
+    const uint8_t* staging = nullptr; // source in device memory (null in direct mode: the pieces)
+    uint64_t lo = 0;                 // group: image offset of its first byte
     uint64_t n = 0;
     uint64_t* area_done = nullptr;   // group: device counter bumped once the staging area has been read
     const uint64_t* seq = nullptr;   // group: pinned, the value it is set to
@@ -319,7 +333,10 @@ struct ckpt_ctx {
     uint64_t LG = 1;         // groups per pack launch (1 in ring mode)
     uint64_t n_launches = 0; // pack launches per snapshot
     bool ring = false;
-    uint64_t n_slots = 0;  // ring slots of G chunks each (ring mode)
+    uint64_t n_slots = 0;  // ring slots of G chunks each (ring mode; direct mode: restore's ring)
+    bool direct = false;   // direct D2H: no snapshot staging, the engines copy the fragments
+    std::vector<Piece> pieces, gaps;              // direct D2H, by group (CSR below)
+    std::vector<uint64_t> piece_first, gap_first; // [n_groups + 1]
 
     // device memory
     FragDev* d_frags = nullptr;
@@ -330,7 +347,8 @@ struct ckpt_ctx {
     unsigned long long* d_expected = nullptr;
     unsigned long long* d_recomputed = nullptr;
     uint8_t* d_bad = nullptr;
-    uint64_t* d_area_done = nullptr;          // per staging area: number of finished copies out of it
+    uint64_t* d_area_done = nullptr;          // per staging area (direct D2H: per group): number of
+                                              // finished copies out of it
 
     // pinned host memory
     uint8_t* h_img[2] = {nullptr, nullptr};
@@ -449,6 +467,14 @@ bool res_done(const RecRes* res, uint32_t groups_copied, bool bounce);
 void parallel_zero(uint8_t* p, uint64_t n);
 std::vector<uint8_t> build_envelope(const ckpt_ctx* c, uint64_t step, const std::vector<uint8_t>& meta,
                                     const uint64_t* sums);
+
+// Direct D2H: zero group g's padding runs in `dst` (host memory holding the
+// group's first image byte at dst), then copy its fragment pieces into place
+// on `engine`, each after the previous one (the first after first_dep); the
+// group's last piece signals res->copied[g].  Returns the pieces issued:
+// fewer than the group's means a copy could not be issued (ckpt_runtime.cpp).
+uint64_t issue_pieces(ckpt_ctx* c, RecRes* res, uint64_t g, uint8_t* dst, hsa_agent_t dst_agent,
+                      const hsa_signal_t* first_dep, hsa_amd_sdma_engine_id_t engine);
 
 // Bounce mode (ckpt_bounce.cpp)
 bool poll_zero(hsa_signal_t sig, int seconds);

@@ -41,12 +41,18 @@ constexpr uint32_t kMaxTileShift = 13;
 //   pack:     fragment bytes -> image window; image byte x goes to dst + (x - dst_origin);
 //             a non-null release is an HSA signal value the launch sets to 0
 //             as it starts (after the stream's previous kernel finished)
+//   sums:     the sums the pack would compute, from the fragments alone (no image
+//             window is written); release as for the pack
 //   scatter:  image window -> fragment bytes (image byte x read at src + (x - src_origin))
 //   checksum: image window only
 hipError_t launch_pack(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
                        const Geometry& g, uint64_t t_lo, uint64_t t_hi, uint8_t* dst, uint64_t dst_origin,
                        unsigned long long* partials, uint32_t grid_cap, hipStream_t s, hipEvent_t t0 = nullptr,
                        hipEvent_t t1 = nullptr, int64_t* release = nullptr);
+hipError_t launch_sums(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
+                       const Geometry& g, uint64_t t_lo, uint64_t t_hi, unsigned long long* partials,
+                       uint32_t grid_cap, hipStream_t s, hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr,
+                       int64_t* release = nullptr);
 hipError_t launch_scatter(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
                           const Geometry& g, uint64_t t_lo, uint64_t t_hi, const uint8_t* src, uint64_t src_origin,
                           unsigned long long* partials, uint32_t grid_cap, hipStream_t s, hipEvent_t t0 = nullptr,

@@ -1,11 +1,14 @@
 // ckpt_kernels.hip -- gfx950 kernels of libckpt.
 //
-// Three bandwidth-bound tile kernels over the snapshot image (the contiguous
+// Four bandwidth-bound tile kernels over the snapshot image (the contiguous
 // buffer of the D2H phase, paper Sec. V-B):
 //   PACK     gather fragment bytes into the image window and sum each chunk,
 //   SCATTER  write an image window back into the fragments (recovery, paper
 //            Sec. VI-E) while re-summing and checking each chunk,
-//   VERIFY   re-sum and check an image window only.
+//   VERIFY   re-sum and check an image window only,
+//   SUMS     sum each chunk of the image the fragments would make, reading
+//            the fragments only (direct D2H: the DMA engines gather the
+//            fragments into the host image themselves).
 // The chunk sum is the sum of the chunk's 8-byte little-endian words modulo
 // 2^64 (padding included).  Bytes are moved as opaque 128-bit words: no
 // floating-point instruction touches them, so NaN payloads, -0 and
@@ -49,7 +52,7 @@ constexpr int kBlock = 256;      // lanes per workgroup (4 wave64)
 constexpr int kLdsFrags = 256;  // fragment offsets cached per tile (an 8 KiB tile holds at most 33 non-empty ones)
 constexpr int kUnroll = 2;      // 16-byte vectors per lane per batch: one batch covers an 8 KiB tile
 
-enum Mode { PACK = 0, SCATTER = 1, VERIFY = 2 };
+enum Mode { PACK = 0, SCATTER = 1, VERIFY = 2, SUMS = 3 };
 
 struct Args {
     const FragDev* frags;
@@ -57,10 +60,10 @@ struct Args {
     const uint32_t* tile_last;  // last fragment holding a byte of tile t
     Geometry g;
     uint64_t t_lo, t_hi;
-    uint8_t* img; // PACK: destination window; SCATTER/VERIFY: source window
+    uint8_t* img; // PACK: destination window; SCATTER/VERIFY: source window; SUMS: unused
     uint64_t origin;
     unsigned long long* partials; // one sum per tile
-    int64_t* release;             // PACK: an HSA signal value to set to 0 at the start (or null)
+    int64_t* release;             // PACK, SUMS: an HSA signal value to set to 0 (or null)
 };
 
 struct ReduceArgs {
@@ -305,7 +308,7 @@ __device__ __forceinline__ void do_tile(const Args& a, uint64_t t, uint64_t* s_o
         // Wave w owns vectors [v0, v1) of the tile (empty past a short tile's end).
         const uint32_t v0 = w * kSlice;
         const uint32_t v1 = v0 + kSlice < nvec ? v0 + kSlice : (nvec > v0 ? nvec : v0);
-        uint8_t* win = a.img + (base - a.origin);
+        uint8_t* win = MODE == SUMS ? nullptr : a.img + (base - a.origin);
         unsigned long long acc = 0;
         if (MODE == VERIFY) {
             acc = slice_stream<UNROLL, NTL, NTS, false>(reinterpret_cast<const u32x4*>(win) + v0, nullptr, v1 - v0, lane);
@@ -316,20 +319,25 @@ __device__ __forceinline__ void do_tile(const Args& a, uint64_t t, uint64_t* s_o
                 const uint64_t p0 = base - F.off;
                 if ((F.ptr & 15) == 0 && p0 + (end - base) <= F.nbytes) {
                     u32x4* fr = reinterpret_cast<u32x4*>(F.ptr + p0) + v0;
-                    u32x4* wv = reinterpret_cast<u32x4*>(win) + v0;
-                    if (MODE == PACK)
-                        acc = slice_stream<UNROLL, NTL, NTS, true>(fr, wv, v1 - v0, lane);
+                    if (MODE == SUMS)
+                        acc = slice_stream<UNROLL, NTL, NTS, false>(fr, nullptr, v1 - v0, lane);
+                    else if (MODE == PACK)
+                        acc = slice_stream<UNROLL, NTL, NTS, true>(fr, reinterpret_cast<u32x4*>(win) + v0, v1 - v0,
+                                                                   lane);
                     else
-                        acc = slice_stream<UNROLL, NTL, NTS, true>(wv, fr, v1 - v0, lane);
+                        acc = slice_stream<UNROLL, NTL, NTS, true>(reinterpret_cast<u32x4*>(win) + v0, fr, v1 - v0,
+                                                                   lane);
                 } else {
                     for (uint32_t v = v0 + lane; v < v1; v += 64) {
                         const uint64_t p = p0 + 16ull * v;
-                        u32x4* wv = reinterpret_cast<u32x4*>(win) + v;
-                        if (MODE == PACK) {
+                        if (MODE == SUMS) {
+                            acc += vsum(fetch_general(F.ptr, F.nbytes, p));
+                        } else if (MODE == PACK) {
                             const u32x4 r = fetch_general(F.ptr, F.nbytes, p);
-                            st_stream(r, wv);
+                            st_stream(r, reinterpret_cast<u32x4*>(win) + v);
                             acc += vsum(r);
                         } else {
+                            u32x4* wv = reinterpret_cast<u32x4*>(win) + v;
                             const u32x4 r = __builtin_nontemporal_load(wv);
                             store_general(F.ptr, F.nbytes, p, r);
                             acc += vsum(r);
@@ -352,12 +360,14 @@ __device__ __forceinline__ void do_tile(const Args& a, uint64_t t, uint64_t* s_o
                     const uint32_t i = in_lds ? f0 + find_frag_lds(s_off, nf, x) : find_frag_global(a.frags, f0, f1, x);
                     const FragDev F = a.frags[i];
                     const uint64_t p = x - F.off;
-                    u32x4* wv = reinterpret_cast<u32x4*>(win) + v;
-                    if (MODE == PACK) {
+                    if (MODE == SUMS) {
+                        acc += vsum(fetch_general(F.ptr, F.nbytes, p));
+                    } else if (MODE == PACK) {
                         const u32x4 r = fetch_general(F.ptr, F.nbytes, p);
-                        st_stream(r, wv);
+                        st_stream(r, reinterpret_cast<u32x4*>(win) + v);
                         acc += vsum(r);
                     } else {
+                        u32x4* wv = reinterpret_cast<u32x4*>(win) + v;
                         const u32x4 r = __builtin_nontemporal_load(wv);
                         store_general(F.ptr, F.nbytes, p, r);
                         acc += vsum(r);
@@ -384,7 +394,7 @@ __global__ __launch_bounds__(BLOCK) void tile_kernel(Args a)
         const uint64_t t = a.t_lo + first;
         if (t < a.t_hi) do_tile<MODE, BLOCK, UNROLL, NTL, NTS>(a, t, s_off);
     }
-    if (MODE == PACK) release_signal(a.release);
+    if (MODE == PACK || MODE == SUMS) release_signal(a.release);
 }
 
 // One workgroup per chunk: add the chunk's tile sums; when expected is given,
@@ -568,6 +578,14 @@ hipError_t launch_pack(const FragDev* frags, const uint32_t* tile_first, const u
 {
     Args a{frags, tile_first, tile_last, g, t_lo, t_hi, dst, dst_origin, partials, release};
     return launch_tiles<PACK>(a, grid_cap, s, t0, t1);
+}
+
+hipError_t launch_sums(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
+                       const Geometry& g, uint64_t t_lo, uint64_t t_hi, unsigned long long* partials,
+                       uint32_t grid_cap, hipStream_t s, hipEvent_t t0, hipEvent_t t1, int64_t* release)
+{
+    Args a{frags, tile_first, tile_last, g, t_lo, t_hi, nullptr, 0, partials, release};
+    return launch_tiles<SUMS>(a, grid_cap, s, t0, t1);
 }
 
 hipError_t launch_scatter(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,

@@ -249,6 +249,8 @@ void destroy_res(RecRes* r)
         if (s.handle) hsa_signal_destroy(s);
     for (auto s : r->flagged)
         if (s.handle) hsa_signal_destroy(s);
+    for (auto s : r->piece_done)
+        if (s.handle) hsa_signal_destroy(s);
     if (r->dep_sums.handle) hsa_signal_destroy(r->dep_sums);
     if (r->done.handle) hsa_signal_destroy(r->done);
     if (r->h_seq) (void)hipHostFree(r->h_seq);
@@ -292,6 +294,12 @@ ckpt_status new_res(ckpt_ctx* c, RecRes** out)
         if (st == CKPT_OK) st = gpu_only_signal(c, &r->dep[g], &r->dep_val[g]);
         if (st == CKPT_OK) st = gpu_consumed_signal(c, &r->copied[g]);
         if (st == CKPT_OK) st = gpu_consumed_signal(c, &r->flagged[g]);
+    }
+    if (c->direct) { // a completion signal per piece (its group's last piece signals `copied`)
+        r->piece_done.assign(c->pieces.size(), hsa_signal_t{0});
+        for (uint64_t g = 0; g < n && st == CKPT_OK; ++g)
+            for (uint64_t k = c->piece_first[g]; k + 1 < c->piece_first[g + 1] && st == CKPT_OK; ++k)
+                st = gpu_consumed_signal(c, &r->piece_done[k]);
     }
     if (st == CKPT_OK) st = make_event(c, &r->t0, true);
     if (st == CKPT_OK) st = make_event(c, &r->t_red, true);
@@ -525,7 +533,7 @@ struct Lane {
 
 Lane restore_lane(ckpt_ctx* c)
 {
-    return Lane{c->s_copy, c->s_pack, c->d_staging, c->ring, c->n_slots, c->G, c->n_groups, &c->area_free,
+    return Lane{c->s_copy, c->s_pack, c->d_staging, c->ring || c->direct, c->n_slots, c->G, c->n_groups, &c->area_free,
                 &c->ev_loaded, &c->tk0, &c->tk1, c->ev_done, c->tt0, c->tc0, c->tc1};
 }
 
@@ -794,6 +802,7 @@ ckpt_status ckpt_create(const ckpt_config* cfg, ckpt_ctx** out)
     if (d.device_staging_bytes && d.device_staging_bytes < 2 * C) return CKPT_EINVAL;
     if (d.bounce_bytes && d.bounce_bytes < 2 * C) return CKPT_EINVAL;
     if (d.host_threads > 256) return CKPT_EINVAL;
+    if (d.direct_d2h && (d.device_staging_bytes || d.poison)) return CKPT_EINVAL; // no snapshot staging
     int ndev = 0;
     if (hipGetDeviceCount(&ndev) != hipSuccess || d.device < 0 || d.device >= ndev) return CKPT_EINVAL;
     ckpt_ctx* c = new ckpt_ctx();
@@ -808,6 +817,7 @@ ckpt_status ckpt_create(const ckpt_config* cfg, ckpt_ctx** out)
     if (d.pack_launch_bytes) c->launch_cfg = d.pack_launch_bytes;
     c->d2h_engines_cfg = d.d2h_engines;
     c->poison = d.poison != 0;
+    c->direct = d.direct_d2h != 0;
     c->host_threads = d.host_threads ? d.host_threads : kDefaultHostThreads;
     ckpt_status st = CKPT_OK;
     if (hipSetDevice(c->device) != hipSuccess)
@@ -917,9 +927,10 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
     // spends less time in the gaps between launches, but slows concurrent
     // training kernels more, so the default is one group per launch; each
     // group keeps its own DMA request.  In ring mode a launch fills one slot.
-    c->LG = (c->ring || !c->launch_cfg) ? 1 : std::max<uint64_t>(1, c->launch_cfg / (c->G * c->C));
+    c->LG = (c->ring || c->direct || !c->launch_cfg) ? 1 : std::max<uint64_t>(1, c->launch_cfg / (c->G * c->C));
     c->n_launches = (c->n_groups + c->LG - 1) / c->LG;
     if (c->ring) c->n_slots = std::max<uint64_t>(1, std::min<uint64_t>(c->staging_cap / (c->G * c->C), c->n_groups));
+    if (c->direct) c->n_slots = std::min<uint64_t>(kDirectRestoreSlots, c->n_groups);
     const uint64_t unit = c->G * c->C; // bytes of one chunk group
     if (c->bounce_cfg) {
         if (c->bounce_cfg / unit < 2)
@@ -935,6 +946,39 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
         fd[i].nbytes = nb[i];
         fd[i].off = pl.off[i];
         fd[i].end = pl.end[i];
+    }
+    if (c->direct) {
+        // Each group's fragment pieces (in image order) and the padding runs
+        // between them; every chunk starts with a fragment byte, so no group
+        // is all padding.
+        c->pieces.clear();
+        c->gaps.clear();
+        c->piece_first.assign(c->n_groups + 1, 0);
+        c->gap_first.assign(c->n_groups + 1, 0);
+        uint32_t i = 0;
+        for (uint64_t g = 0; g < c->n_groups; ++g) {
+            const uint64_t lo = group_lo(c, g), hi = group_hi(c, g);
+            c->piece_first[g] = c->pieces.size();
+            c->gap_first[g] = c->gaps.size();
+            uint64_t x = lo; // next image byte not yet covered
+            while (i < n && (c->frags[i].nbytes == 0 || c->frags[i].off + c->frags[i].nbytes <= lo)) ++i;
+            for (uint32_t k = i; k < n && c->frags[k].off < hi; ++k) {
+                const Frag& f = c->frags[k];
+                if (!f.nbytes) continue;
+                const uint64_t a = std::max(lo, f.off), b = std::min(hi, f.off + f.nbytes);
+                if (a > x) c->gaps.push_back(Piece{0, x, a - x});
+                c->pieces.push_back(Piece{f.ptr + (a - f.off), a, b - a});
+                x = b;
+            }
+            if (x < hi) c->gaps.push_back(Piece{0, x, hi - x});
+            if (c->pieces.size() == c->piece_first[g])
+                return fail(c, CKPT_EINVAL, "chunk group %llu holds no fragment byte", (unsigned long long)g);
+            if (c->pieces.size() > kMaxDirectPieces)
+                return fail(c, CKPT_EINVAL, "direct D2H: more than %llu fragment pieces",
+                            (unsigned long long)kMaxDirectPieces);
+        }
+        c->piece_first[c->n_groups] = c->pieces.size();
+        c->gap_first[c->n_groups] = c->gaps.size();
     }
     const uint64_t nt = pl.n_tiles;
     const uint64_t n_areas = c->ring ? c->n_slots : c->n_groups;
@@ -954,7 +998,7 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
     ALLOC(c->d_recomputed, c->n_chunks * 8);
     ALLOC(c->d_bad, c->n_chunks);
     ALLOC(c->d_area_done, n_areas * 8);
-    ALLOC(c->d_staging, c->ring ? c->n_slots * c->G * c->C : c->I);
+    ALLOC(c->d_staging, (c->ring || c->direct) ? c->n_slots * c->G * c->C : c->I);
     c->n_vslots = std::min<uint64_t>(kVerifySlots, c->n_groups);
     ALLOC(c->d_vring, c->n_vslots * c->G * c->C);
 #undef ALLOC
@@ -1131,6 +1175,165 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
 
 namespace ckpt {
 
+// The snapshot's chunk-sum copy (after the reduce has released dep_sums),
+// and in image-file mode its commit record, behind the group copies.
+ckpt_status issue_sums_copy(ckpt_ctx* c, SnapRec& r)
+{
+    RecRes* res = r.res;
+    if (r.bounce) { // behind the snapshot's group copies
+        {
+            std::lock_guard<std::mutex> l(c->pump->m);
+            PumpItem sums;
+            sums.res = res;
+            sums.sums = true;
+            sums.image = (uint8_t*)c->h_sums[r.buf];
+            sums.staging = (const uint8_t*)res->d_sums;
+            sums.n = c->n_chunks * 8;
+            sums.engine = c->d2h_engine[0];
+            sums.buf = r.buf;
+            sums.need_rec = c->pump->rec_pushed[r.buf];
+            c->pump->issue_q.push_back(sums);
+            if (c->file_map) { // then the commit record, once all of it has landed
+                ++c->pump->rec_pushed[r.buf];
+                PumpItem rec;
+                rec.res = res;
+                rec.groups = r.groups_copied;
+                rec.buf = r.buf;
+                rec.record = true;
+                rec.snap_id = r.id;
+                rec.step = r.step;
+                rec.meta = std::make_shared<const std::vector<uint8_t>>(r.meta);
+                c->pump->issue_q.push_back(std::move(rec));
+            }
+        }
+        c->pump->cv.notify_all();
+        return CKPT_OK;
+    }
+    ckpt_status st = dma(c, c->h_sums[r.buf], c->img_agent[r.buf], res->d_sums, c->gpu_agent, c->n_chunks * 8,
+                         &res->dep_sums, res->done, c->d2h_engine[0]);
+    if (st) hsa_signal_store_screlease(res->done, 0);
+    return st;
+}
+
+uint64_t issue_pieces(ckpt_ctx* c, RecRes* res, uint64_t g, uint8_t* dst, hsa_agent_t dst_agent,
+                      const hsa_signal_t* first_dep, hsa_amd_sdma_engine_id_t engine)
+{
+    const uint64_t lo = group_lo(c, g);
+    for (uint64_t k = c->gap_first[g]; k < c->gap_first[g + 1]; ++k)
+        std::memset(dst + (c->gaps[k].off - lo), 0, c->gaps[k].n);
+    const uint64_t p0 = c->piece_first[g], p1 = c->piece_first[g + 1];
+    const hsa_signal_t* dep = first_dep;
+    for (uint64_t k = p0; k < p1; ++k) {
+        const Piece& pc = c->pieces[k];
+        const hsa_signal_t* done = k + 1 == p1 ? &res->copied[g] : &res->piece_done[k];
+        hsa_signal_store_screlease(*done, 1);
+        if (hsa_amd_memory_async_copy_on_engine(dst + (pc.off - lo), dst_agent, (const void*)(uintptr_t)pc.src,
+                                                c->gpu_agent, pc.n, dep ? 1 : 0, dep, *done, engine,
+                                                true) != HSA_STATUS_SUCCESS) {
+            hsa_signal_store_screlease(*done, 0);
+            return k - p0;
+        }
+        dep = done;
+    }
+    return p1 - p0;
+}
+
+// Direct D2H (no snapshot staging): per group, the sums kernel reads the
+// fragments, and the group's pieces go from the tensors to host memory on a
+// DMA engine once the next launch on the pack stream has released the
+// group (its sums have been read; the trigger has long passed).  The copies
+// finishing bump the group's counter, on which the gate waits.
+ckpt_status issue_groups_direct(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop,
+                                hsa_signal_t& carried)
+{
+    RecRes* res = r.res;
+    uint8_t* himg = c->h_img[r.buf];
+    hsa_agent_t host = c->img_agent[r.buf];
+    HIPCHK(c, hipEventRecord(c->ev_trigger, after));
+    HIPCHK(c, hipStreamWaitEvent(c->s_pack, c->ev_trigger, 0));
+    if (r.timed) HIPCHK(c, hipEventRecord(res->t0, c->s_pack));
+    int64_t* pending = nullptr; // the previous group's release, carried by the next launch
+    for (uint64_t g = 0; g < c->n_groups; ++g) {
+        const uint64_t lo = group_lo(c, g);
+        hipError_t e = launch_sums(c->d_frags, c->d_tile_first, c->d_tile_last, c->geo, tiles_lo(c, g),
+                                   tiles_hi(c, g), c->d_partials, c->grid_cap, c->s_pack,
+                                   r.timed && (r.per_launch || g == 0) ? res->k0[g] : nullptr,
+                                   r.timed && (r.per_launch || g == 0) ? res->k1[g] : nullptr, pending);
+        if (e != hipSuccess) return fail(c, CKPT_EHIP, "sums launch failed: %s", hipGetErrorString(e));
+        pending = nullptr;
+        carried.handle = 0;
+        HIPCHK(c, hipEventRecord(res->captured[g], c->s_pack));
+        if (g >= n_copy) continue; // interrupted offload: this group never leaves the device
+        hsa_signal_store_screlease(res->dep[g], 1);
+        pending = res->dep_val[g];
+        carried = res->dep[g];
+        hsa_signal_store_screlease(res->copied[g], 1);
+        hsa_signal_store_screlease(res->flagged[g], 1);
+        r.groups_copied = (uint32_t)(g + 1);
+        const hsa_amd_sdma_engine_id_t eng = c->d2h_engine[g % c->n_d2h_engines];
+        res->h_seq[g] = c->area_seq[g] + 1;
+        ++c->area_seq[g];
+        if (r.bounce) { // the pump issues the pieces once a ring slot is free
+            {
+                std::lock_guard<std::mutex> l(c->pump->m);
+                PumpItem it;
+                it.res = res;
+                it.g = (uint32_t)g;
+                it.image = himg + lo;
+                it.lo = lo;
+                it.n = group_hi(c, g) - lo;
+                it.area_done = c->d_area_done + g;
+                it.seq = &res->h_seq[g];
+                it.engine = eng;
+                it.buf = r.buf;
+                c->pump->issue_q.push_back(it);
+            }
+            c->pump->cv.notify_all();
+            continue;
+        }
+        const uint64_t want = c->piece_first[g + 1] - c->piece_first[g];
+        const uint64_t got = issue_pieces(c, res, g, himg + lo, host, &res->dep[g], eng);
+        ckpt_status st = CKPT_OK;
+        if (got == want)
+            st = dma(c, c->d_area_done + g, c->gpu_agent, &res->h_seq[g], host, 8, &res->copied[g], res->flagged[g],
+                     c->h2d_engine);
+        if (got != want || st) {
+            // Let the issued pieces run (nothing else will release them),
+            // wait until they have read the tensors, then count the group
+            // as copied so that no gate waits forever; the snapshot is
+            // marked interrupted and never restored.
+            hsa_signal_store_screlease(res->dep[g], 0);
+            carried.handle = 0;
+            if (got && got < want) (void)poll_zero(res->piece_done[c->piece_first[g] + got - 1], 120);
+            if (got == want) (void)poll_zero(res->copied[g], 120);
+            (void)hsa_memory_copy(c->d_area_done + g, &res->h_seq[g], 8);
+            hsa_signal_store_screlease(res->copied[g], 0);
+            hsa_signal_store_screlease(res->flagged[g], 0);
+            return st ? st : fail(c, CKPT_EHIP, "DMA of a fragment piece of group %llu could not be issued",
+                                  (unsigned long long)g);
+        }
+    }
+    if (stop >= 0) {
+        r.aborted = true; // interrupted offload: never committed
+        if (pending) {
+            hipError_t e = launch_release(pending, c->s_pack);
+            if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
+            carried.handle = 0;
+        }
+        return CKPT_OK;
+    }
+    hipError_t e = launch_chunk_reduce(c->geo, 0, c->geo.n_tiles, c->d_partials, res->d_sums, nullptr, nullptr,
+                                       c->s_pack, pending);
+    if (e != hipSuccess) return fail(c, CKPT_EHIP, "reduce launch failed: %s", hipGetErrorString(e));
+    carried.handle = 0;
+    hsa_signal_store_screlease(res->dep_sums, 1);
+    e = launch_release(res->dep_sums_val, c->s_pack);
+    if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
+    if (r.timed) HIPCHK(c, hipEventRecord(res->t_red, c->s_pack));
+    hsa_signal_store_screlease(res->done, 1);
+    return issue_sums_copy(c, r);
+}
+
 // The body of issue_snapshot.  `carried` is the signal of a group whose DMA
 // has been issued while the launch that will release it has not yet been
 // enqueued; on an error return the caller releases it from the host.
@@ -1254,41 +1457,7 @@ ckpt_status issue_groups(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_
         if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
         if (r.timed) HIPCHK(c, hipEventRecord(res->t_red, c->s_pack));
         hsa_signal_store_screlease(res->done, 1);
-        if (r.bounce) { // behind the snapshot's group copies
-            {
-                std::lock_guard<std::mutex> l(c->pump->m);
-                PumpItem sums;
-                sums.res = res;
-                sums.sums = true;
-                sums.image = (uint8_t*)c->h_sums[r.buf];
-                sums.staging = (const uint8_t*)res->d_sums;
-                sums.n = c->n_chunks * 8;
-                sums.engine = c->d2h_engine[0];
-                sums.buf = r.buf;
-                sums.need_rec = c->pump->rec_pushed[r.buf];
-                c->pump->issue_q.push_back(sums);
-                if (c->file_map) { // then the commit record, once all of it has landed
-                    ++c->pump->rec_pushed[r.buf];
-                    PumpItem rec;
-                    rec.res = res;
-                    rec.groups = r.groups_copied;
-                    rec.buf = r.buf;
-                    rec.record = true;
-                    rec.snap_id = r.id;
-                    rec.step = r.step;
-                    rec.meta = std::make_shared<const std::vector<uint8_t>>(r.meta);
-                    c->pump->issue_q.push_back(std::move(rec));
-                }
-            }
-            c->pump->cv.notify_all();
-            return CKPT_OK;
-        }
-        st = dma(c, c->h_sums[r.buf], host, res->d_sums, c->gpu_agent, c->n_chunks * 8, &res->dep_sums, res->done,
-                 c->d2h_engine[0]);
-        if (st) {
-            hsa_signal_store_screlease(res->done, 0);
-            return st;
-        }
+        return issue_sums_copy(c, r);
     }
     return CKPT_OK;
 }
@@ -1296,7 +1465,8 @@ ckpt_status issue_groups(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_
 ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop)
 {
     hsa_signal_t carried{0};
-    const ckpt_status st = issue_groups(c, r, after, n_copy, stop, carried);
+    const ckpt_status st = c->direct ? issue_groups_direct(c, r, after, n_copy, stop, carried)
+                                     : issue_groups(c, r, after, n_copy, stop, carried);
     // A DMA whose release never got enqueued would wait forever: let it run
     // (the snapshot is marked interrupted and is never restored).
     if (st && carried.handle) hsa_signal_store_screlease(carried, 0);
@@ -1372,6 +1542,25 @@ ckpt_status ckpt_wait(ckpt_ctx* c, uint64_t snap_id, uint32_t mode, void* stream
         }
     }
     if (!any) return CKPT_OK; // only empty fragments: nothing to protect
+    if (c->direct) {
+        // The sums of every group up to the range's last (launches run in
+        // order), and the copies of each group holding a byte of the range:
+        // the engines finish groups out of order, and each group's copies
+        // end by setting its counter to this snapshot's use number.
+        uint64_t first = 0;
+        for (uint32_t i = frag_lo; i < frag_hi; ++i)
+            if (c->frags[i].nbytes) {
+                first = c->frags[i].off;
+                break;
+            }
+        const uint64_t unit = c->G * c->C;
+        const uint64_t g0 = first / unit, g1 = last / unit;
+        HIPCHK(c, hipStreamWaitEvent((hipStream_t)stream, r.res->captured[g1], 0));
+        for (uint64_t g = g0; g <= g1 && g < r.groups_copied; ++g)
+            HIPCHK(c, hipStreamWaitValue64((hipStream_t)stream, c->d_area_done + g, r.res->h_seq[g],
+                                           hipStreamWaitValueGte, ~0ull));
+        return CKPT_OK;
+    }
     const uint64_t g = last / (c->G * c->C);
     const uint64_t gl = std::min((g / c->LG + 1) * c->LG, c->n_groups) - 1; // its launch's last group
     HIPCHK(c, hipStreamWaitEvent((hipStream_t)stream, r.res->captured[gl], 0));
@@ -1528,7 +1717,7 @@ ckpt_status ckpt_last_timing(ckpt_ctx* c, uint32_t which, ckpt_timing* out)
         t.kernels = (uint32_t)c->n_launches;
         t.copy_ms = -1.f;
         t.total_ms = -1.f;
-        t.kernel_bytes = 2 * c->payload;
+        t.kernel_bytes = c->direct ? c->payload : 2 * c->payload; // direct: the sums read the fragments only
         t.span_ms = pack_span(c, *best);
         *out = t;
         return CKPT_OK;
@@ -1550,7 +1739,9 @@ ckpt_status ckpt_last_timing(ckpt_ctx* c, uint32_t which, ckpt_timing* out)
         t.kernels = (uint32_t)c->n_launches;
         t.copies = (uint32_t)c->n_groups;
         t.span_ms = pack_span(c, *best);
-        // DMA span: first image copy start to last image copy end (engine timestamps).
+        // DMA span: first image copy start to last image copy end (engine
+        // timestamps; in direct mode a group's first piece starts its copies
+        // and its last, which signals `copied`, ends them).
         uint64_t t_start = UINT64_MAX, t_end = 0;
         bool ok = true;
         for (uint64_t g = 0; g < c->n_groups; ++g) {
@@ -1558,6 +1749,14 @@ ckpt_status ckpt_last_timing(ckpt_ctx* c, uint32_t which, ckpt_timing* out)
             if (hsa_amd_profiling_get_async_copy_time(r->copied[g], &ct) != HSA_STATUS_SUCCESS) {
                 ok = false;
                 break;
+            }
+            if (c->direct && c->piece_first[g + 1] - c->piece_first[g] > 1) {
+                hsa_amd_profiling_async_copy_time_t c0;
+                if (hsa_amd_profiling_get_async_copy_time(r->piece_done[c->piece_first[g]], &c0) != HSA_STATUS_SUCCESS) {
+                    ok = false;
+                    break;
+                }
+                ct.start = c0.start;
             }
             t_start = std::min<uint64_t>(t_start, ct.start);
             t_end = std::max<uint64_t>(t_end, ct.end);
@@ -1577,7 +1776,7 @@ ckpt_status ckpt_last_timing(ckpt_ctx* c, uint32_t which, ckpt_timing* out)
             const float k0 = elapsed(r->k0[0], r->k1[0]);
             if (k0 >= 0.f) t.total_ms = k0 + (float)((double)(commit - t_start) * 1e3 / (double)c->ts_freq);
         }
-        t.kernel_bytes = 2 * c->payload;
+        t.kernel_bytes = c->direct ? c->payload : 2 * c->payload;
         t.copy_bytes = c->I;
         *out = t;
         return CKPT_OK;

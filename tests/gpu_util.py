@@ -30,14 +30,14 @@ def garbage_fill(tensors, value=0x5A):
 
 
 def snapshot_and_check(tensors, host, chunk, align=256, staging=0, group=0, dtypes=None, classes=None,
-                       meta=b"", step=3, grid=0, bounce=0, threads=0, launch=0):
+                       meta=b"", step=3, grid=0, bounce=0, threads=0, launch=0, direct=False):
     """Snapshot, compare image and sums with the oracle, trash the tensors,
     restore and compare them; returns the Checkpointer and snapshot id."""
     import paper_2607_01646_amd as P
 
     ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=chunk, align_bytes=align,
                         device_staging_bytes=staging, group_bytes=group, grid_blocks=grid, bounce_bytes=bounce,
-                        host_threads=threads, pack_launch_bytes=launch)
+                        host_threads=threads, pack_launch_bytes=launch, direct=direct)
     snap = ck.snapshot(step=step, meta=meta)
     ck.wait_committed(snap)
     assert ck.state(snap) == P.CKPT_SNAP_COMMITTED

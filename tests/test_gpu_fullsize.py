@@ -31,7 +31,7 @@ def release_memory():
         torch.cuda.empty_cache()
 
 
-def check_shard(wid, staging=0, full_restore=True, bounce=0, digests=False):
+def check_shard(wid, staging=0, full_restore=True, bounce=0, digests=False, direct=False):
     """Snapshot workload wid, check every chunk and sum against the oracle,
     verify, then trash the tensors, restore and check every fragment: against
     device copies (full_restore) or against torch digests taken before the
@@ -43,7 +43,7 @@ def check_shard(wid, staging=0, full_restore=True, bounce=0, digests=False):
     before = [t.clone() for t in tensors] if full_restore else None
     dig = fragment_digests(tensors) if digests else None
     ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=chunk,
-                        device_staging_bytes=staging, bounce_bytes=bounce)
+                        device_staging_bytes=staging, bounce_bytes=bounce, direct=direct)
     off, I, nc = O.layout(sizes, 256, chunk)
     assert np.array_equal(ck.offsets, off) and (ck.image_bytes, ck.n_chunks) == (I, nc)
     snap = ck.snapshot(step=wid)
@@ -76,6 +76,17 @@ def test_gpt_1_3b_shard():
 def test_llama65b_tp8pp8_rank_shard():
     """One rank of a 65B LLaMA under TP=8 x PP=8: 360 fragments, 14.17 GB."""
     ck, *_ = check_shard(3)
+    assert ck.n_chunks == 212
+    ck.close()
+
+
+@pytest.mark.parametrize("bounce", [0, 4 << 30])
+def test_llama65b_tp8pp8_rank_shard_direct(bounce):
+    """The same rank with direct D2H (no device staging; the engines copy the
+    fragments, pinned images or pageable ones behind 4 GiB rings): every
+    chunk and sum against the oracle, every fragment restored through the
+    four-group restore ring."""
+    ck, *_ = check_shard(3, bounce=bounce, direct=True)
     assert ck.n_chunks == 212
     ck.close()
 
