@@ -27,9 +27,12 @@ launches, release kernels, chunk-sum reduce); D2H against the host link's
 measured peak (plain pinned 1 GiB copies in the same process);
 restore/verify rates; the step-time overhead of a snapshot every step for 50
 steps under the shard's bf16 GEMM load (8192x4096x11008), timed per the
-paper's Sec. VII-B per-iteration statistic; and the CPU oracle on a bounded
-sample, and the comparison of per-bucket and whole-range waits before the
-update with a staging ring (one rank of a 65B model under TP=8 x PP=8).
+paper's Sec. VII-B per-iteration statistic, with the snapshots in direct D2H
+mode (no device staging: the DMA engines copy the fragments into host memory
+and the kernels only sum them; --overlap-mode full for the staged pack); and
+the CPU oracle on a bounded sample, and the comparison of per-bucket and
+whole-range waits before the update with a staging ring (one rank of a 65B
+model under TP=8 x PP=8).
 """
 import argparse
 import json
@@ -97,8 +100,11 @@ def parse():
                     help="full-image staging: bytes per pack launch (whole groups); 0 = the library default (one group)")
     ap.add_argument("--d2h-engines", type=int, default=0, help="DMA engines of the snapshot copies (0 = library default)")
     ap.add_argument("--direct", action="store_true",
-                    help="direct D2H (ckpt_config.direct_d2h): no device staging, the DMA engines copy the fragments "
-                         "and the kernels only sum (timed steps and overlap leg)")
+                    help="direct D2H (ckpt_config.direct_d2h) in the timed steps: no device staging, the DMA engines "
+                         "copy the fragments and the kernels only sum")
+    ap.add_argument("--overlap-mode", choices=["direct", "full"], default="direct",
+                    help="snapshot mode of the overlap leg: direct D2H (default; the mode for a compute window "
+                         "longer than the snapshot) or full-image staging with the pack kernel")
     ap.add_argument("--overlap-R", type=int, default=0, help="overlap leg: GEMMs per step (0 = from the ratio)")
     ap.add_argument("--ceiling-bytes", type=int, default=8 << 30,
                     help="size of the contiguous fragment the pack ceiling is measured on")
@@ -811,7 +817,7 @@ def standalone_snapshot(P, ck, link_d2h_gbps, runs=3, warm=1):
 
 def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_steps=0, bounce=0, threads=0,
                 grid_blocks=0, staging=0, group=0, shared=None, gating="buckets", n_buckets=8, launch=0,
-                snap=None, engines=0, fixed_R=0, direct=False):
+                snap=None, engines=0, fixed_R=0, direct=False, state=None):
     """Step-time overhead of per-step snapshots under a bf16 GEMM load.
 
     One step: R back-to-back GEMMs on the compute stream, then the optimizer
@@ -824,10 +830,11 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
     Overhead compares the mean step (paper Sec. VII-B per-iteration
     statistic) with and without snapshots; the no-snapshot runs bracket the
     snapshot run.  shared = (tensors, plan, checkpointer) reuses a registered
-    state instead of making one."""
+    state instead of making one; state = (tensors, plan) registers existing
+    tensors in a context of this leg's own."""
     base_steps = base_steps or steps
     if shared is None:
-        tensors, plan = W.make_state(wid, device="cuda")
+        tensors, plan = state if state is not None else W.make_state(wid, device="cuda")
         ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan],
                             chunk_bytes=W.WORKLOADS[wid]["chunk"], bounce_bytes=bounce, host_threads=threads,
                             grid_blocks=grid_blocks, device_staging_bytes=staging, group_bytes=group,
@@ -898,8 +905,12 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
         del tensors
     del x, w
     torch.cuda.empty_cache()
+    mode = ("direct D2H: no device staging; the DMA engines copy the fragments into host memory and the kernels only "
+            "sum them (ckpt_config.direct_d2h)" if direct else
+            "pack into device staging, then DMA from the staging")
     head = sweep[0]
-    out = {"workload": W.WORKLOADS[wid]["name"], "payload_bytes": sum(p[1] for p in plan), "gemm_mkn": [M, K, N],
+    out = {"workload": W.WORKLOADS[wid]["name"], "snapshot_mode": mode,
+           "payload_bytes": sum(p[1] for p in plan), "gemm_mkn": [M, K, N],
            "host_images": "pageable, %d-byte pinned bounce rings" % bounce if bounce else "pinned",
            "device_staging": ("none (direct D2H: the engines copy the fragments, the kernels only sum)"
                               if direct
@@ -1363,7 +1374,7 @@ def main():
         ov = overlap_leg(torch, P, W, owid, args.overlap_steps, link["d2h"], ratios, args.overlap_base_steps, ob,
                          args.host_threads, args.grid_blocks, args.staging_bytes, args.group_bytes,
                          gating=args.overlap_gating, launch=args.pack_launch_bytes, engines=args.d2h_engines,
-                         fixed_R=args.overlap_R, direct=args.direct)
+                         fixed_R=args.overlap_R, direct=args.overlap_mode == "direct")
         print(json.dumps({"overlap": ov, "d2h_link_peak_GBps": round(link["d2h"], 2)}), flush=True)
         return
     wl = W.WORKLOADS[wid]
@@ -1525,12 +1536,18 @@ def main():
     overlap = None
     if not args.no_overlap:
         log("overlap leg")
-        shared = (tensors, plan, ck) if owid == wid else None
+        odirect = args.overlap_mode == "direct"
+        shared = state = None
+        if owid == wid and odirect == args.direct:
+            shared = (tensors, plan, ck)
+        elif owid == wid:  # the same tensors in a context of the overlap's mode; its images replace these
+            ck.close()
+            state = (tensors, plan)
         overlap = overlap_leg(torch, P, W, owid, args.overlap_steps, link["d2h"], ratios, args.overlap_base_steps,
                               bounce if owid == wid else 0, args.host_threads, args.grid_blocks, args.staging_bytes,
                               args.group_bytes, shared=shared, gating=args.overlap_gating,
                               launch=args.pack_launch_bytes, engines=args.d2h_engines, fixed_R=args.overlap_R,
-                              direct=args.direct)
+                              direct=odirect, state=state)
     ck.close()
     if args.image_file and os.path.exists(args.image_file):
         os.unlink(args.image_file)

@@ -195,3 +195,56 @@ def fragment_digests(tensors, piece=1 << 26):
             s2 += (x * pos).sum()
         out.append((n, int(s1), int(s2)))
     return out
+
+
+def hold(stream, ms=40.0):
+    """Keep `stream` busy for about `ms` milliseconds (a chain of fp32
+    matmuls); returns the result, which the caller keeps alive until the
+    chain has run."""
+    a = torch.randn(4096, 4096, device="cuda")
+    with torch.cuda.stream(stream):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        b = a @ a
+        e1.record()
+    e1.synchronize()
+    n = max(1, int(ms / max(e0.elapsed_time(e1), 1e-3)))
+    with torch.cuda.stream(stream):
+        for _ in range(n):
+            b = a @ b
+    return b
+
+
+def runs_beside(a, b):
+    """Whether work on stream b runs while stream a is busy.  HIP maps
+    streams onto a limited set of hardware queues; two streams that share
+    one run in submission order, so a race test that needs two streams to
+    overlap has to check that they do.  Probe: while a holds ~30 ms of
+    matmuls, a marker on b must finish first."""
+    import time
+
+    torch.cuda.synchronize()
+    keep = hold(a, 30.0)
+    done_a = torch.cuda.Event()
+    done_a.record(a)
+    with torch.cuda.stream(b):
+        torch.empty(1, device="cuda").fill_(1.0)
+    done_b = torch.cuda.Event()
+    done_b.record(b)
+    t0 = time.monotonic()
+    while not done_b.query() and time.monotonic() - t0 < 0.01:
+        time.sleep(0.0002)
+    ok = done_b.query() and not done_a.query()
+    torch.cuda.synchronize()
+    del keep
+    return ok
+
+
+def pick_stream(*others, tries=40):
+    """A torch stream that runs beside every stream in `others` (probed with
+    runs_beside); torch hands out streams from a pool of 32 in turn."""
+    for _ in range(tries):
+        c = torch.cuda.Stream()
+        if all(c.cuda_stream != o.cuda_stream and runs_beside(o, c) for o in others):
+            return c
+    raise RuntimeError("no stream runs beside %d given streams" % len(others))

@@ -13,7 +13,8 @@ import pytest
 import torch
 
 import oracle as O
-from gpu_util import EDGE_SIZES, assert_located, garbage_fill, host_bytes, random_byte_fragments, snapshot_and_check
+from gpu_util import (EDGE_SIZES, assert_located, garbage_fill, hold, host_bytes, pick_stream,
+                      random_byte_fragments, snapshot_and_check)
 
 pytestmark = pytest.mark.gpu
 
@@ -124,23 +125,6 @@ def _state(n_frag=96, numel=1 << 20, seed=43):
     return [torch.randn(numel, generator=g, device="cuda") for _ in range(n_frag)]
 
 
-def _hold(stream, ms=40.0):
-    """Keep `stream` busy for about `ms` milliseconds (fp32 matmuls), so that
-    a snapshot triggered after it starts late."""
-    a = torch.randn(4096, 4096, device="cuda")
-    with torch.cuda.stream(stream):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        b = a @ a
-        e1.record()
-    e1.synchronize()
-    n = max(1, int(ms / max(e0.elapsed_time(e1), 1e-3)))
-    with torch.cuda.stream(stream):
-        for _ in range(n):
-            b = a @ b
-    return b
-
-
 CHUNK = 1 << 20
 
 
@@ -155,7 +139,7 @@ def test_gate_orders_update_after_the_copies(bounce):
     main, side = torch.cuda.current_stream(), torch.cuda.Stream()
     torch.cuda.synchronize()
     before = [host_bytes(t) for t in tensors]
-    keep = _hold(main)
+    keep = hold(main)
     s = ck.snapshot(step=1, stream=main)
     ck.wait_captured(s, 0, len(tensors), stream=side)
     with torch.cuda.stream(side):
@@ -176,11 +160,13 @@ def test_gate_negative_control_detects_the_race():
     for its trigger, and the image holds updated values.  Shows the gate test
     can see a missing wait."""
     tensors = _state()
-    ck = P.Checkpointer(tensors, chunk_bytes=CHUNK, group_bytes=CHUNK, direct=True)
-    main, side = torch.cuda.current_stream(), torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+    pk = pick_stream(main)
+    side = pick_stream(main, pk)
+    ck = P.Checkpointer(tensors, chunk_bytes=CHUNK, group_bytes=CHUNK, direct=True, side_stream=pk)
     torch.cuda.synchronize()
     before = [host_bytes(t) for t in tensors]
-    keep = _hold(main)
+    keep = hold(main)
     s = ck.snapshot(step=1, stream=main)
     with torch.cuda.stream(side):
         for t in tensors:
@@ -201,8 +187,9 @@ def test_gate_covers_only_its_range():
     their own range it does not.  The chunks before them hold the trigger's
     bytes either way."""
     tensors = _state()
-    ck = P.Checkpointer(tensors, chunk_bytes=CHUNK, group_bytes=CHUNK, direct=True)
-    side = torch.cuda.Stream()
+    pk = pick_stream(torch.cuda.current_stream())
+    side = pick_stream(pk)
+    ck = P.Checkpointer(tensors, chunk_bytes=CHUNK, group_bytes=CHUNK, direct=True, side_stream=pk)
     n = len(tensors)
     for lo, hi, leaks in [(0, 8, True), (n - 8, n, False)]:
         torch.cuda.synchronize()
@@ -233,7 +220,7 @@ def test_trigger_captures_writes_queued_before_it(bounce):
     ck = P.Checkpointer(tensors, chunk_bytes=CHUNK, group_bytes=CHUNK, bounce_bytes=bounce, direct=True)
     main = torch.cuda.current_stream()
     torch.cuda.synchronize()
-    keep = _hold(main)
+    keep = hold(main)
     for t in tensors:
         t.add_(1.0)
     updated = torch.cuda.Event()

@@ -13,7 +13,7 @@ import torch
 
 import oracle as O
 import workloads as W
-from gpu_util import (EDGE_SIZES, assert_located, garbage_fill, host_bytes, random_byte_fragments,
+from gpu_util import (EDGE_SIZES, assert_located, garbage_fill, host_bytes, pick_stream, random_byte_fragments,
                       snapshot_and_check)
 
 pytestmark = pytest.mark.gpu
@@ -308,10 +308,15 @@ def test_gate_orders_optimizer_after_capture(staging):
 def test_gate_negative_control_detects_the_race(staging):
     """Same without the wait: the update on the other stream runs while the
     pack still waits for its trigger, so the snapshot holds updated values.
-    Shows the gate test can see a missing wait."""
+    Shows the gate test can see a missing wait.  The pack runs on a stream
+    of the test's, and the update on one probed to run beside it and the
+    training stream (streams that share a hardware queue would run in
+    submission order and hide the race)."""
     tensors = _step_state(n_frag=96)
-    ck = P.Checkpointer(tensors, chunk_bytes=GATE_CHUNK, device_staging_bytes=staging)
-    main, side = torch.cuda.current_stream(), torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+    pk = pick_stream(main)
+    side = pick_stream(main, pk)
+    ck = P.Checkpointer(tensors, chunk_bytes=GATE_CHUNK, device_staging_bytes=staging, side_stream=pk)
     torch.cuda.synchronize()
     before = [host_bytes(t) for t in tensors]
     keep = _hold(main)
@@ -334,10 +339,12 @@ def test_ring_gate_covers_only_its_range():
     first) does not cover the last eight fragments.  Updating those after
     that wait races the D2H-paced pack and reaches the image; updating them
     after a wait on their own range does not.  Shows that in ring mode the
-    gate's range decides what is protected."""
+    gate's range decides what is protected.  The update runs on a stream
+    probed to run beside the pack's."""
     tensors = _step_state(n_frag=96)
-    ck = P.Checkpointer(tensors, chunk_bytes=GATE_CHUNK, device_staging_bytes=16 << 20)
-    side = torch.cuda.Stream()
+    pk = pick_stream(torch.cuda.current_stream())
+    side = pick_stream(pk)
+    ck = P.Checkpointer(tensors, chunk_bytes=GATE_CHUNK, device_staging_bytes=16 << 20, side_stream=pk)
     n = len(tensors)
     for lo, hi, leaks in [(0, 8, True), (n - 8, n, False)]:
         torch.cuda.synchronize()
@@ -394,10 +401,14 @@ def test_trigger_captures_writes_queued_before_it(staging):
 def test_trigger_negative_control_on_an_idle_stream():
     """Same, with the snapshot issued on an idle stream: nothing orders it
     after the update pending on the training stream, so it packs the bytes
-    from before the update.  Shows the trigger test can see a missing order."""
+    from before the update.  Shows the trigger test can see a missing order.
+    Both the idle stream and the pack's are probed to run beside the
+    training stream."""
     tensors = _step_state(n_frag=96)
-    ck = P.Checkpointer(tensors, chunk_bytes=GATE_CHUNK)
-    main, idle = torch.cuda.current_stream(), torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+    pk = pick_stream(main)
+    idle = pick_stream(main)
+    ck = P.Checkpointer(tensors, chunk_bytes=GATE_CHUNK, side_stream=pk)
     torch.cuda.synchronize()
     before = [host_bytes(t) for t in tensors]
     keep = _hold(main)

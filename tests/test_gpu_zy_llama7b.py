@@ -60,3 +60,22 @@ def test_llama7b_shard_pageable_images():
     del tensors
     gc.collect()
     torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+def test_llama7b_shard_direct_d2h():
+    """The same shard in direct D2H mode, as the benchmark's overlap leg runs
+    it: no device staging (the engines copy the 1164 fragments from the
+    tensors into 4 GiB pinned rings, host threads move them into the pageable
+    images).  Every chunk and sum against the oracle, every chunk verified,
+    every fragment restored through the four-group restore ring (digests)."""
+    need = 2 * W.payload_bytes(4) / (1 << 30) + 8 + 16
+    if _host_mem_gib() < need:
+        pytest.skip("two pageable 94.3 GB images need about %.0f GiB of free host memory; %.0f GiB available"
+                    % (need, _host_mem_gib()))
+    ck, tensors, plan, snap = check_shard(4, full_restore=False, bounce=4 << 30, digests=True, direct=True)
+    assert ck.n_chunks == 1406
+    ck.close()
+    del tensors
+    gc.collect()
+    torch.cuda.empty_cache()
