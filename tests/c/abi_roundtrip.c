@@ -7,7 +7,8 @@
  * device memory; snapshot; compare the committed host image and chunk sums
  * with the oracle; trash the fragments; restore and compare; verify; flip one
  * bit in the host image and check that verify reports exactly that chunk;
- * error codes of a few misuses.  Exit status 0 = every check passed.
+ * error codes of a few misuses.  Twice: with the staged pack, then with
+ * direct D2H (ckpt_config.direct_d2h).  Exit status 0 = every check passed.
  */
 #include <stdint.h>
 #include <stdio.h>
@@ -47,33 +48,17 @@ static uint8_t next_byte(void)
 
 enum { NF = 9 };
 
-int main(void)
+/* One context over the fragments: snapshot, oracle comparison, restore,
+ * verify, a located flip and the error codes; direct selects
+ * ckpt_config.direct_d2h.  The fragments hold their original bytes again
+ * when it returns 0. */
+static int roundtrip(uint8_t *const *dev, uint8_t *const *host, const uint64_t *sizes, uint64_t chunk, int direct)
 {
-    const uint64_t sizes[NF] = {1, 17, 4095, 0, 70001, 256, 3, 200000, 65536};
-    const uint64_t chunk = 16384;
-    uint8_t *host[NF], *dev[NF];
-    uint8_t *backing = NULL;
-    int ndev = 0;
-    if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) {
-        printf("SKIP no GPU\n");
-        return 77;
-    }
-    /* fragment 2 is a view at byte offset 3 of a larger allocation */
-    HIP(hipMalloc((void **)&backing, 8192));
-    for (int i = 0; i < NF; ++i) {
-        host[i] = (uint8_t *)malloc(sizes[i] ? sizes[i] : 1);
-        for (uint64_t k = 0; k < sizes[i]; ++k) host[i][k] = next_byte();
-        if (i == 2) {
-            dev[i] = backing + 3;
-        } else {
-            HIP(hipMalloc((void **)&dev[i], sizes[i] ? sizes[i] : 1));
-        }
-        if (sizes[i]) HIP(hipMemcpy(dev[i], host[i], sizes[i], hipMemcpyHostToDevice));
-    }
-
     ckpt_config cfg;
     memset(&cfg, 0, sizeof cfg);
     cfg.chunk_bytes = chunk;
+    cfg.group_bytes = 2 * chunk; /* several groups, fragments cut at their boundaries */
+    cfg.direct_d2h = (uint32_t)direct;
     ckpt_ctx *ctx = NULL;
     CHECK(ckpt_create(&cfg, &ctx) == CKPT_OK && ctx, "create");
     uint64_t sid = 0;
@@ -139,12 +124,42 @@ int main(void)
     free(env);
     free(want);
     free(want_sums);
+    printf("OK %s pass: %llu image bytes, %llu chunks\n", direct ? "direct D2H" : "staged", (unsigned long long)I,
+           (unsigned long long)nc);
+    return 0;
+}
+
+int main(void)
+{
+    const uint64_t sizes[NF] = {1, 17, 4095, 0, 70001, 256, 3, 200000, 65536};
+    const uint64_t chunk = 16384;
+    uint8_t *host[NF], *dev[NF];
+    uint8_t *backing = NULL;
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) {
+        printf("SKIP no GPU\n");
+        return 77;
+    }
+    /* fragment 2 is a view at byte offset 3 of a larger allocation */
+    HIP(hipMalloc((void **)&backing, 8192));
+    for (int i = 0; i < NF; ++i) {
+        host[i] = (uint8_t *)malloc(sizes[i] ? sizes[i] : 1);
+        for (uint64_t k = 0; k < sizes[i]; ++k) host[i][k] = next_byte();
+        if (i == 2) {
+            dev[i] = backing + 3;
+        } else {
+            HIP(hipMalloc((void **)&dev[i], sizes[i] ? sizes[i] : 1));
+        }
+        if (sizes[i]) HIP(hipMemcpy(dev[i], host[i], sizes[i], hipMemcpyHostToDevice));
+    }
+
+    if (roundtrip(dev, host, sizes, chunk, 0) != 0) return 1;
+    if (roundtrip(dev, host, sizes, chunk, 1) != 0) return 1;
     for (int i = 0; i < NF; ++i) {
         if (i != 2) HIP(hipFree(dev[i]));
         free(host[i]);
     }
     HIP(hipFree(backing));
-    printf("OK abi_roundtrip: %d fragments, %llu image bytes, %llu chunks\n", NF, (unsigned long long)I,
-           (unsigned long long)nc);
+    printf("OK abi_roundtrip: %d fragments, staged and direct D2H\n", NF);
     return 0;
 }

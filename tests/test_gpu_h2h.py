@@ -31,15 +31,17 @@ def tiny_state():
     return tensors, dtypes, classes
 
 
-@pytest.mark.parametrize("bounce", [0, 2 << 20])
-def test_replica_of_the_optimizer_state_matches_the_oracle(bounce):
+@pytest.mark.parametrize("bounce,direct", [(0, False), (2 << 20, False), (0, True), (2 << 20, True)])
+def test_replica_of_the_optimizer_state_matches_the_oracle(bounce, direct):
     """Workload 1 registered class-major, 1 MiB chunks: the peer's committed
     replica equals the oracle's chunks, sums and envelope, and leaves out the
-    chunks that hold parameters only."""
+    chunks that hold parameters only (also with direct D2H, whose host
+    image the replication reads the same way)."""
     tensors, dtypes, classes = tiny_state()
     chunk = 1 << 20
     peer = P.Peer()
-    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=chunk, group_bytes=chunk, bounce_bytes=bounce)
+    ck = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=chunk, group_bytes=chunk, bounce_bytes=bounce,
+                        direct=direct)
     ck.replicate_to(peer.port, OPT)
     host = [host_bytes(t) for t in tensors]
     s = ck.snapshot(step=7, meta=b"rng")

@@ -33,20 +33,22 @@ class Image:
         self.snap, self.step, self.data = snap, step, data  # data None: interrupted
 
 
-@pytest.mark.parametrize("bounce, staging, file, threads", [
-    (0, 0, False, 0), (4 << 20, 0, False, 0), (0, 3 * GROUP, False, 0), (4 << 20, 3 * GROUP, False, 0),
-    (4 << 20, 0, True, 0),
-    (4 << 20, 3 * GROUP, False, 1),  # one host copy thread: the drainer lags far behind the engines
+@pytest.mark.parametrize("bounce, staging, file, threads, direct", [
+    (0, 0, False, 0, False), (4 << 20, 0, False, 0, False), (0, 3 * GROUP, False, 0, False),
+    (4 << 20, 3 * GROUP, False, 0, False), (4 << 20, 0, True, 0, False),
+    (4 << 20, 3 * GROUP, False, 1, False),  # one host copy thread: the drainer lags far behind the engines
+    (0, 0, False, 0, True), (4 << 20, 0, False, 0, True), (4 << 20, 0, True, 0, True),  # direct D2H
+    (4 << 20, 0, False, 1, True),
 ])
-def test_random_walk_against_the_ping_pong_model(bounce, staging, file, threads, tmp_path):
-    rng = np.random.default_rng(1234 + bounce + staging + file + threads)
+def test_random_walk_against_the_ping_pong_model(bounce, staging, file, threads, direct, tmp_path):
+    rng = np.random.default_rng(1234 + bounce + staging + file + threads + 7 * direct)
     tensors, plan = W.make_state(1, device="cuda")
     tensors, plan = tensors[:72], plan[:72]  # the first 18 parameter tensors with their optimizer state
     torch.cuda.synchronize()
     sizes = [p[1] for p in plan]
     ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=CHUNK, group_bytes=GROUP,
                         bounce_bytes=bounce, device_staging_bytes=staging, host_threads=threads,
-                        image_file=str(tmp_path / "images") if file else None)
+                        image_file=str(tmp_path / "images") if file else None, direct=direct)
     _, I, nc = O.layout(sizes, 256, CHUNK)
     n_groups = -(-I // GROUP)
     hold = [None, None]
@@ -151,7 +153,7 @@ def test_random_walk_against_the_ping_pong_model(bounce, staging, file, threads,
             ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=CHUNK,
                                 group_bytes=GROUP, bounce_bytes=bounce, device_staging_bytes=staging,
                                 host_threads=threads, image_file=str(tmp_path / "images"),
-                                image_file_mode=P.CKPT_FILE_ADOPT)
+                                image_file_mode=P.CKPT_FILE_ADOPT, direct=direct)
             seen = {}
             if newest is None:
                 hold = [None, None]

@@ -53,14 +53,17 @@ def assert_tensors(tensors, want):
         assert np.array_equal(host_bytes(t), w), "fragment %d differs" % i
 
 
-@pytest.mark.parametrize("bounce, staging", [(0, 0), (2 << 20, 0), (0, 3 << 20)])
-def test_replacement_takes_the_optimizer_state_back(bounce, staging):
+@pytest.mark.parametrize("bounce, staging, direct", [(0, 0, False), (2 << 20, 0, False), (0, 3 << 20, False),
+                                                     (0, 0, True), (2 << 20, 0, True)])
+def test_replacement_takes_the_optimizer_state_back(bounce, staging, direct):
     """Rank A replicates snapshot (step 7) to the peer and is lost; replacement
     B, registered with A's layout, restores from the peer: the optimizer
-    fragments equal A's at step 7, parameter-only fragments keep B's bytes."""
+    fragments equal A's at step 7, parameter-only fragments keep B's bytes.
+    With direct D2H both ranks stage nothing and B restores through its
+    device ring."""
     tensors, dtypes, classes = state()
     peer = P.Peer()
-    a = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=CHUNK)
+    a = P.Checkpointer(tensors, dtypes, classes, chunk_bytes=CHUNK, direct=direct)
     a.replicate_to(peer.port, OPT)
     failed_host = [host_bytes(t) for t in tensors]
     s = a.snapshot(step=7, meta=b"rng")
@@ -72,7 +75,7 @@ def test_replacement_takes_the_optimizer_state_back(bounce, staging):
 
     before = [host_bytes(t) for t in fresh]
     b = P.Checkpointer(fresh, dtypes, classes, chunk_bytes=CHUNK, group_bytes=CHUNK, bounce_bytes=bounce,
-                       device_staging_bytes=staging)
+                       device_staging_bytes=staging, direct=direct)
     sid, step, bad = b.restore_from_peer(peer.port)
     assert (sid, step, bad) == (s, 7, [])
     assert_tensors(fresh, expected_after(failed_host, before, classes, ids))
