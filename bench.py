@@ -798,9 +798,10 @@ def standalone_snapshot(P, ck, link_d2h_gbps, runs=3, warm=1):
     """Snapshot time alone, trigger to commit: the median of `runs` snapshots
     after `warm` warm-up snapshots (the first snapshots of a context also set
     up its records).  Returns (median ms, [runs ms], [DMA spans ms], pack
-    launches per snapshot)."""
+    launches per snapshot, [kernel GB/s of each run: the snapshot's
+    algorithmic kernel bytes over its launches' summed durations])."""
     P.ckpt_set_timing(ck.ctx, True)
-    t_runs, copy_runs = [], []
+    t_runs, copy_runs, kernel_runs = [], [], []
     for k in range(warm + runs):
         s = ck.snapshot(step=k)
         ck.wait_committed(s)
@@ -811,8 +812,9 @@ def standalone_snapshot(P, ck, link_d2h_gbps, runs=3, warm=1):
         if k >= warm:
             t_runs.append(t)
             copy_runs.append(tm["copy_ms"])
+            kernel_runs.append(tm["kernel_bytes"] / tm["kernel_ms"] / 1e6 if tm["kernel_ms"] > 0 else None)
     P.ckpt_set_timing(ck.ctx, False)
-    return sorted(t_runs)[len(t_runs) // 2], t_runs, copy_runs, tm["kernels"]
+    return sorted(t_runs)[len(t_runs) // 2], t_runs, copy_runs, tm["kernels"], kernel_runs
 
 
 def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_steps=0, bounce=0, threads=0,
@@ -856,7 +858,7 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
     e1.synchronize()
     t_gemm = e0.elapsed_time(e1) / 50
     # Standalone snapshot (trigger to commit), unless the caller measured it
-    t_d2h, d2h_runs, copy_runs, ck_groups = snap or standalone_snapshot(P, ck, link_d2h_gbps)
+    t_d2h, d2h_runs, copy_runs, ck_groups, kernel_runs = snap or standalone_snapshot(P, ck, link_d2h_gbps)
     opt = Optimizer(torch, tensors)
     bks = buckets_of(plan, n_buckets)
     calls = []  # host time of each snapshot call
@@ -921,6 +923,10 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
                      if gating == "buckets" else "one ckpt_wait(CAPTURED) on every fragment",
            "gemm_ms": round(t_gemm, 4), "snapshot_ms": round(t_d2h, 2),
            "snapshot_runs_ms": [round(t, 2) for t in d2h_runs],
+           "snapshot_kernel_GBps": [round(g, 1) if g else None for g in kernel_runs],
+           "snapshot_kernel_note": ("the standalone snapshots' kernels: algorithmic bytes (%s) over the launches' "
+                                    "summed durations (HIP events), HBM peak 8000 GB/s"
+                                    % ("S, the sums read the fragments" if direct else "2 S, the pack")),
            "snapshot_alone_GBps": round(sum(p[1] for p in plan) / t_d2h / 1e6, 2),
            "d2h_alone_GBps": round(ck.image_bytes / sorted(copy_runs)[1] / 1e6, 2) if min(copy_runs) > 0 else None,
            "d2h_link_peak_GBps": round(link_d2h_gbps, 2),
