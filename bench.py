@@ -13,8 +13,9 @@ pinned bounce rings:
   snapshot = triggered right after the update: pack + chunk sums (HBM ->
              HBM staging) -> chunked D2H -> commit     (paper Sec. V-B, VI-A)
   verify   = H2D + re-check every chunk sum, of the previous step's
-             committed snapshot, while this step's snapshot streams out (the
-             host link is full duplex; the first step verifies its own)
+             committed snapshot, after this step's has committed (the
+             snapshot has the host link to itself, as in training; the first
+             step verifies its own)
   restore  = H2D + scatter into the tensors + re-check every chunk sum
 The state is generated on the GPU before timing starts.  Prints one JSON
 line; `value` is the snapshot rate: payload bytes over the trigger-to-commit
@@ -1422,16 +1423,13 @@ def main():
             if prev[0] is not None:
                 ck.wait_captured(prev[0], lo, hi)
             opt.update(lo, hi)
-        # Snapshot k, triggered on the compute stream right after the update;
-        # while it streams out (D2H), the previous committed snapshot is
-        # verified (H2D): the host link carries both directions at once.
+        # Snapshot k, triggered on the compute stream right after the update,
+        # with the host link to itself (as in training); once it has
+        # committed, the previous committed snapshot is verified (H2D) and
+        # snapshot k restored.
         snap = ck.snapshot(step=k, meta=b"step=%d" % k)
-        ck.wait_captured(snap, 0, n)
-        compute.synchronize()  # packed: verify's kernels do not share HBM with the pack
-        bad = ck.verify(prev[0]) if prev[0] is not None else []
         ck.wait_committed(snap)
-        if prev[0] is None:
-            bad += ck.verify(snap)
+        bad = ck.verify(prev[0] if prev[0] is not None else snap)
         bad += ck.restore(snap)  # the tensors already hold these bytes: every chunk must check
         if bad:
             raise RuntimeError("checksum mismatch in chunks %s" % bad)
@@ -1516,18 +1514,14 @@ def main():
     pack_idle_gbps = pack_only(False)
     # The pack stream's span without the per-launch timing events (which
     # lengthen the gaps between launches): snapshots like the timed steps'
-    # (update, then snapshot, verify beside it), timed around the first
-    # launch and after the chunk-sum reduce only.
+    # (update, then snapshot), timed around the first launch and after the
+    # chunk-sum reduce only.
     P.ckpt_set_timing(ck.ctx, 2)
     spans = []
     for k in range(3):
         for lo, hi in bks:
             opt.update(lo, hi)
         s_k = ck.snapshot(step=30_000 + k)
-        ck.wait_captured(s_k, 0, n)
-        compute.synchronize()
-        if ck.verify(prev[0]):
-            raise RuntimeError("verify failed beside the span snapshots")
         ck.wait_committed(s_k)
         spans.append(P.ckpt_last_timing(ck.ctx, P.CKPT_OP_SNAPSHOT)["span_ms"])
         prev[0] = s_k
@@ -1569,8 +1563,8 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 2), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "u64", "data": "synthetic",
         "config": {"workload": "%s shard: %d fragments, %d payload bytes, %d MiB chunks; per step: optimizer update "
-                               "(per-bucket gate), snapshot (pack + sums + D2H + commit) with verify of the previous "
-                               "snapshot beside it, restore" % (wl["name"], n, S, wl["chunk"] >> 20),
+                               "(per-bucket gate), snapshot (pack + sums + D2H + commit), verify of the previous "
+                               "snapshot, restore" % (wl["name"], n, S, wl["chunk"] >> 20),
                    "value": "snapshot GB/s: payload bytes / trigger-to-commit time of the timed steps' snapshots "
                             "(pack + chunk sums + D2H into host memory + commit)",
                    "payload_bytes": S, "image_bytes": int(sn["copy_bytes"]), "chunk_bytes": wl["chunk"],
@@ -1596,8 +1590,7 @@ def main():
                        "d2h_GBps": d2h_gbps and round(d2h_gbps, 2),
                        "d2h_link_peak_GBps": round(link["d2h"], 2),
                        "d2h_frac_of_link": d2h_gbps and round(d2h_gbps / link["d2h"], 4),
-                       "d2h_note": "DMA span of the timed snapshots, with the previous snapshot's verify (H2D) "
-                                   "running beside it",
+                       "d2h_note": "DMA span of the timed snapshots (alone on the host link)",
                        "h2d_GBps": round(h2d_gbps, 2), "h2d_link_peak_GBps": round(link["h2d"], 2),
                        "restore_GBps": round(restore_gbps, 2), "scatter_verify_GBps": round(scatter_gbps, 1),
                        "verify_GBps": round(verify_gbps, 2), "verify_kernel_GBps": round(verify_kernel_gbps, 1)},
