@@ -397,6 +397,53 @@ __global__ __launch_bounds__(BLOCK) void tile_kernel(Args a)
     if (MODE == PACK || MODE == SUMS) release_signal(a.release);
 }
 
+// SUMS over runs of kSumsTiles tiles: workgroup b takes tiles
+// [t_lo + kSumsTiles * b, t_lo + kSumsTiles * (b + 1)).  When they are all
+// full 8 KiB tiles inside one 16-byte-aligned fragment, the workgroup streams
+// them in one batch: wave w owns a quarter of the run, kSumsTiles 2 KiB
+// slices (two vectors per lane per slice, all loads issued first), and
+// stores each slice's sum in that slice's partial slot.  Otherwise each tile
+// takes the per-tile path.  A read-only stream has no stores to keep the
+// memory busy while a workgroup waits for its table lookups, so it needs
+// more bytes per workgroup than the pack.  Measured on the 1.3B shard's
+// layout: one 8 KiB tile per workgroup ~6.15 TB/s, two ~6.6 TB/s, four
+// ~6.4 TB/s, eight ~6.0 TB/s.
+constexpr uint32_t kSumsTiles = 2;
+
+__global__ __launch_bounds__(kBlock) void sums_run_kernel(Args a)
+{
+    __shared__ uint64_t s_off[kLdsFrags];
+    constexpr uint32_t kRun = kSumsTiles << kMaxTileShift; // bytes per workgroup
+    const uint64_t t = a.t_lo + (uint64_t)kSumsTiles * blockIdx.x; // < t_hi (grid: ceil(tiles / kSumsTiles))
+    bool fast = false;
+    FragDev F{};
+    if (t + kSumsTiles <= a.t_hi && a.g.tile_shift == kMaxTileShift) {
+        const uint32_t f0 = a.tile_first[t], f1 = a.tile_last[t + kSumsTiles - 1];
+        if (f0 == f1) { // the run holds bytes of this fragment only (or its padding)
+            F = a.frags[f0];
+            fast = (F.ptr & 15) == 0 && (t << kMaxTileShift) - F.off + kRun <= F.nbytes;
+        }
+    }
+    if (fast) {
+        const uint32_t lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+        const u32x4* src = reinterpret_cast<const u32x4*>(F.ptr + ((t << kMaxTileShift) - F.off)) +
+                           w * (kSumsTiles * 128);
+        u32x4 r[2 * kSumsTiles];
+#pragma unroll
+        for (uint32_t u = 0; u < 2 * kSumsTiles; ++u) r[u] = __builtin_nontemporal_load(src + lane + u * 64);
+        unsigned long long* p = a.partials + t * kTileParts + w * kSumsTiles; // slice w * kSumsTiles of the run
+#pragma unroll
+        for (uint32_t k = 0; k < kSumsTiles; ++k) {
+            const unsigned long long sk = wave_sum(vsum(r[2 * k]) + vsum(r[2 * k + 1]));
+            if (lane == 0) p[k] = sk;
+        }
+    } else {
+        for (uint32_t k = 0; k < kSumsTiles && t + k < a.t_hi; ++k)
+            do_tile<SUMS, kBlock, kUnroll, true, true>(a, t + k, s_off);
+    }
+    release_signal(a.release);
+}
+
 // One workgroup per chunk: add the chunk's tile sums; when expected is given,
 // also flag a mismatch.  A 64 MiB chunk has 32768 partial sums; each lane
 // keeps eight independent loads in flight (a plain strided loop with one
@@ -585,7 +632,14 @@ hipError_t launch_sums(const FragDev* frags, const uint32_t* tile_first, const u
                        uint32_t grid_cap, hipStream_t s, hipEvent_t t0, hipEvent_t t1, int64_t* release)
 {
     Args a{frags, tile_first, tile_last, g, t_lo, t_hi, nullptr, 0, partials, release};
-    return launch_tiles<SUMS>(a, grid_cap, s, t0, t1);
+    if (t_hi <= t_lo) return hipSuccess;
+    const uint64_t runs = (t_hi - t_lo + kSumsTiles - 1) / kSumsTiles;
+    if (runs > grid_cap) return launch_tiles<SUMS>(a, grid_cap, s, t0, t1); // a capped grid strides over tiles
+    if (t0 && t1)
+        hipExtLaunchKernelGGL(sums_run_kernel, dim3((uint32_t)runs), dim3(kBlock), 0, s, t0, t1, 0, a);
+    else
+        hipLaunchKernelGGL(sums_run_kernel, dim3((uint32_t)runs), dim3(kBlock), 0, s, a);
+    return hipGetLastError();
 }
 
 hipError_t launch_scatter(const FragDev* frags, const uint32_t* tile_first, const uint32_t* tile_last,
