@@ -320,6 +320,18 @@ ckpt_status ckpt_debug_tile_plan(const uint64_t* nbytes, uint32_t n, uint64_t ch
                                  uint64_t* tile_bytes, uint64_t* n_tiles, uint32_t* tile_first,
                                  uint32_t* tile_last);
 
+/* Test access to the copy plan of ckpt_config.direct_d2h (host-only): for
+ * fragments of these sizes, chunk size, alignment and group_bytes (0 =
+ * defaults), counts[0..2] = chunk groups, fragment pieces, padding runs.
+ * With pieces != NULL also fills, in image order: pieces (4 words each:
+ * fragment index, byte offset inside the fragment, image offset, bytes),
+ * gaps (2 words each: image offset, bytes) and piece_first / gap_first
+ * (groups + 1 entries: each group's first piece and run).  Call with
+ * pieces == NULL to get the counts first.  Errors: EINVAL. */
+ckpt_status ckpt_debug_direct_plan(const uint64_t* nbytes, uint32_t n, uint64_t chunk_bytes, uint32_t align_bytes,
+                                   uint64_t group_bytes, uint64_t* counts, uint64_t* pieces, uint64_t* gaps,
+                                   uint64_t* piece_first, uint64_t* gap_first);
+
 /* ---- Crash-surviving local snapshots (Sec. V-B: the host copy lets a
  * rank come back from its own host memory alone; Sec. V-C: a local reset
  * re-enters as a replacement) ----

@@ -101,6 +101,7 @@ def lib():
             "ckpt_last_timing": ([vp, u32, P(ckpt_timing)], i32),
             "ckpt_plan": ([P(u64), u32, u64, u32, P(u64), P(u64), P(u64)], i32),
             "ckpt_debug_tile_plan": ([P(u64), u32, u64, u32, P(u64), P(u64), P(u32), P(u32)], i32),
+            "ckpt_debug_direct_plan": ([P(u64), u32, u64, u32, u64, P(u64), P(u64), P(u64), P(u64), P(u64)], i32),
             "ckpt_last_error": ([vp], C.c_char_p),
             "ckpt_image_file": ([vp, C.c_char_p, u32], i32),
             "ckpt_latest": ([vp, P(u64), P(u64)], i32),
@@ -335,6 +336,23 @@ def ckpt_debug_tile_plan(nbytes, chunk_bytes=0, align_bytes=0):
     _check(None, lib().ckpt_debug_tile_plan(_u64p(nb), nb.size, chunk_bytes, align_bytes, C.byref(tb),
                                             C.byref(nt), _u32p(tf), _u32p(tl)))
     return tb.value, tf, tl
+
+
+def ckpt_debug_direct_plan(nbytes, chunk_bytes=0, align_bytes=0, group_bytes=0):
+    """The direct D2H copy plan: (pieces [k, 4]: fragment, offset in it, image
+    offset, bytes; gaps [k, 2]: image offset, bytes; piece_first; gap_first)."""
+    nb = np.ascontiguousarray(np.asarray(nbytes, dtype=np.uint64))
+    counts = np.zeros(3, dtype=np.uint64)
+    _check(None, lib().ckpt_debug_direct_plan(_u64p(nb), nb.size, chunk_bytes, align_bytes, group_bytes,
+                                              _u64p(counts), None, None, None, None))
+    ng, npc, ngp = (int(x) for x in counts)
+    pieces = np.zeros((max(npc, 1), 4), dtype=np.uint64)
+    gaps = np.zeros((max(ngp, 1), 2), dtype=np.uint64)
+    pf = np.zeros(ng + 1, dtype=np.uint64)
+    gf = np.zeros(ng + 1, dtype=np.uint64)
+    _check(None, lib().ckpt_debug_direct_plan(_u64p(nb), nb.size, chunk_bytes, align_bytes, group_bytes,
+                                              _u64p(counts), _u64p(pieces), _u64p(gaps), _u64p(pf), _u64p(gf)))
+    return pieces[:npc], gaps[:ngp], pf, gf
 
 
 def ckpt_last_error(ctx):

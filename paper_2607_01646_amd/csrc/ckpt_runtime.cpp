@@ -112,6 +112,45 @@ bool plan(const uint64_t* nb, uint32_t n, uint64_t C, uint32_t A, Plan* p, bool 
     return true;
 }
 
+// Direct D2H plan: for each chunk group of `unit` bytes of an image of I
+// bytes, the pieces of fragments inside it (src = byte offset inside
+// fragment piece_frag[k]; off = image offset) and the padding runs between
+// them, both in image order, with each group's first piece and run.  False
+// when a group holds no fragment byte (never, for layouts of plan(): every
+// chunk starts with a fragment byte).
+bool direct_plan(const uint64_t* off, const uint64_t* nb, uint32_t n, uint64_t I, uint64_t unit,
+                 std::vector<Piece>& pieces, std::vector<uint32_t>& piece_frag, std::vector<Piece>& gaps,
+                 std::vector<uint64_t>& piece_first, std::vector<uint64_t>& gap_first)
+{
+    const uint64_t n_groups = (I + unit - 1) / unit;
+    pieces.clear();
+    piece_frag.clear();
+    gaps.clear();
+    piece_first.assign(n_groups + 1, 0);
+    gap_first.assign(n_groups + 1, 0);
+    uint32_t i = 0;
+    for (uint64_t g = 0; g < n_groups; ++g) {
+        const uint64_t lo = g * unit, hi = std::min(lo + unit, I);
+        piece_first[g] = pieces.size();
+        gap_first[g] = gaps.size();
+        uint64_t x = lo; // next image byte not yet covered
+        while (i < n && (nb[i] == 0 || off[i] + nb[i] <= lo)) ++i;
+        for (uint32_t k = i; k < n && off[k] < hi; ++k) {
+            if (!nb[k]) continue;
+            const uint64_t a = std::max(lo, off[k]), b = std::min(hi, off[k] + nb[k]);
+            if (a > x) gaps.push_back(Piece{0, x, a - x});
+            pieces.push_back(Piece{a - off[k], a, b - a});
+            piece_frag.push_back(k);
+            x = b;
+        }
+        if (x < hi) gaps.push_back(Piece{0, x, hi - x});
+        if (pieces.size() == piece_first[g]) return false;
+    }
+    piece_first[n_groups] = pieces.size();
+    gap_first[n_groups] = gaps.size();
+    return true;
+}
+
 uint64_t group_lo(const ckpt_ctx* c, uint64_t g) { return g * c->G * c->C; }
 uint64_t group_hi(const ckpt_ctx* c, uint64_t g) { return std::min((g + 1) * c->G * c->C, c->I); }
 uint64_t tiles_lo(const ckpt_ctx* c, uint64_t g) { return group_lo(c, g) >> c->geo.tile_shift; }
@@ -947,38 +986,17 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
         fd[i].off = pl.off[i];
         fd[i].end = pl.end[i];
     }
-    if (c->direct) {
-        // Each group's fragment pieces (in image order) and the padding runs
-        // between them; every chunk starts with a fragment byte, so no group
-        // is all padding.
-        c->pieces.clear();
-        c->gaps.clear();
-        c->piece_first.assign(c->n_groups + 1, 0);
-        c->gap_first.assign(c->n_groups + 1, 0);
-        uint32_t i = 0;
-        for (uint64_t g = 0; g < c->n_groups; ++g) {
-            const uint64_t lo = group_lo(c, g), hi = group_hi(c, g);
-            c->piece_first[g] = c->pieces.size();
-            c->gap_first[g] = c->gaps.size();
-            uint64_t x = lo; // next image byte not yet covered
-            while (i < n && (c->frags[i].nbytes == 0 || c->frags[i].off + c->frags[i].nbytes <= lo)) ++i;
-            for (uint32_t k = i; k < n && c->frags[k].off < hi; ++k) {
-                const Frag& f = c->frags[k];
-                if (!f.nbytes) continue;
-                const uint64_t a = std::max(lo, f.off), b = std::min(hi, f.off + f.nbytes);
-                if (a > x) c->gaps.push_back(Piece{0, x, a - x});
-                c->pieces.push_back(Piece{f.ptr + (a - f.off), a, b - a});
-                x = b;
-            }
-            if (x < hi) c->gaps.push_back(Piece{0, x, hi - x});
-            if (c->pieces.size() == c->piece_first[g])
-                return fail(c, CKPT_EINVAL, "chunk group %llu holds no fragment byte", (unsigned long long)g);
-            if (c->pieces.size() > kMaxDirectPieces)
-                return fail(c, CKPT_EINVAL, "direct D2H: more than %llu fragment pieces",
-                            (unsigned long long)kMaxDirectPieces);
-        }
-        c->piece_first[c->n_groups] = c->pieces.size();
-        c->gap_first[c->n_groups] = c->gaps.size();
+    if (c->direct) { // each group's fragment pieces and padding runs, copied and zeroed per snapshot
+        std::vector<uint64_t> fo(n);
+        for (uint32_t i = 0; i < n; ++i) fo[i] = c->frags[i].off;
+        std::vector<uint32_t> pf;
+        if (!direct_plan(fo.data(), nb.data(), n, c->I, c->G * c->C, c->pieces, pf, c->gaps, c->piece_first,
+                         c->gap_first))
+            return fail(c, CKPT_EINVAL, "a chunk group holds no fragment byte");
+        if (c->pieces.size() > kMaxDirectPieces)
+            return fail(c, CKPT_EINVAL, "direct D2H: %llu fragment pieces, at most %llu",
+                        (unsigned long long)c->pieces.size(), (unsigned long long)kMaxDirectPieces);
+        for (size_t k = 0; k < c->pieces.size(); ++k) c->pieces[k].src += c->frags[pf[k]].ptr;
     }
     const uint64_t nt = pl.n_tiles;
     const uint64_t n_areas = c->ring ? c->n_slots : c->n_groups;
@@ -1815,6 +1833,40 @@ ckpt_status ckpt_debug_tile_plan(const uint64_t* nbytes, uint32_t n, uint64_t ch
     if (tile_last && tile_first) std::memcpy(tile_last, p.tile_last.data(), 4 * p.n_tiles);
     return CKPT_OK;
 }
+ckpt_status ckpt_debug_direct_plan(const uint64_t* nbytes, uint32_t n, uint64_t chunk_bytes, uint32_t align_bytes,
+                                   uint64_t group_bytes, uint64_t* counts, uint64_t* pieces, uint64_t* gaps,
+                                   uint64_t* piece_first, uint64_t* gap_first)
+{
+    const uint64_t C = chunk_bytes ? chunk_bytes : kDefaultChunk;
+    const uint32_t A = align_bytes ? align_bytes : kDefaultAlign;
+    if (!nbytes || n == 0 || !counts || !geometry_ok(C, A)) return CKPT_EINVAL;
+    Plan p;
+    if (!plan(nbytes, n, C, A, &p, false)) return CKPT_EINVAL;
+    const uint64_t unit = std::max<uint64_t>(1, (group_bytes ? group_bytes : kDefaultGroup) / C) * C;
+    std::vector<Piece> pc, gp;
+    std::vector<uint32_t> pf;
+    std::vector<uint64_t> p0, g0;
+    if (!direct_plan(p.off.data(), nbytes, n, p.I, unit, pc, pf, gp, p0, g0)) return CKPT_EINVAL;
+    counts[0] = p0.size() - 1;
+    counts[1] = pc.size();
+    counts[2] = gp.size();
+    if (!pieces) return CKPT_OK;
+    if (!gaps || !piece_first || !gap_first) return CKPT_EINVAL;
+    for (size_t k = 0; k < pc.size(); ++k) {
+        pieces[4 * k] = pf[k];
+        pieces[4 * k + 1] = pc[k].src;
+        pieces[4 * k + 2] = pc[k].off;
+        pieces[4 * k + 3] = pc[k].n;
+    }
+    for (size_t k = 0; k < gp.size(); ++k) {
+        gaps[2 * k] = gp[k].off;
+        gaps[2 * k + 1] = gp[k].n;
+    }
+    std::memcpy(piece_first, p0.data(), 8 * p0.size());
+    std::memcpy(gap_first, g0.data(), 8 * g0.size());
+    return CKPT_OK;
+}
+
 ckpt_status ckpt_latest(ckpt_ctx* c, uint64_t* snap_id, uint64_t* step)
 {
     if (!c || !snap_id) return CKPT_EINVAL;

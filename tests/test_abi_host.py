@@ -97,6 +97,50 @@ def test_tile_plan_brute_force(P):
             assert tl[t] == holder(x1)
 
 
+def test_direct_plan_brute_force(P):
+    """The copy plan of direct D2H, checked byte by byte over the oracle's
+    layout: in every chunk group the fragment pieces and the padding runs tile
+    the group exactly, in image order; each piece is the fragment's own bytes
+    at the fragment's own offset (so the engines copy every fragment byte once,
+    to its place); each run is padding, which no fragment byte lies in."""
+    rng = np.random.default_rng(6)
+    for C, A, G in [(256, 256, 0), (4096, 256, 4096), (4096, 16, 3 * 4096), (768, 256, 2 * 768), (1 << 17, 256, 0)]:
+        sizes = [int(s) for s in rng.integers(0, 9000, 150)]
+        sizes[7:11] = [0, 0, 0, 0]
+        sizes[0] = 0
+        sizes[-1] = 1
+        sizes[20] = 5 * C + 3  # spans several groups
+        pieces, gaps, pf, gf = P.ckpt_debug_direct_plan(sizes, C, A, G)
+        off, I, nc = O.layout(sizes, A, C)
+        unit = max(1, (G or (1 << 30)) // C) * C
+        n_groups = -(-I // unit)
+        assert len(pf) == len(gf) == n_groups + 1
+        owner = np.full(I, -1, dtype=np.int64)  # fragment holding each image byte, -1 = padding
+        pos = np.zeros(I, dtype=np.int64)       # its offset inside that fragment
+        for i, (o, s) in enumerate(zip(off, sizes)):
+            owner[int(o):int(o) + s] = i
+            pos[int(o):int(o) + s] = np.arange(s)
+        for g in range(n_groups):
+            lo, hi = g * unit, min((g + 1) * unit, I)
+            ps = pieces[int(pf[g]):int(pf[g + 1])]
+            gs = gaps[int(gf[g]):int(gf[g + 1])]
+            assert len(ps) >= 1
+            spans = sorted([(int(p[2]), int(p[3]), int(p[0]), int(p[1])) for p in ps] +
+                           [(int(r[0]), int(r[1]), -1, 0) for r in gs])
+            x = lo
+            for a, n, frag, src in spans:
+                assert a == x and n > 0, (g, a, x, n)
+                if frag >= 0:
+                    assert np.all(owner[a:a + n] == frag) and np.array_equal(pos[a:a + n], np.arange(src, src + n))
+                else:
+                    assert np.all(owner[a:a + n] == -1)
+                x = a + n
+            assert x == hi
+            assert np.all(np.diff(ps[:, 2].astype(np.int64)) > 0)  # pieces in image order
+        for i, s in enumerate(sizes):  # every fragment byte in exactly one piece
+            assert int(pieces[pieces[:, 0] == i][:, 3].sum()) == s
+
+
 def test_plan_rejects_bad_geometry(P):
     with pytest.raises(P.CkptError):
         P.ckpt_plan([10, 20], 1000, 256)  # chunk not a multiple of the alignment
