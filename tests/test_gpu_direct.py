@@ -37,6 +37,69 @@ def test_edge_sizes(chunk, align, group, bounce):
     ck.close()
 
 
+def test_capped_grid_strides_over_tiles():
+    """With the workgroup count capped, the sums kernel's workgroups loop
+    over many tiles (the per-tile path instead of the two-tile runs)."""
+    tensors, host = random_byte_fragments(EDGE_SIZES, seed=55)
+    for grid in [1, 7, 64]:
+        ck, _ = snapshot_and_check(tensors, host, 1 << 16, group=1 << 16, grid=grid, direct=True)
+        ck.close()
+
+
+def test_many_small_fragments_in_one_tile():
+    """32 fragments per 8 KiB tile (the multi-fragment sums path with its LDS
+    search), then more fragments in one tile than the LDS offset cache holds
+    (the search in global memory)."""
+    rng = np.random.default_rng(31)
+    sizes = [int(s) for s in rng.integers(1, 41, 600)]
+    tensors, host = random_byte_fragments(sizes, seed=32)
+    ck, _ = snapshot_and_check(tensors, host, 1 << 20, direct=True)
+    ck.close()
+    sizes = [0] * 3000 + [5, 0, 9] + [0] * 1500 + [300]
+    tensors, host = random_byte_fragments(sizes, seed=33)
+    ck, _ = snapshot_and_check(tensors, host, 1 << 16, direct=True)
+    ck.close()
+
+
+def test_dense_tiny_fragments_at_odd_offsets():
+    """20,000 fragments of 1..1199 bytes at arbitrary byte offsets in one
+    buffer, 16-byte alignment: nearly every tile holds several misaligned
+    fragments, so the sums kernel's general path carries the image and the
+    engines copy 20,000 small pieces.  The restore writes every fragment
+    back and leaves the bytes between them untouched."""
+    rng = np.random.default_rng(4343)
+    n = 20_000
+    sizes = rng.integers(1, 1200, n)
+    gaps = rng.integers(0, 64, n)
+    offs = np.cumsum(gaps + np.concatenate(([0], sizes[:-1])))
+    total = int(offs[-1] + sizes[-1] + 64)
+    host_all = rng.integers(0, 256, total, dtype=np.uint8)
+    dev_all = torch.from_numpy(host_all.copy()).cuda()
+    frags = [dev_all[int(o):int(o) + int(z)] for o, z in zip(offs, sizes)]
+    host = [host_all[int(o):int(o) + int(z)] for o, z in zip(offs, sizes)]
+    chunk = 1 << 20
+    ck = P.Checkpointer(frags, chunk_bytes=chunk, align_bytes=16, group_bytes=2 * chunk, direct=True)
+    snap = ck.snapshot(step=1)
+    ck.wait_committed(snap)
+    img, sums = ck.host_image(snap)
+    want, off, nc = O.pack(host, 16, chunk)
+    assert np.array_equal(ck.offsets, off) and img.size == want.size
+    diff = np.flatnonzero(img != want)
+    assert diff.size == 0, "image differs at %d bytes, first at %d" % (diff.size, diff[0])
+    assert np.array_equal(sums, O.chunk_sums(want, 0, want.size, chunk))
+    dev_all.fill_(0x5A)
+    assert ck.restore(snap) == []
+    torch.cuda.synchronize()
+    got = dev_all.cpu().numpy()
+    marks = np.zeros(total + 1, dtype=np.int64)
+    np.add.at(marks, offs, 1)
+    np.add.at(marks, offs + sizes, -1)
+    in_frag = np.cumsum(marks[:-1]) > 0
+    assert np.array_equal(got[in_frag], host_all[in_frag]), "a fragment byte was not restored"
+    assert np.all(got[~in_frag] == 0x5A), "the restore wrote outside the fragments"
+    ck.close()
+
+
 @pytest.mark.parametrize("bounce", [0, 4 * 8192])
 def test_misaligned_views_and_bit_patterns(bounce):
     """Views at odd byte offsets of one buffer, with NaN payloads, -0,
