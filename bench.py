@@ -149,6 +149,7 @@ DEFAULT_BOUNCE = 8 << 30
 PACK_KERNEL = "tile_kernel<0"  # PACK instantiation of the tile kernel
 SCATTER_KERNEL = "tile_kernel<1"
 VERIFY_KERNEL = "tile_kernel<2"
+SUMS_KERNEL = "sums_run_kernel"  # direct D2H
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 CALIBRATION_BYTES = 1 << 30
 
@@ -180,7 +181,7 @@ def pmc_summary(fetch_dir, write_dir, command):
     same counters on a plain copy kernel of known size (1 GiB read, 1 GiB
     written), into HBM bytes per launch."""
     out = {"kernel_source_sha": kernel_source_sha(), "command": command}
-    others = {"scatter": SCATTER_KERNEL, "verify": VERIFY_KERNEL}
+    others = {"scatter": SCATTER_KERNEL, "verify": VERIFY_KERNEL, "sums": SUMS_KERNEL}
     for name, d in [("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)]:
         rows = [r for r in read_counter_csv(d) if r["Counter_Name"] == name]
         copy = [float(r["Counter_Value"]) for r in rows if COPY_KERNEL in r["Kernel_Name"]
@@ -1264,7 +1265,8 @@ def h2h_leg(torch, P, W, wid, steps, n_peers=1, bounce_bytes=0, host_threads=0):
 def pmc_run(torch, P, W, wid, bounce):
     """Short run whose dispatches the counter summary reads: a 1 GiB plain
     device copy (calibration), then two snapshots of workload wid, one
-    restore and one verify."""
+    restore and one verify, then one snapshot in direct D2H mode (its sums
+    kernel)."""
     a = torch.empty(CALIBRATION_BYTES, dtype=torch.uint8, device="cuda")
     b = torch.empty(CALIBRATION_BYTES, dtype=torch.uint8, device="cuda")
     a.fill_(1)
@@ -1279,9 +1281,15 @@ def pmc_run(torch, P, W, wid, bounce):
         print("pmc run: snapshot %d committed" % k, flush=True)
     if ck.restore(s) or ck.verify(s):  # one pass of the scatter and of the verify kernel
         raise SystemExit("checksum mismatch in the counter run")
-    print("pmc run done: %s, %d payload bytes, %d-byte image" % (W.WORKLOADS[wid]["name"], sum(p[1] for p in plan),
-                                                                  ck.image_bytes), flush=True)
+    image_bytes = ck.image_bytes
     ck.close()
+    ck = P.Checkpointer(tensors, chunk_bytes=W.WORKLOADS[wid]["chunk"], bounce_bytes=bounce, direct=True)
+    s = ck.snapshot(step=2)
+    ck.wait_committed(s)
+    print("pmc run: direct snapshot committed", flush=True)
+    ck.close()
+    print("pmc run done: %s, %d payload bytes, %d-byte image" % (W.WORKLOADS[wid]["name"], sum(p[1] for p in plan),
+                                                                  image_bytes), flush=True)
 
 
 def main():
@@ -1301,10 +1309,11 @@ def main():
                   "# (%d payload bytes, 1 GiB launches), from two rocprofv3 --pmc runs of\n"
                   "# `python bench.py --pmc-run`: FETCH_SIZE, then WRITE_SIZE (KiB per dispatch), each scaled by\n"
                   "# the same counter on a plain 1 GiB device copy (__amd_rocclr_copyBuffer).  The same run's\n"
-                  "# restore (tile_kernel<SCATTER>) and verify (tile_kernel<VERIFY>) passes are summarized too.\n"
+                  "# restore (tile_kernel<SCATTER>), verify (tile_kernel<VERIFY>) and direct D2H snapshot\n"
+                  "# (sums_run_kernel) passes are summarized too.\n"
                   "# Algorithmic bytes per dispatch (%d per pass, the last one short): pack and scatter\n"
-                  "# %d (read + write), verify %d (read)." % (W.WORKLOADS[wid]["name"], S, per, 2 * S // per,
-                                                               I // per))
+                  "# %d (read + write), verify %d (read), sums %d (read)." % (W.WORKLOADS[wid]["name"], S, per,
+                                                                              2 * S // per, I // per, S // per))
         out = args.traffic
         write_summary(out, d, header)
         print(open(out).read())
