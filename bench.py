@@ -1558,6 +1558,19 @@ def main():
                               launch=args.pack_launch_bytes, engines=args.d2h_engines, fixed_R=args.overlap_R,
                               direct=odirect, state=state)
     ck.close()
+    if overlap and args.overlap_mode == "direct":
+        # The overlap's snapshot kernel (direct D2H: sums only) against the
+        # same HBM roofline, from the overlap leg's standalone snapshots.
+        ks = sorted(g for g in overlap["snapshot_kernel_GBps"] if g)
+        if ks:
+            per = -(-int(sn["copy_bytes"]) // (1 << 30))  # 1 GiB launches
+            st = None
+            if summ.get("kernel_source_sha") == kernel_source_sha() and "traffic_bytes_per_sums_dispatch" in summ:
+                st = round(float(summ["traffic_bytes_per_sums_dispatch"]))
+            overlap["sums_roofline"] = {"kernel": "sums_run_kernel (direct D2H)", "bound": "hbm",
+                                        "achieved": ks[len(ks) // 2], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                                        "frac": round(ks[len(ks) // 2] / HBM_PEAK_GBPS, 4),
+                                        "algorithmic_bytes_per_launch": S // per, "traffic": st}
     if args.image_file and os.path.exists(args.image_file):
         os.unlink(args.image_file)
     del tensors
