@@ -904,6 +904,22 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
         sweep.append({"window_over_d2h": ratio, "R": R, "base_ms": round(b, 2), "with_snapshot_ms": round(wv, 2),
                       "overhead_pct": round(100 * (wv - b) / b, 3),
                       "floor_pct": round(100 * max(0.0, t_d2h - b) / b, 3)})
+    # The recovery side in this context's mode: verify, then restore, of the
+    # newest committed snapshot (the tensors already hold its bytes).
+    recovery = None
+    if ck.latest()[0]:
+        P.ckpt_set_timing(ck.ctx, True)
+        bad = ck.verify(0)
+        tv = P.ckpt_last_timing(ck.ctx, P.CKPT_OP_VERIFY)
+        bad += ck.restore(0)
+        tr = P.ckpt_last_timing(ck.ctx, P.CKPT_OP_RESTORE)
+        P.ckpt_set_timing(ck.ctx, False)
+        if bad:
+            raise RuntimeError("checksum mismatch after the overlap run: %s" % bad)
+        recovery = {"verify_GBps": round(tv["copy_bytes"] / tv["total_ms"] / 1e6, 2),
+                    "restore_GBps": round(tr["copy_bytes"] / tr["total_ms"] / 1e6, 2),
+                    "scatter_GBps": round(tr["kernel_bytes"] / tr["kernel_ms"] / 1e6, 1),
+                    "note": "H2D + checks (+ scatter) of the newest committed snapshot, after the overlap run"}
     if shared is None:
         ck.close()
         del tensors
@@ -939,6 +955,8 @@ def overlap_leg(torch, P, W, wid, steps, link_d2h_gbps, ratios=(1.5,), base_step
            "statistic": "mean after dropping 10 warm-up steps and the slowest 5%"}
     if out["d2h_alone_GBps"]:
         out["d2h_alone_frac_of_link"] = round(out["d2h_alone_GBps"] / link_d2h_gbps, 4)
+    if recovery:
+        out["recovery"] = recovery
     if len(sweep) > 1:
         out["sweep"] = sweep
     return out
