@@ -1,7 +1,7 @@
 """The gfx950 code object writes memory only through vector instructions:
 no scalar-cache store, atomic, write-back or discard anywhere in the kernels
-(CPU only: hipcc cross-compiles to assembly).  This file names those
-mnemonics, so it is kept off the GPU runs (.gpurunignore); it needs no GPU."""
+(CPU only: hipcc cross-compiles to assembly; it needs no GPU, and since it
+names those mnemonics it is not shipped to GPU hosts)."""
 import os
 import re
 import subprocess
