@@ -78,6 +78,8 @@ def parse():
                     help="time the load's GEMM alone, beside host-to-device copies and beside a snapshot's "
                          "device-to-host copies (workload 3)")
     ap.add_argument("--gating-workload", type=int, default=3)
+    ap.add_argument("--gating-direct", action="store_true",
+                    help="gate comparison in direct D2H mode instead of with a staging ring")
     ap.add_argument("--gating-ratios", default="0.75",
                     help="compute window / snapshot time ratios of the gate comparison (the full sweep: "
                          "0.5,0.75,1.0,1.5)")
@@ -1114,17 +1116,18 @@ def gemm_beside_leg(torch, P, W, wid=3, reps=5):
     return out
 
 
-def gating_leg(torch, P, W, wid, ratios, steps, base_steps, staging, n_buckets=8):
+def gating_leg(torch, P, W, wid, ratios, steps, base_steps, staging, n_buckets=8, direct=False):
     """Does waiting only on the chunks each bucket overwrites pay?  With a
-    staging ring the capture of the later chunks is paced by the D2H, so a
-    single wait on every fragment holds the whole update back until the last
-    chunk is packed, while per-bucket waits let each bucket go as soon as its
-    own chunks are.  Same loop as the overlap leg, for each window/D2H ratio:
-    no snapshots, snapshots with one whole-range wait, snapshots with
-    per-bucket waits (each run on the same registered state)."""
+    staging ring (or direct D2H) the capture of the later chunks is paced by
+    the D2H, so a single wait on every fragment holds the whole update back
+    until the last chunk is captured, while per-bucket waits let each bucket
+    go as soon as its own chunks are.  Same loop as the overlap leg, for each
+    window/D2H ratio: no snapshots, snapshots with one whole-range wait,
+    snapshots with per-bucket waits (each run on the same registered
+    state)."""
     tensors, plan = W.make_state(wid, device="cuda")
     ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=W.WORKLOADS[wid]["chunk"],
-                        device_staging_bytes=staging)
+                        device_staging_bytes=0 if direct else staging, direct=direct)
     shared = (tensors, plan, ck)
     rows = []
     link = link_peak(torch)["d2h"]
@@ -1133,7 +1136,7 @@ def gating_leg(torch, P, W, wid, ratios, steps, base_steps, staging, n_buckets=8
         res = {}
         for mode in ("whole", "buckets"):
             res[mode] = overlap_leg(torch, P, W, wid, steps, link, (ratio,), base_steps, shared=shared, gating=mode,
-                                    n_buckets=n_buckets, snap=snap)
+                                    n_buckets=n_buckets, snap=snap, direct=direct)
         rows.append({"window_over_d2h": ratio, "R": res["whole"]["R"], "gemm_ms": res["whole"]["gemm_ms"],
                      "update_ms": round(res["whole"]["base_ms"] - res["whole"]["R"] * res["whole"]["gemm_ms"], 2),
                      "base_ms": res["whole"]["base_ms"],
@@ -1151,7 +1154,8 @@ def gating_leg(torch, P, W, wid, ratios, steps, base_steps, staging, n_buckets=8
     del tensors, shared
     torch.cuda.empty_cache()
     return {"workload": W.WORKLOADS[wid]["name"], "payload_bytes": sum(p[1] for p in plan),
-            "device_staging": staging_text(staging, W.WORKLOADS[wid]["chunk"]), "buckets": n_buckets,
+            "device_staging": ("none (direct D2H: the gate waits for the copies)" if direct
+                               else staging_text(staging, W.WORKLOADS[wid]["chunk"])), "buckets": n_buckets,
             "gemm_mkn": list(W.OVERLAP_GEMM[wid]), "steps": steps, "base_steps": base_steps, "rows": rows}
 
 
@@ -1398,7 +1402,7 @@ def main():
         return
     if args.gating_only:
         g = gating_leg(torch, P, W, args.gating_workload, [float(r) for r in args.gating_ratios.split(",") if r],
-                       args.gating_steps, args.gating_base_steps, args.gating_staging_bytes)
+                       args.gating_steps, args.gating_base_steps, args.gating_staging_bytes, direct=args.gating_direct)
         print(json.dumps({"gating": g}), flush=True)
         return
     if args.overlap_only:
