@@ -622,7 +622,14 @@ ckpt_status check_image(ckpt_ctx* c, int b, hipStream_t stream, bool scatter, co
         const uint64_t ev = u % L.n_units;
         const uint64_t area = L.ring ? u % L.n_slots : ev;
         uint8_t* stage = L.ring ? L.base + area * unit : L.base + lo;
-        HIPCHK(c, hipStreamWaitEvent(L.s_copy, (*L.area_free)[area], 0));
+        // A device slot is reused once the kernel of the span that last used
+        // it has finished.  With pageable images the host paces every span
+        // (it fills the pinned slot first), so it waits for that kernel itself
+        // right before the copy: the same wait as a device-side one on the
+        // copy stream, which here cost ~6% of the link (verify 53.5 against
+        // 56.8 GB/s through the bounce rings).
+        const bool host_wait = c->bounce && L.ring;
+        if (!host_wait) HIPCHK(c, hipStreamWaitEvent(L.s_copy, (*L.area_free)[area], 0));
         if (timed && u == 0) HIPCHK(c, hipEventRecord(L.c0, L.s_copy));
         if (fill && !fill(lo, hi)) { // the span's bytes did not arrive: let the issued work finish, then fail
             (void)hipStreamSynchronize(L.s_copy);
@@ -636,6 +643,7 @@ ckpt_status check_image(ckpt_ctx* c, int b, hipStream_t stream, bool scatter, co
             c->pool->copy(c->h_bin + slot * unit, src, hi - lo);
             src = c->h_bin + slot * unit;
         }
+        if (host_wait) HIPCHK(c, hipEventSynchronize((*L.area_free)[area]));
         HIPCHK(c, hipMemcpyAsync(stage, src, hi - lo, hipMemcpyHostToDevice, L.s_copy));
         if (c->bounce) HIPCHK(c, hipEventRecord(c->bin_done[u % c->n_bslots], L.s_copy));
         if (timed && u + 1 == n_spans) HIPCHK(c, hipEventRecord(L.c1, L.s_copy));
