@@ -72,7 +72,8 @@ typedef int32_t ckpt_status;
 #define CKPT_ERANGE (-8)   /* snapshot id unknown or no longer retained */
 
 /* ckpt_wait modes */
-#define CKPT_WAIT_CAPTURED 0  /* stream-ordered: packed into device staging */
+#define CKPT_WAIT_CAPTURED 0  /* stream-ordered: the fragments may be overwritten (packed into device
+                                 staging; with direct_d2h, summed and copied to the host) */
 #define CKPT_WAIT_COMMITTED 1 /* host-blocking: image and sums landed in host memory */
 #define CKPT_WAIT_REPLICATED 2 /* host-blocking: the ring peer has checked and committed the replica */
 
