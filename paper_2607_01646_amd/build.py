@@ -18,8 +18,8 @@ DEVICE_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC",
                 "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 # The runtime has no device code: plain g++ against the HIP headers.
 HOST_CXX = os.environ.get("CXX_HOST", "g++")
-HOST_SOURCES = ["ckpt_runtime.cpp", "ckpt_bounce.cpp", "ckpt_file.cpp", "ckpt_h2h.cpp", "ckpt_peer.cpp",
-                "ckpt_recover.cpp", "ckpt_noalloc.cpp"]
+HOST_SOURCES = ["ckpt_runtime.cpp", "ckpt_snapshot.cpp", "ckpt_check.cpp", "ckpt_bounce.cpp", "ckpt_file.cpp",
+                "ckpt_h2h.cpp", "ckpt_peer.cpp", "ckpt_recover.cpp", "ckpt_noalloc.cpp"]
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-pthread", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__",
               "-I", "/opt/rocm/include"]
 

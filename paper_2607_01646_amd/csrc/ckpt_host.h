@@ -443,6 +443,30 @@ const char* hsa_text(hsa_status_t s);
 
 uint64_t round_up(uint64_t x, uint64_t a);
 bool geometry_ok(uint64_t C, uint32_t A);
+
+// Chunk group g: image bytes [group_lo, group_hi), tiles [tiles_lo,
+// tiles_hi), its staging area (a ring slot, or its own place in the full
+// device image) and where that area starts.
+inline uint64_t group_lo(const ckpt_ctx* c, uint64_t g) { return g * c->G * c->C; }
+inline uint64_t group_hi(const ckpt_ctx* c, uint64_t g) { return std::min((g + 1) * c->G * c->C, c->I); }
+inline uint64_t tiles_lo(const ckpt_ctx* c, uint64_t g) { return group_lo(c, g) >> c->geo.tile_shift; }
+inline uint64_t tiles_hi(const ckpt_ctx* c, uint64_t g)
+{
+    return (group_hi(c, g) + (1ull << c->geo.tile_shift) - 1) >> c->geo.tile_shift;
+}
+inline uint64_t area_of(const ckpt_ctx* c, uint64_t g) { return c->ring ? g % c->n_slots : g; }
+inline uint8_t* staging_of(const ckpt_ctx* c, uint64_t g)
+{
+    return c->ring ? c->d_staging + (g % c->n_slots) * c->G * c->C : c->d_staging + group_lo(c, g);
+}
+
+ckpt_status make_event(ckpt_ctx* c, hipEvent_t* e, bool timed);
+// Milliseconds between two recorded timing events (-1 when unavailable).
+float elapsed(hipEvent_t a, hipEvent_t b);
+// Issue one SDMA copy of n bytes on `engine`, after *dep (when non-null),
+// completing into `completion`.
+ckpt_status dma(ckpt_ctx* c, void* dst, hsa_agent_t dst_agent, const void* src, hsa_agent_t src_agent, uint64_t n,
+                const hsa_signal_t* dep, hsa_signal_t completion, hsa_amd_sdma_engine_id_t engine);
 // Text of this thread's last failed ckpt_pack_noalloc ("" if none).
 const char* noalloc_error();
 
@@ -454,7 +478,7 @@ ckpt_status drain(ckpt_ctx* c);
 // The host image the next snapshot would fill (EBUSY while a snapshot is
 // uncommitted or that image is being sent to the peer).
 ckpt_status pick_target_image(ckpt_ctx* c, int* out);
-// Restore (scatter) or verify host image b against h_sums[b]: all chunks,
+// Restore (scatter) or verify host image b against h_sums[b] (ckpt_check.cpp): all chunks,
 // or only `ids` (increasing).  Fills the bad list like ckpt_restore.  With
 // `fill`, each span [lo, hi) of image bytes is first handed to fill, which
 // puts them in place (the host -> device work of earlier spans runs
@@ -468,11 +492,16 @@ void parallel_zero(uint8_t* p, uint64_t n);
 std::vector<uint8_t> build_envelope(const ckpt_ctx* c, uint64_t step, const std::vector<uint8_t>& meta,
                                     const uint64_t* sums);
 
+// Issue snapshot r (ckpt_snapshot.cpp): its kernels on the pack stream after
+// the work already on `after`, and its copies; groups from n_copy on stay on
+// the device, and stop >= 0 marks the snapshot interrupted (never committed).
+ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop);
+
 // Direct D2H: zero group g's padding runs in `dst` (host memory holding the
 // group's first image byte at dst), then copy its fragment pieces into place
 // on `engine`, each after the previous one (the first after first_dep); the
 // group's last piece signals res->copied[g].  Returns the pieces issued:
-// fewer than the group's means a copy could not be issued (ckpt_runtime.cpp).
+// fewer than the group's means a copy could not be issued (ckpt_snapshot.cpp).
 uint64_t issue_pieces(ckpt_ctx* c, RecRes* res, uint64_t g, uint8_t* dst, hsa_agent_t dst_agent,
                       const hsa_signal_t* first_dep, hsa_amd_sdma_engine_id_t engine);
 

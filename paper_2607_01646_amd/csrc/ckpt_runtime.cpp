@@ -34,10 +34,12 @@
 // group: DMA host image -> staging on the copy stream, then the scatter
 // kernel on the pack stream writes the fragments and re-checks the sums.
 //
-// Also here: registration, restore and verify, and the accessors.  The
-// bounce-mode pump, the image file and replication have files of their own
-// (ckpt_bounce.cpp, ckpt_file.cpp, ckpt_h2h.cpp); ckpt_host.h holds what
-// they share.
+// Here: context set-up, registration and its layout, the snapshot records,
+// the gate, restore and verify entry points, and the accessors.  Issuing a
+// snapshot (ckpt_snapshot.cpp), the restore and verify pipeline
+// (ckpt_check.cpp), the bounce-mode pump (ckpt_bounce.cpp), the image file
+// (ckpt_file.cpp) and replication (ckpt_h2h.cpp) have files of their own;
+// ckpt_host.h holds what they share.
 #include "ckpt_host.h"
 
 namespace ckpt {
@@ -149,19 +151,6 @@ bool direct_plan(const uint64_t* off, const uint64_t* nb, uint32_t n, uint64_t I
     piece_first[n_groups] = pieces.size();
     gap_first[n_groups] = gaps.size();
     return true;
-}
-
-uint64_t group_lo(const ckpt_ctx* c, uint64_t g) { return g * c->G * c->C; }
-uint64_t group_hi(const ckpt_ctx* c, uint64_t g) { return std::min((g + 1) * c->G * c->C, c->I); }
-uint64_t tiles_lo(const ckpt_ctx* c, uint64_t g) { return group_lo(c, g) >> c->geo.tile_shift; }
-uint64_t tiles_hi(const ckpt_ctx* c, uint64_t g)
-{
-    return (group_hi(c, g) + (1ull << c->geo.tile_shift) - 1) >> c->geo.tile_shift;
-}
-uint64_t area_of(const ckpt_ctx* c, uint64_t g) { return c->ring ? g % c->n_slots : g; }
-uint8_t* staging_of(const ckpt_ctx* c, uint64_t g)
-{
-    return c->ring ? c->d_staging + (g % c->n_slots) * c->G * c->C : c->d_staging + group_lo(c, g);
 }
 
 ckpt_status make_event(ckpt_ctx* c, hipEvent_t* e, bool timed)
@@ -554,152 +543,6 @@ float elapsed(hipEvent_t a, hipEvent_t b)
     return ms;
 }
 
-// Where restore and verify stage image bytes on the device, and the streams
-// and events that order them.  Unit u covers chunks [u*G, (u+1)*G).
-struct Lane {
-    hipStream_t s_copy, s_ker;
-    uint8_t* base;   // staging: full image, or ring slots of G chunks each
-    bool ring;
-    uint64_t n_slots;
-    uint64_t G;
-    uint64_t n_units;
-    std::vector<hipEvent_t>* area_free; // per slot (ring) or per unit
-    std::vector<hipEvent_t>* loaded;    // per unit
-    std::vector<hipEvent_t>* tk0;       // per unit, timing
-    std::vector<hipEvent_t>* tk1;
-    hipEvent_t done, t0, c0, c1;
-};
-
-Lane restore_lane(ckpt_ctx* c)
-{
-    return Lane{c->s_copy, c->s_pack, c->d_staging, c->ring || c->direct, c->n_slots, c->G, c->n_groups, &c->area_free,
-                &c->ev_loaded, &c->tk0, &c->tk1, c->ev_done, c->tt0, c->tc0, c->tc1};
-}
-
-Lane verify_lane(ckpt_ctx* c)
-{
-    return Lane{c->s_vcopy, c->s_vker, c->d_vring, true, c->n_vslots, c->G, c->n_groups, &c->vfree,
-                &c->vloaded, &c->vk0, &c->vk1, c->ev_vdone, c->vt0, c->vc0, c->vc1};
-}
-
-// Restore (scatter=true) or verify (scatter=false) the chunks of host image
-// b against the sums in h_sums[b]: every chunk, or only the chunks `ids`
-// (increasing) when given.  The caller has checked the arguments and, for a
-// restore, drained every snapshot.
-ckpt_status check_image(ckpt_ctx* c, int b, hipStream_t stream, bool scatter, const std::vector<uint64_t>* ids,
-                        uint32_t* bad_chunks, uint32_t cap, uint32_t* n_bad,
-                        const std::function<bool(uint64_t, uint64_t)>& fill)
-{
-    const Lane L = scatter ? restore_lane(c) : verify_lane(c);
-    const int op = scatter ? CKPT_OP_RESTORE : CKPT_OP_VERIFY;
-    const uint64_t unit = L.G * c->C;
-    // Byte spans to move, each within one unit's size: whole units, or the
-    // runs of consecutive chunk ids cut at that size.
-    std::vector<std::pair<uint64_t, uint64_t>> spans;
-    if (!ids) {
-        for (uint64_t u = 0; u < L.n_units; ++u) spans.emplace_back(u * unit, std::min((u + 1) * unit, c->I));
-    } else {
-        for (size_t j = 0; j < ids->size();) {
-            size_t k = j + 1;
-            while (k < ids->size() && (*ids)[k] == (*ids)[k - 1] + 1 && k - j < L.G) ++k;
-            spans.emplace_back((*ids)[j] * c->C, std::min(((*ids)[k - 1] + 1) * c->C, c->I));
-            j = k;
-        }
-    }
-    const uint64_t n_spans = spans.size();
-    // Per-span events are reused round-robin past the unit count; timing is
-    // kept for whole-image operations only.
-    const bool timed = c->timing && !ids;
-    unsigned long long* partials = c->d_partials + c->geo.n_tiles * kTileParts;
-    HIPCHK(c, hipMemcpyAsync(c->d_expected, c->h_sums[b], c->n_chunks * 8, hipMemcpyHostToDevice, L.s_copy));
-    if (scatter) {
-        HIPCHK(c, hipEventRecord(c->ev_trigger, stream));
-        HIPCHK(c, hipStreamWaitEvent(L.s_ker, c->ev_trigger, 0));
-    }
-    if (timed) HIPCHK(c, hipEventRecord(L.t0, L.s_copy));
-    for (uint64_t u = 0; u < n_spans; ++u) {
-        const uint64_t lo = spans[u].first, hi = spans[u].second;
-        const uint64_t ev = u % L.n_units;
-        const uint64_t area = L.ring ? u % L.n_slots : ev;
-        uint8_t* stage = L.ring ? L.base + area * unit : L.base + lo;
-        // A device slot is reused once the kernel of the span that last used
-        // it has finished.  With pageable images the host paces every span
-        // (it fills the pinned slot first), so it waits for that kernel itself
-        // right before the copy: the same wait as a device-side one on the
-        // copy stream, which here cost ~6% of the link (verify 53.5 against
-        // 56.8 GB/s through the bounce rings).
-        const bool host_wait = c->bounce && L.ring;
-        if (!host_wait) HIPCHK(c, hipStreamWaitEvent(L.s_copy, (*L.area_free)[area], 0));
-        if (timed && u == 0) HIPCHK(c, hipEventRecord(L.c0, L.s_copy));
-        if (fill && !fill(lo, hi)) { // the span's bytes did not arrive: let the issued work finish, then fail
-            (void)hipStreamSynchronize(L.s_copy);
-            (void)hipStreamSynchronize(L.s_ker);
-            return CKPT_EHIP;
-        }
-        const uint8_t* src = c->h_img[b] + lo;
-        if (c->bounce) { // pageable image: through a pinned ring slot
-            const uint64_t slot = u % c->n_bslots;
-            if (u >= c->n_bslots) HIPCHK(c, hipEventSynchronize(c->bin_done[slot]));
-            c->pool->copy(c->h_bin + slot * unit, src, hi - lo);
-            src = c->h_bin + slot * unit;
-        }
-        if (host_wait) HIPCHK(c, hipEventSynchronize((*L.area_free)[area]));
-        HIPCHK(c, hipMemcpyAsync(stage, src, hi - lo, hipMemcpyHostToDevice, L.s_copy));
-        if (c->bounce) HIPCHK(c, hipEventRecord(c->bin_done[u % c->n_bslots], L.s_copy));
-        if (timed && u + 1 == n_spans) HIPCHK(c, hipEventRecord(L.c1, L.s_copy));
-        HIPCHK(c, hipEventRecord((*L.loaded)[ev], L.s_copy));
-        HIPCHK(c, hipStreamWaitEvent(L.s_ker, (*L.loaded)[ev], 0));
-        const uint64_t t_lo = lo >> c->geo.tile_shift, t_hi = (hi + (1ull << c->geo.tile_shift) - 1) >> c->geo.tile_shift;
-        hipEvent_t k0 = timed ? (*L.tk0)[u] : nullptr, k1 = timed ? (*L.tk1)[u] : nullptr;
-        hipError_t e;
-        if (scatter)
-            e = launch_scatter(c->d_frags, c->d_tile_first, c->d_tile_last, c->geo, t_lo, t_hi, stage, lo, partials,
-                               c->grid_cap, L.s_ker, k0, k1);
-        else
-            e = launch_checksum(c->geo, t_lo, t_hi, stage, lo, partials, c->grid_cap, L.s_ker, k0, k1);
-        if (e != hipSuccess) return fail(c, CKPT_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
-        e = launch_chunk_reduce(c->geo, t_lo, t_hi, partials, c->d_recomputed, c->d_expected, c->d_bad, L.s_ker);
-        if (e != hipSuccess) return fail(c, CKPT_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
-        HIPCHK(c, hipEventRecord((*L.area_free)[area], L.s_ker));
-    }
-    HIPCHK(c, hipMemcpyAsync(c->h_bad, c->d_bad, c->n_chunks, hipMemcpyDeviceToHost, L.s_ker));
-    HIPCHK(c, hipMemcpyAsync(c->h_recomputed, c->d_recomputed, c->n_chunks * 8, hipMemcpyDeviceToHost, L.s_ker));
-    HIPCHK(c, hipEventRecord(L.done, L.s_ker));
-    if (scatter) HIPCHK(c, hipStreamWaitEvent(stream, L.done, 0));
-    HIPCHK(c, hipEventSynchronize(L.done));
-    if (timed) {
-        ckpt_timing t{};
-        for (uint64_t u = 0; u < L.n_units; ++u) t.kernel_ms += elapsed((*L.tk0)[u], (*L.tk1)[u]);
-        t.kernels = (uint32_t)L.n_units;
-        t.copies = (uint32_t)L.n_units;
-        t.copy_ms = elapsed(L.c0, L.c1);
-        t.total_ms = elapsed(L.t0, (*L.tk1)[L.n_units - 1]);
-        t.kernel_bytes = scatter ? 2 * c->payload : c->I;
-        t.copy_bytes = c->I;
-        t.span_ms = -1.f;
-        c->op_timing[op].t = t;
-        c->op_timing[op].valid = true;
-    }
-    uint32_t nb = 0;
-    auto flag = [&](uint64_t k) {
-        if (!c->h_bad[k]) return;
-        if (nb < cap) bad_chunks[nb] = (uint32_t)k;
-        ++nb;
-    };
-    if (ids) {
-        for (uint64_t k : *ids) flag(k);
-    } else {
-        c->last_sums.assign(c->h_recomputed, c->h_recomputed + c->n_chunks);
-        c->have_last_sums = true;
-        for (uint64_t k = 0; k < c->n_chunks; ++k) flag(k);
-    }
-    *n_bad = nb;
-    if (nb)
-        return fail(c, CKPT_ECORRUPT, "%u of %llu chunks failed their checksum", nb,
-                    (unsigned long long)(ids ? ids->size() : c->n_chunks));
-    return CKPT_OK;
-}
-
 // Restore (scatter=true) or verify (scatter=false) from a committed image.
 // Restore first waits for every outstanding snapshot (it rewrites the live
 // tensors and shares the snapshot staging).  Verify only reads a committed
@@ -830,7 +673,6 @@ std::vector<uint8_t> build_envelope(const ckpt_ctx* c, uint64_t step, const std:
     return buf;
 }
 
-ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop);
 
 } // namespace ckpt
 
@@ -1198,308 +1040,6 @@ ckpt_status ckpt_snapshot_async(ckpt_ctx* c, void* after_stream, uint64_t step, 
 }
 
 } // extern "C"
-
-namespace ckpt {
-
-// The snapshot's chunk-sum copy (after the reduce has released dep_sums),
-// and in image-file mode its commit record, behind the group copies.
-ckpt_status issue_sums_copy(ckpt_ctx* c, SnapRec& r)
-{
-    RecRes* res = r.res;
-    if (r.bounce) { // behind the snapshot's group copies
-        {
-            std::lock_guard<std::mutex> l(c->pump->m);
-            PumpItem sums;
-            sums.res = res;
-            sums.sums = true;
-            sums.image = (uint8_t*)c->h_sums[r.buf];
-            sums.staging = (const uint8_t*)res->d_sums;
-            sums.n = c->n_chunks * 8;
-            sums.engine = c->d2h_engine[0];
-            sums.buf = r.buf;
-            sums.need_rec = c->pump->rec_pushed[r.buf];
-            c->pump->issue_q.push_back(sums);
-            if (c->file_map) { // then the commit record, once all of it has landed
-                ++c->pump->rec_pushed[r.buf];
-                PumpItem rec;
-                rec.res = res;
-                rec.groups = r.groups_copied;
-                rec.buf = r.buf;
-                rec.record = true;
-                rec.snap_id = r.id;
-                rec.step = r.step;
-                rec.meta = std::make_shared<const std::vector<uint8_t>>(r.meta);
-                c->pump->issue_q.push_back(std::move(rec));
-            }
-        }
-        c->pump->cv.notify_all();
-        return CKPT_OK;
-    }
-    ckpt_status st = dma(c, c->h_sums[r.buf], c->img_agent[r.buf], res->d_sums, c->gpu_agent, c->n_chunks * 8,
-                         &res->dep_sums, res->done, c->d2h_engine[0]);
-    if (st) hsa_signal_store_screlease(res->done, 0);
-    return st;
-}
-
-uint64_t issue_pieces(ckpt_ctx* c, RecRes* res, uint64_t g, uint8_t* dst, hsa_agent_t dst_agent,
-                      const hsa_signal_t* first_dep, hsa_amd_sdma_engine_id_t engine)
-{
-    const uint64_t lo = group_lo(c, g);
-    for (uint64_t k = c->gap_first[g]; k < c->gap_first[g + 1]; ++k)
-        std::memset(dst + (c->gaps[k].off - lo), 0, c->gaps[k].n);
-    const uint64_t p0 = c->piece_first[g], p1 = c->piece_first[g + 1];
-    const hsa_signal_t* dep = first_dep;
-    for (uint64_t k = p0; k < p1; ++k) {
-        const Piece& pc = c->pieces[k];
-        const hsa_signal_t* done = k + 1 == p1 ? &res->copied[g] : &res->piece_done[k];
-        hsa_signal_store_screlease(*done, 1);
-        if (hsa_amd_memory_async_copy_on_engine(dst + (pc.off - lo), dst_agent, (const void*)(uintptr_t)pc.src,
-                                                c->gpu_agent, pc.n, dep ? 1 : 0, dep, *done, engine,
-                                                true) != HSA_STATUS_SUCCESS) {
-            hsa_signal_store_screlease(*done, 0);
-            return k - p0;
-        }
-        dep = done;
-    }
-    return p1 - p0;
-}
-
-// Direct D2H (no snapshot staging): per group, the sums kernel reads the
-// fragments, and the group's pieces go from the tensors to host memory on a
-// DMA engine once the next launch on the pack stream has released the
-// group (its sums have been read; the trigger has long passed).  The copies
-// finishing bump the group's counter, on which the gate waits.
-ckpt_status issue_groups_direct(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop,
-                                hsa_signal_t& carried)
-{
-    RecRes* res = r.res;
-    uint8_t* himg = c->h_img[r.buf];
-    hsa_agent_t host = c->img_agent[r.buf];
-    HIPCHK(c, hipEventRecord(c->ev_trigger, after));
-    HIPCHK(c, hipStreamWaitEvent(c->s_pack, c->ev_trigger, 0));
-    if (r.timed) HIPCHK(c, hipEventRecord(res->t0, c->s_pack));
-    int64_t* pending = nullptr; // the previous group's release, carried by the next launch
-    for (uint64_t g = 0; g < c->n_groups; ++g) {
-        const uint64_t lo = group_lo(c, g);
-        hipError_t e = launch_sums(c->d_frags, c->d_tile_first, c->d_tile_last, c->geo, tiles_lo(c, g),
-                                   tiles_hi(c, g), c->d_partials, c->grid_cap, c->s_pack,
-                                   r.timed && (r.per_launch || g == 0) ? res->k0[g] : nullptr,
-                                   r.timed && (r.per_launch || g == 0) ? res->k1[g] : nullptr, pending);
-        if (e != hipSuccess) return fail(c, CKPT_EHIP, "sums launch failed: %s", hipGetErrorString(e));
-        pending = nullptr;
-        carried.handle = 0;
-        HIPCHK(c, hipEventRecord(res->captured[g], c->s_pack));
-        if (g >= n_copy) continue; // interrupted offload: this group never leaves the device
-        hsa_signal_store_screlease(res->dep[g], 1);
-        pending = res->dep_val[g];
-        carried = res->dep[g];
-        hsa_signal_store_screlease(res->copied[g], 1);
-        hsa_signal_store_screlease(res->flagged[g], 1);
-        r.groups_copied = (uint32_t)(g + 1);
-        const hsa_amd_sdma_engine_id_t eng = c->d2h_engine[g % c->n_d2h_engines];
-        res->h_seq[g] = c->area_seq[g] + 1;
-        ++c->area_seq[g];
-        if (r.bounce) { // the pump issues the pieces once a ring slot is free
-            {
-                std::lock_guard<std::mutex> l(c->pump->m);
-                PumpItem it;
-                it.res = res;
-                it.g = (uint32_t)g;
-                it.image = himg + lo;
-                it.lo = lo;
-                it.n = group_hi(c, g) - lo;
-                it.area_done = c->d_area_done + g;
-                it.seq = &res->h_seq[g];
-                it.engine = eng;
-                it.buf = r.buf;
-                c->pump->issue_q.push_back(it);
-            }
-            c->pump->cv.notify_all();
-            continue;
-        }
-        const uint64_t want = c->piece_first[g + 1] - c->piece_first[g];
-        const uint64_t got = issue_pieces(c, res, g, himg + lo, host, &res->dep[g], eng);
-        ckpt_status st = CKPT_OK;
-        if (got == want)
-            st = dma(c, c->d_area_done + g, c->gpu_agent, &res->h_seq[g], host, 8, &res->copied[g], res->flagged[g],
-                     c->h2d_engine);
-        if (got != want || st) {
-            // Let the issued pieces run (nothing else will release them),
-            // wait until they have read the tensors, then count the group
-            // as copied so that no gate waits forever; the snapshot is
-            // marked interrupted and never restored.
-            hsa_signal_store_screlease(res->dep[g], 0);
-            carried.handle = 0;
-            if (got && got < want) (void)poll_zero(res->piece_done[c->piece_first[g] + got - 1], 120);
-            if (got == want) (void)poll_zero(res->copied[g], 120);
-            (void)hsa_memory_copy(c->d_area_done + g, &res->h_seq[g], 8);
-            hsa_signal_store_screlease(res->copied[g], 0);
-            hsa_signal_store_screlease(res->flagged[g], 0);
-            return st ? st : fail(c, CKPT_EHIP, "DMA of a fragment piece of group %llu could not be issued",
-                                  (unsigned long long)g);
-        }
-    }
-    if (stop >= 0) {
-        r.aborted = true; // interrupted offload: never committed
-        if (pending) {
-            hipError_t e = launch_release(pending, c->s_pack);
-            if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
-            carried.handle = 0;
-        }
-        return CKPT_OK;
-    }
-    hipError_t e = launch_chunk_reduce(c->geo, 0, c->geo.n_tiles, c->d_partials, res->d_sums, nullptr, nullptr,
-                                       c->s_pack, pending);
-    if (e != hipSuccess) return fail(c, CKPT_EHIP, "reduce launch failed: %s", hipGetErrorString(e));
-    carried.handle = 0;
-    hsa_signal_store_screlease(res->dep_sums, 1);
-    e = launch_release(res->dep_sums_val, c->s_pack);
-    if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
-    if (r.timed) HIPCHK(c, hipEventRecord(res->t_red, c->s_pack));
-    hsa_signal_store_screlease(res->done, 1);
-    return issue_sums_copy(c, r);
-}
-
-// The body of issue_snapshot.  `carried` is the signal of a group whose DMA
-// has been issued while the launch that will release it has not yet been
-// enqueued; on an error return the caller releases it from the host.
-ckpt_status issue_groups(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop,
-                         hsa_signal_t& carried)
-{
-    RecRes* res = r.res;
-    uint8_t* himg = c->h_img[r.buf];
-    hsa_agent_t host = c->img_agent[r.buf];
-    ckpt_status st = CKPT_OK;
-    HIPCHK(c, hipEventRecord(c->ev_trigger, after));
-    HIPCHK(c, hipStreamWaitEvent(c->s_pack, c->ev_trigger, 0));
-    if (r.timed) HIPCHK(c, hipEventRecord(res->t0, c->s_pack));
-    // Each launch packs LG groups; each copied group's DMA waits for the
-    // signal of its launch's first group to drop to 0.  With a full-size
-    // image the next launch on the pack stream (the next pack, or the
-    // chunk-sum reduce after the last) sets it, which happens only after this
-    // launch's pack has finished; in ring mode the next pack may first wait
-    // for a slot, so a one-lane kernel releases the group right after its
-    // pack instead.
-    const bool carry = !c->ring;
-    int64_t* pending = nullptr; // the previous launch's release, carried by the next launch
-    for (uint64_t g = 0; g < c->n_groups; ++g) {
-        const uint64_t lo = group_lo(c, g), hi = group_hi(c, g);
-        const uint64_t area = area_of(c, g);
-        const uint64_t j = g / c->LG;      // this group's launch
-        const uint64_t g0 = j * c->LG;     // its first group
-        const uint64_t g1 = std::min(g0 + c->LG, c->n_groups);
-        if (g == g0) {
-            // A staging area is free once every copy issued out of it so far
-            // has finished (each finished copy bumps area_done by one); the
-            // launch writes the areas of all its groups.
-            for (uint64_t h = g0; h < g1; ++h) {
-                const uint64_t a = area_of(c, h);
-                if (c->area_seq[a])
-                    HIPCHK(c, hipStreamWaitValue64(c->s_pack, c->d_area_done + a, c->area_seq[a],
-                                                  hipStreamWaitValueGte, ~0ull));
-            }
-            if (c->poison) { // debug check: the canary, then the pack over it (stream order)
-                uint32_t w[4];
-                std::memcpy(w, CKPT_CANARY, 16);
-                hipError_t e = launch_fill16(staging_of(c, g0), group_hi(c, g1 - 1) - lo, w, c->s_pack);
-                if (e != hipSuccess) return fail(c, CKPT_EHIP, "canary fill failed: %s", hipGetErrorString(e));
-            }
-            hipError_t e = launch_pack(c->d_frags, c->d_tile_first, c->d_tile_last, c->geo, tiles_lo(c, g0),
-                                       tiles_hi(c, g1 - 1), staging_of(c, g0), lo, c->d_partials, c->grid_cap,
-                                       c->s_pack, r.timed && (r.per_launch || j == 0) ? res->k0[j] : nullptr,
-                                       r.timed && (r.per_launch || j == 0) ? res->k1[j] : nullptr,
-                                       pending);
-            if (e != hipSuccess) return fail(c, CKPT_EHIP, "pack launch failed: %s", hipGetErrorString(e));
-            pending = nullptr; // enqueued: the GPU releases it
-            carried.handle = 0;
-            // The gate and the launch's copies need the packed bytes only; the
-            // chunk sums are added up once, after the last launch (below).
-            HIPCHK(c, hipEventRecord(res->captured[g1 - 1], c->s_pack));
-            if (g0 < n_copy) {
-                hsa_signal_store_screlease(res->dep[g0], 1); // before any copy is issued or a launch clears it
-                if (carry) {
-                    pending = res->dep_val[g0];
-                    carried = res->dep[g0];
-                } else {
-                    e = launch_release(res->dep_val[g0], c->s_pack);
-                    if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
-                }
-            }
-        }
-        if (g >= n_copy) continue; // interrupted offload: this group never leaves the device
-        hsa_signal_store_screlease(res->copied[g], 1);
-        hsa_signal_store_screlease(res->flagged[g], 1);
-        r.groups_copied = (uint32_t)(g + 1);
-        const hsa_amd_sdma_engine_id_t eng = c->d2h_engine[g % c->n_d2h_engines];
-        res->h_seq[g] = c->area_seq[area] + 1;
-        if (r.bounce) { // the pump issues the copies once a ring slot is free
-            {
-                std::lock_guard<std::mutex> l(c->pump->m);
-                PumpItem it;
-                it.res = res;
-                it.g = (uint32_t)g;
-                it.image = himg + lo;
-                it.staging = staging_of(c, g);
-                it.n = hi - lo;
-                it.area_done = c->d_area_done + area;
-                it.seq = &res->h_seq[g];
-                it.engine = eng;
-                it.buf = r.buf;
-                c->pump->issue_q.push_back(it);
-            }
-            c->pump->cv.notify_all();
-            ++c->area_seq[area];
-            continue;
-        }
-        st = dma(c, himg + lo, host, staging_of(c, g), c->gpu_agent, hi - lo, &res->dep[g0], res->copied[g], eng);
-        if (!st)
-            st = dma(c, c->d_area_done + area, c->gpu_agent, &res->h_seq[g], host, 8, &res->copied[g],
-                     res->flagged[g], c->h2d_engine);
-        if (st) {
-            // nothing will lower the signals of this group
-            hsa_signal_store_screlease(res->copied[g], 0);
-            hsa_signal_store_screlease(res->flagged[g], 0);
-            return st;
-        }
-        ++c->area_seq[area];
-    }
-    if (stop >= 0) {
-        r.aborted = true; // interrupted offload: never committed (its pack timing stays readable)
-        if (pending) {    // the last copied group was the last group
-            hipError_t e = launch_release(pending, c->s_pack);
-            if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
-            carried.handle = 0;
-        }
-    } else {
-        // Every chunk's sum from its tiles' partial sums, in one launch: only
-        // the sums copy below needs them, and one launch per group would cost
-        // the caller host time per group.  It also releases the last group.
-        hipError_t e = launch_chunk_reduce(c->geo, 0, c->geo.n_tiles, c->d_partials, res->d_sums, nullptr, nullptr,
-                                           c->s_pack, pending);
-        if (e != hipSuccess) return fail(c, CKPT_EHIP, "reduce launch failed: %s", hipGetErrorString(e));
-        carried.handle = 0;
-        hsa_signal_store_screlease(res->dep_sums, 1);
-        e = launch_release(res->dep_sums_val, c->s_pack);
-        if (e != hipSuccess) return fail(c, CKPT_EHIP, "release launch failed: %s", hipGetErrorString(e));
-        if (r.timed) HIPCHK(c, hipEventRecord(res->t_red, c->s_pack));
-        hsa_signal_store_screlease(res->done, 1);
-        return issue_sums_copy(c, r);
-    }
-    return CKPT_OK;
-}
-
-ckpt_status issue_snapshot(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_copy, int32_t stop)
-{
-    hsa_signal_t carried{0};
-    const ckpt_status st = c->direct ? issue_groups_direct(c, r, after, n_copy, stop, carried)
-                                     : issue_groups(c, r, after, n_copy, stop, carried);
-    // A DMA whose release never got enqueued would wait forever: let it run
-    // (the snapshot is marked interrupted and is never restored).
-    if (st && carried.handle) hsa_signal_store_screlease(carried, 0);
-    return st;
-}
-
-} // namespace ckpt
 
 extern "C" {
 
