@@ -301,7 +301,9 @@ def stats_summary(d, command):
 
 def gemm_inflation(d, command):
     """GEMM dispatch durations of an overlap run, split by what ran beside
-    them: a pack launch of the library, a device-to-host copy, or neither."""
+    them: a pack (or, in direct D2H mode, sums) launch of the library, a
+    device-to-host copy, or neither; and the GEMM time each adds over the
+    median of the GEMMs that ran alone."""
     import bisect
     import csv
     import glob
@@ -309,12 +311,14 @@ def gemm_inflation(d, command):
 
     kt = glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True)
     mt = glob.glob(os.path.join(d, "**", "*memory_copy_trace.csv"), recursive=True)
-    gemms, packs, copies = [], [], []
+    gemms, packs, sums, copies = [], [], [], []
     for f in kt:
         for r in csv.DictReader(open(f)):
             a, b, n = int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"]
             if PACK_KERNEL in n:
                 packs.append((a, b))
+            elif SUMS_KERNEL in n:
+                sums.append((a, b))
             elif "Cijk" in n or "gemm" in n.lower():
                 gemms.append((a, b))
     for f in mt:
@@ -330,23 +334,25 @@ def gemm_inflation(d, command):
                 return True
         return False
 
-    packs.sort()
-    copies.sort()
-    ps, cs = [p[0] for p in packs], [c[0] for c in copies]
-    groups = {"beside_pack": [], "beside_d2h": [], "alone": []}
+    sides = [("beside_pack", sorted(packs)), ("beside_sums", sorted(sums)), ("beside_d2h", sorted(copies))]
+    starts = {k: [iv[0] for iv in lst] for k, lst in sides}
+    groups = {k: [] for k, _ in sides}
+    groups["alone"] = []
     for g in gemms:
-        key = "beside_pack" if overlaps(g, packs, ps) else "beside_d2h" if overlaps(g, copies, cs) else "alone"
+        key = next((k for k, lst in sides if overlaps(g, lst, starts[k])), "alone")
         groups[key].append((g[1] - g[0]) / 1e3)
     base = statistics.median(groups["alone"]) if groups["alone"] else float("nan")
     lines = ["# GEMM durations under snapshots (rocprofv3 kernel + memory-copy trace)", "",
              "command: `%s`" % command, "",
-             "%d GEMM dispatches, %d pack launches, %d device-to-host copies in the trace." % (
-                 len(gemms), len(packs), len(copies)), "",
-             "| GEMMs | count | median (us) | mean (us) | median vs alone |", "|---|---|---|---|---|"]
+             "%d GEMM dispatches, %d pack launches, %d sums launches, %d device-to-host copies in the trace." % (
+                 len(gemms), len(packs), len(sums), len(copies)), "",
+             "| GEMMs | count | median (us) | mean (us) | median vs alone | added over the alone median, in all (ms) |",
+             "|---|---|---|---|---|---|"]
     for k, v in groups.items():
         if v:
-            lines.append("| %s | %d | %.1f | %.1f | %+.2f%% |" % (k, len(v), statistics.median(v), statistics.mean(v),
-                                                                  100 * (statistics.median(v) / base - 1)))
+            lines.append("| %s | %d | %.1f | %.1f | %+.2f%% | %.1f |" % (
+                k, len(v), statistics.median(v), statistics.mean(v), 100 * (statistics.median(v) / base - 1),
+                sum(x - base for x in v) / 1e3))
     return "\n".join(lines)
 
 
