@@ -6,6 +6,8 @@ import torch
 import oracle as O
 
 EDGE_SIZES = [1, 2, 3, 15, 16, 17, 255, 256, 257, 0, 4095, 4096, 4097, 100_003, 0, 0, 65536, 65537, 1 << 20, 7]
+# Empty fragments before the first byte and after the last one.
+ENDS_EMPTY = [0, 0, 5, 4096, 0, 3 * 4096 + 1, 17, 0, 0]
 
 
 def host_bytes(t):

@@ -104,11 +104,12 @@ def test_direct_plan_brute_force(P):
     at the fragment's own offset (so the engines copy every fragment byte once,
     to its place); each run is padding, which no fragment byte lies in."""
     rng = np.random.default_rng(6)
-    for C, A, G in [(256, 256, 0), (4096, 256, 4096), (4096, 16, 3 * 4096), (768, 256, 2 * 768), (1 << 17, 256, 0)]:
+    geometries = [(256, 256, 0), (4096, 256, 4096), (4096, 16, 3 * 4096), (768, 256, 2 * 768), (1 << 17, 256, 0)]
+    for (C, A, G), tail in [(g, t) for g in geometries for t in ([1], [0, 0], [5 * 4096, 0])]:
         sizes = [int(s) for s in rng.integers(0, 9000, 150)]
         sizes[7:11] = [0, 0, 0, 0]
         sizes[0] = 0
-        sizes[-1] = 1
+        sizes[-len(tail):] = tail  # the image ends on a byte, on empty fragments, or on a long one
         sizes[20] = 5 * C + 3  # spans several groups
         pieces, gaps, pf, gf = P.ckpt_debug_direct_plan(sizes, C, A, G)
         off, I, nc = O.layout(sizes, A, C)

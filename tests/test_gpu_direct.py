@@ -13,7 +13,7 @@ import pytest
 import torch
 
 import oracle as O
-from gpu_util import (EDGE_SIZES, assert_located, garbage_fill, hold, host_bytes, pick_stream,
+from gpu_util import (EDGE_SIZES, ENDS_EMPTY, assert_located, garbage_fill, hold, host_bytes, pick_stream,
                       random_byte_fragments, snapshot_and_check)
 
 pytestmark = pytest.mark.gpu
@@ -34,6 +34,15 @@ if torch.cuda.is_available():
 def test_edge_sizes(chunk, align, group, bounce):
     tensors, host = random_byte_fragments(EDGE_SIZES, seed=chunk + align + group + bounce)
     ck, _ = snapshot_and_check(tensors, host, chunk, align, group=group, bounce=bounce, direct=True)
+    ck.close()
+
+
+@pytest.mark.parametrize("bounce", [0, 2 * 4096])
+def test_empty_fragments_at_both_ends(bounce):
+    """Empty fragments first and last: no piece and no padding run for them,
+    and the copies end on the last non-empty fragment's padding."""
+    tensors, host = random_byte_fragments(ENDS_EMPTY, seed=43 + bounce)
+    ck, _ = snapshot_and_check(tensors, host, 4096, 256, group=4096, bounce=bounce, direct=True)
     ck.close()
 
 

@@ -13,8 +13,8 @@ import torch
 
 import oracle as O
 import workloads as W
-from gpu_util import (EDGE_SIZES, assert_located, garbage_fill, host_bytes, pick_stream, random_byte_fragments,
-                      snapshot_and_check)
+from gpu_util import (EDGE_SIZES, ENDS_EMPTY, assert_located, garbage_fill, host_bytes, pick_stream,
+                      random_byte_fragments, snapshot_and_check)
 
 pytestmark = pytest.mark.gpu
 
@@ -50,6 +50,19 @@ def test_edge_sizes_multi_group_launches(chunk, align, staging, group, launch):
 def test_edge_sizes_all_geometries(chunk, align, staging, group):
     tensors, host = random_byte_fragments(EDGE_SIZES, seed=chunk + align)
     ck, _ = snapshot_and_check(tensors, host, chunk, align, staging, group)
+    ck.close()
+
+
+@pytest.mark.parametrize("staging,group,bounce", [
+    (0, 0, 0),                  # full device image, pinned host images
+    (4 * 4096, 4096, 0),        # ring of four one-chunk slots
+    (0, 4096, 2 * 4096),        # pageable images behind a ring of two one-chunk groups
+])
+def test_empty_fragments_at_both_ends(staging, group, bounce):
+    """Empty fragments first and last take no image space: the image starts
+    with the first non-empty fragment and ends on the last one's padding."""
+    tensors, host = random_byte_fragments(ENDS_EMPTY, seed=41 + staging + bounce)
+    ck, _ = snapshot_and_check(tensors, host, 4096, 256, staging, group, bounce=bounce)
     ck.close()
 
 
