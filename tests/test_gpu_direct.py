@@ -28,6 +28,7 @@ if torch.cuda.is_available():
     (4096, 16, 3 * 4096, 0),              # 16-byte alignment, three-chunk groups
     (768, 256, 768, 0),                   # chunk not a power of two
     (1 << 20, 256, 1 << 20, 0),           # chunks larger than most fragments
+    (1 << 16, 4096, 1 << 16, 0),          # 4 KiB alignment: padding runs of up to 4095 bytes
     (4096, 256, 4096, 4 * 4096),          # pageable images behind a ring of four groups
     (8192, 16, 2 * 8192, 2 * 2 * 8192),   # ... and of two groups of two chunks
 ])
