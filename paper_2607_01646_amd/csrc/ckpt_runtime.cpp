@@ -1109,10 +1109,13 @@ ckpt_status ckpt_wait(ckpt_ctx* c, uint64_t snap_id, uint32_t mode, void* stream
     }
     if (!any) return CKPT_OK; // only empty fragments: nothing to protect
     if (c->direct) {
-        // The sums of every group up to the range's last (launches run in
-        // order), and the copies of each group holding a byte of the range:
-        // the engines finish groups out of order, and each group's copies
-        // end by setting its counter to this snapshot's use number.
+        // The copies of each group holding a byte of the range (the engines
+        // finish groups out of order), each ending by setting the group's
+        // counter to this snapshot's use number.  A group's copies start only
+        // once the launch after its sums has started, so its counter also
+        // covers the sums of every group up to it (launches run in order).
+        // Groups an interrupted snapshot never copies have an event after
+        // their sums instead.
         uint64_t first = 0;
         for (uint32_t i = frag_lo; i < frag_hi; ++i)
             if (c->frags[i].nbytes) {
@@ -1121,7 +1124,7 @@ ckpt_status ckpt_wait(ckpt_ctx* c, uint64_t snap_id, uint32_t mode, void* stream
             }
         const uint64_t unit = c->G * c->C;
         const uint64_t g0 = first / unit, g1 = last / unit;
-        HIPCHK(c, hipStreamWaitEvent((hipStream_t)stream, r.res->captured[g1], 0));
+        if (g1 >= r.groups_copied) HIPCHK(c, hipStreamWaitEvent((hipStream_t)stream, r.res->captured[g1], 0));
         for (uint64_t g = g0; g <= g1 && g < r.groups_copied; ++g)
             HIPCHK(c, hipStreamWaitValue64((hipStream_t)stream, c->d_area_done + g, r.res->h_seq[g],
                                            hipStreamWaitValueGte, ~0ull));

@@ -95,8 +95,13 @@ ckpt_status issue_groups_direct(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint
         if (e != hipSuccess) return fail(c, CKPT_EHIP, "sums launch failed: %s", hipGetErrorString(e));
         pending = nullptr;
         carried.handle = 0;
-        HIPCHK(c, hipEventRecord(res->captured[g], c->s_pack));
-        if (g >= n_copy) continue; // interrupted offload: this group never leaves the device
+        if (g >= n_copy) { // interrupted offload: this group never leaves the device, the gate waits for its sums
+            HIPCHK(c, hipEventRecord(res->captured[g], c->s_pack));
+            continue;
+        }
+        // A copied group needs no event: its copies wait for the release that
+        // the next launch stores once this one has finished, so the counter
+        // the gate waits for implies the group's sums have been read too.
         hsa_signal_store_screlease(res->dep[g], 1);
         pending = res->dep_val[g];
         carried = res->dep[g];
