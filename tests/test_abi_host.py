@@ -5,6 +5,8 @@ import re
 
 import numpy as np
 import pytest
+from hypothesis import HealthCheck, given, settings
+from hypothesis import strategies as st
 
 import oracle as O
 
@@ -97,6 +99,40 @@ def test_tile_plan_brute_force(P):
             assert tl[t] == holder(x1)
 
 
+def check_direct_plan(P, sizes, C, A, G):
+    """The copy plan of direct D2H for one layout, byte by byte (see
+    test_direct_plan_brute_force)."""
+    pieces, gaps, pf, gf = P.ckpt_debug_direct_plan(sizes, C, A, G)
+    off, I, nc = O.layout(sizes, A, C)
+    unit = max(1, (G or (1 << 30)) // C) * C
+    n_groups = -(-I // unit)
+    assert len(pf) == len(gf) == n_groups + 1
+    owner = np.full(I, -1, dtype=np.int64)  # fragment holding each image byte, -1 = padding
+    pos = np.zeros(I, dtype=np.int64)       # its offset inside that fragment
+    for i, (o, s) in enumerate(zip(off, sizes)):
+        owner[int(o):int(o) + s] = i
+        pos[int(o):int(o) + s] = np.arange(s)
+    for g in range(n_groups):
+        lo, hi = g * unit, min((g + 1) * unit, I)
+        ps = pieces[int(pf[g]):int(pf[g + 1])]
+        gs = gaps[int(gf[g]):int(gf[g + 1])]
+        assert len(ps) >= 1
+        spans = sorted([(int(p[2]), int(p[3]), int(p[0]), int(p[1])) for p in ps] +
+                       [(int(r[0]), int(r[1]), -1, 0) for r in gs])
+        x = lo
+        for a, n, frag, src in spans:
+            assert a == x and n > 0, (g, a, x, n)
+            if frag >= 0:
+                assert np.all(owner[a:a + n] == frag) and np.array_equal(pos[a:a + n], np.arange(src, src + n))
+            else:
+                assert np.all(owner[a:a + n] == -1)
+            x = a + n
+        assert x == hi
+        assert np.all(np.diff(ps[:, 2].astype(np.int64)) > 0)  # pieces in image order
+    for i, s in enumerate(sizes):  # every fragment byte in exactly one piece
+        assert int(pieces[pieces[:, 0] == i][:, 3].sum()) == s
+
+
 def test_direct_plan_brute_force(P):
     """The copy plan of direct D2H, checked byte by byte over the oracle's
     layout: in every chunk group the fragment pieces and the padding runs tile
@@ -111,35 +147,7 @@ def test_direct_plan_brute_force(P):
         sizes[0] = 0
         sizes[-len(tail):] = tail  # the image ends on a byte, on empty fragments, or on a long one
         sizes[20] = 5 * C + 3  # spans several groups
-        pieces, gaps, pf, gf = P.ckpt_debug_direct_plan(sizes, C, A, G)
-        off, I, nc = O.layout(sizes, A, C)
-        unit = max(1, (G or (1 << 30)) // C) * C
-        n_groups = -(-I // unit)
-        assert len(pf) == len(gf) == n_groups + 1
-        owner = np.full(I, -1, dtype=np.int64)  # fragment holding each image byte, -1 = padding
-        pos = np.zeros(I, dtype=np.int64)       # its offset inside that fragment
-        for i, (o, s) in enumerate(zip(off, sizes)):
-            owner[int(o):int(o) + s] = i
-            pos[int(o):int(o) + s] = np.arange(s)
-        for g in range(n_groups):
-            lo, hi = g * unit, min((g + 1) * unit, I)
-            ps = pieces[int(pf[g]):int(pf[g + 1])]
-            gs = gaps[int(gf[g]):int(gf[g + 1])]
-            assert len(ps) >= 1
-            spans = sorted([(int(p[2]), int(p[3]), int(p[0]), int(p[1])) for p in ps] +
-                           [(int(r[0]), int(r[1]), -1, 0) for r in gs])
-            x = lo
-            for a, n, frag, src in spans:
-                assert a == x and n > 0, (g, a, x, n)
-                if frag >= 0:
-                    assert np.all(owner[a:a + n] == frag) and np.array_equal(pos[a:a + n], np.arange(src, src + n))
-                else:
-                    assert np.all(owner[a:a + n] == -1)
-                x = a + n
-            assert x == hi
-            assert np.all(np.diff(ps[:, 2].astype(np.int64)) > 0)  # pieces in image order
-        for i, s in enumerate(sizes):  # every fragment byte in exactly one piece
-            assert int(pieces[pieces[:, 0] == i][:, 3].sum()) == s
+        check_direct_plan(P, sizes, C, A, G)
 
 
 def test_plan_rejects_bad_geometry(P):
@@ -210,3 +218,49 @@ def test_canary_of_the_header_and_the_binding_agree(P):
     pieces = re.findall(r'"((?:[^"\\]|\\.)*)"', line)
     value = b"".join(codecs.escape_decode(p.encode())[0] for p in pieces)
     assert value == P.CKPT_CANARY and len(value) == 16
+
+
+@st.composite
+def layouts(draw):
+    """A fragment list and a geometry: alignment 16..4096, chunk a multiple of
+    it, group a multiple of the chunk (0 = the default), fragment sizes mixing
+    empty, tiny, sub-chunk and multi-chunk ones, at least one byte in all."""
+    A = 1 << draw(st.integers(4, 12))
+    C = A * draw(st.integers(1, max(1, (64 << 10) // A)))
+    G = C * draw(st.integers(0, 5))
+    size = st.one_of(st.just(0), st.integers(1, 300), st.integers(1, 5000), st.integers(1, 2 * C))
+    sizes = draw(st.lists(size, min_size=1, max_size=40).filter(any))
+    return sizes, C, A, G
+
+
+@settings(max_examples=150, deadline=None, suppress_health_check=[HealthCheck.too_slow])
+@given(layouts())
+def test_direct_plan_properties(P, layout):
+    """The direct D2H copy plan over random layouts, with the same byte-by-byte
+    check as the fixed cases."""
+    sizes, C, A, G = layout
+    check_direct_plan(P, sizes, C, A, G)
+
+
+@settings(max_examples=150, deadline=None, suppress_health_check=[HealthCheck.too_slow])
+@given(layouts())
+def test_layout_and_tile_plan_properties(P, layout):
+    """Layout and tile table over random layouts: offsets, image size and chunk
+    count equal the oracle's, and each tile's first and last fragment hold its
+    first and last byte."""
+    sizes, C, A, _ = layout
+    off, I, nc = O.layout(sizes, A, C)
+    poff, pI, pnc = P.ckpt_plan(sizes, C, A)
+    assert [int(o) for o in poff] == [int(o) for o in off] and (pI, pnc) == (I, nc)
+    tb, tf, tl = P.ckpt_debug_tile_plan(sizes, C, A)
+    assert C % tb == 0 and tb & (tb - 1) == 0 and 16 <= tb <= 8192
+    nonempty = [i for i, n in enumerate(sizes) if n]
+    starts = np.array([int(off[i]) for i in nonempty])
+
+    def holder(x):  # last non-empty fragment starting at or before x
+        return nonempty[int(np.searchsorted(starts, x, side="right")) - 1]
+
+    assert len(tf) == -(-I // tb)
+    for t in range(len(tf)):
+        x0, x1 = t * tb, min((t + 1) * tb, I) - 1
+        assert tf[t] == holder(x0) and tl[t] == holder(x1), t
