@@ -91,6 +91,17 @@ def test_llama65b_tp8pp8_rank_shard_direct(bounce):
     ck.close()
 
 
+@pytest.mark.parametrize("staging,bounce", [(1 << 30, 0), (256 << 20, 4 << 30)])
+def test_llama65b_tp8pp8_rank_shard_ring_staging(staging, bounce):
+    """The same rank through a bounded device staging ring (1 GiB of four
+    256 MiB slots, or four one-chunk slots with pageable images behind 4 GiB
+    rings): the packs follow the copies out of each slot, and every chunk,
+    sum and restored fragment still matches."""
+    ck, *_ = check_shard(3, staging=staging, bounce=bounce)
+    assert ck.n_chunks == 212
+    ck.close()
+
+
 def test_llama65b_rank_shard_in_full_precision():
     """The same rank with every tensor in fp32, the paper's training setting:
     360 fragments, 16.19 GB (16 bytes per parameter)."""
