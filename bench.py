@@ -94,7 +94,8 @@ def parse():
     ap.add_argument("--host-threads", type=int, default=0, help="bounce mode: host copy threads (0 = library default)")
     ap.add_argument("--group-bytes", type=int, default=0,
                     help="bytes per pack launch and DMA request (whole chunks); 0 = the library default (1 GiB, or "
-                         "a quarter of the staging ring)")
+                         "a quarter of the staging ring), except for the timed steps with pageable images, which "
+                         "default to 256 MiB groups in 1 GiB pack launches")
     ap.add_argument("--staging-bytes", type=int, default=0,
                     help="device staging: 0 = a full-size image (default); else a ring of slots of one chunk group "
                          "each, at most this many bytes in all, the next pack of a slot waiting for its copy (main "
@@ -1442,10 +1443,17 @@ def main():
         cpu = cpu_baseline(tensors, wl["chunk"], args.cpu_sample_bytes)
     log("registering %d fragments (%d payload bytes; host images %s)" % (
         n, S, "pageable behind %d-byte bounce rings" % bounce if bounce else "pinned"))
+    # Pageable images: 256 MiB DMA groups, packed four to a 1 GiB launch.  The
+    # host copy of each landed group (bounce slot -> image) overlaps the DMA of
+    # the next one, so the commit waits for a quarter of a gigabyte after the
+    # last copy instead of a whole one; the pack keeps its 1 GiB launches.
+    group_bytes, launch_bytes = args.group_bytes, args.pack_launch_bytes
+    if bounce and not (args.staging_bytes or args.direct or group_bytes or launch_bytes):
+        group_bytes, launch_bytes = 256 << 20, 1 << 30
     ck = P.Checkpointer(tensors, [p[2] for p in plan], [p[3] for p in plan], chunk_bytes=wl["chunk"],
                         bounce_bytes=bounce, host_threads=args.host_threads,
                         image_file=args.image_file or None, device_staging_bytes=args.staging_bytes,
-                        group_bytes=args.group_bytes, pack_launch_bytes=args.pack_launch_bytes,
+                        group_bytes=group_bytes, pack_launch_bytes=launch_bytes,
                         d2h_engines=args.d2h_engines, direct=args.direct)
     P.ckpt_set_timing(ck.ctx, True)
     opt = Optimizer(torch, tensors)
@@ -1575,7 +1583,10 @@ def main():
         log("overlap leg")
         odirect = args.overlap_mode == "direct"
         shared = state = None
-        if owid == wid and odirect == args.direct:
+        # The overlap leg keeps the library's group sizes (or the ones given):
+        # it shares the timed steps' context only when that has them too.
+        same_groups = (group_bytes, launch_bytes) == (args.group_bytes, args.pack_launch_bytes)
+        if owid == wid and odirect == args.direct and same_groups:
             shared = (tensors, plan, ck)
         elif owid == wid:  # the same tensors in a context of the overlap's mode; its images replace these
             ck.close()
@@ -1624,6 +1635,7 @@ def main():
                    "device_staging": ("none (direct D2H)" if args.direct
                                       else staging_text(args.staging_bytes, wl["chunk"])),
                    "groups_per_snapshot": int(sn["copies"]), "pack_launches_per_snapshot": int(sn["kernels"]),
+                   "group_bytes": group_bytes or None, "pack_launch_bytes": launch_bytes or None,
                    "parallelism": "one rank, one GPU"},
         "roofline": roofline,
         "cpu_baseline": cpu,
