@@ -33,6 +33,26 @@ def test_edge_sizes_through_bounce_rings(chunk, staging, group, bounce, threads)
     ck.close()
 
 
+@pytest.mark.parametrize("group,launch,bounce", [
+    (4096, 4 * 4096, 2 * 4096),          # four one-chunk groups per pack launch, a ring of two groups
+    (2 * 4096, 8 * 4096, 3 * 2 * 4096),  # four two-chunk groups per launch, a ring of three
+])
+def test_several_groups_per_pack_launch_through_bounce_rings(group, launch, bounce):
+    """Pack launches of several groups, each group its own DMA request into the
+    bounce ring (the layout the benchmark uses for pageable images)."""
+    tensors, host = random_byte_fragments(EDGE_SIZES, seed=group + launch)
+    ck, first = snapshot_and_check(tensors, host, 4096, group=group, bounce=bounce, launch=launch)
+    # a second snapshot reuses the ring slots and fills the other image
+    snap = ck.snapshot(step=4)
+    ck.wait_committed(snap)
+    img, sums = ck.host_image(snap)
+    want, _, _ = O.pack(host, 256, 4096)
+    assert np.array_equal(img, want)
+    assert np.array_equal(sums, O.chunk_sums(want, 0, want.size, 4096))
+    assert ck.state(first) == P.CKPT_SNAP_COMMITTED and ck.verify(first) == []  # the other image still holds it
+    ck.close()
+
+
 def test_large_groups_use_the_copy_pool():
     """Groups of 32 MiB, so that each ring-to-image copy is cut into parts
     run by several threads."""
