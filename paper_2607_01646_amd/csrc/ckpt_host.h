@@ -371,6 +371,8 @@ struct ckpt_ctx {
     bool own_pack = true; // false: s_pack is the caller's side stream (never destroyed here)
     hipEvent_t ev_trigger = nullptr, ev_done = nullptr;
     std::vector<uint64_t> area_seq;     // per staging area: copies issued out of it
+    std::vector<hsa_signal_t> area_flag; // per staging area: completion signal of its latest counter copy
+                                         // (0 once that copy, and the image copy before it, are done)
     std::vector<hipEvent_t> area_free;  // restore/verify: per staging area
     std::vector<hipEvent_t> ev_loaded;  // restore/verify: per group
     std::vector<RecRes*> free_res;

@@ -875,6 +875,7 @@ ckpt_status ckpt_register_tensors(ckpt_ctx* c, const ckpt_tensor* t, uint32_t n)
     HIPCHK(c, hipMemcpy(c->d_tile_last, pl.tile_last.data(), nt * 4, hipMemcpyHostToDevice));
     HIPCHK(c, hipMemset(c->d_area_done, 0, n_areas * 8));
     c->area_seq.assign(n_areas, 0);
+    c->area_flag.assign(n_areas, hsa_signal_t{0});
     if (c->bounce) {
         for (uint8_t** ring : {&c->h_bout, &c->h_bin}) {
             if (hipHostMalloc((void**)ring, c->n_bslots * unit, hipHostMallocDefault) != hipSuccess) {

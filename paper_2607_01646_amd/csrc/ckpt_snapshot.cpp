@@ -203,10 +203,14 @@ ckpt_status issue_groups(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_
         if (g == g0) {
             // A staging area is free once every copy issued out of it so far
             // has finished (each finished copy bumps area_done by one); the
-            // launch writes the areas of all its groups.
+            // launch writes the areas of all its groups.  The pack stream
+            // waits for that only while the host still sees the area's latest
+            // copy running: each wait is a packet the command processor works
+            // through between two packs, and with a full-size image the
+            // previous snapshot has committed, so its copies are all done.
             for (uint64_t h = g0; h < g1; ++h) {
                 const uint64_t a = area_of(c, h);
-                if (c->area_seq[a])
+                if (c->area_seq[a] && hsa_signal_load_scacquire(c->area_flag[a]) != 0)
                     HIPCHK(c, hipStreamWaitValue64(c->s_pack, c->d_area_done + a, c->area_seq[a],
                                                   hipStreamWaitValueGte, ~0ull));
             }
@@ -261,6 +265,7 @@ ckpt_status issue_groups(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_
             }
             c->pump->cv.notify_all();
             ++c->area_seq[area];
+            c->area_flag[area] = res->flagged[g];
             continue;
         }
         st = dma(c, himg + lo, host, staging_of(c, g), c->gpu_agent, hi - lo, &res->dep[g0], res->copied[g], eng);
@@ -274,6 +279,7 @@ ckpt_status issue_groups(ckpt_ctx* c, SnapRec& r, hipStream_t after, uint64_t n_
             return st;
         }
         ++c->area_seq[area];
+        c->area_flag[area] = res->flagged[g];
     }
     if (stop >= 0) {
         r.aborted = true; // interrupted offload: never committed (its pack timing stays readable)
