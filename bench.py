@@ -254,7 +254,7 @@ def timed_d2h_from_trace(d, bench):
     """Per timed snapshot of the bench's workload-2 steps: image bytes / (last
     group copy's end - first group copy's start), from the memory-copy trace.
     The group copies are the device-to-host copies longer than 1 ms, in time
-    order: (warmup + steps) snapshots of `launches / steps` copies each come
+    order: (warmup + steps) snapshots of one copy per chunk group each come
     first (the calibration copies before them are blit kernels, not copies)."""
     import csv
     import glob
@@ -268,7 +268,7 @@ def timed_d2h_from_trace(d, bench):
             if "DEVICE_TO_HOST" in kind and b - a > 1_000_000:
                 copies.append((a, b))
     copies.sort()
-    per = bench["roofline"]["launches"] // bench["steps"]
+    per = bench["config"].get("groups_per_snapshot") or bench["roofline"]["launches"] // bench["steps"]
     image = bench["config"]["image_bytes"]
     rates = []
     for k in range(bench["warmup"], bench["warmup"] + bench["steps"]):

@@ -61,6 +61,24 @@ def test_gemm_split_by_what_ran_beside(bench, tmp_path):
     assert lines["alone"][:2] == ["73", "500.0"]  # the host-to-device copy does not count
 
 
+def test_d2h_per_snapshot_from_a_copy_trace(bench, tmp_path):
+    """Each timed snapshot's D2H rate from the memory-copy trace groups one
+    copy per chunk group (here four 256 MiB groups per snapshot, packed in one
+    launch, so groups and launches differ), after the warm-up snapshots."""
+    ms = 1_000_000  # ns
+    rows = []
+    for k in range(5):  # 2 warm-up + 3 timed snapshots, 100 ms apart
+        t = k * 100 * ms
+        for g in range(4):  # four 5 ms copies back to back, then the 8-byte counter copies (short)
+            rows.append((t + g * 5 * ms, t + (g + 1) * 5 * ms, "MEMORY_COPY_DEVICE_TO_HOST"))
+            rows.append((t + (g + 1) * 5 * ms, t + (g + 1) * 5 * ms + 2000, "MEMORY_COPY_DEVICE_TO_HOST"))
+    _write(tmp_path / "x_memory_copy_trace.csv", ["Start_Timestamp", "End_Timestamp", "Direction"], rows)
+    b = {"steps": 3, "warmup": 2, "roofline": {"launches": 3}, "config": {"image_bytes": 20 * ms,
+                                                                        "groups_per_snapshot": 4}}
+    rates, med = bench.timed_d2h_from_trace(str(tmp_path), b)
+    assert rates == [pytest.approx(1.0)] * 3 and med == pytest.approx(1.0)  # 20e6 bytes in 20 ms = 1 GB/s
+
+
 def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
                        text=True, timeout=60)
